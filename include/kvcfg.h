@@ -1,0 +1,210 @@
+/* kvcfg.h - batched KV-cache tier-configuration evaluation on one MI355X.
+ *
+ * Kareto (arXiv 2603.08739) searches storage configurations for an LLM
+ * service's KV cache by replaying a historical trace of KV-block hashes
+ * through a model of the HBM / DRAM / disk hierarchy and comparing the
+ * candidates on (cost, throughput, latency) (Eq. 1, Eq. 2; Section 4.1).
+ * This library is that inner loop, batched: it evaluates many candidate
+ * configurations over one device-resident trace and filters the
+ * non-dominated ones.
+ *
+ *   kv_trace_load    canonicalise a trace of block hashes (once per trace)
+ *   kv_eval_configs  per configuration: exact per-tier hit / miss / insert /
+ *                    eviction counts, then (cost, throughput, latency)
+ *   kv_pareto        non-dominated filter under optional bounds
+ *
+ * Conventions for every call:
+ *   - Return KV_OK or a negative kv_status; kv_last_error() then describes
+ *     the failure (thread-local).  No C++ exception crosses this interface.
+ *   - Arguments are validated before any device work; on a validation
+ *     failure no output is touched and nothing is allocated or leaked.
+ *   - "device" pointers are HIP device allocations on the current device;
+ *     "host" pointers are ordinary process memory.  The library keeps no
+ *     pointer to caller memory after a call returns.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Device work is
+ *     enqueued on it; device outputs are valid once the stream has completed.
+ *   - Capacities and weights are in granules; a granule is the unit KV block
+ *     size of the trace (e.g. 16 tokens = 128 KiB).
+ */
+#ifndef KVCFG_H
+#define KVCFG_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum kv_status {
+  KV_OK = 0,
+  KV_ERR_INVALID = -1,     /* argument or data violates this contract        */
+  KV_ERR_NOMEM = -2,       /* device memory exhausted (nothing left allocated) */
+  KV_ERR_DEVICE = -3,      /* a HIP runtime or kernel-launch error            */
+  KV_ERR_UNSUPPORTED = -4  /* well-formed request outside the supported set   */
+} kv_status;
+
+enum { KV_MAX_GROUPS = 16, KV_TIERS = 3, KV_FIELDS = 8 };
+
+/* Tier organisation of a configuration. */
+enum {
+  /* Every tier is an independent cache that sees every access; an access is
+   * served by the fastest tier holding its block, then each tier applies its
+   * own hit or insert (with eviction) rule. */
+  KV_MODE_INCLUSIVE = 0,
+  /* LRU hierarchy with write-back demotion: a block lives in at most one
+   * tier; a hit in a lower tier promotes the block to the top tier, and an
+   * overfull tier demotes its least recently used block to the next tier
+   * (dropping it past the last tier).  Requires LRU and a trace whose
+   * blocks all have the same weight. */
+  KV_MODE_EXCLUSIVE_DEMOTE = 1
+};
+
+/* Eviction policy of a tier cache.  A miss inserts the block after evicting
+ * victims until used + w <= capacity.  LRU evicts the least recently used
+ * block (Section 2.1 names LRU); FIFO the oldest insertion; LFU the smallest
+ * (in-cache access count, last access position) - the count starts at 1 on
+ * insertion and is forgotten on eviction. */
+enum { KV_POLICY_LRU = 0, KV_POLICY_FIFO = 1, KV_POLICY_LFU = 2 };
+
+/* Record fields of kv_eval_configs' counts, per (config, group, tier).
+ *   hit    accesses served by this tier
+ *   miss   accesses that reached this tier (no faster tier served them) and
+ *          were not served by it
+ *   ins    blocks inserted into this tier (tier-local misses in the
+ *          inclusive mode; arrivals by promotion or demotion otherwise)
+ *   evict  blocks that left this tier for lack of room (demotions count),
+ *          charged to the evicted block's group
+ *   *_w    the same, summed in granules
+ * A tier of capacity 0 is absent and records zeros. */
+enum {
+  KV_F_HIT = 0, KV_F_MISS = 1, KV_F_INS = 2, KV_F_EVICT = 3,
+  KV_F_HIT_W = 4, KV_F_MISS_W = 5, KV_F_INS_W = 6, KV_F_EVICT_W = 7
+};
+
+/* A trace of KV-block accesses in time order: the paper's traces carry, per
+ * request, its arrival time and the salted hashes of its KV blocks
+ * (Section 3.3 and Section 4.1).  All arrays are device pointers.  Blocks of
+ * one request are listed in block-index order; each distinct hash must carry
+ * one weight and one group throughout. */
+typedef struct kv_trace_desc {
+  uint64_t n;                  /* accesses; 1 <= n <= 2^29                   */
+  const uint64_t* hash;        /* [n] block hash per access                  */
+  const uint32_t* req;         /* [n] request index, non-decreasing, < n_req */
+  const uint8_t* group;        /* [n] tenant group < n_groups, or NULL (= 0) */
+  const uint8_t* weight;       /* [n] block size in granules >= 1, or NULL (= 1) */
+  uint32_t n_req;              /* requests; >= 1                             */
+  const double* req_time;      /* [n_req] arrival time in seconds, non-decreasing */
+  uint32_t n_groups;           /* 1..16                                      */
+  uint32_t tokens_per_granule; /* >= 1                                       */
+  uint64_t granule_bytes;      /* >= 1                                       */
+} kv_trace_desc;
+
+typedef struct kv_trace kv_trace; /* opaque, device-resident canonical trace */
+
+typedef struct kv_trace_stats {
+  uint64_t n;                        /* accesses                              */
+  uint64_t n_distinct;               /* distinct blocks U                     */
+  uint64_t n_w;                      /* total weight of all accesses          */
+  uint64_t distinct_w;               /* total weight of distinct blocks       */
+  uint64_t n_g[KV_MAX_GROUPS];       /* accesses per group                    */
+  uint64_t n_w_g[KV_MAX_GROUPS];     /* weight per group                      */
+  uint64_t u_g[KV_MAX_GROUPS];       /* distinct blocks per group             */
+  uint64_t u_w_g[KV_MAX_GROUPS];     /* distinct weight per group             */
+  uint64_t max_multiplicity;         /* most accesses to one block            */
+  uint32_t n_req, n_groups;
+  uint32_t w_min, w_max;             /* smallest / largest block weight       */
+  double span;                       /* req_time[n_req-1] - req_time[0]       */
+} kv_trace_stats;
+
+/* One candidate configuration (the planner's candidates, Section 4.1). */
+typedef struct kv_config {
+  uint64_t cap[KV_TIERS];            /* granules per tier, HBM/DRAM/SSD; 0 = absent.
+                                        Each nonzero capacity must be >= the
+                                        trace's largest block weight.         */
+  uint64_t cap_group[KV_TIERS][KV_MAX_GROUPS]; /* partitioned: per-group capacity of
+                                        each tier; sum over groups <= cap[k]  */
+  uint8_t mode;                      /* KV_MODE_*                             */
+  uint8_t partitioned;               /* 0: one cache per tier shared by all groups,
+                                        policy[0]; 1: group g owns cap_group[k][g]
+                                        of tier k and uses policy[g]          */
+  uint8_t policy[KV_MAX_GROUPS];     /* KV_POLICY_* (same policy on every tier) */
+  uint8_t reserved[6];               /* must be 0                             */
+} kv_config;
+
+/* Inputs of the objective proxy (all > 0). */
+typedef struct kv_cost_model {
+  double price_gpu_per_hour;         /* compute price per wall-clock hour     */
+  double price_per_gib_hour[KV_TIERS]; /* capacity price per GiB per hour (>= 0) */
+  double bw_dram;                    /* DRAM -> HBM bytes/s                   */
+  double ssd_bw_base;                /* disk bytes/s at zero capacity         */
+  double ssd_bw_per_gib;             /* extra disk bytes/s per provisioned GiB */
+  double ssd_bw_max;                 /* disk bytes/s cap                      */
+  double t_prefill_per_token;        /* seconds to recompute one token's KV   */
+} kv_cost_model;
+
+/* Canonicalise a trace (Section 4.1: the simulator replays request arrival
+ * times and token-level KV-block hashes).  Reads the caller's device arrays
+ * during the call only and builds, on the device, dense block ids and the
+ * previous/next occurrence of every access.  On success *out owns device
+ * memory until kv_trace_free.  Errors: KV_ERR_INVALID for bad sizes, a group
+ * >= n_groups, a zero weight, a hash seen with two weights or two groups, or
+ * a non-monotone req / req_time; *out is then NULL. */
+kv_status kv_trace_load(const kv_trace_desc* desc, void* stream, kv_trace** out);
+
+/* Free a trace (NULL is accepted).  A handle already freed is detected and
+ * rejected with KV_ERR_INVALID while its memory has not been reused. */
+kv_status kv_trace_free(kv_trace* t);
+
+/* Copy the trace's summary statistics into a host struct (synchronous). */
+kv_status kv_trace_info(const kv_trace* t, kv_trace_stats* out);
+
+/* Evaluate n_cfg configurations over the trace (the simulator's per-candidate
+ * evaluation, Section 4.1; objectives after Eq. 1 and Eq. 2).
+ *   cfg     host [n_cfg]
+ *   model   host
+ *   counts  device uint64 [n_cfg][n_groups][3][8], fields KV_F_* (required)
+ *   obj     device double [n_cfg][3] = (cost, throughput, latency), or NULL
+ * Counts are exact.  Objectives, per configuration, with H_w[k] = granules
+ * served by tier k (all groups), I_w = granules inserted into the disk tier,
+ * R_w = N_w - sum H_w, gb = granule bytes, tpg = tokens per granule:
+ *   capGiB[k] = cap[k]*gb/2^30;  bw_ssd = min(ssd_bw_base + ssd_bw_per_gib*capGiB[2], ssd_bw_max)
+ *   T_busy = R_w*tpg*t_prefill_per_token + H_w[1]*gb/bw_dram + (H_w[2]+I_w)*gb/bw_ssd
+ *   T_wall = max(span, T_busy)
+ *   cost = (price_gpu_per_hour + sum_k capGiB[k]*price_per_gib_hour[k]) * T_wall/3600
+ *   throughput = N_w*tpg/T_wall (tokens/s);  latency = T_busy/n_req (s)
+ * evaluated left to right in IEEE double without contraction.
+ * Errors: KV_ERR_INVALID for a capacity in (0, w_max), partitioned capacities
+ * that exceed cap[k], an unknown mode or policy, nonzero reserved bytes, or a
+ * nonpositive cost-model rate; KV_ERR_UNSUPPORTED for the exclusive mode with
+ * FIFO/LFU or with blocks of different weights.  n_cfg == 0 is a no-op. */
+kv_status kv_eval_configs(const kv_trace* t, const kv_config* cfg, uint32_t n_cfg,
+                          const kv_cost_model* model, uint64_t* counts, double* obj,
+                          void* stream);
+
+/* Pareto-based selection (Section 4.1): on_front[i] = 1 iff row i satisfies
+ * the bounds and no other bounded row of the same segment dominates it, where
+ * a dominates b when a.cost <= b.cost, a.throughput >= b.throughput and
+ * a.latency <= b.latency with at least one strict.  Equal rows are all kept.
+ *   obj       device double [n][3]
+ *   segment   device uint32 [n] or NULL (one segment)
+ *   bounds    host double [3] or NULL: cost <= b0, throughput >= b1,
+ *             latency <= b2; NaN disables a bound
+ *   on_front  device uint8 [n]
+ *   n_front   host, or NULL; when non-NULL the call waits for the stream and
+ *             stores the number of flagged rows
+ * A row with a NaN objective is never on the front and never dominates.
+ * Errors: KV_ERR_INVALID for NULL obj/on_front with n > 0, or n > 2^26; when
+ * n_front is non-NULL, also KV_ERR_INVALID if any objective is NaN (flags are
+ * still written).  n == 0 is a no-op (n_front = 0). */
+kv_status kv_pareto(const double* obj, const uint32_t* segment, uint32_t n,
+                    const double* bounds, uint8_t* on_front, uint32_t* n_front,
+                    void* stream);
+
+/* Message describing the calling thread's most recent failure ("" if none). */
+const char* kv_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVCFG_H */

@@ -1,0 +1,245 @@
+// k_eval.hip - per-configuration counts, objectives and the Pareto filter.
+#include "kv_device.h"
+#include "kv_internal.h"
+
+namespace kv {
+namespace {
+
+// cumulative value of field f at capacity `cap` (0 for an absent tier)
+__device__ __forceinline__ uint64_t cum_at(const OrderView& ov, uint32_t g, uint64_t cap, int f) {
+  if (cap == 0) return 0;
+  const uint32_t c = cap > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)cap;
+  const uint32_t lo = ov.off[g], hi = ov.off[g + 1];
+  const uint32_t m = lower_bound(ov.thr, lo, hi, c);
+  return ov.hist[(uint64_t)(m + g) * 4 + f];
+}
+
+// LRU records from the stack-distance histograms.
+//  inclusive: hit_k = hits(C_k) - hits(M) if C_k > M (M = largest faster
+//             capacity), miss_k = N - hits(max(M, C_k)), ins_k = N - hits(C_k),
+//             evict_k = ins_k - final residents at C_k.
+//  exclusive (uniform weight w0): the tiers are one LRU stack cut at the
+//             cumulative block capacities S_k; hit_k = hits(S_k) - hits(S_{k-1}),
+//             miss_k = N - hits(S_k), evict_k = N - hits(S_k) - finals(S_k)
+//             (a block crosses depth S_k once per reuse interval whose distance
+//             exceeds S_k and once more if it ends deeper); ins of the top tier
+//             = N - hit_top, of a lower tier = evictions of the tier above.
+__global__ __launch_bounds__(256) void k_lru_counts(const kv_config* __restrict__ cfg,
+                                                    uint32_t n_cfg, uint32_t G, OrderView sh,
+                                                    OrderView pt,
+                                                    const GroupStats* __restrict__ gs,
+                                                    uint64_t* __restrict__ counts) {
+  const uint64_t tid = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (tid >= (uint64_t)n_cfg * G) return;
+  const uint32_t c = (uint32_t)(tid / G), g = (uint32_t)(tid % G);
+  const kv_config& C = cfg[c];
+  const bool part = C.partitioned != 0;
+  const uint32_t pol = part ? C.policy[g] : C.policy[0];
+  if (pol != KV_POLICY_LRU) return;
+  const OrderView& ov = (part && G > 1) ? pt : sh;
+  uint64_t cap[3];
+  for (int k = 0; k < 3; ++k) cap[k] = part ? C.cap_group[k][g] : C.cap[k];
+  const uint64_t N = gs[g].n_g, NW = gs[g].n_w_g;
+  uint64_t* out = counts + ((uint64_t)c * G + g) * 3 * 8;
+  if (C.mode == KV_MODE_INCLUSIVE) {
+    uint64_t M = 0;
+    for (int k = 0; k < 3; ++k) {
+      uint64_t* r = out + k * 8;
+      if (cap[k] == 0) {
+        for (int f = 0; f < 8; ++f) r[f] = 0;
+        continue;
+      }
+      const uint64_t Mx = cap[k] > M ? cap[k] : M;
+      const uint64_t hC = cum_at(ov, g, cap[k], 0), wC = cum_at(ov, g, cap[k], 1);
+      const uint64_t hM = cum_at(ov, g, M, 0), wM = cum_at(ov, g, M, 1);
+      const uint64_t hX = cum_at(ov, g, Mx, 0), wX = cum_at(ov, g, Mx, 1);
+      const uint64_t fC = cum_at(ov, g, cap[k], 2), fwC = cum_at(ov, g, cap[k], 3);
+      r[KV_F_HIT] = cap[k] > M ? hC - hM : 0;
+      r[KV_F_HIT_W] = cap[k] > M ? wC - wM : 0;
+      r[KV_F_MISS] = N - hX;
+      r[KV_F_MISS_W] = NW - wX;
+      r[KV_F_INS] = N - hC;
+      r[KV_F_INS_W] = NW - wC;
+      r[KV_F_EVICT] = (N - hC) - fC;
+      r[KV_F_EVICT_W] = (NW - wC) - fwC;
+      M = Mx;
+    }
+  } else {
+    const uint64_t w0 = gs[g].w0;
+    uint64_t S = 0, prev_ev = 0;
+    bool top = true;
+    for (int k = 0; k < 3; ++k) {
+      uint64_t* r = out + k * 8;
+      if (cap[k] == 0) {
+        for (int f = 0; f < 8; ++f) r[f] = 0;
+        continue;
+      }
+      const uint64_t Sp = S;
+      S += cap[k] / w0;
+      const uint64_t hS = cum_at(ov, g, S * w0, 0);
+      const uint64_t hP = cum_at(ov, g, Sp * w0, 0);
+      const uint64_t fS = cum_at(ov, g, S * w0, 2);
+      const uint64_t hit = hS - hP;
+      const uint64_t miss = N - hS;
+      const uint64_t ev = N - hS - fS;
+      const uint64_t ins = top ? N - hit : prev_ev;
+      r[KV_F_HIT] = hit;
+      r[KV_F_MISS] = miss;
+      r[KV_F_INS] = ins;
+      r[KV_F_EVICT] = ev;
+      r[KV_F_HIT_W] = hit * w0;
+      r[KV_F_MISS_W] = miss * w0;
+      r[KV_F_INS_W] = ins * w0;
+      r[KV_F_EVICT_W] = ev * w0;
+      prev_ev = ev;
+      top = false;
+    }
+  }
+}
+
+struct CostArgs {
+  double pg, p0, p1, p2, bw_dram, ssd_base, ssd_per_gib, ssd_max, tpf;
+  double gb, tpg, span, n_req;
+  uint64_t n_w;
+};
+
+// (cost, throughput, latency) in IEEE double, left to right, no contraction.
+__global__ __launch_bounds__(256) void k_objectives(const kv_config* __restrict__ cfg,
+                                                    uint32_t n_cfg, uint32_t G,
+                                                    const uint64_t* __restrict__ counts,
+                                                    CostArgs a, double* __restrict__ obj) {
+  const uint32_t c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= n_cfg) return;
+  uint64_t hw0 = 0, hw1 = 0, hw2 = 0, iw2 = 0;
+  for (uint32_t g = 0; g < G; ++g) {
+    const uint64_t* r = counts + ((uint64_t)c * G + g) * 24;
+    hw0 += r[0 * 8 + KV_F_HIT_W];
+    hw1 += r[1 * 8 + KV_F_HIT_W];
+    hw2 += r[2 * 8 + KV_F_HIT_W];
+    iw2 += r[2 * 8 + KV_F_INS_W];
+  }
+  const uint64_t rw = a.n_w - (hw0 + hw1 + hw2);
+  const double kGiB = 1073741824.0;
+  const double c0 = ((double)cfg[c].cap[0] * a.gb) / kGiB;
+  const double c1 = ((double)cfg[c].cap[1] * a.gb) / kGiB;
+  const double c2 = ((double)cfg[c].cap[2] * a.gb) / kGiB;
+  const double bw_lin = a.ssd_base + a.ssd_per_gib * c2;
+  const double bw_ssd = (a.ssd_max < bw_lin) ? a.ssd_max : bw_lin;
+  const double t_dram = ((double)hw1 * a.gb) / a.bw_dram;
+  const double t_ssd = ((double)(hw2 + iw2) * a.gb) / bw_ssd;
+  const double t_rec = ((double)rw * a.tpg) * a.tpf;
+  const double t_busy = (t_rec + t_dram) + t_ssd;
+  const double t_wall = (a.span < t_busy) ? t_busy : a.span;
+  const double thr = ((double)a.n_w * a.tpg) / t_wall;
+  const double lat = t_busy / a.n_req;
+  const double cost = (((a.pg + c0 * a.p0) + c1 * a.p1) + c2 * a.p2) * (t_wall / 3600.0);
+  obj[3 * (uint64_t)c + 0] = cost;
+  obj[3 * (uint64_t)c + 1] = thr;
+  obj[3 * (uint64_t)c + 2] = lat;
+}
+
+struct Bounds {
+  double b0, b1, b2;
+};
+
+__device__ __forceinline__ bool feasible(double o0, double o1, double o2, const Bounds& b) {
+  if (o0 != o0 || o1 != o1 || o2 != o2) return false;
+  if (b.b0 == b.b0 && !(o0 <= b.b0)) return false;
+  if (b.b1 == b.b1 && !(o1 >= b.b1)) return false;
+  if (b.b2 == b.b2 && !(o2 <= b.b2)) return false;
+  return true;
+}
+
+// All-pairs dominance, candidate rows staged through LDS 256 at a time.
+__global__ __launch_bounds__(256) void k_pareto(const double* __restrict__ obj,
+                                                const uint32_t* __restrict__ seg, uint32_t n,
+                                                Bounds bd, uint8_t* __restrict__ flag,
+                                                uint32_t* __restrict__ counters) {
+  __shared__ double so[3][256];
+  __shared__ uint32_t ss[256];
+  __shared__ uint32_t sf[256];
+  const uint32_t b = blockIdx.x * 256 + threadIdx.x;
+  double ob0 = 0, ob1 = 0, ob2 = 0;
+  uint32_t sb = 0;
+  bool fb = false, nan = false;
+  if (b < n) {
+    ob0 = obj[3 * (uint64_t)b];
+    ob1 = obj[3 * (uint64_t)b + 1];
+    ob2 = obj[3 * (uint64_t)b + 2];
+    sb = seg ? seg[b] : 0u;
+    nan = (ob0 != ob0) || (ob1 != ob1) || (ob2 != ob2);
+    fb = feasible(ob0, ob1, ob2, bd);
+  }
+  bool dom = false;
+  for (uint32_t a0 = 0; a0 < n; a0 += 256) {
+    const uint32_t a = a0 + threadIdx.x;
+    if (a < n) {
+      const double x0 = obj[3 * (uint64_t)a], x1 = obj[3 * (uint64_t)a + 1],
+                   x2 = obj[3 * (uint64_t)a + 2];
+      so[0][threadIdx.x] = x0;
+      so[1][threadIdx.x] = x1;
+      so[2][threadIdx.x] = x2;
+      ss[threadIdx.x] = seg ? seg[a] : 0u;
+      sf[threadIdx.x] = feasible(x0, x1, x2, bd) ? 1u : 0u;
+    }
+    __syncthreads();
+    const uint32_t m = min(256u, n - a0);
+    if (fb && !dom) {
+      for (uint32_t j = 0; j < m; ++j) {
+        if (a0 + j == b || !sf[j] || ss[j] != sb) continue;
+        const double x0 = so[0][j], x1 = so[1][j], x2 = so[2][j];
+        const bool le = x0 <= ob0 && x1 >= ob1 && x2 <= ob2;
+        const bool lt = x0 < ob0 || x1 > ob1 || x2 < ob2;
+        if (le && lt) {
+          dom = true;
+          break;
+        }
+      }
+    }
+    __syncthreads();
+  }
+  if (b < n) {
+    const bool on = fb && !dom;
+    flag[b] = on ? 1 : 0;
+    if (on) atomicAdd(&counters[0], 1u);
+    if (nan) atomicOr(&counters[1], 1u);
+  }
+}
+
+}  // namespace
+
+kv_status lru_counts(const kv_config* cfg_dev, uint32_t n_cfg, uint32_t n_groups,
+                     OrderView shared, OrderView part, const GroupStats* gs_dev,
+                     uint64_t* counts, hipStream_t s) {
+  const uint64_t m = (uint64_t)n_cfg * n_groups;
+  if (m == 0) return KV_OK;
+  hipLaunchKernelGGL(k_lru_counts, dim3(div_up(m, 256)), dim3(256), 0, s, cfg_dev, n_cfg,
+                     n_groups, shared, part, gs_dev, counts);
+  KV_HIP(hipGetLastError());
+  return KV_OK;
+}
+
+kv_status objectives(const kv_config* cfg_dev, uint32_t n_cfg, uint32_t n_groups,
+                     const uint64_t* counts, const kv_cost_model& m, double gb, double tpg,
+                     double span, double n_req, uint64_t n_w, double* obj, hipStream_t s) {
+  if (n_cfg == 0) return KV_OK;
+  CostArgs a{m.price_gpu_per_hour, m.price_per_gib_hour[0], m.price_per_gib_hour[1],
+             m.price_per_gib_hour[2], m.bw_dram, m.ssd_bw_base, m.ssd_bw_per_gib,
+             m.ssd_bw_max, m.t_prefill_per_token, gb, tpg, span, n_req, n_w};
+  hipLaunchKernelGGL(k_objectives, dim3(div_up(n_cfg, 256)), dim3(256), 0, s, cfg_dev, n_cfg,
+                     n_groups, counts, a, obj);
+  KV_HIP(hipGetLastError());
+  return KV_OK;
+}
+
+kv_status pareto(const double* obj, const uint32_t* segment, uint32_t n, const double* bounds,
+                 uint8_t* flag, uint32_t* counters_dev, hipStream_t s) {
+  const double nan = __builtin_nan("");
+  Bounds bd{bounds ? bounds[0] : nan, bounds ? bounds[1] : nan, bounds ? bounds[2] : nan};
+  hipLaunchKernelGGL(k_pareto, dim3(div_up(n, 256)), dim3(256), 0, s, obj, segment, n, bd, flag,
+                     counters_dev);
+  KV_HIP(hipGetLastError());
+  return KV_OK;
+}
+
+}  // namespace kv

@@ -1,0 +1,578 @@
+// k_stack.hip - one pass that serves every LRU capacity at once.
+//
+// Under LRU a block is resident in a cache of capacity C exactly when its
+// stack distance D_i <= C, where D_i is the weight of the block itself plus
+// the weight of the distinct other blocks touched since its previous access
+// (Mattson et al., "Evaluation techniques for storage hierarchies", IBM
+// Systems Journal 1970; with unit weights D_i counts distinct blocks).  The
+// paper's tiers use LRU (Section 2.1) and its simulator models the tier
+// hierarchy by replay (Section 3.2); the inclusion property lets one pass
+// over the trace answer every tier capacity of every configuration.
+//
+// With p = prev(i) and key_j = prev(j) + 1 (0 for a first access):
+//   D_i = w_i + sum_{p < j < i} w_j [key_j <= p]
+// (a block touched in (p, i) is counted at its first touch there, the one
+// whose own previous access lies before p).  Positions are cut into 8192-wide
+// blocks; with P = block(p), I = block(i):
+//   P == I:  D_i = w_i + A(i) - Wloc(p)
+//   P <  I:  D_i = w_i + A(i) + E(p) + RQ[I-1][P]
+// where, inside one block,
+//   A(i)    = sum_{j in block(i), j < i} w_j [key_j < key_i]     (dominance count)
+//   Wloc(p) = sum_{j in block(p), j <= p} w_j
+//   E(p)    = Cnt_P(p) - Wloc(p) + C(p)
+//   Cnt_P(p)= sum_{j in block P} w_j [key_j <= p]
+//   C(p)    = sum_{q in block P, q < p} w_q [P < block(next(q)) < block(next(p))]
+// and across blocks RQ[X][Y] = sum_{X'=Y+1..X} Q[X'][Y] with
+//   Q[X][Y] = sum_{j in block X} w_j [key_j <= Y * 8192]
+// stored as a lower triangle.  The two in-block dominance counts come from
+// an LDS merge sort that accumulates, for every element of a right-hand run,
+// the weight of smaller keys in the left-hand run.
+//
+// Outputs per (group, bin): the count / weight of accesses whose D falls in
+// the bin (bins cut at the batch's capacity values), and the count / weight
+// of blocks whose final stack depth (the weight of distinct blocks accessed
+// at or after their last access) falls in the bin; cumulative over bins on
+// return, so hits(C) is one lookup.
+#include "kv_device.h"
+#include "kv_internal.h"
+
+namespace kv {
+namespace {
+
+constexpr int kLocNT = 512;
+constexpr int kLocItems = 16;
+static_assert(kLocNT * kLocItems == (int)kSdB, "block tile mismatch");
+constexpr uint32_t kSentinel = 0xFFFFFFFFu;
+constexpr uint32_t kRowChunk = 16384;   // LDS histogram bins per row chunk
+constexpr uint32_t kColRows = 64;       // rows per column-scan chunk
+constexpr uint32_t kThrLds = 6144;      // thresholds kept in LDS for binning
+
+__host__ __device__ __forceinline__ uint64_t tri_off(uint64_t x) { return x * (x - 1) / 2; }
+
+// ---------------------------------------------------------------------------
+// Q rows: Q[X][Y] for Y < X, inclusive prefix over ceil(key / 8192).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_sd_rowhist(const uint32_t* __restrict__ key,
+                                                    const uint8_t* __restrict__ w8, uint64_t n,
+                                                    uint32_t* __restrict__ Q) {
+  __shared__ uint32_t h[kRowChunk];
+  __shared__ uint32_t sh[8];
+  const uint32_t X = blockIdx.x;
+  if (X == 0) return;
+  const uint64_t base = (uint64_t)X * kSdB;
+  const uint32_t nb = (uint32_t)min<uint64_t>(kSdB, n - base);
+  const uint64_t row = tri_off(X);
+  for (uint32_t c0 = 0; c0 < X; c0 += kRowChunk) {
+    const uint32_t width = min(kRowChunk, X - c0);
+    for (uint32_t j = threadIdx.x; j < width; j += 256) h[j] = 0;
+    __syncthreads();
+    uint32_t carry = 0;
+    for (uint32_t j = threadIdx.x; j < nb; j += 256) {
+      const uint32_t c = (key[base + j] + (kSdB - 1)) >> kSdLogB;
+      const uint32_t w = w8[base + j];
+      if (c < c0) carry += w;
+      else if (c < c0 + width) atomicAdd(&h[c - c0], w);
+    }
+    carry = block_sum<256>(carry, sh);
+    // inclusive scan of h[0, width) in LDS, each thread a contiguous run
+    const uint32_t per = (width + 255) / 256;
+    const uint32_t a = min(width, threadIdx.x * per), b = min(width, a + per);
+    uint32_t run = 0;
+    for (uint32_t j = a; j < b; ++j) run += h[j];
+    uint32_t tot;
+    uint32_t pre = block_excl_scan<256>(run, sh, &tot) + carry;
+    for (uint32_t j = a; j < b; ++j) {
+      pre += h[j];
+      h[j] = pre;
+    }
+    __syncthreads();
+    for (uint32_t j = threadIdx.x; j < width; j += 256) Q[row + c0 + j] = h[j];
+    __syncthreads();
+  }
+}
+
+// Column sums of Q over chunks of kColRows rows (only rows X > Y count).
+__global__ __launch_bounds__(256) void k_sd_colsum(const uint32_t* __restrict__ Q, uint32_t G,
+                                                   uint32_t* __restrict__ csum) {
+  const uint32_t Y = blockIdx.x * 256 + threadIdx.x;
+  const uint32_t c = blockIdx.y;
+  if (Y >= G) return;
+  const uint32_t x0 = max(Y + 1, c * kColRows), x1 = min(G, (c + 1) * kColRows);
+  uint32_t s = 0;
+  for (uint32_t X = x0; X < x1; ++X) s += Q[tri_off(X) + Y];
+  csum[(uint64_t)c * G + Y] = s;
+}
+
+__global__ __launch_bounds__(256) void k_sd_colchunks(uint32_t* __restrict__ csum, uint32_t G,
+                                                      uint32_t nchunks) {
+  const uint32_t Y = blockIdx.x * 256 + threadIdx.x;
+  if (Y >= G) return;
+  uint32_t run = 0;
+  for (uint32_t c = 0; c < nchunks; ++c) {
+    const uint32_t v = csum[(uint64_t)c * G + Y];
+    csum[(uint64_t)c * G + Y] = run;
+    run += v;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_sd_colapply(uint32_t* __restrict__ Q, uint32_t G,
+                                                     const uint32_t* __restrict__ csum) {
+  const uint32_t Y = blockIdx.x * 256 + threadIdx.x;
+  const uint32_t c = blockIdx.y;
+  if (Y >= G) return;
+  const uint32_t x0 = max(Y + 1, c * kColRows), x1 = min(G, (c + 1) * kColRows);
+  uint32_t run = csum[(uint64_t)c * G + Y];
+  for (uint32_t X = x0; X < x1; ++X) {
+    run += Q[tri_off(X) + Y];
+    Q[tri_off(X) + Y] = run;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// In-block dominance by LDS merge sort.
+// ---------------------------------------------------------------------------
+struct SortLds {
+  uint32_t v[kSdB];     // sorted keys of the current runs
+  uint32_t pw[kSdB];    // inclusive prefix weight inside each run
+  uint32_t acc[kSdB];   // accumulated weight of smaller keys at earlier positions
+  uint16_t idx[kSdB];   // local position of the element
+};
+
+template <int N>
+__device__ __forceinline__ void cswap(uint32_t (&v)[N], uint32_t (&w)[N], uint32_t (&a)[N],
+                                      uint32_t (&x)[N], int i, int l, bool up) {
+  const bool sw = (v[i] > v[l]) == up;
+  if (sw) {
+    uint32_t t;
+    t = v[i]; v[i] = v[l]; v[l] = t;
+    t = w[i]; w[i] = w[l]; w[l] = t;
+    t = a[i]; a[i] = a[l]; a[l] = t;
+    t = x[i]; x[i] = x[l]; x[l] = t;
+  }
+}
+
+// On return S holds the block's elements sorted by v, each with
+// acc = sum over earlier positions j of w_j [v_j < v] (exact whenever v is
+// unique in the block, i.e. for every element whose acc is used).
+__device__ void block_sort_dominance(SortLds& S, const uint32_t (&vin)[kLocItems],
+                                     const uint32_t (&win)[kLocItems]) {
+  const uint32_t t = threadIdx.x;
+  uint32_t v[kLocItems], w[kLocItems], a[kLocItems], x[kLocItems];
+#pragma unroll
+  for (int e = 0; e < kLocItems; ++e) {
+    v[e] = vin[e];
+    w[e] = win[e];
+    x[e] = t * kLocItems + e;
+    uint32_t s = 0;
+#pragma unroll
+    for (int f = 0; f < e; ++f) s += (vin[f] < vin[e]) ? win[f] : 0u;
+    a[e] = s;
+  }
+  // bitonic network on 16 register-resident elements
+#pragma unroll
+  for (int k = 2; k <= kLocItems; k <<= 1) {
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1) {
+#pragma unroll
+      for (int i = 0; i < kLocItems; ++i) {
+        const int l = i ^ j;
+        if (l > i) cswap<kLocItems>(v, w, a, x, i, l, (i & k) == 0);
+      }
+    }
+  }
+  uint32_t run = 0;
+#pragma unroll
+  for (int e = 0; e < kLocItems; ++e) {
+    run += w[e];
+    const uint32_t s = t * kLocItems + e;
+    S.v[s] = v[e];
+    S.pw[s] = run;
+    S.acc[s] = a[e];
+    S.idx[s] = (uint16_t)x[e];
+  }
+  uint32_t pw[kLocItems];
+  for (uint32_t s = kLocItems; s < kSdB; s <<= 1) {
+    __syncthreads();
+    const uint32_t o0 = t * kLocItems;
+    const uint32_t pair = o0 & ~(2 * s - 1);
+    const uint32_t d0 = o0 - pair;
+    const uint32_t Lb = pair, Rb = pair + s;
+    uint32_t lo = d0 > s ? d0 - s : 0u, hi = min(d0, s);
+    while (lo < hi) {
+      const uint32_t mid = (lo + hi) >> 1;
+      if (S.v[Lb + mid] <= S.v[Rb + d0 - mid - 1]) lo = mid + 1; else hi = mid;
+    }
+    uint32_t ia = lo, ib = d0 - lo;
+#pragma unroll
+    for (int e = 0; e < kLocItems; ++e) {
+      const bool takeL = (ib >= s) || (ia < s && S.v[Lb + ia] <= S.v[Rb + ib]);
+      if (takeL) {
+        v[e] = S.v[Lb + ia];
+        a[e] = S.acc[Lb + ia];
+        x[e] = S.idx[Lb + ia];
+        pw[e] = S.pw[Lb + ia] + (ib ? S.pw[Rb + ib - 1] : 0u);
+        ++ia;
+      } else {
+        const uint32_t pl = ia ? S.pw[Lb + ia - 1] : 0u;
+        v[e] = S.v[Rb + ib];
+        a[e] = S.acc[Rb + ib] + pl;
+        x[e] = S.idx[Rb + ib];
+        pw[e] = pl + S.pw[Rb + ib];
+        ++ib;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < kLocItems; ++e) {
+      const uint32_t o = o0 + e;
+      S.v[o] = v[e];
+      S.acc[o] = a[e];
+      S.idx[o] = (uint16_t)x[e];
+      S.pw[o] = pw[e];
+    }
+  }
+  __syncthreads();
+}
+
+// Per position block: A(i) and same-block distances -> partial[i]; E(p) for
+// positions whose next access lies in a later block.
+__global__ __launch_bounds__(kLocNT, 1) void k_sd_local(const uint32_t* __restrict__ key,
+                                                        const uint32_t* __restrict__ nxt,
+                                                        const uint8_t* __restrict__ w8,
+                                                        uint64_t n, uint32_t G,
+                                                        uint32_t* __restrict__ partial,
+                                                        uint32_t* __restrict__ E) {
+  __shared__ SortLds S;
+  __shared__ uint32_t P[kSdB];
+  __shared__ uint32_t sh[kLocNT / 64 + 1];
+  const uint32_t X = blockIdx.x;
+  const uint64_t base = (uint64_t)X * kSdB;
+  const uint32_t nb = (uint32_t)min<uint64_t>(kSdB, n - base);
+  const uint32_t t = threadIdx.x;
+  for (uint32_t j = t; j < kSdB; j += kLocNT) {
+    const bool in = j < nb;
+    S.v[j] = in ? key[base + j] : kSentinel;
+    S.acc[j] = in ? nxt[base + j] : kNone;
+    S.pw[j] = in ? (uint32_t)w8[base + j] : 0u;
+  }
+  __syncthreads();
+  uint32_t k[kLocItems], nx[kLocItems], w[kLocItems];
+#pragma unroll
+  for (int e = 0; e < kLocItems; ++e) {
+    const uint32_t j = t * kLocItems + e;
+    k[e] = S.v[j];
+    nx[e] = S.acc[j];
+    w[e] = S.pw[j];
+  }
+  __syncthreads();
+  // Wloc (inclusive, position order) -> P;  same-block-next prefix -> sn
+  uint32_t loc[kLocItems], sn[kLocItems];
+  uint32_t run = 0, run2 = 0;
+#pragma unroll
+  for (int e = 0; e < kLocItems; ++e) {
+    run += w[e];
+    loc[e] = run;
+    sn[e] = run2;
+    const bool same = nx[e] != kNone && (nx[e] >> kSdLogB) == X;
+    run2 += same ? w[e] : 0u;
+  }
+  uint32_t tot;
+  const uint32_t pre = block_excl_scan<kLocNT>(run, sh, &tot);
+  const uint32_t pre2 = block_excl_scan<kLocNT>(run2, sh, &tot);
+#pragma unroll
+  for (int e = 0; e < kLocItems; ++e) {
+    P[t * kLocItems + e] = loc[e] + pre;
+    sn[e] += pre2;
+  }
+  // ---- sort 1: keys -> A(i)
+  block_sort_dominance(S, k, w);
+#pragma unroll
+  for (int e = 0; e < kLocItems; ++e) {
+    const uint32_t s = t * kLocItems + e;
+    const uint32_t i = S.idx[s];
+    const uint32_t kk = S.v[s];
+    if (i < nb && kk != 0u) {
+      const uint32_t wi = S.pw[s] - (s ? S.pw[s - 1] : 0u);
+      const uint32_t p = kk - 1u;
+      uint32_t d = wi + S.acc[s];
+      if ((uint64_t)p >= base) d -= P[p - base];
+      partial[base + i] = d;
+    }
+  }
+  // Cnt_X(p) - Wloc(p) for positions whose next access is in a later block
+  uint32_t ev[kLocItems];
+#pragma unroll
+  for (int e = 0; e < kLocItems; ++e) {
+    const uint32_t lp = t * kLocItems + e;
+    ev[e] = 0;
+    if (lp < nb && nx[e] != kNone && (nx[e] >> kSdLogB) > X) {
+      const uint32_t p = (uint32_t)(base + lp);
+      const uint32_t ub = upper_bound(S.v, 0u, kSdB, p);
+      ev[e] = (ub ? S.pw[ub - 1] : 0u) - P[lp];
+    }
+  }
+  __syncthreads();
+  // ---- sort 2: (block of next access, reversed position) -> C(p)
+  uint32_t v2[kLocItems];
+#pragma unroll
+  for (int e = 0; e < kLocItems; ++e) {
+    const uint32_t lp = t * kLocItems + e;
+    const uint32_t nbk = (nx[e] == kNone) ? G : (nx[e] >> kSdLogB);
+    v2[e] = (lp < nb) ? ((nbk << kSdLogB) | (kSdB - 1u - lp)) : kSentinel;
+  }
+  block_sort_dominance(S, v2, w);
+#pragma unroll
+  for (int e = 0; e < kLocItems; ++e) {
+    const uint32_t s = t * kLocItems + e;
+    const uint32_t i = S.idx[s];
+    if (i < nb) P[i] = S.acc[s];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int e = 0; e < kLocItems; ++e) {
+    const uint32_t lp = t * kLocItems + e;
+    if (lp < nb && nx[e] != kNone && (nx[e] >> kSdLogB) > X)
+      E[base + lp] = ev[e] + (P[lp] - sn[e]);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Assembly of cross-block distances and binning.
+// ---------------------------------------------------------------------------
+struct BinArgs {
+  const uint32_t* thr;   // thresholds of all groups, concatenated
+  const uint32_t* off;   // [n_groups + 1]
+  uint32_t n_thr, n_groups;
+  uint64_t* hist;        // u64[bins][4]
+};
+
+template <bool kLds>
+__global__ __launch_bounds__(256) void k_sd_assemble(const uint32_t* __restrict__ key,
+                                                     const uint8_t* __restrict__ w8,
+                                                     const uint8_t* __restrict__ g8, uint64_t n,
+                                                     uint32_t G,
+                                                     const uint32_t* __restrict__ partial,
+                                                     const uint32_t* __restrict__ E,
+                                                     const uint32_t* __restrict__ RQ,
+                                                     BinArgs ba) {
+  __shared__ uint32_t sthr[kLds ? kThrLds : 1];
+  __shared__ uint32_t scnt[kLds ? kThrLds + KV_MAX_GROUPS : 1];
+  __shared__ uint32_t sw[kLds ? kThrLds + KV_MAX_GROUPS : 1];
+  __shared__ uint32_t soff[KV_MAX_GROUPS + 1];
+  const uint32_t nbins = ba.n_thr + ba.n_groups;
+  if (threadIdx.x <= ba.n_groups) soff[threadIdx.x] = ba.off[threadIdx.x];
+  if (kLds) {
+    for (uint32_t j = threadIdx.x; j < ba.n_thr; j += 256) sthr[j] = ba.thr[j];
+    for (uint32_t j = threadIdx.x; j < nbins; j += 256) {
+      scnt[j] = 0;
+      sw[j] = 0;
+    }
+  }
+  __syncthreads();
+  for (uint32_t X = blockIdx.x; X < G; X += gridDim.x) {
+    const uint64_t base = (uint64_t)X * kSdB;
+    const uint32_t nb = (uint32_t)min<uint64_t>(kSdB, n - base);
+    const uint64_t row = X >= 2 ? tri_off(X - 1) : 0;
+    for (uint32_t j = threadIdx.x; j < nb; j += 256) {
+      const uint64_t i = base + j;
+      const uint32_t kk = key[i];
+      if (kk == 0) continue;
+      const uint32_t p = kk - 1u;
+      const uint32_t Pb = p >> kSdLogB;
+      uint32_t d = partial[i];
+      if (Pb < X) {
+        d += E[p];
+        if (Pb + 1 < X) d += RQ[row + Pb];
+      }
+      const uint32_t g = g8[i];
+      const uint32_t w = w8[i];
+      const uint32_t lo = soff[g], hi = soff[g + 1];
+      if (kLds) {
+        const uint32_t b = lower_bound(sthr, lo, hi, d) - lo;
+        const uint32_t bin = lo + g + b;
+        atomicAdd(&scnt[bin], 1u);
+        atomicAdd(&sw[bin], w);
+      } else {
+        const uint32_t b = lower_bound(ba.thr, lo, hi, d) - lo;
+        const uint32_t bin = lo + g + b;
+        atomicAdd((unsigned long long*)&ba.hist[bin * 4 + 0], 1ull);
+        atomicAdd((unsigned long long*)&ba.hist[bin * 4 + 1], (unsigned long long)w);
+      }
+    }
+  }
+  if (kLds) {
+    __syncthreads();
+    for (uint32_t j = threadIdx.x; j < nbins; j += 256) {
+      if (scnt[j]) {
+        atomicAdd((unsigned long long*)&ba.hist[j * 4 + 0], (unsigned long long)scnt[j]);
+        atomicAdd((unsigned long long*)&ba.hist[j * 4 + 1], (unsigned long long)sw[j]);
+      }
+    }
+  }
+}
+
+// weight of last occurrences, position order (scanned afterwards)
+__global__ __launch_bounds__(256) void k_sd_lastw(const uint32_t* __restrict__ nxt,
+                                                  const uint8_t* __restrict__ w8, uint64_t n,
+                                                  uint32_t* __restrict__ lw) {
+  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (uint64_t)gridDim.x * blockDim.x)
+    lw[i] = nxt[i] == kNone ? (uint32_t)w8[i] : 0u;
+}
+
+struct SegArgs {
+  uint64_t seg[KV_MAX_GROUPS + 1];
+  uint32_t partitioned;
+};
+
+// Final stack depth of each block = weight of distinct blocks whose last
+// access is at or after its own (inside its segment); bin it.
+template <bool kLds>
+__global__ __launch_bounds__(256) void k_sd_finocc(const uint32_t* __restrict__ nxt,
+                                                   const uint8_t* __restrict__ w8,
+                                                   const uint8_t* __restrict__ g8, uint64_t n,
+                                                   const uint32_t* __restrict__ S,
+                                                   SegArgs sa, BinArgs ba) {
+  __shared__ uint32_t sthr[kLds ? kThrLds : 1];
+  __shared__ uint32_t scnt[kLds ? kThrLds + KV_MAX_GROUPS : 1];
+  __shared__ uint32_t sw[kLds ? kThrLds + KV_MAX_GROUPS : 1];
+  __shared__ uint32_t soff[KV_MAX_GROUPS + 1];
+  __shared__ uint32_t send[KV_MAX_GROUPS];
+  const uint32_t nbins = ba.n_thr + ba.n_groups;
+  if (threadIdx.x <= ba.n_groups) soff[threadIdx.x] = ba.off[threadIdx.x];
+  if (threadIdx.x < KV_MAX_GROUPS) {
+    const uint64_t e = sa.partitioned ? sa.seg[threadIdx.x + 1] : n;
+    const uint64_t b = sa.partitioned ? sa.seg[threadIdx.x] : 0;
+    send[threadIdx.x] = (e > b) ? S[e - 1] : 0u;
+  }
+  if (kLds) {
+    for (uint32_t j = threadIdx.x; j < ba.n_thr; j += 256) sthr[j] = ba.thr[j];
+    for (uint32_t j = threadIdx.x; j < nbins; j += 256) {
+      scnt[j] = 0;
+      sw[j] = 0;
+    }
+  }
+  __syncthreads();
+  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (uint64_t)gridDim.x * blockDim.x) {
+    if (nxt[i] != kNone) continue;
+    const uint32_t g = g8[i];
+    const uint32_t w = w8[i];
+    const uint32_t segend = sa.partitioned ? send[g] : send[0];
+    const uint32_t depth = segend - (S[i] - w);
+    const uint32_t lo = soff[g], hi = soff[g + 1];
+    if (kLds) {
+      const uint32_t bin = lo + g + (lower_bound(sthr, lo, hi, depth) - lo);
+      atomicAdd(&scnt[bin], 1u);
+      atomicAdd(&sw[bin], w);
+    } else {
+      const uint32_t bin = lo + g + (lower_bound(ba.thr, lo, hi, depth) - lo);
+      atomicAdd((unsigned long long*)&ba.hist[bin * 4 + 2], 1ull);
+      atomicAdd((unsigned long long*)&ba.hist[bin * 4 + 3], (unsigned long long)w);
+    }
+  }
+  if (kLds) {
+    __syncthreads();
+    for (uint32_t j = threadIdx.x; j < nbins; j += 256) {
+      if (scnt[j]) {
+        atomicAdd((unsigned long long*)&ba.hist[j * 4 + 2], (unsigned long long)scnt[j]);
+        atomicAdd((unsigned long long*)&ba.hist[j * 4 + 3], (unsigned long long)sw[j]);
+      }
+    }
+  }
+}
+
+// cumulative over the bins of each group, one thread per (group, field)
+__global__ void k_hist_cum(uint64_t* hist, const uint32_t* __restrict__ off, uint32_t n_groups) {
+  const uint32_t g = threadIdx.x / 4, f = threadIdx.x % 4;
+  if (g >= n_groups) return;
+  const uint32_t b0 = off[g] + g, b1 = off[g + 1] + g + 1;
+  uint64_t run = 0;
+  for (uint32_t b = b0; b < b1; ++b) {
+    run += hist[b * 4 + f];
+    hist[b * 4 + f] = run;
+  }
+}
+
+uint32_t grid_of(uint64_t m, uint32_t cap = 32768) {
+  uint64_t g = (m + 255) / 256;
+  if (g > cap) g = cap;
+  return (uint32_t)(g ? g : 1);
+}
+
+}  // namespace
+
+kv_status stack_pass(Trace& t, Order& o, bool partitioned, const ThresholdSet& ts,
+                     const uint32_t* thr_dev, const uint32_t* off_dev, uint64_t* hist,
+                     hipStream_t s) {
+  const uint64_t n = t.n;
+  const uint32_t G = div_up(n, kSdB);
+  kv_status st;
+  const uint64_t tri = G >= 2 ? tri_off(G) : 1;
+  const uint32_t nchunks = div_up(G, kColRows);
+  DevBuf& b_partial = t.ws[0];
+  DevBuf& b_E = t.ws[1];
+  DevBuf& b_Q = t.ws[2];
+  DevBuf& b_csum = t.ws[3];
+  DevBuf& b_scan = t.ws[4];
+  if ((st = b_partial.reserve(n * 4)) != KV_OK) return st;
+  if ((st = b_E.reserve(n * 4)) != KV_OK) return st;
+  if ((st = b_Q.reserve(tri * 4)) != KV_OK) return st;
+  if ((st = b_csum.reserve((uint64_t)nchunks * G * 4)) != KV_OK) return st;
+  if ((st = b_scan.reserve(std::max<uint64_t>(scan_scratch_elems(n), 1) * 4)) != KV_OK) return st;
+  const uint32_t* key = o.key.as<uint32_t>();
+  const uint32_t* nxt = o.nxt.as<uint32_t>();
+  const uint8_t* w8 = o.w.as<uint8_t>();
+  const uint8_t* g8 = o.g.as<uint8_t>();
+  uint32_t* Q = b_Q.as<uint32_t>();
+  if (G >= 2) {
+    hipLaunchKernelGGL(k_sd_rowhist, dim3(G), dim3(256), 0, s, key, w8, n, Q);
+    KV_HIP(hipGetLastError());
+    const dim3 cg(div_up(G, 256), nchunks);
+    hipLaunchKernelGGL(k_sd_colsum, cg, dim3(256), 0, s, Q, G, b_csum.as<uint32_t>());
+    KV_HIP(hipGetLastError());
+    hipLaunchKernelGGL(k_sd_colchunks, dim3(div_up(G, 256)), dim3(256), 0, s,
+                       b_csum.as<uint32_t>(), G, nchunks);
+    KV_HIP(hipGetLastError());
+    hipLaunchKernelGGL(k_sd_colapply, cg, dim3(256), 0, s, Q, G,
+                       (const uint32_t*)b_csum.as<uint32_t>());
+    KV_HIP(hipGetLastError());
+  }
+  hipLaunchKernelGGL(k_sd_local, dim3(G), dim3(kLocNT), 0, s, key, nxt, w8, n, G,
+                     b_partial.as<uint32_t>(), b_E.as<uint32_t>());
+  KV_HIP(hipGetLastError());
+  BinArgs ba{thr_dev, off_dev, (uint32_t)ts.values.size(), ts.n_groups, hist};
+  const bool lds = ts.values.size() + ts.n_groups <= kThrLds;
+  const uint32_t ga = std::min<uint32_t>(G, 2048);
+  if (lds)
+    hipLaunchKernelGGL(k_sd_assemble<true>, dim3(ga), dim3(256), 0, s, key, w8, g8, n, G,
+                       (const uint32_t*)b_partial.as<uint32_t>(),
+                       (const uint32_t*)b_E.as<uint32_t>(), (const uint32_t*)Q, ba);
+  else
+    hipLaunchKernelGGL(k_sd_assemble<false>, dim3(ga), dim3(256), 0, s, key, w8, g8, n, G,
+                       (const uint32_t*)b_partial.as<uint32_t>(),
+                       (const uint32_t*)b_E.as<uint32_t>(), (const uint32_t*)Q, ba);
+  KV_HIP(hipGetLastError());
+  // final occupancy: reuse `partial` for the scanned last-occurrence weights
+  uint32_t* S = b_partial.as<uint32_t>();
+  hipLaunchKernelGGL(k_sd_lastw, dim3(grid_of(n)), dim3(256), 0, s, nxt, w8, n, S);
+  KV_HIP(hipGetLastError());
+  if ((st = scan_u32(S, S, n, true, b_scan.as<uint32_t>(), s)) != KV_OK) return st;
+  SegArgs sa{};
+  for (int g = 0; g <= KV_MAX_GROUPS; ++g) sa.seg[g] = o.seg[g];
+  sa.partitioned = partitioned ? 1u : 0u;
+  const uint32_t gf = grid_of(n, 2048);
+  if (lds)
+    hipLaunchKernelGGL(k_sd_finocc<true>, dim3(gf), dim3(256), 0, s, nxt, w8, g8, n,
+                       (const uint32_t*)S, sa, ba);
+  else
+    hipLaunchKernelGGL(k_sd_finocc<false>, dim3(gf), dim3(256), 0, s, nxt, w8, g8, n,
+                       (const uint32_t*)S, sa, ba);
+  KV_HIP(hipGetLastError());
+  hipLaunchKernelGGL(k_hist_cum, dim3(1), dim3(4 * KV_MAX_GROUPS), 0, s, hist, off_dev,
+                     ts.n_groups);
+  KV_HIP(hipGetLastError());
+  return KV_OK;
+}
+
+}  // namespace kv

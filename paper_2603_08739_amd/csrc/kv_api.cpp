@@ -1,0 +1,416 @@
+// kv_api.cpp - the C ABI of libkvcfg: validation, planning and launch order.
+//
+// kv_trace_load canonicalises a trace once; kv_eval_configs then evaluates a
+// batch of candidate tier configurations (the planner's candidates and the
+// simulator's per-candidate evaluation, Section 4.1):
+//   1. host: validate, then collect the capacities the LRU configurations
+//      need, per access order and group (the thresholds of the stack pass);
+//   2. device: one stack-distance pass per needed order (k_stack.hip) and the
+//      closed-form LRU records (k_eval.hip);
+//   3. device: one replay per distinct (order, group, policy, capacity) for
+//      FIFO / LFU tiers, combined per configuration (k_replay.hip);
+//   4. device: (cost, throughput, latency) per configuration (Eq. 1, Eq. 2).
+// kv_pareto is the selector's dominance filter (Section 4.1).
+#include <algorithm>
+#include <atomic>
+#include <cmath>
+#include <cstdlib>
+#include <map>
+#include <mutex>
+#include <set>
+#include <tuple>
+
+#include "kv_internal.h"
+
+namespace kv {
+
+namespace {
+thread_local std::string g_last_error;
+std::mutex g_reg_mu;
+std::set<const void*> g_live;  // live trace handles
+std::atomic<uint64_t> g_bytes{0};
+
+uint64_t mem_cap() {
+  // Test hook: cap the bytes this library may hold on the device, so that
+  // the out-of-memory path can be exercised without exhausting the GPU.
+  static const uint64_t cap = [] {
+    const char* e = std::getenv("KVCFG_TEST_MEM_CAP");
+    return e ? std::strtoull(e, nullptr, 10) : 0ull;
+  }();
+  return cap;
+}
+
+bool is_live(const void* t) {
+  std::lock_guard<std::mutex> lk(g_reg_mu);
+  return g_live.count(t) != 0;
+}
+}  // namespace
+
+kv_status fail(kv_status s, const std::string& msg) {
+  g_last_error = msg;
+  return s;
+}
+
+kv_status hip_fail(hipError_t e, const char* what) {
+  if (e == hipErrorOutOfMemory) return fail(KV_ERR_NOMEM, std::string("out of device memory: ") + what);
+  return fail(KV_ERR_DEVICE, std::string(hipGetErrorString(e)) + " in " + what);
+}
+
+kv_status DevBuf::reserve(size_t b) {
+  if (b <= bytes && p) return KV_OK;
+  release();
+  if (b == 0) b = 1;
+  const uint64_t cap = mem_cap();
+  if (cap && g_bytes.load() + b > cap)
+    return fail(KV_ERR_NOMEM, "device memory cap reached (test limit)");
+  void* q = nullptr;
+  hipError_t e = hipMalloc(&q, b);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(KV_ERR_NOMEM, "hipMalloc of " + std::to_string(b) + " bytes failed");
+  }
+  p = q;
+  bytes = b;
+  g_bytes += b;
+  return KV_OK;
+}
+
+void DevBuf::release() {
+  if (p) {
+    (void)hipFree(p);
+    g_bytes -= bytes;
+  }
+  p = nullptr;
+  bytes = 0;
+}
+
+namespace {
+
+bool finite_pos(double x) { return std::isfinite(x) && x > 0; }
+bool finite_nonneg(double x) { return std::isfinite(x) && x >= 0; }
+
+kv_status validate_model(const kv_cost_model* m) {
+  if (!m) return fail(KV_ERR_INVALID, "kv_eval_configs: model is NULL");
+  if (!finite_nonneg(m->price_gpu_per_hour) || !finite_nonneg(m->price_per_gib_hour[0]) ||
+      !finite_nonneg(m->price_per_gib_hour[1]) || !finite_nonneg(m->price_per_gib_hour[2]))
+    return fail(KV_ERR_INVALID, "kv_eval_configs: prices must be finite and >= 0");
+  if (!finite_pos(m->bw_dram) || !finite_pos(m->ssd_bw_base) || !finite_pos(m->ssd_bw_max) ||
+      !finite_nonneg(m->ssd_bw_per_gib) || !finite_pos(m->t_prefill_per_token))
+    return fail(KV_ERR_INVALID, "kv_eval_configs: bandwidths and t_prefill must be finite and > 0");
+  return KV_OK;
+}
+
+uint32_t group_policy(const kv_config& c, uint32_t g) {
+  return c.partitioned ? c.policy[g] : c.policy[0];
+}
+
+uint64_t group_cap(const kv_config& c, int k, uint32_t g) {
+  return c.partitioned ? c.cap_group[k][g] : c.cap[k];
+}
+
+kv_status validate_configs(const Trace& t, const kv_config* cfg, uint32_t n_cfg) {
+  const uint32_t G = t.n_groups;
+  const uint64_t wmax = t.st.w_max;
+  for (uint32_t c = 0; c < n_cfg; ++c) {
+    const kv_config& C = cfg[c];
+    const std::string at = "kv_eval_configs: config " + std::to_string(c) + ": ";
+    if (C.mode > KV_MODE_EXCLUSIVE_DEMOTE) return fail(KV_ERR_INVALID, at + "unknown mode");
+    if (C.partitioned > 1) return fail(KV_ERR_INVALID, at + "partitioned must be 0 or 1");
+    for (int r = 0; r < 6; ++r)
+      if (C.reserved[r]) return fail(KV_ERR_INVALID, at + "reserved bytes must be zero");
+    for (int k = 0; k < 3; ++k)
+      if (C.cap[k] != 0 && C.cap[k] < wmax)
+        return fail(KV_ERR_INVALID, at + "a tier capacity is below the largest block weight");
+    const uint32_t ng = C.partitioned ? G : 1;
+    for (uint32_t g = 0; g < ng; ++g)
+      if (C.policy[g] > KV_POLICY_LFU) return fail(KV_ERR_INVALID, at + "unknown policy");
+    if (C.partitioned) {
+      for (int k = 0; k < 3; ++k) {
+        uint64_t sum = 0;
+        for (uint32_t g = 0; g < G; ++g) {
+          const uint64_t x = C.cap_group[k][g];
+          if (x != 0 && x < wmax)
+            return fail(KV_ERR_INVALID, at + "a group capacity is below the largest block weight");
+          sum += x;
+          if (sum < x) return fail(KV_ERR_INVALID, at + "group capacities overflow");
+        }
+        if (sum > C.cap[k]) return fail(KV_ERR_INVALID, at + "group capacities exceed the tier");
+      }
+    }
+    if (C.mode == KV_MODE_EXCLUSIVE_DEMOTE) {
+      for (uint32_t g = 0; g < ng; ++g)
+        if (C.policy[g] != KV_POLICY_LRU)
+          return fail(KV_ERR_UNSUPPORTED, at + "the exclusive mode supports LRU only");
+      if (t.st.w_min != t.st.w_max)
+        return fail(KV_ERR_UNSUPPORTED, at + "the exclusive mode needs uniform block weights");
+    }
+  }
+  return KV_OK;
+}
+
+uint32_t clamp32(uint64_t x) { return x > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)x; }
+
+// Capacities the closed-form LRU records will look up, per group.
+void add_thresholds(std::vector<std::vector<uint32_t>>& per_group, const kv_config& C, uint32_t g,
+                    uint32_t slot, uint64_t w0) {
+  if (C.mode == KV_MODE_INCLUSIVE) {
+    for (int k = 0; k < 3; ++k) {
+      const uint64_t x = group_cap(C, k, g);
+      if (x) per_group[slot].push_back(clamp32(x));
+    }
+  } else {
+    uint64_t S = 0;
+    for (int k = 0; k < 3; ++k) {
+      const uint64_t x = group_cap(C, k, g);
+      if (!x) continue;
+      S += x / w0;
+      per_group[slot].push_back(clamp32(S * w0));
+    }
+  }
+}
+
+void finish_set(ThresholdSet& ts, std::vector<std::vector<uint32_t>>& per_group, uint32_t G) {
+  ts.values.clear();
+  ts.n_groups = G;
+  ts.off[0] = 0;
+  for (uint32_t g = 0; g < G; ++g) {
+    auto& v = per_group[g];
+    std::sort(v.begin(), v.end());
+    v.erase(std::unique(v.begin(), v.end()), v.end());
+    ts.values.insert(ts.values.end(), v.begin(), v.end());
+    ts.off[g + 1] = (uint32_t)ts.values.size();
+  }
+  for (uint32_t g = G + 1; g <= KV_MAX_GROUPS; ++g) ts.off[g] = ts.off[G];
+}
+
+struct StackSlot {
+  int ws_thr, ws_hist;
+};
+
+kv_status run_stack(Trace& t, Order& o, bool partitioned, ThresholdSet& ts, StackSlot slot,
+                    OrderView& view, hipStream_t s) {
+  kv_status st;
+  DevBuf& bt = t.ws[slot.ws_thr];
+  DevBuf& bh = t.ws[slot.ws_hist];
+  const uint64_t nthr = ts.values.size();
+  if ((st = bt.reserve((nthr + KV_MAX_GROUPS + 1) * 4)) != KV_OK) return st;
+  const uint64_t nbins = ts.total_bins();
+  if ((st = bh.reserve(nbins * 4 * 8)) != KV_OK) return st;
+  uint32_t* thr = bt.as<uint32_t>();
+  uint32_t* off = thr + nthr;
+  if (nthr) KV_HIP(hipMemcpyAsync(thr, ts.values.data(), nthr * 4, hipMemcpyHostToDevice, s));
+  KV_HIP(hipMemcpyAsync(off, ts.off, (KV_MAX_GROUPS + 1) * 4, hipMemcpyHostToDevice, s));
+  if ((st = fill_u64(bh.as<uint64_t>(), 0, nbins * 4, s)) != KV_OK) return st;
+  if ((st = stack_pass(t, o, partitioned, ts, thr, off, bh.as<uint64_t>(), s)) != KV_OK) return st;
+  view.thr = thr;
+  view.off = off;
+  view.hist = bh.as<uint64_t>();
+  return KV_OK;
+}
+
+}  // namespace
+}  // namespace kv
+
+using namespace kv;
+
+extern "C" {
+
+const char* kv_last_error(void) { return kv::g_last_error.c_str(); }
+
+kv_status kv_trace_load(const kv_trace_desc* d, void* stream, kv_trace** out) {
+  if (!out) return fail(KV_ERR_INVALID, "kv_trace_load: out is NULL");
+  *out = nullptr;
+  if (!d) return fail(KV_ERR_INVALID, "kv_trace_load: desc is NULL");
+  if (d->n < 1 || d->n > kMaxN)
+    return fail(KV_ERR_INVALID, "kv_trace_load: n must be in [1, 2^29]");
+  if (!d->hash || !d->req || !d->req_time)
+    return fail(KV_ERR_INVALID, "kv_trace_load: hash, req and req_time are required");
+  if (d->n_req < 1) return fail(KV_ERR_INVALID, "kv_trace_load: n_req must be >= 1");
+  if (d->n_groups < 1 || d->n_groups > KV_MAX_GROUPS)
+    return fail(KV_ERR_INVALID, "kv_trace_load: n_groups must be in [1, 16]");
+  if (d->tokens_per_granule < 1 || d->granule_bytes < 1)
+    return fail(KV_ERR_INVALID, "kv_trace_load: tokens_per_granule and granule_bytes must be >= 1");
+  hipStream_t s = (hipStream_t)stream;
+  Trace* t = new Trace();
+  KV_HIP(hipGetDevice(&t->device));
+  kv_status st = canon_build(*t, *d, s);
+  if (st == KV_OK && t->st.n_w >= 0xFFFFFFFFull) {
+    st = fail(KV_ERR_UNSUPPORTED, "kv_trace_load: total weight must stay below 2^32 granules");
+  }
+  if (st != KV_OK) {
+    (void)hipStreamSynchronize(s);
+    delete t;
+    return st;
+  }
+  t->magic = kTraceMagic;
+  t->gb = d->granule_bytes;
+  t->tpg = d->tokens_per_granule;
+  {
+    std::lock_guard<std::mutex> lk(g_reg_mu);
+    g_live.insert(t);
+  }
+  *out = reinterpret_cast<kv_trace*>(t);
+  return KV_OK;
+}
+
+kv_status kv_trace_free(kv_trace* h) {
+  if (!h) return KV_OK;
+  Trace* t = reinterpret_cast<Trace*>(h);
+  {
+    std::lock_guard<std::mutex> lk(g_reg_mu);
+    if (!g_live.count(t)) return fail(KV_ERR_INVALID, "kv_trace_free: not a live trace handle");
+    g_live.erase(t);
+  }
+  (void)hipDeviceSynchronize();
+  t->magic = kDeadMagic;
+  delete t;
+  return KV_OK;
+}
+
+kv_status kv_trace_info(const kv_trace* h, kv_trace_stats* out) {
+  if (!h || !out) return fail(KV_ERR_INVALID, "kv_trace_info: NULL argument");
+  const Trace* t = reinterpret_cast<const Trace*>(h);
+  if (!is_live(t)) return fail(KV_ERR_INVALID, "kv_trace_info: not a live trace handle");
+  *out = t->st;
+  return KV_OK;
+}
+
+kv_status kv_eval_configs(const kv_trace* h, const kv_config* cfg, uint32_t n_cfg,
+                          const kv_cost_model* model, uint64_t* counts, double* obj,
+                          void* stream) {
+  if (!h) return fail(KV_ERR_INVALID, "kv_eval_configs: trace is NULL");
+  Trace* t = const_cast<Trace*>(reinterpret_cast<const Trace*>(h));
+  if (!is_live(t)) return fail(KV_ERR_INVALID, "kv_eval_configs: not a live trace handle");
+  kv_status st;
+  if ((st = validate_model(model)) != KV_OK) return st;
+  if (n_cfg == 0) return KV_OK;
+  if (!cfg || !counts) return fail(KV_ERR_INVALID, "kv_eval_configs: cfg and counts are required");
+  if ((st = validate_configs(*t, cfg, n_cfg)) != KV_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  const uint32_t G = t->n_groups;
+  t->cfg_stage.assign(cfg, cfg + n_cfg);
+
+  // ---- plan: thresholds per order, replay jobs
+  std::vector<std::vector<uint32_t>> tsh(G), tpt(G);
+  bool need_shared = false, need_part = false;
+  const uint64_t w0 = t->st.w_max;
+  std::map<std::tuple<uint32_t, uint32_t, uint32_t, uint64_t>, uint32_t> job_index;
+  std::vector<ReplayJob> jobs;
+  for (uint32_t c = 0; c < n_cfg; ++c) {
+    const kv_config& C = cfg[c];
+    const bool part_order = C.partitioned && G > 1;
+    const uint32_t ng = C.partitioned ? G : 1;
+    for (uint32_t g = 0; g < ng; ++g) {
+      const uint32_t pol = group_policy(C, g);
+      if (pol == KV_POLICY_LRU) {
+        if (part_order) {
+          need_part = true;
+          add_thresholds(tpt, C, g, g, w0);
+        } else {
+          need_shared = true;
+          if (C.partitioned) {
+            add_thresholds(tsh, C, g, 0, w0);
+          } else {
+            for (uint32_t gg = 0; gg < G; ++gg) add_thresholds(tsh, C, 0, gg, w0);
+          }
+        }
+        continue;
+      }
+      for (int k = 0; k < 3; ++k) {
+        const uint64_t x = group_cap(C, k, g);
+        if (!x) continue;
+        const uint32_t ord = part_order ? 1u : 0u;
+        const uint32_t grp = part_order ? g : (uint32_t)KV_MAX_GROUPS;
+        auto key = std::make_tuple(ord, grp, pol, x);
+        if (job_index.count(key)) continue;
+        job_index[key] = (uint32_t)jobs.size();
+        ReplayJob j{};
+        j.order = ord;
+        j.group = grp;
+        j.policy = pol;
+        j.cap = x;
+        const uint64_t dw = part_order ? t->st.u_w_g[g] : t->st.distinct_w;
+        j.closed = x >= dw ? 1u : 0u;
+        jobs.push_back(j);
+      }
+    }
+  }
+  if (need_part || (!jobs.empty() && G > 1)) {
+    if ((st = canon_partition(*t, s)) != KV_OK) return st;
+  }
+  for (auto& j : jobs) {
+    const Order& o = j.order ? t->part : t->shared;
+    j.begin = j.order ? o.seg[j.group] : 0;
+    j.end = j.order ? o.seg[j.group + 1] : t->n;
+  }
+
+  // ---- device copies of the batch and per-group statistics
+  DevBuf& bcfg = t->ws[9];
+  DevBuf& bgs = t->ws[10];
+  if ((st = bcfg.reserve((uint64_t)n_cfg * sizeof(kv_config))) != KV_OK) return st;
+  if ((st = bgs.reserve(sizeof(GroupStats) * KV_MAX_GROUPS)) != KV_OK) return st;
+  for (uint32_t g = 0; g < KV_MAX_GROUPS; ++g)
+    t->gs_stage[g] = GroupStats{t->st.n_g[g], t->st.n_w_g[g], t->st.u_g[g], w0};
+  KV_HIP(hipMemcpyAsync(bcfg.p, t->cfg_stage.data(), (uint64_t)n_cfg * sizeof(kv_config),
+                        hipMemcpyHostToDevice, s));
+  KV_HIP(hipMemcpyAsync(bgs.p, t->gs_stage, sizeof(t->gs_stage), hipMemcpyHostToDevice, s));
+  const kv_config* cfg_dev = bcfg.as<kv_config>();
+
+  // ---- LRU: stack-distance passes + closed forms
+  OrderView vsh, vpt;
+  if (need_shared) {
+    finish_set(t->shared_ts, tsh, G);
+    if ((st = run_stack(*t, t->shared, false, t->shared_ts, StackSlot{5, 6}, vsh, s)) != KV_OK)
+      return st;
+  }
+  if (need_part) {
+    finish_set(t->part_ts, tpt, G);
+    if ((st = run_stack(*t, t->part, true, t->part_ts, StackSlot{7, 8}, vpt, s)) != KV_OK)
+      return st;
+  }
+  if (need_shared || need_part) {
+    if ((st = lru_counts(cfg_dev, n_cfg, G, vsh, vpt, bgs.as<GroupStats>(), counts, s)) != KV_OK)
+      return st;
+  }
+  // ---- FIFO / LFU: replay jobs
+  if (!jobs.empty()) {
+    if ((st = replay_run(*t, jobs, cfg, cfg_dev, n_cfg, counts, s)) != KV_OK) return st;
+  }
+  // ---- objectives
+  if (obj) {
+    st = objectives(cfg_dev, n_cfg, G, counts, *model, (double)t->gb, (double)t->tpg,
+                    t->st.span, (double)t->st.n_req, t->st.n_w, obj, s);
+    if (st != KV_OK) return st;
+  }
+  return KV_OK;
+}
+
+kv_status kv_pareto(const double* obj, const uint32_t* segment, uint32_t n, const double* bounds,
+                    uint8_t* on_front, uint32_t* n_front, void* stream) {
+  if (n == 0) {
+    if (n_front) *n_front = 0;
+    return KV_OK;
+  }
+  if (!obj || !on_front) return fail(KV_ERR_INVALID, "kv_pareto: obj and on_front are required");
+  if (n > (1u << 26)) return fail(KV_ERR_INVALID, "kv_pareto: n must be <= 2^26");
+  hipStream_t s = (hipStream_t)stream;
+  uint32_t* counters = nullptr;
+  KV_HIP(hipMallocAsync((void**)&counters, 2 * sizeof(uint32_t), s));
+  kv_status st = fill_u32(counters, 0, 2, s);
+  if (st == KV_OK) st = pareto(obj, segment, n, bounds, on_front, counters, s);
+  uint32_t hc[2] = {0, 0};
+  if (st == KV_OK && n_front) {
+    hipError_t e = hipMemcpyAsync(hc, counters, sizeof(hc), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) st = hip_fail(e, "kv_pareto result copy");
+  }
+  (void)hipFreeAsync(counters, s);
+  if (st != KV_OK) return st;
+  if (n_front) {
+    *n_front = hc[0];
+    if (hc[1]) return fail(KV_ERR_INVALID, "kv_pareto: an objective is NaN");
+  }
+  return KV_OK;
+}
+
+}  // extern "C"

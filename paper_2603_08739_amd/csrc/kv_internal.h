@@ -1,0 +1,153 @@
+// kv_internal.h - internal declarations shared by the HIP translation units
+// of libkvcfg (never installed; the public contract is include/kvcfg.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "../../include/kvcfg.h"
+
+namespace kv {
+
+constexpr uint32_t kNone = 0xFFFFFFFFu;
+constexpr int kSdLogB = 13;                 // stack-distance position block: 8192
+constexpr uint32_t kSdB = 1u << kSdLogB;
+constexpr uint64_t kMaxN = 1ull << 29;
+
+// ---------------------------------------------------------------------------
+// error state
+// ---------------------------------------------------------------------------
+kv_status fail(kv_status s, const std::string& msg);
+kv_status hip_fail(hipError_t e, const char* what);
+
+#define KV_HIP(call)                                          \
+  do {                                                        \
+    hipError_t e_ = (call);                                   \
+    if (e_ != hipSuccess) return ::kv::hip_fail(e_, #call);   \
+  } while (0)
+
+// A device allocation owned by its holder.
+struct DevBuf {
+  void* p = nullptr;
+  size_t bytes = 0;
+  DevBuf() = default;
+  DevBuf(const DevBuf&) = delete;
+  DevBuf& operator=(const DevBuf&) = delete;
+  ~DevBuf() { release(); }
+  void release();
+  // Grow to at least `b` bytes (contents are not preserved on growth).
+  kv_status reserve(size_t b);
+  template <class T>
+  T* as() const { return static_cast<T*>(p); }
+};
+
+// One order of the accesses: the trace order, or the accesses regrouped
+// stably by tenant group (for per-group partitioned caches).
+struct Order {
+  DevBuf key;   // u32[n]: previous occurrence + 1 in this order, 0 = first access
+  DevBuf nxt;   // u32[n]: next occurrence in this order, kNone = last access
+  DevBuf bid;   // u32[n]: dense block id
+  DevBuf w;     // u8[n]
+  DevBuf g;     // u8[n]
+  uint64_t seg[KV_MAX_GROUPS + 1] = {0};  // group segments (partitioned order)
+  bool built = false;
+};
+
+struct ThresholdSet {
+  // thresholds (granules, clamped to u32) per group, concatenated; bins per
+  // group = count + 1 (the last bin collects distances above every threshold)
+  std::vector<uint32_t> values;
+  uint32_t off[KV_MAX_GROUPS + 1] = {0};  // thresholds of group g: [off[g], off[g+1])
+  uint32_t n_groups = 1;
+  uint32_t total_bins() const { return off[n_groups] + n_groups; }
+  uint32_t bin_base(uint32_t g) const { return off[g] + g; }
+};
+
+struct GroupStats {
+  uint64_t n_g, n_w_g, u_g, w0;  // accesses, weight, distinct blocks, uniform weight
+};
+
+struct Trace {
+  uint64_t magic = 0;
+  int device = 0;
+  kv_trace_stats st{};
+  uint64_t n = 0, u = 0;
+  uint32_t n_groups = 1;
+  uint64_t gb = 0;    // granule bytes
+  uint32_t tpg = 0;   // tokens per granule
+  Order shared;       // trace order
+  Order part;         // partitioned order (built on first use when n_groups > 1)
+  DevBuf blk_w;       // u8[u]  weight per dense block id
+  DevBuf blk_g;       // u8[u]  group per dense block id
+  // workspace reused across kv_eval_configs calls on this trace
+  DevBuf ws[24];
+  // host staging of the latest kv_eval_configs call (alive across its copies)
+  ThresholdSet shared_ts, part_ts;
+  std::vector<kv_config> cfg_stage;
+  GroupStats gs_stage[KV_MAX_GROUPS];
+  std::vector<uint8_t> job_stage, rec_stage;
+  std::vector<unsigned long long> jc_stage;
+};
+
+constexpr uint64_t kTraceMagic = 0x6b7663666774726bull;  // "kvcfgtrk"
+constexpr uint64_t kDeadMagic = 0x646561646b766366ull;
+
+// ---------------------------------------------------------------------------
+// launchers (each defined in the .hip file that holds its kernels)
+// ---------------------------------------------------------------------------
+// exclusive (inclusive=false) or inclusive prefix sum of u32, any length;
+// `scratch` holds scan_scratch_elems(m) u32 of device memory.  in == out is allowed.
+uint64_t scan_scratch_elems(uint64_t m);
+kv_status scan_u32(const uint32_t* in, uint32_t* out, uint64_t m, bool inclusive,
+                   uint32_t* scratch, hipStream_t s);
+kv_status fill_u32(uint32_t* p, uint32_t v, uint64_t m, hipStream_t s);
+kv_status fill_u64(uint64_t* p, uint64_t v, uint64_t m, hipStream_t s);
+
+// canonicalisation (k_canon.hip)
+kv_status canon_build(Trace& t, const kv_trace_desc& d, hipStream_t s);
+kv_status canon_partition(Trace& t, hipStream_t s);
+
+// stack-distance pass (k_stack.hip)
+// hist: u64[total_bins][4] = {count, weight, final count, final weight},
+// made cumulative over the bins of each group on return.
+// thr_dev / off_dev: device copies of ts.values / ts.off; hist must be zeroed.
+kv_status stack_pass(Trace& t, Order& o, bool partitioned, const ThresholdSet& ts,
+                     const uint32_t* thr_dev, const uint32_t* off_dev, uint64_t* hist,
+                     hipStream_t s);
+
+// per-configuration evaluation (k_eval.hip)
+
+// Device view of one order's threshold sets and cumulative histograms.
+struct OrderView {
+  const uint32_t* thr = nullptr;
+  const uint32_t* off = nullptr;
+  const uint64_t* hist = nullptr;
+};
+// Writes the records of every (config, group) whose policy is LRU.  Groups of
+// partitioned configs read `part` when n_groups > 1, `shared` otherwise.
+kv_status lru_counts(const kv_config* cfg_dev, uint32_t n_cfg, uint32_t n_groups,
+                     OrderView shared, OrderView part, const GroupStats* gs_dev,
+                     uint64_t* counts, hipStream_t s);
+kv_status objectives(const kv_config* cfg_dev, uint32_t n_cfg, uint32_t n_groups,
+                     const uint64_t* counts, const kv_cost_model& m, double gb, double tpg,
+                     double span, double n_req, uint64_t n_w, double* obj, hipStream_t s);
+kv_status pareto(const double* obj, const uint32_t* segment, uint32_t n, const double* bounds,
+                 uint8_t* flag, uint32_t* counters_dev, hipStream_t s);
+
+// replay of non-LRU policies (k_replay.hip)
+struct ReplayJob {
+  uint32_t order;     // 0 = trace order, 1 = partitioned order
+  uint32_t group;     // partitioned: the group; shared: KV_MAX_GROUPS
+  uint32_t policy;    // KV_POLICY_FIFO or KV_POLICY_LFU
+  uint32_t closed;    // 1: capacity covers every distinct block -> no replay
+  uint64_t cap;       // granules
+  uint64_t begin, end;  // positions [begin, end) in the order
+};
+kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_config* cfg_host,
+                     const kv_config* cfg_dev, uint32_t n_cfg, uint64_t* counts,
+                     hipStream_t s);
+
+}  // namespace kv

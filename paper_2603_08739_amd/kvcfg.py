@@ -1,0 +1,201 @@
+"""ctypes binding of libkvcfg (include/kvcfg.h): argument marshalling only.
+
+Every computation runs in the HIP library; this module converts torch device
+tensors and numpy host arrays into the C structs and pointers of the ABI.
+PyTorch serves as the device allocator and the source of the current HIP
+stream.  If the compiled library is missing the import fails: there is no
+fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libkvcfg.so")
+
+KV_OK, KV_ERR_INVALID, KV_ERR_NOMEM, KV_ERR_DEVICE, KV_ERR_UNSUPPORTED = 0, -1, -2, -3, -4
+KV_MAX_GROUPS, KV_TIERS, KV_FIELDS = 16, 3, 8
+KV_MODE_INCLUSIVE, KV_MODE_EXCLUSIVE_DEMOTE = 0, 1
+KV_POLICY_LRU, KV_POLICY_FIFO, KV_POLICY_LFU = 0, 1, 2
+FIELDS = ("hit", "miss", "ins", "evict", "hit_w", "miss_w", "ins_w", "evict_w")
+
+_u64, _u32, _u8, _f64, _vp = (ctypes.c_uint64, ctypes.c_uint32, ctypes.c_uint8,
+                              ctypes.c_double, ctypes.c_void_p)
+
+
+class kv_trace_desc(ctypes.Structure):
+    _fields_ = [("n", _u64), ("hash", _vp), ("req", _vp), ("group", _vp), ("weight", _vp),
+                ("n_req", _u32), ("req_time", _vp), ("n_groups", _u32),
+                ("tokens_per_granule", _u32), ("granule_bytes", _u64)]
+
+
+class kv_trace_stats(ctypes.Structure):
+    _fields_ = [("n", _u64), ("n_distinct", _u64), ("n_w", _u64), ("distinct_w", _u64),
+                ("n_g", _u64 * KV_MAX_GROUPS), ("n_w_g", _u64 * KV_MAX_GROUPS),
+                ("u_g", _u64 * KV_MAX_GROUPS), ("u_w_g", _u64 * KV_MAX_GROUPS),
+                ("max_multiplicity", _u64), ("n_req", _u32), ("n_groups", _u32),
+                ("w_min", _u32), ("w_max", _u32), ("span", _f64)]
+
+
+class kv_config(ctypes.Structure):
+    _fields_ = [("cap", _u64 * KV_TIERS), ("cap_group", (_u64 * KV_MAX_GROUPS) * KV_TIERS),
+                ("mode", _u8), ("partitioned", _u8), ("policy", _u8 * KV_MAX_GROUPS),
+                ("reserved", _u8 * 6)]
+
+
+class kv_cost_model(ctypes.Structure):
+    _fields_ = [("price_gpu_per_hour", _f64), ("price_per_gib_hour", _f64 * KV_TIERS),
+                ("bw_dram", _f64), ("ssd_bw_base", _f64), ("ssd_bw_per_gib", _f64),
+                ("ssd_bw_max", _f64), ("t_prefill_per_token", _f64)]
+
+
+assert ctypes.sizeof(kv_config) == 432
+
+
+class KvError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"[{status}] {msg}")
+        self.status = status
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run python -m paper_2603_08739_amd.build")
+    lib = ctypes.CDLL(LIB_PATH)
+    lib.kv_trace_load.restype = ctypes.c_int
+    lib.kv_trace_load.argtypes = [ctypes.POINTER(kv_trace_desc), _vp, ctypes.POINTER(_vp)]
+    lib.kv_trace_free.restype = ctypes.c_int
+    lib.kv_trace_free.argtypes = [_vp]
+    lib.kv_trace_info.restype = ctypes.c_int
+    lib.kv_trace_info.argtypes = [_vp, ctypes.POINTER(kv_trace_stats)]
+    lib.kv_eval_configs.restype = ctypes.c_int
+    lib.kv_eval_configs.argtypes = [_vp, _vp, _u32, ctypes.POINTER(kv_cost_model), _vp, _vp, _vp]
+    lib.kv_pareto.restype = ctypes.c_int
+    lib.kv_pareto.argtypes = [_vp, _vp, _u32, _vp, _vp, ctypes.POINTER(_u32), _vp]
+    lib.kv_last_error.restype = ctypes.c_char_p
+    lib.kv_last_error.argtypes = []
+    return lib
+
+
+LIB = _load()
+EXPORTS = ("kv_trace_load", "kv_trace_free", "kv_trace_info", "kv_eval_configs", "kv_pareto",
+           "kv_last_error")
+
+
+def kv_last_error() -> str:
+    return LIB.kv_last_error().decode()
+
+
+def _check(status: int):
+    if status != KV_OK:
+        raise KvError(status, kv_last_error())
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, int):
+        return ctypes.c_void_p(stream)
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+class Trace:
+    """A device-resident canonical trace (owns the kv_trace handle)."""
+
+    def __init__(self, handle):
+        self.handle = handle
+
+    def info(self) -> kv_trace_stats:
+        st = kv_trace_stats()
+        _check(LIB.kv_trace_info(self.handle, ctypes.byref(st)))
+        return st
+
+    def free(self):
+        if self.handle is not None:
+            _check(LIB.kv_trace_free(self.handle))
+            self.handle = None
+
+    def __del__(self):
+        try:
+            if self.handle is not None:
+                LIB.kv_trace_free(self.handle)
+        except Exception:
+            pass
+
+
+def kv_trace_load(hash, req, req_time, group=None, weight=None, n_groups=1,
+                  tokens_per_granule=16, granule_bytes=128 * 1024, stream=None) -> Trace:
+    """hash: int64/uint64 device tensor [n]; req: int32 [n]; req_time: float64 [n_req];
+    group, weight: uint8 [n] or None."""
+    d = kv_trace_desc()
+    d.n = int(hash.numel())
+    d.hash = _ptr(hash)
+    d.req = _ptr(req)
+    d.group = _ptr(group)
+    d.weight = _ptr(weight)
+    d.n_req = int(req_time.numel())
+    d.req_time = _ptr(req_time)
+    d.n_groups = int(n_groups)
+    d.tokens_per_granule = int(tokens_per_granule)
+    d.granule_bytes = int(granule_bytes)
+    h = ctypes.c_void_p()
+    _check(LIB.kv_trace_load(ctypes.byref(d), _stream(stream), ctypes.byref(h)))
+    return Trace(h)
+
+
+def config_array(cap, cap_group, mode, partitioned, policy):
+    """numpy arrays (n,3) (n,3,16) (n,) (n,) (n,16) -> ctypes kv_config[n]."""
+    n = int(np.asarray(cap).shape[0])
+    arr = (kv_config * max(n, 1))()
+    raw = np.frombuffer(arr, dtype=np.uint8).reshape(max(n, 1), 432)
+    if n:
+        raw[:n, 0:24] = np.ascontiguousarray(cap, dtype=np.uint64).view(np.uint8).reshape(n, 24)
+        raw[:n, 24:408] = np.ascontiguousarray(cap_group, dtype=np.uint64).view(
+            np.uint8).reshape(n, 384)
+        raw[:n, 408] = np.asarray(mode, dtype=np.uint8)
+        raw[:n, 409] = np.asarray(partitioned, dtype=np.uint8)
+        raw[:n, 410:426] = np.asarray(policy, dtype=np.uint8)
+        raw[:n, 426:432] = 0
+    return arr, n
+
+
+def cost_model(price_gpu_per_hour, price_per_gib_hour, bw_dram, ssd_bw_base, ssd_bw_per_gib,
+               ssd_bw_max, t_prefill_per_token) -> kv_cost_model:
+    m = kv_cost_model()
+    m.price_gpu_per_hour = price_gpu_per_hour
+    for k in range(3):
+        m.price_per_gib_hour[k] = price_per_gib_hour[k]
+    m.bw_dram = bw_dram
+    m.ssd_bw_base = ssd_bw_base
+    m.ssd_bw_per_gib = ssd_bw_per_gib
+    m.ssd_bw_max = ssd_bw_max
+    m.t_prefill_per_token = t_prefill_per_token
+    return m
+
+
+def kv_eval_configs(trace: Trace, cfg_arr, n_cfg: int, model: kv_cost_model, counts, obj=None,
+                    stream=None):
+    """counts: int64/uint64 device tensor [n_cfg, n_groups, 3, 8]; obj: float64 [n_cfg, 3]."""
+    _check(LIB.kv_eval_configs(trace.handle, ctypes.cast(cfg_arr, _vp), n_cfg,
+                               ctypes.byref(model), _ptr(counts), _ptr(obj), _stream(stream)))
+
+
+def kv_pareto(obj, on_front, segment=None, bounds=None, want_count=True, stream=None):
+    """obj: float64 device [n,3]; on_front: uint8 device [n]; segment: int32/uint32 device [n]."""
+    n = int(obj.shape[0])
+    b = None
+    if bounds is not None:
+        barr = (ctypes.c_double * 3)(*[float(x) for x in bounds])
+        b = ctypes.cast(barr, _vp)
+    cnt = _u32(0)
+    _check(LIB.kv_pareto(_ptr(obj), _ptr(segment), n, b, _ptr(on_front),
+                         ctypes.byref(cnt) if want_count else None, _stream(stream)))
+    return int(cnt.value) if want_count else None

@@ -1,0 +1,205 @@
+"""GPU parity: the HIP library against the CPU oracle, element by element.
+
+Integer counts must be identical; objectives within 1e-6 relative (both
+sides evaluate the same IEEE-double expression without contraction, so they
+are expected to agree exactly); Pareto membership identical.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import tracegen as tg
+
+pytestmark = pytest.mark.gpu
+
+RTOL = 1e-6
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a device"
+    from paper_2603_08739_amd import host, kvcfg
+    return host, kvcfg
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def compare(lib, O, trace, cfgs, cost=tg.DEFAULT_COST, label=""):
+    host, _ = lib
+    say(f"  case {label}: n={trace.n} groups={trace.n_groups} configs={cfgs.n}")
+    h = host.load(trace)
+    counts, obj = host.evaluate(h, cfgs, cost, trace.n_groups)
+    h.free()
+    ref = O.replay(trace, cfgs)
+    ref_obj = O.objectives(trace, cfgs, ref, cost)
+    if not np.array_equal(counts, ref):
+        bad = np.argwhere(counts != ref)
+        c, g, k, f = bad[0]
+        raise AssertionError(
+            f"{label}: {len(bad)} count mismatches; first cfg={c} group={g} tier={k} "
+            f"field={f}: gpu={counts[c, g, k, f]} oracle={ref[c, g, k, f]} "
+            f"cap={cfgs.cap[c]} mode={cfgs.mode[c]} pol={cfgs.policy[c, :3]} "
+            f"part={cfgs.partitioned[c]}\n gpu={counts[c, g]}\n ref={ref[c, g]}")
+    np.testing.assert_allclose(obj, ref_obj, rtol=RTOL, atol=0, err_msg=label)
+    return counts, obj, ref_obj
+
+
+def test_belady_and_hand_cases(lib, oracle_mod):
+    t = tg.from_blocks([1, 2, 3, 4, 1, 2, 5, 1, 2, 3, 4, 5])
+    cfgs = tg.from_list([{"cap": (c, 0, 0), "policy": p} for c in (1, 2, 3, 4, 5) for p in range(3)]
+                        + [{"cap": (1, 2, 3), "policy": p} for p in range(3)]
+                        + [{"cap": (2, 1, 3), "mode": 1}, {"cap": (0, 3, 1), "mode": 1}])
+    counts, _, _ = compare(lib, oracle_mod, t, cfgs, label="belady")
+    assert counts[6, 0, 0, 1] == 10 and counts[7, 0, 0, 1] == 9   # LRU@3, FIFO@3 misses
+
+
+def test_single_access_and_constant_traces(lib, oracle_mod):
+    for blocks in ([7], [7, 7, 7, 7], list(range(50)), [3, 1] * 40):
+        t = tg.from_blocks(blocks)
+        cfgs = tg.from_list([{"cap": (1, 0, 0), "policy": p} for p in range(3)]
+                            + [{"cap": (2, 5, 100), "policy": p} for p in range(3)]
+                            + [{"cap": (1, 1, 1), "mode": 1}])
+        compare(lib, oracle_mod, t, cfgs, label=f"blocks{len(blocks)}")
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_random_small(lib, oracle_mod, seed):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(1, 3000))
+    groups = int(rng.choice([1, 1, 2, 3, 5]))
+    weights = (1,) if seed % 3 else (1, 4)
+    t = tg.random_trace(seed, n, int(rng.integers(1, 400)), n_groups=groups,
+                        weight_choices=weights, zipf_s=float(rng.choice([0, 0.7, 1.2])),
+                        reuse_bias=float(rng.choice([0, 0.3])))
+    cfgs = tg.random_configs(seed, 24, groups, max(weights), int(rng.integers(8, 600)))
+    compare(lib, oracle_mod, t, cfgs, label=f"rand{seed}")
+    if weights == (1,):
+        ex = tg.random_configs(seed + 1000, 16, groups, 1, int(rng.integers(4, 400)),
+                               exclusive=True)
+        compare(lib, oracle_mod, t, ex, label=f"rand{seed}-excl")
+
+
+@pytest.mark.parametrize("n", [8191, 8192, 8193, 16384 + 5, 3 * 8192 + 77])
+def test_block_boundaries(lib, oracle_mod, n):
+    """Traces that end at, just before and just after an 8192-position block."""
+    t = tg.random_trace(n, n, 2500, n_groups=2, weight_choices=(1, 4), zipf_s=0.9)
+    cfgs = tg.random_configs(n, 20, 2, 4, 4000, policies=(0,))
+    compare(lib, oracle_mod, t, cfgs, label=f"n{n}")
+
+
+def test_long_reuse_many_blocks(lib, oracle_mod):
+    """Reuse distances spanning many position blocks (cross-block matrix path)."""
+    t = tg.random_trace(77, 120_000, 30_000, weight_choices=(1, 4), zipf_s=0.6)
+    cfgs = tg.from_list([{"cap": (c, d, s)} for c in (16, 600, 5000)
+                         for d in (0, 9000) for s in (0, 40000, 200000)])
+    compare(lib, oracle_mod, t, cfgs, label="longreuse")
+
+
+def test_tiny_workload_all_configs(lib, oracle_mod):
+    t = tg.tiny()
+    cfgs = tg.configs_for("tiny", t)
+    compare(lib, oracle_mod, t, cfgs, label="tiny-64")
+
+
+def test_tiny_workload_replay_policies(lib, oracle_mod):
+    t = tg.tiny(n_req=600)
+    base = tg.configs_for("tiny", t)
+    parts = []
+    for p in (tg.POLICY_FIFO, tg.POLICY_LFU):
+        c = base.subset(np.arange(0, 64, 5))
+        c.policy[:, :] = p
+        parts.append(c)
+    compare(lib, oracle_mod, t, tg.ConfigBatch.concat(parts), label="tiny-replay")
+
+
+def test_tenant_small_partitioned(lib, oracle_mod):
+    t = tg.tenant(total_req=3000)
+    cfgs = tg.configs_for("tenant", t)
+    # scale the capacities down so that the small trace sees evictions
+    small = cfgs.subset(np.arange(0, cfgs.n, 7))
+    small.cap //= 64
+    small.cap_group //= 64
+    small.cap_group[small.cap_group == 0] = 0
+    compare(lib, oracle_mod, t, small, label="tenant-small")
+
+
+def test_longctx_small_exclusive(lib, oracle_mod):
+    t = tg.longctx(n_req=400, n_docs=60)
+    cfgs = tg.configs_for("longctx", t).subset(np.arange(0, 2048, 37))
+    cfgs.cap //= 256
+    compare(lib, oracle_mod, t, cfgs, label="longctx-small")
+
+
+def test_full_small_mixed(lib, oracle_mod):
+    t = tg.full(n_req=4000)
+    cfgs = tg.configs_for("full", t)
+    pick = np.concatenate([np.arange(0, 10000, 397), np.arange(10000, 11000, 83)])
+    sub = cfgs.subset(pick)
+    sub.cap //= 16
+    sub.cap[(sub.cap > 0) & (sub.cap < 4)] = 4
+    compare(lib, oracle_mod, t, sub, label="full-small")
+
+
+def test_pareto_parity(lib, oracle_mod):
+    host, _ = lib
+    rng = np.random.default_rng(5)
+    for trial in range(30):
+        n = int(rng.integers(1, 700))
+        obj = rng.integers(0, 8, (n, 3)).astype(np.float64)
+        seg = rng.integers(0, 3, n).astype(np.uint32) if trial % 2 else None
+        bounds = None if trial % 3 else [6.0, 1.0, float("nan")]
+        say(f"  pareto trial {trial} n={n}")
+        f, cnt = host.pareto(obj, seg, bounds)
+        ref = oracle_mod.pareto(obj, seg, bounds)
+        np.testing.assert_array_equal(f, ref)
+        assert cnt == int(ref.sum())
+
+
+def test_pareto_on_objectives(lib, oracle_mod):
+    host, _ = lib
+    t = tg.tiny()
+    cfgs = tg.configs_for("tiny", t)
+    h = host.load(t)
+    _, obj = host.evaluate(h, cfgs, tg.DEFAULT_COST, 1)
+    h.free()
+    f, _ = host.pareto(obj)
+    np.testing.assert_array_equal(f, oracle_mod.pareto(obj))
+
+
+def test_error_paths(lib):
+    host, kvcfg = lib
+    import torch
+    # a hash that carries two weights
+    t = tg.from_blocks([1, 2, 1])
+    t.weight = np.array([1, 1, 4], dtype=np.uint8)
+    with pytest.raises(kvcfg.KvError) as e:
+        host.load(t)
+    assert e.value.status == kvcfg.KV_ERR_INVALID
+    t = tg.from_blocks([1, 2, 3, 1], weights={1: 4, 2: 4, 3: 1})
+    h = host.load(t)
+    st = h.info()
+    assert (st.n, st.n_distinct, st.w_min, st.w_max) == (4, 3, 1, 4)
+    for bad, status in [({"cap": (2, 0, 0)}, kvcfg.KV_ERR_INVALID),
+                        ({"cap": (8, 0, 0), "mode": 1}, kvcfg.KV_ERR_UNSUPPORTED),
+                        ({"cap": (8, 0, 0), "policy": 5}, kvcfg.KV_ERR_INVALID)]:
+        with pytest.raises(kvcfg.KvError) as e:
+            host.evaluate(h, tg.from_list([bad]), tg.DEFAULT_COST, 1)
+        assert e.value.status == status, bad
+    h.free()
+    obj = np.array([[1.0, 2.0, float("nan")], [1.0, 1.0, 1.0]])
+    with pytest.raises(kvcfg.KvError):
+        host.pareto(obj)
+    torch.cuda.synchronize()
+
+
+def test_double_free_detected(lib):
+    host, kvcfg = lib
+    h = host.load(tg.from_blocks([1, 2, 3]))
+    raw = h.handle
+    h.free()
+    assert kvcfg.LIB.kv_trace_free(raw) == kvcfg.KV_ERR_INVALID

@@ -214,3 +214,44 @@ DEFAULT_COST = {
     "ssd_bw_max": 4.0e9,
     "t_prefill_per_token": 1.0 / 20000.0,
 }
+
+
+def random_configs(seed: int, n: int, n_groups: int, w_max: int, cap_hi: int,
+                   policies=(POLICY_LRU, POLICY_FIFO, POLICY_LFU), exclusive: bool = False,
+                   partitioned_frac: float = 0.5, zero_frac: float = 0.25) -> ConfigBatch:
+    """Random candidate configurations for correctness tests.
+
+    Capacities are 0 (absent, with probability ``zero_frac``) or uniform in
+    [w_max, cap_hi]; with ``exclusive`` every configuration uses the
+    exclusive LRU hierarchy, otherwise the inclusive one with random policies.
+    """
+    rng = np.random.default_rng([seed, 7])
+    b = empty(n)
+
+    def cap():
+        if rng.random() < zero_frac:
+            return 0
+        return int(rng.integers(w_max, max(w_max, cap_hi) + 1))
+
+    for i in range(n):
+        caps = [cap() for _ in range(3)]
+        if not any(caps):
+            caps[int(rng.integers(0, 3))] = int(rng.integers(w_max, max(w_max, cap_hi) + 1))
+        part = n_groups > 1 and rng.random() < partitioned_frac
+        if exclusive:
+            b.mode[i] = MODE_EXCLUSIVE_DEMOTE
+            pol = [POLICY_LRU] * MAX_GROUPS
+        else:
+            pol = [int(rng.choice(policies)) for _ in range(MAX_GROUPS)]
+        b.policy[i] = pol
+        if part:
+            b.partitioned[i] = 1
+            for k in range(3):
+                tot = 0
+                for g in range(n_groups):
+                    x = cap() if caps[k] else 0
+                    b.cap_group[i, k, g] = x
+                    tot += x
+                caps[k] = max(caps[k], tot) if tot else caps[k]
+        b.cap[i] = caps
+    return b
