@@ -203,6 +203,26 @@ kv_status kv_pareto(const double* obj, const uint32_t* segment, uint32_t n,
 /* Message describing the calling thread's most recent failure ("" if none). */
 const char* kv_last_error(void);
 
+/* Device-time observability.  While enabled, every call records a pair of
+ * HIP events on its stream around each stage below; kv_timing_read waits for
+ * the recorded events and returns, per stage, the number of launches and the
+ * summed device milliseconds between each pair.  Process-wide; not meant for
+ * concurrent callers.  Stages:
+ *   0 load: validation        1 load: radix sort       2 load: links and ids
+ *   3 group-partitioned order 4 stack: block matrix    5 stack: in-block sort
+ *   6 stack: assembly, bins   7 stack: final depths    8 LRU records
+ *   9 replay: job setup       10 replay: jobs          11 replay: combine
+ *   12 objectives             13 Pareto filter */
+enum { KV_STAGES = 14 };
+typedef struct kv_timing {
+  uint64_t calls[KV_STAGES];
+  double ms[KV_STAGES];
+} kv_timing;
+
+kv_status kv_timing_enable(int on);
+/* Fill *out (host) with the totals since the last reset; reset if `reset`. */
+kv_status kv_timing_read(kv_timing* out, int reset);
+
 #ifdef __cplusplus
 }
 #endif

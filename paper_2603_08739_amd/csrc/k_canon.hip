@@ -346,6 +346,8 @@ kv_status canon_build(Trace& t, const kv_trace_desc& d, hipStream_t s) {
   KV_HIP(hipMemsetAsync(dstats, 0, sizeof(DevStats), s));
   KV_HIP(hipMemsetAsync(&dstats->w_min, 0xFF, 4, s));
 
+  {
+  StageTimer tm(kStLoadValidate, s);
   hipLaunchKernelGGL(k_validate, dim3(grid_of(n)), dim3(256), 0, s, d.hash, d.req, d.group,
                      d.weight, n, d.n_req, d.n_groups, o.g.as<uint8_t>(), o.w.as<uint8_t>(),
                      ka.as<uint64_t>(), va.as<uint32_t>(), dstats);
@@ -353,32 +355,41 @@ kv_status canon_build(Trace& t, const kv_trace_desc& d, hipStream_t s) {
   hipLaunchKernelGGL(k_check_times, dim3(std::min<uint32_t>(div_up(d.n_req, 256), 4096)),
                      dim3(256), 0, s, d.req_time, d.n_req, dstats);
   KV_HIP(hipGetLastError());
+  }
 
   // 8 stable passes of 8 bits: (hash, position) sorted by hash, ties by position
   uint64_t *kin = ka.as<uint64_t>(), *kout = kb.as<uint64_t>();
   uint32_t *vin = va.as<uint32_t>(), *vout = vb.as<uint32_t>();
-  for (int shift = 0; shift < 64; shift += 8) {
-    st = radix_pass(kin, vin, kout, vout, n, shift, counts.as<uint32_t>(),
-                    scratch.as<uint32_t>(), s);
-    if (st != KV_OK) return st;
-    std::swap(kin, kout);
-    std::swap(vin, vout);
+  {
+    StageTimer tm(kStLoadSort, s);
+    for (int shift = 0; shift < 64; shift += 8) {
+      st = radix_pass(kin, vin, kout, vout, n, shift, counts.as<uint32_t>(),
+                      scratch.as<uint32_t>(), s);
+      if (st != KV_OK) return st;
+      std::swap(kin, kout);
+      std::swap(vin, vout);
+    }
   }
   // kin / vin now hold the sorted pairs; the other pair of buffers is free.
   uint32_t* newflag = reinterpret_cast<uint32_t*>(kout);          // n u32
   uint32_t* incl = reinterpret_cast<uint32_t*>(kout) + n;         // n u32
+  uint32_t u32 = 0;
+  {
+  StageTimer tm(kStLoadLinks, s);
   hipLaunchKernelGGL(k_links, dim3(grid_of(n)), dim3(256), 0, s, kin, vin, n,
                      o.key.as<uint32_t>(), o.nxt.as<uint32_t>(), newflag, o.w.as<uint8_t>(),
                      o.g.as<uint8_t>(), dstats);
   KV_HIP(hipGetLastError());
   if ((st = scan_u32(newflag, incl, n, true, scratch.as<uint32_t>(), s)) != KV_OK) return st;
-  uint32_t u32 = 0;
+  }
   KV_HIP(hipMemcpyAsync(&u32, incl + (n - 1), 4, hipMemcpyDeviceToHost, s));
   KV_HIP(hipStreamSynchronize(s));
   const uint64_t u = u32;
   if ((st = t.blk_w.reserve(u)) != KV_OK) return st;
   if ((st = t.blk_g.reserve(u)) != KV_OK) return st;
   uint32_t* runstart = vout;  // n >= u entries available
+  {
+  StageTimer tm(kStLoadLinks, s);
   hipLaunchKernelGGL(k_ids, dim3(grid_of(n)), dim3(256), 0, s, vin, incl, newflag, n,
                      o.bid.as<uint32_t>(), t.blk_w.as<uint8_t>(), t.blk_g.as<uint8_t>(),
                      runstart, o.w.as<uint8_t>(), o.g.as<uint8_t>(), dstats);
@@ -386,6 +397,7 @@ kv_status canon_build(Trace& t, const kv_trace_desc& d, hipStream_t s) {
   hipLaunchKernelGGL(k_mult, dim3(grid_of(n)), dim3(256), 0, s, incl, newflag, n, runstart,
                      dstats);
   KV_HIP(hipGetLastError());
+  }
 
   DevStats hs;
   double t0 = 0, t1 = 0;
@@ -451,6 +463,7 @@ kv_status canon_partition(Trace& t, hipStream_t s) {
   if ((st = counts.reserve(ncount * 4)) != KV_OK) return st;
   if ((st = scratch.reserve(std::max<uint64_t>(scan_scratch_elems(ncount), 1) * 4)) != KV_OK)
     return st;
+  StageTimer tm(kStPartition, s);
   hipLaunchKernelGGL(k_group_keys, dim3(grid_of(n)), dim3(256), 0, s, o.g.as<uint8_t>(), n,
                      ka.as<uint64_t>(), va.as<uint32_t>());
   KV_HIP(hipGetLastError());

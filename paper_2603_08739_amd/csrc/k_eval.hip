@@ -213,6 +213,7 @@ kv_status lru_counts(const kv_config* cfg_dev, uint32_t n_cfg, uint32_t n_groups
                      uint64_t* counts, hipStream_t s) {
   const uint64_t m = (uint64_t)n_cfg * n_groups;
   if (m == 0) return KV_OK;
+  StageTimer tm(kStLruCounts, s);
   hipLaunchKernelGGL(k_lru_counts, dim3(div_up(m, 256)), dim3(256), 0, s, cfg_dev, n_cfg,
                      n_groups, shared, part, gs_dev, counts);
   KV_HIP(hipGetLastError());
@@ -226,6 +227,7 @@ kv_status objectives(const kv_config* cfg_dev, uint32_t n_cfg, uint32_t n_groups
   CostArgs a{m.price_gpu_per_hour, m.price_per_gib_hour[0], m.price_per_gib_hour[1],
              m.price_per_gib_hour[2], m.bw_dram, m.ssd_bw_base, m.ssd_bw_per_gib,
              m.ssd_bw_max, m.t_prefill_per_token, gb, tpg, span, n_req, n_w};
+  StageTimer tm(kStObjectives, s);
   hipLaunchKernelGGL(k_objectives, dim3(div_up(n_cfg, 256)), dim3(256), 0, s, cfg_dev, n_cfg,
                      n_groups, counts, a, obj);
   KV_HIP(hipGetLastError());
@@ -236,6 +238,7 @@ kv_status pareto(const double* obj, const uint32_t* segment, uint32_t n, const d
                  uint8_t* flag, uint32_t* counters_dev, hipStream_t s) {
   const double nan = __builtin_nan("");
   Bounds bd{bounds ? bounds[0] : nan, bounds ? bounds[1] : nan, bounds ? bounds[2] : nan};
+  StageTimer tm(kStPareto, s);
   hipLaunchKernelGGL(k_pareto, dim3(div_up(n, 256)), dim3(256), 0, s, obj, segment, n, bd, flag,
                      counters_dev);
   KV_HIP(hipGetLastError());

@@ -23,6 +23,7 @@
 //        oldest live member.
 #include <cstring>
 #include <map>
+#include <optional>
 #include <tuple>
 
 #include "kv_device.h"
@@ -521,6 +522,8 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
   uint64_t* reuse[2] = {ob, ob + per_order};
   uint64_t* planes[2] = {ob + nwords, ob + per_order + nwords};
   uint64_t* gmask[2] = {ob + 9 * nwords, ob + per_order + 9 * nwords};
+  std::optional<StageTimer> tm;
+  tm.emplace(kStReplayInit, s);
   for (int o = 0; o < 2; ++o) {
     const Order& od = o ? t.part : t.shared;
     if (o == 1 && !have_part) continue;
@@ -558,12 +561,16 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
     hipLaunchKernelGGL(k_replay_init, dim3(64, nj), dim3(256), 0, s, bj.as<JobDev>(),
                        bstate.as<uint64_t>(), bcls.as<uint32_t>(), ja);
     KV_HIP(hipGetLastError());
+    tm.reset();
+    tm.emplace(kStReplay, s);
     hipLaunchKernelGGL(k_replay, dim3(nj), dim3(64), 0, s, bj.as<JobDev>(), ja,
                        bstate.as<uint64_t>(), bcls.as<uint32_t>(), bbits.as<uint64_t>(),
                        bjc.as<unsigned long long>());
     KV_HIP(hipGetLastError());
   }
+  tm.reset();
   if (!recs.empty()) {
+    tm.emplace(kStCombine, s);
     CombineArgs ca{};
     ca.jobs = bj.as<JobDev>();
     ca.bits = bbits.as<uint64_t>();

@@ -526,6 +526,7 @@ kv_status stack_pass(Trace& t, Order& o, bool partitioned, const ThresholdSet& t
   const uint8_t* g8 = o.g.as<uint8_t>();
   uint32_t* Q = b_Q.as<uint32_t>();
   if (G >= 2) {
+    StageTimer tm(kStStackMatrix, s);
     hipLaunchKernelGGL(k_sd_rowhist, dim3(G), dim3(256), 0, s, key, w8, n, Q);
     KV_HIP(hipGetLastError());
     const dim3 cg(div_up(G, 256), nchunks);
@@ -538,12 +539,17 @@ kv_status stack_pass(Trace& t, Order& o, bool partitioned, const ThresholdSet& t
                        (const uint32_t*)b_csum.as<uint32_t>());
     KV_HIP(hipGetLastError());
   }
-  hipLaunchKernelGGL(k_sd_local, dim3(G), dim3(kLocNT), 0, s, key, nxt, w8, n, G,
-                     b_partial.as<uint32_t>(), b_E.as<uint32_t>());
-  KV_HIP(hipGetLastError());
+  {
+    StageTimer tm(kStStackLocal, s);
+    hipLaunchKernelGGL(k_sd_local, dim3(G), dim3(kLocNT), 0, s, key, nxt, w8, n, G,
+                       b_partial.as<uint32_t>(), b_E.as<uint32_t>());
+    KV_HIP(hipGetLastError());
+  }
   BinArgs ba{thr_dev, off_dev, (uint32_t)ts.values.size(), ts.n_groups, hist};
   const bool lds = ts.values.size() + ts.n_groups <= kThrLds;
   const uint32_t ga = std::min<uint32_t>(G, 2048);
+  {
+  StageTimer tm(kStStackAssemble, s);
   if (lds)
     hipLaunchKernelGGL(k_sd_assemble<true>, dim3(ga), dim3(256), 0, s, key, w8, g8, n, G,
                        (const uint32_t*)b_partial.as<uint32_t>(),
@@ -553,6 +559,8 @@ kv_status stack_pass(Trace& t, Order& o, bool partitioned, const ThresholdSet& t
                        (const uint32_t*)b_partial.as<uint32_t>(),
                        (const uint32_t*)b_E.as<uint32_t>(), (const uint32_t*)Q, ba);
   KV_HIP(hipGetLastError());
+  }
+  StageTimer tm(kStStackFinal, s);
   // final occupancy: reuse `partial` for the scanned last-occurrence weights
   uint32_t* S = b_partial.as<uint32_t>();
   hipLaunchKernelGGL(k_sd_lastw, dim3(grid_of(n)), dim3(256), 0, s, nxt, w8, n, S);

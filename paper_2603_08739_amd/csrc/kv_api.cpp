@@ -44,7 +44,44 @@ bool is_live(const void* t) {
   std::lock_guard<std::mutex> lk(g_reg_mu);
   return g_live.count(t) != 0;
 }
+
+// stage timing: recorded event pairs, resolved in kv_timing_read
+std::mutex g_tmu;
+bool g_timing = false;
+struct EvPair {
+  int stage;
+  hipEvent_t a, b;
+};
+std::vector<EvPair> g_pairs;
+std::vector<hipEvent_t> g_free_events;
+kv_timing g_acc{};
+
+hipEvent_t take_event() {
+  if (!g_free_events.empty()) {
+    hipEvent_t e = g_free_events.back();
+    g_free_events.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
 }  // namespace
+
+StageTimer::StageTimer(Stage st, hipStream_t stream) : slot(-1), s(stream) {
+  std::lock_guard<std::mutex> lk(g_tmu);
+  if (!g_timing) return;
+  hipEvent_t a = take_event(), b = take_event();
+  if (!a || !b) return;
+  if (hipEventRecord(a, s) != hipSuccess) return;
+  g_pairs.push_back(EvPair{(int)st, a, b});
+  slot = (int)g_pairs.size() - 1;
+}
+
+StageTimer::~StageTimer() {
+  std::lock_guard<std::mutex> lk(g_tmu);
+  if (slot >= 0 && slot < (int)g_pairs.size()) (void)hipEventRecord(g_pairs[slot].b, s);
+}
 
 kv_status fail(kv_status s, const std::string& msg) {
   g_last_error = msg;
@@ -216,6 +253,30 @@ using namespace kv;
 extern "C" {
 
 const char* kv_last_error(void) { return kv::g_last_error.c_str(); }
+
+kv_status kv_timing_enable(int on) {
+  std::lock_guard<std::mutex> lk(kv::g_tmu);
+  kv::g_timing = on != 0;
+  return KV_OK;
+}
+
+kv_status kv_timing_read(kv_timing* out, int reset) {
+  if (!out) return fail(KV_ERR_INVALID, "kv_timing_read: out is NULL");
+  std::lock_guard<std::mutex> lk(kv::g_tmu);
+  for (auto& p : kv::g_pairs) {
+    KV_HIP(hipEventSynchronize(p.b));
+    float ms = 0;
+    KV_HIP(hipEventElapsedTime(&ms, p.a, p.b));
+    kv::g_acc.calls[p.stage] += 1;
+    kv::g_acc.ms[p.stage] += ms;
+    kv::g_free_events.push_back(p.a);
+    kv::g_free_events.push_back(p.b);
+  }
+  kv::g_pairs.clear();
+  *out = kv::g_acc;
+  if (reset) kv::g_acc = kv_timing{};
+  return KV_OK;
+}
 
 kv_status kv_trace_load(const kv_trace_desc* d, void* stream, kv_trace** out) {
   if (!out) return fail(KV_ERR_INVALID, "kv_trace_load: out is NULL");

@@ -96,6 +96,22 @@ constexpr uint64_t kTraceMagic = 0x6b7663666774726bull;  // "kvcfgtrk"
 constexpr uint64_t kDeadMagic = 0x646561646b766366ull;
 
 // ---------------------------------------------------------------------------
+// stage timing (kv_timing_enable / kv_timing_read)
+// ---------------------------------------------------------------------------
+enum Stage {
+  kStLoadValidate = 0, kStLoadSort, kStLoadLinks, kStPartition, kStStackMatrix,
+  kStStackLocal, kStStackAssemble, kStStackFinal, kStLruCounts, kStReplayInit, kStReplay,
+  kStCombine, kStObjectives, kStPareto
+};
+// Records an event pair around a scope when timing is enabled.
+struct StageTimer {
+  StageTimer(Stage st, hipStream_t s);
+  ~StageTimer();
+  int slot;
+  hipStream_t s;
+};
+
+// ---------------------------------------------------------------------------
 // launchers (each defined in the .hip file that holds its kernels)
 // ---------------------------------------------------------------------------
 // exclusive (inclusive=false) or inclusive prefix sum of u32, any length;

@@ -52,6 +52,16 @@ class kv_cost_model(ctypes.Structure):
                 ("ssd_bw_max", _f64), ("t_prefill_per_token", _f64)]
 
 
+KV_STAGES = 14
+STAGE_NAMES = ("load_validate", "load_sort", "load_links", "partition", "stack_matrix",
+               "stack_local", "stack_assemble", "stack_final", "lru_counts", "replay_init",
+               "replay", "replay_combine", "objectives", "pareto")
+
+
+class kv_timing(ctypes.Structure):
+    _fields_ = [("calls", _u64 * KV_STAGES), ("ms", _f64 * KV_STAGES)]
+
+
 assert ctypes.sizeof(kv_config) == 432
 
 
@@ -77,12 +87,27 @@ def _load():
     lib.kv_pareto.argtypes = [_vp, _vp, _u32, _vp, _vp, ctypes.POINTER(_u32), _vp]
     lib.kv_last_error.restype = ctypes.c_char_p
     lib.kv_last_error.argtypes = []
+    lib.kv_timing_enable.restype = ctypes.c_int
+    lib.kv_timing_enable.argtypes = [ctypes.c_int]
+    lib.kv_timing_read.restype = ctypes.c_int
+    lib.kv_timing_read.argtypes = [ctypes.POINTER(kv_timing), ctypes.c_int]
     return lib
 
 
 LIB = _load()
 EXPORTS = ("kv_trace_load", "kv_trace_free", "kv_trace_info", "kv_eval_configs", "kv_pareto",
-           "kv_last_error")
+           "kv_last_error", "kv_timing_enable", "kv_timing_read")
+
+
+def kv_timing_enable(on: bool = True):
+    _check(LIB.kv_timing_enable(1 if on else 0))
+
+
+def kv_timing_read(reset: bool = True) -> dict:
+    """{stage name: (launches, device ms)} since the last reset."""
+    t = kv_timing()
+    _check(LIB.kv_timing_read(ctypes.byref(t), 1 if reset else 0))
+    return {STAGE_NAMES[i]: (int(t.calls[i]), float(t.ms[i])) for i in range(KV_STAGES)}
 
 
 def kv_last_error() -> str:

@@ -5,7 +5,7 @@ cost-model inputs (:mod:`tracegen.configs`).  Both the GPU library's tests
 and benchmark and the CPU oracle draw their inputs from here; the module
 holds none of the cache-evaluation arithmetic.
 """
-from .workloads import (Trace, make, tiny, chat, tenant, longctx, full, from_blocks,
+from .workloads import (Trace, Recipe, recipe, make, tiny, chat, tenant, longctx, full, from_blocks,
                         random_trace, WORKLOADS)
 from .configs import (ConfigBatch, configs_for, grid, from_list, empty, split_capacity,
                       random_configs,
@@ -13,7 +13,7 @@ from .configs import (ConfigBatch, configs_for, grid, from_list, empty, split_ca
                       POLICY_FIFO, POLICY_LFU, MAX_GROUPS, GIB, TIB)
 
 __all__ = [
-    "Trace", "make", "tiny", "chat", "tenant", "longctx", "full", "from_blocks",
+    "Trace", "Recipe", "recipe", "make", "tiny", "chat", "tenant", "longctx", "full", "from_blocks",
     "random_trace", "WORKLOADS", "ConfigBatch", "configs_for", "grid", "from_list",
     "empty", "split_capacity", "random_configs", "DEFAULT_COST", "MODE_INCLUSIVE", "MODE_EXCLUSIVE_DEMOTE",
     "POLICY_LRU", "POLICY_FIFO", "POLICY_LFU", "MAX_GROUPS", "GIB", "TIB",

@@ -100,11 +100,19 @@ def poisson_arrivals(rng: np.random.Generator, n: int, mean_gap: float) -> np.nd
 
 @dataclass
 class _Requests:
-    """Requests of one generator, in the generator's own id order."""
+    """Requests of one generator, in the generator's own id order.
+
+    Request r reads ``len0[r]`` hashes of ``table`` from ``start0[r]``, then
+    ``len1[r]`` hashes from ``start1[r]`` (a shared prefix, then its own
+    continuation).
+    """
     time: np.ndarray          # float64[r]
     tag: int
-    nblk: np.ndarray          # int64[r] blocks read by each request
-    flat: np.ndarray          # uint64[sum nblk] hashes, request after request
+    table: np.ndarray         # uint64[t] hash streams of this generator
+    start0: np.ndarray        # int64[r]
+    len0: np.ndarray          # int64[r]
+    start1: np.ndarray        # int64[r]
+    len1: np.ndarray          # int64[r]
     group: np.ndarray         # uint8[r]
     weight: int
 
@@ -123,22 +131,13 @@ def _prompt_suffix_requests(rng, salt, tag_prompt, n_prompts, prompt_ent_base,
     total = (prompt_len[choice] + suffix) // tokens_per_block
     shared = np.minimum(pblk[choice], total)
     nsuf = total - shared
-    # suffix chain continues from the last shared prompt block
+    # the suffix chain continues from the last shared prompt block
     last = p_hash[p_off[choice] + shared - 1]
     s_hash, s_off = chain_streams(TAG_SUFFIX, req_ent_base + np.arange(n_req), nsuf,
                                   last, first_index=shared)
-    # assemble request-major flat hashes
-    r_off = np.zeros(n_req + 1, dtype=np.int64)
-    np.cumsum(total, out=r_off[1:])
-    flat = np.empty(int(r_off[-1]), dtype=np.uint64)
-    # shared part: gather from the prompt table
-    rid_sh = np.repeat(np.arange(n_req), shared)
-    pos_sh = np.arange(rid_sh.size) - np.repeat(np.cumsum(shared) - shared, shared)
-    flat[r_off[rid_sh] + pos_sh] = p_hash[p_off[choice[rid_sh]] + pos_sh]
-    rid_sf = np.repeat(np.arange(n_req), nsuf)
-    pos_sf = np.arange(rid_sf.size) - np.repeat(s_off[:-1], nsuf)
-    flat[r_off[rid_sf] + shared[rid_sf] + pos_sf] = s_hash
-    return _Requests(time=t, tag=out_tag, nblk=total, flat=flat,
+    table = np.concatenate([p_hash, s_hash])
+    return _Requests(time=t, tag=out_tag, table=table, start0=p_off[choice], len0=shared,
+                     start1=len(p_hash) + s_off[:-1], len1=nsuf,
                      group=np.full(n_req, group_id, dtype=np.uint8), weight=1)
 
 
@@ -162,29 +161,21 @@ def _chat_requests(rng, salt, n_sessions, n_turns_cap, span, ent_base, tag):
     sess = np.repeat(np.arange(n_sessions), turns)
     first = np.cumsum(turns) - turns                       # first turn index per session
     tpos = np.arange(n_t) - np.repeat(first, turns)        # turn number inside the session
-    # cumulative tokens and times inside each session
     cum_tok = np.cumsum(tokens)
     base_tok = np.repeat(cum_tok[first] - tokens[first], turns)
     hist_tok = cum_tok - base_tok
-    cum_think = np.cumsum(think)
     gap_before = np.where(tpos == 0, 0.0, think[np.maximum(np.arange(n_t) - 1, 0)])
     cum_gap = np.cumsum(gap_before)
     base_gap = np.repeat(cum_gap[first], turns)
     t = np.repeat(start, turns) + (cum_gap - base_gap)
-    del cum_think
     nblk = hist_tok // 16
     # session stream length = blocks read by the session's last turn
-    last_turn = first + turns - 1
-    slen = nblk[last_turn]
+    slen = nblk[first + turns - 1]
     s_hash, s_off = chain_streams(tag, ent_base + np.arange(n_sessions), slen,
                                   np.full(n_sessions, salt, dtype=np.uint64))
-    r_off = np.zeros(n_t + 1, dtype=np.int64)
-    np.cumsum(nblk, out=r_off[1:])
-    rid = np.repeat(np.arange(n_t), nblk)
-    pos = np.arange(rid.size) - np.repeat(r_off[:-1], nblk)
-    flat = s_hash[s_off[sess[rid]] + pos]
-    return _Requests(time=t, tag=tag, nblk=nblk, flat=flat,
-                     group=np.zeros(n_t, dtype=np.uint8), weight=1)
+    z = np.zeros(n_t, dtype=np.int64)
+    return _Requests(time=t, tag=tag, table=s_hash, start0=s_off[sess], len0=nblk,
+                     start1=z, len1=z, group=np.zeros(n_t, dtype=np.uint8), weight=1)
 
 
 def _longctx_requests(rng, salt, n_req, n_docs, span, ent_base, tag, weight):
@@ -197,60 +188,98 @@ def _longctx_requests(rng, salt, n_req, n_docs, span, ent_base, tag, weight):
     np.maximum.at(dlen, doc, nblk)
     d_hash, d_off = chain_streams(tag, ent_base + np.arange(n_docs), dlen,
                                   np.full(n_docs, salt, dtype=np.uint64))
-    r_off = np.zeros(n_req + 1, dtype=np.int64)
-    np.cumsum(nblk, out=r_off[1:])
-    total = int(r_off[-1])
-    flat = np.empty(total, dtype=np.uint64)
-    # chunked gather keeps peak memory bounded on large traces
-    step = 1 << 22
-    for a in range(0, n_req, step):
-        b = min(n_req, a + step)
-        nb = nblk[a:b]
-        rid = np.repeat(np.arange(a, b), nb)
-        pos = np.arange(rid.size, dtype=np.int64) - np.repeat(r_off[a:b] - r_off[a], nb)
-        flat[r_off[a]:r_off[b]] = d_hash[d_off[doc[rid]] + pos]
-    return _Requests(time=t, tag=tag, nblk=nblk, flat=flat,
-                     group=np.zeros(n_req, dtype=np.uint8), weight=weight)
+    z = np.zeros(n_req, dtype=np.int64)
+    return _Requests(time=t, tag=tag, table=d_hash, start0=d_off[doc], len0=nblk,
+                     start1=z, len1=z, group=np.zeros(n_req, dtype=np.uint8), weight=weight)
 
 
-def _merge(name, parts, n_groups, tokens_per_granule, granule_bytes, meta):
-    """Order all requests by (time, tag, id) and lay out the access arrays."""
+@dataclass
+class Recipe:
+    """A trace before expansion: hash streams plus per-request segments.
+
+    Requests are already in trace order; request r reads table[start0[r]:
+    start0[r]+len0[r]] then table[start1[r]: start1[r]+len1[r]].
+    ``expand`` materialises the per-access arrays with torch, on the CPU or
+    directly on a GPU; both give the same integers.
+    """
+    name: str
+    table: np.ndarray
+    start0: np.ndarray
+    len0: np.ndarray
+    start1: np.ndarray
+    len1: np.ndarray
+    group: np.ndarray       # uint8 per request
+    weight: np.ndarray      # uint8 per request
+    req_time: np.ndarray
+    n_groups: int
+    tokens_per_granule: int
+    granule_bytes: int
+    meta: dict
+
+    @property
+    def n(self) -> int:
+        return int(self.len0.sum() + self.len1.sum())
+
+    def expand(self, device="cpu", max_requests=None):
+        """Per-access tensors: hash (int64 bits of the uint64 hash), req (int32),
+        group (uint8), weight (uint8); plus req_time (float64)."""
+        import torch
+        R = len(self.len0) if max_requests is None else min(max_requests, len(self.len0))
+        dev = torch.device(device)
+        L0 = torch.from_numpy(self.len0[:R]).to(dev)
+        L1 = torch.from_numpy(self.len1[:R]).to(dev)
+        S0 = torch.from_numpy(self.start0[:R]).to(dev)
+        S1 = torch.from_numpy(self.start1[:R]).to(dev)
+        tot = L0 + L1
+        off = torch.zeros(R + 1, dtype=torch.int64, device=dev)
+        torch.cumsum(tot, 0, out=off[1:])
+        n = int(off[-1])
+        if n >= (1 << 32) - 1:
+            raise ValueError("trace too long for 32-bit positions")
+        rid = torch.repeat_interleave(torch.arange(R, device=dev), tot, output_size=n)
+        pos = torch.arange(n, device=dev) - off[:-1][rid]
+        first = pos < L0[rid]
+        src = torch.where(first, S0[rid] + pos, S1[rid] + (pos - L0[rid]))
+        table = torch.from_numpy(self.table.view(np.int64)).to(dev)
+        out = {
+            "hash": table[src],
+            "req": rid.to(torch.int32),
+            "group": torch.from_numpy(self.group[:R]).to(dev)[rid],
+            "weight": torch.from_numpy(self.weight[:R]).to(dev)[rid],
+            "req_time": torch.from_numpy(self.req_time[:R].copy()).to(dev),
+        }
+        return out
+
+    def to_trace(self, max_requests=None) -> "Trace":
+        d = self.expand("cpu", max_requests)
+        return Trace(name=self.name, hash=d["hash"].numpy().view(np.uint64),
+                     req=d["req"].numpy().view(np.uint32), group=d["group"].numpy(),
+                     weight=d["weight"].numpy(), req_time=d["req_time"].numpy(),
+                     n_groups=self.n_groups, tokens_per_granule=self.tokens_per_granule,
+                     granule_bytes=self.granule_bytes, meta=dict(self.meta))
+
+
+def _merge(name, parts, n_groups, tokens_per_granule, granule_bytes, meta) -> Recipe:
+    """Order all requests by (time, tag, id) and concatenate the hash tables."""
+    toff = np.cumsum([0] + [len(p.table) for p in parts])
+    table = np.concatenate([p.table for p in parts]) if len(parts) > 1 else parts[0].table
     times = np.concatenate([p.time for p in parts])
     tags = np.concatenate([np.full(len(p.time), p.tag, dtype=np.int64) for p in parts])
     ids = np.concatenate([np.arange(len(p.time), dtype=np.int64) for p in parts])
-    nblk = np.concatenate([p.nblk for p in parts])
+    s0 = np.concatenate([p.start0 + toff[i] for i, p in enumerate(parts)])
+    s1 = np.concatenate([p.start1 + toff[i] for i, p in enumerate(parts)])
+    l0 = np.concatenate([p.len0 for p in parts])
+    l1 = np.concatenate([p.len1 for p in parts])
     grp = np.concatenate([p.group for p in parts])
     wts = np.concatenate([np.full(len(p.time), p.weight, dtype=np.uint8) for p in parts])
-    src = np.concatenate([p.flat for p in parts]) if len(parts) > 1 else parts[0].flat
-    src_off = np.zeros(len(nblk) + 1, dtype=np.int64)
-    np.cumsum(nblk, out=src_off[1:])
     order = np.lexsort((ids, tags, times))
-    n_req = len(order)
-    o_nblk = nblk[order]
-    o_off = np.zeros(n_req + 1, dtype=np.int64)
-    np.cumsum(o_nblk, out=o_off[1:])
-    n = int(o_off[-1])
-    if n >= (1 << 32) - 1:
-        raise ValueError("trace too long for 32-bit positions")
-    hashes = np.empty(n, dtype=np.uint64)
-    req = np.empty(n, dtype=np.uint32)
-    group = np.empty(n, dtype=np.uint8)
-    weight = np.empty(n, dtype=np.uint8)
-    step = 1 << 20
-    for a in range(0, n_req, step):
-        b = min(n_req, a + step)
-        nb = o_nblk[a:b]
-        loc = np.repeat(np.arange(a, b), nb)
-        pos = np.arange(loc.size, dtype=np.int64) - np.repeat(o_off[a:b] - o_off[a], nb)
-        sl = slice(o_off[a], o_off[b])
-        hashes[sl] = src[src_off[order[loc]] + pos]
-        req[sl] = loc.astype(np.uint32)
-        group[sl] = grp[order[loc]]
-        weight[sl] = wts[order[loc]]
-    return Trace(name=name, hash=hashes, req=req, group=group, weight=weight,
-                 req_time=times[order].astype(np.float64), n_groups=n_groups,
-                 tokens_per_granule=tokens_per_granule, granule_bytes=granule_bytes,
-                 meta=meta)
+    return Recipe(name=name, table=np.ascontiguousarray(table, dtype=np.uint64),
+                  start0=s0[order].astype(np.int64), len0=l0[order].astype(np.int64),
+                  start1=s1[order].astype(np.int64), len1=l1[order].astype(np.int64),
+                  group=grp[order].astype(np.uint8), weight=wts[order],
+                  req_time=times[order].astype(np.float64), n_groups=n_groups,
+                  tokens_per_granule=tokens_per_granule, granule_bytes=granule_bytes,
+                  meta=meta)
 
 
 def _salt(seed: int, which: int) -> np.uint64:
@@ -261,7 +290,7 @@ def _salt(seed: int, which: int) -> np.uint64:
 # the five workloads
 # --------------------------------------------------------------------------
 
-def tiny(seed: int = 0, n_req: int = 2000) -> Trace:
+def tiny_recipe(seed: int = 0, n_req: int = 2000) -> Recipe:
     """2,000 requests, Poisson 20/s, Zipf(1.1) over 100 system prompts + unique suffix."""
     rng = np.random.default_rng(seed)
     part = _prompt_suffix_requests(rng, _salt(seed, 1), TAG_PROMPT, 100, 0, 1.1,
@@ -269,7 +298,7 @@ def tiny(seed: int = 0, n_req: int = 2000) -> Trace:
     return _merge("tiny", [part], 1, 16, GRANULE_128K, {"seed": seed, "n_req": n_req})
 
 
-def chat(seed: int = 1, n_sessions: int = 20000) -> Trace:
+def chat_recipe(seed: int = 1, n_sessions: int = 20000) -> Recipe:
     """Multi-turn chat: 20,000 sessions over two hours."""
     rng = np.random.default_rng(seed)
     part = _chat_requests(rng, _salt(seed, 3), n_sessions, None, SPAN_2H, 0, TAG_CHAT)
@@ -295,7 +324,7 @@ def _tenant_parts(rng, seed, total_req, n_groups=8, span=SPAN_2H, ent_base=0, re
     return parts
 
 
-def tenant(seed: int = 2, total_req: int = 100000, n_groups: int = 8) -> Trace:
+def tenant_recipe(seed: int = 2, total_req: int = 100000, n_groups: int = 8) -> Recipe:
     """Mixed-tenant trace: 8 groups with their own Zipf prompt pools and rates."""
     rng = np.random.default_rng(seed)
     parts = _tenant_parts(rng, seed, total_req, n_groups)
@@ -303,7 +332,7 @@ def tenant(seed: int = 2, total_req: int = 100000, n_groups: int = 8) -> Trace:
                   {"seed": seed, "total_req": total_req})
 
 
-def longctx(seed: int = 3, n_req: int = 100000, n_docs: int = 2000) -> Trace:
+def longctx_recipe(seed: int = 3, n_req: int = 100000, n_docs: int = 2000) -> Recipe:
     """Long-context/agentic trace: 64-token blocks, one granule = one 512 KiB block."""
     rng = np.random.default_rng(seed)
     part = _longctx_requests(rng, _salt(seed, 5), n_req, n_docs, SPAN_2H, 0, TAG_DOC, 1)
@@ -311,7 +340,7 @@ def longctx(seed: int = 3, n_req: int = 100000, n_docs: int = 2000) -> Trace:
                   {"seed": seed, "n_req": n_req, "n_docs": n_docs})
 
 
-def full(seed: int = 4, n_req: int = 1_000_000) -> Trace:
+def full_recipe(seed: int = 4, n_req: int = 1_000_000) -> Recipe:
     """Full-scale sweep: chat/tenant/long-context mixed 40/30/30 over two hours.
 
     Granules are 128 KiB (16 tokens); the long-context 64-token blocks weigh
@@ -331,18 +360,44 @@ def full(seed: int = 4, n_req: int = 1_000_000) -> Trace:
                   {"seed": seed, "n_req": n_req})
 
 
-WORKLOADS = {
-    "tiny": tiny,
-    "chat": chat,
-    "tenant": tenant,
-    "longctx": longctx,
-    "full": full,
+RECIPES = {
+    "tiny": tiny_recipe,
+    "chat": chat_recipe,
+    "tenant": tenant_recipe,
+    "longctx": longctx_recipe,
+    "full": full_recipe,
 }
+WORKLOADS = tuple(RECIPES)
+
+
+def recipe(name: str, seed: int | None = None, **kw) -> Recipe:
+    fn = RECIPES[name]
+    return fn(**kw) if seed is None else fn(seed=seed, **kw)
 
 
 def make(name: str, seed: int | None = None, **kw) -> Trace:
-    fn = WORKLOADS[name]
-    return fn(**kw) if seed is None else fn(seed=seed, **kw)
+    """Host copy of a workload trace (expanded on the CPU)."""
+    return recipe(name, seed, **kw).to_trace()
+
+
+def tiny(seed: int = 0, n_req: int = 2000) -> Trace:
+    return tiny_recipe(seed, n_req).to_trace()
+
+
+def chat(seed: int = 1, n_sessions: int = 20000) -> Trace:
+    return chat_recipe(seed, n_sessions).to_trace()
+
+
+def tenant(seed: int = 2, total_req: int = 100000, n_groups: int = 8) -> Trace:
+    return tenant_recipe(seed, total_req, n_groups).to_trace()
+
+
+def longctx(seed: int = 3, n_req: int = 100000, n_docs: int = 2000) -> Trace:
+    return longctx_recipe(seed, n_req, n_docs).to_trace()
+
+
+def full(seed: int = 4, n_req: int = 1_000_000) -> Trace:
+    return full_recipe(seed, n_req).to_trace()
 
 
 # --------------------------------------------------------------------------
