@@ -203,3 +203,19 @@ def test_double_free_detected(lib):
     raw = h.handle
     h.free()
     assert kvcfg.LIB.kv_trace_free(raw) == kvcfg.KV_ERR_INVALID
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_replay_chunks(lib, oracle_mod, seed):
+    """FIFO / LFU replays long enough to cross many chunks, at capacities from a
+    few blocks to most of the working set (serial, chunked and fallback paths)."""
+    rng = np.random.default_rng(100 + seed)
+    weights = (1,) if seed % 2 else (1, 4)
+    t = tg.random_trace(200 + seed, int(rng.integers(20_000, 70_000)), int(rng.integers(500, 20_000)),
+                        n_groups=1 + seed % 3, weight_choices=weights,
+                        zipf_s=float(rng.choice([0.6, 0.9, 1.2])), reuse_bias=0.2)
+    caps = [4, 60, 64, 300, 1000, 4096, 5000, 16384, 40000]
+    items = [{"cap": (c, 0, 0), "policy": p} for c in caps for p in (1, 2)]
+    items += [{"cap": (caps[i], caps[i + 2], caps[i + 4]), "policy": p}
+              for i in range(4) for p in (1, 2)]
+    compare(lib, oracle_mod, t, tg.from_list(items), label=f"chunks{seed}")
