@@ -62,20 +62,30 @@ struct JobArgs {
 };
 
 constexpr int kRNT = 1024;                 // threads of a replay workgroup
+constexpr int kRNW = kRNT / 64;            // its wavefronts
 constexpr int kRIt = 4;                    // accesses per thread per chunk
 constexpr uint32_t kRChunk = kRNT * kRIt;  // longest chunk
 constexpr uint32_t kCand = 4096;           // LFU eviction candidates per chunk
+constexpr int kCScan = 2;                  // candidate positions per thread and pass
 constexpr uint32_t kMinFast = 256;         // shorter LFU chunks go serial
 constexpr uint16_t kInf16 = 0xFFFF;
+constexpr uint32_t kLdsClass = kRNT;       // LFU count classes held in LDS
+constexpr uint32_t kLdsClassWords = kLdsClass / 64;
+static_assert(kRIt == 4, "hit words are assembled from four ballots");
 
 // Optional per-job replay statistics (diagnostics build only).
 #ifdef KV_REPLAY_STATS
 enum { kStFastOk = 0, kStFailPool, kStFailElig, kStFailConv, kStSerialAcc, kStIters,
-       kStScanned, kStFastAcc, kStats };
+       kStScanned, kStFastAcc, kStT0, kStT1, kStT2, kStT3, kStT4, kStT5, kStT6, kStT7, kStT8, kStats };
 __device__ unsigned long long g_rstats[256][kStats];
-#define RSTAT(j, k, v) do { if (threadIdx.x == 0) atomicAdd(&g_rstats[(j) & 255][k], (unsigned long long)(v)); } while (0)
+__shared__ unsigned long long s_rstats[kStats];  // flushed to g_rstats when the job ends
+#define RSTAT(j, k, v) do { if (threadIdx.x == 0) s_rstats[k] += (unsigned long long)(v); } while (0)
+#define RCLK(t) const unsigned long long t = clock64()
+#define RTIME(k, t0, t1) RSTAT(blockIdx.x, k, (t1) - (t0))
 #else
 #define RSTAT(j, k, v) do { } while (0)
+#define RCLK(t) do { } while (0)
+#define RTIME(k, t0, t1) do { } while (0)
 #endif
 
 __device__ __forceinline__ uint32_t ld_acq(const uint32_t* p) {
@@ -128,18 +138,61 @@ __device__ __forceinline__ void write_counters(const GroupCounters& c, uint32_t 
   }
 }
 
-// Build the hit-bit words of [a, a + len) (a multiple of 64) from LDS flags.
-__device__ __forceinline__ void store_bits(const uint8_t* s_hit, uint64_t a, uint32_t len,
+// The kRIt consecutive accesses [p0, p0 + 4) of a thread; p0 is a multiple of
+// 4, so when all four are valid one 16-byte (or 4-byte) load fetches them.
+__device__ __forceinline__ void load4_u32(const uint32_t* __restrict__ a, uint64_t p0, bool all,
+                                          const bool v[kRIt], uint32_t out[kRIt]) {
+  if (all) {
+    const uint4 x = *reinterpret_cast<const uint4*>(a + p0);
+    out[0] = x.x;
+    out[1] = x.y;
+    out[2] = x.z;
+    out[3] = x.w;
+  } else {
+#pragma unroll
+    for (int e = 0; e < kRIt; ++e) out[e] = v[e] ? a[p0 + e] : 0u;
+  }
+}
+
+__device__ __forceinline__ void load4_u8(const uint8_t* __restrict__ a, uint64_t p0, bool all,
+                                         const bool v[kRIt], uint32_t out[kRIt]) {
+  if (all) {
+    const uint32_t x = *reinterpret_cast<const uint32_t*>(a + p0);
+#pragma unroll
+    for (int e = 0; e < kRIt; ++e) out[e] = (x >> (8 * e)) & 0xFFu;
+  } else {
+#pragma unroll
+    for (int e = 0; e < kRIt; ++e) out[e] = v[e] ? (uint32_t)a[p0 + e] : 0u;
+  }
+}
+
+// Hit words of a chunk starting at c0 (a multiple of 64).  Thread t holds
+// positions 4t..4t+3, so the 16 lanes of each quarter wavefront hold one
+// 64-position word: bit 4m+e of word q is item e of lane 16q+m.
+__device__ __forceinline__ void store_hits(const bool hit[kRIt], uint64_t c0, uint32_t L,
                                            const JobDev& j, uint64_t* __restrict__ bits) {
-  const uint32_t nwords = (len + 63) / 64;
-  for (uint32_t wd = threadIdx.x; wd < nwords; wd += kRNT) {
+  uint64_t bal[kRIt];
+#pragma unroll
+  for (int e = 0; e < kRIt; ++e) bal[e] = __ballot(hit[e]);
+  const uint32_t q = lane_id();
+  if (q < 4) {
     uint64_t word = 0;
-    for (uint32_t k = 0; k < 64; ++k) {
-      const uint32_t loc = wd * 64 + k;
-      if (loc < len && s_hit[loc]) word |= 1ull << k;
-    }
-    const uint64_t base = a + (uint64_t)wd * 64;
-    if (base < j.end && base + 64 > j.begin) bits[(base >> 6) - j.word0] = word;
+#pragma unroll
+    for (int e = 0; e < kRIt; ++e) word |= spread4(bal[e] >> (16 * q)) << e;
+    const uint32_t wloc = (threadIdx.x / 64) * 4 + q;
+    const uint64_t base = c0 + (uint64_t)wloc * 64;
+    if (wloc * 64 < L && base < j.end && base + 64 > j.begin) bits[(base >> 6) - j.word0] = word;
+  }
+}
+
+// Adds per-thread (count, weight) partials of one group: one LDS atomic per
+// wavefront.
+__device__ __forceinline__ void add_uniform(unsigned long long* dc, unsigned long long* dw,
+                                            uint32_t c, uint32_t w) {
+  const uint32_t sc = wave_sum(c), sw = wave_sum(w);
+  if (lane_id() == 0 && sc) {
+    atomicAdd(dc, (unsigned long long)sc);
+    atomicAdd(dw, (unsigned long long)sw);
   }
 }
 
@@ -151,109 +204,132 @@ __device__ __forceinline__ void store_bits(const uint8_t* s_hit, uint64_t a, uin
 // so iterating "misses -> W -> misses" from "no misses" rises monotonically
 // to the exact answer.
 // ---------------------------------------------------------------------------
+struct FifoLds {
+  uint8_t ex[kRChunk];
+  uint32_t red[2 * kRNW];
+  unsigned long long fin[KV_MAX_GROUPS], finw[KV_MAX_GROUPS];
+};
+
 __device__ void fifo_chunked(const JobDev& j, const JobArgs& a, uint64_t* __restrict__ S,
-                             uint64_t* __restrict__ bits, unsigned long long* cnt) {
-  __shared__ uint8_t s_ex[kRChunk];
-  __shared__ uint8_t s_hit[kRChunk];
-  __shared__ uint64_t s_red[kRNT / 64 + 1];
-  __shared__ GroupCounters gc;
+                             uint64_t* __restrict__ bits, GroupCounters& gc, FifoLds& F,
+                             bool g1, uint32_t g0) {
   const uint32_t tid = threadIdx.x;
   const uint32_t o = j.order;
-  if (tid < KV_MAX_GROUPS) gc.ins[tid] = gc.insw[tid] = gc.ev[tid] = gc.evw[tid] = 0;
-  __syncthreads();
   const uint32_t L = j.chunk;
+  const uint32_t l0 = tid * kRIt;
   uint64_t W0 = 0;
   for (uint64_t c0 = j.begin & ~63ull; c0 < j.end; c0 += L) {
+    RCLK(f_a);
     const uint64_t c1 = min(c0 + L, j.end);
-    uint32_t bb[kRIt], ww[kRIt], gg[kRIt];
-    int lp[kRIt];
-    uint64_t ss[kRIt], wi[kRIt];
+    const uint64_t p0 = c0 + l0;
     bool v[kRIt], miss[kRIt];
 #pragma unroll
+    for (int e = 0; e < kRIt; ++e) v[e] = l0 + e < L && p0 + e >= j.begin && p0 + e < c1;
+    const bool all = v[0] && v[kRIt - 1];
+    uint32_t bb[kRIt], ww[kRIt], gg[kRIt] = {g0, g0, g0, g0}, kk[kRIt];
+    load4_u32(a.bid[o], p0, all, v, bb);
+    load4_u8(a.w8[o], p0, all, v, ww);
+    load4_u32(a.key[o], p0, all, v, kk);
+    if (!g1) load4_u8(a.g8[o], p0, all, v, gg);
+    int lp[kRIt];
+    uint64_t ss[kRIt], wi[kRIt];
+#pragma unroll
     for (int e = 0; e < kRIt; ++e) {
-      const uint32_t loc = tid * kRIt + e;
-      const uint64_t p = c0 + loc;
-      v[e] = loc < L && p >= j.begin && p < c1;
-      bb[e] = v[e] ? a.bid[o][p] : 0u;
-      ww[e] = v[e] ? a.w8[o][p] : 0u;
-      gg[e] = v[e] ? a.g8[o][p] : 0u;
-      const uint32_t k = v[e] ? a.key[o][p] : 0u;
-      lp[e] = (k != 0 && (uint64_t)(k - 1) >= c0) ? (int)((uint64_t)(k - 1) - c0) : -1;
+      lp[e] = (kk[e] != 0 && (uint64_t)(kk[e] - 1) >= c0) ? (int)((uint64_t)(kk[e] - 1) - c0) : -1;
       ss[e] = v[e] ? S[bb[e]] : kNoIns;
       miss[e] = false;
     }
-    uint64_t tot = 0;
+    uint32_t tot = 0;
+    RCLK(f_b);
+    RTIME(kStT0, f_a, f_b);
     for (uint32_t it = 0; it < L + 2; ++it) {
-      uint64_t x = 0;
+      RSTAT(blockIdx.x, kStIters, 1);
+      uint32_t x = 0;
 #pragma unroll
       for (int e = 0; e < kRIt; ++e) x += miss[e] ? ww[e] : 0u;
-      const uint64_t pre = block_excl_scan<kRNT>(x, s_red, &tot);
+      RCLK(g_a);
+      const uint32_t pre = block_excl_scan_u32<kRNT>(x, F.red, tot);
+      RCLK(g_b);
+      RTIME(kStT6, g_a, g_b);
       uint64_t run = W0 + pre;
+      uint32_t exw = 0;
 #pragma unroll
       for (int e = 0; e < kRIt; ++e) {
         wi[e] = run;
         const bool ex = v[e] && (ss[e] == kNoIns || run - ss[e] > j.cap);
-        s_ex[tid * kRIt + e] = ex ? 1 : 0;
+        exw |= (ex ? 1u : 0u) << (8 * e);
         run += miss[e] ? ww[e] : 0u;
       }
+      *reinterpret_cast<uint32_t*>(&F.ex[l0]) = exw;
       __syncthreads();
+      RCLK(g_c);
+      RTIME(kStT7, g_b, g_c);
       bool changed = false;
 #pragma unroll
       for (int e = 0; e < kRIt; ++e) {
-        const bool ex = s_ex[tid * kRIt + e] != 0;
-        const bool nm = ex && (lp[e] < 0 || s_ex[lp[e]] == 0);
+        const bool ex = (exw >> (8 * e)) & 1u;
+        const bool nm = ex && (lp[e] < 0 || F.ex[lp[e]] == 0);
         changed |= nm != miss[e];
         miss[e] = nm;
       }
-      if (!__syncthreads_or(changed)) break;
+      const bool again = __syncthreads_or(changed);
+      RCLK(g_d);
+      RTIME(kStT8, g_c, g_d);
+      if (!again) break;
     }
     // tot and wi belong to the final miss set
+    RCLK(f_c);
+    RTIME(kStT1, f_b, f_c);
+    bool hit[kRIt];
+    uint32_t ci = 0, cw = 0;
 #pragma unroll
     for (int e = 0; e < kRIt; ++e) {
+      hit[e] = v[e] && !miss[e];
       if (v[e] && miss[e]) {
         S[bb[e]] = wi[e];
-        atomicAdd(&gc.ins[gg[e]], 1ull);
-        atomicAdd(&gc.insw[gg[e]], (unsigned long long)ww[e]);
+        if (g1) {
+          ++ci;
+          cw += ww[e];
+        } else {
+          atomicAdd(&gc.ins[gg[e]], 1ull);
+          atomicAdd(&gc.insw[gg[e]], (unsigned long long)ww[e]);
+        }
       }
-      s_hit[tid * kRIt + e] = (v[e] && !miss[e]) ? 1 : 0;
     }
+    if (g1) add_uniform(&gc.ins[g0], &gc.insw[g0], ci, cw);
     W0 += tot;
-    __syncthreads();
-    store_bits(s_hit, c0, L, j, bits);
-    __syncthreads();
+    store_hits(hit, c0, L, j, bits);
+    RCLK(f_d);
+    RTIME(kStT2, f_c, f_d);
+    RSTAT(blockIdx.x, kStFastOk, 1);
   }
   // evictions = insertions - blocks still queued at the end
-  __shared__ unsigned long long sfin[KV_MAX_GROUPS], sfinw[KV_MAX_GROUPS];
-  if (tid < KV_MAX_GROUPS) sfin[tid] = sfinw[tid] = 0;
+  if (tid < KV_MAX_GROUPS) F.fin[tid] = F.finw[tid] = 0;
   __syncthreads();
   for (uint64_t b = tid; b < a.u; b += kRNT) {
     const uint64_t s = S[b];
     if (s != kNoIns && W0 - s <= j.cap) {
       const uint32_t g = a.blk_g[b];
-      atomicAdd(&sfin[g], 1ull);
-      atomicAdd(&sfinw[g], (unsigned long long)a.blk_w[b]);
+      atomicAdd(&F.fin[g], 1ull);
+      atomicAdd(&F.finw[g], (unsigned long long)a.blk_w[b]);
     }
   }
   __syncthreads();
   if (tid < KV_MAX_GROUPS) {
-    gc.ev[tid] = gc.ins[tid] - sfin[tid];
-    gc.evw[tid] = gc.insw[tid] - sfinw[tid];
+    gc.ev[tid] = gc.ins[tid] - F.fin[tid];
+    gc.evw[tid] = gc.insw[tid] - F.finw[tid];
   }
-  __syncthreads();
-  write_counters(gc, a.n_groups, cnt);
 }
 
 // FIFO for capacities below 64 blocks: lanes of wave 0 gather a batch of 64
 // accesses, one lane resolves them in trace order.
 __device__ void fifo_serial(const JobDev& j, const JobArgs& a, uint64_t* __restrict__ S,
-                            uint64_t* __restrict__ bits, unsigned long long* cnt) {
+                            uint64_t* __restrict__ bits, GroupCounters& gc) {
   __shared__ uint32_t sb[64], sw[64], sg[64];
   __shared__ int sdup[64];
   __shared__ uint64_t ss[64], snew[64];
-  __shared__ GroupCounters gc;
   const uint32_t lane = threadIdx.x;
   const uint32_t o = j.order;
-  if (lane < KV_MAX_GROUPS) gc.ins[lane] = gc.insw[lane] = gc.ev[lane] = gc.evw[lane] = 0;
   uint64_t wcur = 0;
   for (uint64_t base = j.begin & ~63ull; base < j.end; base += 64) {
     const uint64_t i = base + lane;
@@ -318,53 +394,110 @@ __device__ void fifo_serial(const JobDev& j, const JobArgs& a, uint64_t* __restr
     gc.ev[lane] = gc.ins[lane] - sfin[lane];
     gc.evw[lane] = gc.insw[lane] - sfinw[lane];
   }
-  __syncthreads();
-  write_counters(gc, a.n_groups, cnt);
 }
 
 // ---------------------------------------------------------------------------
 // LFU.  State per block: (last access position << 32) | in-cache count (0 =
 // absent).  The members of count class f in victim order are the positions
 // of their last accesses, so class f is a queue over positions scanned by a
-// head pointer head[f]; cnt[f] counts members, nz has a bit per nonempty class.
+// head pointer head[f].  Member counts and a nonempty-class bitmap locate the
+// lowest nonempty class; classes below kLdsClass keep them in LDS (the
+// workgroup owns its job for the whole replay), higher ones in HBM.
 // ---------------------------------------------------------------------------
-struct LfuShared {
-  uint64_t used;
-  uint32_t fmin;
-  uint32_t head1;
+struct LfuLds {
+  // per access of the chunk (local position)
+  int16_t lp[kRChunk];        // previous touch in the chunk; pointer-jumped to the chain root
+  uint16_t occ[kRChunk];      // earlier touches of the same block inside the chunk
+  int16_t lmiss[kRChunk];     // latest miss of the block at or before this touch
+  uint16_t nxloc[kRChunk];    // next touch in the chunk or kInf16
+  uint8_t pw[kRChunk];        // weight
+  uint8_t capm[kRChunk];      // stamp of the iteration that found a capacity miss here
+  uint8_t mskip[kRChunk];     // the entry inserted here is promoted before its eviction
+  uint8_t mcons[kRChunk];     // the entry inserted here is evicted inside the chunk
+  uint16_t mpos[kRChunk];     // misses in order: local position
+  uint32_t mneed[kRChunk];    // ...and the weight that must have left the cache by then
+  // count-1 residents from before the chunk, oldest first
+  uint32_t cq[kCand];         // position of their last touch
+  uint32_t cb[kCand];         // block
+  uint16_t ca[kCand];         // first touch inside the chunk or kInf16
+  uint8_t cw[kCand];
+  uint8_t cskip[kCand];
+  uint8_t ccons[kCand];
+  uint32_t red[2 * kRNW];
+  uint32_t sfx[2 * kRNW];
+  uint32_t red8[kRNW][8];
+  uint32_t ccnt[kLdsClass];   // members of class f < kLdsClass
+  uint64_t cnz[kLdsClassWords];
+  uint64_t used;              // cached weight
+  uint32_t fmin, head1;       // lowest nonempty class; no live count-1 member before head1
+  uint32_t nc, h;             // candidate scan: entries found, next position
+  uint64_t vw;                // candidate scan: untouched weight found
+  int ok;
 };
 
-__device__ __forceinline__ uint32_t next_class(const uint64_t* nz, uint32_t nw, uint32_t f) {
+struct Classes {
+  uint32_t* lcnt;   // LDS counts, classes < kLdsClass
+  uint64_t* lnz;    // LDS bitmap words, classes < kLdsClass
+  uint32_t* gcnt;   // HBM counts (classes >= kLdsClass)
+  uint64_t* gnz;    // HBM bitmap words (words >= kLdsClassWords)
+  uint32_t nw;      // bitmap words in all
+};
+
+__device__ __forceinline__ uint64_t class_word(const Classes& c, uint32_t wi) {
+  return wi < kLdsClassWords ? c.lnz[wi] : ld_acq64(&c.gnz[wi]);
+}
+
+__device__ __forceinline__ uint32_t next_class(const Classes& c, uint32_t f) {
   uint32_t wi = f >> 6;
-  if (wi >= nw) return 0xFFFFFFFFu;
-  uint64_t m = ld_acq64(&nz[wi]) & (~0ull << (f & 63));
+  if (wi >= c.nw) return 0xFFFFFFFFu;
+  uint64_t m = class_word(c, wi) & (~0ull << (f & 63));
   while (m == 0) {
-    if (++wi >= nw) return 0xFFFFFFFFu;
-    m = ld_acq64(&nz[wi]);
+    if (++wi >= c.nw) return 0xFFFFFFFFu;
+    m = class_word(c, wi);
   }
   return (wi << 6) + (uint32_t)__ffsll((long long)m) - 1u;
 }
 
-__device__ __forceinline__ void class_add(uint32_t* cnt, uint64_t* nz, uint32_t f, int d) {
-  if (d > 0) {
-    if (atomicAdd(&cnt[f], 1u) == 0u) atomicOr((unsigned long long*)&nz[f >> 6], 1ull << (f & 63));
+__device__ __forceinline__ uint32_t class_count(const Classes& c, uint32_t f) {
+  return f < kLdsClass ? c.lcnt[f] : ld_acq(&c.gcnt[f]);
+}
+
+// Serial update by one thread (the others wait at a barrier).
+__device__ __forceinline__ void class_add1(const Classes& c, uint32_t f, int d) {
+  const uint64_t bit = 1ull << (f & 63);
+  if (f < kLdsClass) {
+    if (d > 0) {
+      if (c.lcnt[f]++ == 0u) c.lnz[f >> 6] |= bit;
+    } else {
+      if (--c.lcnt[f] == 0u) c.lnz[f >> 6] &= ~bit;
+    }
+  } else if (d > 0) {
+    if (atomicAdd(&c.gcnt[f], 1u) == 0u) atomicOr((unsigned long long*)&c.gnz[f >> 6], bit);
   } else {
-    if (atomicSub(&cnt[f], 1u) == 1u)
-      atomicAnd((unsigned long long*)&nz[f >> 6], ~(1ull << (f & 63)));
+    if (atomicSub(&c.gcnt[f], 1u) == 1u) atomicAnd((unsigned long long*)&c.gnz[f >> 6], ~bit);
+  }
+}
+
+// Concurrent count update; bitmap words are rebuilt afterwards.
+__device__ __forceinline__ void class_add_par(const Classes& c, uint32_t f, int d) {
+  if (f < kLdsClass) {
+    if (d > 0) atomicAdd(&c.lcnt[f], 1u); else atomicSub(&c.lcnt[f], 1u);
+  } else {
+    if (d > 0) atomicAdd(&c.gcnt[f], 1u); else atomicSub(&c.gcnt[f], 1u);
   }
 }
 
 // Exact replay of [p0, p1) by one thread (thread 0); returns false if the
 // state is found inconsistent.
 __device__ bool lfu_serial_range(const JobDev& j, const JobArgs& a, uint64_t* __restrict__ st,
-                                 uint32_t* head, uint32_t* ccount, uint64_t* nz, uint32_t nw,
-                                 LfuShared& ls, GroupCounters& gc, uint64_t* __restrict__ bits,
-                                 uint64_t p0, uint64_t p1) {
+                                 uint32_t* head, const Classes& cl, LfuLds& S,
+                                 GroupCounters& gc, uint64_t* __restrict__ bits, uint64_t p0,
+                                 uint64_t p1) {
   const uint32_t o = j.order;
   const uint32_t* __restrict__ bid = a.bid[o];
-  head[1] = ls.head1;
-  uint64_t used = ls.used;
-  uint32_t fmin = ls.fmin;
+  head[1] = S.head1;
+  uint64_t used = S.used;
+  uint32_t fmin = S.fmin;
   uint64_t word = 0;
   bool ok = true;
   for (uint64_t i = p0; i < p1 && ok; ++i) {
@@ -376,9 +509,9 @@ __device__ bool lfu_serial_range(const JobDev& j, const JobArgs& a, uint64_t* __
       if (f) {
         word |= 1ull << (i & 63);
         const uint32_t f1 = f + 1;
-        class_add(ccount, nz, f, -1);
-        class_add(ccount, nz, f1, +1);
-        if (f == fmin && ld_acq(&ccount[f]) == 0) fmin = f1;
+        class_add1(cl, f, -1);
+        class_add1(cl, f1, +1);
+        if (f == fmin && class_count(cl, f) == 0) fmin = f1;
         st[b] = ((uint64_t)i << 32) | f1;
       } else {
         while (used + w > j.cap) {
@@ -401,14 +534,14 @@ __device__ bool lfu_serial_range(const JobDev& j, const JobArgs& a, uint64_t* __
           used -= vw;
           gc.ev[vg] += 1;
           gc.evw[vg] += vw;
-          class_add(ccount, nz, fmin, -1);
-          if (ld_acq(&ccount[fmin]) == 0) {
-            const uint32_t nf = next_class(nz, nw, fmin);
+          class_add1(cl, fmin, -1);
+          if (class_count(cl, fmin) == 0) {
+            const uint32_t nf = next_class(cl, fmin);
             if (nf != 0xFFFFFFFFu) fmin = nf;
           }
         }
         st[b] = ((uint64_t)i << 32) | 1u;
-        class_add(ccount, nz, 1, +1);
+        class_add1(cl, 1, +1);
         fmin = 1;
         used += w;
         const uint32_t g = a.g8[o][i];
@@ -421,42 +554,18 @@ __device__ bool lfu_serial_range(const JobDev& j, const JobArgs& a, uint64_t* __
       word = 0;
     }
   }
-  ls.used = used;
-  ls.fmin = fmin;
-  ls.head1 = head[1];
+  S.used = used;
+  S.fmin = fmin;
+  S.head1 = head[1];
   return ok;
 }
 
-struct LfuLds {
-  // per access of the chunk (local position)
-  int16_t lp[kRChunk];        // previous touch in the chunk; pointer-jumped to the chain root
-  uint16_t occ[kRChunk];      // earlier touches of the same block inside the chunk
-  int16_t lmiss[kRChunk];     // latest miss of the block at or before this touch
-  uint16_t nxloc[kRChunk];    // next touch in the chunk or kInf16
-  uint8_t pw[kRChunk];        // weight
-  uint8_t hit[kRChunk];
-  uint8_t capm[kRChunk];      // miss because the block was evicted earlier in the chunk
-  uint8_t mskip[kRChunk];     // the entry inserted here is promoted before its eviction
-  uint8_t mcons[kRChunk];     // the entry inserted here is evicted inside the chunk
-  uint16_t mpos[kRChunk];     // misses in order: local position
-  uint32_t mneed[kRChunk];    // ...and the weight that must have left the cache by then
-  // count-1 residents from before the chunk, oldest first
-  uint32_t cq[kCand];         // position of their last touch
-  uint32_t cb[kCand];         // block
-  uint16_t ca[kCand];         // first touch inside the chunk or kInf16
-  uint8_t cw[kCand];
-  uint8_t cskip[kCand];
-  uint8_t ccons[kCand];
-  uint64_t red[kRNT / 64 + 1];
-  uint32_t red32[kRNT / 64 + 1];
-};
-
 constexpr int kCPT = (kCand + kRChunk) / kRNT;  // queue entries per thread
 
-// Exclusive suffix minimum over the threads of the block (threads above t).
-template <int NT>
-__device__ __forceinline__ uint32_t block_suffix_min_excl(uint32_t v, uint32_t* sh) {
-  constexpr int NW = NT / 64;
+// Exclusive suffix minimum over the threads of the block (threads above t),
+// and whether any thread raised `flag`; two barriers.
+__device__ __forceinline__ void block_suffix_min_flag(uint32_t v, bool flag, uint32_t* sh,
+                                                      uint32_t& smin, bool& any) {
   const uint32_t lane = lane_id();
   const int w = threadIdx.x / 64;
   uint32_t x = v;
@@ -466,12 +575,23 @@ __device__ __forceinline__ uint32_t block_suffix_min_excl(uint32_t v, uint32_t* 
     if (lane + d < 64) x = min(x, y);
   }
   const uint32_t above = __shfl_down(x, 1, 64);
-  if (lane == 0) sh[w] = x;
+  const bool wflag = __ballot(flag) != 0ull;
+  if (lane == 0) {
+    sh[w] = x;
+    sh[kRNW + w] = wflag ? 1u : 0u;
+  }
   __syncthreads();
   uint32_t r = (lane < 63) ? above : 0xFFFFFFFFu;
-  for (int ww = w + 1; ww < NW; ++ww) r = min(r, sh[ww]);
+  uint32_t f = 0;
+#pragma unroll
+  for (int ww = 0; ww < kRNW; ++ww) {
+    const uint32_t y = sh[ww];
+    r = (ww > w) ? min(r, y) : r;
+    f |= sh[kRNW + ww];
+  }
   __syncthreads();
-  return r;
+  smin = r;
+  any = f != 0u;
 }
 
 // One chunk [c0, c1) without the serial walk.
@@ -488,129 +608,147 @@ __device__ __forceinline__ uint32_t block_suffix_min_excl(uint32_t v, uint32_t* 
 // a queue entry inserted before it, and the old entries are exhausted before
 // any new one is taken.  Returns false, with no block state changed, when
 // that fails; the caller then retries with a shorter chunk.
+//
+// The count-1 residents from before the chunk are found without reading the
+// block states: every count-1 member at or after head1 is a block inserted
+// by a miss at that position and not touched since, and every such block is
+// still a member (count-1 members only leave by a touch or, oldest first, by
+// eviction, which moves head1 past them).
 __device__ bool lfu_fast(const JobDev& j, const JobArgs& a, uint64_t* __restrict__ st,
-                         uint32_t* ccount, uint64_t* nz, uint32_t nw, LfuShared& ls,
-                         GroupCounters& gc, LfuLds& S, uint64_t* __restrict__ bits,
-                         uint64_t c0, uint64_t c1) {
+                         const Classes& cl, GroupCounters& gc, LfuLds& S,
+                         uint64_t* __restrict__ bits, uint64_t c0, uint64_t c1, bool g1,
+                         uint32_t g0) {
   const uint32_t tid = threadIdx.x;
   const uint32_t o = j.order;
   const uint32_t L = (uint32_t)(c1 - c0);
-  __shared__ uint32_t s_nc, s_h, s_lastp, s_lastm;
-  __shared__ uint64_t s_vw, s_victw;
-  uint32_t bb[kRIt], ww[kRIt], gg[kRIt], f0[kRIt];
-  bool v[kRIt], cm[kRIt], res0[kRIt];
+  const uint32_t l0 = tid * kRIt;
+  const uint64_t p0 = c0 + l0;
+  RCLK(t_a);
+  bool v[kRIt];
+#pragma unroll
+  for (int e = 0; e < kRIt; ++e) v[e] = l0 + e < L && p0 + e >= j.begin;
+  const bool all = v[0] && v[kRIt - 1];
+  uint32_t bb[kRIt], ww[kRIt], gg[kRIt] = {g0, g0, g0, g0}, kk[kRIt], nx[kRIt], f0[kRIt];
+  bool cm[kRIt], res0[kRIt];
+  load4_u32(a.bid[o], p0, all, v, bb);
+  load4_u8(a.w8[o], p0, all, v, ww);
+  load4_u32(a.key[o], p0, all, v, kk);
+  load4_u32(a.nxt[o], p0, all, v, nx);
+  if (!g1) load4_u8(a.g8[o], p0, all, v, gg);
+  uint32_t h = S.head1;
 #pragma unroll
   for (int e = 0; e < kRIt; ++e) {
-    const uint32_t loc = tid * kRIt + e;
-    const uint64_t p = c0 + loc;
-    v[e] = loc < L && p >= j.begin;
-    bb[e] = v[e] ? a.bid[o][p] : 0u;
-    ww[e] = v[e] ? a.w8[o][p] : 0u;
-    gg[e] = v[e] ? a.g8[o][p] : 0u;
-    const uint32_t k = v[e] ? a.key[o][p] : 0u;
-    const int lp = (k != 0 && (uint64_t)(k - 1) >= c0) ? (int)((uint64_t)(k - 1) - c0) : -1;
-    const uint32_t nx = v[e] ? a.nxt[o][p] : kNone;
-    const bool again = nx != kNone && (uint64_t)nx < c1;
+    const uint32_t loc = l0 + e;
+    const int lp = (kk[e] != 0 && (uint64_t)(kk[e] - 1) >= c0) ? (int)((uint64_t)(kk[e] - 1) - c0)
+                                                               : -1;
+    const bool again = v[e] && nx[e] != kNone && (uint64_t)nx[e] < c1;
     const uint64_t s = v[e] ? st[bb[e]] : 0ull;
     f0[e] = (uint32_t)s;
     res0[e] = f0[e] != 0;
     cm[e] = v[e] && lp < 0 && !res0[e];
     S.lp[loc] = (int16_t)lp;
     S.occ[loc] = lp >= 0 ? 1 : 0;
-    S.nxloc[loc] = again ? (uint16_t)((uint64_t)nx - c0) : kInf16;
+    S.nxloc[loc] = again ? (uint16_t)((uint64_t)nx[e] - c0) : kInf16;
     S.pw[loc] = (uint8_t)ww[e];
     S.capm[loc] = 0;
     S.mskip[loc] = again ? 1 : 0;
     S.mcons[loc] = 0;
   }
-  uint64_t x = 0;
+  uint32_t x = 0;
 #pragma unroll
   for (int e = 0; e < kRIt; ++e) x += cm[e] ? ww[e] : 0u;
-  uint64_t itot0;
-  block_excl_scan<kRNT>(x, S.red, &itot0);
-  const uint64_t used0 = ls.used;
+  uint32_t itot0;
+  block_excl_scan_u32<kRNT>(x, S.red, itot0);
+  const uint64_t used0 = S.used;
   const uint64_t ev0 = (used0 + itot0 > j.cap) ? used0 + itot0 - j.cap : 0ull;
-  if (tid == 0) {
-    s_nc = 0;
-    s_vw = 0;
-    s_h = ls.head1;
-    s_lastp = 0;
-    s_lastm = 0;
-    s_victw = 0;
-  }
-  __syncthreads();
+  RCLK(t_b);
+  RTIME(kStT0, t_a, t_b);
   uint32_t nc0 = 0;
   bool reached = false;
   if (ev0 > 0) {
-    // old count-1 residents from head1 on, until the untouched ones alone
-    // cover the first-touch demand (a capacity miss adds as much demand as
-    // it adds victims), the chunk start is reached, or the buffer is full
+    // count-1 residents from head1 on, until the untouched ones alone cover
+    // the first-touch demand (a capacity miss adds as much demand as it adds
+    // victims), the chunk start is reached, or the buffer is full
+    uint32_t n0 = 0;
+    uint64_t vw = 0;
     for (;;) {
-      const uint32_t h = s_h;
-      const uint64_t vw = s_vw;
-      const uint32_t n0 = s_nc;
-      if (vw >= ev0 || (uint64_t)h >= c0 || n0 + kRNT > kCand) break;
-      const uint64_t q = (uint64_t)h + tid;
-      bool live = false, touched = false;
-      uint32_t bq = 0, aq = kInf16;
-      if (q < c0) {
-        bq = a.bid[o][q];
-        const uint64_t sq = st[bq];
-        live = (uint32_t)sq == 1u && (sq >> 32) == q;
-        if (live) {
-          const uint32_t nx = a.nxt[o][q];
-          touched = nx != kNone && (uint64_t)nx < c1;
-          aq = touched ? (uint32_t)((uint64_t)nx - c0) : kInf16;
+      if (vw >= ev0 || (uint64_t)h >= c0 || n0 + kRNT * kCScan > kCand) break;
+      RSTAT(blockIdx.x, kStScanned, 1);
+      bool live[kCScan], touched[kCScan];
+      uint32_t bq[kCScan], wq[kCScan], aq[kCScan];
+#pragma unroll
+      for (int e = 0; e < kCScan; ++e) {
+        const uint64_t q = (uint64_t)h + tid * kCScan + e;
+        live[e] = false;
+        touched[e] = false;
+        aq[e] = kInf16;
+        bq[e] = 0;
+        wq[e] = 0;
+        if (q < c0) {
+          const uint64_t word = bits[(q >> 6) - j.word0];
+          const uint32_t nxq = a.nxt[o][q];
+          bq[e] = a.bid[o][q];
+          wq[e] = a.w8[o][q];
+          live[e] = !((word >> (q & 63)) & 1ull) && (nxq == kNone || (uint64_t)nxq >= c0);
+          touched[e] = live[e] && nxq != kNone && (uint64_t)nxq < c1;
+          aq[e] = touched[e] ? (uint32_t)((uint64_t)nxq - c0) : kInf16;
         }
       }
-      uint32_t cnt_live;
-      const uint32_t pos = block_excl_scan<kRNT>(live ? 1u : 0u, S.red32, &cnt_live);
-      const uint32_t wq = live ? (uint32_t)a.blk_w[bq] : 0u;
-      if (live) {
-        S.cq[n0 + pos] = (uint32_t)q;
-        S.cb[n0 + pos] = bq;
-        S.cw[n0 + pos] = (uint8_t)wq;
-        S.ca[n0 + pos] = (uint16_t)aq;
-        S.cskip[n0 + pos] = touched ? 1 : 0;
-        S.ccons[n0 + pos] = 0;
+      uint32_t cl_ = 0, cw_ = 0;
+#pragma unroll
+      for (int e = 0; e < kCScan; ++e) {
+        cl_ += live[e] ? 1u : 0u;
+        cw_ += (live[e] && !touched[e]) ? wq[e] : 0u;
       }
-      uint64_t vsum;
-      block_excl_scan<kRNT>((uint64_t)((live && !touched) ? wq : 0u), S.red, &vsum);
-      if (tid == 0) {
-        s_nc = n0 + cnt_live;
-        s_vw = vw + vsum;
-        s_h = (uint32_t)min<uint64_t>((uint64_t)h + kRNT, c0);
+      uint32_t pos, dummy, cnt_live, vsum;
+      block_excl_scan2_u32<kRNT>(cl_, cw_, S.red, pos, dummy, cnt_live, vsum);
+#pragma unroll
+      for (int e = 0; e < kCScan; ++e) {
+        if (!live[e]) continue;
+        const uint32_t k = n0 + pos++;
+        S.cq[k] = h + tid * kCScan + e;
+        S.cb[k] = bq[e];
+        S.cw[k] = (uint8_t)wq[e];
+        S.ca[k] = (uint16_t)aq[e];
+        S.cskip[k] = touched[e] ? 1 : 0;
+        S.ccons[k] = 0;
       }
-      __syncthreads();
+      n0 += cnt_live;
+      vw += vsum;
+      h = (uint32_t)min<uint64_t>((uint64_t)h + kRNT * kCScan, c0);
     }
-    nc0 = s_nc;
-    reached = (uint64_t)s_h >= c0;
-    // entries before the first live one are dead for good: skip them from now on
-    if (tid == 0) ls.head1 = nc0 ? S.cq[0] : s_h;
+    __syncthreads();
+    nc0 = n0;
+    reached = (uint64_t)h >= c0;
+    // positions before the first live entry hold no count-1 member any more
+    if (tid == 0) S.head1 = nc0 ? S.cq[0] : h;
   }
+  RCLK(t_c);
+  RTIME(kStT1, t_b, t_c);
   // ---- fixed point over (misses, promotions, evictions)
-  uint64_t itot = itot0;
+  uint32_t itot = itot0;
   bool converged = ev0 == 0;
+  uint8_t cur = 0xFF;  // stamp of the latest capacity-miss set (0xFF: none yet)
   for (int it = 0; !converged && it < 24; ++it) {
-    bool mi[kRIt];
-    uint64_t xw = 0;
-    uint32_t xm = 0;
+    RSTAT(blockIdx.x, kStIters, 1);
+    bool mi[kRIt], oldcap[kRIt];
+    uint32_t xw = 0, xm = 0;
 #pragma unroll
     for (int e = 0; e < kRIt; ++e) {
-      mi[e] = cm[e] || (v[e] && S.capm[tid * kRIt + e]);
+      oldcap[e] = v[e] && S.capm[l0 + e] == cur;
+      mi[e] = cm[e] || oldcap[e];
       xw += mi[e] ? ww[e] : 0u;
       xm += mi[e] ? 1u : 0u;
     }
-    uint64_t wpre = block_excl_scan<kRNT>(xw, S.red, &itot);
-    uint32_t nm;
-    uint32_t mpre = block_excl_scan<kRNT>(xm, S.red32, &nm);
+    uint32_t wpre, mpre, nm;
+    block_excl_scan2_u32<kRNT>(xw, xm, S.red, wpre, mpre, itot, nm);
     const uint64_t evtot = (used0 + itot > j.cap) ? used0 + itot - j.cap : 0ull;
 #pragma unroll
     for (int e = 0; e < kRIt; ++e) {
       if (mi[e]) {
         wpre += ww[e];
         const int64_t need = (int64_t)(used0 + wpre) - (int64_t)j.cap;
-        S.mpos[mpre] = (uint16_t)(tid * kRIt + e);
+        S.mpos[mpre] = (uint16_t)(l0 + e);
         S.mneed[mpre] = need > 0 ? (uint32_t)need : 0u;
         ++mpre;
       }
@@ -632,18 +770,29 @@ __device__ bool lfu_fast(const JobDev& j, const JobArgs& a, uint64_t* __restrict
       xs += qw[e];
     }
     uint32_t elig;
-    uint32_t run = block_excl_scan<kRNT>(xs, S.red32, &elig);
+    uint32_t run = block_excl_scan_u32<kRNT>(xs, S.red, elig);
     bool bad = (uint64_t)elig < evtot;
+    // entry k is consumed by the first miss whose demand exceeds the
+    // eligible weight queued before k; demands and prefixes both rise, so
+    // the search resumes where the previous entry's ended
     uint32_t evk[kCPT];
+    uint32_t lo = 0;
+    bool started = false;
 #pragma unroll
     for (int e = 0; e < kCPT; ++e) {
       const uint32_t k = tid * kCPT + e;
       evk[e] = kInf16;
       if (k < nq && qw[e] && (uint64_t)run < evtot) {
-        uint32_t lo = 0, hi = nm;
-        while (lo < hi) {
-          const uint32_t mid = (lo + hi) >> 1;
-          if (S.mneed[mid] > run) hi = mid; else lo = mid + 1;
+        if (!started) {
+          lo = upper_bound(S.mneed, 0u, nm, run);
+          started = true;
+        } else {
+          int s = 0;
+          while (lo < nm && S.mneed[lo] <= run && s < 4) {
+            ++lo;
+            ++s;
+          }
+          if (lo < nm && S.mneed[lo] <= run) lo = upper_bound(S.mneed, lo, nm, run);
         }
         evk[e] = (lo < nm) ? S.mpos[lo] : kInf16;
         if (k >= nc0) {
@@ -654,7 +803,6 @@ __device__ bool lfu_fast(const JobDev& j, const JobArgs& a, uint64_t* __restrict
       }
       run += qw[e];
     }
-    if (__syncthreads_or(bad)) return false;
     // the pointer reaches entry k when the first consumed entry at or after k goes
     uint32_t suf[kCPT];
     uint32_t mn = kInf16;
@@ -663,16 +811,14 @@ __device__ bool lfu_fast(const JobDev& j, const JobArgs& a, uint64_t* __restrict
       mn = min(mn, evk[e]);
       suf[e] = mn;
     }
-    const uint32_t tmin = block_suffix_min_excl<kRNT>(mn, S.red32);
-    // capacity misses are rebuilt from scratch: remember the old ones, clear
-    bool oldcap[kRIt];
-#pragma unroll
-    for (int e = 0; e < kRIt; ++e) {
-      const uint32_t loc = tid * kRIt + e;
-      oldcap[e] = S.capm[loc] != 0;
-      S.capm[loc] = 0;
+    uint32_t tmin;
+    bool anybad;
+    block_suffix_min_flag(mn, bad, S.sfx, tmin, anybad);
+    if (anybad) {
+      RSTAT(blockIdx.x, kStFailElig, 1);
+      return false;
     }
-    __syncthreads();
+    const uint8_t ns = (uint8_t)(it + 1);
     bool changed = false;
 #pragma unroll
     for (int e = 0; e < kCPT; ++e) {
@@ -693,96 +839,125 @@ __device__ bool lfu_fast(const JobDev& j, const JobArgs& a, uint64_t* __restrict
         S.mskip[m] = nskip ? 1 : 0;
         S.mcons[m] = cons ? 1 : 0;
       }
-      if (ncap) S.capm[ak] = 1;  // each touch position is the next touch of one entry
+      if (ncap) S.capm[ak] = ns;  // each touch position is the next touch of one entry
     }
     __syncthreads();
 #pragma unroll
     for (int e = 0; e < kRIt; ++e) {
-      const uint32_t loc = tid * kRIt + e;
-      changed |= oldcap[e] != (S.capm[loc] != 0);
+      const uint32_t loc = l0 + e;
+      changed |= oldcap[e] != (v[e] && S.capm[loc] == ns);
       // entries that stopped being misses lose their queue flags
       if (v[e] && !mi[e] && S.mcons[loc]) {
         S.mcons[loc] = 0;
         changed = true;
       }
     }
+    cur = ns;
     if (!__syncthreads_or(changed)) converged = true;
   }
-  if (!converged) return false;
+  if (!converged) {
+    RSTAT(blockIdx.x, kStFailConv, 1);
+    return false;
+  }
+  RCLK(t_d);
+  RTIME(kStT2, t_c, t_d);
   // ---- consistent: apply.  Pointer jumping gives each touch the number of
   // earlier touches of its block in the chunk and the latest miss among them.
+  bool miss[kRIt];
 #pragma unroll
   for (int e = 0; e < kRIt; ++e) {
-    const uint32_t loc = tid * kRIt + e;
-    const bool miss = cm[e] || (v[e] && S.capm[loc]);
-    S.lmiss[loc] = miss ? (int16_t)loc : (int16_t)-1;
+    const uint32_t loc = l0 + e;
+    miss[e] = cm[e] || (v[e] && S.capm[loc] == cur);
+    S.lmiss[loc] = miss[e] ? (int16_t)loc : (int16_t)-1;
   }
   __syncthreads();
-  for (uint32_t r = 0; (1u << r) < L; ++r) {
+  for (;;) {
     int16_t np[kRIt], nl[kRIt];
     uint16_t no[kRIt];
+    bool moved = false;
 #pragma unroll
     for (int e = 0; e < kRIt; ++e) {
-      const uint32_t loc = tid * kRIt + e;
+      const uint32_t loc = l0 + e;
       const int16_t p = S.lp[loc];
       no[e] = S.occ[loc];
       np[e] = p;
       nl[e] = S.lmiss[loc];
       if (p >= 0) {
-        no[e] = (uint16_t)(S.occ[loc] + S.occ[p]);
-        np[e] = S.lp[p] >= 0 ? S.lp[p] : p;
+        const int16_t pp = S.lp[p];
+        if (pp >= 0) {
+          no[e] = (uint16_t)(no[e] + S.occ[p]);
+          np[e] = pp;
+          moved = true;
+        }
         if (nl[e] < 0) nl[e] = S.lmiss[p];
       }
     }
     __syncthreads();
 #pragma unroll
     for (int e = 0; e < kRIt; ++e) {
-      const uint32_t loc = tid * kRIt + e;
+      const uint32_t loc = l0 + e;
       S.lp[loc] = np[e];
       S.occ[loc] = no[e];
       S.lmiss[loc] = nl[e];
     }
-    __syncthreads();
+    if (!__syncthreads_or(moved)) break;
   }
-  // old entries evicted without being touched again
-  uint64_t vw = 0;
+  RCLK(t_e);
+  RTIME(kStT3, t_d, t_e);
+  // per-thread partials: insertions, evictions, victim weight, last entries taken
+  uint32_t p_ins = 0, p_insw = 0, p_ev = 0, p_evw = 0, p_vw = 0, p_lastp = 0, p_lastm = 0,
+           p_n1 = 0;
+  // old entries evicted
   for (uint32_t k = tid; k < nc0; k += kRNT) {
     if (!S.ccons[k]) continue;
     const uint32_t b = S.cb[k];
-    const uint32_t g = a.blk_g[b];
-    atomicAdd(&gc.ev[g], 1ull);
-    atomicAdd(&gc.evw[g], (unsigned long long)S.cw[k]);
-    vw += S.cw[k];
-    atomicMax(&s_lastp, k + 1);
-    if (S.ca[k] == kInf16) {
+    const uint32_t w = S.cw[k];
+    if (g1) {
+      ++p_ev;
+      p_evw += w;
+    } else {
+      const uint32_t g = a.blk_g[b];
+      atomicAdd(&gc.ev[g], 1ull);
+      atomicAdd(&gc.evw[g], (unsigned long long)w);
+    }
+    p_vw += w;
+    p_lastp = max(p_lastp, k + 1);
+    if (S.ca[k] == kInf16) {  // not touched again in the chunk: leaves class 1 for good
       st[b] = 0;
-      atomicSub(&ccount[1], 1u);
+      ++p_n1;
     }
   }
+  bool hit[kRIt];
 #pragma unroll
   for (int e = 0; e < kRIt; ++e) {
-    const uint32_t loc = tid * kRIt + e;
-    const bool miss = cm[e] || (v[e] && S.capm[loc]);
-    S.hit[loc] = (v[e] && !miss) ? 1 : 0;
-    if (!v[e]) continue;
-    if (miss) {
+    const uint32_t loc = l0 + e;
+    hit[e] = v[e] && !miss[e];
+    if (!(v[e] && miss[e])) continue;
+    const bool cons = S.mcons[loc] != 0;  // inserted here, evicted later in the chunk
+    if (g1) {
+      ++p_ins;
+      p_insw += ww[e];
+      p_ev += cons ? 1u : 0u;
+      p_evw += cons ? ww[e] : 0u;
+    } else {
       atomicAdd(&gc.ins[gg[e]], 1ull);
       atomicAdd(&gc.insw[gg[e]], (unsigned long long)ww[e]);
-      if (S.mcons[loc]) {  // inserted here, evicted later in the chunk
+      if (cons) {
         atomicAdd(&gc.ev[gg[e]], 1ull);
         atomicAdd(&gc.evw[gg[e]], (unsigned long long)ww[e]);
-        vw += ww[e];
-        atomicMax(&s_lastm, loc + 1);
       }
     }
+    if (cons) {
+      p_vw += ww[e];
+      p_lastm = max(p_lastm, loc + 1);
+    }
   }
-  if (vw) atomicAdd((unsigned long long*)&s_victw, (unsigned long long)vw);
   // final state of every touched block, at its last touch
   uint32_t fnew[kRIt];
   bool fin[kRIt];
 #pragma unroll
   for (int e = 0; e < kRIt; ++e) {
-    const uint32_t loc = tid * kRIt + e;
+    const uint32_t loc = l0 + e;
     fnew[e] = 0;
     fin[e] = v[e] && S.nxloc[loc] == kInf16;
     if (!fin[e]) continue;
@@ -793,98 +968,150 @@ __device__ bool lfu_fast(const JobDev& j, const JobArgs& a, uint64_t* __restrict
       fnew[e] = f0[e] + (uint32_t)S.occ[loc] + 1u;
     }
     st[bb[e]] = fnew[e] ? (((uint64_t)(c0 + loc) << 32) | fnew[e]) : 0ull;
-    if (res0[e]) atomicSub(&ccount[f0[e]], 1u);
-    if (fnew[e]) atomicAdd(&ccount[fnew[e]], 1u);
+    if (res0[e]) class_add_par(cl, f0[e], -1);
+    if (fnew[e]) class_add_par(cl, fnew[e], +1);
+  }
+  {
+    const uint32_t w = tid / 64;
+    const uint32_t r[8] = {wave_sum(p_ins), wave_sum(p_insw), wave_sum(p_ev), wave_sum(p_evw),
+                           wave_sum(p_vw), wave_max_u32(p_lastp), wave_max_u32(p_lastm),
+                           wave_sum(p_n1)};
+    if (lane_id() == 0) {
+#pragma unroll
+      for (int f = 0; f < 8; ++f) S.red8[w][f] = r[f];
+      if (r[7]) atomicSub(&S.ccnt[1], r[7]);
+    }
   }
   __syncthreads();
-  // nonempty-class bits from the final counts of every class touched above
+  RCLK(t_f);
+  RTIME(kStT4, t_e, t_f);
+  // nonempty-class bits: LDS words from the counts, HBM words for the
+  // high classes touched above
+  {
+    const uint64_t bal = __ballot(S.ccnt[tid] != 0u);
+    if (lane_id() == 0) S.cnz[tid / 64] = bal;
+  }
 #pragma unroll
   for (int e = 0; e < kRIt; ++e) {
     if (!fin[e]) continue;
 #pragma unroll
     for (int z = 0; z < 2; ++z) {
       const uint32_t f = z == 0 ? (res0[e] ? f0[e] : 0u) : fnew[e];
-      if (f == 0) continue;
+      if (f < kLdsClass) continue;
       const uint64_t bit = 1ull << (f & 63);
-      if (ld_acq(&ccount[f]) > 0) atomicOr((unsigned long long*)&nz[f >> 6], bit);
-      else atomicAnd((unsigned long long*)&nz[f >> 6], ~bit);
+      if (ld_acq(&cl.gcnt[f]) > 0) atomicOr((unsigned long long*)&cl.gnz[f >> 6], bit);
+      else atomicAnd((unsigned long long*)&cl.gnz[f >> 6], ~bit);
     }
   }
+  store_hits(hit, c0, L, j, bits);
   if (tid == 0) {
-    if (ld_acq(&ccount[1]) > 0) atomicOr((unsigned long long*)&nz[0], 2ull);
-    else atomicAnd((unsigned long long*)&nz[0], ~2ull);
+    uint32_t t[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (int w = 0; w < kRNW; ++w) {
+      for (int f = 0; f < 8; ++f)
+        t[f] = (f == 5 || f == 6) ? max(t[f], S.red8[w][f]) : t[f] + S.red8[w][f];
+    }
+    if (g1) {
+      gc.ins[g0] += t[0];
+      gc.insw[g0] += t[1];
+      gc.ev[g0] += t[2];
+      gc.evw[g0] += t[3];
+    }
+    S.used = used0 + itot - t[4];
+    if (t[6]) S.head1 = (uint32_t)(c0 + t[6]);          // last new entry taken + 1
+    else if (t[5]) S.head1 = S.cq[t[5] - 1] + 1;         // last old entry taken + 1
   }
   __syncthreads();
-  store_bits(S.hit, c0, L, j, bits);
   if (tid == 0) {
-    ls.used = used0 + itot - s_victw;
-    if (s_lastm) ls.head1 = (uint32_t)(c0 + s_lastm);           // last new entry taken + 1
-    else if (s_lastp) ls.head1 = S.cq[s_lastp - 1] + 1;          // last old entry taken + 1
-    const uint32_t nf = next_class(nz, nw, 1);
-    if (nf != 0xFFFFFFFFu) ls.fmin = nf;
+    const uint32_t nf = next_class(cl, 1);
+    if (nf != 0xFFFFFFFFu) S.fmin = nf;
   }
-  __syncthreads();
+  RCLK(t_g);
+  RTIME(kStT5, t_f, t_g);
+  RSTAT(blockIdx.x, kStFastOk, 1);
+  RSTAT(blockIdx.x, kStFastAcc, L);
   return true;
 }
 
 __device__ void lfu_chunked(const JobDev& j, const JobArgs& a, uint64_t* __restrict__ st,
                             uint32_t* __restrict__ cls, uint64_t* __restrict__ bits,
-                            unsigned long long* cnt) {
-  __shared__ LfuLds S;
-  __shared__ LfuShared ls;
-  __shared__ GroupCounters gc;
-  __shared__ bool s_ok;
+                            GroupCounters& gc, LfuLds& S, bool g1, uint32_t g0) {
   const uint32_t tid = threadIdx.x;
   uint32_t* head = cls + j.class_off;
-  uint32_t* ccount = head + a.n_class;
-  uint64_t* nz = reinterpret_cast<uint64_t*>(ccount + a.n_class);
-  const uint32_t nw = (a.n_class + 63) / 64;
-  if (tid < KV_MAX_GROUPS) gc.ins[tid] = gc.insw[tid] = gc.ev[tid] = gc.evw[tid] = 0;
+  Classes cl;
+  cl.lcnt = S.ccnt;
+  cl.lnz = S.cnz;
+  cl.gcnt = head + a.n_class;
+  cl.gnz = reinterpret_cast<uint64_t*>(head + 2 * a.n_class);
+  cl.nw = (a.n_class + 63) / 64;
+  for (uint32_t f = tid; f < kLdsClass; f += kRNT) S.ccnt[f] = 0;
+  if (tid < kLdsClassWords) S.cnz[tid] = 0;
   if (tid == 0) {
-    ls.used = 0;
-    ls.fmin = 1;
-    ls.head1 = (uint32_t)j.begin;
-    s_ok = true;
+    S.used = 0;
+    S.fmin = 1;
+    S.head1 = (uint32_t)j.begin;
+    S.ok = 1;
   }
   __syncthreads();
   uint64_t pos = j.begin & ~63ull;
   uint32_t len = j.chunk;
   while (pos < j.end) {
     const uint32_t l = (uint32_t)min<uint64_t>(len, j.end - pos);
-    if (lfu_fast(j, a, st, ccount, nz, nw, ls, gc, S, bits, pos, pos + l)) {
+    if (lfu_fast(j, a, st, cl, gc, S, bits, pos, pos + l, g1, g0)) {
       pos += l;
       len = min<uint32_t>(len * 2, j.chunk);
     } else if (l > kMinFast) {
       len = max<uint32_t>(kMinFast, (l / 2) & ~63u);
     } else {
       __syncthreads();
-      if (tid == 0) s_ok = lfu_serial_range(j, a, st, head, ccount, nz, nw, ls, gc, bits, pos,
-                                            pos + l);
+      if (tid == 0) S.ok = lfu_serial_range(j, a, st, head, cl, S, gc, bits, pos, pos + l) ? 1 : 0;
       RSTAT(blockIdx.x, kStSerialAcc, l);
       __syncthreads();
-      if (!s_ok) break;
+      if (!S.ok) break;
       pos += l;
     }
   }
   __syncthreads();
-  write_counters(gc, a.n_groups, cnt);
-  if (tid == 0 && !s_ok) cnt[0] = ~0ull;  // poison: surfaced as an impossible count
 }
+
+union ReplayLds {
+  FifoLds f;
+  LfuLds l;
+};
 
 __global__ __launch_bounds__(kRNT) void k_replay(const JobDev* __restrict__ jobs, JobArgs a,
                                                  uint64_t* __restrict__ state,
                                                  uint32_t* __restrict__ cls,
                                                  uint64_t* __restrict__ bits,
                                                  unsigned long long* __restrict__ jcnt) {
+  __shared__ ReplayLds lds;
+  __shared__ GroupCounters gc;
   const JobDev j = jobs[blockIdx.x];
   if (j.closed) return;
+  const uint32_t tid = threadIdx.x;
+  if (tid < KV_MAX_GROUPS) gc.ins[tid] = gc.insw[tid] = gc.ev[tid] = gc.evw[tid] = 0;
+#ifdef KV_REPLAY_STATS
+  if (tid < kStats) s_rstats[tid] = 0;
+#endif
+  __syncthreads();
+  // one group for every access of the job: counters add up per wavefront
+  const bool g1 = a.n_groups == 1 || j.group != KV_MAX_GROUPS;
+  const uint32_t g0 = j.group == KV_MAX_GROUPS ? 0u : j.group;
   unsigned long long* cnt = jcnt + (uint64_t)blockIdx.x * a.n_groups * 4;
-  if (j.kind == kJobFifoChunk)
-    fifo_chunked(j, a, state + j.state_off, bits + j.bits_off, cnt);
-  else if (j.kind == kJobFifoSerial)
-    fifo_serial(j, a, state + j.state_off, bits + j.bits_off, cnt);
-  else
-    lfu_chunked(j, a, state + j.state_off, cls, bits + j.bits_off, cnt);
+  bool ok = true;
+  if (j.kind == kJobFifoChunk) {
+    fifo_chunked(j, a, state + j.state_off, bits + j.bits_off, gc, lds.f, g1, g0);
+  } else if (j.kind == kJobFifoSerial) {
+    fifo_serial(j, a, state + j.state_off, bits + j.bits_off, gc);
+  } else {
+    lfu_chunked(j, a, state + j.state_off, cls, bits + j.bits_off, gc, lds.l, g1, g0);
+    ok = lds.l.ok != 0;
+  }
+  __syncthreads();
+  write_counters(gc, a.n_groups, cnt);
+  if (tid == 0 && !ok) cnt[0] = ~0ull;  // poison: surfaced as an impossible count
+#ifdef KV_REPLAY_STATS
+  if (tid < kStats) g_rstats[blockIdx.x & 255][tid] += s_rstats[tid];
+#endif
 }
 
 // Per order: re-access bits (key != 0), weight bit-planes, group masks.
@@ -1183,12 +1410,15 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
     unsigned long long hs[256][kStats];
     KV_HIP(hipMemcpyFromSymbol(hs, HIP_SYMBOL(g_rstats), sizeof(hs)));
     for (uint32_t q = 0; q < nj && q < 256; ++q) {
-      if (jd[q].closed || jd[q].kind != kJobLfu) continue;
-      fprintf(stderr, "[replay-stats] job %u cap %llu: fast %llu (acc %llu) failpool %llu "
-              "failelig %llu failconv %llu serial_acc %llu iters %llu scanned %llu\n", q,
+      if (jd[q].closed) continue;
+      fprintf(stderr, "[replay-stats] %s job %u cap %llu: fast %llu (acc %llu) failpool %llu "
+              "failelig %llu failconv %llu serial_acc %llu iters %llu scanned %llu "
+              "clk load %llu scan %llu fix %llu jump %llu apply %llu fin %llu x6 %llu x7 %llu x8 %llu\n",
+              jd[q].kind == kJobLfu ? "lfu" : "fifo", q,
               (unsigned long long)jd[q].cap, hs[q][kStFastOk], hs[q][kStFastAcc],
               hs[q][kStFailPool], hs[q][kStFailElig], hs[q][kStFailConv], hs[q][kStSerialAcc],
-              hs[q][kStIters], hs[q][kStScanned]);
+              hs[q][kStIters], hs[q][kStScanned], hs[q][kStT0], hs[q][kStT1], hs[q][kStT2],
+              hs[q][kStT3], hs[q][kStT4], hs[q][kStT5], hs[q][kStT6], hs[q][kStT7], hs[q][kStT8]);
     }
   }
 #endif

@@ -25,6 +25,84 @@ __device__ __forceinline__ T wave_incl_scan(T v) {
   return v;
 }
 
+// Inclusive prefix sum of 32-bit values across the 64 lanes with DPP: row
+// shifts build the sums inside each row of 16 lanes, two row broadcasts carry
+// them across rows.  Lanes outside a DPP source row add 0.
+__device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t v) {
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xf, 0xf, false);  // row_shr:1
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xf, 0xf, false);  // row_shr:2
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xf, 0xf, false);  // row_shr:4
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xf, 0xf, false);  // row_shr:8
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xc, 0xf, false);  // row_bcast:31
+  return v;
+}
+
+// Exclusive prefix sums of two 32-bit values over a block of NT threads.
+// `sh` holds 2 * (NT / 64) words of shared memory; two barriers.
+template <int NT>
+__device__ __forceinline__ void block_excl_scan2_u32(uint32_t a, uint32_t b, uint32_t* sh,
+                                                     uint32_t& pa, uint32_t& pb, uint32_t& ta,
+                                                     uint32_t& tb) {
+  constexpr int NW = NT / 64;
+  const int w = threadIdx.x / 64;
+  const uint32_t ia = wave_incl_scan_u32(a), ib = wave_incl_scan_u32(b);
+  if (lane_id() == 63) {
+    sh[w] = ia;
+    sh[NW + w] = ib;
+  }
+  __syncthreads();
+  uint32_t sa = 0, sb = 0, xa = 0, xb = 0;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) {
+    const uint32_t ya = sh[i], yb = sh[NW + i];
+    xa += (i < w) ? ya : 0u;
+    xb += (i < w) ? yb : 0u;
+    sa += ya;
+    sb += yb;
+  }
+  __syncthreads();
+  pa = xa + ia - a;
+  pb = xb + ib - b;
+  ta = sa;
+  tb = sb;
+}
+
+template <int NT>
+__device__ __forceinline__ uint32_t block_excl_scan_u32(uint32_t a, uint32_t* sh, uint32_t& ta) {
+  constexpr int NW = NT / 64;
+  const int w = threadIdx.x / 64;
+  const uint32_t ia = wave_incl_scan_u32(a);
+  if (lane_id() == 63) sh[w] = ia;
+  __syncthreads();
+  uint32_t xa = 0, sa = 0;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) {
+    const uint32_t ya = sh[i];
+    xa += (i < w) ? ya : 0u;
+    sa += ya;
+  }
+  __syncthreads();
+  ta = sa;
+  return xa + ia - a;
+}
+
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) v = max(v, (uint32_t)__shfl_xor(v, d, 64));
+  return v;
+}
+
+// Bit m of the low 16 bits moves to bit 4m.
+__device__ __forceinline__ uint64_t spread4(uint64_t x) {
+  x &= 0xFFFFull;
+  x = (x | (x << 24)) & 0x000000FF000000FFull;
+  x = (x | (x << 12)) & 0x000F000F000F000Full;
+  x = (x | (x << 6)) & 0x0303030303030303ull;
+  x = (x | (x << 3)) & 0x1111111111111111ull;
+  return x;
+}
+
 template <class T>
 __device__ __forceinline__ T wave_sum(T v) {
 #pragma unroll

@@ -14,7 +14,8 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libkvcfg.so")
+# KVCFG_LIB names another build of the same library (e.g. a diagnostics build)
+LIB_PATH = os.environ.get("KVCFG_LIB") or os.path.join(_HERE, "libkvcfg.so")
 
 KV_OK, KV_ERR_INVALID, KV_ERR_NOMEM, KV_ERR_DEVICE, KV_ERR_UNSUPPORTED = 0, -1, -2, -3, -4
 KV_MAX_GROUPS, KV_TIERS, KV_FIELDS = 16, 3, 8
