@@ -208,9 +208,33 @@ __global__ __launch_bounds__(256) void k_links(const uint64_t* __restrict__ K,
   if (err) atomicOr(&st->err, err);
 }
 
+// First occurrences in trace order: flag[pos] = 1 where the block appears
+// for the first time.
+__global__ __launch_bounds__(256) void k_first_flags(const uint32_t* __restrict__ key,
+                                                     uint64_t n, uint32_t* __restrict__ flag) {
+  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (uint64_t)gridDim.x * blockDim.x)
+    flag[i] = key[i] == 0u ? 1u : 0u;
+}
+
+// Position of each hash group's first element (its first occurrence: ties
+// in the sort go by position).
+__global__ __launch_bounds__(256) void k_first_pos(const uint32_t* __restrict__ V,
+                                                   const uint32_t* __restrict__ incl,
+                                                   const uint32_t* __restrict__ newflag,
+                                                   uint64_t n, uint32_t* __restrict__ firstpos) {
+  for (uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; k < n;
+       k += (uint64_t)gridDim.x * blockDim.x)
+    if (newflag[k]) firstpos[incl[k] - 1u] = V[k];
+}
+
+// Dense block ids in order of first occurrence, so that blocks met close
+// together in the trace sit close together in the per-block state arrays.
 __global__ __launch_bounds__(256) void k_ids(const uint32_t* __restrict__ V,
                                              const uint32_t* __restrict__ incl,
-                                             const uint32_t* __restrict__ newflag, uint64_t n,
+                                             const uint32_t* __restrict__ newflag,
+                                             const uint32_t* __restrict__ firstpos,
+                                             const uint32_t* __restrict__ fincl, uint64_t n,
                                              uint32_t* __restrict__ bid,
                                              uint8_t* __restrict__ blk_w,
                                              uint8_t* __restrict__ blk_g,
@@ -226,13 +250,14 @@ __global__ __launch_bounds__(256) void k_ids(const uint32_t* __restrict__ V,
   for (uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; k < n;
        k += (uint64_t)gridDim.x * blockDim.x) {
     const uint32_t pos = V[k];
-    const uint32_t id = incl[k] - 1u;
+    const uint32_t grp = incl[k] - 1u;
+    const uint32_t id = fincl[firstpos[grp]] - 1u;
     bid[pos] = id;
     if (newflag[k]) {
       const uint8_t w = w8[pos], g = g8[pos];
       blk_w[id] = w;
       blk_g[id] = g;
-      runstart[id] = (uint32_t)k;
+      runstart[grp] = (uint32_t)k;
       atomicAdd(&su[g], 1ull);
       atomicAdd(&suw[g], (unsigned long long)w);
     }
@@ -388,10 +413,21 @@ kv_status canon_build(Trace& t, const kv_trace_desc& d, hipStream_t s) {
   if ((st = t.blk_w.reserve(u)) != KV_OK) return st;
   if ((st = t.blk_g.reserve(u)) != KV_OK) return st;
   uint32_t* runstart = vout;  // n >= u entries available
+  // the sorted keys are no longer needed: their buffer holds the first-
+  // occurrence flags / ranks (n) and the groups' first positions (u <= n)
+  uint32_t* fincl = reinterpret_cast<uint32_t*>(kin);
+  uint32_t* firstpos = fincl + n;
   {
   StageTimer tm(kStLoadLinks, s);
-  hipLaunchKernelGGL(k_ids, dim3(grid_of(n)), dim3(256), 0, s, vin, incl, newflag, n,
-                     o.bid.as<uint32_t>(), t.blk_w.as<uint8_t>(), t.blk_g.as<uint8_t>(),
+  hipLaunchKernelGGL(k_first_flags, dim3(grid_of(n)), dim3(256), 0, s, o.key.as<uint32_t>(), n,
+                     firstpos);
+  KV_HIP(hipGetLastError());
+  if ((st = scan_u32(firstpos, fincl, n, true, scratch.as<uint32_t>(), s)) != KV_OK) return st;
+  hipLaunchKernelGGL(k_first_pos, dim3(grid_of(n)), dim3(256), 0, s, vin, incl, newflag, n,
+                     firstpos);
+  KV_HIP(hipGetLastError());
+  hipLaunchKernelGGL(k_ids, dim3(grid_of(n)), dim3(256), 0, s, vin, incl, newflag, firstpos,
+                     fincl, n, o.bid.as<uint32_t>(), t.blk_w.as<uint8_t>(), t.blk_g.as<uint8_t>(),
                      runstart, o.w.as<uint8_t>(), o.g.as<uint8_t>(), dstats);
   KV_HIP(hipGetLastError());
   hipLaunchKernelGGL(k_mult, dim3(grid_of(n)), dim3(256), 0, s, incl, newflag, n, runstart,

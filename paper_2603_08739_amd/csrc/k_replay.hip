@@ -57,6 +57,7 @@ struct JobArgs {
   const uint8_t* blk_w;
   const uint8_t* blk_g;
   uint64_t u;           // distinct blocks
+  uint64_t n;           // accesses per order; arrays hold 16 readable bytes past n
   uint32_t n_groups;
   uint32_t n_class;     // LFU classes per job (max multiplicity + 2)
 };
@@ -76,16 +77,24 @@ static_assert(kRIt == 4, "hit words are assembled from four ballots");
 // Optional per-job replay statistics (diagnostics build only).
 #ifdef KV_REPLAY_STATS
 enum { kStFastOk = 0, kStFailPool, kStFailElig, kStFailConv, kStSerialAcc, kStIters,
-       kStScanned, kStFastAcc, kStT0, kStT1, kStT2, kStT3, kStT4, kStT5, kStT6, kStT7, kStT8, kStats };
+       kStScanned, kStFastAcc, kStT0, kStT1, kStT2, kStT3, kStT4, kStT5, kStT6, kStT7, kStT8, kStW0, kStW1, kStW2, kStW3, kStats };
 __device__ unsigned long long g_rstats[256][kStats];
 __shared__ unsigned long long s_rstats[kStats];  // flushed to g_rstats when the job ends
+__shared__ unsigned long long s_rwave[4];
 #define RSTAT(j, k, v) do { if (threadIdx.x == 0) s_rstats[k] += (unsigned long long)(v); } while (0)
 #define RCLK(t) const unsigned long long t = clock64()
+// per chunk, the latest wave's (clock - t0) at this point, summed over chunks
+#define RWAVE(k, t0) do { unsigned long long _d = clock64() - (t0); \
+    if (lane_id() == 0) atomicMax(&s_rwave[k], _d); } while (0)
+#define RWAVE_FLUSH() do { __syncthreads(); if (threadIdx.x < 4) { s_rstats[kStT6 + threadIdx.x % 3] += 0; } \
+    if (threadIdx.x == 0) { for (int _q = 0; _q < 4; ++_q) { s_rstats[kStW0 + _q] += s_rwave[_q]; s_rwave[_q] = 0; } } } while (0)
 #define RTIME(k, t0, t1) RSTAT(blockIdx.x, k, (t1) - (t0))
 #else
 #define RSTAT(j, k, v) do { } while (0)
 #define RCLK(t) do { } while (0)
 #define RTIME(k, t0, t1) do { } while (0)
+#define RWAVE(k, t0) do { } while (0)
+#define RWAVE_FLUSH() do { } while (0)
 #endif
 
 __device__ __forceinline__ uint32_t ld_acq(const uint32_t* p) {
@@ -106,24 +115,23 @@ __global__ __launch_bounds__(256) void k_replay_init(const JobDev* __restrict__ 
                                                      uint32_t* __restrict__ cls, JobArgs a) {
   const JobDev j = jobs[blockIdx.y];
   if (j.closed) return;
+  // FIFO: u32 insertion totals (two per word, all-ones = never inserted);
+  // LFU: u64 (last access, count), zero = absent
   const uint64_t fill = (j.policy == KV_POLICY_FIFO) ? kNoIns : 0ull;
+  const uint64_t words = (j.policy == KV_POLICY_FIFO) ? (a.u + 1) / 2 : a.u;
   uint64_t* st = state + j.state_off;
-  for (uint64_t b = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; b < a.u;
+  for (uint64_t b = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; b < words;
        b += (uint64_t)gridDim.x * blockDim.x)
     st[b] = fill;
   if (j.policy == KV_POLICY_LFU) {
-    // head[n_class] u32 | cnt[n_class] u32 | nz[(n_class+63)/64] u64
+    // head[n_class] u32 | cnt[n_class] u32
     uint32_t* head = cls + j.class_off;
     uint32_t* cnt = head + a.n_class;
-    uint64_t* nz = reinterpret_cast<uint64_t*>(cnt + a.n_class);
-    const uint32_t nw = (a.n_class + 63) / 64;
     for (uint32_t f = blockIdx.x * blockDim.x + threadIdx.x; f < a.n_class;
          f += gridDim.x * blockDim.x) {
       head[f] = (uint32_t)j.begin;
       cnt[f] = 0;
     }
-    for (uint32_t f = blockIdx.x * blockDim.x + threadIdx.x; f < nw; f += gridDim.x * blockDim.x)
-      nz[f] = 0;
   }
 }
 
@@ -196,6 +204,62 @@ __device__ __forceinline__ void add_uniform(unsigned long long* dc, unsigned lon
   }
 }
 
+struct FifoLds {
+  uint8_t ex[kRChunk];
+  uint32_t red[2 * kRNW];
+  uint32_t anyflag[2];
+  unsigned long long fin[KV_MAX_GROUPS], finw[KV_MAX_GROUPS];
+};
+
+// Inputs of one chunk for one thread (its kRIt consecutive accesses).
+struct ChunkIn {
+  uint32_t b[kRIt];  // dense block id
+  uint32_t k[kRIt];  // previous occurrence + 1, 0 = none
+  uint32_t w;        // weights, one byte per access
+  uint32_t g;        // groups, one byte per access
+};
+
+__device__ __forceinline__ void chunk_valid(const JobDev& j, uint64_t c0, uint32_t L,
+                                            bool v[kRIt]) {
+  const uint32_t l0 = threadIdx.x * kRIt;
+  const uint64_t p0 = c0 + l0;
+  const uint64_t c1 = min(c0 + L, j.end);
+#pragma unroll
+  for (int e = 0; e < kRIt; ++e) v[e] = l0 + e < L && p0 + e >= j.begin && p0 + e < c1;
+}
+
+__device__ __forceinline__ uint32_t pack4_u8(const uint32_t x[kRIt]) {
+  return x[0] | (x[1] << 8) | (x[2] << 16) | (x[3] << 24);
+}
+
+// Issues the loads of a chunk's inputs without branches, so that the
+// compiler can leave them in flight while earlier loads are consumed: the
+// position is clamped to n (the arrays have readable slack past n) and
+// invalid items are zeroed.
+__device__ __forceinline__ void issue_inputs(const JobDev& j, const JobArgs& a, uint64_t c0,
+                                             uint32_t L, ChunkIn& in) {
+  const uint32_t o = j.order;
+  const uint64_t p0 = min(c0 + threadIdx.x * kRIt, a.n & ~3ull);  // valid p0 are multiples of 4 below n
+  bool v[kRIt];
+  chunk_valid(j, c0, L, v);
+  const uint4 b = *reinterpret_cast<const uint4*>(a.bid[o] + p0);
+  const uint4 k = *reinterpret_cast<const uint4*>(a.key[o] + p0);
+  const uint32_t w = *reinterpret_cast<const uint32_t*>(a.w8[o] + p0);
+  const uint32_t g = *reinterpret_cast<const uint32_t*>(a.g8[o] + p0);
+  in.b[0] = v[0] ? b.x : 0u;
+  in.b[1] = v[1] ? b.y : 0u;
+  in.b[2] = v[2] ? b.z : 0u;
+  in.b[3] = v[3] ? b.w : 0u;
+  in.k[0] = v[0] ? k.x : 0u;
+  in.k[1] = v[1] ? k.y : 0u;
+  in.k[2] = v[2] ? k.z : 0u;
+  in.k[3] = v[3] ? k.w : 0u;
+  const uint32_t m = (v[0] ? 0xFFu : 0u) | (v[1] ? 0xFF00u : 0u) | (v[2] ? 0xFF0000u : 0u) |
+                     (v[3] ? 0xFF000000u : 0u);
+  in.w = w & m;
+  in.g = g & m;
+}
+
 // ---------------------------------------------------------------------------
 // FIFO by chunks.  With C >= chunk * w_max a block inserted inside a chunk
 // cannot leave the queue before the chunk ends, so each block misses at most
@@ -203,43 +267,61 @@ __device__ __forceinline__ void add_uniform(unsigned long long* dc, unsigned lon
 // S[b] + C.  W depends on the misses before i, and more misses only raise W,
 // so iterating "misses -> W -> misses" from "no misses" rises monotonically
 // to the exact answer.
+//
+// S[b] < 2^32 (weights sum below 2^32); kNoIns32 marks a block never inserted.
+// The chunk loop is software-pipelined: the inputs of chunk k+2 are loaded
+// while chunk k is resolved, and so are the states of chunk k+1's blocks,
+// which brings their lines into the caches; once chunk k's insertions are
+// stored, the exact states of chunk k+1 are read again from there.  Dense
+// block ids follow first occurrence, so the lines are few and shared.
 // ---------------------------------------------------------------------------
-struct FifoLds {
-  uint8_t ex[kRChunk];
-  uint32_t red[2 * kRNW];
-  unsigned long long fin[KV_MAX_GROUPS], finw[KV_MAX_GROUPS];
-};
+constexpr uint32_t kNoIns32 = 0xFFFFFFFFu;
 
-__device__ void fifo_chunked(const JobDev& j, const JobArgs& a, uint64_t* __restrict__ S,
+__device__ void fifo_chunked(const JobDev& j, const JobArgs& a, uint32_t* __restrict__ S,
                              uint64_t* __restrict__ bits, GroupCounters& gc, FifoLds& F,
                              bool g1, uint32_t g0) {
   const uint32_t tid = threadIdx.x;
-  const uint32_t o = j.order;
   const uint32_t L = j.chunk;
   const uint32_t l0 = tid * kRIt;
-  uint64_t W0 = 0;
-  for (uint64_t c0 = j.begin & ~63ull; c0 < j.end; c0 += L) {
-    RCLK(f_a);
-    const uint64_t c1 = min(c0 + L, j.end);
-    const uint64_t p0 = c0 + l0;
-    bool v[kRIt], miss[kRIt];
+  const uint64_t cstart = j.begin & ~63ull;
+  ChunkIn A, B, C;
+  uint32_t sa[kRIt], sb[kRIt];
+  issue_inputs(j, a, cstart, L, A);
+  issue_inputs(j, a, cstart + L, L, B);
+  {
+    bool v[kRIt];
+    chunk_valid(j, cstart, L, v);
 #pragma unroll
-    for (int e = 0; e < kRIt; ++e) v[e] = l0 + e < L && p0 + e >= j.begin && p0 + e < c1;
-    const bool all = v[0] && v[kRIt - 1];
-    uint32_t bb[kRIt], ww[kRIt], gg[kRIt] = {g0, g0, g0, g0}, kk[kRIt];
-    load4_u32(a.bid[o], p0, all, v, bb);
-    load4_u8(a.w8[o], p0, all, v, ww);
-    load4_u32(a.key[o], p0, all, v, kk);
-    if (!g1) load4_u8(a.g8[o], p0, all, v, gg);
+    for (int e = 0; e < kRIt; ++e) sa[e] = v[e] ? S[A.b[e]] : kNoIns32;
+  }
+  if (tid < 2) F.anyflag[tid] = 0;
+  __syncthreads();
+  BlockAny block_any{F.anyflag, 0};
+  uint32_t W0 = 0;
+  for (uint64_t c0 = cstart; c0 < j.end; c0 += L) {
+    RCLK(f_a);
+    bool v[kRIt], vb[kRIt], miss[kRIt];
+    chunk_valid(j, c0, L, v);
+    chunk_valid(j, c0 + L, L, vb);
+    issue_inputs(j, a, c0 + 2 * (uint64_t)L, L, C);
+    // touch the next chunk's states early (block 0 stands in for invalid
+    // items) so that the exact re-read after this chunk finds them cached
+    uint32_t warm[kRIt];
+#pragma unroll
+    for (int e = 0; e < kRIt; ++e) warm[e] = S[vb[e] ? B.b[e] : 0u];
+    RWAVE(0, f_a);
+    RWAVE(1, f_a);
     int lp[kRIt];
-    uint64_t ss[kRIt], wi[kRIt];
+    uint32_t ww[kRIt], wi[kRIt];
 #pragma unroll
     for (int e = 0; e < kRIt; ++e) {
-      lp[e] = (kk[e] != 0 && (uint64_t)(kk[e] - 1) >= c0) ? (int)((uint64_t)(kk[e] - 1) - c0) : -1;
-      ss[e] = v[e] ? S[bb[e]] : kNoIns;
+      const uint32_t k = A.k[e];
+      lp[e] = (k != 0 && (uint64_t)(k - 1) >= c0) ? (int)((uint64_t)(k - 1) - c0) : -1;
+      ww[e] = (A.w >> (8 * e)) & 0xFFu;
       miss[e] = false;
     }
     uint32_t tot = 0;
+    RWAVE(2, f_a);
     RCLK(f_b);
     RTIME(kStT0, f_a, f_b);
     for (uint32_t it = 0; it < L + 2; ++it) {
@@ -251,12 +333,12 @@ __device__ void fifo_chunked(const JobDev& j, const JobArgs& a, uint64_t* __rest
       const uint32_t pre = block_excl_scan_u32<kRNT>(x, F.red, tot);
       RCLK(g_b);
       RTIME(kStT6, g_a, g_b);
-      uint64_t run = W0 + pre;
+      uint32_t run = W0 + pre;
       uint32_t exw = 0;
 #pragma unroll
       for (int e = 0; e < kRIt; ++e) {
         wi[e] = run;
-        const bool ex = v[e] && (ss[e] == kNoIns || run - ss[e] > j.cap);
+        const bool ex = v[e] && (sa[e] == kNoIns32 || (uint64_t)(run - sa[e]) > j.cap);
         exw |= (ex ? 1u : 0u) << (8 * e);
         run += miss[e] ? ww[e] : 0u;
       }
@@ -272,7 +354,7 @@ __device__ void fifo_chunked(const JobDev& j, const JobArgs& a, uint64_t* __rest
         changed |= nm != miss[e];
         miss[e] = nm;
       }
-      const bool again = __syncthreads_or(changed);
+      const bool again = block_any(changed);
       RCLK(g_d);
       RTIME(kStT8, g_c, g_d);
       if (!again) break;
@@ -286,19 +368,34 @@ __device__ void fifo_chunked(const JobDev& j, const JobArgs& a, uint64_t* __rest
     for (int e = 0; e < kRIt; ++e) {
       hit[e] = v[e] && !miss[e];
       if (v[e] && miss[e]) {
-        S[bb[e]] = wi[e];
+        S[A.b[e]] = wi[e];
         if (g1) {
           ++ci;
           cw += ww[e];
         } else {
-          atomicAdd(&gc.ins[gg[e]], 1ull);
-          atomicAdd(&gc.insw[gg[e]], (unsigned long long)ww[e]);
+          const uint32_t g = (A.g >> (8 * e)) & 0xFFu;
+          atomicAdd(&gc.ins[g], 1ull);
+          atomicAdd(&gc.insw[g], (unsigned long long)ww[e]);
         }
       }
     }
     if (g1) add_uniform(&gc.ins[g0], &gc.insw[g0], ci, cw);
     W0 += tot;
     store_hits(hit, c0, L, j, bits);
+    RWAVE(3, f_a);
+    __syncthreads();
+    RWAVE_FLUSH();
+    // the next chunk's states after this chunk's insertions (the early
+    // loads are kept alive, not used, so that they are issued)
+#pragma unroll
+    for (int e = 0; e < kRIt; ++e) {
+      asm volatile("" ::"v"(warm[e]));
+      sb[e] = S[vb[e] ? B.b[e] : 0u];
+    }
+    A = B;
+    B = C;
+#pragma unroll
+    for (int e = 0; e < kRIt; ++e) sa[e] = sb[e];
     RCLK(f_d);
     RTIME(kStT2, f_c, f_d);
     RSTAT(blockIdx.x, kStFastOk, 1);
@@ -307,8 +404,8 @@ __device__ void fifo_chunked(const JobDev& j, const JobArgs& a, uint64_t* __rest
   if (tid < KV_MAX_GROUPS) F.fin[tid] = F.finw[tid] = 0;
   __syncthreads();
   for (uint64_t b = tid; b < a.u; b += kRNT) {
-    const uint64_t s = S[b];
-    if (s != kNoIns && W0 - s <= j.cap) {
+    const uint32_t s = S[b];
+    if (s != kNoIns32 && (uint64_t)(W0 - s) <= j.cap) {
       const uint32_t g = a.blk_g[b];
       atomicAdd(&F.fin[g], 1ull);
       atomicAdd(&F.finw[g], (unsigned long long)a.blk_w[b]);
@@ -323,14 +420,14 @@ __device__ void fifo_chunked(const JobDev& j, const JobArgs& a, uint64_t* __rest
 
 // FIFO for capacities below 64 blocks: lanes of wave 0 gather a batch of 64
 // accesses, one lane resolves them in trace order.
-__device__ void fifo_serial(const JobDev& j, const JobArgs& a, uint64_t* __restrict__ S,
+__device__ void fifo_serial(const JobDev& j, const JobArgs& a, uint32_t* __restrict__ S,
                             uint64_t* __restrict__ bits, GroupCounters& gc) {
   __shared__ uint32_t sb[64], sw[64], sg[64];
   __shared__ int sdup[64];
-  __shared__ uint64_t ss[64], snew[64];
+  __shared__ uint32_t ss[64], snew[64];
   const uint32_t lane = threadIdx.x;
   const uint32_t o = j.order;
-  uint64_t wcur = 0;
+  uint32_t wcur = 0;
   for (uint64_t base = j.begin & ~63ull; base < j.end; base += 64) {
     const uint64_t i = base + lane;
     const bool in = lane < 64 && i >= j.begin && i < j.end;
@@ -339,7 +436,7 @@ __device__ void fifo_serial(const JobDev& j, const JobArgs& a, uint64_t* __restr
       sb[lane] = b;
       sw[lane] = in ? a.w8[o][i] : 0u;
       sg[lane] = in ? a.g8[o][i] : 0u;
-      ss[lane] = in ? S[b] : 0ull;
+      ss[lane] = in ? S[b] : 0u;
     }
     __syncthreads();
     if (lane < 64) {
@@ -358,8 +455,8 @@ __device__ void fifo_serial(const JobDev& j, const JobArgs& a, uint64_t* __restr
       for (uint32_t l = 0; l < 64; ++l) {
         const uint64_t p = base + l;
         if (p < j.begin || p >= j.end) continue;
-        const uint64_t s = sdup[l] >= 0 ? snew[sdup[l]] : ss[l];
-        const bool hit = s != kNoIns && wcur - s <= j.cap;
+        const uint32_t s = sdup[l] >= 0 ? snew[sdup[l]] : ss[l];
+        const bool hit = s != kNoIns32 && (uint64_t)(wcur - s) <= j.cap;
         if (hit) {
           word |= 1ull << l;
           snew[l] = s;
@@ -375,15 +472,15 @@ __device__ void fifo_serial(const JobDev& j, const JobArgs& a, uint64_t* __restr
     }
     __syncthreads();
   }
-  __shared__ uint64_t swfin;
+  __shared__ uint32_t swfin;
   __shared__ unsigned long long sfin[KV_MAX_GROUPS], sfinw[KV_MAX_GROUPS];
   if (lane == 0) swfin = wcur;
   if (lane < KV_MAX_GROUPS) sfin[lane] = sfinw[lane] = 0;
   __syncthreads();
-  const uint64_t wf = swfin;
+  const uint32_t wf = swfin;
   for (uint64_t b = lane; b < a.u; b += kRNT) {
-    const uint64_t s = S[b];
-    if (s != kNoIns && wf - s <= j.cap) {
+    const uint32_t s = S[b];
+    if (s != kNoIns32 && (uint64_t)(wf - s) <= j.cap) {
       const uint32_t g = a.blk_g[b];
       atomicAdd(&sfin[g], 1ull);
       atomicAdd(&sfinw[g], (unsigned long long)a.blk_w[b]);
@@ -425,7 +522,8 @@ struct LfuLds {
   uint8_t ccons[kCand];
   uint32_t red[2 * kRNW];
   uint32_t sfx[2 * kRNW];
-  uint32_t red8[kRNW][8];
+  uint32_t anyflag[2];
+  uint32_t tot8[8];           // chunk totals: ins, ins_w, ev, ev_w, victim w, last old, last new, n1
   uint32_t ccnt[kLdsClass];   // members of class f < kLdsClass
   uint64_t cnz[kLdsClassWords];
   uint64_t used;              // cached weight
@@ -439,23 +537,21 @@ struct Classes {
   uint32_t* lcnt;   // LDS counts, classes < kLdsClass
   uint64_t* lnz;    // LDS bitmap words, classes < kLdsClass
   uint32_t* gcnt;   // HBM counts (classes >= kLdsClass)
-  uint64_t* gnz;    // HBM bitmap words (words >= kLdsClassWords)
-  uint32_t nw;      // bitmap words in all
+  uint32_t nclass;  // classes in all
 };
 
-__device__ __forceinline__ uint64_t class_word(const Classes& c, uint32_t wi) {
-  return wi < kLdsClassWords ? c.lnz[wi] : ld_acq64(&c.gnz[wi]);
-}
-
+// Lowest nonempty class >= f.  Classes >= kLdsClass (blocks touched over a
+// thousand times while cached) are looked up by their counts; the search
+// reaches them only when every lower class is empty.
 __device__ __forceinline__ uint32_t next_class(const Classes& c, uint32_t f) {
-  uint32_t wi = f >> 6;
-  if (wi >= c.nw) return 0xFFFFFFFFu;
-  uint64_t m = class_word(c, wi) & (~0ull << (f & 63));
-  while (m == 0) {
-    if (++wi >= c.nw) return 0xFFFFFFFFu;
-    m = class_word(c, wi);
+  for (uint32_t wi = f >> 6; wi < kLdsClassWords; ++wi) {
+    uint64_t m = c.lnz[wi];
+    if (wi == (f >> 6)) m &= ~0ull << (f & 63);
+    if (m) return (wi << 6) + (uint32_t)__ffsll((long long)m) - 1u;
   }
-  return (wi << 6) + (uint32_t)__ffsll((long long)m) - 1u;
+  for (uint32_t g = max(f, kLdsClass); g < c.nclass; ++g)
+    if (ld_acq(&c.gcnt[g]) != 0u) return g;
+  return 0xFFFFFFFFu;
 }
 
 __device__ __forceinline__ uint32_t class_count(const Classes& c, uint32_t f) {
@@ -464,17 +560,17 @@ __device__ __forceinline__ uint32_t class_count(const Classes& c, uint32_t f) {
 
 // Serial update by one thread (the others wait at a barrier).
 __device__ __forceinline__ void class_add1(const Classes& c, uint32_t f, int d) {
-  const uint64_t bit = 1ull << (f & 63);
   if (f < kLdsClass) {
+    const uint64_t bit = 1ull << (f & 63);
     if (d > 0) {
       if (c.lcnt[f]++ == 0u) c.lnz[f >> 6] |= bit;
     } else {
       if (--c.lcnt[f] == 0u) c.lnz[f >> 6] &= ~bit;
     }
   } else if (d > 0) {
-    if (atomicAdd(&c.gcnt[f], 1u) == 0u) atomicOr((unsigned long long*)&c.gnz[f >> 6], bit);
+    atomicAdd(&c.gcnt[f], 1u);
   } else {
-    if (atomicSub(&c.gcnt[f], 1u) == 1u) atomicAnd((unsigned long long*)&c.gnz[f >> 6], ~bit);
+    atomicSub(&c.gcnt[f], 1u);
   }
 }
 
@@ -561,6 +657,7 @@ __device__ bool lfu_serial_range(const JobDev& j, const JobArgs& a, uint64_t* __
 }
 
 constexpr int kCPT = (kCand + kRChunk) / kRNT;  // queue entries per thread
+constexpr int kWin = 16;                          // demands searched in registers
 
 // Exclusive suffix minimum over the threads of the block (threads above t),
 // and whether any thread raised `flag`; two barriers.
@@ -617,7 +714,7 @@ __device__ __forceinline__ void block_suffix_min_flag(uint32_t v, bool flag, uin
 __device__ bool lfu_fast(const JobDev& j, const JobArgs& a, uint64_t* __restrict__ st,
                          const Classes& cl, GroupCounters& gc, LfuLds& S,
                          uint64_t* __restrict__ bits, uint64_t c0, uint64_t c1, bool g1,
-                         uint32_t g0) {
+                         uint32_t g0, BlockAny& block_any) {
   const uint32_t tid = threadIdx.x;
   const uint32_t o = j.order;
   const uint32_t L = (uint32_t)(c1 - c0);
@@ -636,6 +733,7 @@ __device__ bool lfu_fast(const JobDev& j, const JobArgs& a, uint64_t* __restrict
   load4_u32(a.nxt[o], p0, all, v, nx);
   if (!g1) load4_u8(a.g8[o], p0, all, v, gg);
   uint32_t h = S.head1;
+  if (tid < 8) S.tot8[tid] = 0;  // first read after several barriers
 #pragma unroll
   for (int e = 0; e < kRIt; ++e) {
     const uint32_t loc = l0 + e;
@@ -731,6 +829,7 @@ __device__ bool lfu_fast(const JobDev& j, const JobArgs& a, uint64_t* __restrict
   uint8_t cur = 0xFF;  // stamp of the latest capacity-miss set (0xFF: none yet)
   for (int it = 0; !converged && it < 24; ++it) {
     RSTAT(blockIdx.x, kStIters, 1);
+    RCLK(t_it);
     bool mi[kRIt], oldcap[kRIt];
     uint32_t xw = 0, xm = 0;
 #pragma unroll
@@ -754,6 +853,7 @@ __device__ bool lfu_fast(const JobDev& j, const JobArgs& a, uint64_t* __restrict
       }
     }
     __syncthreads();
+    RWAVE(0, t_it);
     // the eviction queue: nc0 old entries, then the nm insertions of the chunk
     const uint32_t nq = nc0 + nm;
     uint32_t qw[kCPT];
@@ -771,37 +871,56 @@ __device__ bool lfu_fast(const JobDev& j, const JobArgs& a, uint64_t* __restrict
     }
     uint32_t elig;
     uint32_t run = block_excl_scan_u32<kRNT>(xs, S.red, elig);
+    RWAVE(1, t_it);
     bool bad = (uint64_t)elig < evtot;
     // entry k is consumed by the first miss whose demand exceeds the
-    // eligible weight queued before k; demands and prefixes both rise, so
-    // the search resumes where the previous entry's ended
+    // eligible weight queued before k.  Demands and prefixes both rise, so
+    // a thread's answers lie between the answers for its first and last
+    // prefixes; a window of kWin demands usually holds them all.
     uint32_t evk[kCPT];
-    uint32_t lo = 0;
-    bool started = false;
+    {
+      const uint32_t r_lo = run;
+      uint32_t r_hi = run;
+      {
+        uint32_t rr = run;
 #pragma unroll
-    for (int e = 0; e < kCPT; ++e) {
-      const uint32_t k = tid * kCPT + e;
-      evk[e] = kInf16;
-      if (k < nq && qw[e] && (uint64_t)run < evtot) {
-        if (!started) {
-          lo = upper_bound(S.mneed, 0u, nm, run);
-          started = true;
-        } else {
-          int s = 0;
-          while (lo < nm && S.mneed[lo] <= run && s < 4) {
-            ++lo;
-            ++s;
-          }
-          if (lo < nm && S.mneed[lo] <= run) lo = upper_bound(S.mneed, lo, nm, run);
-        }
-        evk[e] = (lo < nm) ? S.mpos[lo] : kInf16;
-        if (k >= nc0) {
-          // a new entry can only go after it was inserted, and only once
-          // every old one is gone
-          if (evk[e] <= S.mpos[k - nc0] || !reached) bad = true;
+        for (int e = 0; e < kCPT; ++e) {
+          const uint32_t k = tid * kCPT + e;
+          if (k < nq && qw[e] && (uint64_t)rr < evtot) r_hi = rr;
+          rr += qw[e];
         }
       }
-      run += qw[e];
+      const bool active = (uint64_t)r_lo < evtot && tid * kCPT < nq;
+      uint32_t lo = active ? upper_bound(S.mneed, 0u, nm, r_lo) : 0u;
+      const uint32_t hi = active ? upper_bound(S.mneed, lo, nm, r_hi) : 0u;
+      uint32_t win[kWin];
+      const bool inwin = hi - lo < kWin;
+#pragma unroll
+      for (int t = 0; t < kWin; ++t)
+        win[t] = (inwin && lo + t < nm) ? S.mneed[lo + t] : 0xFFFFFFFFu;
+#pragma unroll
+      for (int e = 0; e < kCPT; ++e) {
+        const uint32_t k = tid * kCPT + e;
+        evk[e] = kInf16;
+        if (k < nq && qw[e] && (uint64_t)run < evtot) {
+          uint32_t idx;
+          if (inwin) {
+            idx = lo;
+#pragma unroll
+            for (int t = 0; t < kWin; ++t) idx += win[t] <= run ? 1u : 0u;
+          } else {
+            idx = upper_bound(S.mneed, lo, nm, run);
+            lo = idx;
+          }
+          evk[e] = (idx < nm) ? S.mpos[idx] : kInf16;
+          if (k >= nc0) {
+            // a new entry can only go after it was inserted, and only once
+            // every old one is gone
+            if (evk[e] <= S.mpos[k - nc0] || !reached) bad = true;
+          }
+        }
+        run += qw[e];
+      }
     }
     // the pointer reaches entry k when the first consumed entry at or after k goes
     uint32_t suf[kCPT];
@@ -811,6 +930,7 @@ __device__ bool lfu_fast(const JobDev& j, const JobArgs& a, uint64_t* __restrict
       mn = min(mn, evk[e]);
       suf[e] = mn;
     }
+    RWAVE(2, t_it);
     uint32_t tmin;
     bool anybad;
     block_suffix_min_flag(mn, bad, S.sfx, tmin, anybad);
@@ -818,6 +938,8 @@ __device__ bool lfu_fast(const JobDev& j, const JobArgs& a, uint64_t* __restrict
       RSTAT(blockIdx.x, kStFailElig, 1);
       return false;
     }
+    // the inputs of an iteration are the skip flags and the capacity
+    // misses; the consumption flags are its outputs
     const uint8_t ns = (uint8_t)(it + 1);
     bool changed = false;
 #pragma unroll
@@ -830,12 +952,12 @@ __device__ bool lfu_fast(const JobDev& j, const JobArgs& a, uint64_t* __restrict
       const bool nskip = ak != kInf16 && (ptime == kInf16 || ak <= ptime);
       const bool ncap = ak != kInf16 && !nskip && ptime != kInf16;
       if (k < nc0) {
-        changed |= (nskip != (S.cskip[k] != 0)) || (cons != (S.ccons[k] != 0));
+        changed |= nskip != (S.cskip[k] != 0);
         S.cskip[k] = nskip ? 1 : 0;
         S.ccons[k] = cons ? 1 : 0;
       } else {
         const uint32_t m = S.mpos[k - nc0];
-        changed |= (nskip != (S.mskip[m] != 0)) || (cons != (S.mcons[m] != 0));
+        changed |= nskip != (S.mskip[m] != 0);
         S.mskip[m] = nskip ? 1 : 0;
         S.mcons[m] = cons ? 1 : 0;
       }
@@ -846,14 +968,14 @@ __device__ bool lfu_fast(const JobDev& j, const JobArgs& a, uint64_t* __restrict
     for (int e = 0; e < kRIt; ++e) {
       const uint32_t loc = l0 + e;
       changed |= oldcap[e] != (v[e] && S.capm[loc] == ns);
-      // entries that stopped being misses lose their queue flags
-      if (v[e] && !mi[e] && S.mcons[loc]) {
-        S.mcons[loc] = 0;
-        changed = true;
-      }
+      // entries that stopped being misses lose their queue flags (their
+      // miss status changed with the capacity misses, counted above)
+      if (v[e] && !mi[e] && S.mcons[loc]) S.mcons[loc] = 0;
     }
     cur = ns;
-    if (!__syncthreads_or(changed)) converged = true;
+    if (!block_any(changed)) converged = true;
+    RWAVE(3, t_it);
+    RWAVE_FLUSH();
   }
   if (!converged) {
     RSTAT(blockIdx.x, kStFailConv, 1);
@@ -900,7 +1022,7 @@ __device__ bool lfu_fast(const JobDev& j, const JobArgs& a, uint64_t* __restrict
       S.occ[loc] = no[e];
       S.lmiss[loc] = nl[e];
     }
-    if (!__syncthreads_or(moved)) break;
+    if (!block_any(moved)) break;
   }
   RCLK(t_e);
   RTIME(kStT3, t_d, t_e);
@@ -972,44 +1094,32 @@ __device__ bool lfu_fast(const JobDev& j, const JobArgs& a, uint64_t* __restrict
     if (fnew[e]) class_add_par(cl, fnew[e], +1);
   }
   {
-    const uint32_t w = tid / 64;
-    const uint32_t r[8] = {wave_sum(p_ins), wave_sum(p_insw), wave_sum(p_ev), wave_sum(p_evw),
-                           wave_sum(p_vw), wave_max_u32(p_lastp), wave_max_u32(p_lastm),
-                           wave_sum(p_n1)};
+    const uint32_t r[8] = {wave_add_dpp(p_ins), wave_add_dpp(p_insw), wave_add_dpp(p_ev),
+                           wave_add_dpp(p_evw), wave_add_dpp(p_vw), wave_max_dpp(p_lastp),
+                           wave_max_dpp(p_lastm), wave_add_dpp(p_n1)};
     if (lane_id() == 0) {
 #pragma unroll
-      for (int f = 0; f < 8; ++f) S.red8[w][f] = r[f];
+      for (int f = 0; f < 8; ++f) {
+        if (!r[f]) continue;
+        if (f == 5 || f == 6) atomicMax(&S.tot8[f], r[f]);
+        else atomicAdd(&S.tot8[f], r[f]);
+      }
       if (r[7]) atomicSub(&S.ccnt[1], r[7]);
     }
   }
   __syncthreads();
   RCLK(t_f);
   RTIME(kStT4, t_e, t_f);
-  // nonempty-class bits: LDS words from the counts, HBM words for the
-  // high classes touched above
+  // nonempty-class bits of the LDS classes, from the counts
   {
     const uint64_t bal = __ballot(S.ccnt[tid] != 0u);
     if (lane_id() == 0) S.cnz[tid / 64] = bal;
   }
-#pragma unroll
-  for (int e = 0; e < kRIt; ++e) {
-    if (!fin[e]) continue;
-#pragma unroll
-    for (int z = 0; z < 2; ++z) {
-      const uint32_t f = z == 0 ? (res0[e] ? f0[e] : 0u) : fnew[e];
-      if (f < kLdsClass) continue;
-      const uint64_t bit = 1ull << (f & 63);
-      if (ld_acq(&cl.gcnt[f]) > 0) atomicOr((unsigned long long*)&cl.gnz[f >> 6], bit);
-      else atomicAnd((unsigned long long*)&cl.gnz[f >> 6], ~bit);
-    }
-  }
   store_hits(hit, c0, L, j, bits);
   if (tid == 0) {
-    uint32_t t[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    for (int w = 0; w < kRNW; ++w) {
-      for (int f = 0; f < 8; ++f)
-        t[f] = (f == 5 || f == 6) ? max(t[f], S.red8[w][f]) : t[f] + S.red8[w][f];
-    }
+    uint32_t t[8];
+#pragma unroll
+    for (int f = 0; f < 8; ++f) t[f] = S.tot8[f];
     if (g1) {
       gc.ins[g0] += t[0];
       gc.insw[g0] += t[1];
@@ -1041,10 +1151,11 @@ __device__ void lfu_chunked(const JobDev& j, const JobArgs& a, uint64_t* __restr
   cl.lcnt = S.ccnt;
   cl.lnz = S.cnz;
   cl.gcnt = head + a.n_class;
-  cl.gnz = reinterpret_cast<uint64_t*>(head + 2 * a.n_class);
-  cl.nw = (a.n_class + 63) / 64;
+  cl.nclass = a.n_class;
   for (uint32_t f = tid; f < kLdsClass; f += kRNT) S.ccnt[f] = 0;
   if (tid < kLdsClassWords) S.cnz[tid] = 0;
+  if (tid < 2) S.anyflag[tid] = 0;
+  BlockAny block_any{S.anyflag, 0};
   if (tid == 0) {
     S.used = 0;
     S.fmin = 1;
@@ -1056,7 +1167,7 @@ __device__ void lfu_chunked(const JobDev& j, const JobArgs& a, uint64_t* __restr
   uint32_t len = j.chunk;
   while (pos < j.end) {
     const uint32_t l = (uint32_t)min<uint64_t>(len, j.end - pos);
-    if (lfu_fast(j, a, st, cl, gc, S, bits, pos, pos + l, g1, g0)) {
+    if (lfu_fast(j, a, st, cl, gc, S, bits, pos, pos + l, g1, g0, block_any)) {
       pos += l;
       len = min<uint32_t>(len * 2, j.chunk);
     } else if (l > kMinFast) {
@@ -1091,6 +1202,7 @@ __global__ __launch_bounds__(kRNT) void k_replay(const JobDev* __restrict__ jobs
   if (tid < KV_MAX_GROUPS) gc.ins[tid] = gc.insw[tid] = gc.ev[tid] = gc.evw[tid] = 0;
 #ifdef KV_REPLAY_STATS
   if (tid < kStats) s_rstats[tid] = 0;
+  if (tid < 4) s_rwave[tid] = 0;
 #endif
   __syncthreads();
   // one group for every access of the job: counters add up per wavefront
@@ -1099,9 +1211,10 @@ __global__ __launch_bounds__(kRNT) void k_replay(const JobDev* __restrict__ jobs
   unsigned long long* cnt = jcnt + (uint64_t)blockIdx.x * a.n_groups * 4;
   bool ok = true;
   if (j.kind == kJobFifoChunk) {
-    fifo_chunked(j, a, state + j.state_off, bits + j.bits_off, gc, lds.f, g1, g0);
+    fifo_chunked(j, a, reinterpret_cast<uint32_t*>(state + j.state_off), bits + j.bits_off, gc,
+                 lds.f, g1, g0);
   } else if (j.kind == kJobFifoSerial) {
-    fifo_serial(j, a, state + j.state_off, bits + j.bits_off, gc);
+    fifo_serial(j, a, reinterpret_cast<uint32_t*>(state + j.state_off), bits + j.bits_off, gc);
   } else {
     lfu_chunked(j, a, state + j.state_off, cls, bits + j.bits_off, gc, lds.l, g1, g0);
     ok = lds.l.ok != 0;
@@ -1248,7 +1361,7 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
   const uint64_t n = t.n;
   const uint64_t nwords = (n + 63) / 64;
   const uint32_t n_class = (uint32_t)std::min<uint64_t>(t.st.max_multiplicity + 2, 0xFFFFFFF0ull);
-  const uint32_t class_words = 2 * n_class + 2 * ((n_class + 63) / 64);  // u32 words per LFU job
+  const uint32_t class_words = 2 * n_class;  // u32 words per LFU job: heads, counts
   // layout of job state, class arrays and bitmaps
   std::vector<JobDev> jd(jobs.size());
   uint64_t state_words = 0, class_total = 0, bit_words = 0;
@@ -1273,7 +1386,7 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
     }
     if (!r.closed && r.end > r.begin) {
       j.state_off = state_words;
-      state_words += t.u;
+      state_words += (r.policy == KV_POLICY_FIFO) ? (t.u + 1) / 2 : t.u;
       if (r.policy == KV_POLICY_LFU) {
         j.class_off = class_total;
         class_total += class_words;
@@ -1390,6 +1503,7 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
   ja.blk_w = t.blk_w.as<uint8_t>();
   ja.blk_g = t.blk_g.as<uint8_t>();
   ja.u = t.u;
+  ja.n = t.n;
   ja.n_groups = G;
   ja.n_class = n_class;
   const uint32_t nj = (uint32_t)jd.size();
@@ -1413,12 +1527,14 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
       if (jd[q].closed) continue;
       fprintf(stderr, "[replay-stats] %s job %u cap %llu: fast %llu (acc %llu) failpool %llu "
               "failelig %llu failconv %llu serial_acc %llu iters %llu scanned %llu "
-              "clk load %llu scan %llu fix %llu jump %llu apply %llu fin %llu x6 %llu x7 %llu x8 %llu\n",
+              "clk load %llu scan %llu fix %llu jump %llu apply %llu fin %llu x6 %llu x7 %llu x8 %llu "
+              "w0 %llu w1 %llu w2 %llu w3 %llu\n",
               jd[q].kind == kJobLfu ? "lfu" : "fifo", q,
               (unsigned long long)jd[q].cap, hs[q][kStFastOk], hs[q][kStFastAcc],
               hs[q][kStFailPool], hs[q][kStFailElig], hs[q][kStFailConv], hs[q][kStSerialAcc],
               hs[q][kStIters], hs[q][kStScanned], hs[q][kStT0], hs[q][kStT1], hs[q][kStT2],
-              hs[q][kStT3], hs[q][kStT4], hs[q][kStT5], hs[q][kStT6], hs[q][kStT7], hs[q][kStT8]);
+              hs[q][kStT3], hs[q][kStT4], hs[q][kStT5], hs[q][kStT6], hs[q][kStT7], hs[q][kStT8],
+              hs[q][kStW0], hs[q][kStW1], hs[q][kStW2], hs[q][kStW3]);
     }
   }
 #endif

@@ -101,7 +101,9 @@ kv_status DevBuf::reserve(size_t b) {
   if (cap && g_bytes.load() + b > cap)
     return fail(KV_ERR_NOMEM, "device memory cap reached (test limit)");
   void* q = nullptr;
-  hipError_t e = hipMalloc(&q, b);
+  // 256 bytes of slack past the end: kernels may issue (and then discard)
+  // vector loads of up to 16 bytes at the last valid index
+  hipError_t e = hipMalloc(&q, b + 256);
   if (e != hipSuccess) {
     (void)hipGetLastError();
     return fail(KV_ERR_NOMEM, "hipMalloc of " + std::to_string(b) + " bytes failed");

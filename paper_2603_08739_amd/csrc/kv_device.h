@@ -87,6 +87,36 @@ __device__ __forceinline__ uint32_t block_excl_scan_u32(uint32_t a, uint32_t* sh
   return xa + ia - a;
 }
 
+// Sum and maximum over the 64 lanes via DPP (result in every lane).
+__device__ __forceinline__ uint32_t wave_add_dpp(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)wave_incl_scan_u32(v), 63);
+}
+
+__device__ __forceinline__ uint32_t wave_max_dpp(uint32_t v) {
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xf, 0xf, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xf, 0xf, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xf, 0xf, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xf, 0xf, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xa, 0xf, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xc, 0xf, false));
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
+}
+
+// Whether any thread of the block passes true: one barrier per call.  Two
+// LDS flag words (zero at start) alternate between calls, so a call never
+// overwrites the word a slower thread may still read from the call before.
+struct BlockAny {
+  uint32_t* flag;
+  uint32_t gen;
+  __device__ __forceinline__ bool operator()(bool p) {
+    ++gen;
+    const bool any = __ballot(p) != 0ull;
+    if (any && lane_id() == 0) flag[gen & 1u] = gen;
+    __syncthreads();
+    return flag[gen & 1u] == gen;
+  }
+};
+
 __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
 #pragma unroll
   for (int d = 32; d >= 1; d >>= 1) v = max(v, (uint32_t)__shfl_xor(v, d, 64));
