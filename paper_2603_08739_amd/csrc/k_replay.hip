@@ -277,9 +277,10 @@ __device__ __forceinline__ void issue_inputs(const JobDev& j, const JobArgs& a, 
 // ---------------------------------------------------------------------------
 constexpr uint32_t kNoIns32 = 0xFFFFFFFFu;
 
-__device__ void fifo_chunked(const JobDev& j, const JobArgs& a, uint32_t* __restrict__ S,
-                             uint64_t* __restrict__ bits, GroupCounters& gc, FifoLds& F,
-                             bool g1, uint32_t g0) {
+__device__ __forceinline__ void fifo_chunked(const JobDev& j, const JobArgs& a,
+                                             uint32_t* __restrict__ S,
+                                             uint64_t* __restrict__ bits, GroupCounters& gc,
+                                             FifoLds& F, bool g1, uint32_t g0) {
   const uint32_t tid = threadIdx.x;
   const uint32_t L = j.chunk;
   const uint32_t l0 = tid * kRIt;
@@ -420,8 +421,9 @@ __device__ void fifo_chunked(const JobDev& j, const JobArgs& a, uint32_t* __rest
 
 // FIFO for capacities below 64 blocks: lanes of wave 0 gather a batch of 64
 // accesses, one lane resolves them in trace order.
-__device__ void fifo_serial(const JobDev& j, const JobArgs& a, uint32_t* __restrict__ S,
-                            uint64_t* __restrict__ bits, GroupCounters& gc) {
+__device__ __forceinline__ void fifo_serial(const JobDev& j, const JobArgs& a,
+                                            uint32_t* __restrict__ S, uint64_t* __restrict__ bits,
+                                            GroupCounters& gc) {
   __shared__ uint32_t sb[64], sw[64], sg[64];
   __shared__ int sdup[64];
   __shared__ uint32_t ss[64], snew[64];
@@ -585,10 +587,11 @@ __device__ __forceinline__ void class_add_par(const Classes& c, uint32_t f, int 
 
 // Exact replay of [p0, p1) by one thread (thread 0); returns false if the
 // state is found inconsistent.
-__device__ bool lfu_serial_range(const JobDev& j, const JobArgs& a, uint64_t* __restrict__ st,
-                                 uint32_t* head, const Classes& cl, LfuLds& S,
-                                 GroupCounters& gc, uint64_t* __restrict__ bits, uint64_t p0,
-                                 uint64_t p1) {
+__device__ __forceinline__ bool lfu_serial_range(const JobDev& j, const JobArgs& a,
+                                                 uint64_t* __restrict__ st, uint32_t* head,
+                                                 const Classes& cl, LfuLds& S, GroupCounters& gc,
+                                                 uint64_t* __restrict__ bits, uint64_t p0,
+                                                 uint64_t p1) {
   const uint32_t o = j.order;
   const uint32_t* __restrict__ bid = a.bid[o];
   head[1] = S.head1;
@@ -711,10 +714,11 @@ __device__ __forceinline__ void block_suffix_min_flag(uint32_t v, bool flag, uin
 // by a miss at that position and not touched since, and every such block is
 // still a member (count-1 members only leave by a touch or, oldest first, by
 // eviction, which moves head1 past them).
-__device__ bool lfu_fast(const JobDev& j, const JobArgs& a, uint64_t* __restrict__ st,
-                         const Classes& cl, GroupCounters& gc, LfuLds& S,
-                         uint64_t* __restrict__ bits, uint64_t c0, uint64_t c1, bool g1,
-                         uint32_t g0, BlockAny& block_any) {
+__device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
+                                         uint64_t* __restrict__ st, const Classes& cl,
+                                         GroupCounters& gc, LfuLds& S,
+                                         uint64_t* __restrict__ bits, uint64_t c0, uint64_t c1,
+                                         bool g1, uint32_t g0, BlockAny& block_any) {
   const uint32_t tid = threadIdx.x;
   const uint32_t o = j.order;
   const uint32_t L = (uint32_t)(c1 - c0);
@@ -1142,9 +1146,10 @@ __device__ bool lfu_fast(const JobDev& j, const JobArgs& a, uint64_t* __restrict
   return true;
 }
 
-__device__ void lfu_chunked(const JobDev& j, const JobArgs& a, uint64_t* __restrict__ st,
-                            uint32_t* __restrict__ cls, uint64_t* __restrict__ bits,
-                            GroupCounters& gc, LfuLds& S, bool g1, uint32_t g0) {
+__device__ __forceinline__ void lfu_chunked(const JobDev& j, const JobArgs& a,
+                                            uint64_t* __restrict__ st, uint32_t* __restrict__ cls,
+                                            uint64_t* __restrict__ bits, GroupCounters& gc,
+                                            LfuLds& S, bool g1, uint32_t g0) {
   const uint32_t tid = threadIdx.x;
   uint32_t* head = cls + j.class_off;
   Classes cl;
@@ -1189,15 +1194,26 @@ union ReplayLds {
   LfuLds l;
 };
 
-__global__ __launch_bounds__(kRNT) void k_replay(const JobDev* __restrict__ jobs, JobArgs a,
+__global__ __launch_bounds__(kRNT) void k_replay(const JobDev* __restrict__ jobs, JobArgs a_in,
                                                  uint64_t* __restrict__ state,
                                                  uint32_t* __restrict__ cls,
                                                  uint64_t* __restrict__ bits,
                                                  unsigned long long* __restrict__ jcnt) {
   __shared__ ReplayLds lds;
   __shared__ GroupCounters gc;
-  const JobDev j = jobs[blockIdx.x];
+  JobDev j = jobs[blockIdx.x];
   if (j.closed) return;
+  // the job's access order in slot 0, so that every pointer is known
+  // without indexing (kept in registers)
+  JobArgs a = a_in;
+  if (j.order) {
+    a.bid[0] = a_in.bid[1];
+    a.key[0] = a_in.key[1];
+    a.nxt[0] = a_in.nxt[1];
+    a.w8[0] = a_in.w8[1];
+    a.g8[0] = a_in.g8[1];
+  }
+  j.order = 0;
   const uint32_t tid = threadIdx.x;
   if (tid < KV_MAX_GROUPS) gc.ins[tid] = gc.insw[tid] = gc.ev[tid] = gc.evw[tid] = 0;
 #ifdef KV_REPLAY_STATS
