@@ -24,6 +24,7 @@
 #include <cstdio>
 #include <cstring>
 #include <map>
+#include <mutex>
 #include <optional>
 #include <tuple>
 
@@ -70,7 +71,8 @@ constexpr uint32_t kCand = 4096;           // LFU eviction candidates per chunk
 constexpr int kCScan = 2;                  // candidate positions per thread and pass
 constexpr uint32_t kMinFast = 256;         // shorter LFU chunks go serial
 constexpr uint16_t kInf16 = 0xFFFF;
-constexpr uint32_t kLdsClass = kRNT;       // LFU count classes held in LDS
+constexpr int kLfuNT = 512;                // threads of an LFU replay workgroup
+constexpr uint32_t kLdsClass = 1024;       // LFU count classes held in LDS
 constexpr uint32_t kLdsClassWords = kLdsClass / 64;
 static_assert(kRIt == 4, "hit words are assembled from four ballots");
 
@@ -188,6 +190,67 @@ __device__ __forceinline__ void store_hits(const bool hit[kRIt], uint64_t c0, ui
 #pragma unroll
     for (int e = 0; e < kRIt; ++e) word |= spread4(bal[e] >> (16 * q)) << e;
     const uint32_t wloc = (threadIdx.x / 64) * 4 + q;
+    const uint64_t base = c0 + (uint64_t)wloc * 64;
+    if (wloc * 64 < L && base < j.end && base + 64 > j.begin) bits[(base >> 6) - j.word0] = word;
+  }
+}
+
+// IT consecutive accesses [p0, p0 + IT) of a thread (p0 a multiple of IT):
+// vector loads when all are valid.
+template <int IT>
+__device__ __forceinline__ void loadn_u32(const uint32_t* __restrict__ a, uint64_t p0, bool all,
+                                          const bool* v, uint32_t* out) {
+  if (all) {
+#pragma unroll
+    for (int q = 0; q < IT / 4; ++q) {
+      const uint4 x = *reinterpret_cast<const uint4*>(a + p0 + 4 * q);
+      out[4 * q] = x.x;
+      out[4 * q + 1] = x.y;
+      out[4 * q + 2] = x.z;
+      out[4 * q + 3] = x.w;
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < IT; ++e) out[e] = v[e] ? a[p0 + e] : 0u;
+  }
+}
+
+template <int IT>
+__device__ __forceinline__ void loadn_u8(const uint8_t* __restrict__ a, uint64_t p0, bool all,
+                                         const bool* v, uint32_t* out) {
+  if (all) {
+#pragma unroll
+    for (int q = 0; q < IT / 4; ++q) {
+      const uint32_t x = *reinterpret_cast<const uint32_t*>(a + p0 + 4 * q);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) out[4 * q + e] = (x >> (8 * e)) & 0xFFu;
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < IT; ++e) out[e] = v[e] ? (uint32_t)a[p0 + e] : 0u;
+  }
+}
+
+// Hit words of a chunk starting at c0 (a multiple of 64) when thread t holds
+// positions IT*t .. IT*t+IT-1: the 64/IT lanes of word q are lanes
+// q*64/IT.., and bit m*IT+e of the word is item e of its lane m.
+template <int IT>
+__device__ __forceinline__ void store_hits_n(const bool* hit, uint64_t c0, uint32_t L,
+                                             const JobDev& j, uint64_t* __restrict__ bits) {
+  constexpr int LPW = 64 / IT;  // lanes per word
+  uint64_t bal[IT];
+#pragma unroll
+  for (int e = 0; e < IT; ++e) bal[e] = __ballot(hit[e]);
+  const uint32_t q = lane_id();
+  if (q < (uint32_t)IT) {
+    uint64_t word = 0;
+#pragma unroll
+    for (int e = 0; e < IT; ++e) {
+      const uint64_t part = bal[e] >> (LPW * q);
+#pragma unroll
+      for (int m = 0; m < LPW; ++m) word |= ((part >> m) & 1ull) << (m * IT + e);
+    }
+    const uint32_t wloc = (threadIdx.x / 64) * IT + q;
     const uint64_t base = c0 + (uint64_t)wloc * 64;
     if (wloc * 64 < L && base < j.end && base + 64 > j.begin) bits[(base >> 6) - j.word0] = word;
   }
@@ -659,13 +722,14 @@ __device__ __forceinline__ bool lfu_serial_range(const JobDev& j, const JobArgs&
   return ok;
 }
 
-constexpr int kCPT = (kCand + kRChunk) / kRNT;  // queue entries per thread
 constexpr int kWin = 16;                          // demands searched in registers
 
 // Exclusive suffix minimum over the threads of the block (threads above t),
 // and whether any thread raised `flag`; two barriers.
+template <int NT>
 __device__ __forceinline__ void block_suffix_min_flag(uint32_t v, bool flag, uint32_t* sh,
                                                       uint32_t& smin, bool& any) {
+  constexpr int NW = NT / 64;
   const uint32_t lane = lane_id();
   const int w = threadIdx.x / 64;
   uint32_t x = v;
@@ -678,16 +742,16 @@ __device__ __forceinline__ void block_suffix_min_flag(uint32_t v, bool flag, uin
   const bool wflag = __ballot(flag) != 0ull;
   if (lane == 0) {
     sh[w] = x;
-    sh[kRNW + w] = wflag ? 1u : 0u;
+    sh[NW + w] = wflag ? 1u : 0u;
   }
   __syncthreads();
   uint32_t r = (lane < 63) ? above : 0xFFFFFFFFu;
   uint32_t f = 0;
 #pragma unroll
-  for (int ww = 0; ww < kRNW; ++ww) {
+  for (int ww = 0; ww < NW; ++ww) {
     const uint32_t y = sh[ww];
     r = (ww > w) ? min(r, y) : r;
-    f |= sh[kRNW + ww];
+    f |= sh[NW + ww];
   }
   __syncthreads();
   smin = r;
@@ -714,38 +778,55 @@ __device__ __forceinline__ void block_suffix_min_flag(uint32_t v, bool flag, uin
 // by a miss at that position and not touched since, and every such block is
 // still a member (count-1 members only leave by a touch or, oldest first, by
 // eviction, which moves head1 past them).
+template <int NT>
 __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
                                          uint64_t* __restrict__ st, const Classes& cl,
                                          GroupCounters& gc, LfuLds& S,
                                          uint64_t* __restrict__ bits, uint64_t c0, uint64_t c1,
-                                         bool g1, uint32_t g0, BlockAny& block_any) {
+                                         bool g1, uint32_t g0, BlockAny& block_any,
+                                         bool have_pref, const uint32_t* pb, const uint32_t* pf,
+                                         uint32_t* nb, uint32_t* nf) {
+  constexpr int IT = kRChunk / NT;               // accesses per thread
+  constexpr int CPT = (kCand + kRChunk) / NT;    // queue entries per thread
   const uint32_t tid = threadIdx.x;
   const uint32_t o = j.order;
   const uint32_t L = (uint32_t)(c1 - c0);
-  const uint32_t l0 = tid * kRIt;
+  const uint32_t l0 = tid * IT;
   const uint64_t p0 = c0 + l0;
   RCLK(t_a);
-  bool v[kRIt];
+  bool v[IT];
 #pragma unroll
-  for (int e = 0; e < kRIt; ++e) v[e] = l0 + e < L && p0 + e >= j.begin;
-  const bool all = v[0] && v[kRIt - 1];
-  uint32_t bb[kRIt], ww[kRIt], gg[kRIt] = {g0, g0, g0, g0}, kk[kRIt], nx[kRIt], f0[kRIt];
-  bool cm[kRIt], res0[kRIt];
-  load4_u32(a.bid[o], p0, all, v, bb);
-  load4_u8(a.w8[o], p0, all, v, ww);
-  load4_u32(a.key[o], p0, all, v, kk);
-  load4_u32(a.nxt[o], p0, all, v, nx);
-  if (!g1) load4_u8(a.g8[o], p0, all, v, gg);
+  for (int e = 0; e < IT; ++e) v[e] = l0 + e < L && p0 + e >= j.begin;
+  const bool all = v[0] && v[IT - 1];
+  uint32_t bb[IT], ww[IT], gg[IT], kk[IT], nx[IT], f0[IT];
+  bool cm[IT], res0[IT];
+  if (have_pref) {
+#pragma unroll
+    for (int e = 0; e < IT; ++e) bb[e] = pb[e];
+  } else {
+    loadn_u32<IT>(a.bid[o], p0, all, v, bb);
+  }
+  loadn_u8<IT>(a.w8[o], p0, all, v, ww);
+  loadn_u32<IT>(a.key[o], p0, all, v, kk);
+  loadn_u32<IT>(a.nxt[o], p0, all, v, nx);
+#pragma unroll
+  for (int e = 0; e < IT; ++e) gg[e] = g0;
+  if (!g1) loadn_u8<IT>(a.g8[o], p0, all, v, gg);
   uint32_t h = S.head1;
   if (tid < 8) S.tot8[tid] = 0;  // first read after several barriers
+  // in-cache counts (the low words of the states); prefetched by the
+  // previous chunk when it covered the whole chunk before this one
+  const uint32_t* st32 = reinterpret_cast<const uint32_t*>(st);
+  uint32_t s0[IT];
 #pragma unroll
-  for (int e = 0; e < kRIt; ++e) {
+  for (int e = 0; e < IT; ++e) s0[e] = have_pref ? pf[e] : (v[e] ? st32[2 * (uint64_t)bb[e]] : 0u);
+#pragma unroll
+  for (int e = 0; e < IT; ++e) {
     const uint32_t loc = l0 + e;
     const int lp = (kk[e] != 0 && (uint64_t)(kk[e] - 1) >= c0) ? (int)((uint64_t)(kk[e] - 1) - c0)
                                                                : -1;
     const bool again = v[e] && nx[e] != kNone && (uint64_t)nx[e] < c1;
-    const uint64_t s = v[e] ? st[bb[e]] : 0ull;
-    f0[e] = (uint32_t)s;
+    f0[e] = v[e] ? s0[e] : 0u;
     res0[e] = f0[e] != 0;
     cm[e] = v[e] && lp < 0 && !res0[e];
     S.lp[loc] = (int16_t)lp;
@@ -756,15 +837,49 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     S.mskip[loc] = again ? 1 : 0;
     S.mcons[loc] = 0;
   }
-  uint32_t x = 0;
+  // the first-touch misses: the fixed point's first miss list
+  uint32_t x = 0, xc = 0;
 #pragma unroll
-  for (int e = 0; e < kRIt; ++e) x += cm[e] ? ww[e] : 0u;
-  uint32_t itot0;
-  block_excl_scan_u32<kRNT>(x, S.red, itot0);
+  for (int e = 0; e < IT; ++e) {
+    x += cm[e] ? ww[e] : 0u;
+    xc += cm[e] ? 1u : 0u;
+  }
+  uint32_t itot0, nm0, wpre0, mpre0;
+  block_excl_scan2_u32<NT>(x, xc, S.red, wpre0, mpre0, itot0, nm0);
   const uint64_t used0 = S.used;
   const uint64_t ev0 = (used0 + itot0 > j.cap) ? used0 + itot0 - j.cap : 0ull;
+  if (ev0 > 0) {
+#pragma unroll
+    for (int e = 0; e < IT; ++e) {
+      if (cm[e]) {
+        wpre0 += ww[e];
+        const int64_t need = (int64_t)(used0 + wpre0) - (int64_t)j.cap;
+        S.mpos[mpre0] = (uint16_t)(l0 + e);
+        S.mneed[mpre0] = need > 0 ? (uint32_t)need : 0u;
+        ++mpre0;
+      }
+    }
+  }
   RCLK(t_b);
   RTIME(kStT0, t_a, t_b);
+  {
+    // the next full chunk's blocks.  The read position is clamped to the
+    // arrays' readable slack; whatever lies outside the job (or past n, where
+    // the slack holds no block ids) becomes block 0, a valid index for the
+    // state gather below.
+    const uint64_t pnext = c0 + kRChunk + l0;
+    const uint64_t pn = min<uint64_t>(pnext, a.n & ~3ull);
+#pragma unroll
+    for (int q = 0; q < IT / 4; ++q) {
+      const uint4 x = *reinterpret_cast<const uint4*>(a.bid[o] + pn + 4 * q);
+      const uint32_t xv[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const uint64_t pe = pnext + 4 * q + r;
+        nb[4 * q + r] = (pn == pnext && pe >= j.begin && pe < j.end) ? xv[r] : 0u;
+      }
+    }
+  }
   uint32_t nc0 = 0;
   bool reached = false;
   if (ev0 > 0) {
@@ -774,7 +889,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     uint32_t n0 = 0;
     uint64_t vw = 0;
     for (;;) {
-      if (vw >= ev0 || (uint64_t)h >= c0 || n0 + kRNT * kCScan > kCand) break;
+      if (vw >= ev0 || (uint64_t)h >= c0 || n0 + NT * kCScan > kCand) break;
       RSTAT(blockIdx.x, kStScanned, 1);
       bool live[kCScan], touched[kCScan];
       uint32_t bq[kCScan], wq[kCScan], aq[kCScan];
@@ -803,7 +918,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
         cw_ += (live[e] && !touched[e]) ? wq[e] : 0u;
       }
       uint32_t pos, dummy, cnt_live, vsum;
-      block_excl_scan2_u32<kRNT>(cl_, cw_, S.red, pos, dummy, cnt_live, vsum);
+      block_excl_scan2_u32<NT>(cl_, cw_, S.red, pos, dummy, cnt_live, vsum);
 #pragma unroll
       for (int e = 0; e < kCScan; ++e) {
         if (!live[e]) continue;
@@ -817,7 +932,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       }
       n0 += cnt_live;
       vw += vsum;
-      h = (uint32_t)min<uint64_t>((uint64_t)h + kRNT * kCScan, c0);
+      h = (uint32_t)min<uint64_t>((uint64_t)h + NT * kCScan, c0);
     }
     __syncthreads();
     nc0 = n0;
@@ -834,37 +949,47 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   for (int it = 0; !converged && it < 24; ++it) {
     RSTAT(blockIdx.x, kStIters, 1);
     RCLK(t_it);
-    bool mi[kRIt], oldcap[kRIt];
-    uint32_t xw = 0, xm = 0;
+    bool mi[IT], oldcap[IT];
+    uint32_t nm = nm0;
 #pragma unroll
-    for (int e = 0; e < kRIt; ++e) {
-      oldcap[e] = v[e] && S.capm[l0 + e] == cur;
-      mi[e] = cm[e] || oldcap[e];
-      xw += mi[e] ? ww[e] : 0u;
-      xm += mi[e] ? 1u : 0u;
+    for (int e = 0; e < IT; ++e) {
+      oldcap[e] = false;
+      mi[e] = cm[e];
     }
-    uint32_t wpre, mpre, nm;
-    block_excl_scan2_u32<kRNT>(xw, xm, S.red, wpre, mpre, itot, nm);
-    const uint64_t evtot = (used0 + itot > j.cap) ? used0 + itot - j.cap : 0ull;
+    if (it > 0) {  // the first miss list is the first touches, listed above
+      uint32_t xw = 0, xm = 0;
 #pragma unroll
-    for (int e = 0; e < kRIt; ++e) {
-      if (mi[e]) {
-        wpre += ww[e];
-        const int64_t need = (int64_t)(used0 + wpre) - (int64_t)j.cap;
-        S.mpos[mpre] = (uint16_t)(l0 + e);
-        S.mneed[mpre] = need > 0 ? (uint32_t)need : 0u;
-        ++mpre;
+      for (int e = 0; e < IT; ++e) {
+        oldcap[e] = v[e] && S.capm[l0 + e] == cur;
+        mi[e] = cm[e] || oldcap[e];
+        xw += mi[e] ? ww[e] : 0u;
+        xm += mi[e] ? 1u : 0u;
       }
+      uint32_t wpre, mpre;
+      block_excl_scan2_u32<NT>(xw, xm, S.red, wpre, mpre, itot, nm);
+#pragma unroll
+      for (int e = 0; e < IT; ++e) {
+        if (mi[e]) {
+          wpre += ww[e];
+          const int64_t need = (int64_t)(used0 + wpre) - (int64_t)j.cap;
+          S.mpos[mpre] = (uint16_t)(l0 + e);
+          S.mneed[mpre] = need > 0 ? (uint32_t)need : 0u;
+          ++mpre;
+        }
+      }
+      __syncthreads();
     }
-    __syncthreads();
+    const uint64_t evtot = (used0 + itot > j.cap) ? used0 + itot - j.cap : 0ull;
     RWAVE(0, t_it);
-    // the eviction queue: nc0 old entries, then the nm insertions of the chunk
+    // the eviction queue: nc0 old entries, then the nm insertions of the
+    // chunk; thread t holds entries t*qpt .. t*qpt+qpt-1
     const uint32_t nq = nc0 + nm;
-    uint32_t qw[kCPT];
+    const uint32_t qpt = (nq + NT - 1) / NT;
+    uint32_t qw[CPT];
     uint32_t xs = 0;
 #pragma unroll
-    for (int e = 0; e < kCPT; ++e) {
-      const uint32_t k = tid * kCPT + e;
+    for (int e = 0; e < CPT; ++e) {
+      const uint32_t k = (uint32_t)e < qpt ? tid * qpt + e : nq;
       qw[e] = 0;
       if (k < nc0) qw[e] = S.cskip[k] ? 0u : S.cw[k];
       else if (k < nq) {
@@ -874,27 +999,27 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       xs += qw[e];
     }
     uint32_t elig;
-    uint32_t run = block_excl_scan_u32<kRNT>(xs, S.red, elig);
+    uint32_t run = block_excl_scan_u32<NT>(xs, S.red, elig);
     RWAVE(1, t_it);
     bool bad = (uint64_t)elig < evtot;
     // entry k is consumed by the first miss whose demand exceeds the
     // eligible weight queued before k.  Demands and prefixes both rise, so
     // a thread's answers lie between the answers for its first and last
     // prefixes; a window of kWin demands usually holds them all.
-    uint32_t evk[kCPT];
+    uint32_t evk[CPT];
     {
       const uint32_t r_lo = run;
       uint32_t r_hi = run;
       {
         uint32_t rr = run;
 #pragma unroll
-        for (int e = 0; e < kCPT; ++e) {
-          const uint32_t k = tid * kCPT + e;
+        for (int e = 0; e < CPT; ++e) {
+          const uint32_t k = (uint32_t)e < qpt ? tid * qpt + e : nq;
           if (k < nq && qw[e] && (uint64_t)rr < evtot) r_hi = rr;
           rr += qw[e];
         }
       }
-      const bool active = (uint64_t)r_lo < evtot && tid * kCPT < nq;
+      const bool active = (uint64_t)r_lo < evtot && tid * qpt < nq;
       uint32_t lo = active ? upper_bound(S.mneed, 0u, nm, r_lo) : 0u;
       const uint32_t hi = active ? upper_bound(S.mneed, lo, nm, r_hi) : 0u;
       uint32_t win[kWin];
@@ -903,8 +1028,8 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       for (int t = 0; t < kWin; ++t)
         win[t] = (inwin && lo + t < nm) ? S.mneed[lo + t] : 0xFFFFFFFFu;
 #pragma unroll
-      for (int e = 0; e < kCPT; ++e) {
-        const uint32_t k = tid * kCPT + e;
+      for (int e = 0; e < CPT; ++e) {
+        const uint32_t k = (uint32_t)e < qpt ? tid * qpt + e : nq;
         evk[e] = kInf16;
         if (k < nq && qw[e] && (uint64_t)run < evtot) {
           uint32_t idx;
@@ -927,17 +1052,17 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       }
     }
     // the pointer reaches entry k when the first consumed entry at or after k goes
-    uint32_t suf[kCPT];
+    uint32_t suf[CPT];
     uint32_t mn = kInf16;
 #pragma unroll
-    for (int e = kCPT - 1; e >= 0; --e) {
+    for (int e = CPT - 1; e >= 0; --e) {
       mn = min(mn, evk[e]);
       suf[e] = mn;
     }
     RWAVE(2, t_it);
     uint32_t tmin;
     bool anybad;
-    block_suffix_min_flag(mn, bad, S.sfx, tmin, anybad);
+    block_suffix_min_flag<NT>(mn, bad, S.sfx, tmin, anybad);
     if (anybad) {
       RSTAT(blockIdx.x, kStFailElig, 1);
       return false;
@@ -947,8 +1072,8 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     const uint8_t ns = (uint8_t)(it + 1);
     bool changed = false;
 #pragma unroll
-    for (int e = 0; e < kCPT; ++e) {
-      const uint32_t k = tid * kCPT + e;
+    for (int e = 0; e < CPT; ++e) {
+      const uint32_t k = (uint32_t)e < qpt ? tid * qpt + e : nq;
       if (k >= nq) continue;
       const uint32_t ptime = min(suf[e], tmin);
       const bool cons = evk[e] != kInf16;
@@ -969,7 +1094,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     }
     __syncthreads();
 #pragma unroll
-    for (int e = 0; e < kRIt; ++e) {
+    for (int e = 0; e < IT; ++e) {
       const uint32_t loc = l0 + e;
       changed |= oldcap[e] != (v[e] && S.capm[loc] == ns);
       // entries that stopped being misses lose their queue flags (their
@@ -989,20 +1114,20 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   RTIME(kStT2, t_c, t_d);
   // ---- consistent: apply.  Pointer jumping gives each touch the number of
   // earlier touches of its block in the chunk and the latest miss among them.
-  bool miss[kRIt];
+  bool miss[IT];
 #pragma unroll
-  for (int e = 0; e < kRIt; ++e) {
+  for (int e = 0; e < IT; ++e) {
     const uint32_t loc = l0 + e;
     miss[e] = cm[e] || (v[e] && S.capm[loc] == cur);
     S.lmiss[loc] = miss[e] ? (int16_t)loc : (int16_t)-1;
   }
   __syncthreads();
   for (;;) {
-    int16_t np[kRIt], nl[kRIt];
-    uint16_t no[kRIt];
+    int16_t np[IT], nl[IT];
+    uint16_t no[IT];
     bool moved = false;
 #pragma unroll
-    for (int e = 0; e < kRIt; ++e) {
+    for (int e = 0; e < IT; ++e) {
       const uint32_t loc = l0 + e;
       const int16_t p = S.lp[loc];
       no[e] = S.occ[loc];
@@ -1020,7 +1145,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     }
     __syncthreads();
 #pragma unroll
-    for (int e = 0; e < kRIt; ++e) {
+    for (int e = 0; e < IT; ++e) {
       const uint32_t loc = l0 + e;
       S.lp[loc] = np[e];
       S.occ[loc] = no[e];
@@ -1034,7 +1159,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   uint32_t p_ins = 0, p_insw = 0, p_ev = 0, p_evw = 0, p_vw = 0, p_lastp = 0, p_lastm = 0,
            p_n1 = 0;
   // old entries evicted
-  for (uint32_t k = tid; k < nc0; k += kRNT) {
+  for (uint32_t k = tid; k < nc0; k += NT) {
     if (!S.ccons[k]) continue;
     const uint32_t b = S.cb[k];
     const uint32_t w = S.cw[k];
@@ -1053,9 +1178,9 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       ++p_n1;
     }
   }
-  bool hit[kRIt];
+  bool hit[IT];
 #pragma unroll
-  for (int e = 0; e < kRIt; ++e) {
+  for (int e = 0; e < IT; ++e) {
     const uint32_t loc = l0 + e;
     hit[e] = v[e] && !miss[e];
     if (!(v[e] && miss[e])) continue;
@@ -1079,10 +1204,10 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     }
   }
   // final state of every touched block, at its last touch
-  uint32_t fnew[kRIt];
-  bool fin[kRIt];
+  uint32_t fnew[IT];
+  bool fin[IT];
 #pragma unroll
-  for (int e = 0; e < kRIt; ++e) {
+  for (int e = 0; e < IT; ++e) {
     const uint32_t loc = l0 + e;
     fnew[e] = 0;
     fin[e] = v[e] && S.nxloc[loc] == kInf16;
@@ -1114,12 +1239,15 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   __syncthreads();
   RCLK(t_f);
   RTIME(kStT4, t_e, t_f);
+  // the next chunk's in-cache counts, now that this chunk's are stored
+#pragma unroll
+  for (int e = 0; e < IT; ++e) nf[e] = st32[2 * (uint64_t)nb[e]];
   // nonempty-class bits of the LDS classes, from the counts
-  {
-    const uint64_t bal = __ballot(S.ccnt[tid] != 0u);
-    if (lane_id() == 0) S.cnz[tid / 64] = bal;
+  for (uint32_t f = tid; f < kLdsClass; f += NT) {
+    const uint64_t bal = __ballot(S.ccnt[f] != 0u);
+    if (lane_id() == 0) S.cnz[f / 64] = bal;
   }
-  store_hits(hit, c0, L, j, bits);
+  store_hits_n<IT>(hit, c0, L, j, bits);
   if (tid == 0) {
     uint32_t t[8];
 #pragma unroll
@@ -1146,6 +1274,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   return true;
 }
 
+template <int NT>
 __device__ __forceinline__ void lfu_chunked(const JobDev& j, const JobArgs& a,
                                             uint64_t* __restrict__ st, uint32_t* __restrict__ cls,
                                             uint64_t* __restrict__ bits, GroupCounters& gc,
@@ -1157,7 +1286,7 @@ __device__ __forceinline__ void lfu_chunked(const JobDev& j, const JobArgs& a,
   cl.lnz = S.cnz;
   cl.gcnt = head + a.n_class;
   cl.nclass = a.n_class;
-  for (uint32_t f = tid; f < kLdsClass; f += kRNT) S.ccnt[f] = 0;
+  for (uint32_t f = tid; f < kLdsClass; f += NT) S.ccnt[f] = 0;
   if (tid < kLdsClassWords) S.cnz[tid] = 0;
   if (tid < 2) S.anyflag[tid] = 0;
   BlockAny block_any{S.anyflag, 0};
@@ -1170,9 +1299,19 @@ __device__ __forceinline__ void lfu_chunked(const JobDev& j, const JobArgs& a,
   __syncthreads();
   uint64_t pos = j.begin & ~63ull;
   uint32_t len = j.chunk;
+  constexpr int IT = kRChunk / NT;
+  uint32_t pb[IT], pf[IT], nb[IT], nf[IT];  // prefetched blocks and counts of the chunk at ppos
+  uint64_t ppos = ~0ull;
   while (pos < j.end) {
     const uint32_t l = (uint32_t)min<uint64_t>(len, j.end - pos);
-    if (lfu_fast(j, a, st, cl, gc, S, bits, pos, pos + l, g1, g0, block_any)) {
+    if (lfu_fast<NT>(j, a, st, cl, gc, S, bits, pos, pos + l, g1, g0, block_any, ppos == pos, pb,
+                     pf, nb, nf)) {
+      ppos = (l == kRChunk) ? pos + l : ~0ull;
+#pragma unroll
+      for (int e = 0; e < IT; ++e) {
+        pb[e] = nb[e];
+        pf[e] = nf[e];
+      }
       pos += l;
       len = min<uint32_t>(len * 2, j.chunk);
     } else if (l > kMinFast) {
@@ -1184,27 +1323,16 @@ __device__ __forceinline__ void lfu_chunked(const JobDev& j, const JobArgs& a,
       __syncthreads();
       if (!S.ok) break;
       pos += l;
+      ppos = ~0ull;
     }
   }
   __syncthreads();
 }
 
-union ReplayLds {
-  FifoLds f;
-  LfuLds l;
-};
 
-__global__ __launch_bounds__(kRNT) void k_replay(const JobDev* __restrict__ jobs, JobArgs a_in,
-                                                 uint64_t* __restrict__ state,
-                                                 uint32_t* __restrict__ cls,
-                                                 uint64_t* __restrict__ bits,
-                                                 unsigned long long* __restrict__ jcnt) {
-  __shared__ ReplayLds lds;
-  __shared__ GroupCounters gc;
-  JobDev j = jobs[blockIdx.x];
-  if (j.closed) return;
-  // the job's access order in slot 0, so that every pointer is known
-  // without indexing (kept in registers)
+// The job's access order moved to slot 0, so that every pointer is known
+// without indexing (kept in registers).
+__device__ __forceinline__ JobArgs job_args(const JobArgs& a_in, JobDev& j) {
   JobArgs a = a_in;
   if (j.order) {
     a.bid[0] = a_in.bid[1];
@@ -1214,6 +1342,19 @@ __global__ __launch_bounds__(kRNT) void k_replay(const JobDev* __restrict__ jobs
     a.g8[0] = a_in.g8[1];
   }
   j.order = 0;
+  return a;
+}
+
+// FIFO jobs (LFU jobs are left to k_replay_lfu).
+__global__ __launch_bounds__(kRNT) void k_replay(const JobDev* __restrict__ jobs, JobArgs a_in,
+                                                 uint64_t* __restrict__ state,
+                                                 uint64_t* __restrict__ bits,
+                                                 unsigned long long* __restrict__ jcnt) {
+  __shared__ FifoLds lds;
+  __shared__ GroupCounters gc;
+  JobDev j = jobs[blockIdx.x];
+  if (j.closed || j.kind == kJobLfu) return;
+  const JobArgs a = job_args(a_in, j);
   const uint32_t tid = threadIdx.x;
   if (tid < KV_MAX_GROUPS) gc.ins[tid] = gc.insw[tid] = gc.ev[tid] = gc.evw[tid] = 0;
 #ifdef KV_REPLAY_STATS
@@ -1225,16 +1366,42 @@ __global__ __launch_bounds__(kRNT) void k_replay(const JobDev* __restrict__ jobs
   const bool g1 = a.n_groups == 1 || j.group != KV_MAX_GROUPS;
   const uint32_t g0 = j.group == KV_MAX_GROUPS ? 0u : j.group;
   unsigned long long* cnt = jcnt + (uint64_t)blockIdx.x * a.n_groups * 4;
-  bool ok = true;
-  if (j.kind == kJobFifoChunk) {
+  if (j.kind == kJobFifoChunk)
     fifo_chunked(j, a, reinterpret_cast<uint32_t*>(state + j.state_off), bits + j.bits_off, gc,
-                 lds.f, g1, g0);
-  } else if (j.kind == kJobFifoSerial) {
+                 lds, g1, g0);
+  else
     fifo_serial(j, a, reinterpret_cast<uint32_t*>(state + j.state_off), bits + j.bits_off, gc);
-  } else {
-    lfu_chunked(j, a, state + j.state_off, cls, bits + j.bits_off, gc, lds.l, g1, g0);
-    ok = lds.l.ok != 0;
-  }
+  __syncthreads();
+  write_counters(gc, a.n_groups, cnt);
+#ifdef KV_REPLAY_STATS
+  if (tid < kStats) g_rstats[blockIdx.x & 255][tid] += s_rstats[tid];
+#endif
+}
+
+// LFU jobs, kLfuNT threads per job.
+template <int NT>
+__global__ __launch_bounds__(NT) void k_replay_lfu(const JobDev* __restrict__ jobs, JobArgs a_in,
+                                                   uint64_t* __restrict__ state,
+                                                   uint32_t* __restrict__ cls,
+                                                   uint64_t* __restrict__ bits,
+                                                   unsigned long long* __restrict__ jcnt) {
+  __shared__ LfuLds lds;
+  __shared__ GroupCounters gc;
+  JobDev j = jobs[blockIdx.x];
+  if (j.closed || j.kind != kJobLfu) return;
+  const JobArgs a = job_args(a_in, j);
+  const uint32_t tid = threadIdx.x;
+  if (tid < KV_MAX_GROUPS) gc.ins[tid] = gc.insw[tid] = gc.ev[tid] = gc.evw[tid] = 0;
+#ifdef KV_REPLAY_STATS
+  if (tid < kStats) s_rstats[tid] = 0;
+  if (tid < 4) s_rwave[tid] = 0;
+#endif
+  __syncthreads();
+  const bool g1 = a.n_groups == 1 || j.group != KV_MAX_GROUPS;
+  const uint32_t g0 = j.group == KV_MAX_GROUPS ? 0u : j.group;
+  unsigned long long* cnt = jcnt + (uint64_t)blockIdx.x * a.n_groups * 4;
+  lfu_chunked<NT>(j, a, state + j.state_off, cls, bits + j.bits_off, gc, lds, g1, g0);
+  const bool ok = lds.ok != 0;
   __syncthreads();
   write_counters(gc, a.n_groups, cnt);
   if (tid == 0 && !ok) cnt[0] = ~0ull;  // poison: surfaced as an impossible count
@@ -1367,6 +1534,31 @@ __global__ __launch_bounds__(256) void k_combine(const RecDev* __restrict__ recs
 }
 
 }  // namespace
+
+// A second stream per device (default priority) with a fork and a join
+// event, created on first use and kept until the process ends.
+struct AuxStream {
+  hipStream_t s = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+  std::mutex mu;
+};
+
+static kv_status aux_stream(AuxStream** out) {
+  static std::mutex mu;
+  static AuxStream aux[64];
+  int dev = 0;
+  KV_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= 64) return fail(KV_ERR_DEVICE, "device index out of range");
+  std::lock_guard<std::mutex> g(mu);
+  AuxStream& a = aux[dev];
+  if (!a.s) {
+    KV_HIP(hipStreamCreateWithFlags(&a.s, hipStreamNonBlocking));
+    KV_HIP(hipEventCreateWithFlags(&a.fork, hipEventDisableTiming));
+    KV_HIP(hipEventCreateWithFlags(&a.join, hipEventDisableTiming));
+  }
+  *out = &a;
+  return KV_OK;
+}
 
 kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_config* cfg_host,
                      const kv_config* cfg_dev, uint32_t n_cfg, uint64_t* counts,
@@ -1529,10 +1721,37 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
     KV_HIP(hipGetLastError());
     tm.reset();
     tm.emplace(kStReplay, s);
-    hipLaunchKernelGGL(k_replay, dim3(nj), dim3(kRNT), 0, s, bj.as<JobDev>(), ja,
-                       bstate.as<uint64_t>(), bcls.as<uint32_t>(), bbits.as<uint64_t>(),
-                       bjc.as<unsigned long long>());
-    KV_HIP(hipGetLastError());
+    bool any_fifo = false, any_lfu = false;
+    for (const JobDev& q : jd) {
+      any_fifo |= !q.closed && q.kind != kJobLfu;
+      any_lfu |= !q.closed && q.kind == kJobLfu;
+    }
+    // FIFO and LFU jobs run concurrently: FIFO on a second stream forked
+    // from and joined back into the caller's
+    AuxStream* aux = nullptr;
+    std::unique_lock<std::mutex> lk;
+    if (any_fifo && any_lfu) {
+      if ((st = aux_stream(&aux)) != KV_OK) return st;
+      lk = std::unique_lock<std::mutex>(aux->mu);
+      KV_HIP(hipEventRecord(aux->fork, s));
+      KV_HIP(hipStreamWaitEvent(aux->s, aux->fork, 0));
+    }
+    if (any_fifo) {
+      hipLaunchKernelGGL(k_replay, dim3(nj), dim3(kRNT), 0, aux ? aux->s : s, bj.as<JobDev>(),
+                         ja, bstate.as<uint64_t>(), bbits.as<uint64_t>(),
+                         bjc.as<unsigned long long>());
+      KV_HIP(hipGetLastError());
+    }
+    if (any_lfu) {
+      hipLaunchKernelGGL(k_replay_lfu<kLfuNT>, dim3(nj), dim3(kLfuNT), 0, s, bj.as<JobDev>(), ja,
+                         bstate.as<uint64_t>(), bcls.as<uint32_t>(), bbits.as<uint64_t>(),
+                         bjc.as<unsigned long long>());
+      KV_HIP(hipGetLastError());
+    }
+    if (aux) {
+      KV_HIP(hipEventRecord(aux->join, aux->s));
+      KV_HIP(hipStreamWaitEvent(s, aux->join, 0));
+    }
   }
 #ifdef KV_REPLAY_STATS
   {
