@@ -980,7 +980,6 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       __syncthreads();
     }
     const uint64_t evtot = (used0 + itot > j.cap) ? used0 + itot - j.cap : 0ull;
-    RWAVE(0, t_it);
     // the eviction queue: nc0 old entries, then the nm insertions of the
     // chunk; thread t holds entries t*qpt .. t*qpt+qpt-1
     const uint32_t nq = nc0 + nm;
@@ -1000,7 +999,6 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     }
     uint32_t elig;
     uint32_t run = block_excl_scan_u32<NT>(xs, S.red, elig);
-    RWAVE(1, t_it);
     bool bad = (uint64_t)elig < evtot;
     // entry k is consumed by the first miss whose demand exceeds the
     // eligible weight queued before k.  Demands and prefixes both rise, so
@@ -1059,7 +1057,6 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       mn = min(mn, evk[e]);
       suf[e] = mn;
     }
-    RWAVE(2, t_it);
     uint32_t tmin;
     bool anybad;
     block_suffix_min_flag<NT>(mn, bad, S.sfx, tmin, anybad);
@@ -1103,8 +1100,6 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     }
     cur = ns;
     if (!block_any(changed)) converged = true;
-    RWAVE(3, t_it);
-    RWAVE_FLUSH();
   }
   if (!converged) {
     RSTAT(blockIdx.x, kStFailConv, 1);
@@ -1158,11 +1153,13 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   // per-thread partials: insertions, evictions, victim weight, last entries taken
   uint32_t p_ins = 0, p_insw = 0, p_ev = 0, p_evw = 0, p_vw = 0, p_lastp = 0, p_lastm = 0,
            p_n1 = 0;
-  // old entries evicted
+  // old entries evicted (loads issued unconditionally, several in flight)
   for (uint32_t k = tid; k < nc0; k += NT) {
-    if (!S.ccons[k]) continue;
+    const bool cons = S.ccons[k] != 0;
     const uint32_t b = S.cb[k];
     const uint32_t w = S.cw[k];
+    const bool untouched = S.ca[k] == kInf16;
+    if (!cons) continue;
     if (g1) {
       ++p_ev;
       p_evw += w;
@@ -1173,18 +1170,35 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     }
     p_vw += w;
     p_lastp = max(p_lastp, k + 1);
-    if (S.ca[k] == kInf16) {  // not touched again in the chunk: leaves class 1 for good
+    if (untouched) {  // not touched again in the chunk: leaves class 1 for good
       st[b] = 0;
       ++p_n1;
     }
   }
-  bool hit[IT];
+  // per-access chunk data, loaded for all items at once
+  uint32_t mc[IT], nxl[IT], lm[IT], oc[IT];
 #pragma unroll
   for (int e = 0; e < IT; ++e) {
     const uint32_t loc = l0 + e;
+    mc[e] = S.mcons[loc];
+    nxl[e] = S.nxloc[loc];
+    lm[e] = (uint32_t)(int32_t)S.lmiss[loc];
+    oc[e] = S.occ[loc];
+  }
+  uint32_t mocc[IT], mcm[IT];
+#pragma unroll
+  for (int e = 0; e < IT; ++e) {
+    const uint32_t m = (int32_t)lm[e] >= 0 ? lm[e] : 0u;
+    mocc[e] = S.occ[m];
+    mcm[e] = S.mcons[m];
+  }
+  bool hit[IT];
+#pragma unroll
+  for (int e = 0; e < IT; ++e) {
     hit[e] = v[e] && !miss[e];
     if (!(v[e] && miss[e])) continue;
-    const bool cons = S.mcons[loc] != 0;  // inserted here, evicted later in the chunk
+    const uint32_t loc = l0 + e;
+    const bool cons = mc[e] != 0;  // inserted here, evicted later in the chunk
     if (g1) {
       ++p_ins;
       p_insw += ww[e];
@@ -1210,13 +1224,12 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   for (int e = 0; e < IT; ++e) {
     const uint32_t loc = l0 + e;
     fnew[e] = 0;
-    fin[e] = v[e] && S.nxloc[loc] == kInf16;
+    fin[e] = v[e] && nxl[e] == kInf16;
     if (!fin[e]) continue;
-    const int16_t m = S.lmiss[loc];
-    if (m >= 0) {
-      fnew[e] = S.mcons[m] ? 0u : (uint32_t)(S.occ[loc] - S.occ[m]) + 1u;
+    if ((int32_t)lm[e] >= 0) {
+      fnew[e] = mcm[e] ? 0u : oc[e] - mocc[e] + 1u;
     } else {
-      fnew[e] = f0[e] + (uint32_t)S.occ[loc] + 1u;
+      fnew[e] = f0[e] + oc[e] + 1u;
     }
     st[bb[e]] = fnew[e] ? (((uint64_t)(c0 + loc) << 32) | fnew[e]) : 0ull;
     if (res0[e]) class_add_par(cl, f0[e], -1);
