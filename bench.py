@@ -56,6 +56,9 @@ def parse():
     ap.add_argument("--workload", default="full", choices=sorted(WORKLOAD_TEXT))
     ap.add_argument("--cpu-baseline-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="first run one plain device-to-device copy of BYTES (a reference "
+                         "for hardware byte counters)")
     return ap.parse_args()
 
 
@@ -149,6 +152,14 @@ def main():
     import tracegen as tg
     from paper_2603_08739_amd import host, kvcfg as K
 
+    if args.copy_calibration:
+        src = torch.ones(args.copy_calibration // 4, dtype=torch.int32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(f"[bench] copy calibration: {src.numel() * 4} bytes", file=sys.stderr, flush=True)
+        del src, dst
     print(f"[bench] generating workload {args.workload}", file=sys.stderr, flush=True)
     rec = tg.recipe(args.workload)
     cfgs = tg.configs_for(args.workload, rec)
