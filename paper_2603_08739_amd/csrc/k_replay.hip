@@ -117,14 +117,15 @@ __global__ __launch_bounds__(256) void k_replay_init(const JobDev* __restrict__ 
                                                      uint32_t* __restrict__ cls, JobArgs a) {
   const JobDev j = jobs[blockIdx.y];
   if (j.closed) return;
-  // FIFO: u32 insertion totals (two per word, all-ones = never inserted);
-  // LFU: u64 (last access, count), zero = absent
-  const uint64_t fill = (j.policy == KV_POLICY_FIFO) ? kNoIns : 0ull;
-  const uint64_t words = (j.policy == KV_POLICY_FIFO) ? (a.u + 1) / 2 : a.u;
-  uint64_t* st = state + j.state_off;
-  for (uint64_t b = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; b < words;
-       b += (uint64_t)gridDim.x * blockDim.x)
-    st[b] = fill;
+  // FIFO: u32 insertion totals per block (two per word, all-ones = never
+  // inserted).  LFU: u32 counts per position, each written before it is read.
+  if (j.policy == KV_POLICY_FIFO) {
+    const uint64_t words = (a.u + 1) / 2;
+    uint64_t* st = state + j.state_off;
+    for (uint64_t b = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; b < words;
+         b += (uint64_t)gridDim.x * blockDim.x)
+      st[b] = kNoIns;
+  }
   if (j.policy == KV_POLICY_LFU) {
     // head[n_class] u32 | cnt[n_class] u32
     uint32_t* head = cls + j.class_off;
@@ -559,12 +560,17 @@ __device__ __forceinline__ void fifo_serial(const JobDev& j, const JobArgs& a,
 }
 
 // ---------------------------------------------------------------------------
-// LFU.  State per block: (last access position << 32) | in-cache count (0 =
-// absent).  The members of count class f in victim order are the positions
-// of their last accesses, so class f is a queue over positions scanned by a
-// head pointer head[f].  Member counts and a nonempty-class bitmap locate the
-// lowest nonempty class; classes below kLdsClass keep them in LDS (the
-// workgroup owns its job for the whole replay), higher ones in HBM.
+// LFU.  The state is kept per trace position, not per block: cnt[p] is the
+// block's in-cache count after its access at p (0: evicted), read through
+// the next access's link to p.  Stores are therefore confined to the chunk
+// being replayed.  Members of count class f in victim order are the
+// positions of their latest accesses, so class f is a queue over positions
+// scanned by a head pointer head[f].  Class 1 loses members oldest first, so
+// a count-1 block whose latest access lies before head[1] has been evicted:
+// those evictions need no store at all.  Member counts and a nonempty-class
+// bitmap locate the lowest nonempty class; classes below kLdsClass keep them
+// in LDS (the workgroup owns its job for the whole replay), higher ones in
+// HBM.
 // ---------------------------------------------------------------------------
 struct LfuLds {
   // per access of the chunk (local position)
@@ -580,7 +586,6 @@ struct LfuLds {
   uint32_t mneed[kRChunk];    // ...and the weight that must have left the cache by then
   // count-1 residents from before the chunk, oldest first
   uint32_t cq[kCand];         // position of their last touch
-  uint32_t cb[kCand];         // block
   uint16_t ca[kCand];         // first touch inside the chunk or kInf16
   uint8_t cw[kCand];
   uint8_t cskip[kCand];
@@ -597,6 +602,11 @@ struct LfuLds {
   uint64_t vw;                // candidate scan: untouched weight found
   int ok;
 };
+
+// In-cache count of a block whose latest access is q with stored count c.
+__device__ __forceinline__ uint32_t lfu_live_count(uint32_t c, uint64_t q, uint64_t head1) {
+  return (c >= 2u || (c == 1u && q >= head1)) ? c : 0u;
+}
 
 struct Classes {
   uint32_t* lcnt;   // LDS counts, classes < kLdsClass
@@ -651,12 +661,14 @@ __device__ __forceinline__ void class_add_par(const Classes& c, uint32_t f, int 
 // Exact replay of [p0, p1) by one thread (thread 0); returns false if the
 // state is found inconsistent.
 __device__ __forceinline__ bool lfu_serial_range(const JobDev& j, const JobArgs& a,
-                                                 uint64_t* __restrict__ st, uint32_t* head,
+                                                 uint32_t* __restrict__ cnt, uint32_t* head,
                                                  const Classes& cl, LfuLds& S, GroupCounters& gc,
                                                  uint64_t* __restrict__ bits, uint64_t p0,
                                                  uint64_t p1) {
   const uint32_t o = j.order;
-  const uint32_t* __restrict__ bid = a.bid[o];
+  const uint32_t* __restrict__ key = a.key[o];
+  const uint32_t* __restrict__ nxt = a.nxt[o];
+  const uint64_t b0 = j.begin;
   head[1] = S.head1;
   uint64_t used = S.used;
   uint32_t fmin = S.fmin;
@@ -664,35 +676,32 @@ __device__ __forceinline__ bool lfu_serial_range(const JobDev& j, const JobArgs&
   bool ok = true;
   for (uint64_t i = p0; i < p1 && ok; ++i) {
     if (i >= j.begin) {
-      const uint32_t b = bid[i];
       const uint32_t w = a.w8[o][i];
-      const uint64_t s = st[b];
-      const uint32_t f = (uint32_t)s;
+      const uint32_t k = key[i];
+      const uint32_t f = k ? lfu_live_count(cnt[k - 1 - b0], k - 1, head[1]) : 0u;
       if (f) {
         word |= 1ull << (i & 63);
         const uint32_t f1 = f + 1;
         class_add1(cl, f, -1);
         class_add1(cl, f1, +1);
         if (f == fmin && class_count(cl, f) == 0) fmin = f1;
-        st[b] = ((uint64_t)i << 32) | f1;
+        cnt[i - b0] = f1;
       } else {
         while (used + w > j.cap) {
-          uint32_t q = head[fmin];
-          uint32_t v = 0;
+          uint64_t q = head[fmin];
           // the oldest live member of class fmin lies before position i; the
           // bound only guards against corrupted state
           for (; q < i; ++q) {
-            v = bid[q];
-            const uint64_t sv = st[v];
-            if ((uint32_t)sv == fmin && (uint32_t)(sv >> 32) == q) break;
+            const uint32_t nq = nxt[q];
+            if (cnt[q - b0] == fmin && (nq == kNone || nq >= i)) break;
           }
           if (q >= i) {
             ok = false;
             break;
           }
-          head[fmin] = q + 1;
-          st[v] = 0;
-          const uint32_t vw = a.blk_w[v], vg = a.blk_g[v];
+          head[fmin] = (uint32_t)(q + 1);
+          cnt[q - b0] = 0;
+          const uint32_t vw = a.w8[o][q], vg = a.g8[o][q];
           used -= vw;
           gc.ev[vg] += 1;
           gc.evw[vg] += vw;
@@ -702,7 +711,7 @@ __device__ __forceinline__ bool lfu_serial_range(const JobDev& j, const JobArgs&
             if (nf != 0xFFFFFFFFu) fmin = nf;
           }
         }
-        st[b] = ((uint64_t)i << 32) | 1u;
+        cnt[i - b0] = 1;
         class_add1(cl, 1, +1);
         fmin = 1;
         used += w;
@@ -780,12 +789,12 @@ __device__ __forceinline__ void block_suffix_min_flag(uint32_t v, bool flag, uin
 // eviction, which moves head1 past them).
 template <int NT>
 __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
-                                         uint64_t* __restrict__ st, const Classes& cl,
+                                         uint32_t* __restrict__ cnt, const Classes& cl,
                                          GroupCounters& gc, LfuLds& S,
                                          uint64_t* __restrict__ bits, uint64_t c0, uint64_t c1,
                                          bool g1, uint32_t g0, BlockAny& block_any,
-                                         bool have_pref, const uint32_t* pb, const uint32_t* pf,
-                                         uint32_t* nb, uint32_t* nf) {
+                                         bool have_pref, const uint32_t* pk, const uint32_t* pf,
+                                         uint32_t* nk, uint32_t* nf) {
   constexpr int IT = kRChunk / NT;               // accesses per thread
   constexpr int CPT = (kCand + kRChunk) / NT;    // queue entries per thread
   const uint32_t tid = threadIdx.x;
@@ -798,35 +807,38 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
 #pragma unroll
   for (int e = 0; e < IT; ++e) v[e] = l0 + e < L && p0 + e >= j.begin;
   const bool all = v[0] && v[IT - 1];
-  uint32_t bb[IT], ww[IT], gg[IT], kk[IT], nx[IT], f0[IT];
+  uint32_t ww[IT], gg[IT], kk[IT], nx[IT], f0[IT];
   bool cm[IT], res0[IT];
   if (have_pref) {
 #pragma unroll
-    for (int e = 0; e < IT; ++e) bb[e] = pb[e];
+    for (int e = 0; e < IT; ++e) kk[e] = pk[e];
   } else {
-    loadn_u32<IT>(a.bid[o], p0, all, v, bb);
+    loadn_u32<IT>(a.key[o], p0, all, v, kk);
   }
   loadn_u8<IT>(a.w8[o], p0, all, v, ww);
-  loadn_u32<IT>(a.key[o], p0, all, v, kk);
   loadn_u32<IT>(a.nxt[o], p0, all, v, nx);
 #pragma unroll
   for (int e = 0; e < IT; ++e) gg[e] = g0;
   if (!g1) loadn_u8<IT>(a.g8[o], p0, all, v, gg);
   uint32_t h = S.head1;
   if (tid < 8) S.tot8[tid] = 0;  // first read after several barriers
-  // in-cache counts (the low words of the states); prefetched by the
-  // previous chunk when it covered the whole chunk before this one
-  const uint32_t* st32 = reinterpret_cast<const uint32_t*>(st);
+  // stored counts at the latest earlier accesses (prefetched by the
+  // previous chunk when it covered the whole chunk before this one); only a
+  // block's first access in the chunk needs one
   uint32_t s0[IT];
 #pragma unroll
-  for (int e = 0; e < IT; ++e) s0[e] = have_pref ? pf[e] : (v[e] ? st32[2 * (uint64_t)bb[e]] : 0u);
+  for (int e = 0; e < IT; ++e) {
+    const bool old_prev = v[e] && kk[e] != 0 && (uint64_t)(kk[e] - 1) < c0;
+    s0[e] = have_pref ? pf[e] : (old_prev ? cnt[kk[e] - 1 - j.begin] : 0u);
+  }
 #pragma unroll
   for (int e = 0; e < IT; ++e) {
     const uint32_t loc = l0 + e;
     const int lp = (kk[e] != 0 && (uint64_t)(kk[e] - 1) >= c0) ? (int)((uint64_t)(kk[e] - 1) - c0)
                                                                : -1;
     const bool again = v[e] && nx[e] != kNone && (uint64_t)nx[e] < c1;
-    f0[e] = v[e] ? s0[e] : 0u;
+    // the block's count at the chunk start (first accesses only)
+    f0[e] = (v[e] && kk[e] != 0 && lp < 0) ? lfu_live_count(s0[e], kk[e] - 1, h) : 0u;
     res0[e] = f0[e] != 0;
     cm[e] = v[e] && lp < 0 && !res0[e];
     S.lp[loc] = (int16_t)lp;
@@ -871,12 +883,12 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     const uint64_t pn = min<uint64_t>(pnext, a.n & ~3ull);
 #pragma unroll
     for (int q = 0; q < IT / 4; ++q) {
-      const uint4 x = *reinterpret_cast<const uint4*>(a.bid[o] + pn + 4 * q);
+      const uint4 x = *reinterpret_cast<const uint4*>(a.key[o] + pn + 4 * q);
       const uint32_t xv[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const uint64_t pe = pnext + 4 * q + r;
-        nb[4 * q + r] = (pn == pnext && pe >= j.begin && pe < j.end) ? xv[r] : 0u;
+        nk[4 * q + r] = (pn == pnext && pe >= j.begin && pe < j.end) ? xv[r] : 0u;
       }
     }
   }
@@ -892,19 +904,17 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       if (vw >= ev0 || (uint64_t)h >= c0 || n0 + NT * kCScan > kCand) break;
       RSTAT(blockIdx.x, kStScanned, 1);
       bool live[kCScan], touched[kCScan];
-      uint32_t bq[kCScan], wq[kCScan], aq[kCScan];
+      uint32_t wq[kCScan], aq[kCScan];
 #pragma unroll
       for (int e = 0; e < kCScan; ++e) {
         const uint64_t q = (uint64_t)h + tid * kCScan + e;
         live[e] = false;
         touched[e] = false;
         aq[e] = kInf16;
-        bq[e] = 0;
         wq[e] = 0;
         if (q < c0) {
           const uint64_t word = bits[(q >> 6) - j.word0];
           const uint32_t nxq = a.nxt[o][q];
-          bq[e] = a.bid[o][q];
           wq[e] = a.w8[o][q];
           live[e] = !((word >> (q & 63)) & 1ull) && (nxq == kNone || (uint64_t)nxq >= c0);
           touched[e] = live[e] && nxq != kNone && (uint64_t)nxq < c1;
@@ -924,7 +934,6 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
         if (!live[e]) continue;
         const uint32_t k = n0 + pos++;
         S.cq[k] = h + tid * kCScan + e;
-        S.cb[k] = bq[e];
         S.cw[k] = (uint8_t)wq[e];
         S.ca[k] = (uint16_t)aq[e];
         S.cskip[k] = touched[e] ? 1 : 0;
@@ -1115,6 +1124,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     const uint32_t loc = l0 + e;
     miss[e] = cm[e] || (v[e] && S.capm[loc] == cur);
     S.lmiss[loc] = miss[e] ? (int16_t)loc : (int16_t)-1;
+    S.mneed[loc] = f0[e];  // a block's count at the chunk start, read via its first access
   }
   __syncthreads();
   for (;;) {
@@ -1156,7 +1166,6 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   // old entries evicted (loads issued unconditionally, several in flight)
   for (uint32_t k = tid; k < nc0; k += NT) {
     const bool cons = S.ccons[k] != 0;
-    const uint32_t b = S.cb[k];
     const uint32_t w = S.cw[k];
     const bool untouched = S.ca[k] == kInf16;
     if (!cons) continue;
@@ -1164,16 +1173,14 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       ++p_ev;
       p_evw += w;
     } else {
-      const uint32_t g = a.blk_g[b];
+      const uint32_t g = a.g8[o][S.cq[k]];
       atomicAdd(&gc.ev[g], 1ull);
       atomicAdd(&gc.evw[g], (unsigned long long)w);
     }
     p_vw += w;
     p_lastp = max(p_lastp, k + 1);
-    if (untouched) {  // not touched again in the chunk: leaves class 1 for good
-      st[b] = 0;
-      ++p_n1;
-    }
+    if (untouched) ++p_n1;  // not touched again in the chunk: leaves class 1 for good
+                            // (head1 passes it: no store)
   }
   // per-access chunk data, loaded for all items at once
   uint32_t mc[IT], nxl[IT], lm[IT], oc[IT];
@@ -1185,12 +1192,14 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     lm[e] = (uint32_t)(int32_t)S.lmiss[loc];
     oc[e] = S.occ[loc];
   }
-  uint32_t mocc[IT], mcm[IT];
+  uint32_t mocc[IT], mcm[IT], rf0[IT];
 #pragma unroll
   for (int e = 0; e < IT; ++e) {
     const uint32_t m = (int32_t)lm[e] >= 0 ? lm[e] : 0u;
     mocc[e] = S.occ[m];
     mcm[e] = S.mcons[m];
+    const int16_t r = S.lp[l0 + e];  // the block's first access in the chunk
+    rf0[e] = r >= 0 ? S.mneed[r] : f0[e];
   }
   bool hit[IT];
 #pragma unroll
@@ -1217,23 +1226,36 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       p_lastm = max(p_lastm, loc + 1);
     }
   }
-  // final state of every touched block, at its last touch
+  // final state of every touched block, at its last touch.  Moves into and
+  // out of classes 1 and 2 (the crowded ones) add up per wavefront by
+  // ballot; the others go one by one.
   uint32_t fnew[IT];
   bool fin[IT];
+  int d12[2] = {0, 0};
 #pragma unroll
   for (int e = 0; e < IT; ++e) {
     const uint32_t loc = l0 + e;
     fnew[e] = 0;
     fin[e] = v[e] && nxl[e] == kInf16;
-    if (!fin[e]) continue;
-    if ((int32_t)lm[e] >= 0) {
-      fnew[e] = mcm[e] ? 0u : oc[e] - mocc[e] + 1u;
-    } else {
-      fnew[e] = f0[e] + oc[e] + 1u;
+    if (fin[e]) {
+      if ((int32_t)lm[e] >= 0) {
+        fnew[e] = mcm[e] ? 0u : oc[e] - mocc[e] + 1u;
+      } else {
+        fnew[e] = rf0[e] + oc[e] + 1u;
+      }
+      cnt[c0 + loc - j.begin] = fnew[e];
     }
-    st[bb[e]] = fnew[e] ? (((uint64_t)(c0 + loc) << 32) | fnew[e]) : 0ull;
-    if (res0[e]) class_add_par(cl, f0[e], -1);
-    if (fnew[e]) class_add_par(cl, fnew[e], +1);
+    const uint32_t fo = fin[e] ? rf0[e] : 0u, fn = fnew[e];
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+      d12[c] += __popcll(__ballot(fn == (uint32_t)(c + 1))) -
+                __popcll(__ballot(fo == (uint32_t)(c + 1)));
+    if (fo > 2) class_add_par(cl, fo, -1);
+    if (fn > 2) class_add_par(cl, fn, +1);
+  }
+  if (lane_id() == 0) {
+    if (d12[0]) atomicAdd(&S.ccnt[1], (uint32_t)d12[0]);
+    if (d12[1]) atomicAdd(&S.ccnt[2], (uint32_t)d12[1]);
   }
   {
     const uint32_t r[8] = {wave_add_dpp(p_ins), wave_add_dpp(p_insw), wave_add_dpp(p_ev),
@@ -1252,9 +1274,14 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   __syncthreads();
   RCLK(t_f);
   RTIME(kStT4, t_e, t_f);
-  // the next chunk's in-cache counts, now that this chunk's are stored
+  // the next chunk's stored counts, now that this chunk's are stored (an
+  // access with no earlier one, or one inside the next chunk, reads the
+  // job's first slot and ignores it)
 #pragma unroll
-  for (int e = 0; e < IT; ++e) nf[e] = st32[2 * (uint64_t)nb[e]];
+  for (int e = 0; e < IT; ++e) {
+    const bool old_prev = nk[e] != 0 && (uint64_t)(nk[e] - 1) < c0 + kRChunk;
+    nf[e] = cnt[old_prev ? nk[e] - 1 - j.begin : 0];
+  }
   // nonempty-class bits of the LDS classes, from the counts
   for (uint32_t f = tid; f < kLdsClass; f += NT) {
     const uint64_t bal = __ballot(S.ccnt[f] != 0u);
@@ -1289,7 +1316,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
 
 template <int NT>
 __device__ __forceinline__ void lfu_chunked(const JobDev& j, const JobArgs& a,
-                                            uint64_t* __restrict__ st, uint32_t* __restrict__ cls,
+                                            uint32_t* __restrict__ cnt, uint32_t* __restrict__ cls,
                                             uint64_t* __restrict__ bits, GroupCounters& gc,
                                             LfuLds& S, bool g1, uint32_t g0) {
   const uint32_t tid = threadIdx.x;
@@ -1313,16 +1340,16 @@ __device__ __forceinline__ void lfu_chunked(const JobDev& j, const JobArgs& a,
   uint64_t pos = j.begin & ~63ull;
   uint32_t len = j.chunk;
   constexpr int IT = kRChunk / NT;
-  uint32_t pb[IT], pf[IT], nb[IT], nf[IT];  // prefetched blocks and counts of the chunk at ppos
+  uint32_t pk[IT], pf[IT], nk[IT], nf[IT];  // prefetched links and counts of the chunk at ppos
   uint64_t ppos = ~0ull;
   while (pos < j.end) {
     const uint32_t l = (uint32_t)min<uint64_t>(len, j.end - pos);
-    if (lfu_fast<NT>(j, a, st, cl, gc, S, bits, pos, pos + l, g1, g0, block_any, ppos == pos, pb,
-                     pf, nb, nf)) {
+    if (lfu_fast<NT>(j, a, cnt, cl, gc, S, bits, pos, pos + l, g1, g0, block_any, ppos == pos, pk,
+                     pf, nk, nf)) {
       ppos = (l == kRChunk) ? pos + l : ~0ull;
 #pragma unroll
       for (int e = 0; e < IT; ++e) {
-        pb[e] = nb[e];
+        pk[e] = nk[e];
         pf[e] = nf[e];
       }
       pos += l;
@@ -1331,7 +1358,7 @@ __device__ __forceinline__ void lfu_chunked(const JobDev& j, const JobArgs& a,
       len = max<uint32_t>(kMinFast, (l / 2) & ~63u);
     } else {
       __syncthreads();
-      if (tid == 0) S.ok = lfu_serial_range(j, a, st, head, cl, S, gc, bits, pos, pos + l) ? 1 : 0;
+      if (tid == 0) S.ok = lfu_serial_range(j, a, cnt, head, cl, S, gc, bits, pos, pos + l) ? 1 : 0;
       RSTAT(blockIdx.x, kStSerialAcc, l);
       __syncthreads();
       if (!S.ok) break;
@@ -1413,7 +1440,8 @@ __global__ __launch_bounds__(NT) void k_replay_lfu(const JobDev* __restrict__ jo
   const bool g1 = a.n_groups == 1 || j.group != KV_MAX_GROUPS;
   const uint32_t g0 = j.group == KV_MAX_GROUPS ? 0u : j.group;
   unsigned long long* cnt = jcnt + (uint64_t)blockIdx.x * a.n_groups * 4;
-  lfu_chunked<NT>(j, a, state + j.state_off, cls, bits + j.bits_off, gc, lds, g1, g0);
+  lfu_chunked<NT>(j, a, reinterpret_cast<uint32_t*>(state + j.state_off), cls, bits + j.bits_off,
+                  gc, lds, g1, g0);
   const bool ok = lds.ok != 0;
   __syncthreads();
   write_counters(gc, a.n_groups, cnt);
@@ -1607,7 +1635,7 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
     }
     if (!r.closed && r.end > r.begin) {
       j.state_off = state_words;
-      state_words += (r.policy == KV_POLICY_FIFO) ? (t.u + 1) / 2 : t.u;
+      state_words += (r.policy == KV_POLICY_FIFO) ? (t.u + 1) / 2 : (r.end - r.begin + 1) / 2;
       if (r.policy == KV_POLICY_LFU) {
         j.class_off = class_total;
         class_total += class_words;
