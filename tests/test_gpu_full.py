@@ -1,0 +1,198 @@
+"""Full-size checks: the full-scale sweep (3.87e8 accesses, 11,000
+configurations) in the launch configuration the benchmark times.
+
+The oracle cannot replay this trace in test time, so the outputs are held to
+properties that hold at any size: conservation of accesses over the tiers,
+capacity bounds, the LRU inclusion property (a tier's cumulative hits depend
+only on the largest capacity up to it, and grow with it), closed-form
+results for caches that hold every distinct block, trace statistics
+recomputed independently with torch, and the Pareto fronts recomputed by
+brute force on the host.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import tracegen as tg
+
+pytestmark = pytest.mark.gpu
+
+HIT, MISS, INS, EVICT, HIT_W, MISS_W, INS_W, EVICT_W = range(8)
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def full_run():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a device"
+    from paper_2603_08739_amd import host, kvcfg as K
+    say("  full sweep: generating the trace on the device")
+    rec = tg.recipe("full")
+    cfgs = tg.configs_for("full", rec)
+    dev = rec.expand("cuda")
+    torch.cuda.synchronize()
+    n = int(dev["hash"].numel())
+    say(f"  full sweep: {n} accesses, {cfgs.n} configurations; loading")
+    h = K.kv_trace_load(dev["hash"], dev["req"], dev["req_time"], group=dev["group"],
+                        weight=dev["weight"], n_groups=rec.n_groups,
+                        tokens_per_granule=rec.tokens_per_granule,
+                        granule_bytes=rec.granule_bytes)
+    st = h.info()
+    say("  full sweep: evaluating")
+    counts, obj = host.evaluate(h, cfgs, tg.DEFAULT_COST, rec.n_groups)
+    h.free()
+    say("  full sweep: Pareto fronts")
+    front, nfront = host.pareto(obj)
+    front_seg, _ = host.pareto(obj, segment=cfgs.segment)
+    # independent statistics of the trace
+    n_w = int(dev["weight"].to(torch.int64).sum().item())
+    uniq, first = torch.unique(dev["hash"], return_inverse=True)
+    u = int(uniq.numel())
+    wfirst = torch.zeros(u, dtype=torch.int64, device="cuda")
+    wfirst.scatter_(0, first, dev["weight"].to(torch.int64))
+    distinct_w = int(wfirst.sum().item())
+    del uniq, first, wfirst, dev
+    torch.cuda.empty_cache()
+    say("  full sweep: done")
+    return dict(cfgs=cfgs, counts=counts.astype(np.int64), obj=obj, front=front,
+                nfront=nfront, front_seg=front_seg, st=st, n=n, n_w=n_w, u=u,
+                distinct_w=distinct_w)
+
+
+def test_trace_statistics(full_run):
+    r = full_run
+    st = r["st"]
+    assert st.n == r["n"]
+    assert st.n_w == r["n_w"]
+    assert st.n_distinct == r["u"]
+    assert st.distinct_w == r["distinct_w"]
+
+
+def test_counts_conserve_accesses(full_run):
+    r = full_run
+    c, cfgs = r["counts"][:, 0], r["cfgs"]
+    assert (c >= 0).all()
+    cum = np.zeros(cfgs.n, dtype=np.int64)
+    cumw = np.zeros(cfgs.n, dtype=np.int64)
+    for k in range(3):
+        present = cfgs.cap[:, k] > 0
+        cum = cum + np.where(present, c[:, k, HIT], 0)
+        cumw = cumw + np.where(present, c[:, k, HIT_W], 0)
+        assert (cum[present] + c[present, k, MISS] == r["n"]).all()
+        assert (cumw[present] + c[present, k, MISS_W] == r["n_w"]).all()
+        absent = ~present
+        assert (c[absent, k] == 0).all()
+
+
+def test_capacity_bounds(full_run):
+    r = full_run
+    c, cfgs = r["counts"][:, 0], r["cfgs"]
+    for k in range(3):
+        present = cfgs.cap[:, k] > 0
+        assert (c[present, k, INS] >= c[present, k, EVICT]).all()
+        resident_w = c[present, k, INS_W] - c[present, k, EVICT_W]
+        assert (resident_w <= cfgs.cap[present, k].astype(np.int64)).all()
+        assert (resident_w <= r["distinct_w"]).all()
+        # each insertion is a miss of that tier's own cache
+        assert (c[present, k, INS] <= r["n"]).all()
+
+
+def test_lru_inclusion(full_run):
+    """Inclusive LRU: hits up to tier k equal hits of one LRU cache of the
+    largest capacity up to k, a non-decreasing function of that capacity;
+    tier k's own misses (its insertions) are the misses of its own capacity."""
+    r = full_run
+    c, cfgs = r["counts"][:, 0], r["cfgs"]
+    lru = (cfgs.policy[:, 0] == tg.POLICY_LRU) & (cfgs.mode == tg.MODE_INCLUSIVE)
+    idx = np.nonzero(lru)[0]
+    hits_at = {}
+    cum = np.zeros(cfgs.n, dtype=np.int64)
+    mx = np.zeros(cfgs.n, dtype=np.int64)
+    for k in range(3):
+        present = cfgs.cap[:, k] > 0
+        cum = cum + np.where(present, c[:, k, HIT], 0)
+        mx = np.where(present, np.maximum(mx, cfgs.cap[:, k].astype(np.int64)), mx)
+        for i in idx[present[idx]]:
+            m = int(mx[i])
+            v = int(cum[i])
+            assert hits_at.setdefault(m, v) == v, f"cfg {i}: hits({m}) {v} != {hits_at[m]}"
+    caps = sorted(hits_at)
+    vals = [hits_at[m] for m in caps]
+    assert all(a <= b for a, b in zip(vals, vals[1:])), "LRU hits must grow with capacity"
+    assert vals[-1] <= r["n"] - r["u"]
+    # own misses of tier k: N - hits(cap_k) wherever hits(cap_k) is known
+    checked = 0
+    for k in range(3):
+        for i in idx[(cfgs.cap[idx, k] > 0)]:
+            ck = int(cfgs.cap[i, k])
+            if ck in hits_at:
+                assert c[i, k, INS] == r["n"] - hits_at[ck]
+                checked += 1
+    assert checked > 1000
+
+
+def test_replayed_closed_caches(full_run):
+    """A FIFO or LFU cache that holds every distinct block misses exactly on
+    first accesses and never evicts."""
+    r = full_run
+    c, cfgs = r["counts"][:, 0], r["cfgs"]
+    rep = cfgs.policy[:, 0] != tg.POLICY_LRU
+    assert rep.sum() == 1000
+    seen = 0
+    for k in range(3):
+        big = rep & (cfgs.cap[:, k].astype(np.int64) >= r["distinct_w"])
+        seen += int(big.sum())
+        assert (c[big, k, INS] == r["u"]).all()
+        assert (c[big, k, INS_W] == r["distinct_w"]).all()
+        assert (c[big, k, EVICT] == 0).all()
+    assert seen > 0
+    # a replayed tier is one cache whatever the configuration around it
+    for pol in (tg.POLICY_FIFO, tg.POLICY_LFU):
+        sel = np.nonzero(cfgs.policy[:, 0] == pol)[0]
+        for k in range(3):
+            own = {}
+            for i in sel:
+                ck = int(cfgs.cap[i, k])
+                if ck == 0:
+                    continue
+                key = tuple(c[i, k, [INS, EVICT, INS_W, EVICT_W]])
+                assert own.setdefault(ck, key) == key
+
+
+def test_objectives_sane(full_run):
+    r = full_run
+    obj = r["obj"]
+    assert np.isfinite(obj).all()
+    assert (obj[:, 0] > 0).all() and (obj[:, 1] > 0).all() and (obj[:, 2] >= 0).all()
+
+
+def _front(obj, seg=None):
+    """Brute-force non-dominated flags (minimise cost, maximise throughput,
+    minimise latency)."""
+    x = np.stack([obj[:, 0], -obj[:, 1], obj[:, 2]], axis=1)
+    n = len(x)
+    keep = np.ones(n, dtype=bool)
+    seg = np.zeros(n, dtype=np.int64) if seg is None else np.asarray(seg, dtype=np.int64)
+    for s in np.unique(seg):
+        ids = np.nonzero(seg == s)[0]
+        xs = x[ids]
+        for b in range(0, len(ids), 512):
+            blk = xs[b:b + 512]
+            le = (xs[None, :, :] <= blk[:, None, :]).all(axis=2)
+            lt = (xs[None, :, :] < blk[:, None, :]).any(axis=2)
+            keep[ids[b:b + 512]] = ~(le & lt).any(axis=1)
+    return keep
+
+
+def test_pareto_fronts(full_run):
+    r = full_run
+    want = _front(r["obj"])
+    assert np.array_equal(r["front"].astype(bool), want)
+    assert r["nfront"] == int(want.sum())
+    want_seg = _front(r["obj"], r["cfgs"].segment)
+    assert np.array_equal(r["front_seg"].astype(bool), want_seg)

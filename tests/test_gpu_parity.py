@@ -219,3 +219,13 @@ def test_replay_chunks(lib, oracle_mod, seed):
     items += [{"cap": (caps[i], caps[i + 2], caps[i + 4]), "policy": p}
               for i in range(4) for p in (1, 2)]
     compare(lib, oracle_mod, t, tg.from_list(items), label=f"chunks{seed}")
+
+
+def test_full_prefix_real_capacities(lib, oracle_mod):
+    """The first 40,000 requests of the full-scale trace (about 1.5e7
+    accesses) with configurations drawn from the full grid at their real
+    capacities: LRU, FIFO and LFU tiers that do evict."""
+    t = tg.full(n_req=40000)
+    cfgs = tg.configs_for("full", t)
+    pick = np.concatenate([np.arange(0, 10000, 1251), np.arange(10000, 11000, 125)])
+    compare(lib, oracle_mod, t, cfgs.subset(pick), label="full-prefix")
