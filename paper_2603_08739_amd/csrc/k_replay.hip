@@ -791,7 +791,7 @@ template <int NT>
 __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
                                          uint32_t* __restrict__ cnt, const Classes& cl,
                                          GroupCounters& gc, LfuLds& S,
-                                         uint64_t* __restrict__ bits, uint64_t c0, uint64_t c1,
+                                         uint64_t* __restrict__ bits, uint32_t c0, uint32_t c1,
                                          bool g1, uint32_t g0, BlockAny& block_any,
                                          bool have_pref, const uint32_t* pk, const uint32_t* pf,
                                          uint32_t* nk, uint32_t* nf) {
@@ -799,13 +799,16 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   constexpr int CPT = (kCand + kRChunk) / NT;    // queue entries per thread
   const uint32_t tid = threadIdx.x;
   const uint32_t o = j.order;
-  const uint32_t L = (uint32_t)(c1 - c0);
+  // positions fit in 32 bits (n <= 2^29), as do the capacities of replayed
+  // jobs (below the trace's distinct weight, itself below 2^32)
+  const uint32_t jb = (uint32_t)j.begin, je = (uint32_t)j.end, jw0 = (uint32_t)j.word0;
+  const uint32_t L = c1 - c0;
   const uint32_t l0 = tid * IT;
-  const uint64_t p0 = c0 + l0;
+  const uint32_t p0 = c0 + l0;
   RCLK(t_a);
   bool v[IT];
 #pragma unroll
-  for (int e = 0; e < IT; ++e) v[e] = l0 + e < L && p0 + e >= j.begin;
+  for (int e = 0; e < IT; ++e) v[e] = l0 + e < L && p0 + e >= jb;
   const bool all = v[0] && v[IT - 1];
   uint32_t ww[IT], gg[IT], kk[IT], nx[IT], f0[IT];
   bool cm[IT], res0[IT];
@@ -828,22 +831,21 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   uint32_t s0[IT];
 #pragma unroll
   for (int e = 0; e < IT; ++e) {
-    const bool old_prev = v[e] && kk[e] != 0 && (uint64_t)(kk[e] - 1) < c0;
-    s0[e] = have_pref ? pf[e] : (old_prev ? cnt[kk[e] - 1 - j.begin] : 0u);
+    const bool old_prev = v[e] && kk[e] != 0 && kk[e] - 1 < c0;
+    s0[e] = have_pref ? pf[e] : (old_prev ? cnt[kk[e] - 1 - jb] : 0u);
   }
 #pragma unroll
   for (int e = 0; e < IT; ++e) {
     const uint32_t loc = l0 + e;
-    const int lp = (kk[e] != 0 && (uint64_t)(kk[e] - 1) >= c0) ? (int)((uint64_t)(kk[e] - 1) - c0)
-                                                               : -1;
-    const bool again = v[e] && nx[e] != kNone && (uint64_t)nx[e] < c1;
+    const int lp = (kk[e] != 0 && kk[e] - 1 >= c0) ? (int)(kk[e] - 1 - c0) : -1;
+    const bool again = v[e] && nx[e] != kNone && nx[e] < c1;
     // the block's count at the chunk start (first accesses only)
     f0[e] = (v[e] && kk[e] != 0 && lp < 0) ? lfu_live_count(s0[e], kk[e] - 1, h) : 0u;
     res0[e] = f0[e] != 0;
     cm[e] = v[e] && lp < 0 && !res0[e];
     S.lp[loc] = (int16_t)lp;
     S.occ[loc] = lp >= 0 ? 1 : 0;
-    S.nxloc[loc] = again ? (uint16_t)((uint64_t)nx[e] - c0) : kInf16;
+    S.nxloc[loc] = again ? (uint16_t)(nx[e] - c0) : kInf16;
     S.pw[loc] = (uint8_t)ww[e];
     S.capm[loc] = 0;
     S.mskip[loc] = again ? 1 : 0;
@@ -859,13 +861,16 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   uint32_t itot0, nm0, wpre0, mpre0;
   block_excl_scan2_u32<NT>(x, xc, S.red, wpre0, mpre0, itot0, nm0);
   const uint64_t used0 = S.used;
-  const uint64_t ev0 = (used0 + itot0 > j.cap) ? used0 + itot0 - j.cap : 0ull;
+  // evictions the chunk needs never exceed its insertions (used0 <= cap)
+  const uint32_t ev0 = (used0 + itot0 > j.cap) ? (uint32_t)(used0 + itot0 - j.cap) : 0u;
+  // used0 - cap, clamped so that adding a chunk's miss weight stays in 32 bits
+  const int32_t room = (int32_t)max<int64_t>((int64_t)used0 - (int64_t)j.cap, -(1ll << 30));
   if (ev0 > 0) {
 #pragma unroll
     for (int e = 0; e < IT; ++e) {
       if (cm[e]) {
         wpre0 += ww[e];
-        const int64_t need = (int64_t)(used0 + wpre0) - (int64_t)j.cap;
+        const int32_t need = room + (int32_t)wpre0;
         S.mpos[mpre0] = (uint16_t)(l0 + e);
         S.mneed[mpre0] = need > 0 ? (uint32_t)need : 0u;
         ++mpre0;
@@ -879,16 +884,16 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     // arrays' readable slack; whatever lies outside the job (or past n, where
     // the slack holds no block ids) becomes block 0, a valid index for the
     // state gather below.
-    const uint64_t pnext = c0 + kRChunk + l0;
-    const uint64_t pn = min<uint64_t>(pnext, a.n & ~3ull);
+    const uint32_t pnext = c0 + kRChunk + l0;
+    const uint32_t pn = min<uint32_t>(pnext, (uint32_t)a.n & ~3u);
 #pragma unroll
     for (int q = 0; q < IT / 4; ++q) {
       const uint4 x = *reinterpret_cast<const uint4*>(a.key[o] + pn + 4 * q);
       const uint32_t xv[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const uint64_t pe = pnext + 4 * q + r;
-        nk[4 * q + r] = (pn == pnext && pe >= j.begin && pe < j.end) ? xv[r] : 0u;
+        const uint32_t pe = pnext + 4 * q + r;
+        nk[4 * q + r] = (pn == pnext && pe >= jb && pe < je) ? xv[r] : 0u;
       }
     }
   }
@@ -901,24 +906,24 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     uint32_t n0 = 0;
     uint64_t vw = 0;
     for (;;) {
-      if (vw >= ev0 || (uint64_t)h >= c0 || n0 + NT * kCScan > kCand) break;
+      if (vw >= ev0 || h >= c0 || n0 + NT * kCScan > kCand) break;
       RSTAT(blockIdx.x, kStScanned, 1);
       bool live[kCScan], touched[kCScan];
       uint32_t wq[kCScan], aq[kCScan];
 #pragma unroll
       for (int e = 0; e < kCScan; ++e) {
-        const uint64_t q = (uint64_t)h + tid * kCScan + e;
+        const uint32_t q = h + tid * kCScan + e;
         live[e] = false;
         touched[e] = false;
         aq[e] = kInf16;
         wq[e] = 0;
         if (q < c0) {
-          const uint64_t word = bits[(q >> 6) - j.word0];
+          const uint64_t word = bits[(q >> 6) - jw0];
           const uint32_t nxq = a.nxt[o][q];
           wq[e] = a.w8[o][q];
-          live[e] = !((word >> (q & 63)) & 1ull) && (nxq == kNone || (uint64_t)nxq >= c0);
-          touched[e] = live[e] && nxq != kNone && (uint64_t)nxq < c1;
-          aq[e] = touched[e] ? (uint32_t)((uint64_t)nxq - c0) : kInf16;
+          live[e] = !((word >> (q & 63)) & 1ull) && (nxq == kNone || nxq >= c0);
+          touched[e] = live[e] && nxq != kNone && nxq < c1;
+          aq[e] = touched[e] ? nxq - c0 : kInf16;
         }
       }
       uint32_t cl_ = 0, cw_ = 0;
@@ -941,11 +946,11 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       }
       n0 += cnt_live;
       vw += vsum;
-      h = (uint32_t)min<uint64_t>((uint64_t)h + NT * kCScan, c0);
+      h = min<uint32_t>(h + NT * kCScan, c0);
     }
     __syncthreads();
     nc0 = n0;
-    reached = (uint64_t)h >= c0;
+    reached = h >= c0;
     // positions before the first live entry hold no count-1 member any more
     if (tid == 0) S.head1 = nc0 ? S.cq[0] : h;
   }
@@ -980,7 +985,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       for (int e = 0; e < IT; ++e) {
         if (mi[e]) {
           wpre += ww[e];
-          const int64_t need = (int64_t)(used0 + wpre) - (int64_t)j.cap;
+          const int32_t need = room + (int32_t)wpre;
           S.mpos[mpre] = (uint16_t)(l0 + e);
           S.mneed[mpre] = need > 0 ? (uint32_t)need : 0u;
           ++mpre;
@@ -988,7 +993,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       }
       __syncthreads();
     }
-    const uint64_t evtot = (used0 + itot > j.cap) ? used0 + itot - j.cap : 0ull;
+    const uint32_t evtot = (used0 + itot > j.cap) ? (uint32_t)(used0 + itot - j.cap) : 0u;
     // the eviction queue: nc0 old entries, then the nm insertions of the
     // chunk; thread t holds entries t*qpt .. t*qpt+qpt-1
     const uint32_t nq = nc0 + nm;
@@ -1008,7 +1013,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     }
     uint32_t elig;
     uint32_t run = block_excl_scan_u32<NT>(xs, S.red, elig);
-    bool bad = (uint64_t)elig < evtot;
+    bool bad = elig < evtot;
     // entry k is consumed by the first miss whose demand exceeds the
     // eligible weight queued before k.  Demands and prefixes both rise, so
     // a thread's answers lie between the answers for its first and last
@@ -1022,11 +1027,11 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
 #pragma unroll
         for (int e = 0; e < CPT; ++e) {
           const uint32_t k = (uint32_t)e < qpt ? tid * qpt + e : nq;
-          if (k < nq && qw[e] && (uint64_t)rr < evtot) r_hi = rr;
+          if (k < nq && qw[e] && rr < evtot) r_hi = rr;
           rr += qw[e];
         }
       }
-      const bool active = (uint64_t)r_lo < evtot && tid * qpt < nq;
+      const bool active = r_lo < evtot && tid * qpt < nq;
       uint32_t lo = active ? upper_bound(S.mneed, 0u, nm, r_lo) : 0u;
       const uint32_t hi = active ? upper_bound(S.mneed, lo, nm, r_hi) : 0u;
       uint32_t win[kWin];
@@ -1038,7 +1043,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       for (int e = 0; e < CPT; ++e) {
         const uint32_t k = (uint32_t)e < qpt ? tid * qpt + e : nq;
         evk[e] = kInf16;
-        if (k < nq && qw[e] && (uint64_t)run < evtot) {
+        if (k < nq && qw[e] && run < evtot) {
           uint32_t idx;
           if (inwin) {
             idx = lo;
@@ -1243,7 +1248,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       } else {
         fnew[e] = rf0[e] + oc[e] + 1u;
       }
-      cnt[c0 + loc - j.begin] = fnew[e];
+      cnt[c0 + loc - jb] = fnew[e];
     }
     const uint32_t fo = fin[e] ? rf0[e] : 0u, fn = fnew[e];
 #pragma unroll
@@ -1279,8 +1284,8 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   // job's first slot and ignores it)
 #pragma unroll
   for (int e = 0; e < IT; ++e) {
-    const bool old_prev = nk[e] != 0 && (uint64_t)(nk[e] - 1) < c0 + kRChunk;
-    nf[e] = cnt[old_prev ? nk[e] - 1 - j.begin : 0];
+    const bool old_prev = nk[e] != 0 && nk[e] - 1 < c0 + kRChunk;
+    nf[e] = cnt[old_prev ? nk[e] - 1 - jb : 0];
   }
   // nonempty-class bits of the LDS classes, from the counts
   for (uint32_t f = tid; f < kLdsClass; f += NT) {
@@ -1299,7 +1304,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       gc.evw[g0] += t[3];
     }
     S.used = used0 + itot - t[4];
-    if (t[6]) S.head1 = (uint32_t)(c0 + t[6]);          // last new entry taken + 1
+    if (t[6]) S.head1 = c0 + t[6];          // last new entry taken + 1
     else if (t[5]) S.head1 = S.cq[t[5] - 1] + 1;         // last old entry taken + 1
   }
   __syncthreads();
@@ -1344,8 +1349,8 @@ __device__ __forceinline__ void lfu_chunked(const JobDev& j, const JobArgs& a,
   uint64_t ppos = ~0ull;
   while (pos < j.end) {
     const uint32_t l = (uint32_t)min<uint64_t>(len, j.end - pos);
-    if (lfu_fast<NT>(j, a, cnt, cl, gc, S, bits, pos, pos + l, g1, g0, block_any, ppos == pos, pk,
-                     pf, nk, nf)) {
+    if (lfu_fast<NT>(j, a, cnt, cl, gc, S, bits, (uint32_t)pos, (uint32_t)(pos + l), g1, g0,
+                     block_any, ppos == pos, pk, pf, nk, nf)) {
       ppos = (l == kRChunk) ? pos + l : ~0ull;
 #pragma unroll
       for (int e = 0; e < IT; ++e) {
