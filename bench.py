@@ -44,7 +44,8 @@ WORKLOAD_TEXT = {
 ALGO_BYTES = {
     "load_sort": 18.0,        # read hash 8 + weight 1 + group 1, write prev 4 + next 4
     "stack_local": 5.0,       # read key 4 + weight 1 once for every LRU capacity
-    "replay": 5.0,            # read block id 4 + weight 1 per job-access
+    "replay_lfu": 5.0,        # read block id 4 + weight 1 per LFU job-access
+    "replay_fifo": 5.0,       # read block id 4 + weight 1 per FIFO job-access
 }
 
 
@@ -63,13 +64,14 @@ def parse():
 
 
 def stage_units(stage, n, jobs_accesses):
-    if stage == "replay":
-        return jobs_accesses
+    if stage.startswith("replay_") and stage[7:] in jobs_accesses:
+        return jobs_accesses[stage[7:]]
     return n
 
 
 def replay_job_accesses(cfgs, stats, n):
-    """Accesses walked by replay jobs per step (closed-form jobs excluded)."""
+    """Accesses walked by replay jobs per step (closed-form jobs excluded),
+    per policy: {"fifo": ..., "lfu": ...}."""
     import tracegen as tg
     G = stats.n_groups
     jobs = set()
@@ -84,9 +86,9 @@ def replay_job_accesses(cfgs, stats, n):
                 dw = stats.u_w_g[g] if part else stats.distinct_w
                 if x and x < dw:
                     jobs.add((part, g if part else -1, pol, x))
-    total = 0
-    for (part, g, _, _) in jobs:
-        total += stats.n_g[g] if part else n
+    total = {"fifo": 0, "lfu": 0}
+    for (part, g, pol, _) in jobs:
+        total["lfu" if pol == tg.POLICY_LFU else "fifo"] += stats.n_g[g] if part else n
     return total
 
 

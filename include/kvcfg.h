@@ -211,9 +211,11 @@ const char* kv_last_error(void);
  *   0 load: validation        1 load: radix sort       2 load: links and ids
  *   3 group-partitioned order 4 stack: block matrix    5 stack: in-block sort
  *   6 stack: assembly, bins   7 stack: final depths    8 LRU records
- *   9 replay: job setup       10 replay: jobs          11 replay: combine
- *   12 objectives             13 Pareto filter */
-enum { KV_STAGES = 14 };
+ *   9 replay: job setup       10 replay: LFU jobs      11 replay: combine
+ *   12 objectives             13 Pareto filter         14 replay: FIFO jobs
+ * The replay kernels run on streams of their own, concurrently with the LRU
+ * stages, so stage times may overlap. */
+enum { KV_STAGES = 15 };
 typedef struct kv_timing {
   uint64_t calls[KV_STAGES];
   double ms[KV_STAGES];

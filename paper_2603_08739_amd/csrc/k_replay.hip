@@ -23,6 +23,7 @@
 //        oldest live member.
 #include <cstdio>
 #include <cstring>
+#include <functional>
 #include <map>
 #include <mutex>
 #include <optional>
@@ -1581,11 +1582,11 @@ __global__ __launch_bounds__(256) void k_combine(const RecDev* __restrict__ recs
 
 }  // namespace
 
-// A second stream per device (default priority) with a fork and a join
-// event, created on first use and kept until the process ends.
+// Two more streams per device (default priority) with a fork event and a
+// join event each, created on first use and kept until the process ends.
 struct AuxStream {
-  hipStream_t s = nullptr;
-  hipEvent_t fork = nullptr, join = nullptr;
+  hipStream_t s[2] = {nullptr, nullptr};
+  hipEvent_t fork = nullptr, join[2] = {nullptr, nullptr};
   std::mutex mu;
 };
 
@@ -1597,10 +1598,12 @@ static kv_status aux_stream(AuxStream** out) {
   if (dev < 0 || dev >= 64) return fail(KV_ERR_DEVICE, "device index out of range");
   std::lock_guard<std::mutex> g(mu);
   AuxStream& a = aux[dev];
-  if (!a.s) {
-    KV_HIP(hipStreamCreateWithFlags(&a.s, hipStreamNonBlocking));
+  if (!a.s[0]) {
+    for (int i = 0; i < 2; ++i) {
+      KV_HIP(hipStreamCreateWithFlags(&a.s[i], hipStreamNonBlocking));
+      KV_HIP(hipEventCreateWithFlags(&a.join[i], hipEventDisableTiming));
+    }
     KV_HIP(hipEventCreateWithFlags(&a.fork, hipEventDisableTiming));
-    KV_HIP(hipEventCreateWithFlags(&a.join, hipEventDisableTiming));
   }
   *out = &a;
   return KV_OK;
@@ -1608,7 +1611,7 @@ static kv_status aux_stream(AuxStream** out) {
 
 kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_config* cfg_host,
                      const kv_config* cfg_dev, uint32_t n_cfg, uint64_t* counts,
-                     hipStream_t s) {
+                     hipStream_t s, const std::function<kv_status()>& meanwhile) {
   (void)cfg_dev;
   kv_status st;
   const uint32_t G = t.n_groups;
@@ -1766,39 +1769,47 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
                        bstate.as<uint64_t>(), bcls.as<uint32_t>(), ja);
     KV_HIP(hipGetLastError());
     tm.reset();
-    tm.emplace(kStReplay, s);
-    bool any_fifo = false, any_lfu = false;
-    for (const JobDev& q : jd) {
-      any_fifo |= !q.closed && q.kind != kJobLfu;
-      any_lfu |= !q.closed && q.kind == kJobLfu;
-    }
-    // FIFO and LFU jobs run concurrently: FIFO on a second stream forked
-    // from and joined back into the caller's
-    AuxStream* aux = nullptr;
-    std::unique_lock<std::mutex> lk;
-    if (any_fifo && any_lfu) {
-      if ((st = aux_stream(&aux)) != KV_OK) return st;
-      lk = std::unique_lock<std::mutex>(aux->mu);
-      KV_HIP(hipEventRecord(aux->fork, s));
-      KV_HIP(hipStreamWaitEvent(aux->s, aux->fork, 0));
-    }
-    if (any_fifo) {
-      hipLaunchKernelGGL(k_replay, dim3(nj), dim3(kRNT), 0, aux ? aux->s : s, bj.as<JobDev>(),
-                         ja, bstate.as<uint64_t>(), bbits.as<uint64_t>(),
-                         bjc.as<unsigned long long>());
-      KV_HIP(hipGetLastError());
-    }
-    if (any_lfu) {
-      hipLaunchKernelGGL(k_replay_lfu<kLfuNT>, dim3(nj), dim3(kLfuNT), 0, s, bj.as<JobDev>(), ja,
-                         bstate.as<uint64_t>(), bcls.as<uint32_t>(), bbits.as<uint64_t>(),
-                         bjc.as<unsigned long long>());
-      KV_HIP(hipGetLastError());
-    }
-    if (aux) {
-      KV_HIP(hipEventRecord(aux->join, aux->s));
-      KV_HIP(hipStreamWaitEvent(s, aux->join, 0));
-    }
   }
+  bool any_fifo = false, any_lfu = false;
+  for (const JobDev& q : jd) {
+    any_fifo |= !q.closed && q.kind != kJobLfu;
+    any_lfu |= !q.closed && q.kind == kJobLfu;
+  }
+  // LFU jobs, FIFO jobs and the caller's other work (the LRU stack pass) run
+  // concurrently: the replay kernels on two streams forked from the caller's
+  // and joined back into it before the records are combined
+  AuxStream* aux = nullptr;
+  std::unique_lock<std::mutex> lk;
+  if (any_fifo || any_lfu) {
+    if ((st = aux_stream(&aux)) != KV_OK) return st;
+    lk = std::unique_lock<std::mutex>(aux->mu);
+    KV_HIP(hipEventRecord(aux->fork, s));
+  }
+  if (any_lfu) {
+    KV_HIP(hipStreamWaitEvent(aux->s[0], aux->fork, 0));
+    tm.emplace(kStReplay, aux->s[0]);
+    hipLaunchKernelGGL(k_replay_lfu<kLfuNT>, dim3(nj), dim3(kLfuNT), 0, aux->s[0],
+                       bj.as<JobDev>(), ja, bstate.as<uint64_t>(), bcls.as<uint32_t>(),
+                       bbits.as<uint64_t>(), bjc.as<unsigned long long>());
+    KV_HIP(hipGetLastError());
+    tm.reset();
+    KV_HIP(hipEventRecord(aux->join[0], aux->s[0]));
+  }
+  if (any_fifo) {
+    KV_HIP(hipStreamWaitEvent(aux->s[1], aux->fork, 0));
+    tm.emplace(kStReplayFifo, aux->s[1]);
+    hipLaunchKernelGGL(k_replay, dim3(nj), dim3(kRNT), 0, aux->s[1], bj.as<JobDev>(), ja,
+                       bstate.as<uint64_t>(), bbits.as<uint64_t>(),
+                       bjc.as<unsigned long long>());
+    KV_HIP(hipGetLastError());
+    tm.reset();
+    KV_HIP(hipEventRecord(aux->join[1], aux->s[1]));
+  }
+  const kv_status st_mid = meanwhile();
+  if (any_lfu) KV_HIP(hipStreamWaitEvent(s, aux->join[0], 0));
+  if (any_fifo) KV_HIP(hipStreamWaitEvent(s, aux->join[1], 0));
+  lk = std::unique_lock<std::mutex>();
+  if (st_mid != KV_OK) return st_mid;
 #ifdef KV_REPLAY_STATS
   {
     KV_HIP(hipStreamSynchronize(s));

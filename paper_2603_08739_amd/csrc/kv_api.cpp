@@ -420,24 +420,28 @@ kv_status kv_eval_configs(const kv_trace* h, const kv_config* cfg, uint32_t n_cf
   const kv_config* cfg_dev = bcfg.as<kv_config>();
 
   // ---- LRU: stack-distance passes + closed forms
-  OrderView vsh, vpt;
-  if (need_shared) {
-    finish_set(t->shared_ts, tsh, G);
-    if ((st = run_stack(*t, t->shared, false, t->shared_ts, StackSlot{5, 6}, vsh, s)) != KV_OK)
-      return st;
-  }
-  if (need_part) {
-    finish_set(t->part_ts, tpt, G);
-    if ((st = run_stack(*t, t->part, true, t->part_ts, StackSlot{7, 8}, vpt, s)) != KV_OK)
-      return st;
-  }
-  if (need_shared || need_part) {
-    if ((st = lru_counts(cfg_dev, n_cfg, G, vsh, vpt, bgs.as<GroupStats>(), counts, s)) != KV_OK)
-      return st;
-  }
-  // ---- FIFO / LFU: replay jobs
+  auto lru = [&]() -> kv_status {
+    kv_status r;
+    OrderView vsh, vpt;
+    if (need_shared) {
+      finish_set(t->shared_ts, tsh, G);
+      if ((r = run_stack(*t, t->shared, false, t->shared_ts, StackSlot{5, 6}, vsh, s)) != KV_OK)
+        return r;
+    }
+    if (need_part) {
+      finish_set(t->part_ts, tpt, G);
+      if ((r = run_stack(*t, t->part, true, t->part_ts, StackSlot{7, 8}, vpt, s)) != KV_OK)
+        return r;
+    }
+    if (need_shared || need_part)
+      return lru_counts(cfg_dev, n_cfg, G, vsh, vpt, bgs.as<GroupStats>(), counts, s);
+    return KV_OK;
+  };
+  // ---- FIFO / LFU: replay jobs, with the LRU work running meanwhile
   if (!jobs.empty()) {
-    if ((st = replay_run(*t, jobs, cfg, cfg_dev, n_cfg, counts, s)) != KV_OK) return st;
+    if ((st = replay_run(*t, jobs, cfg, cfg_dev, n_cfg, counts, s, lru)) != KV_OK) return st;
+  } else if ((st = lru()) != KV_OK) {
+    return st;
   }
   // ---- objectives
   if (obj) {

@@ -6,6 +6,7 @@
 
 #include <cstdint>
 #include <string>
+#include <functional>
 #include <vector>
 
 #include "../../include/kvcfg.h"
@@ -101,7 +102,7 @@ constexpr uint64_t kDeadMagic = 0x646561646b766366ull;
 enum Stage {
   kStLoadValidate = 0, kStLoadSort, kStLoadLinks, kStPartition, kStStackMatrix,
   kStStackLocal, kStStackAssemble, kStStackFinal, kStLruCounts, kStReplayInit, kStReplay,
-  kStCombine, kStObjectives, kStPareto
+  kStCombine, kStObjectives, kStPareto, kStReplayFifo
 };
 // Records an event pair around a scope when timing is enabled.
 struct StageTimer {
@@ -162,8 +163,11 @@ struct ReplayJob {
   uint64_t cap;       // granules
   uint64_t begin, end;  // positions [begin, end) in the order
 };
+// Replays FIFO/LFU jobs on two forked streams; `meanwhile` enqueues other
+// work on s (it runs concurrently), then the streams are joined and the
+// per-configuration records are combined on s.
 kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_config* cfg_host,
                      const kv_config* cfg_dev, uint32_t n_cfg, uint64_t* counts,
-                     hipStream_t s);
+                     hipStream_t s, const std::function<kv_status()>& meanwhile);
 
 }  // namespace kv

@@ -53,10 +53,10 @@ class kv_cost_model(ctypes.Structure):
                 ("ssd_bw_max", _f64), ("t_prefill_per_token", _f64)]
 
 
-KV_STAGES = 14
+KV_STAGES = 15
 STAGE_NAMES = ("load_validate", "load_sort", "load_links", "partition", "stack_matrix",
                "stack_local", "stack_assemble", "stack_final", "lru_counts", "replay_init",
-               "replay", "replay_combine", "objectives", "pareto")
+               "replay_lfu", "replay_combine", "objectives", "pareto", "replay_fifo")
 
 
 class kv_timing(ctypes.Structure):
