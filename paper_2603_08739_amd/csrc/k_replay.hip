@@ -61,7 +61,7 @@ struct JobArgs {
   uint64_t u;           // distinct blocks
   uint64_t n;           // accesses per order; arrays hold 16 readable bytes past n
   uint32_t n_groups;
-  uint32_t n_class;     // LFU classes per job (max multiplicity + 2)
+  uint32_t n_class;     // LFU class heads per job (kLdsClass)
 };
 
 constexpr int kRNT = 1024;                 // threads of a replay workgroup
@@ -72,8 +72,16 @@ constexpr uint32_t kCand = 4096;           // LFU eviction candidates per chunk
 constexpr int kCScan = 2;                  // candidate positions per thread and pass
 constexpr uint32_t kMinFast = 256;         // shorter LFU chunks go serial
 constexpr uint16_t kInf16 = 0xFFFF;
-constexpr int kLfuNT = 512;                // threads of an LFU replay workgroup
-constexpr uint32_t kLdsClass = 1024;       // LFU count classes held in LDS
+#ifndef KV_LFU_NT
+#define KV_LFU_NT 1024
+#endif
+constexpr int kLfuNT = KV_LFU_NT;           // threads of an LFU replay workgroup
+#ifndef KV_LFU_CHUNK
+#define KV_LFU_CHUNK 4096
+#endif
+constexpr uint32_t kLChunk = KV_LFU_CHUNK;  // longest LFU chunk
+constexpr uint32_t kLdsClass = 1024;       // LFU count classes (held in LDS)
+constexpr uint32_t kTopClass = kLdsClass - 1;  // the class of every count >= kTopClass
 constexpr uint32_t kLdsClassWords = kLdsClass / 64;
 static_assert(kRIt == 4, "hit words are assembled from four ballots");
 
@@ -128,14 +136,11 @@ __global__ __launch_bounds__(256) void k_replay_init(const JobDev* __restrict__ 
       st[b] = kNoIns;
   }
   if (j.policy == KV_POLICY_LFU) {
-    // head[n_class] u32 | cnt[n_class] u32
+    // head[n_class] u32
     uint32_t* head = cls + j.class_off;
-    uint32_t* cnt = head + a.n_class;
     for (uint32_t f = blockIdx.x * blockDim.x + threadIdx.x; f < a.n_class;
-         f += gridDim.x * blockDim.x) {
+         f += gridDim.x * blockDim.x)
       head[f] = (uint32_t)j.begin;
-      cnt[f] = 0;
-    }
   }
 }
 
@@ -569,22 +574,24 @@ __device__ __forceinline__ void fifo_serial(const JobDev& j, const JobArgs& a,
 // scanned by a head pointer head[f].  Class 1 loses members oldest first, so
 // a count-1 block whose latest access lies before head[1] has been evicted:
 // those evictions need no store at all.  Member counts and a nonempty-class
-// bitmap locate the lowest nonempty class; classes below kLdsClass keep them
-// in LDS (the workgroup owns its job for the whole replay), higher ones in
-// HBM.
+// bitmap, in LDS (the workgroup owns its job for the whole replay), locate
+// the lowest nonempty class.  Counts from kTopClass up share the top class:
+// only when it is the lowest nonempty one (every resident block was touched
+// over a thousand times while cached) is its victim needed, and then a scan
+// of the job's positions finds the least (count, latest access).
 // ---------------------------------------------------------------------------
 struct LfuLds {
   // per access of the chunk (local position)
-  int16_t lp[kRChunk];        // previous touch in the chunk; pointer-jumped to the chain root
-  uint16_t occ[kRChunk];      // earlier touches of the same block inside the chunk
-  int16_t lmiss[kRChunk];     // latest miss of the block at or before this touch
-  uint16_t nxloc[kRChunk];    // next touch in the chunk or kInf16
-  uint8_t pw[kRChunk];        // weight
-  uint8_t capm[kRChunk];      // stamp of the iteration that found a capacity miss here
-  uint8_t mskip[kRChunk];     // the entry inserted here is promoted before its eviction
-  uint8_t mcons[kRChunk];     // the entry inserted here is evicted inside the chunk
-  uint16_t mpos[kRChunk];     // misses in order: local position
-  uint32_t mneed[kRChunk];    // ...and the weight that must have left the cache by then
+  int16_t lp[kLChunk];        // previous touch in the chunk; pointer-jumped to the chain root
+  uint16_t occ[kLChunk];      // earlier touches of the same block inside the chunk
+  int16_t lmiss[kLChunk];     // latest miss of the block at or before this touch
+  uint16_t nxloc[kLChunk];    // next touch in the chunk or kInf16
+  uint8_t pw[kLChunk];        // weight
+  uint8_t capm[kLChunk];      // stamp of the iteration that found a capacity miss here
+  uint8_t mskip[kLChunk];     // the entry inserted here is promoted before its eviction
+  uint8_t mcons[kLChunk];     // the entry inserted here is evicted inside the chunk
+  uint16_t mpos[kLChunk];     // misses in order: local position
+  uint32_t mneed[kLChunk];    // ...and the weight that must have left the cache by then
   // count-1 residents from before the chunk, oldest first
   uint32_t cq[kCand];         // position of their last touch
   uint16_t ca[kCand];         // first touch inside the chunk or kInf16
@@ -610,53 +617,40 @@ __device__ __forceinline__ uint32_t lfu_live_count(uint32_t c, uint64_t q, uint6
 }
 
 struct Classes {
-  uint32_t* lcnt;   // LDS counts, classes < kLdsClass
-  uint64_t* lnz;    // LDS bitmap words, classes < kLdsClass
-  uint32_t* gcnt;   // HBM counts (classes >= kLdsClass)
-  uint32_t nclass;  // classes in all
+  uint32_t* lcnt;   // LDS member counts per class
+  uint64_t* lnz;    // LDS nonempty-class bitmap words
 };
 
-// Lowest nonempty class >= f.  Classes >= kLdsClass (blocks touched over a
-// thousand times while cached) are looked up by their counts; the search
-// reaches them only when every lower class is empty.
+// The class of a block of in-cache count f.
+__device__ __forceinline__ uint32_t class_of(uint32_t f) { return min(f, kTopClass); }
+
+// Lowest nonempty class >= f.
 __device__ __forceinline__ uint32_t next_class(const Classes& c, uint32_t f) {
   for (uint32_t wi = f >> 6; wi < kLdsClassWords; ++wi) {
     uint64_t m = c.lnz[wi];
     if (wi == (f >> 6)) m &= ~0ull << (f & 63);
     if (m) return (wi << 6) + (uint32_t)__ffsll((long long)m) - 1u;
   }
-  for (uint32_t g = max(f, kLdsClass); g < c.nclass; ++g)
-    if (ld_acq(&c.gcnt[g]) != 0u) return g;
   return 0xFFFFFFFFu;
 }
 
 __device__ __forceinline__ uint32_t class_count(const Classes& c, uint32_t f) {
-  return f < kLdsClass ? c.lcnt[f] : ld_acq(&c.gcnt[f]);
+  return c.lcnt[f];
 }
 
 // Serial update by one thread (the others wait at a barrier).
 __device__ __forceinline__ void class_add1(const Classes& c, uint32_t f, int d) {
-  if (f < kLdsClass) {
-    const uint64_t bit = 1ull << (f & 63);
-    if (d > 0) {
-      if (c.lcnt[f]++ == 0u) c.lnz[f >> 6] |= bit;
-    } else {
-      if (--c.lcnt[f] == 0u) c.lnz[f >> 6] &= ~bit;
-    }
-  } else if (d > 0) {
-    atomicAdd(&c.gcnt[f], 1u);
+  const uint64_t bit = 1ull << (f & 63);
+  if (d > 0) {
+    if (c.lcnt[f]++ == 0u) c.lnz[f >> 6] |= bit;
   } else {
-    atomicSub(&c.gcnt[f], 1u);
+    if (--c.lcnt[f] == 0u) c.lnz[f >> 6] &= ~bit;
   }
 }
 
 // Concurrent count update; bitmap words are rebuilt afterwards.
 __device__ __forceinline__ void class_add_par(const Classes& c, uint32_t f, int d) {
-  if (f < kLdsClass) {
-    if (d > 0) atomicAdd(&c.lcnt[f], 1u); else atomicSub(&c.lcnt[f], 1u);
-  } else {
-    if (d > 0) atomicAdd(&c.gcnt[f], 1u); else atomicSub(&c.gcnt[f], 1u);
-  }
+  if (d > 0) atomicAdd(&c.lcnt[f], 1u); else atomicSub(&c.lcnt[f], 1u);
 }
 
 // Exact replay of [p0, p1) by one thread (thread 0); returns false if the
@@ -683,24 +677,41 @@ __device__ __forceinline__ bool lfu_serial_range(const JobDev& j, const JobArgs&
       if (f) {
         word |= 1ull << (i & 63);
         const uint32_t f1 = f + 1;
-        class_add1(cl, f, -1);
-        class_add1(cl, f1, +1);
-        if (f == fmin && class_count(cl, f) == 0) fmin = f1;
+        const uint32_t cf = class_of(f), cf1 = class_of(f1);
+        if (cf != cf1) {
+          class_add1(cl, cf, -1);
+          class_add1(cl, cf1, +1);
+          if (cf == fmin && class_count(cl, cf) == 0) fmin = cf1;
+        }
         cnt[i - b0] = f1;
       } else {
         while (used + w > j.cap) {
-          uint64_t q = head[fmin];
-          // the oldest live member of class fmin lies before position i; the
-          // bound only guards against corrupted state
-          for (; q < i; ++q) {
-            const uint32_t nq = nxt[q];
-            if (cnt[q - b0] == fmin && (nq == kNone || nq >= i)) break;
+          uint64_t q;
+          if (fmin < kTopClass) {
+            // the oldest live member of class fmin lies before position i;
+            // the bound only guards against corrupted state
+            for (q = head[fmin]; q < i; ++q) {
+              const uint32_t nq = nxt[q];
+              if (cnt[q - b0] == fmin && (nq == kNone || nq >= i)) break;
+            }
+          } else {
+            // top class: the least count, then the earliest latest access
+            uint32_t best = 0xFFFFFFFFu;
+            q = i;
+            for (uint64_t r = b0; r < i; ++r) {
+              const uint32_t c = cnt[r - b0];
+              if (c < kTopClass || c >= best) continue;
+              const uint32_t nr = nxt[r];
+              if (nr != kNone && nr < i) continue;
+              best = c;
+              q = r;
+            }
           }
           if (q >= i) {
             ok = false;
             break;
           }
-          head[fmin] = (uint32_t)(q + 1);
+          if (fmin < kTopClass) head[fmin] = (uint32_t)(q + 1);
           cnt[q - b0] = 0;
           const uint32_t vw = a.w8[o][q], vg = a.g8[o][q];
           used -= vw;
@@ -796,8 +807,9 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
                                          bool g1, uint32_t g0, BlockAny& block_any,
                                          bool have_pref, const uint32_t* pk, const uint32_t* pf,
                                          uint32_t* nk, uint32_t* nf) {
-  constexpr int IT = kRChunk / NT;               // accesses per thread
-  constexpr int CPT = (kCand + kRChunk) / NT;    // queue entries per thread
+  constexpr int IT = kLChunk / NT;               // accesses per thread
+  constexpr int CPT = (kCand + kLChunk) / NT;    // queue entries per thread
+  static_assert(IT % 4 == 0 && IT <= 64, "accesses are loaded four at a time");
   const uint32_t tid = threadIdx.x;
   const uint32_t o = j.order;
   // positions fit in 32 bits (n <= 2^29), as do the capacities of replayed
@@ -885,7 +897,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     // arrays' readable slack; whatever lies outside the job (or past n, where
     // the slack holds no block ids) becomes block 0, a valid index for the
     // state gather below.
-    const uint32_t pnext = c0 + kRChunk + l0;
+    const uint32_t pnext = c0 + kLChunk + l0;
     const uint32_t pn = min<uint32_t>(pnext, (uint32_t)a.n & ~3u);
 #pragma unroll
     for (int q = 0; q < IT / 4; ++q) {
@@ -1188,6 +1200,8 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     if (untouched) ++p_n1;  // not touched again in the chunk: leaves class 1 for good
                             // (head1 passes it: no store)
   }
+  RCLK(t_e1);
+  RTIME(kStT6, t_e, t_e1);
   // per-access chunk data, loaded for all items at once
   uint32_t mc[IT], nxl[IT], lm[IT], oc[IT];
 #pragma unroll
@@ -1232,6 +1246,8 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       p_lastm = max(p_lastm, loc + 1);
     }
   }
+  RCLK(t_e2);
+  RTIME(kStT7, t_e1, t_e2);
   // final state of every touched block, at its last touch.  Moves into and
   // out of classes 1 and 2 (the crowded ones) add up per wavefront by
   // ballot; the others go one by one.
@@ -1256,9 +1272,14 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     for (int c = 0; c < 2; ++c)
       d12[c] += __popcll(__ballot(fn == (uint32_t)(c + 1))) -
                 __popcll(__ballot(fo == (uint32_t)(c + 1)));
-    if (fo > 2) class_add_par(cl, fo, -1);
-    if (fn > 2) class_add_par(cl, fn, +1);
+    const uint32_t co = class_of(fo), cn = class_of(fn);
+    if (co != cn) {
+      if (fo > 2) class_add_par(cl, co, -1);
+      if (fn > 2) class_add_par(cl, cn, +1);
+    }
   }
+  RCLK(t_e3);
+  RTIME(kStT8, t_e2, t_e3);
   if (lane_id() == 0) {
     if (d12[0]) atomicAdd(&S.ccnt[1], (uint32_t)d12[0]);
     if (d12[1]) atomicAdd(&S.ccnt[2], (uint32_t)d12[1]);
@@ -1285,7 +1306,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   // job's first slot and ignores it)
 #pragma unroll
   for (int e = 0; e < IT; ++e) {
-    const bool old_prev = nk[e] != 0 && nk[e] - 1 < c0 + kRChunk;
+    const bool old_prev = nk[e] != 0 && nk[e] - 1 < c0 + kLChunk;
     nf[e] = cnt[old_prev ? nk[e] - 1 - jb : 0];
   }
   // nonempty-class bits of the LDS classes, from the counts
@@ -1330,8 +1351,6 @@ __device__ __forceinline__ void lfu_chunked(const JobDev& j, const JobArgs& a,
   Classes cl;
   cl.lcnt = S.ccnt;
   cl.lnz = S.cnz;
-  cl.gcnt = head + a.n_class;
-  cl.nclass = a.n_class;
   for (uint32_t f = tid; f < kLdsClass; f += NT) S.ccnt[f] = 0;
   if (tid < kLdsClassWords) S.cnz[tid] = 0;
   if (tid < 2) S.anyflag[tid] = 0;
@@ -1345,14 +1364,14 @@ __device__ __forceinline__ void lfu_chunked(const JobDev& j, const JobArgs& a,
   __syncthreads();
   uint64_t pos = j.begin & ~63ull;
   uint32_t len = j.chunk;
-  constexpr int IT = kRChunk / NT;
+  constexpr int IT = kLChunk / NT;
   uint32_t pk[IT], pf[IT], nk[IT], nf[IT];  // prefetched links and counts of the chunk at ppos
   uint64_t ppos = ~0ull;
   while (pos < j.end) {
     const uint32_t l = (uint32_t)min<uint64_t>(len, j.end - pos);
     if (lfu_fast<NT>(j, a, cnt, cl, gc, S, bits, (uint32_t)pos, (uint32_t)(pos + l), g1, g0,
                      block_any, ppos == pos, pk, pf, nk, nf)) {
-      ppos = (l == kRChunk) ? pos + l : ~0ull;
+      ppos = (l == kLChunk) ? pos + l : ~0ull;
 #pragma unroll
       for (int e = 0; e < IT; ++e) {
         pk[e] = nk[e];
@@ -1617,8 +1636,8 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
   const uint32_t G = t.n_groups;
   const uint64_t n = t.n;
   const uint64_t nwords = (n + 63) / 64;
-  const uint32_t n_class = (uint32_t)std::min<uint64_t>(t.st.max_multiplicity + 2, 0xFFFFFFF0ull);
-  const uint32_t class_words = 2 * n_class;  // u32 words per LFU job: heads, counts
+  const uint32_t n_class = kLdsClass;
+  const uint32_t class_words = n_class;  // u32 words per LFU job: class heads
   // layout of job state, class arrays and bitmaps
   std::vector<JobDev> jd(jobs.size());
   uint64_t state_words = 0, class_total = 0, bit_words = 0;
@@ -1639,7 +1658,7 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
       j.chunk = (uint32_t)std::max<uint64_t>(lc, 64);
     } else {
       j.kind = kJobLfu;
-      j.chunk = kRChunk;
+      j.chunk = kLChunk;
     }
     if (!r.closed && r.end > r.begin) {
       j.state_off = state_words;

@@ -221,6 +221,45 @@ def test_replay_chunks(lib, oracle_mod, seed):
     compare(lib, oracle_mod, t, tg.from_list(items), label=f"chunks{seed}")
 
 
+def _hot_sequence(rng, n_phases, keep):
+    """Phases that each bring in a new block and touch it many times (counts
+    on both sides of a thousand), with re-touches of recent blocks between."""
+    seq, recent = [], []
+    for label in range(n_phases):
+        m = int(rng.choice([1, 2, 40, 1021, 1022, 1023, 1024, 1025, 1400]))
+        for _ in range(m):
+            seq.append(label)
+            if recent and rng.random() < 0.25:
+                seq.append(int(rng.choice(recent)))
+        recent = (recent + [label])[-keep:]
+    return seq
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_lfu_hot_blocks(lib, oracle_mod, seed):
+    """LFU caches whose residents were all touched over a thousand times
+    while cached: a miss must then evict the least count among them, ties to
+    the earliest latest access."""
+    rng = np.random.default_rng(300 + seed)
+    seq = _hot_sequence(rng, 36, keep=3 + seed)
+    weights = None if seed == 0 else rng.choice([1, 3], size=64)
+    t = tg.from_blocks(seq, weights=weights)
+    u = 1 if weights is None else 3   # no tier may be smaller than a block
+    caps = [u * c for c in (1, 2, 3, 4, 5, 6, 9, 12)]
+    items = [{"cap": (c, 0, 0), "policy": p} for c in caps for p in (1, 2)]
+    items += [{"cap": (2 * u, 3 * u, 5 * u), "policy": 2},
+              {"cap": (u, 4 * u, 6 * u), "policy": 2}]
+    compare(lib, oracle_mod, t, tg.from_list(items), label=f"hot{seed}")
+    if seed == 0:
+        # two residents at count 1100: the earlier latest access goes first;
+        # then counts 1500 against 1024
+        hand = [0] * 1100 + [1] * 1100 + [2] + [1] * 400 + [3] + [4] * 1024 + [5] + [1] + [6]
+        cases = [{"cap": (c, 0, 0), "policy": 2} for c in (1, 2, 3)]
+        counts, _, _ = compare(lib, oracle_mod, tg.from_blocks(hand), tg.from_list(cases),
+                               label="hot-hand")
+        assert counts[1, 0, 0, 3] == 5   # cap 2: a victim at each miss from block 2 on
+
+
 def test_full_prefix_real_capacities(lib, oracle_mod):
     """The first 40,000 requests of the full-scale trace (about 1.5e7
     accesses) with configurations drawn from the full grid at their real
