@@ -88,17 +88,17 @@ static_assert(kRIt == 4, "hit words are assembled from four ballots");
 // Optional per-job replay statistics (diagnostics build only).
 #ifdef KV_REPLAY_STATS
 enum { kStFastOk = 0, kStFailPool, kStFailElig, kStFailConv, kStSerialAcc, kStIters,
-       kStScanned, kStFastAcc, kStT0, kStT1, kStT2, kStT3, kStT4, kStT5, kStT6, kStT7, kStT8, kStW0, kStW1, kStW2, kStW3, kStats };
+       kStScanned, kStFastAcc, kStT0, kStT1, kStT2, kStT3, kStT4, kStT5, kStT6, kStT7, kStT8, kStW0, kStW1, kStW2, kStW3, kStW4, kStW5, kStW6, kStW7, kStats };
 __device__ unsigned long long g_rstats[256][kStats];
 __shared__ unsigned long long s_rstats[kStats];  // flushed to g_rstats when the job ends
-__shared__ unsigned long long s_rwave[4];
+__shared__ unsigned long long s_rwave[8];
 #define RSTAT(j, k, v) do { if (threadIdx.x == 0) s_rstats[k] += (unsigned long long)(v); } while (0)
 #define RCLK(t) const unsigned long long t = clock64()
 // per chunk, the latest wave's (clock - t0) at this point, summed over chunks
 #define RWAVE(k, t0) do { unsigned long long _d = clock64() - (t0); \
     if (lane_id() == 0) atomicMax(&s_rwave[k], _d); } while (0)
 #define RWAVE_FLUSH() do { __syncthreads(); if (threadIdx.x < 4) { s_rstats[kStT6 + threadIdx.x % 3] += 0; } \
-    if (threadIdx.x == 0) { for (int _q = 0; _q < 4; ++_q) { s_rstats[kStW0 + _q] += s_rwave[_q]; s_rwave[_q] = 0; } } } while (0)
+    if (threadIdx.x == 0) { for (int _q = 0; _q < 8; ++_q) { s_rstats[kStW0 + _q] += s_rwave[_q]; s_rwave[_q] = 0; } } } while (0)
 #define RTIME(k, t0, t1) RSTAT(blockIdx.x, k, (t1) - (t0))
 #else
 #define RSTAT(j, k, v) do { } while (0)
@@ -581,35 +581,72 @@ __device__ __forceinline__ void fifo_serial(const JobDev& j, const JobArgs& a,
 // of the job's positions finds the least (count, latest access).
 // ---------------------------------------------------------------------------
 struct LfuLds {
-  // per access of the chunk (local position)
-  int16_t lp[kLChunk];        // previous touch in the chunk; pointer-jumped to the chain root
-  uint16_t occ[kLChunk];      // earlier touches of the same block inside the chunk
-  int16_t lmiss[kLChunk];     // latest miss of the block at or before this touch
-  uint16_t nxloc[kLChunk];    // next touch in the chunk or kInf16
-  uint8_t pw[kLChunk];        // weight
-  uint8_t capm[kLChunk];      // stamp of the iteration that found a capacity miss here
-  uint8_t mskip[kLChunk];     // the entry inserted here is promoted before its eviction
-  uint8_t mcons[kLChunk];     // the entry inserted here is evicted inside the chunk
-  uint16_t mpos[kLChunk];     // misses in order: local position
-  uint32_t mneed[kLChunk];    // ...and the weight that must have left the cache by then
-  // count-1 residents from before the chunk, oldest first
-  uint32_t cq[kCand];         // position of their last touch
-  uint16_t ca[kCand];         // first touch inside the chunk or kInf16
-  uint8_t cw[kCand];
-  uint8_t cskip[kCand];
-  uint8_t ccons[kCand];
+  // Small fields and the per-access fields of the hot loops come first, so
+  // that they lie within reach of the LDS instructions' 16-bit offsets.
   uint32_t red[2 * kRNW];
   uint32_t sfx[2 * kRNW];
   uint32_t anyflag[2];
   uint32_t tot8[8];           // chunk totals: ins, ins_w, ev, ev_w, victim w, last old, last new, n1
-  uint32_t ccnt[kLdsClass];   // members of class f < kLdsClass
   uint64_t cnz[kLdsClassWords];
   uint64_t used;              // cached weight
   uint32_t fmin, head1;       // lowest nonempty class; no live count-1 member before head1
   uint32_t nc, h;             // candidate scan: entries found, next position
   uint64_t vw;                // candidate scan: untouched weight found
   int ok;
+  // per access of the chunk (local position).  Members of one union serve
+  // the fixed point and the apply step respectively, never both at once.
+  union {
+    struct {                  // fixed point
+      uint8_t pw[kLChunk];    // weight
+      uint8_t capm[kLChunk];  // stamp of the iteration that found a capacity miss here
+      uint8_t mskip[kLChunk]; // the entry inserted here is promoted before its eviction
+    };
+    uint16_t occ[kLChunk];    // apply: earlier touches of the same block inside the chunk
+  };
+  uint8_t mcons[kLChunk];     // the entry inserted here is evicted inside the chunk
+  uint16_t nxloc[kLChunk];    // next touch in the chunk or kInf16
+  int16_t lp[kLChunk];        // previous touch in the chunk; pointer-jumped to the chain root
+  union {
+    uint16_t mpos[kLChunk];   // fixed point: local position of the m-th miss
+    int16_t lmiss[kLChunk];   // apply: latest miss of the block at or before this touch
+  };
+  // fixed point: the weight that must have left the cache by the m-th miss;
+  // apply: a block's count at the chunk start, at its first touch
+  uint32_t mneed[kLChunk];
+  uint32_t ccnt[kLdsClass];   // members of class f < kLdsClass
+  // count-1 residents from before the chunk, oldest first
+  uint8_t cw[kCand];
+  uint8_t cskip[kCand];
+  uint8_t ccons[kCand];
+  uint16_t ca[kCand];         // first touch inside the chunk or kInf16
+  uint32_t cq[kCand];         // position of their last touch
+  // a block's count after its last touch in the chunk (0 elsewhere)
+  alignas(16) uint32_t fnl[kLChunk];
+  // the next full chunk, per access: its block link and the stored count
+  // at that link (each thread reads and writes only its own accesses)
+  alignas(16) uint32_t pkey[kLChunk];
+  alignas(16) uint32_t pcnt[kLChunk];
 };
+
+// A thread's IT consecutive words of an LDS array (16-byte aligned), moved
+// four at a time.
+template <int IT>
+__device__ __forceinline__ void lds_get(const uint32_t* p, uint32_t* v) {
+#pragma unroll
+  for (int q = 0; q < IT / 4; ++q) {
+    const uint4 x = reinterpret_cast<const uint4*>(p)[q];
+    v[4 * q] = x.x;
+    v[4 * q + 1] = x.y;
+    v[4 * q + 2] = x.z;
+    v[4 * q + 3] = x.w;
+  }
+}
+template <int IT>
+__device__ __forceinline__ void lds_put(uint32_t* p, const uint32_t* v) {
+#pragma unroll
+  for (int q = 0; q < IT / 4; ++q)
+    reinterpret_cast<uint4*>(p)[q] = make_uint4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+}
 
 // In-cache count of a block whose latest access is q with stored count c.
 __device__ __forceinline__ uint32_t lfu_live_count(uint32_t c, uint64_t q, uint64_t head1) {
@@ -799,14 +836,15 @@ __device__ __forceinline__ void block_suffix_min_flag(uint32_t v, bool flag, uin
 // by a miss at that position and not touched since, and every such block is
 // still a member (count-1 members only leave by a touch or, oldest first, by
 // eviction, which moves head1 past them).
-template <int NT>
+// G1: every access of the job belongs to group g0 (counters add up per
+// wavefront); otherwise each access's group is read.
+template <int NT, bool G1>
 __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
                                          uint32_t* __restrict__ cnt, const Classes& cl,
                                          GroupCounters& gc, LfuLds& S,
                                          uint64_t* __restrict__ bits, uint32_t c0, uint32_t c1,
-                                         bool g1, uint32_t g0, BlockAny& block_any,
-                                         bool have_pref, const uint32_t* pk, const uint32_t* pf,
-                                         uint32_t* nk, uint32_t* nf) {
+                                         uint32_t g0, BlockAny& block_any, bool have_pref) {
+  constexpr bool g1 = G1;
   constexpr int IT = kLChunk / NT;               // accesses per thread
   constexpr int CPT = (kCand + kLChunk) / NT;    // queue entries per thread
   static_assert(IT % 4 == 0 && IT <= 64, "accesses are loaded four at a time");
@@ -826,38 +864,59 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   uint32_t ww[IT], gg[IT], kk[IT], nx[IT], f0[IT];
   bool cm[IT], res0[IT];
   if (have_pref) {
-#pragma unroll
-    for (int e = 0; e < IT; ++e) kk[e] = pk[e];
+    lds_get<IT>(S.pkey + l0, kk);
   } else {
     loadn_u32<IT>(a.key[o], p0, all, v, kk);
   }
   loadn_u8<IT>(a.w8[o], p0, all, v, ww);
   loadn_u32<IT>(a.nxt[o], p0, all, v, nx);
+  {
+    // the next full chunk's block links.  The read position is clamped to
+    // the arrays' readable slack; whatever lies outside the job (or past n,
+    // where the slack holds no links) becomes 0, no earlier access.
+    const uint32_t pnext = c0 + kLChunk + l0;
+    const uint32_t pn = min<uint32_t>(pnext, (uint32_t)a.n & ~3u);
+    uint32_t nk[IT];
+#pragma unroll
+    for (int q = 0; q < IT / 4; ++q) {
+      const uint4 x = *reinterpret_cast<const uint4*>(a.key[o] + pn + 4 * q);
+      const uint32_t xv[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const uint32_t pe = pnext + 4 * q + r;
+        nk[4 * q + r] = (pn == pnext && pe >= jb && pe < je) ? xv[r] : 0u;
+      }
+    }
+    lds_put<IT>(S.pkey + l0, nk);
+  }
 #pragma unroll
   for (int e = 0; e < IT; ++e) gg[e] = g0;
-  if (!g1) loadn_u8<IT>(a.g8[o], p0, all, v, gg);
+  if constexpr (!G1) loadn_u8<IT>(a.g8[o], p0, all, v, gg);
   uint32_t h = S.head1;
   if (tid < 8) S.tot8[tid] = 0;  // first read after several barriers
   // stored counts at the latest earlier accesses (prefetched by the
   // previous chunk when it covered the whole chunk before this one); only a
   // block's first access in the chunk needs one
   uint32_t s0[IT];
+  if (have_pref) {
+    lds_get<IT>(S.pcnt + l0, s0);
+  } else {
 #pragma unroll
-  for (int e = 0; e < IT; ++e) {
-    const bool old_prev = v[e] && kk[e] != 0 && kk[e] - 1 < c0;
-    s0[e] = have_pref ? pf[e] : (old_prev ? cnt[kk[e] - 1 - jb] : 0u);
+    for (int e = 0; e < IT; ++e) {
+      const bool old_prev = v[e] && kk[e] != 0 && kk[e] - 1 < c0;
+      s0[e] = old_prev ? cnt[kk[e] - 1 - jb] : 0u;
+    }
   }
 #pragma unroll
   for (int e = 0; e < IT; ++e) {
     const uint32_t loc = l0 + e;
     const int lp = (kk[e] != 0 && kk[e] - 1 >= c0) ? (int)(kk[e] - 1 - c0) : -1;
     const bool again = v[e] && nx[e] != kNone && nx[e] < c1;
+    S.lp[loc] = (int16_t)lp;
     // the block's count at the chunk start (first accesses only)
     f0[e] = (v[e] && kk[e] != 0 && lp < 0) ? lfu_live_count(s0[e], kk[e] - 1, h) : 0u;
     res0[e] = f0[e] != 0;
     cm[e] = v[e] && lp < 0 && !res0[e];
-    S.lp[loc] = (int16_t)lp;
-    S.occ[loc] = lp >= 0 ? 1 : 0;
     S.nxloc[loc] = again ? (uint16_t)(nx[e] - c0) : kInf16;
     S.pw[loc] = (uint8_t)ww[e];
     S.capm[loc] = 0;
@@ -872,6 +931,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     xc += cm[e] ? 1u : 0u;
   }
   uint32_t itot0, nm0, wpre0, mpre0;
+  RWAVE(0, t_a);
   block_excl_scan2_u32<NT>(x, xc, S.red, wpre0, mpre0, itot0, nm0);
   const uint64_t used0 = S.used;
   // evictions the chunk needs never exceed its insertions (used0 <= cap)
@@ -892,24 +952,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   }
   RCLK(t_b);
   RTIME(kStT0, t_a, t_b);
-  {
-    // the next full chunk's blocks.  The read position is clamped to the
-    // arrays' readable slack; whatever lies outside the job (or past n, where
-    // the slack holds no block ids) becomes block 0, a valid index for the
-    // state gather below.
-    const uint32_t pnext = c0 + kLChunk + l0;
-    const uint32_t pn = min<uint32_t>(pnext, (uint32_t)a.n & ~3u);
-#pragma unroll
-    for (int q = 0; q < IT / 4; ++q) {
-      const uint4 x = *reinterpret_cast<const uint4*>(a.key[o] + pn + 4 * q);
-      const uint32_t xv[4] = {x.x, x.y, x.z, x.w};
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const uint32_t pe = pnext + 4 * q + r;
-        nk[4 * q + r] = (pn == pnext && pe >= jb && pe < je) ? xv[r] : 0u;
-      }
-    }
-  }
+  RWAVE(1, t_a);
   uint32_t nc0 = 0;
   bool reached = false;
   if (ev0 > 0) {
@@ -969,10 +1012,13 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   }
   RCLK(t_c);
   RTIME(kStT1, t_b, t_c);
+  RWAVE(2, t_a);
   // ---- fixed point over (misses, promotions, evictions)
   uint32_t itot = itot0;
   bool converged = ev0 == 0;
-  uint8_t cur = 0xFF;  // stamp of the latest capacity-miss set (0xFF: none yet)
+  bool capnow[IT];  // capacity misses of the latest iteration
+#pragma unroll
+  for (int e = 0; e < IT; ++e) capnow[e] = false;
   for (int it = 0; !converged && it < 24; ++it) {
     RSTAT(blockIdx.x, kStIters, 1);
     RCLK(t_it);
@@ -987,7 +1033,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       uint32_t xw = 0, xm = 0;
 #pragma unroll
       for (int e = 0; e < IT; ++e) {
-        oldcap[e] = v[e] && S.capm[l0 + e] == cur;
+        oldcap[e] = capnow[e];
         mi[e] = cm[e] || oldcap[e];
         xw += mi[e] ? ww[e] : 0u;
         xm += mi[e] ? 1u : 0u;
@@ -1120,12 +1166,13 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
 #pragma unroll
     for (int e = 0; e < IT; ++e) {
       const uint32_t loc = l0 + e;
-      changed |= oldcap[e] != (v[e] && S.capm[loc] == ns);
+      capnow[e] = v[e] && S.capm[loc] == ns;
+      changed |= oldcap[e] != capnow[e];
       // entries that stopped being misses lose their queue flags (their
       // miss status changed with the capacity misses, counted above)
       if (v[e] && !mi[e] && S.mcons[loc]) S.mcons[loc] = 0;
     }
-    cur = ns;
+    RWAVE(3, t_a);
     if (!block_any(changed)) converged = true;
   }
   if (!converged) {
@@ -1134,15 +1181,30 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   }
   RCLK(t_d);
   RTIME(kStT2, t_c, t_d);
-  // ---- consistent: apply.  Pointer jumping gives each touch the number of
-  // earlier touches of its block in the chunk and the latest miss among them.
+  // ---- consistent: apply.  First the next chunk's stored counts at links
+  // before this chunk (final already; a link inside it reads this chunk's
+  // final counts once they are known).
+  uint32_t nold[IT], nk[IT];
+  lds_get<IT>(S.pkey + l0, nk);
+#pragma unroll
+  for (int e = 0; e < IT; ++e) {
+    const uint32_t k = nk[e];
+    const bool old = k != 0 && k - 1 < c0;
+    nold[e] = cnt[old ? k - 1 - jb : 0];
+    if (!old) nold[e] = 0;
+  }
+  // Pointer jumping gives each touch the number of earlier touches of its
+  // block in the chunk and the latest miss among them.
+  // (The fixed point's fields are dead: its last reads came before the
+  // barrier that ended it.)
   bool miss[IT];
 #pragma unroll
   for (int e = 0; e < IT; ++e) {
     const uint32_t loc = l0 + e;
-    miss[e] = cm[e] || (v[e] && S.capm[loc] == cur);
+    miss[e] = cm[e] || capnow[e];
     S.lmiss[loc] = miss[e] ? (int16_t)loc : (int16_t)-1;
     S.mneed[loc] = f0[e];  // a block's count at the chunk start, read via its first access
+    S.occ[loc] = S.lp[loc] >= 0 ? 1 : 0;
   }
   __syncthreads();
   for (;;) {
@@ -1178,6 +1240,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   }
   RCLK(t_e);
   RTIME(kStT3, t_d, t_e);
+  RWAVE(4, t_a);
   // per-thread partials: insertions, evictions, victim weight, last entries taken
   uint32_t p_ins = 0, p_insw = 0, p_ev = 0, p_evw = 0, p_vw = 0, p_lastp = 0, p_lastm = 0,
            p_n1 = 0;
@@ -1278,6 +1341,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       if (fn > 2) class_add_par(cl, cn, +1);
     }
   }
+  lds_put<IT>(S.fnl + l0, fnew);
   RCLK(t_e3);
   RTIME(kStT8, t_e2, t_e3);
   if (lane_id() == 0) {
@@ -1298,17 +1362,20 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       if (r[7]) atomicSub(&S.ccnt[1], r[7]);
     }
   }
+  RWAVE(5, t_a);
   __syncthreads();
   RCLK(t_f);
   RTIME(kStT4, t_e, t_f);
-  // the next chunk's stored counts, now that this chunk's are stored (an
-  // access with no earlier one, or one inside the next chunk, reads the
-  // job's first slot and ignores it)
+  // the next chunk's stored counts, now that this chunk's are known (only
+  // a link before the next chunk is ever read)
+  uint32_t nf[IT];
 #pragma unroll
   for (int e = 0; e < IT; ++e) {
-    const bool old_prev = nk[e] != 0 && nk[e] - 1 < c0 + kLChunk;
-    nf[e] = cnt[old_prev ? nk[e] - 1 - jb : 0];
+    const uint32_t k = nk[e];
+    const bool here = k != 0 && k - 1 >= c0 && k - 1 < c0 + kLChunk;
+    nf[e] = here ? S.fnl[k - 1 - c0] : nold[e];
   }
+  lds_put<IT>(S.pcnt + l0, nf);
   // nonempty-class bits of the LDS classes, from the counts
   for (uint32_t f = tid; f < kLdsClass; f += NT) {
     const uint64_t bal = __ballot(S.ccnt[f] != 0u);
@@ -1329,6 +1396,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     if (t[6]) S.head1 = c0 + t[6];          // last new entry taken + 1
     else if (t[5]) S.head1 = S.cq[t[5] - 1] + 1;         // last old entry taken + 1
   }
+  RWAVE(6, t_a);
   __syncthreads();
   if (tid == 0) {
     const uint32_t nf = next_class(cl, 1);
@@ -1336,16 +1404,18 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   }
   RCLK(t_g);
   RTIME(kStT5, t_f, t_g);
+  RWAVE(7, t_a);
+  RWAVE_FLUSH();
   RSTAT(blockIdx.x, kStFastOk, 1);
   RSTAT(blockIdx.x, kStFastAcc, L);
   return true;
 }
 
-template <int NT>
+template <int NT, bool G1>
 __device__ __forceinline__ void lfu_chunked(const JobDev& j, const JobArgs& a,
                                             uint32_t* __restrict__ cnt, uint32_t* __restrict__ cls,
                                             uint64_t* __restrict__ bits, GroupCounters& gc,
-                                            LfuLds& S, bool g1, uint32_t g0) {
+                                            LfuLds& S, uint32_t g0) {
   const uint32_t tid = threadIdx.x;
   uint32_t* head = cls + j.class_off;
   Classes cl;
@@ -1365,22 +1435,17 @@ __device__ __forceinline__ void lfu_chunked(const JobDev& j, const JobArgs& a,
   uint64_t pos = j.begin & ~63ull;
   uint32_t len = j.chunk;
   constexpr int IT = kLChunk / NT;
-  uint32_t pk[IT], pf[IT], nk[IT], nf[IT];  // prefetched links and counts of the chunk at ppos
-  uint64_t ppos = ~0ull;
+  uint64_t ppos = ~0ull;  // the chunk whose links and counts are prefetched in LDS
   while (pos < j.end) {
     const uint32_t l = (uint32_t)min<uint64_t>(len, j.end - pos);
-    if (lfu_fast<NT>(j, a, cnt, cl, gc, S, bits, (uint32_t)pos, (uint32_t)(pos + l), g1, g0,
-                     block_any, ppos == pos, pk, pf, nk, nf)) {
+    if (lfu_fast<NT, G1>(j, a, cnt, cl, gc, S, bits, (uint32_t)pos, (uint32_t)(pos + l), g0,
+                         block_any, ppos == pos)) {
       ppos = (l == kLChunk) ? pos + l : ~0ull;
-#pragma unroll
-      for (int e = 0; e < IT; ++e) {
-        pk[e] = nk[e];
-        pf[e] = nf[e];
-      }
       pos += l;
       len = min<uint32_t>(len * 2, j.chunk);
     } else if (l > kMinFast) {
       len = max<uint32_t>(kMinFast, (l / 2) & ~63u);
+      ppos = ~0ull;  // the failed attempt replaced the prefetched links
     } else {
       __syncthreads();
       if (tid == 0) S.ok = lfu_serial_range(j, a, cnt, head, cl, S, gc, bits, pos, pos + l) ? 1 : 0;
@@ -1394,6 +1459,12 @@ __device__ __forceinline__ void lfu_chunked(const JobDev& j, const JobArgs& a,
   __syncthreads();
 }
 
+
+// Whether every access of a job belongs to one group (a partitioned job, or
+// a trace with one group).
+__host__ __device__ __forceinline__ bool lfu_one_group(const JobDev& j, uint32_t n_groups) {
+  return n_groups == 1 || j.group != KV_MAX_GROUPS;
+}
 
 // The job's access order moved to slot 0, so that every pointer is known
 // without indexing (kept in registers).
@@ -1424,7 +1495,7 @@ __global__ __launch_bounds__(kRNT) void k_replay(const JobDev* __restrict__ jobs
   if (tid < KV_MAX_GROUPS) gc.ins[tid] = gc.insw[tid] = gc.ev[tid] = gc.evw[tid] = 0;
 #ifdef KV_REPLAY_STATS
   if (tid < kStats) s_rstats[tid] = 0;
-  if (tid < 4) s_rwave[tid] = 0;
+  if (tid < 8) s_rwave[tid] = 0;
 #endif
   __syncthreads();
   // one group for every access of the job: counters add up per wavefront
@@ -1443,8 +1514,9 @@ __global__ __launch_bounds__(kRNT) void k_replay(const JobDev* __restrict__ jobs
 #endif
 }
 
-// LFU jobs, kLfuNT threads per job.
-template <int NT>
+// LFU jobs, NT threads per job; G1: the jobs whose accesses all belong to
+// one group (the others are left to the G1 = false instance).
+template <int NT, bool G1>
 __global__ __launch_bounds__(NT) void k_replay_lfu(const JobDev* __restrict__ jobs, JobArgs a_in,
                                                    uint64_t* __restrict__ state,
                                                    uint32_t* __restrict__ cls,
@@ -1454,19 +1526,19 @@ __global__ __launch_bounds__(NT) void k_replay_lfu(const JobDev* __restrict__ jo
   __shared__ GroupCounters gc;
   JobDev j = jobs[blockIdx.x];
   if (j.closed || j.kind != kJobLfu) return;
+  if (lfu_one_group(j, a_in.n_groups) != G1) return;
   const JobArgs a = job_args(a_in, j);
   const uint32_t tid = threadIdx.x;
   if (tid < KV_MAX_GROUPS) gc.ins[tid] = gc.insw[tid] = gc.ev[tid] = gc.evw[tid] = 0;
 #ifdef KV_REPLAY_STATS
   if (tid < kStats) s_rstats[tid] = 0;
-  if (tid < 4) s_rwave[tid] = 0;
+  if (tid < 8) s_rwave[tid] = 0;
 #endif
   __syncthreads();
-  const bool g1 = a.n_groups == 1 || j.group != KV_MAX_GROUPS;
   const uint32_t g0 = j.group == KV_MAX_GROUPS ? 0u : j.group;
   unsigned long long* cnt = jcnt + (uint64_t)blockIdx.x * a.n_groups * 4;
-  lfu_chunked<NT>(j, a, reinterpret_cast<uint32_t*>(state + j.state_off), cls, bits + j.bits_off,
-                  gc, lds, g1, g0);
+  lfu_chunked<NT, G1>(j, a, reinterpret_cast<uint32_t*>(state + j.state_off), cls,
+                      bits + j.bits_off, gc, lds, g0);
   const bool ok = lds.ok != 0;
   __syncthreads();
   write_counters(gc, a.n_groups, cnt);
@@ -1603,9 +1675,10 @@ __global__ __launch_bounds__(256) void k_combine(const RecDev* __restrict__ recs
 
 // Two more streams per device (default priority) with a fork event and a
 // join event each, created on first use and kept until the process ends.
+constexpr int kAux = 3;  // LFU one-group jobs, other LFU jobs, FIFO jobs
 struct AuxStream {
-  hipStream_t s[2] = {nullptr, nullptr};
-  hipEvent_t fork = nullptr, join[2] = {nullptr, nullptr};
+  hipStream_t s[kAux] = {};
+  hipEvent_t fork = nullptr, join[kAux] = {};
   std::mutex mu;
 };
 
@@ -1618,7 +1691,7 @@ static kv_status aux_stream(AuxStream** out) {
   std::lock_guard<std::mutex> g(mu);
   AuxStream& a = aux[dev];
   if (!a.s[0]) {
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < kAux; ++i) {
       KV_HIP(hipStreamCreateWithFlags(&a.s[i], hipStreamNonBlocking));
       KV_HIP(hipEventCreateWithFlags(&a.join[i], hipEventDisableTiming));
     }
@@ -1789,44 +1862,48 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
     KV_HIP(hipGetLastError());
     tm.reset();
   }
-  bool any_fifo = false, any_lfu = false;
+  // LFU jobs of one group, other LFU jobs, FIFO jobs and the caller's other
+  // work (the LRU stack pass) run concurrently: the replay kernels on
+  // streams forked from the caller's and joined back into it before the
+  // records are combined
+  bool any[kAux] = {false, false, false};
   for (const JobDev& q : jd) {
-    any_fifo |= !q.closed && q.kind != kJobLfu;
-    any_lfu |= !q.closed && q.kind == kJobLfu;
+    if (q.closed) continue;
+    if (q.kind != kJobLfu) any[2] = true;
+    else if (lfu_one_group(q, G)) any[0] = true;
+    else any[1] = true;
   }
-  // LFU jobs, FIFO jobs and the caller's other work (the LRU stack pass) run
-  // concurrently: the replay kernels on two streams forked from the caller's
-  // and joined back into it before the records are combined
   AuxStream* aux = nullptr;
   std::unique_lock<std::mutex> lk;
-  if (any_fifo || any_lfu) {
+  if (any[0] || any[1] || any[2]) {
     if ((st = aux_stream(&aux)) != KV_OK) return st;
     lk = std::unique_lock<std::mutex>(aux->mu);
     KV_HIP(hipEventRecord(aux->fork, s));
   }
-  if (any_lfu) {
-    KV_HIP(hipStreamWaitEvent(aux->s[0], aux->fork, 0));
-    tm.emplace(kStReplay, aux->s[0]);
-    hipLaunchKernelGGL(k_replay_lfu<kLfuNT>, dim3(nj), dim3(kLfuNT), 0, aux->s[0],
-                       bj.as<JobDev>(), ja, bstate.as<uint64_t>(), bcls.as<uint32_t>(),
-                       bbits.as<uint64_t>(), bjc.as<unsigned long long>());
+  for (int k = 0; k < kAux; ++k) {
+    if (!any[k]) continue;
+    hipStream_t sk = aux->s[k];
+    KV_HIP(hipStreamWaitEvent(sk, aux->fork, 0));
+    tm.emplace(k == 2 ? kStReplayFifo : kStReplay, sk);
+    if (k == 0)
+      hipLaunchKernelGGL((k_replay_lfu<kLfuNT, true>), dim3(nj), dim3(kLfuNT), 0, sk,
+                         bj.as<JobDev>(), ja, bstate.as<uint64_t>(), bcls.as<uint32_t>(),
+                         bbits.as<uint64_t>(), bjc.as<unsigned long long>());
+    else if (k == 1)
+      hipLaunchKernelGGL((k_replay_lfu<kLfuNT, false>), dim3(nj), dim3(kLfuNT), 0, sk,
+                         bj.as<JobDev>(), ja, bstate.as<uint64_t>(), bcls.as<uint32_t>(),
+                         bbits.as<uint64_t>(), bjc.as<unsigned long long>());
+    else
+      hipLaunchKernelGGL(k_replay, dim3(nj), dim3(kRNT), 0, sk, bj.as<JobDev>(), ja,
+                         bstate.as<uint64_t>(), bbits.as<uint64_t>(),
+                         bjc.as<unsigned long long>());
     KV_HIP(hipGetLastError());
     tm.reset();
-    KV_HIP(hipEventRecord(aux->join[0], aux->s[0]));
-  }
-  if (any_fifo) {
-    KV_HIP(hipStreamWaitEvent(aux->s[1], aux->fork, 0));
-    tm.emplace(kStReplayFifo, aux->s[1]);
-    hipLaunchKernelGGL(k_replay, dim3(nj), dim3(kRNT), 0, aux->s[1], bj.as<JobDev>(), ja,
-                       bstate.as<uint64_t>(), bbits.as<uint64_t>(),
-                       bjc.as<unsigned long long>());
-    KV_HIP(hipGetLastError());
-    tm.reset();
-    KV_HIP(hipEventRecord(aux->join[1], aux->s[1]));
+    KV_HIP(hipEventRecord(aux->join[k], sk));
   }
   const kv_status st_mid = meanwhile();
-  if (any_lfu) KV_HIP(hipStreamWaitEvent(s, aux->join[0], 0));
-  if (any_fifo) KV_HIP(hipStreamWaitEvent(s, aux->join[1], 0));
+  for (int k = 0; k < kAux; ++k)
+    if (any[k]) KV_HIP(hipStreamWaitEvent(s, aux->join[k], 0));
   lk = std::unique_lock<std::mutex>();
   if (st_mid != KV_OK) return st_mid;
 #ifdef KV_REPLAY_STATS
@@ -1839,13 +1916,14 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
       fprintf(stderr, "[replay-stats] %s job %u cap %llu: fast %llu (acc %llu) failpool %llu "
               "failelig %llu failconv %llu serial_acc %llu iters %llu scanned %llu "
               "clk load %llu scan %llu fix %llu jump %llu apply %llu fin %llu x6 %llu x7 %llu x8 %llu "
-              "w0 %llu w1 %llu w2 %llu w3 %llu\n",
+              "w0 %llu w1 %llu w2 %llu w3 %llu w4 %llu w5 %llu w6 %llu w7 %llu\n",
               jd[q].kind == kJobLfu ? "lfu" : "fifo", q,
               (unsigned long long)jd[q].cap, hs[q][kStFastOk], hs[q][kStFastAcc],
               hs[q][kStFailPool], hs[q][kStFailElig], hs[q][kStFailConv], hs[q][kStSerialAcc],
               hs[q][kStIters], hs[q][kStScanned], hs[q][kStT0], hs[q][kStT1], hs[q][kStT2],
               hs[q][kStT3], hs[q][kStT4], hs[q][kStT5], hs[q][kStT6], hs[q][kStT7], hs[q][kStT8],
-              hs[q][kStW0], hs[q][kStW1], hs[q][kStW2], hs[q][kStW3]);
+              hs[q][kStW0], hs[q][kStW1], hs[q][kStW2], hs[q][kStW3], hs[q][kStW4],
+              hs[q][kStW5], hs[q][kStW6], hs[q][kStW7]);
     }
   }
 #endif
