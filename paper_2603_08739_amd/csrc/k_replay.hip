@@ -88,7 +88,7 @@ static_assert(kRIt == 4, "hit words are assembled from four ballots");
 // Optional per-job replay statistics (diagnostics build only).
 #ifdef KV_REPLAY_STATS
 enum { kStFastOk = 0, kStFailPool, kStFailElig, kStFailConv, kStSerialAcc, kStIters,
-       kStScanned, kStFastAcc, kStT0, kStT1, kStT2, kStT3, kStT4, kStT5, kStT6, kStT7, kStT8, kStW0, kStW1, kStW2, kStW3, kStW4, kStW5, kStW6, kStW7, kStats };
+       kStScanned, kStFastAcc, kStT0, kStT1, kStT2, kStT3, kStT4, kStT5, kStT6, kStT7, kStT8, kStW0, kStW1, kStW2, kStW3, kStW4, kStW5, kStW6, kStW7, kStF0, kStF1, kStF2, kStF3, kStF4, kStats };
 __device__ unsigned long long g_rstats[256][kStats];
 __shared__ unsigned long long s_rstats[kStats];  // flushed to g_rstats when the job ends
 __shared__ unsigned long long s_rwave[8];
@@ -780,7 +780,7 @@ __device__ __forceinline__ bool lfu_serial_range(const JobDev& j, const JobArgs&
   return ok;
 }
 
-constexpr int kWin = 16;                          // demands searched in registers
+constexpr int kWin = 8;                           // demands searched in registers
 
 // Exclusive suffix minimum over the threads of the block (threads above t),
 // and whether any thread raised `flag`; two barriers.
@@ -1072,6 +1072,8 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     }
     uint32_t elig;
     uint32_t run = block_excl_scan_u32<NT>(xs, S.red, elig);
+    RCLK(t_f0);
+    RTIME(kStF0, t_it, t_f0);
     bool bad = elig < evtot;
     // entry k is consumed by the first miss whose demand exceeds the
     // eligible weight queued before k.  Demands and prefixes both rise, so
@@ -1092,12 +1094,12 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       }
       const bool active = r_lo < evtot && tid * qpt < nq;
       uint32_t lo = active ? upper_bound(S.mneed, 0u, nm, r_lo) : 0u;
-      const uint32_t hi = active ? upper_bound(S.mneed, lo, nm, r_hi) : 0u;
       uint32_t win[kWin];
-      const bool inwin = hi - lo < kWin;
 #pragma unroll
-      for (int t = 0; t < kWin; ++t)
-        win[t] = (inwin && lo + t < nm) ? S.mneed[lo + t] : 0xFFFFFFFFu;
+      for (int t = 0; t < kWin; ++t) win[t] = lo + t < nm ? S.mneed[lo + t] : 0xFFFFFFFFu;
+      // the window holds every answer when its last demand exceeds r_hi (or
+      // it reaches past the last miss)
+      const bool inwin = lo + kWin >= nm || win[kWin - 1] > r_hi;
 #pragma unroll
       for (int e = 0; e < CPT; ++e) {
         const uint32_t k = (uint32_t)e < qpt ? tid * qpt + e : nq;
@@ -1122,6 +1124,8 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
         run += qw[e];
       }
     }
+    RCLK(t_f2);
+    RTIME(kStF1, t_f0, t_f2);
     // the pointer reaches entry k when the first consumed entry at or after k goes
     uint32_t suf[CPT];
     uint32_t mn = kInf16;
@@ -1133,6 +1137,8 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     uint32_t tmin;
     bool anybad;
     block_suffix_min_flag<NT>(mn, bad, S.sfx, tmin, anybad);
+    RCLK(t_f3);
+    RTIME(kStF2, t_f2, t_f3);
     if (anybad) {
       RSTAT(blockIdx.x, kStFailElig, 1);
       return false;
@@ -1163,6 +1169,8 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       if (ncap) S.capm[ak] = ns;  // each touch position is the next touch of one entry
     }
     __syncthreads();
+    RCLK(t_f4);
+    RTIME(kStF3, t_f3, t_f4);
 #pragma unroll
     for (int e = 0; e < IT; ++e) {
       const uint32_t loc = l0 + e;
@@ -1174,6 +1182,8 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     }
     RWAVE(3, t_a);
     if (!block_any(changed)) converged = true;
+    RCLK(t_f5);
+    RTIME(kStF4, t_f4, t_f5);
   }
   if (!converged) {
     RSTAT(blockIdx.x, kStFailConv, 1);
@@ -1916,14 +1926,16 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
       fprintf(stderr, "[replay-stats] %s job %u cap %llu: fast %llu (acc %llu) failpool %llu "
               "failelig %llu failconv %llu serial_acc %llu iters %llu scanned %llu "
               "clk load %llu scan %llu fix %llu jump %llu apply %llu fin %llu x6 %llu x7 %llu x8 %llu "
-              "w0 %llu w1 %llu w2 %llu w3 %llu w4 %llu w5 %llu w6 %llu w7 %llu\n",
+              "w0 %llu w1 %llu w2 %llu w3 %llu w4 %llu w5 %llu w6 %llu w7 %llu "
+              "f0 %llu f1 %llu f2 %llu f3 %llu f4 %llu\n",
               jd[q].kind == kJobLfu ? "lfu" : "fifo", q,
               (unsigned long long)jd[q].cap, hs[q][kStFastOk], hs[q][kStFastAcc],
               hs[q][kStFailPool], hs[q][kStFailElig], hs[q][kStFailConv], hs[q][kStSerialAcc],
               hs[q][kStIters], hs[q][kStScanned], hs[q][kStT0], hs[q][kStT1], hs[q][kStT2],
               hs[q][kStT3], hs[q][kStT4], hs[q][kStT5], hs[q][kStT6], hs[q][kStT7], hs[q][kStT8],
               hs[q][kStW0], hs[q][kStW1], hs[q][kStW2], hs[q][kStW3], hs[q][kStW4],
-              hs[q][kStW5], hs[q][kStW6], hs[q][kStW7]);
+              hs[q][kStW5], hs[q][kStW6], hs[q][kStW7], hs[q][kStF0], hs[q][kStF1],
+              hs[q][kStF2], hs[q][kStF3], hs[q][kStF4]);
     }
   }
 #endif
