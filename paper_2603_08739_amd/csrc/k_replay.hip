@@ -583,7 +583,7 @@ __device__ __forceinline__ void fifo_serial(const JobDev& j, const JobArgs& a,
 struct LfuLds {
   // Small fields and the per-access fields of the hot loops come first, so
   // that they lie within reach of the LDS instructions' 16-bit offsets.
-  uint32_t red[2 * kRNW];
+  uint32_t red[2][2 * kRNW];  // block scans, alternating (no trailing barrier)
   uint32_t sfx[2 * kRNW];
   uint32_t anyflag[2];
   uint32_t tot8[8];           // chunk totals: ins, ins_w, ev, ev_w, victim w, last old, last new, n1
@@ -782,38 +782,44 @@ __device__ __forceinline__ bool lfu_serial_range(const JobDev& j, const JobArgs&
 
 constexpr int kWin = 8;                           // demands searched in registers
 
-// Exclusive suffix minimum over the threads of the block (threads above t),
-// and whether any thread raised `flag`; two barriers.
+// Exclusive suffix minimum over the threads of the block (threads above t)
+// of values below 2^31, and whether any thread raised `flag`; one barrier.
+// `sh` (NT / 64 words) may be written again only after another barrier.
 template <int NT>
 __device__ __forceinline__ void block_suffix_min_flag(uint32_t v, bool flag, uint32_t* sh,
                                                       uint32_t& smin, bool& any) {
   constexpr int NW = NT / 64;
+  constexpr int kInf = 0x7FFFFFFF;
   const uint32_t lane = lane_id();
   const int w = threadIdx.x / 64;
-  uint32_t x = v;
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const uint32_t y = __shfl_down(x, d, 64);
-    if (lane + d < 64) x = min(x, y);
-  }
-  const uint32_t above = __shfl_down(x, 1, 64);
+  // inclusive suffix minimum within rows of 16 lanes (row_shl: from lane + n)
+  int x = (int)v;
+  x = min(x, __builtin_amdgcn_update_dpp(kInf, x, 0x101, 0xf, 0xf, false));
+  x = min(x, __builtin_amdgcn_update_dpp(kInf, x, 0x102, 0xf, 0xf, false));
+  x = min(x, __builtin_amdgcn_update_dpp(kInf, x, 0x104, 0xf, 0xf, false));
+  x = min(x, __builtin_amdgcn_update_dpp(kInf, x, 0x108, 0xf, 0xf, false));
+  // ... then across rows, from the row heads
+  const int r1 = __builtin_amdgcn_readlane(x, 16), r2 = __builtin_amdgcn_readlane(x, 32),
+            r3 = __builtin_amdgcn_readlane(x, 48);
+  const int row = (int)(lane >> 4);
+  x = min(x, row < 3 ? r3 : kInf);
+  x = min(x, row < 2 ? r2 : kInf);
+  x = min(x, row < 1 ? r1 : kInf);
+  const int wmin = __builtin_amdgcn_readlane(x, 0);
+  // exclusive: the next lane's inclusive value (wave_shl:1; lane 63 gets none)
+  int r = __builtin_amdgcn_update_dpp(kInf, x, 0x130, 0xf, 0xf, false);
   const bool wflag = __ballot(flag) != 0ull;
-  if (lane == 0) {
-    sh[w] = x;
-    sh[NW + w] = wflag ? 1u : 0u;
-  }
+  if (lane == 0) sh[w] = (uint32_t)wmin | (wflag ? 0x80000000u : 0u);
   __syncthreads();
-  uint32_t r = (lane < 63) ? above : 0xFFFFFFFFu;
-  uint32_t f = 0;
+  bool f = false;
 #pragma unroll
   for (int ww = 0; ww < NW; ++ww) {
     const uint32_t y = sh[ww];
-    r = (ww > w) ? min(r, y) : r;
-    f |= sh[NW + ww];
+    r = (ww > w) ? min(r, (int)(y & 0x7FFFFFFFu)) : r;
+    f |= (y >> 31) != 0u;
   }
-  __syncthreads();
-  smin = r;
-  any = f != 0u;
+  smin = (uint32_t)r;
+  any = f;
 }
 
 // One chunk [c0, c1) without the serial walk.
@@ -932,7 +938,11 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   }
   uint32_t itot0, nm0, wpre0, mpre0;
   RWAVE(0, t_a);
-  block_excl_scan2_u32<NT>(x, xc, S.red, wpre0, mpre0, itot0, nm0);
+  // block scans alternate between two LDS buffers and skip their trailing
+  // barrier (every call has a barrier, so a buffer is reused only after
+  // all threads have left the call before)
+  uint32_t rg = 0;
+  block_excl_scan2_u32<NT, false>(x, xc, S.red[rg++ & 1], wpre0, mpre0, itot0, nm0);
   const uint64_t used0 = S.used;
   // evictions the chunk needs never exceed its insertions (used0 <= cap)
   const uint32_t ev0 = (used0 + itot0 > j.cap) ? (uint32_t)(used0 + itot0 - j.cap) : 0u;
@@ -989,7 +999,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
         cw_ += (live[e] && !touched[e]) ? wq[e] : 0u;
       }
       uint32_t pos, dummy, cnt_live, vsum;
-      block_excl_scan2_u32<NT>(cl_, cw_, S.red, pos, dummy, cnt_live, vsum);
+      block_excl_scan2_u32<NT, false>(cl_, cw_, S.red[rg++ & 1], pos, dummy, cnt_live, vsum);
 #pragma unroll
       for (int e = 0; e < kCScan; ++e) {
         if (!live[e]) continue;
@@ -1039,7 +1049,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
         xm += mi[e] ? 1u : 0u;
       }
       uint32_t wpre, mpre;
-      block_excl_scan2_u32<NT>(xw, xm, S.red, wpre, mpre, itot, nm);
+      block_excl_scan2_u32<NT, false>(xw, xm, S.red[rg++ & 1], wpre, mpre, itot, nm);
 #pragma unroll
       for (int e = 0; e < IT; ++e) {
         if (mi[e]) {
@@ -1071,7 +1081,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       xs += qw[e];
     }
     uint32_t elig;
-    uint32_t run = block_excl_scan_u32<NT>(xs, S.red, elig);
+    uint32_t run = block_excl_scan_u32<NT, false>(xs, S.red[rg++ & 1], elig);
     RCLK(t_f0);
     RTIME(kStF0, t_it, t_f0);
     bool bad = elig < evtot;

@@ -39,8 +39,10 @@ __device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t v) {
 }
 
 // Exclusive prefix sums of two 32-bit values over a block of NT threads.
-// `sh` holds 2 * (NT / 64) words of shared memory; two barriers.
-template <int NT>
+// `sh` holds 2 * (NT / 64) words of shared memory; two barriers.  With
+// Trail = false the second barrier (which lets the next call reuse `sh`) is
+// left out: consecutive calls must then alternate between two buffers.
+template <int NT, bool Trail = true>
 __device__ __forceinline__ void block_excl_scan2_u32(uint32_t a, uint32_t b, uint32_t* sh,
                                                      uint32_t& pa, uint32_t& pb, uint32_t& ta,
                                                      uint32_t& tb) {
@@ -61,14 +63,14 @@ __device__ __forceinline__ void block_excl_scan2_u32(uint32_t a, uint32_t b, uin
     sa += ya;
     sb += yb;
   }
-  __syncthreads();
+  if constexpr (Trail) __syncthreads();
   pa = xa + ia - a;
   pb = xb + ib - b;
   ta = sa;
   tb = sb;
 }
 
-template <int NT>
+template <int NT, bool Trail = true>
 __device__ __forceinline__ uint32_t block_excl_scan_u32(uint32_t a, uint32_t* sh, uint32_t& ta) {
   constexpr int NW = NT / 64;
   const int w = threadIdx.x / 64;
@@ -82,7 +84,7 @@ __device__ __forceinline__ uint32_t block_excl_scan_u32(uint32_t a, uint32_t* sh
     xa += (i < w) ? ya : 0u;
     sa += ya;
   }
-  __syncthreads();
+  if constexpr (Trail) __syncthreads();
   ta = sa;
   return xa + ia - a;
 }
