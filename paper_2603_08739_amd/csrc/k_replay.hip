@@ -1603,7 +1603,9 @@ struct RecDev {
   uint32_t order;
   uint64_t begin, end;   // positions in the order
   uint32_t filter;       // 1: count only accesses of `group`
-  uint32_t pad;
+  int16_t src[3];        // tiled combine: staged hit-bit source per tier, -1 = none
+  uint16_t pad;
+  uint64_t m_cnt, m_w;   // accesses (and weight) the record counts over
 };
 
 struct CombineArgs {
@@ -1688,6 +1690,173 @@ __global__ __launch_bounds__(256) void k_combine(const RecDev* __restrict__ recs
       rec[KV_F_EVICT] = jc[2];
       rec[KV_F_EVICT_W] = jc[3];
     }
+  }
+}
+
+
+// Records combined tile by tile.  A block owns a range of words (64 accesses
+// each) and every record of the launch (one per thread); each batch of kCbB
+// words of every hit-bit source (job bitmaps, re-access bits), weight plane
+// and group mask is staged once in LDS and read by all records, so the
+// sources cross HBM once instead of once per record.  The next batch is
+// loaded while the current one is counted.
+constexpr int kCbB = 32;          // words per batch
+constexpr int kCbSrc = 128;       // hit-bit sources at most
+constexpr int kCbNT = 1024;       // records per launch
+constexpr int kCbRows = kCbSrc + 16 + KV_MAX_GROUPS;  // sources, 2 x 8 planes, group masks
+constexpr int kCbLd = (kCbRows * kCbB + kCbNT - 1) / kCbNT;  // staged words per thread
+
+struct CbSrc {
+  const uint64_t* p;   // word w at p[w - wlo]
+  uint64_t wlo, whi;   // readable words [wlo, whi]
+};
+
+struct CombineTileArgs {
+  const RecDev* recs;
+  uint32_t n_recs, rec0;
+  const CbSrc* src;
+  uint32_t n_src;
+  const uint64_t* planes[2];
+  uint32_t plane_mask;   // weight bits present
+  uint32_t uniform_w;    // 0 = mixed weights
+  const uint64_t* gmask; // shared order
+  uint32_t n_gm;         // group masks staged (0: no filtered record)
+  uint64_t nwords, wpb;  // words in all, words per block
+  unsigned long long* part;  // [n_recs][6]: hits of u0, u1, u2, then their weights
+};
+
+__device__ __forceinline__ uint64_t cb_load(const CombineTileArgs& a, uint32_t row, uint64_t w) {
+  if (w >= a.nwords) return 0ull;
+  if (row < (uint32_t)kCbSrc) {
+    if (row >= a.n_src) return 0ull;
+    const CbSrc c = a.src[row];
+    return (w >= c.wlo && w <= c.whi) ? c.p[w - c.wlo] : 0ull;
+  }
+  if (row < (uint32_t)kCbSrc + 16) {
+    const uint32_t o = (row - kCbSrc) >> 3, b = (row - kCbSrc) & 7;
+    if (!a.planes[o] || !((a.plane_mask >> b) & 1u)) return 0ull;
+    return a.planes[o][(uint64_t)b * a.nwords + w];
+  }
+  const uint32_t g = row - kCbSrc - 16;
+  return g < a.n_gm ? a.gmask[(uint64_t)g * a.nwords + w] : 0ull;
+}
+
+__global__ __launch_bounds__(kCbNT) void k_combine_tile(CombineTileArgs a) {
+  // rows padded by one word: records read different rows at the same word
+  __shared__ uint64_t sw[2][kCbRows][kCbB + 1];
+  __shared__ CbSrc ssrc[kCbSrc];
+  const uint32_t tid = threadIdx.x;
+  if (tid < a.n_src) ssrc[tid] = a.src[tid];
+  __syncthreads();
+  a.src = ssrc;
+  const uint32_t ri = a.rec0 + tid;
+  const bool have = ri < a.n_recs;
+  RecDev r{};
+  if (have) r = a.recs[ri];
+  const uint64_t rwlo = r.begin >> 6, rwhi = r.end > r.begin ? (r.end - 1) >> 6 : 0;
+  const bool live = have && r.end > r.begin;
+  const uint64_t w0 = (uint64_t)blockIdx.x * a.wpb;
+  const uint64_t w1 = min<uint64_t>(a.nwords, w0 + a.wpb);
+  unsigned long long acc[6] = {0, 0, 0, 0, 0, 0};
+  uint64_t nxt[kCbLd];
+  auto fetch = [&](uint64_t wb) {
+#pragma unroll
+    for (int q = 0; q < kCbLd; ++q) {
+      const uint32_t item = tid + q * kCbNT;
+      nxt[q] = item < (uint32_t)(kCbRows * kCbB) ? cb_load(a, item / kCbB, wb + item % kCbB) : 0ull;
+    }
+  };
+  auto put = [&](int buf) {
+#pragma unroll
+    for (int q = 0; q < kCbLd; ++q) {
+      const uint32_t item = tid + q * kCbNT;
+      if (item < (uint32_t)(kCbRows * kCbB)) sw[buf][item / kCbB][item % kCbB] = nxt[q];
+    }
+  };
+  if (w0 < w1) {
+    fetch(w0);
+    put(0);
+  }
+  __syncthreads();
+  int cur = 0;
+  for (uint64_t wb = w0; wb < w1; wb += kCbB) {
+    if (wb + kCbB < w1) fetch(wb + kCbB);
+    if (live && wb <= rwhi && wb + kCbB > rwlo) {
+      const uint32_t po = kCbSrc + 8 * r.order;
+      for (int b = 0; b < kCbB; ++b) {
+        const uint64_t w = wb + b;
+        if (w < rwlo || w > rwhi || w >= w1) continue;
+        uint64_t m = ~0ull;
+        if (w == rwlo) m &= ~0ull << (r.begin & 63);
+        if (w == rwhi && (r.end & 63)) m &= (1ull << (r.end & 63)) - 1;
+        if (r.filter) m &= sw[cur][kCbSrc + 16 + r.group][b];
+        const uint64_t p0 = r.src[0] >= 0 ? sw[cur][r.src[0]][b] : 0ull;
+        const uint64_t p1 = r.src[1] >= 0 ? sw[cur][r.src[1]][b] : 0ull;
+        const uint64_t p2 = r.src[2] >= 0 ? sw[cur][r.src[2]][b] : 0ull;
+        const uint64_t u0 = p0 & m, u1 = (p0 | p1) & m, u2 = (p0 | p1 | p2) & m;
+        const uint32_t c0 = __popcll(u0), c1 = __popcll(u1), c2 = __popcll(u2);
+        acc[0] += c0;
+        acc[1] += c1;
+        acc[2] += c2;
+        if (a.uniform_w) {
+          acc[3] += (unsigned long long)c0 * a.uniform_w;
+          acc[4] += (unsigned long long)c1 * a.uniform_w;
+          acc[5] += (unsigned long long)c2 * a.uniform_w;
+        } else {
+          uint32_t s0 = 0, s1 = 0, s2 = 0;
+#pragma unroll
+          for (int pb = 0; pb < 8; ++pb) {
+            if (!((a.plane_mask >> pb) & 1u)) continue;
+            const uint64_t pl = sw[cur][po + pb][b];
+            s0 += (uint32_t)__popcll(u0 & pl) << pb;
+            s1 += (uint32_t)__popcll(u1 & pl) << pb;
+            s2 += (uint32_t)__popcll(u2 & pl) << pb;
+          }
+          acc[3] += s0;
+          acc[4] += s1;
+          acc[5] += s2;
+        }
+      }
+    }
+    if (wb + kCbB < w1) put(cur ^ 1);
+    __syncthreads();
+    cur ^= 1;
+  }
+  if (live) {
+    unsigned long long* o = a.part + (uint64_t)ri * 6;
+#pragma unroll
+    for (int f = 0; f < 6; ++f)
+      if (acc[f]) atomicAdd(o + f, acc[f]);
+  }
+}
+
+// Per record: its three tiers' count fields from the summed union counts.
+__global__ __launch_bounds__(256) void k_combine_fin(const RecDev* __restrict__ recs,
+                                                     uint32_t n_recs,
+                                                     const unsigned long long* __restrict__ part,
+                                                     const unsigned long long* __restrict__ jcnt,
+                                                     uint32_t n_groups, uint64_t* __restrict__ counts) {
+  const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n_recs) return;
+  const RecDev r = recs[i];
+  const unsigned long long* pc = part + (uint64_t)i * 6;
+  const unsigned long long tot[8] = {r.m_cnt, pc[0], pc[1], pc[2], r.m_w, pc[3], pc[4], pc[5]};
+  uint64_t* out = counts + ((uint64_t)r.cfg * n_groups + r.group) * 24;
+  for (int k = 0; k < 3; ++k) {
+    uint64_t* rec = out + k * 8;
+    if (r.job[k] < 0) {
+      for (int f = 0; f < 8; ++f) rec[f] = 0;
+      continue;
+    }
+    const unsigned long long* jc = jcnt + ((uint64_t)r.job[k] * n_groups + r.group) * 4;
+    rec[KV_F_HIT] = tot[1 + k] - (k ? tot[k] : 0ull);
+    rec[KV_F_HIT_W] = tot[5 + k] - (k ? tot[4 + k] : 0ull);
+    rec[KV_F_MISS] = tot[0] - tot[1 + k];
+    rec[KV_F_MISS_W] = tot[4] - tot[5 + k];
+    rec[KV_F_INS] = jc[0];
+    rec[KV_F_INS_W] = jc[1];
+    rec[KV_F_EVICT] = jc[2];
+    rec[KV_F_EVICT_W] = jc[3];
   }
 }
 
@@ -1811,10 +1980,28 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
           r.end = n;
           r.filter = G > 1 ? 1u : 0u;
         }
+        // what the record counts over: its group's accesses, or all of them
+        const bool whole = !part_order && G == 1;
+        r.m_cnt = whole ? n : t.st.n_g[gg];
+        r.m_w = whole ? t.st.n_w : t.st.n_w_g[gg];
         recs.push_back(r);
       }
     }
   }
+  // hit-bit sources of the tiled combine: one per replayed job, one per
+  // order for jobs whose cache holds everything (a hit is a re-access)
+  std::vector<int32_t> src_of(jd.size() + 2, -1);  // jobs, then the two orders
+  uint32_t n_src = 0;
+  for (RecDev& r : recs) {
+    for (int k = 0; k < 3; ++k) {
+      r.src[k] = -1;
+      if (r.job[k] < 0) continue;
+      const size_t key = jd[r.job[k]].closed ? jd.size() + r.order : (size_t)r.job[k];
+      if (src_of[key] < 0) src_of[key] = (int32_t)n_src++;
+      r.src[k] = (int16_t)std::min<int32_t>(src_of[key], 0x7FFF);
+    }
+  }
+  const bool tiled = n_src <= (uint32_t)kCbSrc;
   DevBuf& bj = t.ws[11];
   DevBuf& bstate = t.ws[12];
   DevBuf& bcls = t.ws[13];
@@ -1967,9 +2154,69 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
     uint32_t pm = 0;
     for (uint32_t w = t.st.w_min; w <= t.st.w_max; ++w) pm |= w;
     ca.plane_mask = pm;
-    hipLaunchKernelGGL(k_combine, dim3((uint32_t)recs.size()), dim3(256), 0, s,
-                       brec.as<RecDev>(), ca, counts);
-    KV_HIP(hipGetLastError());
+    const uint32_t nrec = (uint32_t)recs.size();
+    if (tiled) {
+      std::vector<CbSrc> srcs(n_src);
+      for (size_t key = 0; key < src_of.size(); ++key) {
+        const int32_t sl = src_of[key];
+        if (sl < 0) continue;
+        CbSrc c{};
+        if (key >= jd.size()) {
+          c.p = ca.reuse[key - jd.size()];
+          c.wlo = 0;
+          c.whi = nwords - 1;
+        } else {
+          const JobDev& q = jd[key];
+          c.p = bbits.as<uint64_t>() + q.bits_off;
+          c.wlo = q.word0;
+          c.whi = (q.end - 1) >> 6;
+        }
+        srcs[sl] = c;
+      }
+      DevBuf& bsrc = t.ws[18];
+      DevBuf& bpart = t.ws[19];
+      if ((st = bsrc.reserve(std::max<size_t>(n_src, 1) * sizeof(CbSrc))) != KV_OK) return st;
+      if ((st = bpart.reserve((size_t)nrec * 6 * 8)) != KV_OK) return st;
+      t.src_stage.resize(srcs.size() * sizeof(CbSrc));
+      std::memcpy(t.src_stage.data(), srcs.data(), t.src_stage.size());
+      if (n_src)
+        KV_HIP(hipMemcpyAsync(bsrc.p, t.src_stage.data(), t.src_stage.size(),
+                              hipMemcpyHostToDevice, s));
+      if ((st = fill_u64(bpart.as<uint64_t>(), 0, (uint64_t)nrec * 6, s)) != KV_OK) return st;
+      bool any_filter = false;
+      for (const RecDev& r : recs) any_filter |= r.filter != 0;
+      CombineTileArgs ta{};
+      ta.recs = brec.as<RecDev>();
+      ta.n_recs = nrec;
+      ta.src = bsrc.as<CbSrc>();
+      ta.n_src = n_src;
+      ta.planes[0] = planes[0];
+      ta.planes[1] = have_part ? planes[1] : nullptr;
+      ta.plane_mask = pm;
+      ta.uniform_w = ca.uniform_w;
+      ta.gmask = gmask[0];
+      ta.n_gm = any_filter ? G : 0u;
+      ta.nwords = nwords;
+      ta.part = bpart.as<unsigned long long>();
+      int ncu = 0;
+      KV_HIP(hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, t.device));
+      const uint64_t nb0 = std::max<uint64_t>(1, std::min<uint64_t>((uint64_t)std::max(ncu, 1),
+                                                                    div_up(nwords, kCbB)));
+      ta.wpb = (uint64_t)div_up(div_up(nwords, nb0), kCbB) * kCbB;
+      const uint32_t nb = div_up(nwords, ta.wpb);
+      for (uint32_t r0 = 0; r0 < nrec; r0 += kCbNT) {
+        ta.rec0 = r0;
+        hipLaunchKernelGGL(k_combine_tile, dim3(nb), dim3(kCbNT), 0, s, ta);
+        KV_HIP(hipGetLastError());
+      }
+      hipLaunchKernelGGL(k_combine_fin, dim3(div_up(nrec, 256)), dim3(256), 0, s,
+                         brec.as<RecDev>(), nrec, bpart.as<unsigned long long>(),
+                         bjc.as<unsigned long long>(), G, counts);
+      KV_HIP(hipGetLastError());
+    } else {
+      hipLaunchKernelGGL(k_combine, dim3(nrec), dim3(256), 0, s, brec.as<RecDev>(), ca, counts);
+      KV_HIP(hipGetLastError());
+    }
   }
   return KV_OK;
 }

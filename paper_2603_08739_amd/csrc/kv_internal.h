@@ -89,7 +89,7 @@ struct Trace {
   ThresholdSet shared_ts, part_ts;
   std::vector<kv_config> cfg_stage;
   GroupStats gs_stage[KV_MAX_GROUPS];
-  std::vector<uint8_t> job_stage, rec_stage;
+  std::vector<uint8_t> job_stage, rec_stage, src_stage;
   std::vector<unsigned long long> jc_stage;
 };
 

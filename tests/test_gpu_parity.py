@@ -260,6 +260,36 @@ def test_lfu_hot_blocks(lib, oracle_mod, seed):
         assert counts[1, 0, 0, 3] == 5   # cap 2: a victim at each miss from block 2 on
 
 
+def test_combine_many_records(lib, oracle_mod):
+    """More per-(config, group) records than one combine launch takes (1024):
+    300 three-tier FIFO/LFU configurations over four groups, shared and
+    partitioned."""
+    rng = np.random.default_rng(17)
+    t = tg.random_trace(401, 20_000, 3_000, n_groups=4, weight_choices=(1, 2, 5),
+                        zipf_s=0.9, reuse_bias=0.2)
+    caps = [20, 60, 150, 400, 900]
+    items = []
+    for i in range(300):
+        c = [int(x) for x in rng.choice(caps, size=3)]
+        pol = int(rng.integers(1, 3))
+        if i % 3 == 2:
+            items.append({"cap_group": [[c[k]] * 4 for k in range(3)], "partitioned": 1,
+                          "policy": [pol] * 4, "cap": tuple(4 * x for x in c)})
+        else:
+            items.append({"cap": tuple(c), "policy": pol, "mode": 0})
+    compare(lib, oracle_mod, t, tg.from_list(items), label="many-records")
+
+
+def test_combine_many_sources(lib, oracle_mod):
+    """More distinct replayed caches (hit-bit sources) than the tiled combine
+    stages (128): the per-record combine path."""
+    t = tg.random_trace(402, 12_000, 2_500, n_groups=2, weight_choices=(1, 3),
+                        zipf_s=0.8, reuse_bias=0.2)
+    items = [{"cap": (10 + 7 * i, 0, 0), "policy": p} for i in range(75) for p in (1, 2)]
+    items += [{"cap": (10 + 7 * i, 20 + 11 * i, 0), "policy": 2} for i in range(0, 75, 5)]
+    compare(lib, oracle_mod, t, tg.from_list(items), label="many-sources")
+
+
 def test_full_prefix_real_capacities(lib, oracle_mod):
     """The first 40,000 requests of the full-scale trace (about 1.5e7
     accesses) with configurations drawn from the full grid at their real
