@@ -204,37 +204,33 @@ __device__ __forceinline__ void store_hits(const bool hit[kRIt], uint64_t c0, ui
 
 // IT consecutive accesses [p0, p0 + IT) of a thread (p0 a multiple of IT):
 // vector loads when all are valid.
+// IT consecutive elements from position p0 (a multiple of 4), branch-free:
+// the read position is clamped to n & ~3 (the arrays' slack covers the
+// vector read there; a clamped read only serves invalid items), and items
+// with v[e] false read as 0.
 template <int IT>
-__device__ __forceinline__ void loadn_u32(const uint32_t* __restrict__ a, uint64_t p0, bool all,
+__device__ __forceinline__ void loadn_u32(const uint32_t* __restrict__ a, uint64_t p0, uint64_t n,
                                           const bool* v, uint32_t* out) {
-  if (all) {
 #pragma unroll
-    for (int q = 0; q < IT / 4; ++q) {
-      const uint4 x = *reinterpret_cast<const uint4*>(a + p0 + 4 * q);
-      out[4 * q] = x.x;
-      out[4 * q + 1] = x.y;
-      out[4 * q + 2] = x.z;
-      out[4 * q + 3] = x.w;
-    }
-  } else {
-#pragma unroll
-    for (int e = 0; e < IT; ++e) out[e] = v[e] ? a[p0 + e] : 0u;
+  for (int q = 0; q < IT / 4; ++q) {
+    const uint64_t pq = min<uint64_t>(p0 + 4 * q, n & ~3ull);
+    const uint4 x = *reinterpret_cast<const uint4*>(a + pq);
+    out[4 * q] = v[4 * q] ? x.x : 0u;
+    out[4 * q + 1] = v[4 * q + 1] ? x.y : 0u;
+    out[4 * q + 2] = v[4 * q + 2] ? x.z : 0u;
+    out[4 * q + 3] = v[4 * q + 3] ? x.w : 0u;
   }
 }
 
 template <int IT>
-__device__ __forceinline__ void loadn_u8(const uint8_t* __restrict__ a, uint64_t p0, bool all,
+__device__ __forceinline__ void loadn_u8(const uint8_t* __restrict__ a, uint64_t p0, uint64_t n,
                                          const bool* v, uint32_t* out) {
-  if (all) {
 #pragma unroll
-    for (int q = 0; q < IT / 4; ++q) {
-      const uint32_t x = *reinterpret_cast<const uint32_t*>(a + p0 + 4 * q);
+  for (int q = 0; q < IT / 4; ++q) {
+    const uint64_t pq = min<uint64_t>(p0 + 4 * q, n & ~3ull);
+    const uint32_t x = *reinterpret_cast<const uint32_t*>(a + pq);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) out[4 * q + e] = (x >> (8 * e)) & 0xFFu;
-    }
-  } else {
-#pragma unroll
-    for (int e = 0; e < IT; ++e) out[e] = v[e] ? (uint32_t)a[p0 + e] : 0u;
+    for (int e = 0; e < 4; ++e) out[4 * q + e] = v[4 * q + e] ? (x >> (8 * e)) & 0xFFu : 0u;
   }
 }
 
@@ -866,16 +862,15 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   bool v[IT];
 #pragma unroll
   for (int e = 0; e < IT; ++e) v[e] = l0 + e < L && p0 + e >= jb;
-  const bool all = v[0] && v[IT - 1];
   uint32_t ww[IT], gg[IT], kk[IT], nx[IT], f0[IT];
   bool cm[IT], res0[IT];
   if (have_pref) {
     lds_get<IT>(S.pkey + l0, kk);
   } else {
-    loadn_u32<IT>(a.key[o], p0, all, v, kk);
+    loadn_u32<IT>(a.key[o], p0, a.n, v, kk);
   }
-  loadn_u8<IT>(a.w8[o], p0, all, v, ww);
-  loadn_u32<IT>(a.nxt[o], p0, all, v, nx);
+  loadn_u8<IT>(a.w8[o], p0, a.n, v, ww);
+  loadn_u32<IT>(a.nxt[o], p0, a.n, v, nx);
   {
     // the next full chunk's block links.  The read position is clamped to
     // the arrays' readable slack; whatever lies outside the job (or past n,
@@ -897,7 +892,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   }
 #pragma unroll
   for (int e = 0; e < IT; ++e) gg[e] = g0;
-  if constexpr (!G1) loadn_u8<IT>(a.g8[o], p0, all, v, gg);
+  if constexpr (!G1) loadn_u8<IT>(a.g8[o], p0, a.n, v, gg);
   uint32_t h = S.head1;
   if (tid < 8) S.tot8[tid] = 0;  // first read after several barriers
   // stored counts at the latest earlier accesses (prefetched by the
@@ -910,7 +905,8 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
 #pragma unroll
     for (int e = 0; e < IT; ++e) {
       const bool old_prev = v[e] && kk[e] != 0 && kk[e] - 1 < c0;
-      s0[e] = old_prev ? cnt[kk[e] - 1 - jb] : 0u;
+      s0[e] = cnt[old_prev ? kk[e] - 1 - jb : 0];
+      if (!old_prev) s0[e] = 0;
     }
   }
 #pragma unroll
