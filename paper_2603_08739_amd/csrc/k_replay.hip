@@ -88,7 +88,7 @@ static_assert(kRIt == 4, "hit words are assembled from four ballots");
 // Optional per-job replay statistics (diagnostics build only).
 #ifdef KV_REPLAY_STATS
 enum { kStFastOk = 0, kStFailPool, kStFailElig, kStFailConv, kStSerialAcc, kStIters,
-       kStScanned, kStFastAcc, kStT0, kStT1, kStT2, kStT3, kStT4, kStT5, kStT6, kStT7, kStT8, kStW0, kStW1, kStW2, kStW3, kStW4, kStW5, kStW6, kStW7, kStF0, kStF1, kStF2, kStF3, kStF4, kStats };
+       kStScanned, kStFastAcc, kStT0, kStT1, kStT2, kStT3, kStT4, kStT5, kStT6, kStT7, kStT8, kStW0, kStW1, kStW2, kStW3, kStW4, kStW5, kStW6, kStW7, kStF0, kStF1, kStF2, kStF3, kStF4, kStG0, kStG1, kStG2, kStats };
 __device__ unsigned long long g_rstats[256][kStats];
 __shared__ unsigned long long s_rstats[kStats];  // flushed to g_rstats when the job ends
 __shared__ unsigned long long s_rwave[8];
@@ -244,7 +244,11 @@ __device__ __forceinline__ void store_hits_n(const bool* hit, uint64_t c0, uint3
   uint64_t bal[IT];
 #pragma unroll
   for (int e = 0; e < IT; ++e) bal[e] = __ballot(hit[e]);
-  const uint32_t q = lane_id();
+  // the lane index, recomputed here (a value kept from the kernel's start
+  // can end up spilled, and its reload would wait for every memory access
+  // in flight)
+  uint32_t q;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(q));
   if (q < (uint32_t)IT) {
     uint64_t word = 0;
 #pragma unroll
@@ -600,7 +604,9 @@ struct LfuLds {
     uint16_t occ[kLChunk];    // apply: earlier touches of the same block inside the chunk
   };
   uint8_t mcons[kLChunk];     // the entry inserted here is evicted inside the chunk
-  uint16_t nxloc[kLChunk];    // next touch in the chunk or kInf16
+  // next touch relative to the chunk start: below L inside the chunk, up to
+  // 2 * kLChunk in the next full chunk, else kInf16
+  uint16_t nxloc[kLChunk];
   int16_t lp[kLChunk];        // previous touch in the chunk; pointer-jumped to the chain root
   union {
     uint16_t mpos[kLChunk];   // fixed point: local position of the m-th miss
@@ -616,8 +622,6 @@ struct LfuLds {
   uint8_t ccons[kCand];
   uint16_t ca[kCand];         // first touch inside the chunk or kInf16
   uint32_t cq[kCand];         // position of their last touch
-  // a block's count after its last touch in the chunk (0 elsewhere)
-  alignas(16) uint32_t fnl[kLChunk];
   // the next full chunk, per access: its block link and the stored count
   // at that link (each thread reads and writes only its own accesses)
   alignas(16) uint32_t pkey[kLChunk];
@@ -642,6 +646,15 @@ __device__ __forceinline__ void lds_put(uint32_t* p, const uint32_t* v) {
 #pragma unroll
   for (int q = 0; q < IT / 4; ++q)
     reinterpret_cast<uint4*>(p)[q] = make_uint4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+}
+
+// Nonempty-class bits from the class counts (whole block).
+template <int NT>
+__device__ __forceinline__ void class_bits_rebuild(LfuLds& S) {
+  for (uint32_t f = threadIdx.x; f < kLdsClass; f += NT) {
+    const uint64_t bal = __ballot(S.ccnt[f] != 0u);
+    if (lane_id() == 0) S.cnz[f / 64] = bal;
+  }
 }
 
 // In-cache count of a block whose latest access is q with stored count c.
@@ -845,7 +858,8 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
                                          uint32_t* __restrict__ cnt, const Classes& cl,
                                          GroupCounters& gc, LfuLds& S,
                                          uint64_t* __restrict__ bits, uint32_t c0, uint32_t c1,
-                                         uint32_t g0, BlockAny& block_any, bool have_pref) {
+                                         uint32_t g0, BlockAny& block_any, bool have_pref,
+                                         uint64_t& used_io, uint32_t& head1_io) {
   constexpr bool g1 = G1;
   constexpr int IT = kLChunk / NT;               // accesses per thread
   constexpr int CPT = (kCand + kLChunk) / NT;    // queue entries per thread
@@ -893,8 +907,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
 #pragma unroll
   for (int e = 0; e < IT; ++e) gg[e] = g0;
   if constexpr (!G1) loadn_u8<IT>(a.g8[o], p0, a.n, v, gg);
-  uint32_t h = S.head1;
-  if (tid < 8) S.tot8[tid] = 0;  // first read after several barriers
+  uint32_t h = head1_io;
   // stored counts at the latest earlier accesses (prefetched by the
   // previous chunk when it covered the whole chunk before this one); only a
   // block's first access in the chunk needs one
@@ -919,7 +932,8 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     f0[e] = (v[e] && kk[e] != 0 && lp < 0) ? lfu_live_count(s0[e], kk[e] - 1, h) : 0u;
     res0[e] = f0[e] != 0;
     cm[e] = v[e] && lp < 0 && !res0[e];
-    S.nxloc[loc] = again ? (uint16_t)(nx[e] - c0) : kInf16;
+    S.nxloc[loc] = (v[e] && nx[e] != kNone && nx[e] - c0 < 2 * kLChunk) ? (uint16_t)(nx[e] - c0)
+                                                                        : kInf16;
     S.pw[loc] = (uint8_t)ww[e];
     S.capm[loc] = 0;
     S.mskip[loc] = again ? 1 : 0;
@@ -939,7 +953,10 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   // all threads have left the call before)
   uint32_t rg = 0;
   block_excl_scan2_u32<NT, false>(x, xc, S.red[rg++ & 1], wpre0, mpre0, itot0, nm0);
-  const uint64_t used0 = S.used;
+  // past the chunk's first barrier every thread has left the previous
+  // chunk, which read the totals last
+  if (tid < 8) S.tot8[tid] = 0;
+  const uint64_t used0 = used_io;
   // evictions the chunk needs never exceed its insertions (used0 <= cap)
   const uint32_t ev0 = (used0 + itot0 > j.cap) ? (uint32_t)(used0 + itot0 - j.cap) : 0u;
   // used0 - cap, clamped so that adding a chunk's miss weight stays in 32 bits
@@ -1014,7 +1031,9 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     nc0 = n0;
     reached = h >= c0;
     // positions before the first live entry hold no count-1 member any more
-    if (tid == 0) S.head1 = nc0 ? S.cq[0] : h;
+    h = nc0 ? S.cq[0] : h;
+  } else {
+    h = head1_io;
   }
   RCLK(t_c);
   RTIME(kStT1, t_b, t_c);
@@ -1159,7 +1178,8 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       if (k >= nq) continue;
       const uint32_t ptime = min(suf[e], tmin);
       const bool cons = evk[e] != kInf16;
-      const uint32_t ak = (k < nc0) ? (uint32_t)S.ca[k] : (uint32_t)S.nxloc[S.mpos[k - nc0]];
+      uint32_t ak = (k < nc0) ? (uint32_t)S.ca[k] : (uint32_t)S.nxloc[S.mpos[k - nc0]];
+      if (ak >= L) ak = kInf16;  // next touch beyond the chunk
       const bool nskip = ak != kInf16 && (ptime == kInf16 || ak <= ptime);
       const bool ncap = ak != kInf16 && !nskip && ptime != kInf16;
       if (k < nc0) {
@@ -1335,16 +1355,16 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   int d12[2] = {0, 0};
 #pragma unroll
   for (int e = 0; e < IT; ++e) {
-    const uint32_t loc = l0 + e;
     fnew[e] = 0;
-    fin[e] = v[e] && nxl[e] == kInf16;
+    fin[e] = v[e] && nxl[e] >= L;
     if (fin[e]) {
       if ((int32_t)lm[e] >= 0) {
         fnew[e] = mcm[e] ? 0u : oc[e] - mocc[e] + 1u;
       } else {
         fnew[e] = rf0[e] + oc[e] + 1u;
       }
-      cnt[c0 + loc - jb] = fnew[e];
+      // the block's next access opens the next full chunk's prefetch slot
+      if (L == kLChunk && nxl[e] != kInf16) S.pcnt[nxl[e] - kLChunk] = fnew[e];
     }
     const uint32_t fo = fin[e] ? rf0[e] : 0u, fn = fnew[e];
 #pragma unroll
@@ -1357,7 +1377,12 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       if (fn > 2) class_add_par(cl, cn, +1);
     }
   }
-  lds_put<IT>(S.fnl + l0, fnew);
+  // the counts at the chunk's positions: the final ones at last touches, 0
+  // at the others (never read: a later access links to a later touch).
+  // Stored unconditionally (items outside the job go to the slot past its
+  // end), so that waits for the earlier gather need not cover them.
+#pragma unroll
+  for (int e = 0; e < IT; ++e) cnt[v[e] ? c0 + l0 + e - jb : je - jb] = fin[e] ? fnew[e] : 0u;
   RCLK(t_e3);
   RTIME(kStT8, t_e2, t_e3);
   if (lane_id() == 0) {
@@ -1382,42 +1407,52 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   __syncthreads();
   RCLK(t_f);
   RTIME(kStT4, t_e, t_f);
-  // the next chunk's stored counts, now that this chunk's are known (only
-  // a link before the next chunk is ever read)
-  uint32_t nf[IT];
+  // the next chunk's stored counts at links before this chunk (a link
+  // inside it was filled in by its last touch above; only a link before the
+  // next chunk is ever read)
 #pragma unroll
   for (int e = 0; e < IT; ++e) {
     const uint32_t k = nk[e];
-    const bool here = k != 0 && k - 1 >= c0 && k - 1 < c0 + kLChunk;
-    nf[e] = here ? S.fnl[k - 1 - c0] : nold[e];
+    if (!(k != 0 && k - 1 >= c0 && k - 1 < c0 + kLChunk)) S.pcnt[l0 + e] = nold[e];
   }
-  lds_put<IT>(S.pcnt + l0, nf);
-  // nonempty-class bits of the LDS classes, from the counts
-  for (uint32_t f = tid; f < kLdsClass; f += NT) {
-    const uint64_t bal = __ballot(S.ccnt[f] != 0u);
-    if (lane_id() == 0) S.cnz[f / 64] = bal;
-  }
+  // the nonempty-class bitmap is rebuilt only when class 1 is empty (the
+  // serial walk rebuilds it before it starts)
+  RCLK(t_f1);
+  RTIME(kStG0, t_f, t_f1);
+  const bool c1empty = S.ccnt[1] == 0u;
+  if (c1empty) class_bits_rebuild<NT>(S);
   store_hits_n<IT>(hit, c0, L, j, bits);
-  if (tid == 0) {
-    uint32_t t[8];
+  // every thread takes the chunk totals: the cached weight and the count-1
+  // queue head go on in registers, with no barrier to end the chunk (the
+  // next chunk's writes touch nothing read here)
+  uint32_t t[8];
 #pragma unroll
-    for (int f = 0; f < 8; ++f) t[f] = S.tot8[f];
-    if (g1) {
-      gc.ins[g0] += t[0];
-      gc.insw[g0] += t[1];
-      gc.ev[g0] += t[2];
-      gc.evw[g0] += t[3];
-    }
-    S.used = used0 + itot - t[4];
-    if (t[6]) S.head1 = c0 + t[6];          // last new entry taken + 1
-    else if (t[5]) S.head1 = S.cq[t[5] - 1] + 1;         // last old entry taken + 1
+  for (int f = 0; f < 8; ++f) t[f] = S.tot8[f];
+  if (g1 && tid == 0) {
+    gc.ins[g0] += t[0];
+    gc.insw[g0] += t[1];
+    gc.ev[g0] += t[2];
+    gc.evw[g0] += t[3];
   }
+  used_io = used0 + itot - t[4];
+  if (t[6]) head1_io = c0 + t[6];                 // last new entry taken + 1
+  else if (t[5]) head1_io = S.cq[t[5] - 1] + 1;   // last old entry taken + 1
+  else head1_io = h;
   RWAVE(6, t_a);
-  __syncthreads();
-  if (tid == 0) {
-    const uint32_t nf = next_class(cl, 1);
-    if (nf != 0xFFFFFFFFu) S.fmin = nf;
+  RCLK(t_f2);
+  RTIME(kStG1, t_f1, t_f2);
+  if (c1empty) {
+    // the lowest nonempty class, for the serial walk (class 1 otherwise)
+    __syncthreads();
+    if (tid == 0) {
+      const uint32_t nf = next_class(cl, 1);
+      if (nf != 0xFFFFFFFFu) S.fmin = nf;
+    }
+  } else if (tid == 0) {
+    S.fmin = 1;
   }
+  RCLK(t_f3);
+  RTIME(kStG2, t_f2, t_f3);
   RCLK(t_g);
   RTIME(kStT5, t_f, t_g);
   RWAVE(7, t_a);
@@ -1442,20 +1477,19 @@ __device__ __forceinline__ void lfu_chunked(const JobDev& j, const JobArgs& a,
   if (tid < 2) S.anyflag[tid] = 0;
   BlockAny block_any{S.anyflag, 0};
   if (tid == 0) {
-    S.used = 0;
     S.fmin = 1;
-    S.head1 = (uint32_t)j.begin;
     S.ok = 1;
   }
   __syncthreads();
   uint64_t pos = j.begin & ~63ull;
   uint32_t len = j.chunk;
-  constexpr int IT = kLChunk / NT;
   uint64_t ppos = ~0ull;  // the chunk whose links and counts are prefetched in LDS
+  uint64_t used = 0;                    // cached weight
+  uint32_t head1 = (uint32_t)j.begin;   // no live count-1 member before head1
   while (pos < j.end) {
     const uint32_t l = (uint32_t)min<uint64_t>(len, j.end - pos);
     if (lfu_fast<NT, G1>(j, a, cnt, cl, gc, S, bits, (uint32_t)pos, (uint32_t)(pos + l), g0,
-                         block_any, ppos == pos)) {
+                         block_any, ppos == pos, used, head1)) {
       ppos = (l == kLChunk) ? pos + l : ~0ull;
       pos += l;
       len = min<uint32_t>(len * 2, j.chunk);
@@ -1464,9 +1498,17 @@ __device__ __forceinline__ void lfu_chunked(const JobDev& j, const JobArgs& a,
       ppos = ~0ull;  // the failed attempt replaced the prefetched links
     } else {
       __syncthreads();
+      class_bits_rebuild<NT>(S);
+      if (tid == 0) {
+        S.used = used;
+        S.head1 = head1;
+      }
+      __syncthreads();
       if (tid == 0) S.ok = lfu_serial_range(j, a, cnt, head, cl, S, gc, bits, pos, pos + l) ? 1 : 0;
       RSTAT(blockIdx.x, kStSerialAcc, l);
       __syncthreads();
+      used = S.used;
+      head1 = S.head1;
       if (!S.ok) break;
       pos += l;
       ppos = ~0ull;
@@ -1920,7 +1962,8 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
     }
     if (!r.closed && r.end > r.begin) {
       j.state_off = state_words;
-      state_words += (r.policy == KV_POLICY_FIFO) ? (t.u + 1) / 2 : (r.end - r.begin + 1) / 2;
+      // LFU: one count per position, and a spare slot past the end
+      state_words += (r.policy == KV_POLICY_FIFO) ? (t.u + 1) / 2 : (r.end - r.begin + 2) / 2;
       if (r.policy == KV_POLICY_LFU) {
         j.class_off = class_total;
         class_total += class_words;
@@ -2120,7 +2163,7 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
               "failelig %llu failconv %llu serial_acc %llu iters %llu scanned %llu "
               "clk load %llu scan %llu fix %llu jump %llu apply %llu fin %llu x6 %llu x7 %llu x8 %llu "
               "w0 %llu w1 %llu w2 %llu w3 %llu w4 %llu w5 %llu w6 %llu w7 %llu "
-              "f0 %llu f1 %llu f2 %llu f3 %llu f4 %llu\n",
+              "f0 %llu f1 %llu f2 %llu f3 %llu f4 %llu g0 %llu g1 %llu g2 %llu\n",
               jd[q].kind == kJobLfu ? "lfu" : "fifo", q,
               (unsigned long long)jd[q].cap, hs[q][kStFastOk], hs[q][kStFastAcc],
               hs[q][kStFailPool], hs[q][kStFailElig], hs[q][kStFailConv], hs[q][kStSerialAcc],
@@ -2128,7 +2171,8 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
               hs[q][kStT3], hs[q][kStT4], hs[q][kStT5], hs[q][kStT6], hs[q][kStT7], hs[q][kStT8],
               hs[q][kStW0], hs[q][kStW1], hs[q][kStW2], hs[q][kStW3], hs[q][kStW4],
               hs[q][kStW5], hs[q][kStW6], hs[q][kStW7], hs[q][kStF0], hs[q][kStF1],
-              hs[q][kStF2], hs[q][kStF3], hs[q][kStF4]);
+              hs[q][kStF2], hs[q][kStF3], hs[q][kStF4], hs[q][kStG0], hs[q][kStG1],
+              hs[q][kStG2]);
     }
   }
 #endif
