@@ -88,7 +88,7 @@ static_assert(kRIt == 4, "hit words are assembled from four ballots");
 // Optional per-job replay statistics (diagnostics build only).
 #ifdef KV_REPLAY_STATS
 enum { kStFastOk = 0, kStFailPool, kStFailElig, kStFailConv, kStSerialAcc, kStIters,
-       kStScanned, kStFastAcc, kStT0, kStT1, kStT2, kStT3, kStT4, kStT5, kStT6, kStT7, kStT8, kStW0, kStW1, kStW2, kStW3, kStW4, kStW5, kStW6, kStW7, kStF0, kStF1, kStF2, kStF3, kStF4, kStG0, kStG1, kStG2, kStats };
+       kStScanned, kStFastAcc, kStT0, kStT1, kStT2, kStT3, kStT4, kStT5, kStT6, kStT7, kStT8, kStW0, kStW1, kStW2, kStW3, kStW4, kStW5, kStW6, kStW7, kStF0, kStF1, kStF2, kStF3, kStF4, kStG0, kStG1, kStG2, kStQpt, kStNc0, kStNm, kStats };
 __device__ unsigned long long g_rstats[256][kStats];
 __shared__ unsigned long long s_rstats[kStats];  // flushed to g_rstats when the job ends
 __shared__ unsigned long long s_rwave[8];
@@ -862,7 +862,10 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
                                          uint64_t& used_io, uint32_t& head1_io) {
   constexpr bool g1 = G1;
   constexpr int IT = kLChunk / NT;               // accesses per thread
-  constexpr int CPT = (kCand + kLChunk) / NT;    // queue entries per thread
+  // queue entries per thread: the queue rarely holds more than about a
+  // chunk's worth (NT * CPT); a longer one fails the chunk, which is then
+  // retried shorter
+  constexpr int CPT = kLChunk / NT + 1;
   static_assert(IT % 4 == 0 && IT <= 64, "accesses are loaded four at a time");
   const uint32_t tid = threadIdx.x;
   const uint32_t o = j.order;
@@ -1082,6 +1085,13 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     // chunk; thread t holds entries t*qpt .. t*qpt+qpt-1
     const uint32_t nq = nc0 + nm;
     const uint32_t qpt = (nq + NT - 1) / NT;
+    if (qpt > (uint32_t)CPT) {
+      RSTAT(blockIdx.x, kStFailPool, 1);
+      return false;
+    }
+    RSTAT(blockIdx.x, kStQpt, qpt);
+    RSTAT(blockIdx.x, kStNc0, nc0);
+    RSTAT(blockIdx.x, kStNm, nm);
     uint32_t qw[CPT];
     uint32_t xs = 0;
 #pragma unroll
@@ -2163,7 +2173,8 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
               "failelig %llu failconv %llu serial_acc %llu iters %llu scanned %llu "
               "clk load %llu scan %llu fix %llu jump %llu apply %llu fin %llu x6 %llu x7 %llu x8 %llu "
               "w0 %llu w1 %llu w2 %llu w3 %llu w4 %llu w5 %llu w6 %llu w7 %llu "
-              "f0 %llu f1 %llu f2 %llu f3 %llu f4 %llu g0 %llu g1 %llu g2 %llu\n",
+              "f0 %llu f1 %llu f2 %llu f3 %llu f4 %llu g0 %llu g1 %llu g2 %llu qpt %llu "
+              "nc0 %llu nm %llu\n",
               jd[q].kind == kJobLfu ? "lfu" : "fifo", q,
               (unsigned long long)jd[q].cap, hs[q][kStFastOk], hs[q][kStFastAcc],
               hs[q][kStFailPool], hs[q][kStFailElig], hs[q][kStFailConv], hs[q][kStSerialAcc],
@@ -2172,7 +2183,7 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
               hs[q][kStW0], hs[q][kStW1], hs[q][kStW2], hs[q][kStW3], hs[q][kStW4],
               hs[q][kStW5], hs[q][kStW6], hs[q][kStW7], hs[q][kStF0], hs[q][kStF1],
               hs[q][kStF2], hs[q][kStF3], hs[q][kStF4], hs[q][kStG0], hs[q][kStG1],
-              hs[q][kStG2]);
+              hs[q][kStG2], hs[q][kStQpt], hs[q][kStNc0], hs[q][kStNm]);
     }
   }
 #endif
