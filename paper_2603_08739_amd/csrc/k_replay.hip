@@ -196,7 +196,7 @@ __device__ __forceinline__ void store_hits(const bool hit[kRIt], uint64_t c0, ui
     uint64_t word = 0;
 #pragma unroll
     for (int e = 0; e < kRIt; ++e) word |= spread4(bal[e] >> (16 * q)) << e;
-    const uint32_t wloc = (threadIdx.x / 64) * 4 + q;
+    const uint32_t wloc = (uint32_t)wave_id() * 4 + q;
     const uint64_t base = c0 + (uint64_t)wloc * 64;
     if (wloc * 64 < L && base < j.end && base + 64 > j.begin) bits[(base >> 6) - j.word0] = word;
   }
@@ -204,13 +204,22 @@ __device__ __forceinline__ void store_hits(const bool hit[kRIt], uint64_t c0, ui
 
 // IT consecutive accesses [p0, p0 + IT) of a thread (p0 a multiple of IT):
 // vector loads when all are valid.
+// Per-item flags of a thread, one bit per item in a vector register (an
+// array of bools holds one scalar lane mask per item, and scalar registers
+// run short).
+struct ItemBits {
+  uint32_t w = 0;
+  __device__ __forceinline__ bool operator[](int e) const { return (w >> e) & 1u; }
+  __device__ __forceinline__ void set(int e, bool b) { w |= (b ? 1u : 0u) << e; }
+};
+
 // IT consecutive elements from position p0 (a multiple of 4), branch-free:
 // the read position is clamped to n & ~3 (the arrays' slack covers the
 // vector read there; a clamped read only serves invalid items), and items
 // with v[e] false read as 0.
 template <int IT>
 __device__ __forceinline__ void loadn_u32(const uint32_t* __restrict__ a, uint64_t p0, uint64_t n,
-                                          const bool* v, uint32_t* out) {
+                                          const ItemBits& v, uint32_t* out) {
 #pragma unroll
   for (int q = 0; q < IT / 4; ++q) {
     const uint64_t pq = min<uint64_t>(p0 + 4 * q, n & ~3ull);
@@ -224,7 +233,7 @@ __device__ __forceinline__ void loadn_u32(const uint32_t* __restrict__ a, uint64
 
 template <int IT>
 __device__ __forceinline__ void loadn_u8(const uint8_t* __restrict__ a, uint64_t p0, uint64_t n,
-                                         const bool* v, uint32_t* out) {
+                                         const ItemBits& v, uint32_t* out) {
 #pragma unroll
   for (int q = 0; q < IT / 4; ++q) {
     const uint64_t pq = min<uint64_t>(p0 + 4 * q, n & ~3ull);
@@ -257,7 +266,7 @@ __device__ __forceinline__ void store_hits_n(const bool* hit, uint64_t c0, uint3
 #pragma unroll
       for (int m = 0; m < LPW; ++m) word |= ((part >> m) & 1ull) << (m * IT + e);
     }
-    const uint32_t wloc = (threadIdx.x / 64) * IT + q;
+    const uint32_t wloc = (uint32_t)wave_id() * IT + q;
     const uint64_t base = c0 + (uint64_t)wloc * 64;
     if (wloc * 64 < L && base < j.end && base + 64 > j.begin) bits[(base >> 6) - j.word0] = word;
   }
@@ -800,7 +809,7 @@ __device__ __forceinline__ void block_suffix_min_flag(uint32_t v, bool flag, uin
   constexpr int NW = NT / 64;
   constexpr int kInf = 0x7FFFFFFF;
   const uint32_t lane = lane_id();
-  const int w = threadIdx.x / 64;
+  const int w = wave_id();
   // inclusive suffix minimum within rows of 16 lanes (row_shl: from lane + n)
   int x = (int)v;
   x = min(x, __builtin_amdgcn_update_dpp(kInf, x, 0x101, 0xf, 0xf, false));
@@ -876,9 +885,9 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   const uint32_t l0 = tid * IT;
   const uint32_t p0 = c0 + l0;
   RCLK(t_a);
-  bool v[IT];
+  ItemBits v;
 #pragma unroll
-  for (int e = 0; e < IT; ++e) v[e] = l0 + e < L && p0 + e >= jb;
+  for (int e = 0; e < IT; ++e) v.set(e, l0 + e < L && p0 + e >= jb);
   uint32_t ww[IT], gg[IT], kk[IT], nx[IT], f0[IT];
   bool cm[IT], res0[IT];
   if (have_pref) {

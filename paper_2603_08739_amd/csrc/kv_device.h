@@ -9,6 +9,12 @@ namespace kv {
 
 __device__ __forceinline__ uint32_t lane_id() { return __lane_id(); }
 
+// The wave's index in the block, as a wave-uniform (scalar) value: tests on
+// it need no per-lane masks.
+__device__ __forceinline__ int wave_id() {
+  return __builtin_amdgcn_readfirstlane((int)(threadIdx.x / 64));
+}
+
 __device__ __forceinline__ uint64_t lanemask_lt() {
   const uint32_t l = lane_id();
   return (l == 0) ? 0ull : (~0ull >> (64 - l));
@@ -47,7 +53,7 @@ __device__ __forceinline__ void block_excl_scan2_u32(uint32_t a, uint32_t b, uin
                                                      uint32_t& pa, uint32_t& pb, uint32_t& ta,
                                                      uint32_t& tb) {
   constexpr int NW = NT / 64;
-  const int w = threadIdx.x / 64;
+  const int w = wave_id();
   const uint32_t ia = wave_incl_scan_u32(a), ib = wave_incl_scan_u32(b);
   if (lane_id() == 63) {
     sh[w] = ia;
@@ -73,7 +79,7 @@ __device__ __forceinline__ void block_excl_scan2_u32(uint32_t a, uint32_t b, uin
 template <int NT, bool Trail = true>
 __device__ __forceinline__ uint32_t block_excl_scan_u32(uint32_t a, uint32_t* sh, uint32_t& ta) {
   constexpr int NW = NT / 64;
-  const int w = threadIdx.x / 64;
+  const int w = wave_id();
   const uint32_t ia = wave_incl_scan_u32(a);
   if (lane_id() == 63) sh[w] = ia;
   __syncthreads();
@@ -148,7 +154,7 @@ __device__ __forceinline__ T wave_sum(T v) {
 template <int NT, class T>
 __device__ __forceinline__ T block_excl_scan(T v, T* sh, T* total) {
   constexpr int NW = NT / 64;
-  const int w = threadIdx.x / 64;
+  const int w = wave_id();
   T inc = wave_incl_scan(v);
   if (lane_id() == 63) sh[w] = inc;
   __syncthreads();
@@ -171,7 +177,7 @@ __device__ __forceinline__ T block_excl_scan(T v, T* sh, T* total) {
 template <int NT, class T>
 __device__ __forceinline__ T block_sum(T v, T* sh) {
   constexpr int NW = NT / 64;
-  const int w = threadIdx.x / 64;
+  const int w = wave_id();
   T s = wave_sum(v);
   if (lane_id() == 0) sh[w] = s;
   __syncthreads();
