@@ -260,11 +260,31 @@ __device__ __forceinline__ void store_hits_n(const bool* hit, uint64_t c0, uint3
   asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(q));
   if (q < (uint32_t)IT) {
     uint64_t word = 0;
+    if constexpr (IT == 4) {
+      // bit m of item e's 16-bit slice goes to bit 4m + e: spread eight
+      // bits at a time to every fourth bit
+      auto spread8 = [](uint32_t x) {
+        x &= 0xFFu;
+        x = (x | (x << 12)) & 0x000F000Fu;
+        x = (x | (x << 6)) & 0x03030303u;
+        x = (x | (x << 3)) & 0x11111111u;
+        return x;
+      };
+      uint32_t lo = 0, hi = 0;
 #pragma unroll
-    for (int e = 0; e < IT; ++e) {
-      const uint64_t part = bal[e] >> (LPW * q);
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t part = (uint32_t)(bal[e] >> (16 * q));
+        lo |= spread8(part) << e;
+        hi |= spread8(part >> 8) << e;
+      }
+      word = ((uint64_t)hi << 32) | lo;
+    } else {
 #pragma unroll
-      for (int m = 0; m < LPW; ++m) word |= ((part >> m) & 1ull) << (m * IT + e);
+      for (int e = 0; e < IT; ++e) {
+        const uint64_t part = bal[e] >> (LPW * q);
+#pragma unroll
+        for (int m = 0; m < LPW; ++m) word |= ((part >> m) & 1ull) << (m * IT + e);
+      }
     }
     const uint32_t wloc = (uint32_t)wave_id() * IT + q;
     const uint64_t base = c0 + (uint64_t)wloc * 64;
