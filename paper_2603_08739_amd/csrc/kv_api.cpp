@@ -93,6 +93,33 @@ kv_status hip_fail(hipError_t e, const char* what) {
   return fail(KV_ERR_DEVICE, std::string(hipGetErrorString(e)) + " in " + what);
 }
 
+// Device blocks released by DevBufs are kept per device and handed out
+// again (a trace's workspaces reach ~100 GiB at full scale; allocating and
+// freeing that much for every trace fragments the device's memory and slows
+// the random-access kernels that follow).  A failed hipMalloc empties the
+// device's cache and tries once more; the cache keeps at most half of the
+// device's memory, so that other users of the device are not starved.
+namespace {
+std::mutex g_pool_mu;
+std::multimap<size_t, void*> g_pool[64];  // per device: block size -> block
+size_t g_pool_bytes[64] = {};
+size_t g_pool_limit[64] = {};
+
+size_t block_size(size_t b) {
+  // 256 bytes of slack past the end: kernels may issue (and then discard)
+  // vector loads of up to 16 bytes at the last valid index
+  const size_t need = b + 256;
+  const size_t g = need >= (1u << 20) ? (2u << 20) : 4096;
+  return (need + g - 1) / g * g;
+}
+
+void pool_flush(int dev) {
+  for (auto& kv : g_pool[dev]) (void)hipFree(kv.second);
+  g_pool[dev].clear();
+  g_pool_bytes[dev] = 0;
+}
+}  // namespace
+
 kv_status DevBuf::reserve(size_t b) {
   if (b <= bytes && p) return KV_OK;
   release();
@@ -100,23 +127,65 @@ kv_status DevBuf::reserve(size_t b) {
   const uint64_t cap = mem_cap();
   if (cap && g_bytes.load() + b > cap)
     return fail(KV_ERR_NOMEM, "device memory cap reached (test limit)");
-  void* q = nullptr;
-  // 256 bytes of slack past the end: kernels may issue (and then discard)
-  // vector loads of up to 16 bytes at the last valid index
-  hipError_t e = hipMalloc(&q, b + 256);
-  if (e != hipSuccess) {
+  int d = 0;
+  if (hipGetDevice(&d) != hipSuccess || d < 0 || d >= 64) {
     (void)hipGetLastError();
-    return fail(KV_ERR_NOMEM, "hipMalloc of " + std::to_string(b) + " bytes failed");
+    return fail(KV_ERR_DEVICE, "no current device");
   }
-  p = q;
-  bytes = b;
+  const size_t sz = block_size(b);
+  void* q = nullptr;
+  {
+    std::lock_guard<std::mutex> lk(g_pool_mu);
+    // a cached block of at least sz and at most twice that
+    auto it = g_pool[d].lower_bound(sz);
+    if (it != g_pool[d].end() && it->first <= 2 * sz) {
+      q = it->second;
+      p = q;
+      bytes = b;
+      cap_bytes = it->first;
+      g_pool_bytes[d] -= it->first;
+      g_pool[d].erase(it);
+    }
+  }
+  if (!q) {
+    hipError_t e = hipMalloc(&q, sz);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      {
+        std::lock_guard<std::mutex> lk(g_pool_mu);
+        pool_flush(d);
+      }
+      e = hipMalloc(&q, sz);
+      if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(KV_ERR_NOMEM, "hipMalloc of " + std::to_string(b) + " bytes failed");
+      }
+    }
+    p = q;
+    bytes = b;
+    cap_bytes = sz;
+  }
+  dev = d;
   g_bytes += b;
   return KV_OK;
 }
 
 void DevBuf::release() {
   if (p) {
-    (void)hipFree(p);
+    std::lock_guard<std::mutex> lk(g_pool_mu);
+    if (!g_pool_limit[dev]) {
+      size_t fr = 0, tot = 0;
+      int cur = 0;
+      if (hipGetDevice(&cur) == hipSuccess && cur == dev && hipMemGetInfo(&fr, &tot) == hipSuccess)
+        g_pool_limit[dev] = tot / 2;
+      (void)hipGetLastError();
+    }
+    if (g_pool_bytes[dev] + cap_bytes <= g_pool_limit[dev]) {
+      g_pool[dev].emplace(cap_bytes, p);
+      g_pool_bytes[dev] += cap_bytes;
+    } else {
+      (void)hipFree(p);
+    }
     g_bytes -= bytes;
   }
   p = nullptr;

@@ -30,10 +30,13 @@ kv_status hip_fail(hipError_t e, const char* what);
     if (e_ != hipSuccess) return ::kv::hip_fail(e_, #call);   \
   } while (0)
 
-// A device allocation owned by its holder.
+// A device allocation owned by its holder; released blocks return to a
+// per-device cache for the next reserve.
 struct DevBuf {
   void* p = nullptr;
-  size_t bytes = 0;
+  size_t bytes = 0;      // bytes asked for
+  size_t cap_bytes = 0;  // size of the block held
+  int dev = 0;           // device the block lives on
   DevBuf() = default;
   DevBuf(const DevBuf&) = delete;
   DevBuf& operator=(const DevBuf&) = delete;
