@@ -849,15 +849,18 @@ __device__ __forceinline__ void block_suffix_min_flag(uint32_t v, bool flag, uin
   const bool wflag = __ballot(flag) != 0ull;
   if (lane == 0) sh[w] = (uint32_t)wmin | (wflag ? 0x80000000u : 0u);
   __syncthreads();
-  bool f = false;
-#pragma unroll
-  for (int ww = 0; ww < NW; ++ww) {
-    const uint32_t y = sh[ww];
-    r = (ww > w) ? min(r, (int)(y & 0x7FFFFFFFu)) : r;
-    f |= (y >> 31) != 0u;
-  }
+  // the waves' minima and flags, one per lane of the first row: a suffix
+  // minimum across the row, read at wave w + 1
+  static_assert(NW <= 16, "one row of lanes holds the wave minima");
+  const uint32_t y = lane < (uint32_t)NW ? sh[lane] : (uint32_t)kInf;
+  any = __ballot((y >> 31) != 0u) != 0ull;
+  int z = (int)(y & 0x7FFFFFFFu);
+  z = min(z, __builtin_amdgcn_update_dpp(kInf, z, 0x101, 0xf, 0xf, false));
+  z = min(z, __builtin_amdgcn_update_dpp(kInf, z, 0x102, 0xf, 0xf, false));
+  z = min(z, __builtin_amdgcn_update_dpp(kInf, z, 0x104, 0xf, 0xf, false));
+  z = min(z, __builtin_amdgcn_update_dpp(kInf, z, 0x108, 0xf, 0xf, false));
+  if (w + 1 < NW) r = min(r, __builtin_amdgcn_readlane(z, w + 1));
   smin = (uint32_t)r;
-  any = f;
 }
 
 // One chunk [c0, c1) without the serial walk.

@@ -44,6 +44,30 @@ __device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t v) {
   return v;
 }
 
+// Inclusive prefix sum over the first row of 16 lanes (lanes past 15 hold
+// partial sums of their own rows, unused here).
+__device__ __forceinline__ uint32_t row_incl_scan_u32(uint32_t v) {
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xf, 0xf, false);  // row_shr:1
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xf, 0xf, false);  // row_shr:2
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xf, 0xf, false);  // row_shr:4
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xf, 0xf, false);  // row_shr:8
+  return v;
+}
+
+// The wave totals `sh[0..NW)` combined for wave w: the sum over waves below
+// w and the sum over all, as wave-uniform values.  Lane i reads total i and
+// a row scan adds them up, so every thread does one LDS read.
+template <int NW>
+__device__ __forceinline__ void wave_totals(const uint32_t* sh, int w, uint32_t& below,
+                                            uint32_t& all) {
+  static_assert(NW <= 16, "one row of lanes holds the wave totals");
+  const uint32_t lane = lane_id();
+  const uint32_t y = lane < (uint32_t)NW ? sh[lane] : 0u;
+  const int incl = (int)row_incl_scan_u32(y);
+  all = (uint32_t)__builtin_amdgcn_readlane(incl, NW - 1);
+  below = w ? (uint32_t)__builtin_amdgcn_readlane(incl, w - 1) : 0u;
+}
+
 // Exclusive prefix sums of two 32-bit values over a block of NT threads.
 // `sh` holds 2 * (NT / 64) words of shared memory; two barriers.  With
 // Trail = false the second barrier (which lets the next call reuse `sh`) is
@@ -60,15 +84,9 @@ __device__ __forceinline__ void block_excl_scan2_u32(uint32_t a, uint32_t b, uin
     sh[NW + w] = ib;
   }
   __syncthreads();
-  uint32_t sa = 0, sb = 0, xa = 0, xb = 0;
-#pragma unroll
-  for (int i = 0; i < NW; ++i) {
-    const uint32_t ya = sh[i], yb = sh[NW + i];
-    xa += (i < w) ? ya : 0u;
-    xb += (i < w) ? yb : 0u;
-    sa += ya;
-    sb += yb;
-  }
+  uint32_t sa, sb, xa, xb;
+  wave_totals<NW>(sh, w, xa, sa);
+  wave_totals<NW>(sh + NW, w, xb, sb);
   if constexpr (Trail) __syncthreads();
   pa = xa + ia - a;
   pb = xb + ib - b;
@@ -83,13 +101,8 @@ __device__ __forceinline__ uint32_t block_excl_scan_u32(uint32_t a, uint32_t* sh
   const uint32_t ia = wave_incl_scan_u32(a);
   if (lane_id() == 63) sh[w] = ia;
   __syncthreads();
-  uint32_t xa = 0, sa = 0;
-#pragma unroll
-  for (int i = 0; i < NW; ++i) {
-    const uint32_t ya = sh[i];
-    xa += (i < w) ? ya : 0u;
-    sa += ya;
-  }
+  uint32_t xa, sa;
+  wave_totals<NW>(sh, w, xa, sa);
   if constexpr (Trail) __syncthreads();
   ta = sa;
   return xa + ia - a;
