@@ -615,7 +615,7 @@ struct LfuLds {
   uint32_t red[2][2 * kRNW];  // block scans, alternating (no trailing barrier)
   uint32_t sfx[2 * kRNW];
   uint32_t anyflag[2];
-  uint32_t tot8[8];           // chunk totals: ins, ins_w, ev, ev_w, victim w, last old, last new, n1
+  uint32_t tot8[8];           // chunk totals: ev | n1 << 16, evicted weight, last old, last new
   uint64_t cnz[kLdsClassWords];
   uint64_t used;              // cached weight
   uint32_t fmin, head1;       // lowest nonempty class; no live count-1 member before head1
@@ -1074,7 +1074,8 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   RTIME(kStT1, t_b, t_c);
   RWAVE(2, t_a);
   // ---- fixed point over (misses, promotions, evictions)
-  uint32_t itot = itot0;
+  uint32_t itot = itot0;   // weight of the chunk's misses (insertions)
+  uint32_t nmiss = nm0;     // and their number
   bool converged = ev0 == 0;
   bool capnow[IT];  // capacity misses of the latest iteration
 #pragma unroll
@@ -1112,6 +1113,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       }
       __syncthreads();
     }
+    nmiss = nm;
     const uint32_t evtot = (used0 + itot > j.cap) ? (uint32_t)(used0 + itot - j.cap) : 0u;
     // the eviction queue: nc0 old entries, then the nm insertions of the
     // chunk; thread t holds entries t*qpt .. t*qpt+qpt-1
@@ -1319,9 +1321,10 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   RCLK(t_e);
   RTIME(kStT3, t_d, t_e);
   RWAVE(4, t_a);
-  // per-thread partials: insertions, evictions, victim weight, last entries taken
-  uint32_t p_ins = 0, p_insw = 0, p_ev = 0, p_evw = 0, p_vw = 0, p_lastp = 0, p_lastm = 0,
-           p_n1 = 0;
+  // per-thread partials: evictions (and, 16 bits up, old count-1 entries
+  // leaving class 1), evicted weight, last entries taken.  Insertions are
+  // the misses, counted by the fixed point.
+  uint32_t p_evn = 0, p_vw = 0, p_lastp = 0, p_lastm = 0;
   // old entries evicted (loads issued unconditionally, several in flight)
   for (uint32_t k = tid; k < nc0; k += NT) {
     const bool cons = S.ccons[k] != 0;
@@ -1329,8 +1332,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     const bool untouched = S.ca[k] == kInf16;
     if (!cons) continue;
     if (g1) {
-      ++p_ev;
-      p_evw += w;
+      ++p_evn;
     } else {
       const uint32_t g = a.g8[o][S.cq[k]];
       atomicAdd(&gc.ev[g], 1ull);
@@ -1338,8 +1340,9 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     }
     p_vw += w;
     p_lastp = max(p_lastp, k + 1);
-    if (untouched) ++p_n1;  // not touched again in the chunk: leaves class 1 for good
-                            // (head1 passes it: no store)
+    // not touched again in the chunk: leaves class 1 for good (head1 passes
+    // it: no store)
+    if (untouched) p_evn += 1u << 16;
   }
   RCLK(t_e1);
   RTIME(kStT6, t_e, t_e1);
@@ -1370,10 +1373,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     const uint32_t loc = l0 + e;
     const bool cons = mc[e] != 0;  // inserted here, evicted later in the chunk
     if (g1) {
-      ++p_ins;
-      p_insw += ww[e];
-      p_ev += cons ? 1u : 0u;
-      p_evw += cons ? ww[e] : 0u;
+      p_evn += cons ? 1u : 0u;
     } else {
       atomicAdd(&gc.ins[gg[e]], 1ull);
       atomicAdd(&gc.insw[gg[e]], (unsigned long long)ww[e]);
@@ -1432,17 +1432,14 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     if (d12[1]) atomicAdd(&S.ccnt[2], (uint32_t)d12[1]);
   }
   {
-    const uint32_t r[8] = {wave_add_dpp(p_ins), wave_add_dpp(p_insw), wave_add_dpp(p_ev),
-                           wave_add_dpp(p_evw), wave_add_dpp(p_vw), wave_max_dpp(p_lastp),
-                           wave_max_dpp(p_lastm), wave_add_dpp(p_n1)};
+    const uint32_t r[4] = {wave_add_dpp(p_evn), wave_add_dpp(p_vw), wave_max_dpp(p_lastp),
+                           wave_max_dpp(p_lastm)};
     if (lane_id() == 0) {
-#pragma unroll
-      for (int f = 0; f < 8; ++f) {
-        if (!r[f]) continue;
-        if (f == 5 || f == 6) atomicMax(&S.tot8[f], r[f]);
-        else atomicAdd(&S.tot8[f], r[f]);
-      }
-      if (r[7]) atomicSub(&S.ccnt[1], r[7]);
+      if (r[0]) atomicAdd(&S.tot8[0], r[0]);
+      if (r[1]) atomicAdd(&S.tot8[1], r[1]);
+      if (r[2]) atomicMax(&S.tot8[2], r[2]);
+      if (r[3]) atomicMax(&S.tot8[3], r[3]);
+      if (r[0] >> 16) atomicSub(&S.ccnt[1], r[0] >> 16);
     }
   }
   RWAVE(5, t_a);
@@ -1467,18 +1464,17 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   // every thread takes the chunk totals: the cached weight and the count-1
   // queue head go on in registers, with no barrier to end the chunk (the
   // next chunk's writes touch nothing read here)
-  uint32_t t[8];
-#pragma unroll
-  for (int f = 0; f < 8; ++f) t[f] = S.tot8[f];
+  const uint32_t t_ev = S.tot8[0] & 0xFFFFu, t_vw = S.tot8[1], t_lastp = S.tot8[2],
+                 t_lastm = S.tot8[3];
   if (g1 && tid == 0) {
-    gc.ins[g0] += t[0];
-    gc.insw[g0] += t[1];
-    gc.ev[g0] += t[2];
-    gc.evw[g0] += t[3];
+    gc.ins[g0] += nmiss;
+    gc.insw[g0] += itot;
+    gc.ev[g0] += t_ev;
+    gc.evw[g0] += t_vw;
   }
-  used_io = used0 + itot - t[4];
-  if (t[6]) head1_io = c0 + t[6];                 // last new entry taken + 1
-  else if (t[5]) head1_io = S.cq[t[5] - 1] + 1;   // last old entry taken + 1
+  used_io = used0 + itot - t_vw;
+  if (t_lastm) head1_io = c0 + t_lastm;                 // last new entry taken + 1
+  else if (t_lastp) head1_io = S.cq[t_lastp - 1] + 1;   // last old entry taken + 1
   else head1_io = h;
   RWAVE(6, t_a);
   RCLK(t_f2);
