@@ -71,6 +71,7 @@ constexpr uint32_t kRChunk = kRNT * kRIt;  // longest chunk
 constexpr uint32_t kCand = 4096;           // LFU eviction candidates per chunk
 constexpr int kCScan = 2;                  // candidate positions per thread and pass
 constexpr uint32_t kMinFast = 256;         // shorter LFU chunks go serial
+constexpr uint32_t kHeadLds = 64;          // class heads held in LDS during a serial walk
 constexpr uint16_t kInf16 = 0xFFFF;
 #ifndef KV_LFU_NT
 #define KV_LFU_NT 1024
@@ -88,7 +89,7 @@ static_assert(kRIt == 4, "hit words are assembled from four ballots");
 // Optional per-job replay statistics (diagnostics build only).
 #ifdef KV_REPLAY_STATS
 enum { kStFastOk = 0, kStFailPool, kStFailElig, kStFailConv, kStSerialAcc, kStIters,
-       kStScanned, kStFastAcc, kStT0, kStT1, kStT2, kStT3, kStT4, kStT5, kStT6, kStT7, kStT8, kStW0, kStW1, kStW2, kStW3, kStW4, kStW5, kStW6, kStW7, kStF0, kStF1, kStF2, kStF3, kStF4, kStG0, kStG1, kStG2, kStQpt, kStNc0, kStNm, kStats };
+       kStScanned, kStFastAcc, kStT0, kStT1, kStT2, kStT3, kStT4, kStT5, kStT6, kStT7, kStT8, kStW0, kStW1, kStW2, kStW3, kStW4, kStW5, kStW6, kStW7, kStF0, kStF1, kStF2, kStF3, kStF4, kStG0, kStG1, kStG2, kStQpt, kStNc0, kStNm, kStJob, kStSer, kStats };
 __device__ unsigned long long g_rstats[256][kStats];
 __shared__ unsigned long long s_rstats[kStats];  // flushed to g_rstats when the job ends
 __shared__ unsigned long long s_rwave[8];
@@ -645,12 +646,24 @@ struct LfuLds {
   // apply: a block's count at the chunk start, at its first touch
   uint32_t mneed[kLChunk];
   uint32_t ccnt[kLdsClass];   // members of class f < kLdsClass
-  // count-1 residents from before the chunk, oldest first
-  uint8_t cw[kCand];
-  uint8_t cskip[kCand];
-  uint8_t ccons[kCand];
-  uint16_t ca[kCand];         // first touch inside the chunk or kInf16
-  uint32_t cq[kCand];         // position of their last touch
+  union {
+    struct {                  // count-1 residents from before the chunk, oldest first
+      uint8_t cw[kCand];
+      uint8_t cskip[kCand];
+      uint8_t ccons[kCand];
+      uint16_t ca[kCand];     // first touch inside the chunk or kInf16
+      uint32_t cq[kCand];     // position of their last touch
+    };
+    struct {                  // serial walk over at most kMinFast accesses
+      uint32_t skey[kMinFast];   // link
+      uint32_t snx[kMinFast];    // next access
+      uint32_t s0[kMinFast];     // count stored at a link before the walk
+      uint32_t scnt[kMinFast];   // count stored here by the walk
+      uint8_t sw[kMinFast];      // weight
+      uint8_t sg[kMinFast];      // group
+      uint32_t shead[kHeadLds];  // heads of the classes below kHeadLds
+    };
+  };
   // the next full chunk, per access: its block link and the stored count
   // at that link (each thread reads and writes only its own accesses)
   alignas(16) uint32_t pkey[kLChunk];
@@ -728,27 +741,62 @@ __device__ __forceinline__ void class_add_par(const Classes& c, uint32_t f, int 
   if (d > 0) atomicAdd(&c.lcnt[f], 1u); else atomicSub(&c.lcnt[f], 1u);
 }
 
-// Exact replay of [p0, p1) by one thread (thread 0); returns false if the
-// state is found inconsistent.
-__device__ __forceinline__ bool lfu_serial_range(const JobDev& j, const JobArgs& a,
-                                                 uint32_t* __restrict__ cnt, uint32_t* head,
-                                                 const Classes& cl, LfuLds& S, GroupCounters& gc,
-                                                 uint64_t* __restrict__ bits, uint64_t p0,
-                                                 uint64_t p1) {
+// The serial walk's inputs for [p0, p1) (at most kMinFast accesses), staged
+// in LDS by the whole block: per access its link, next access, weight and
+// group, and for a link before p0 the count stored there; the heads of the
+// classes below kHeadLds.
+template <int NT>
+__device__ __forceinline__ void lfu_serial_stage(const JobDev& j, const JobArgs& a,
+                                                 const uint32_t* __restrict__ cnt,
+                                                 const uint32_t* head, uint32_t n_class,
+                                                 LfuLds& S, uint32_t p0, uint32_t p1) {
+  const uint32_t o = j.order, b0 = (uint32_t)j.begin;
+  for (uint32_t x = threadIdx.x; x < p1 - p0; x += NT) {
+    const uint32_t i = p0 + x;
+    uint32_t k = 0, nx = kNone, w = 0, g = 0, c = 0;
+    if (i >= b0) {
+      k = a.key[o][i];
+      nx = a.nxt[o][i];
+      w = a.w8[o][i];
+      g = a.g8[o][i];
+      if (k != 0 && k - 1 < p0) c = cnt[k - 1 - b0];
+    }
+    S.skey[x] = k;
+    S.snx[x] = nx;
+    S.sw[x] = (uint8_t)w;
+    S.sg[x] = (uint8_t)g;
+    S.s0[x] = c;
+    S.scnt[x] = 0;
+  }
+  if (threadIdx.x < kHeadLds && threadIdx.x < n_class) S.shead[threadIdx.x] = head[threadIdx.x];
+}
+
+// Exact replay of the staged [p0, p1) by the 64 lanes of one wavefront.
+// Every lane holds the same state and applies the same updates (stores of
+// equal values to one address); only the victim search spreads candidate
+// positions over the lanes.  Returns false if the state is found
+// inconsistent.
+__device__ __forceinline__ bool lfu_serial_wave(const JobDev& j, const JobArgs& a,
+                                                uint32_t* __restrict__ cnt, uint32_t* head,
+                                                uint32_t n_class, const Classes& cl, LfuLds& S,
+                                                GroupCounters& gc, uint64_t* __restrict__ bits,
+                                                uint32_t p0, uint32_t p1, uint64_t& used_io,
+                                                uint32_t& head1_io) {
   const uint32_t o = j.order;
-  const uint32_t* __restrict__ key = a.key[o];
-  const uint32_t* __restrict__ nxt = a.nxt[o];
-  const uint64_t b0 = j.begin;
-  head[1] = S.head1;
-  uint64_t used = S.used;
+  const uint32_t b0 = (uint32_t)j.begin;
+  const uint32_t lane = lane_id();
+  uint32_t head1 = head1_io;
+  uint64_t used = used_io;
   uint32_t fmin = S.fmin;
   uint64_t word = 0;
   bool ok = true;
-  for (uint64_t i = p0; i < p1 && ok; ++i) {
-    if (i >= j.begin) {
-      const uint32_t w = a.w8[o][i];
-      const uint32_t k = key[i];
-      const uint32_t f = k ? lfu_live_count(cnt[k - 1 - b0], k - 1, head[1]) : 0u;
+  for (uint32_t i = p0; i < p1 && ok; ++i) {
+    const uint32_t x = i - p0;
+    if (i >= b0) {
+      const uint32_t w = S.sw[x];
+      const uint32_t k = S.skey[x];
+      uint32_t f = 0;
+      if (k != 0) f = lfu_live_count(k - 1 >= p0 ? S.scnt[k - 1 - p0] : S.s0[x], k - 1, head1);
       if (f) {
         word |= 1ull << (i & 63);
         const uint32_t f1 = f + 1;
@@ -758,37 +806,71 @@ __device__ __forceinline__ bool lfu_serial_range(const JobDev& j, const JobArgs&
           class_add1(cl, cf1, +1);
           if (cf == fmin && class_count(cl, cf) == 0) fmin = cf1;
         }
+        S.scnt[x] = f1;
         cnt[i - b0] = f1;
       } else {
         while (used + w > j.cap) {
-          uint64_t q;
+          // the victim: the oldest live member of class fmin (it lies
+          // before position i; the bound only guards against corrupted
+          // state), or in the top class the least (count, latest access)
+          uint32_t q = i, nq = kNone, vw = 0, vg = 0;
           if (fmin < kTopClass) {
-            // the oldest live member of class fmin lies before position i;
-            // the bound only guards against corrupted state
-            for (q = head[fmin]; q < i; ++q) {
-              const uint32_t nq = nxt[q];
-              if (cnt[q - b0] == fmin && (nq == kNone || nq >= i)) break;
+            const uint32_t h0 = fmin == 1 ? head1 : (fmin < kHeadLds ? S.shead[fmin] : head[fmin]);
+            for (uint32_t base = h0; base < i; base += 64) {
+              const uint32_t r = base + lane;
+              uint32_t c = 0, nr = kNone, wr = 0, gr = 0;
+              if (r < i) {
+                if (r >= p0) {
+                  c = S.scnt[r - p0];
+                  nr = S.snx[r - p0];
+                  wr = S.sw[r - p0];
+                  gr = S.sg[r - p0];
+                } else {
+                  c = cnt[r - b0];
+                  nr = a.nxt[o][r];
+                  wr = a.w8[o][r];
+                  gr = a.g8[o][r];
+                }
+              }
+              const uint64_t m = __ballot(r < i && c == fmin && (nr == kNone || nr >= i));
+              if (m) {
+                const int l = __ffsll((long long)m) - 1;
+                q = base + (uint32_t)l;
+                nq = (uint32_t)__builtin_amdgcn_readlane((int)nr, l);
+                vw = (uint32_t)__builtin_amdgcn_readlane((int)wr, l);
+                vg = (uint32_t)__builtin_amdgcn_readlane((int)gr, l);
+                break;
+              }
             }
           } else {
-            // top class: the least count, then the earliest latest access
-            uint32_t best = 0xFFFFFFFFu;
-            q = i;
-            for (uint64_t r = b0; r < i; ++r) {
-              const uint32_t c = cnt[r - b0];
-              if (c < kTopClass || c >= best) continue;
-              const uint32_t nr = nxt[r];
+            uint64_t best = ~0ull;  // count << 32 | position
+            for (uint32_t r = b0 + lane; r < i; r += 64) {
+              const uint32_t c = r >= p0 ? S.scnt[r - p0] : cnt[r - b0];
+              if (c < kTopClass) continue;
+              const uint32_t nr = r >= p0 ? S.snx[r - p0] : a.nxt[o][r];
               if (nr != kNone && nr < i) continue;
-              best = c;
-              q = r;
+              best = min(best, ((uint64_t)c << 32) | r);
+            }
+#pragma unroll
+            for (int d = 32; d >= 1; d >>= 1) best = min(best, (uint64_t)__shfl_xor(best, d, 64));
+            if (best != ~0ull) {
+              q = (uint32_t)best;
+              nq = q >= p0 ? S.snx[q - p0] : a.nxt[o][q];
+              vw = q >= p0 ? S.sw[q - p0] : a.w8[o][q];
+              vg = q >= p0 ? S.sg[q - p0] : a.g8[o][q];
             }
           }
           if (q >= i) {
             ok = false;
             break;
           }
-          if (fmin < kTopClass) head[fmin] = (uint32_t)(q + 1);
+          if (fmin == 1) head1 = q + 1;
+          else if (fmin < kHeadLds) S.shead[fmin] = q + 1;
+          else if (fmin < kTopClass) head[fmin] = q + 1;
           cnt[q - b0] = 0;
-          const uint32_t vw = a.w8[o][q], vg = a.g8[o][q];
+          // the access that links to q reads the eviction
+          if (q >= p0) S.scnt[q - p0] = 0;
+          else if (nq != kNone && nq < p1) S.s0[nq - p0] = 0;
           used -= vw;
           gc.ev[vg] += 1;
           gc.evw[vg] += vw;
@@ -798,23 +880,25 @@ __device__ __forceinline__ bool lfu_serial_range(const JobDev& j, const JobArgs&
             if (nf != 0xFFFFFFFFu) fmin = nf;
           }
         }
+        S.scnt[x] = 1;
         cnt[i - b0] = 1;
         class_add1(cl, 1, +1);
         fmin = 1;
         used += w;
-        const uint32_t g = a.g8[o][i];
+        const uint32_t g = S.sg[x];
         gc.ins[g] += 1;
         gc.insw[g] += w;
       }
     }
     if ((i & 63) == 63 || i + 1 == p1) {
-      if (i >= j.begin || (i | 63) >= j.begin) bits[(i >> 6) - j.word0] = word;
+      if (i >= b0 || (i | 63) >= b0) bits[(i >> 6) - j.word0] = word;
       word = 0;
     }
   }
-  S.used = used;
+  if (lane >= 2 && lane < kHeadLds && lane < n_class) head[lane] = S.shead[lane];
   S.fmin = fmin;
-  S.head1 = head[1];
+  used_io = used;
+  head1_io = head1;
   return ok;
 }
 
@@ -1537,13 +1621,21 @@ __device__ __forceinline__ void lfu_chunked(const JobDev& j, const JobArgs& a,
     } else {
       __syncthreads();
       class_bits_rebuild<NT>(S);
-      if (tid == 0) {
-        S.used = used;
-        S.head1 = head1;
-      }
+      lfu_serial_stage<NT>(j, a, cnt, head, a.n_class, S, (uint32_t)pos, (uint32_t)(pos + l));
       __syncthreads();
-      if (tid == 0) S.ok = lfu_serial_range(j, a, cnt, head, cl, S, gc, bits, pos, pos + l) ? 1 : 0;
+      RCLK(t_s0);
+      if (wave_id() == 0) {
+        const bool ok = lfu_serial_wave(j, a, cnt, head, a.n_class, cl, S, gc, bits,
+                                        (uint32_t)pos, (uint32_t)(pos + l), used, head1);
+        if (lane_id() == 0) {
+          S.ok = ok ? 1 : 0;
+          S.used = used;
+          S.head1 = head1;
+        }
+      }
       RSTAT(blockIdx.x, kStSerialAcc, l);
+      RCLK(t_s1);
+      RTIME(kStSer, t_s0, t_s1);
       __syncthreads();
       used = S.used;
       head1 = S.head1;
@@ -1623,6 +1715,9 @@ __global__ __launch_bounds__(NT) void k_replay_lfu(const JobDev* __restrict__ jo
   JobDev j = jobs[blockIdx.x];
   if (j.closed || j.kind != kJobLfu) return;
   if (lfu_one_group(j, a_in.n_groups) != G1) return;
+#ifdef KV_REPLAY_STATS
+  const unsigned long long tj0 = wall_clock64();
+#endif
   const JobArgs a = job_args(a_in, j);
   const uint32_t tid = threadIdx.x;
   if (tid < KV_MAX_GROUPS) gc.ins[tid] = gc.insw[tid] = gc.ev[tid] = gc.evw[tid] = 0;
@@ -1640,6 +1735,8 @@ __global__ __launch_bounds__(NT) void k_replay_lfu(const JobDev* __restrict__ jo
   write_counters(gc, a.n_groups, cnt);
   if (tid == 0 && !ok) cnt[0] = ~0ull;  // poison: surfaced as an impossible count
 #ifdef KV_REPLAY_STATS
+  RSTAT(blockIdx.x, kStJob, wall_clock64() - tj0);
+  __syncthreads();
   if (tid < kStats) g_rstats[blockIdx.x & 255][tid] += s_rstats[tid];
 #endif
 }
@@ -2202,7 +2299,7 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
               "clk load %llu scan %llu fix %llu jump %llu apply %llu fin %llu x6 %llu x7 %llu x8 %llu "
               "w0 %llu w1 %llu w2 %llu w3 %llu w4 %llu w5 %llu w6 %llu w7 %llu "
               "f0 %llu f1 %llu f2 %llu f3 %llu f4 %llu g0 %llu g1 %llu g2 %llu qpt %llu "
-              "nc0 %llu nm %llu\n",
+              "nc0 %llu nm %llu job %llu ser %llu\n",
               jd[q].kind == kJobLfu ? "lfu" : "fifo", q,
               (unsigned long long)jd[q].cap, hs[q][kStFastOk], hs[q][kStFastAcc],
               hs[q][kStFailPool], hs[q][kStFailElig], hs[q][kStFailConv], hs[q][kStSerialAcc],
@@ -2211,7 +2308,8 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
               hs[q][kStW0], hs[q][kStW1], hs[q][kStW2], hs[q][kStW3], hs[q][kStW4],
               hs[q][kStW5], hs[q][kStW6], hs[q][kStW7], hs[q][kStF0], hs[q][kStF1],
               hs[q][kStF2], hs[q][kStF3], hs[q][kStF4], hs[q][kStG0], hs[q][kStG1],
-              hs[q][kStG2], hs[q][kStQpt], hs[q][kStNc0], hs[q][kStNm]);
+              hs[q][kStG2], hs[q][kStQpt], hs[q][kStNc0], hs[q][kStNm], hs[q][kStJob],
+              hs[q][kStSer]);
     }
   }
 #endif
