@@ -89,7 +89,8 @@ static_assert(kRIt == 4, "hit words are assembled from four ballots");
 // Optional per-job replay statistics (diagnostics build only).
 #ifdef KV_REPLAY_STATS
 enum { kStFastOk = 0, kStFailPool, kStFailElig, kStFailConv, kStSerialAcc, kStIters,
-       kStScanned, kStFastAcc, kStT0, kStT1, kStT2, kStT3, kStT4, kStT5, kStT6, kStT7, kStT8, kStW0, kStW1, kStW2, kStW3, kStW4, kStW5, kStW6, kStW7, kStF0, kStF1, kStF2, kStF3, kStF4, kStG0, kStG1, kStG2, kStQpt, kStNc0, kStNm, kStJob, kStSer, kStats };
+       kStScanned, kStFastAcc, kStT0, kStT1, kStT2, kStT3, kStT4, kStT5, kStT6, kStT7, kStT8, kStW0, kStW1, kStW2, kStW3, kStW4, kStW5, kStW6, kStW7, kStF0, kStF1, kStF2, kStF3, kStF4, kStG0, kStG1, kStG2, kStQpt, kStNc0, kStNm, kStJob, kStSer, kStFR1, kStFR2, kStFR3, kStFPos, kStFLen, kStats };
+__shared__ unsigned int s_fr, s_fpos;
 __device__ unsigned long long g_rstats[256][kStats];
 __shared__ unsigned long long s_rstats[kStats];  // flushed to g_rstats when the job ends
 __shared__ unsigned long long s_rwave[8];
@@ -1272,6 +1273,10 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
             // a new entry can only go after it was inserted, and only once
             // every old one is gone
             if (evk[e] <= S.mpos[k - nc0] || !reached) bad = true;
+#ifdef KV_REPLAY_STATS
+            if (evk[e] <= S.mpos[k - nc0]) { atomicOr(&s_fr, 2u); atomicMin(&s_fpos, evk[e]); }
+            if (!reached) atomicOr(&s_fr, 4u);
+#endif
           }
         }
         run += qw[e];
@@ -1292,10 +1297,20 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     block_suffix_min_flag<NT>(mn, bad, S.sfx, tmin, anybad);
     RCLK(t_f3);
     RTIME(kStF2, t_f2, t_f3);
-    if (anybad) {
-      RSTAT(blockIdx.x, kStFailElig, 1);
-      return false;
+#ifdef KV_REPLAY_STATS
+    if (anybad && tid == 0) {
+      if (elig < evtot) s_rstats[kStFR1] += 1;
+      if (s_fr & 2u) { s_rstats[kStFR2] += 1; s_rstats[kStFPos] += s_fpos; s_rstats[kStFLen] += L; }
+      if (s_fr & 4u) s_rstats[kStFR3] += 1;
+      s_fr = 0;
+      s_fpos = 0xFFFFFFFFu;
     }
+#endif
+    // A shortfall of count-1 victims found here may be an artefact of the
+    // skip flags, which start out assuming that every entry touched in the
+    // chunk is touched before its turn: the update below can make such an
+    // entry eligible.  A chunk fails only if a shortfall outlives the last
+    // change.
     // the inputs of an iteration are the skip flags and the capacity
     // misses; the consumption flags are its outputs
     const uint8_t ns = (uint8_t)(it + 1);
@@ -1335,7 +1350,13 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       if (v[e] && !mi[e] && S.mcons[loc]) S.mcons[loc] = 0;
     }
     RWAVE(3, t_a);
-    if (!block_any(changed)) converged = true;
+    if (!block_any(changed)) {
+      if (anybad) {
+        RSTAT(blockIdx.x, kStFailElig, 1);
+        return false;
+      }
+      converged = true;
+    }
     RCLK(t_f5);
     RTIME(kStF4, t_f4, t_f5);
   }
@@ -1717,6 +1738,10 @@ __global__ __launch_bounds__(NT) void k_replay_lfu(const JobDev* __restrict__ jo
   if (lfu_one_group(j, a_in.n_groups) != G1) return;
 #ifdef KV_REPLAY_STATS
   const unsigned long long tj0 = wall_clock64();
+  if (threadIdx.x == 0) {
+    s_fr = 0;
+    s_fpos = 0xFFFFFFFFu;
+  }
 #endif
   const JobArgs a = job_args(a_in, j);
   const uint32_t tid = threadIdx.x;
@@ -2299,7 +2324,7 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
               "clk load %llu scan %llu fix %llu jump %llu apply %llu fin %llu x6 %llu x7 %llu x8 %llu "
               "w0 %llu w1 %llu w2 %llu w3 %llu w4 %llu w5 %llu w6 %llu w7 %llu "
               "f0 %llu f1 %llu f2 %llu f3 %llu f4 %llu g0 %llu g1 %llu g2 %llu qpt %llu "
-              "nc0 %llu nm %llu job %llu ser %llu\n",
+              "nc0 %llu nm %llu job %llu ser %llu fr1 %llu fr2 %llu fr3 %llu fpos %llu flen %llu\n",
               jd[q].kind == kJobLfu ? "lfu" : "fifo", q,
               (unsigned long long)jd[q].cap, hs[q][kStFastOk], hs[q][kStFastAcc],
               hs[q][kStFailPool], hs[q][kStFailElig], hs[q][kStFailConv], hs[q][kStSerialAcc],
@@ -2309,7 +2334,8 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
               hs[q][kStW5], hs[q][kStW6], hs[q][kStW7], hs[q][kStF0], hs[q][kStF1],
               hs[q][kStF2], hs[q][kStF3], hs[q][kStF4], hs[q][kStG0], hs[q][kStG1],
               hs[q][kStG2], hs[q][kStQpt], hs[q][kStNc0], hs[q][kStNm], hs[q][kStJob],
-              hs[q][kStSer]);
+              hs[q][kStSer], hs[q][kStFR1], hs[q][kStFR2], hs[q][kStFR3], hs[q][kStFPos],
+              hs[q][kStFLen]);
     }
   }
 #endif
