@@ -1105,8 +1105,11 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     uint32_t n0 = 0;
     uint64_t vw = 0;
     for (;;) {
-      if (vw >= ev0 || h >= c0 || n0 + NT * kCScan > kCand) break;
+      if (vw >= ev0 || h >= c0 || n0 >= kCand) break;
       RSTAT(blockIdx.x, kStScanned, 1);
+      // each position lists at most one entry: near the end of the buffer
+      // the step shrinks to the room left
+      const uint32_t hend = min(min<uint32_t>(h + NT * kCScan, h + (kCand - n0)), c0);
       bool live[kCScan], touched[kCScan];
       uint32_t wq[kCScan], aq[kCScan];
 #pragma unroll
@@ -1116,7 +1119,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
         touched[e] = false;
         aq[e] = kInf16;
         wq[e] = 0;
-        if (q < c0) {
+        if (q < hend) {
           const uint64_t word = bits[(q >> 6) - jw0];
           const uint32_t nxq = a.nxt[o][q];
           wq[e] = a.w8[o][q];
@@ -1145,7 +1148,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       }
       n0 += cnt_live;
       vw += vsum;
-      h = min<uint32_t>(h + NT * kCScan, c0);
+      h = hend;
     }
     __syncthreads();
     nc0 = n0;
