@@ -298,3 +298,23 @@ def test_full_prefix_real_capacities(lib, oracle_mod):
     cfgs = tg.configs_for("full", t)
     pick = np.concatenate([np.arange(0, 10000, 1251), np.arange(10000, 11000, 125)])
     compare(lib, oracle_mod, t, cfgs.subset(pick), label="full-prefix")
+
+
+@pytest.mark.parametrize("seed", range(2))
+def test_lfu_long_victim_queue(lib, oracle_mod, seed):
+    """LFU chunks whose misses outnumber what fits beside the listed count-1
+    residents: sweeps over more blocks than the cache holds, with a few hot
+    blocks, so that whole chunks miss and evict residents listed long ago."""
+    rng = np.random.default_rng(400 + seed)
+    n_blocks = 12_000 + 3_000 * seed
+    hot = list(range(n_blocks, n_blocks + 40))
+    seq = []
+    for _ in range(6):
+        for b in range(n_blocks):
+            seq.append(b)
+            if rng.random() < 0.05:
+                seq.append(int(rng.choice(hot)))
+    t = tg.from_blocks(seq, weights=None if seed == 0 else rng.choice([1, 2], size=n_blocks + 40))
+    caps = [2_000, 3_000, 6_000, 9_000, 11_000]
+    items = [{"cap": (c, 0, 0), "policy": 2} for c in caps]
+    compare(lib, oracle_mod, t, tg.from_list(items), label=f"longq{seed}")
