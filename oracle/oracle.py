@@ -9,6 +9,9 @@ module never imports the GPU library.
                      (hit, miss, ins, evict, hit_w, miss_w, ins_w, evict_w).
 * :func:`objectives` (cost, throughput, latency) per configuration.
 * :func:`pareto`     non-dominated flags by brute force.
+* :func:`ttl_curves` per group and time-to-live, the disk tier's hits and
+                     storage integral from the inter-arrival times
+                     (Section 4.3), in plain Python and numpy.
 """
 from __future__ import annotations
 
@@ -121,3 +124,50 @@ def pareto(obj, segment=None, bounds=None) -> np.ndarray:
     if rc < 0:
         raise ValueError("NaN objective")
     return flag
+
+
+def ttl_curves(trace, ttl):
+    """TTL retention curves of the disk tier (Section 4.3).
+
+    A block stays on disk for ``t`` seconds after each access.  Delta_g is the
+    multiset of inter-arrival times of group g's blocks: for every access
+    whose block was accessed before, the request time of the access minus the
+    request time of the block's previous access.  Per group g and each t:
+
+    * hits[g, k]  = H_g(t) = #{delta in Delta_g : delta <= t}
+    * hitw[g, k]  = the summed block weight of those accesses
+    * store[g, k] = sum over g's blocks b of w_b * (sum of min(t, delta) over
+      b's gaps + t), the storage-time integral in granule-seconds; with unit
+      weights this is C_g(t) = |B_g| * t + sum over Delta_g of min(t, delta).
+
+    A walk over the accesses in trace order (pure Python: small traces).
+    Returns (hits uint64 [G, K], hitw uint64 [G, K], store float64 [G, K]).
+    """
+    G = int(trace.n_groups)
+    ttl = [float(x) for x in ttl]
+    last = {}                               # block hash -> time of its latest access
+    gaps = [[] for _ in range(G)]           # per group: (delta, weight)
+    block_w = [0] * G                       # per group: weight of its distinct blocks
+    times = np.asarray(trace.req_time, dtype=np.float64)
+    for i in range(int(trace.n)):
+        h = int(trace.hash[i])
+        now = float(times[int(trace.req[i])])
+        g = int(trace.group[i])
+        w = int(trace.weight[i])
+        if h in last:
+            gaps[g].append((now - last[h], w))
+        else:
+            block_w[g] += w
+        last[h] = now
+    hits = np.zeros((G, len(ttl)), dtype=np.uint64)
+    hitw = np.zeros((G, len(ttl)), dtype=np.uint64)
+    store = np.zeros((G, len(ttl)), dtype=np.float64)
+    for g in range(G):
+        d = np.array([x for x, _ in gaps[g]], dtype=np.float64)
+        w = np.array([y for _, y in gaps[g]], dtype=np.float64)
+        for k, t in enumerate(ttl):
+            hit = d <= t
+            hits[g, k] = int(hit.sum())
+            hitw[g, k] = int(w[hit].sum())
+            store[g, k] = block_w[g] * t + float((w * np.minimum(t, d)).sum())
+    return hits, hitw, store
