@@ -46,7 +46,11 @@ ALGO_BYTES = {
     "stack_local": 5.0,       # read key 4 + weight 1 once for every LRU capacity
     "replay_lfu": 5.0,        # read block id 4 + weight 1 per LFU job-access
     "replay_fifo": 5.0,       # read block id 4 + weight 1 per FIFO job-access
+    "ttl_curves": 14.0,       # read link 4 + request 4 + weight 1 + group 1, gather the
+                              # previous access's request 4
 }
+# TTL curves of the disk tier: t = 0 and 63 values from 0.25 s to the 2 h span
+TTL_GRID = [0.0] + [float(x) for x in np.geomspace(0.25, 7200.0, 63)]
 
 
 def parse():
@@ -224,6 +228,30 @@ def main():
             "avg_launch_ms": avg_ms, "launches": calls,
             "stage_ms_per_step": {k: round(v[1] / args.steps, 3) for k, v in timing.items()
                                   if v[0]}}
+    # TTL curves (disk-tier retention for the group TTL) over the same trace,
+    # outside the step: one call per measured launch, timed by the library
+    h = K.kv_trace_load(dev["hash"], dev["req"], dev["req_time"], group=dev["group"],
+                        weight=dev["weight"], n_groups=G,
+                        tokens_per_granule=rec.tokens_per_granule,
+                        granule_bytes=rec.granule_bytes)
+    t_hits = torch.zeros((G, len(TTL_GRID)), dtype=torch.int64, device="cuda")
+    t_hitw = torch.zeros_like(t_hits)
+    t_store = torch.zeros((G, len(TTL_GRID)), dtype=torch.float64, device="cuda")
+    K.kv_ttl_curves(h, TTL_GRID, t_hits, t_hitw, t_store)
+    torch.cuda.synchronize()
+    K.kv_timing_enable(True)
+    for _ in range(5):
+        K.kv_ttl_curves(h, TTL_GRID, t_hits, t_hitw, t_store)
+    torch.cuda.synchronize()
+    K.kv_timing_enable(False)
+    t_calls, t_ms = K.kv_timing_read(reset=True)["ttl_curves"]
+    h.free()
+    ttl_ms = t_ms / max(t_calls, 1)
+    ttl_ach = ALGO_BYTES["ttl_curves"] * n / (ttl_ms / 1000.0) / 1e9
+    ttl = {"n_ttl": len(TTL_GRID), "avg_launch_ms": ttl_ms, "launches": t_calls,
+           "bound": "hbm", "achieved": ttl_ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+           "frac": ttl_ach / HBM_PEAK_GBS, "traffic": traffic_for("ttl_curves")}
+    print(f"[bench] TTL curves {ttl_ms:.3f} ms", file=sys.stderr, flush=True)
     cpu = None
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
@@ -235,7 +263,7 @@ def main():
         "data": "synthetic (seeded generators shaped like the paper's traces)",
         "config": {"workload": WORKLOAD_TEXT[args.workload], "name": args.workload,
                    "n_accesses": n, "n_configs": n_cfg, "n_requests": int(rec.len0.shape[0])},
-        "roofline": roof, "cpu_baseline": cpu,
+        "roofline": roof, "cpu_baseline": cpu, "ttl_curves": ttl,
     }
     print(json.dumps(out))
 

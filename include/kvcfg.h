@@ -12,6 +12,8 @@
  *   kv_eval_configs  per configuration: exact per-tier hit / miss / insert /
  *                    eviction counts, then (cost, throughput, latency)
  *   kv_pareto        non-dominated filter under optional bounds
+ *   kv_ttl_curves    per group, hits and storage cost of a disk tier that
+ *                    keeps blocks for a time-to-live, for many TTLs at once
  *
  * Conventions for every call:
  *   - Return KV_OK or a negative kv_status; kv_last_error() then describes
@@ -200,6 +202,35 @@ kv_status kv_pareto(const double* obj, const uint32_t* segment, uint32_t n,
                     const double* bounds, uint8_t* on_front, uint32_t* n_front,
                     void* stream);
 
+/* TTL retention curves of the disk tier (Section 4.3: the cumulative hits
+ * H_g(t) and storage cost C_g(t) of a group under a time-to-live t, the
+ * inputs of the ROI-aware group TTL).  A block stays on disk for ttl seconds
+ * after each access, so an access hits iff its block's previous access lies
+ * at most ttl seconds before it (inclusive).  With delta_i = req_time[req[i]]
+ * - req_time[req[p]] for the previous access p of the same block (an access
+ * without one has no delta), per group g and TTL ttl[k]:
+ *   hits[g][k]  = #{ accesses i of g with a delta : delta_i <= ttl[k] }
+ *   hitw[g][k]  = sum of w_i over those accesses (granules)
+ *   store[g][k] = W_g*ttl[k] + sum over accesses i of g with a delta of
+ *                 w_i*min(ttl[k], delta_i)
+ * in granule-seconds: the storage-time integral of g's blocks, each kept ttl
+ * after every access including its last (W_g = u_w_g of kv_trace_stats).
+ * With unit weights hits and store are the paper's H_g(t) and C_g(t).
+ *   ttl    host double [n_ttl]: finite, >= 0, non-decreasing
+ *   hits   device uint64 [n_groups][n_ttl]
+ *   hitw   device uint64 [n_groups][n_ttl]
+ *   store  device double [n_groups][n_ttl]
+ * hits and hitw are exact.  store is evaluated as
+ * W_g*t + S + t*(P_g - hitw[g][k]), S the sum of w_i*delta_i over the hits
+ * and P_g the summed weight of g's accesses with a delta, the sums of
+ * w_i*delta_i in double in an order of the library's choosing.  Device
+ * outputs are valid once the stream has completed.
+ * Errors: KV_ERR_INVALID for a NULL argument, n_ttl == 0, or a ttl value
+ * that is negative, not finite or below its predecessor;
+ * KV_ERR_UNSUPPORTED when n_groups * (n_ttl + 1) > 4096. */
+kv_status kv_ttl_curves(const kv_trace* t, const double* ttl, uint32_t n_ttl, uint64_t* hits,
+                        uint64_t* hitw, double* store, void* stream);
+
 /* Message describing the calling thread's most recent failure ("" if none). */
 const char* kv_last_error(void);
 
@@ -213,9 +244,10 @@ const char* kv_last_error(void);
  *   6 stack: assembly, bins   7 stack: final depths    8 LRU records
  *   9 replay: job setup       10 replay: LFU jobs      11 replay: combine
  *   12 objectives             13 Pareto filter         14 replay: FIFO jobs
+ *   15 TTL curves
  * The replay kernels run on streams of their own, concurrently with the LRU
  * stages, so stage times may overlap. */
-enum { KV_STAGES = 15 };
+enum { KV_STAGES = 16 };
 typedef struct kv_timing {
   uint64_t calls[KV_STAGES];
   double ms[KV_STAGES];

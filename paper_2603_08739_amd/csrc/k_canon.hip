@@ -370,6 +370,13 @@ kv_status canon_build(Trace& t, const kv_trace_desc& d, hipStream_t s) {
   DevStats* dstats = dst.as<DevStats>();
   KV_HIP(hipMemsetAsync(dstats, 0, sizeof(DevStats), s));
   KV_HIP(hipMemsetAsync(&dstats->w_min, 0xFF, 4, s));
+  // the request of every access and the request times, kept for the
+  // inter-arrival times of the TTL curves
+  if ((st = t.req.reserve(n * 4)) != KV_OK) return st;
+  if ((st = t.req_time.reserve((uint64_t)d.n_req * 8)) != KV_OK) return st;
+  KV_HIP(hipMemcpyAsync(t.req.p, d.req, n * 4, hipMemcpyDeviceToDevice, s));
+  KV_HIP(hipMemcpyAsync(t.req_time.p, d.req_time, (uint64_t)d.n_req * 8,
+                        hipMemcpyDeviceToDevice, s));
 
   {
   StageTimer tm(kStLoadValidate, s);

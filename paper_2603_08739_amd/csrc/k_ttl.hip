@@ -1,0 +1,148 @@
+// k_ttl.hip - TTL retention curves of the disk tier (Section 4.3).
+//
+// Under a time-to-live t a block stays on disk for t seconds after each of
+// its accesses, so an access hits iff the gap delta to its block's previous
+// access is at most t, and a block with accesses a_1 < ... < a_m occupies
+// storage for sum_j min(t, a_{j+1} - a_j) + t seconds.  Per group, the hits
+// H_g(t) and the storage integral C_g(t) for every t of a sorted list follow
+// from one histogram of the gaps over the list's bins:
+//   bin(delta) = #{k : ttl[k] < delta}, so delta <= ttl[k] <=> bin <= k;
+//   H_g(ttl[k])  = sum of the counts of bins 0..k
+//   C_g(ttl[k])  = W_g*ttl[k] + sum_{delta <= ttl[k]} w*delta
+//                  + ttl[k] * (weight of the gaps above ttl[k]).
+// The pass is a stream over the trace with one dependent gather per access
+// (the request of the previous access); the histogram lives in LDS.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+
+#include "kv_device.h"
+#include "kv_internal.h"
+
+namespace kv {
+namespace {
+
+constexpr int kTtlNT = 1024;       // threads per workgroup
+constexpr int kTtlU = 4;           // accesses per thread per step (gathers in flight)
+constexpr uint32_t kTtlMax = 1024; // TTL values per call
+constexpr uint32_t kTtlBins = 4096;  // groups * (TTL values + 1)
+
+// Gap histogram: per (group, bin) the number of gaps, their summed weight
+// and the summed weight * gap, added into the zeroed global arrays.
+__global__ __launch_bounds__(kTtlNT) void k_ttl_hist(
+    const uint32_t* __restrict__ key, const uint32_t* __restrict__ req,
+    const double* __restrict__ rt, const uint8_t* __restrict__ w8,
+    const uint8_t* __restrict__ g8, uint64_t n, const double* __restrict__ ttl, uint32_t n_ttl,
+    uint32_t bins, unsigned long long* __restrict__ cnt, unsigned long long* __restrict__ wsum,
+    double* __restrict__ wd) {
+  __shared__ uint32_t hc[kTtlBins], hw[kTtlBins];
+  __shared__ double hd[kTtlBins];
+  __shared__ double tt[kTtlMax];
+  const uint32_t tid = threadIdx.x;
+  const uint32_t nb = n_ttl + 1;
+  for (uint32_t i = tid; i < bins; i += kTtlNT) {
+    hc[i] = 0;
+    hw[i] = 0;
+    hd[i] = 0.0;
+  }
+  for (uint32_t i = tid; i < n_ttl; i += kTtlNT) tt[i] = ttl[i];
+  __syncthreads();
+  const uint64_t step = (uint64_t)gridDim.x * kTtlNT * kTtlU;
+  for (uint64_t p0 = (uint64_t)blockIdx.x * kTtlNT * kTtlU; p0 < n; p0 += step) {
+    uint32_t k[kTtlU], r[kTtlU], rp[kTtlU], w[kTtlU], g[kTtlU];
+#pragma unroll
+    for (int u = 0; u < kTtlU; ++u) {
+      const uint64_t p = p0 + (uint64_t)u * kTtlNT + tid;
+      const bool in = p < n;
+      k[u] = in ? key[p] : 0u;
+      r[u] = in ? req[p] : 0u;
+      w[u] = in ? w8[p] : 0u;
+      g[u] = in ? g8[p] : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < kTtlU; ++u) rp[u] = k[u] ? req[k[u] - 1] : 0u;
+#pragma unroll
+    for (int u = 0; u < kTtlU; ++u) {
+      if (!k[u]) continue;  // no earlier access: no gap
+      const double delta = rt[r[u]] - rt[rp[u]];
+      const uint32_t b = lower_bound(tt, 0u, n_ttl, delta);
+      const uint32_t idx = g[u] * nb + b;
+      atomicAdd(&hc[idx], 1u);
+      atomicAdd(&hw[idx], w[u]);
+      atomicAdd(&hd[idx], (double)w[u] * delta);
+    }
+  }
+  __syncthreads();
+  for (uint32_t i = tid; i < bins; i += kTtlNT) {
+    if (!hc[i]) continue;
+    atomicAdd(&cnt[i], (unsigned long long)hc[i]);
+    atomicAdd(&wsum[i], (unsigned long long)hw[i]);
+    atomicAdd(&wd[i], hd[i]);
+  }
+}
+
+struct GroupWeights {
+  unsigned long long w[KV_MAX_GROUPS];  // distinct weight per group
+};
+
+// Cumulative curves, one thread per group (bins in ascending order).
+__global__ void k_ttl_fin(const unsigned long long* __restrict__ cnt,
+                          const unsigned long long* __restrict__ wsum,
+                          const double* __restrict__ wd, const double* __restrict__ ttl,
+                          uint32_t n_ttl, uint32_t n_groups, GroupWeights W,
+                          uint64_t* __restrict__ hits, uint64_t* __restrict__ hitw,
+                          double* __restrict__ store) {
+  const uint32_t g = blockIdx.x * blockDim.x + threadIdx.x;
+  if (g >= n_groups) return;
+  const uint32_t nb = n_ttl + 1;
+  const unsigned long long* c = cnt + (uint64_t)g * nb;
+  const unsigned long long* ws = wsum + (uint64_t)g * nb;
+  const double* d = wd + (uint64_t)g * nb;
+  unsigned long long P = 0;  // weight of every gap of the group
+  for (uint32_t b = 0; b < nb; ++b) P += ws[b];
+  unsigned long long hc = 0, hw = 0;
+  double s = 0.0;
+  const double Wg = (double)W.w[g];
+  for (uint32_t k = 0; k < n_ttl; ++k) {
+    hc += c[k];
+    hw += ws[k];
+    s += d[k];
+    const double t = ttl[k];
+    hits[(uint64_t)g * n_ttl + k] = hc;
+    hitw[(uint64_t)g * n_ttl + k] = hw;
+    store[(uint64_t)g * n_ttl + k] = Wg * t + s + t * (double)(P - hw);
+  }
+}
+
+}  // namespace
+
+kv_status ttl_curves(Trace& t, const double* ttl_dev, uint32_t n_ttl, uint64_t* hits,
+                     uint64_t* hitw, double* store, hipStream_t s) {
+  const uint32_t G = t.n_groups;
+  const uint32_t bins = G * (n_ttl + 1);
+  if (n_ttl > kTtlMax || bins > kTtlBins)
+    return fail(KV_ERR_UNSUPPORTED, "kv_ttl_curves: n_groups * (n_ttl + 1) must be <= 4096");
+  DevBuf& bh = t.ws[22];
+  kv_status st;
+  if ((st = bh.reserve((uint64_t)bins * 24)) != KV_OK) return st;
+  unsigned long long* cnt = bh.as<unsigned long long>();
+  unsigned long long* wsum = cnt + bins;
+  double* wd = reinterpret_cast<double*>(wsum + bins);
+  StageTimer tm(kStTtl, s);
+  if ((st = fill_u64(reinterpret_cast<uint64_t*>(cnt), 0, (uint64_t)bins * 3, s)) != KV_OK)
+    return st;
+  const uint64_t per_block = (uint64_t)kTtlNT * kTtlU;
+  const uint32_t nblk = (uint32_t)std::min<uint64_t>((t.n + per_block - 1) / per_block, 1024);
+  hipLaunchKernelGGL(k_ttl_hist, dim3(nblk), dim3(kTtlNT), 0, s, t.shared.key.as<uint32_t>(),
+                     t.req.as<uint32_t>(), t.req_time.as<double>(), t.shared.w.as<uint8_t>(),
+                     t.shared.g.as<uint8_t>(), t.n, ttl_dev, n_ttl, bins, cnt, wsum, wd);
+  KV_HIP(hipGetLastError());
+  GroupWeights W{};
+  for (uint32_t g = 0; g < KV_MAX_GROUPS; ++g) W.w[g] = t.st.u_w_g[g];
+  hipLaunchKernelGGL(k_ttl_fin, dim3(1), dim3(64), 0, s, cnt, wsum, wd, ttl_dev, n_ttl, G, W,
+                     hits, hitw, store);
+  KV_HIP(hipGetLastError());
+  return KV_OK;
+}
+
+}  // namespace kv

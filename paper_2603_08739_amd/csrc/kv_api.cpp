@@ -385,6 +385,32 @@ kv_status kv_trace_load(const kv_trace_desc* d, void* stream, kv_trace** out) {
   return KV_OK;
 }
 
+kv_status kv_ttl_curves(const kv_trace* h, const double* ttl, uint32_t n_ttl, uint64_t* hits,
+                        uint64_t* hitw, double* store, void* stream) {
+  if (!h) return fail(KV_ERR_INVALID, "kv_ttl_curves: trace is NULL");
+  Trace* t = const_cast<Trace*>(reinterpret_cast<const Trace*>(h));
+  if (!is_live(t)) return fail(KV_ERR_INVALID, "kv_ttl_curves: not a live trace handle");
+  if (!ttl || !hits || !hitw || !store)
+    return fail(KV_ERR_INVALID, "kv_ttl_curves: ttl, hits, hitw and store are required");
+  if (n_ttl == 0) return fail(KV_ERR_INVALID, "kv_ttl_curves: n_ttl must be >= 1");
+  for (uint32_t k = 0; k < n_ttl; ++k) {
+    if (!std::isfinite(ttl[k]) || ttl[k] < 0.0)
+      return fail(KV_ERR_INVALID, "kv_ttl_curves: ttl values must be finite and >= 0");
+    if (k && ttl[k] < ttl[k - 1])
+      return fail(KV_ERR_INVALID, "kv_ttl_curves: ttl values must be non-decreasing");
+  }
+  if ((uint64_t)t->n_groups * ((uint64_t)n_ttl + 1) > 4096)
+    return fail(KV_ERR_UNSUPPORTED, "kv_ttl_curves: n_groups * (n_ttl + 1) must be <= 4096");
+  hipStream_t s = (hipStream_t)stream;
+  // the thresholds are staged in the trace so they outlive the async copy
+  t->ttl_stage.assign(ttl, ttl + n_ttl);
+  DevBuf& bt = t->ws[23];
+  kv_status st;
+  if ((st = bt.reserve((uint64_t)n_ttl * 8)) != KV_OK) return st;
+  KV_HIP(hipMemcpyAsync(bt.p, t->ttl_stage.data(), (uint64_t)n_ttl * 8, hipMemcpyHostToDevice, s));
+  return ttl_curves(*t, bt.as<double>(), n_ttl, hits, hitw, store, s);
+}
+
 kv_status kv_trace_free(kv_trace* h) {
   if (!h) return KV_OK;
   Trace* t = reinterpret_cast<Trace*>(h);

@@ -86,6 +86,8 @@ struct Trace {
   Order part;         // partitioned order (built on first use when n_groups > 1)
   DevBuf blk_w;       // u8[u]  weight per dense block id
   DevBuf blk_g;       // u8[u]  group per dense block id
+  DevBuf req;         // u32[n] request of each access (trace order)
+  DevBuf req_time;    // f64[n_req] arrival time of each request
   // workspace reused across kv_eval_configs calls on this trace
   DevBuf ws[24];
   // host staging of the latest kv_eval_configs call (alive across its copies)
@@ -93,6 +95,7 @@ struct Trace {
   std::vector<kv_config> cfg_stage;
   GroupStats gs_stage[KV_MAX_GROUPS];
   std::vector<uint8_t> job_stage, rec_stage, src_stage;
+  std::vector<double> ttl_stage;
   std::vector<unsigned long long> jc_stage;
 };
 
@@ -105,7 +108,7 @@ constexpr uint64_t kDeadMagic = 0x646561646b766366ull;
 enum Stage {
   kStLoadValidate = 0, kStLoadSort, kStLoadLinks, kStPartition, kStStackMatrix,
   kStStackLocal, kStStackAssemble, kStStackFinal, kStLruCounts, kStReplayInit, kStReplay,
-  kStCombine, kStObjectives, kStPareto, kStReplayFifo
+  kStCombine, kStObjectives, kStPareto, kStReplayFifo, kStTtl
 };
 // Records an event pair around a scope when timing is enabled.
 struct StageTimer {
@@ -156,6 +159,11 @@ kv_status objectives(const kv_config* cfg_dev, uint32_t n_cfg, uint32_t n_groups
                      double span, double n_req, uint64_t n_w, double* obj, hipStream_t s);
 kv_status pareto(const double* obj, const uint32_t* segment, uint32_t n, const double* bounds,
                  uint8_t* flag, uint32_t* counters_dev, hipStream_t s);
+
+// TTL curves (k_ttl.hip): validated arguments; ttl_dev holds the n_ttl
+// thresholds on the device.
+kv_status ttl_curves(Trace& t, const double* ttl_dev, uint32_t n_ttl, uint64_t* hits,
+                     uint64_t* hitw, double* store, hipStream_t s);
 
 // replay of non-LRU policies (k_replay.hip)
 struct ReplayJob {

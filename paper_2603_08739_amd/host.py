@@ -60,3 +60,15 @@ def pareto(obj_np, segment=None, bounds=None, device="cuda"):
     n = kvcfg.kv_pareto(obj, flags, segment=seg, bounds=bounds)
     torch.cuda.synchronize()
     return flags.cpu().numpy(), n
+
+
+def ttl_curves(handle, ttl, n_groups: int, device="cuda", stream=None):
+    """Returns (hits uint64 [G,K], hitw uint64 [G,K], store float64 [G,K]) as numpy arrays."""
+    k = len(ttl)
+    hits = torch.zeros((n_groups, k), dtype=torch.int64, device=device)
+    hitw = torch.zeros((n_groups, k), dtype=torch.int64, device=device)
+    store = torch.zeros((n_groups, k), dtype=torch.float64, device=device)
+    kvcfg.kv_ttl_curves(handle, ttl, hits, hitw, store, stream=stream)
+    torch.cuda.synchronize()
+    return (hits.cpu().numpy().view(np.uint64), hitw.cpu().numpy().view(np.uint64),
+            store.cpu().numpy())

@@ -53,10 +53,11 @@ class kv_cost_model(ctypes.Structure):
                 ("ssd_bw_max", _f64), ("t_prefill_per_token", _f64)]
 
 
-KV_STAGES = 15
+KV_STAGES = 16
 STAGE_NAMES = ("load_validate", "load_sort", "load_links", "partition", "stack_matrix",
                "stack_local", "stack_assemble", "stack_final", "lru_counts", "replay_init",
-               "replay_lfu", "replay_combine", "objectives", "pareto", "replay_fifo")
+               "replay_lfu", "replay_combine", "objectives", "pareto", "replay_fifo",
+               "ttl_curves")
 
 
 class kv_timing(ctypes.Structure):
@@ -86,6 +87,8 @@ def _load():
     lib.kv_eval_configs.argtypes = [_vp, _vp, _u32, ctypes.POINTER(kv_cost_model), _vp, _vp, _vp]
     lib.kv_pareto.restype = ctypes.c_int
     lib.kv_pareto.argtypes = [_vp, _vp, _u32, _vp, _vp, ctypes.POINTER(_u32), _vp]
+    lib.kv_ttl_curves.restype = ctypes.c_int
+    lib.kv_ttl_curves.argtypes = [_vp, _vp, _u32, _vp, _vp, _vp, _vp]
     lib.kv_last_error.restype = ctypes.c_char_p
     lib.kv_last_error.argtypes = []
     lib.kv_timing_enable.restype = ctypes.c_int
@@ -97,7 +100,7 @@ def _load():
 
 LIB = _load()
 EXPORTS = ("kv_trace_load", "kv_trace_free", "kv_trace_info", "kv_eval_configs", "kv_pareto",
-           "kv_last_error", "kv_timing_enable", "kv_timing_read")
+           "kv_ttl_curves", "kv_last_error", "kv_timing_enable", "kv_timing_read")
 
 
 def kv_timing_enable(on: bool = True):
@@ -225,3 +228,12 @@ def kv_pareto(obj, on_front, segment=None, bounds=None, want_count=True, stream=
     _check(LIB.kv_pareto(_ptr(obj), _ptr(segment), n, b, _ptr(on_front),
                          ctypes.byref(cnt) if want_count else None, _stream(stream)))
     return int(cnt.value) if want_count else None
+
+
+def kv_ttl_curves(trace: Trace, ttl, hits, hitw, store, stream=None):
+    """ttl: host sequence of float seconds (non-decreasing); hits, hitw: int64/uint64
+    device tensors [n_groups, n_ttl]; store: float64 device [n_groups, n_ttl]."""
+    vals = [float(x) for x in ttl]
+    arr = (ctypes.c_double * max(len(vals), 1))(*vals)
+    _check(LIB.kv_ttl_curves(trace.handle, ctypes.cast(arr, _vp), len(vals), _ptr(hits),
+                             _ptr(hitw), _ptr(store), _stream(stream)))

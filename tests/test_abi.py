@@ -18,8 +18,9 @@ def declared_functions():
 
 def test_header_declares_the_boundary():
     assert declared_functions() == sorted(["kv_trace_load", "kv_trace_free", "kv_trace_info",
-                                           "kv_eval_configs", "kv_pareto", "kv_last_error",
-                                           "kv_timing_enable", "kv_timing_read"])
+                                           "kv_eval_configs", "kv_pareto", "kv_ttl_curves",
+                                           "kv_last_error", "kv_timing_enable",
+                                           "kv_timing_read"])
 
 
 def test_library_exports_every_declared_symbol():
@@ -101,3 +102,9 @@ def test_host_side_validation_without_device():
     assert lib.kv_pareto(None, None, 5, None, None, None, None) == K.KV_ERR_INVALID
     assert lib.kv_pareto(ctypes.c_void_p(16), None, (1 << 26) + 1, None, ctypes.c_void_p(16),
                          None, None) == K.KV_ERR_INVALID
+    ttl = (ctypes.c_double * 2)(0.0, 1.0)
+    assert lib.kv_ttl_curves(None, ttl, 2, ctypes.c_void_p(16), ctypes.c_void_p(16),
+                             ctypes.c_void_p(16), None) == K.KV_ERR_INVALID
+    assert lib.kv_ttl_curves(ctypes.c_void_p(0x1000), ttl, 2, ctypes.c_void_p(16),
+                             ctypes.c_void_p(16), ctypes.c_void_p(16), None) == K.KV_ERR_INVALID
+    assert "live" in K.kv_last_error()

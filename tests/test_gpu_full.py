@@ -19,6 +19,8 @@ import tracegen as tg
 pytestmark = pytest.mark.gpu
 
 HIT, MISS, INS, EVICT, HIT_W, MISS_W, INS_W, EVICT_W = range(8)
+# TTLs of the full-size TTL-curve check (seconds; the trace spans 2 h)
+TTL_FULL = [0.0, 0.5, 1.0, 5.0, 30.0, 60.0, 300.0, 600.0, 1800.0, 3600.0, 7200.0, 1e5]
 
 
 def say(msg):
@@ -45,6 +47,8 @@ def full_run():
     st = h.info()
     say("  full sweep: evaluating")
     counts, obj = host.evaluate(h, cfgs, tg.DEFAULT_COST, rec.n_groups)
+    say("  full sweep: TTL curves")
+    ttl_out = host.ttl_curves(h, TTL_FULL, rec.n_groups)
     h.free()
     say("  full sweep: Pareto fronts")
     front, nfront = host.pareto(obj)
@@ -56,12 +60,39 @@ def full_run():
     wfirst = torch.zeros(u, dtype=torch.int64, device="cuda")
     wfirst.scatter_(0, first, dev["weight"].to(torch.int64))
     distinct_w = int(wfirst.sum().item())
-    del uniq, first, wfirst, dev
+    # TTL curves recomputed with plain torch ops: a stable sort by hash puts
+    # each block's accesses next to each other in time order
+    say("  full sweep: TTL reference")
+    G = rec.n_groups
+    gfirst = torch.zeros(u, dtype=torch.int64, device="cuda")
+    gfirst.scatter_(0, first, dev["group"].to(torch.int64))
+    W = torch.bincount(gfirst, weights=wfirst.to(torch.float64), minlength=G)
+    regap = (torch.bincount(dev["group"].to(torch.int64), minlength=G)
+             - torch.bincount(gfirst, minlength=G)).cpu().numpy()  # accesses - blocks
+    del uniq, first, wfirst, gfirst
+    order = torch.sort(dev["hash"], stable=True).indices
+    hs = dev["hash"][order]
+    same = hs[1:] == hs[:-1]
+    del hs
+    tm = dev["req_time"][dev["req"].to(torch.int64)][order]
+    delta = (tm[1:] - tm[:-1])[same]
+    del tm
+    gg = dev["group"][order][1:][same].to(torch.int64)
+    ww = dev["weight"][order][1:][same].to(torch.float64)
+    del order, same
+    ref_ttl = []
+    for t in TTL_FULL:
+        hit = delta <= t
+        ref_ttl.append((torch.bincount(gg[hit], minlength=G).cpu().numpy(),
+                        torch.bincount(gg[hit], weights=ww[hit], minlength=G).cpu().numpy(),
+                        (W * t + torch.bincount(gg, weights=ww * torch.clamp(delta, max=t),
+                                                minlength=G)).cpu().numpy()))
+    del delta, gg, ww, dev
     torch.cuda.empty_cache()
     say("  full sweep: done")
     return dict(cfgs=cfgs, counts=counts.astype(np.int64), obj=obj, front=front,
                 nfront=nfront, front_seg=front_seg, st=st, n=n, n_w=n_w, u=u,
-                distinct_w=distinct_w)
+                distinct_w=distinct_w, ttl=ttl_out, ref_ttl=ref_ttl, regap=regap)
 
 
 def test_trace_statistics(full_run):
@@ -196,3 +227,18 @@ def test_pareto_fronts(full_run):
     assert r["nfront"] == int(want.sum())
     want_seg = _front(r["obj"], r["cfgs"].segment)
     assert np.array_equal(r["front_seg"].astype(bool), want_seg)
+
+
+def test_ttl_curves_match_torch(full_run):
+    """Hits and hit weights equal the torch recount; storage integrals agree
+    to 1e-9 relative (double sums over 3.9e8 gaps in different orders)."""
+    hits, hitw, store = full_run["ttl"]
+    for k, (rh, rw, rs) in enumerate(full_run["ref_ttl"]):
+        np.testing.assert_array_equal(hits[:, k], rh.astype(np.uint64))
+        np.testing.assert_array_equal(hitw[:, k], rw.astype(np.uint64))
+        np.testing.assert_allclose(store[:, k], rs, rtol=1e-9, atol=0)
+    # a TTL past the span keeps every re-access; t = 0 stores nothing
+    assert (hits[:, -1] == full_run["regap"].astype(np.uint64)).all()
+    assert (store[:, 0] == 0.0).all()
+    assert (np.diff(hits.astype(np.int64), axis=1) >= 0).all()
+    assert (np.diff(store, axis=1) >= 0).all()
