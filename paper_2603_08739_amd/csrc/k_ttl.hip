@@ -23,26 +23,31 @@ namespace kv {
 namespace {
 
 constexpr int kTtlNT = 1024;       // threads per workgroup
-constexpr int kTtlU = 4;           // accesses per thread per step (gathers in flight)
+#ifndef KV_TTL_U
+#define KV_TTL_U 8
+#endif
+constexpr int kTtlU = KV_TTL_U;    // accesses per thread per step (gathers in flight)
 constexpr uint32_t kTtlMax = 1024; // TTL values per call
 constexpr uint32_t kTtlBins = 4096;  // groups * (TTL values + 1)
 
 // Gap histogram: per (group, bin) the number of gaps, their summed weight
-// and the summed weight * gap, added into the zeroed global arrays.
+// and the summed weight * gap, added into the zeroed global arrays.  In LDS
+// the count and the weight share one 64-bit word (count << 32 | weight: with
+// n <= 2^29 over up to 1024 workgroups a workgroup sees at most 2^19
+// accesses of at most 255 granules each, so the weight never carries).
 __global__ __launch_bounds__(kTtlNT) void k_ttl_hist(
     const uint32_t* __restrict__ key, const uint32_t* __restrict__ req,
     const double* __restrict__ rt, const uint8_t* __restrict__ w8,
     const uint8_t* __restrict__ g8, uint64_t n, const double* __restrict__ ttl, uint32_t n_ttl,
     uint32_t bins, unsigned long long* __restrict__ cnt, unsigned long long* __restrict__ wsum,
     double* __restrict__ wd) {
-  __shared__ uint32_t hc[kTtlBins], hw[kTtlBins];
+  __shared__ unsigned long long hcw[kTtlBins];
   __shared__ double hd[kTtlBins];
   __shared__ double tt[kTtlMax];
   const uint32_t tid = threadIdx.x;
   const uint32_t nb = n_ttl + 1;
   for (uint32_t i = tid; i < bins; i += kTtlNT) {
-    hc[i] = 0;
-    hw[i] = 0;
+    hcw[i] = 0;
     hd[i] = 0.0;
   }
   for (uint32_t i = tid; i < n_ttl; i += kTtlNT) tt[i] = ttl[i];
@@ -67,16 +72,16 @@ __global__ __launch_bounds__(kTtlNT) void k_ttl_hist(
       const double delta = rt[r[u]] - rt[rp[u]];
       const uint32_t b = lower_bound(tt, 0u, n_ttl, delta);
       const uint32_t idx = g[u] * nb + b;
-      atomicAdd(&hc[idx], 1u);
-      atomicAdd(&hw[idx], w[u]);
+      atomicAdd(&hcw[idx], (1ull << 32) | w[u]);
       atomicAdd(&hd[idx], (double)w[u] * delta);
     }
   }
   __syncthreads();
   for (uint32_t i = tid; i < bins; i += kTtlNT) {
-    if (!hc[i]) continue;
-    atomicAdd(&cnt[i], (unsigned long long)hc[i]);
-    atomicAdd(&wsum[i], (unsigned long long)hw[i]);
+    const unsigned long long x = hcw[i];
+    if (!x) continue;
+    atomicAdd(&cnt[i], x >> 32);
+    atomicAdd(&wsum[i], x & 0xFFFFFFFFull);
     atomicAdd(&wd[i], hd[i]);
   }
 }
