@@ -27,6 +27,7 @@ constexpr int kTtlNT = 1024;       // threads per workgroup
 #define KV_TTL_U 8
 #endif
 constexpr int kTtlU = KV_TTL_U;    // accesses per thread per step (gathers in flight)
+static_assert(kTtlU % 4 == 0, "accesses are read four at a time");
 constexpr uint32_t kTtlMax = 1024; // TTL values per call
 constexpr uint32_t kTtlBins = 4096;  // groups * (TTL values + 1)
 
@@ -54,15 +55,26 @@ __global__ __launch_bounds__(kTtlNT) void k_ttl_hist(
   __syncthreads();
   const uint64_t step = (uint64_t)gridDim.x * kTtlNT * kTtlU;
   for (uint64_t p0 = (uint64_t)blockIdx.x * kTtlNT * kTtlU; p0 < n; p0 += step) {
+    // each thread takes kTtlU consecutive accesses, read as vectors (the
+    // arrays hold 16 readable bytes past n; accesses past n are dropped)
     uint32_t k[kTtlU], r[kTtlU], rp[kTtlU], w[kTtlU], g[kTtlU];
+    const uint64_t pt = p0 + (uint64_t)tid * kTtlU;
 #pragma unroll
-    for (int u = 0; u < kTtlU; ++u) {
-      const uint64_t p = p0 + (uint64_t)u * kTtlNT + tid;
-      const bool in = p < n;
-      k[u] = in ? key[p] : 0u;
-      r[u] = in ? req[p] : 0u;
-      w[u] = in ? w8[p] : 0u;
-      g[u] = in ? g8[p] : 0u;
+    for (int q = 0; q < kTtlU / 4; ++q) {
+      const uint64_t pq = min<uint64_t>(pt + 4 * q, n & ~3ull);
+      const uint4 kv = *reinterpret_cast<const uint4*>(key + pq);
+      const uint4 rv = *reinterpret_cast<const uint4*>(req + pq);
+      const uint32_t wv = *reinterpret_cast<const uint32_t*>(w8 + pq);
+      const uint32_t gv = *reinterpret_cast<const uint32_t*>(g8 + pq);
+      const uint32_t ka[4] = {kv.x, kv.y, kv.z, kv.w}, ra[4] = {rv.x, rv.y, rv.z, rv.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const bool in = pq == pt + 4 * q && pt + 4 * q + e < n;
+        k[4 * q + e] = in ? ka[e] : 0u;
+        r[4 * q + e] = ra[e];
+        w[4 * q + e] = (wv >> (8 * e)) & 0xFFu;
+        g[4 * q + e] = (gv >> (8 * e)) & 0xFFu;
+      }
     }
 #pragma unroll
     for (int u = 0; u < kTtlU; ++u) rp[u] = k[u] ? req[k[u] - 1] : 0u;
