@@ -189,10 +189,7 @@ __global__ __launch_bounds__(256) void k_links(const uint64_t* __restrict__ K,
                                                const uint32_t* __restrict__ V, uint64_t n,
                                                uint32_t* __restrict__ key,
                                                uint32_t* __restrict__ nxt,
-                                               uint32_t* __restrict__ newflag,
-                                               const uint8_t* __restrict__ w8,
-                                               const uint8_t* __restrict__ g8, DevStats* st) {
-  uint32_t err = 0;
+                                               uint32_t* __restrict__ newflag) {
   for (uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; k < n;
        k += (uint64_t)gridDim.x * blockDim.x) {
     const uint64_t h = K[k];
@@ -203,9 +200,24 @@ __global__ __launch_bounds__(256) void k_links(const uint64_t* __restrict__ K,
     key[pos] = sp ? pv + 1u : 0u;
     nxt[pos] = sn ? V[k + 1] : kNone;
     newflag[k] = sp ? 0u : 1u;
-    if (sp && (w8[pos] != w8[pv] || g8[pos] != g8[pv])) err |= kErrInconsistent;
   }
-  if (err) atomicOr(&st->err, err);
+}
+
+// Every access carries its block's weight and group (those of the block's
+// first occurrence): read in position order, against the per-block tables.
+__global__ __launch_bounds__(256) void k_check_blocks(const uint32_t* __restrict__ bid,
+                                                      const uint8_t* __restrict__ blk_w,
+                                                      const uint8_t* __restrict__ blk_g,
+                                                      const uint8_t* __restrict__ w8,
+                                                      const uint8_t* __restrict__ g8, uint64_t n,
+                                                      DevStats* st) {
+  bool bad = false;
+  for (uint64_t p = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n;
+       p += (uint64_t)gridDim.x * blockDim.x) {
+    const uint32_t id = bid[p];
+    bad |= w8[p] != blk_w[id] || g8[p] != blk_g[id];
+  }
+  if (__ballot(bad) != 0ull && lane_id() == 0) atomicOr(&st->err, (uint32_t)kErrInconsistent);
 }
 
 // First occurrences in trace order: flag[pos] = 1 where the block appears
@@ -409,8 +421,7 @@ kv_status canon_build(Trace& t, const kv_trace_desc& d, hipStream_t s) {
   {
   StageTimer tm(kStLoadLinks, s);
   hipLaunchKernelGGL(k_links, dim3(grid_of(n)), dim3(256), 0, s, kin, vin, n,
-                     o.key.as<uint32_t>(), o.nxt.as<uint32_t>(), newflag, o.w.as<uint8_t>(),
-                     o.g.as<uint8_t>(), dstats);
+                     o.key.as<uint32_t>(), o.nxt.as<uint32_t>(), newflag);
   KV_HIP(hipGetLastError());
   if ((st = scan_u32(newflag, incl, n, true, scratch.as<uint32_t>(), s)) != KV_OK) return st;
   }
@@ -439,6 +450,10 @@ kv_status canon_build(Trace& t, const kv_trace_desc& d, hipStream_t s) {
   KV_HIP(hipGetLastError());
   hipLaunchKernelGGL(k_mult, dim3(grid_of(n)), dim3(256), 0, s, incl, newflag, n, runstart,
                      dstats);
+  KV_HIP(hipGetLastError());
+  hipLaunchKernelGGL(k_check_blocks, dim3(grid_of(n)), dim3(256), 0, s, o.bid.as<uint32_t>(),
+                     t.blk_w.as<uint8_t>(), t.blk_g.as<uint8_t>(), o.w.as<uint8_t>(),
+                     o.g.as<uint8_t>(), n, dstats);
   KV_HIP(hipGetLastError());
   }
 

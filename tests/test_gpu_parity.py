@@ -180,6 +180,12 @@ def test_error_paths(lib):
     with pytest.raises(kvcfg.KvError) as e:
         host.load(t)
     assert e.value.status == kvcfg.KV_ERR_INVALID
+    # ... or two groups (the first occurrence is not the odd one out)
+    t = tg.from_blocks([5, 1, 2, 1, 1], n_groups=2)
+    t.group = np.array([0, 1, 0, 1, 0], dtype=np.uint8)
+    with pytest.raises(kvcfg.KvError) as e:
+        host.load(t)
+    assert e.value.status == kvcfg.KV_ERR_INVALID and "two weights or groups" in str(e.value)
     t = tg.from_blocks([1, 2, 3, 1], weights={1: 4, 2: 4, 3: 1})
     h = host.load(t)
     st = h.info()
