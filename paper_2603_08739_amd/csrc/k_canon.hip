@@ -184,11 +184,12 @@ __global__ __launch_bounds__(kRsNT) void k_rs_scatter(const uint64_t* __restrict
   }
 }
 
-// Neighbours in hash order are the previous / next occurrences.
+// Neighbours in hash order are the previous / next occurrences.  Both links
+// of a position go out in one 8-byte scatter (link | next << 32), split
+// into the two arrays by a pass in position order.
 __global__ __launch_bounds__(256) void k_links(const uint64_t* __restrict__ K,
                                                const uint32_t* __restrict__ V, uint64_t n,
-                                               uint32_t* __restrict__ key,
-                                               uint32_t* __restrict__ nxt,
+                                               uint64_t* __restrict__ kn,
                                                uint32_t* __restrict__ newflag) {
   for (uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; k < n;
        k += (uint64_t)gridDim.x * blockDim.x) {
@@ -197,9 +198,21 @@ __global__ __launch_bounds__(256) void k_links(const uint64_t* __restrict__ K,
     const bool sp = k > 0 && K[k - 1] == h;
     const bool sn = k + 1 < n && K[k + 1] == h;
     const uint32_t pv = sp ? V[k - 1] : 0u;
-    key[pos] = sp ? pv + 1u : 0u;
-    nxt[pos] = sn ? V[k + 1] : kNone;
+    const uint32_t key = sp ? pv + 1u : 0u;
+    const uint32_t nx = sn ? V[k + 1] : kNone;
+    kn[pos] = (uint64_t)key | ((uint64_t)nx << 32);
     newflag[k] = sp ? 0u : 1u;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_split_links(const uint64_t* __restrict__ kn,
+                                                     uint64_t n, uint32_t* __restrict__ key,
+                                                     uint32_t* __restrict__ nxt) {
+  for (uint64_t p = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n;
+       p += (uint64_t)gridDim.x * blockDim.x) {
+    const uint64_t x = kn[p];
+    key[p] = (uint32_t)x;
+    nxt[p] = (uint32_t)(x >> 32);
   }
 }
 
@@ -371,11 +384,12 @@ kv_status canon_build(Trace& t, const kv_trace_desc& d, hipStream_t s) {
   const uint32_t ntiles = div_up(n, kRsTile);
   const uint64_t ncount = (uint64_t)ntiles * 256;
   const uint64_t scratch_elems = std::max(scan_scratch_elems(ncount), scan_scratch_elems(n));
-  DevBuf ka, kb, va, vb, counts, scratch, dst;
+  DevBuf ka, kb, va, vb, kn, counts, scratch, dst;
   if ((st = ka.reserve(n * 8)) != KV_OK) return st;
   if ((st = kb.reserve(n * 8)) != KV_OK) return st;
   if ((st = va.reserve(n * 4)) != KV_OK) return st;
   if ((st = vb.reserve(n * 4)) != KV_OK) return st;
+  if ((st = kn.reserve(n * 8)) != KV_OK) return st;
   if ((st = counts.reserve(std::max<uint64_t>(ncount, 1) * 4)) != KV_OK) return st;
   if ((st = scratch.reserve(std::max<uint64_t>(scratch_elems, 1) * 4)) != KV_OK) return st;
   if ((st = dst.reserve(sizeof(DevStats))) != KV_OK) return st;
@@ -421,7 +435,10 @@ kv_status canon_build(Trace& t, const kv_trace_desc& d, hipStream_t s) {
   {
   StageTimer tm(kStLoadLinks, s);
   hipLaunchKernelGGL(k_links, dim3(grid_of(n)), dim3(256), 0, s, kin, vin, n,
-                     o.key.as<uint32_t>(), o.nxt.as<uint32_t>(), newflag);
+                     kn.as<uint64_t>(), newflag);
+  KV_HIP(hipGetLastError());
+  hipLaunchKernelGGL(k_split_links, dim3(grid_of(n)), dim3(256), 0, s, kn.as<uint64_t>(), n,
+                     o.key.as<uint32_t>(), o.nxt.as<uint32_t>());
   KV_HIP(hipGetLastError());
   if ((st = scan_u32(newflag, incl, n, true, scratch.as<uint32_t>(), s)) != KV_OK) return st;
   }
