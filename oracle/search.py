@@ -18,8 +18,9 @@ Reading of Alg. 1 used here (the paper leaves these open):
   |a - b| / max(|a|, |b|) (0 when both are 0);
 * "adjacent pair" = two simulated configurations on one line of constant t
   (or constant d) with no simulated configuration between them;
-* a midpoint is taken only if it is a new point at least `res` away from
-  both ends: d1 + res * floor((d2 - d1) / (2 * res)), likewise for t;
+* a midpoint is taken only if it is a new point at least one resolution
+  step (`res_d` along d, `res_t` along t) away from both ends:
+  d1 + res_d * floor((d2 - d1) / (2 * res_d)), likewise for t;
 * the DRAM expansion looks at the line t = t_min (the paper's TTL = 0) and
   adds the column d_top + step_d over the initial t grid;
 * rounds stop when no new point is proposed, or after `max_rounds`.
@@ -35,7 +36,7 @@ def _rel(a: float, b: float) -> float:
 
 
 def explore(simulate, d_min, d_max, d_step, t_min, t_max, t_step, tau_e, tau_perf, tau_cost,
-            res=1, max_rounds=64):
+            res_d=1, res_t=1, max_rounds=64):
     """Alg. 1.  Returns (points [(d, t)] in simulation order, objectives
     float64 [n, 3] as (cost, throughput, latency), rounds run)."""
     t_grid = list(range(t_min, t_max + 1, t_step))
@@ -72,6 +73,7 @@ def explore(simulate, d_min, d_max, d_step, t_min, t_max, t_step, tau_e, tau_per
                     pb = (b, fixed) if axis == 0 else (fixed, b)
                     oa, ob = seen[pa], seen[pb]
                     perf = _rel(oa[2], ob[2]) > tau_perf or _rel(oa[1], ob[1]) > tau_perf
+                    res = res_d if axis == 0 else res_t
                     if perf and _rel(oa[0], ob[0]) > tau_cost and b - a >= 2 * res:
                         m = a + res * ((b - a) // (2 * res))
                         todo.append((m, fixed) if axis == 0 else (fixed, m))

@@ -65,3 +65,10 @@ def test_dram_expansion_stops_in_the_long_tail():
                                tau_perf=10.0, tau_cost=10.0)
     assert sorted(pts) == [(d, t) for d in range(0, 100, 10) for t in (0, 5)]
     assert rounds == 8
+
+
+def test_refinement_stays_on_each_axis_resolution():
+    # along d the resolution is 8: the step at 37 is bracketed by 32 and 40
+    pts, _, _ = S.explore(step_evaluator, 0, 64, 32, 0, 0, 1, tau_e=0.5, tau_perf=0.1,
+                          tau_cost=0.01, res_d=8, res_t=3)
+    assert pts == [(0, 0), (32, 0), (64, 0), (48, 0), (40, 0)]
