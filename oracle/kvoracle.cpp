@@ -28,6 +28,13 @@
 //   * Inclusive hierarchy: every tier is an independent cache that sees every
 //     access; the access is served by the fastest tier holding the block; then
 //     every present tier applies its hit update and every other tier inserts.
+//   * Inclusive hierarchy with prefix reuse (LRU, shared caches): contents
+//     evolve exactly as in the inclusive hierarchy, but a request reuses only
+//     a run of its blocks from its first block on, as a radix-tree cache
+//     does (Section 3.2's prefix-shared KV blocks): per tier, block j of a
+//     request is available iff the tier holds it and block j-1 of the same
+//     request was available there (the first block needs only presence); the
+//     access is served by the fastest tier where it is available.
 //   * Exclusive hierarchy with write-back demotion (LRU only): a block lives
 //     in at most one tier; a hit in a lower tier removes it there and promotes
 //     it to the top tier; an overfull tier demotes its LRU block to the next
@@ -57,12 +64,13 @@ constexpr int kTiers = 3;
 constexpr int kFields = 8;  // hit, miss, ins, evict, hit_w, miss_w, ins_w, evict_w
 enum Field { F_HIT = 0, F_MISS, F_INS, F_EVICT, F_HIT_W, F_MISS_W, F_INS_W, F_EVICT_W };
 enum Policy { P_LRU = 0, P_FIFO = 1, P_LFU = 2 };
-enum Mode { M_INCLUSIVE = 0, M_EXCLUSIVE = 1 };
+enum Mode { M_INCLUSIVE = 0, M_EXCLUSIVE = 1, M_INCLUSIVE_PREFIX = 2 };
 
 struct Block {
   uint64_t hash;
   uint32_t w;
   uint32_t g;
+  uint32_t req;
 };
 
 // Counts of one configuration: [group][tier][field].
@@ -190,20 +198,32 @@ void add(Counts& c, uint32_t g, int k, Field f, uint64_t cnt_field_weight) {
   c.v[g][k][f] += cnt_field_weight;
 }
 
-// Inclusive hierarchy over the accesses listed in `idx`.
+// Inclusive hierarchy over the accesses listed in `idx`; with `prefix`, a
+// block is available from a tier only while its request's earlier blocks
+// were.
 void replay_inclusive(const std::vector<Block>& acc, const std::vector<uint32_t>& idx,
-                      const uint64_t cap[kTiers], int policy, Counts& out) {
+                      const uint64_t cap[kTiers], int policy, bool prefix, Counts& out) {
   Tier* tier[kTiers] = {nullptr, nullptr, nullptr};
   for (int k = 0; k < kTiers; ++k)
     if (cap[k] > 0) tier[k] = make_tier(policy, cap[k]);
+  bool run[kTiers] = {false, false, false};  // the request's blocks so far all available
+  bool first = true;
+  uint32_t cur_req = 0;
   for (uint32_t i : idx) {
     const Block& b = acc[i];
+    if (first || b.req != cur_req) {
+      for (int k = 0; k < kTiers; ++k) run[k] = true;
+      cur_req = b.req;
+      first = false;
+    }
     bool present[kTiers] = {false, false, false};
     int served = -1;
     for (int k = 0; k < kTiers; ++k) {
       if (!tier[k]) continue;
       present[k] = tier[k]->contains(b.hash);
-      if (present[k] && served < 0) served = k;
+      const bool avail = present[k] && (!prefix || run[k]);
+      run[k] = avail;
+      if (avail && served < 0) served = k;
     }
     for (int k = 0; k < kTiers; ++k) {
       if (!tier[k]) continue;
@@ -314,11 +334,12 @@ int replay_one(const std::vector<Block>& acc, const std::vector<std::vector<uint
         cg[k] = c.cap_group[k * kMaxGroups + g];
         if (bad_cap(cg[k])) return -1;
       }
+      if (c.mode == M_INCLUSIVE_PREFIX) return -4;
       if (c.mode == M_EXCLUSIVE) {
         if (c.policy[g] != P_LRU) return -4;
         replay_exclusive(acc, by_group[g], cg, out);
       } else {
-        replay_inclusive(acc, by_group[g], cg, c.policy[g], out);
+        replay_inclusive(acc, by_group[g], cg, c.policy[g], false, out);
       }
     }
   } else {
@@ -327,8 +348,11 @@ int replay_one(const std::vector<Block>& acc, const std::vector<std::vector<uint
     if (c.mode == M_EXCLUSIVE) {
       if (c.policy[0] != P_LRU) return -4;
       replay_exclusive(acc, all, c.cap, out);
+    } else if (c.mode == M_INCLUSIVE_PREFIX) {
+      if (c.policy[0] != P_LRU) return -4;
+      replay_inclusive(acc, all, c.cap, P_LRU, true, out);
     } else {
-      replay_inclusive(acc, all, c.cap, c.policy[0], out);
+      replay_inclusive(acc, all, c.cap, c.policy[0], false, out);
     }
   }
   return 0;
@@ -339,10 +363,12 @@ int replay_one(const std::vector<Block>& acc, const std::vector<std::vector<uint
 extern "C" {
 
 // Replays every configuration literally.  counts: uint64[n_cfg][n_groups][3][8].
-// Returns 0, or -1 for an invalid capacity (between 0 and the largest block),
-// -4 for an exclusive hierarchy with a policy other than LRU, -2 for bad sizes.
+// req: request of every access (NULL: one request per access).  Returns 0,
+// or -1 for an invalid capacity (between 0 and the largest block), -4 for an
+// exclusive or prefix hierarchy with a policy other than LRU (or a
+// partitioned prefix one), -2 for bad sizes.
 int oracle_replay(uint64_t n, const uint64_t* hash, const uint8_t* group, const uint8_t* weight,
-                  uint32_t n_groups, uint32_t n_cfg, const uint64_t* cap,
+                  const uint32_t* req, uint32_t n_groups, uint32_t n_cfg, const uint64_t* cap,
                   const uint64_t* cap_group, const uint8_t* mode, const uint8_t* partitioned,
                   const uint8_t* policy, uint32_t n_threads, uint64_t* counts) {
   if (n_groups < 1 || n_groups > (uint32_t)kMaxGroups) return -2;
@@ -354,7 +380,7 @@ int oracle_replay(uint64_t n, const uint64_t* hash, const uint8_t* group, const 
     uint32_t g = group ? group[i] : 0;
     uint32_t w = weight ? weight[i] : 1;
     if (g >= n_groups || w == 0) return -2;
-    acc[i] = Block{hash[i], w, g};
+    acc[i] = Block{hash[i], w, g, req ? req[i] : (uint32_t)i};
     by_group[g].push_back((uint32_t)i);
     all[i] = (uint32_t)i;
     w_max = std::max(w_max, w);

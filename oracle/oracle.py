@@ -50,7 +50,7 @@ def _load():
         lib = ctypes.CDLL(LIB)
         p = ctypes.c_void_p
         lib.oracle_replay.restype = ctypes.c_int
-        lib.oracle_replay.argtypes = [ctypes.c_uint64, p, p, p, ctypes.c_uint32,
+        lib.oracle_replay.argtypes = [ctypes.c_uint64, p, p, p, p, ctypes.c_uint32,
                                       ctypes.c_uint32, p, p, p, p, p, ctypes.c_uint32, p]
         lib.oracle_objectives.restype = ctypes.c_int
         lib.oracle_objectives.argtypes = [ctypes.c_uint32, p, p, ctypes.c_uint32, p,
@@ -84,7 +84,8 @@ def replay(trace, cfgs, threads: int | None = None) -> np.ndarray:
     mode = np.ascontiguousarray(cfgs.mode, dtype=np.uint8)
     part = np.ascontiguousarray(cfgs.partitioned, dtype=np.uint8)
     pol = np.ascontiguousarray(cfgs.policy, dtype=np.uint8)
-    rc = lib.oracle_replay(trace.n, _ptr(h), _ptr(gr), _ptr(w), g, n_cfg, _ptr(cap), _ptr(cg),
+    rq = np.ascontiguousarray(trace.req, dtype=np.uint32)
+    rc = lib.oracle_replay(trace.n, _ptr(h), _ptr(gr), _ptr(w), _ptr(rq), g, n_cfg, _ptr(cap), _ptr(cg),
                            _ptr(mode), _ptr(part), _ptr(pol),
                            threads or default_threads(), _ptr(out))
     if rc != 0:
