@@ -58,7 +58,17 @@ enum {
    * overfull tier demotes its least recently used block to the next tier
    * (dropping it past the last tier).  Requires LRU and a trace whose
    * blocks all have the same weight. */
-  KV_MODE_EXCLUSIVE_DEMOTE = 1
+  KV_MODE_EXCLUSIVE_DEMOTE = 1,
+  /* The inclusive hierarchy with prefix reuse, as in a radix-tree KV cache
+   * (blocks are prefix-chained, Section 3.2): contents evolve exactly as in
+   * KV_MODE_INCLUSIVE, but a request reuses only a run of its blocks from
+   * its first block on.  Per tier, block j of a request is available iff
+   * the tier holds it and block j-1 of the same request was available there
+   * (the first block needs only presence); the access is served by the
+   * fastest tier where it is available.  Insert and evict counts are those
+   * of KV_MODE_INCLUSIVE.  Requires LRU and a shared (non-partitioned)
+   * configuration. */
+  KV_MODE_INCLUSIVE_PREFIX = 2
 };
 
 /* Eviction policy of a tier cache.  A miss inserts the block after evicting
@@ -178,7 +188,8 @@ kv_status kv_trace_info(const kv_trace* t, kv_trace_stats* out);
  * Errors: KV_ERR_INVALID for a capacity in (0, w_max), partitioned capacities
  * that exceed cap[k], an unknown mode or policy, nonzero reserved bytes, or a
  * nonpositive cost-model rate; KV_ERR_UNSUPPORTED for the exclusive mode with
- * FIFO/LFU or with blocks of different weights.  n_cfg == 0 is a no-op. */
+ * FIFO/LFU or with blocks of different weights, and for the prefix-reuse
+ * mode with FIFO/LFU or partitioned capacities.  n_cfg == 0 is a no-op. */
 kv_status kv_eval_configs(const kv_trace* t, const kv_config* cfg, uint32_t n_cfg,
                           const kv_cost_model* model, uint64_t* counts, double* obj,
                           void* stream);

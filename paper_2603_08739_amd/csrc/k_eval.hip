@@ -26,7 +26,7 @@ __device__ __forceinline__ uint64_t cum_at(const OrderView& ov, uint32_t g, uint
 //             = N - hit_top, of a lower tier = evictions of the tier above.
 __global__ __launch_bounds__(256) void k_lru_counts(const kv_config* __restrict__ cfg,
                                                     uint32_t n_cfg, uint32_t G, OrderView sh,
-                                                    OrderView pt,
+                                                    OrderView pt, OrderView px,
                                                     const GroupStats* __restrict__ gs,
                                                     uint64_t* __restrict__ counts) {
   const uint64_t tid = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -41,7 +41,10 @@ __global__ __launch_bounds__(256) void k_lru_counts(const kv_config* __restrict_
   for (int k = 0; k < 3; ++k) cap[k] = part ? C.cap_group[k][g] : C.cap[k];
   const uint64_t N = gs[g].n_g, NW = gs[g].n_w_g;
   uint64_t* out = counts + ((uint64_t)c * G + g) * 3 * 8;
-  if (C.mode == KV_MODE_INCLUSIVE) {
+  if (C.mode == KV_MODE_INCLUSIVE || C.mode == KV_MODE_INCLUSIVE_PREFIX) {
+    // which accesses a tier serves: by stack distance, or with prefix reuse
+    // by the running maximum over the request; what it holds: by distance
+    const OrderView& sv = C.mode == KV_MODE_INCLUSIVE_PREFIX ? px : ov;
     uint64_t M = 0;
     for (int k = 0; k < 3; ++k) {
       uint64_t* r = out + k * 8;
@@ -51,13 +54,14 @@ __global__ __launch_bounds__(256) void k_lru_counts(const kv_config* __restrict_
       }
       const uint64_t Mx = cap[k] > M ? cap[k] : M;
       const uint64_t hC = cum_at(ov, g, cap[k], 0), wC = cum_at(ov, g, cap[k], 1);
-      const uint64_t hM = cum_at(ov, g, M, 0), wM = cum_at(ov, g, M, 1);
-      const uint64_t hX = cum_at(ov, g, Mx, 0), wX = cum_at(ov, g, Mx, 1);
+      const uint64_t sC = cum_at(sv, g, cap[k], 0), swC = cum_at(sv, g, cap[k], 1);
+      const uint64_t sM = cum_at(sv, g, M, 0), swM = cum_at(sv, g, M, 1);
+      const uint64_t sX = cum_at(sv, g, Mx, 0), swX = cum_at(sv, g, Mx, 1);
       const uint64_t fC = cum_at(ov, g, cap[k], 2), fwC = cum_at(ov, g, cap[k], 3);
-      r[KV_F_HIT] = cap[k] > M ? hC - hM : 0;
-      r[KV_F_HIT_W] = cap[k] > M ? wC - wM : 0;
-      r[KV_F_MISS] = N - hX;
-      r[KV_F_MISS_W] = NW - wX;
+      r[KV_F_HIT] = cap[k] > M ? sC - sM : 0;
+      r[KV_F_HIT_W] = cap[k] > M ? swC - swM : 0;
+      r[KV_F_MISS] = N - sX;
+      r[KV_F_MISS_W] = NW - swX;
       r[KV_F_INS] = N - hC;
       r[KV_F_INS_W] = NW - wC;
       r[KV_F_EVICT] = (N - hC) - fC;
@@ -209,13 +213,13 @@ __global__ __launch_bounds__(256) void k_pareto(const double* __restrict__ obj,
 }  // namespace
 
 kv_status lru_counts(const kv_config* cfg_dev, uint32_t n_cfg, uint32_t n_groups,
-                     OrderView shared, OrderView part, const GroupStats* gs_dev,
-                     uint64_t* counts, hipStream_t s) {
+                     OrderView shared, OrderView part, OrderView prefix,
+                     const GroupStats* gs_dev, uint64_t* counts, hipStream_t s) {
   const uint64_t m = (uint64_t)n_cfg * n_groups;
   if (m == 0) return KV_OK;
   StageTimer tm(kStLruCounts, s);
   hipLaunchKernelGGL(k_lru_counts, dim3(div_up(m, 256)), dim3(256), 0, s, cfg_dev, n_cfg,
-                     n_groups, shared, part, gs_dev, counts);
+                     n_groups, shared, part, prefix, gs_dev, counts);
   KV_HIP(hipGetLastError());
   return KV_OK;
 }

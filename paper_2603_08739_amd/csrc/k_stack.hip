@@ -354,7 +354,7 @@ __global__ __launch_bounds__(256) void k_sd_assemble(const uint32_t* __restrict_
                                                      const uint32_t* __restrict__ partial,
                                                      const uint32_t* __restrict__ E,
                                                      const uint32_t* __restrict__ RQ,
-                                                     BinArgs ba) {
+                                                     BinArgs ba, uint32_t* __restrict__ dout) {
   __shared__ uint32_t sthr[kLds ? kThrLds : 1];
   __shared__ uint32_t scnt[kLds ? kThrLds + KV_MAX_GROUPS : 1];
   __shared__ uint32_t sw[kLds ? kThrLds + KV_MAX_GROUPS : 1];
@@ -376,7 +376,10 @@ __global__ __launch_bounds__(256) void k_sd_assemble(const uint32_t* __restrict_
     for (uint32_t j = threadIdx.x; j < nb; j += 256) {
       const uint64_t i = base + j;
       const uint32_t kk = key[i];
-      if (kk == 0) continue;
+      if (kk == 0) {
+        if (dout) dout[i] = kNone;  // a first access: no finite distance
+        continue;
+      }
       const uint32_t p = kk - 1u;
       const uint32_t Pb = p >> kSdLogB;
       uint32_t d = partial[i];
@@ -384,6 +387,7 @@ __global__ __launch_bounds__(256) void k_sd_assemble(const uint32_t* __restrict_
         d += E[p];
         if (Pb + 1 < X) d += RQ[row + Pb];
       }
+      if (dout) dout[i] = d;
       const uint32_t g = g8[i];
       const uint32_t w = w8[i];
       const uint32_t lo = soff[g], hi = soff[g + 1];
@@ -395,6 +399,85 @@ __global__ __launch_bounds__(256) void k_sd_assemble(const uint32_t* __restrict_
       } else {
         const uint32_t b = lower_bound(ba.thr, lo, hi, d) - lo;
         const uint32_t bin = lo + g + b;
+        atomicAdd((unsigned long long*)&ba.hist[bin * 4 + 0], 1ull);
+        atomicAdd((unsigned long long*)&ba.hist[bin * 4 + 1], (unsigned long long)w);
+      }
+    }
+  }
+  if (kLds) {
+    __syncthreads();
+    for (uint32_t j = threadIdx.x; j < nbins; j += 256) {
+      if (scnt[j]) {
+        atomicAdd((unsigned long long*)&ba.hist[j * 4 + 0], (unsigned long long)scnt[j]);
+        atomicAdd((unsigned long long*)&ba.hist[j * 4 + 1], (unsigned long long)sw[j]);
+      }
+    }
+  }
+}
+
+// First position of every request r (rstart[r], r <= n_req; an empty
+// request starts where the next one does): request indices are
+// non-decreasing over the positions.
+__global__ __launch_bounds__(256) void k_sd_rstart(const uint32_t* __restrict__ req, uint64_t n,
+                                                   uint32_t n_req, uint32_t* __restrict__ rstart) {
+  for (uint64_t p = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; p <= n;
+       p += (uint64_t)gridDim.x * blockDim.x) {
+    const uint32_t lo = p == 0 ? 0u : req[p - 1] + 1u;  // requests that start here
+    const uint32_t hi = p == n ? n_req : req[p];
+    for (uint32_t r = lo; r <= hi && r <= n_req; ++r) rstart[r] = (uint32_t)p;
+  }
+}
+
+// Prefix reuse: a block is reused from a cache of capacity C only if every
+// block of its request up to it is (radix-tree caches reuse a request's
+// longest cached prefix), i.e. the running maximum of the stack distances
+// over the request, D'_i = max(D_j : j <= i in i's request), is at most C.
+// One wavefront per request scans its distances 64 at a time and bins D'
+// into fields 0 and 1 of `ba.hist`.
+template <bool kLds>
+__global__ __launch_bounds__(256) void k_sd_prefix(const uint32_t* __restrict__ D,
+                                                   const uint32_t* __restrict__ rstart,
+                                                   uint32_t n_req, const uint8_t* __restrict__ w8,
+                                                   const uint8_t* __restrict__ g8, BinArgs ba) {
+  __shared__ uint32_t sthr[kLds ? kThrLds : 1];
+  __shared__ uint32_t scnt[kLds ? kThrLds + KV_MAX_GROUPS : 1];
+  __shared__ uint32_t sw[kLds ? kThrLds + KV_MAX_GROUPS : 1];
+  __shared__ uint32_t soff[KV_MAX_GROUPS + 1];
+  const uint32_t nbins = ba.n_thr + ba.n_groups;
+  if (threadIdx.x <= ba.n_groups) soff[threadIdx.x] = ba.off[threadIdx.x];
+  if (kLds) {
+    for (uint32_t j = threadIdx.x; j < ba.n_thr; j += 256) sthr[j] = ba.thr[j];
+    for (uint32_t j = threadIdx.x; j < nbins; j += 256) {
+      scnt[j] = 0;
+      sw[j] = 0;
+    }
+  }
+  __syncthreads();
+  const uint32_t lane = lane_id();
+  const uint32_t waves = gridDim.x * 4;
+  for (uint32_t r = blockIdx.x * 4 + threadIdx.x / 64; r < n_req; r += waves) {
+    const uint32_t b = rstart[r], e = rstart[r + 1];
+    uint32_t carry = 0;
+    for (uint32_t c = b; c < e; c += 64) {
+      const uint32_t i = c + lane;
+      uint32_t m = i < e ? D[i] : 0u;
+#pragma unroll
+      for (int s2 = 1; s2 < 64; s2 <<= 1) {
+        const uint32_t o = (uint32_t)__shfl_up((int)m, s2, 64);
+        if (lane >= (uint32_t)s2) m = max(m, o);
+      }
+      m = max(m, carry);
+      carry = (uint32_t)__builtin_amdgcn_readlane((int)m, 63);
+      if (i >= e || m == kNone) continue;   // past the request, or behind a first access
+      const uint32_t g = g8[i];
+      const uint32_t w = w8[i];
+      const uint32_t lo = soff[g], hi = soff[g + 1];
+      if (kLds) {
+        const uint32_t bin = lo + g + (lower_bound(sthr, lo, hi, m) - lo);
+        atomicAdd(&scnt[bin], 1u);
+        atomicAdd(&sw[bin], w);
+      } else {
+        const uint32_t bin = lo + g + (lower_bound(ba.thr, lo, hi, m) - lo);
         atomicAdd((unsigned long long*)&ba.hist[bin * 4 + 0], 1ull);
         atomicAdd((unsigned long long*)&ba.hist[bin * 4 + 1], (unsigned long long)w);
       }
@@ -504,7 +587,7 @@ uint32_t grid_of(uint64_t m, uint32_t cap = 32768) {
 
 kv_status stack_pass(Trace& t, Order& o, bool partitioned, const ThresholdSet& ts,
                      const uint32_t* thr_dev, const uint32_t* off_dev, uint64_t* hist,
-                     hipStream_t s) {
+                     uint64_t* phist, hipStream_t s) {
   const uint64_t n = t.n;
   const uint32_t G = div_up(n, kSdB);
   kv_status st;
@@ -520,6 +603,16 @@ kv_status stack_pass(Trace& t, Order& o, bool partitioned, const ThresholdSet& t
   if ((st = b_Q.reserve(tri * 4)) != KV_OK) return st;
   if ((st = b_csum.reserve((uint64_t)nchunks * G * 4)) != KV_OK) return st;
   if ((st = b_scan.reserve(std::max<uint64_t>(scan_scratch_elems(n), 1) * 4)) != KV_OK) return st;
+  // prefix reuse (trace order only): every access's distance, request starts
+  uint32_t* dist = nullptr;
+  uint32_t* rstart = nullptr;
+  if (phist) {
+    if (partitioned) return fail(KV_ERR_UNSUPPORTED, "prefix reuse needs the trace order");
+    if ((st = t.ws[25].reserve(n * 4)) != KV_OK) return st;
+    if ((st = t.ws[26].reserve(((uint64_t)t.st.n_req + 1) * 4)) != KV_OK) return st;
+    dist = t.ws[25].as<uint32_t>();
+    rstart = t.ws[26].as<uint32_t>();
+  }
   const uint32_t* key = o.key.as<uint32_t>();
   const uint32_t* nxt = o.nxt.as<uint32_t>();
   const uint8_t* w8 = o.w.as<uint8_t>();
@@ -553,12 +646,30 @@ kv_status stack_pass(Trace& t, Order& o, bool partitioned, const ThresholdSet& t
   if (lds)
     hipLaunchKernelGGL(k_sd_assemble<true>, dim3(ga), dim3(256), 0, s, key, w8, g8, n, G,
                        (const uint32_t*)b_partial.as<uint32_t>(),
-                       (const uint32_t*)b_E.as<uint32_t>(), (const uint32_t*)Q, ba);
+                       (const uint32_t*)b_E.as<uint32_t>(), (const uint32_t*)Q, ba, dist);
   else
     hipLaunchKernelGGL(k_sd_assemble<false>, dim3(ga), dim3(256), 0, s, key, w8, g8, n, G,
                        (const uint32_t*)b_partial.as<uint32_t>(),
-                       (const uint32_t*)b_E.as<uint32_t>(), (const uint32_t*)Q, ba);
+                       (const uint32_t*)b_E.as<uint32_t>(), (const uint32_t*)Q, ba, dist);
   KV_HIP(hipGetLastError());
+  if (phist) {
+    const uint32_t nr = t.st.n_req;
+    hipLaunchKernelGGL(k_sd_rstart, dim3(grid_of(n + 1)), dim3(256), 0, s,
+                       t.req.as<uint32_t>(), n, nr, rstart);
+    KV_HIP(hipGetLastError());
+    BinArgs bp{thr_dev, off_dev, (uint32_t)ts.values.size(), ts.n_groups, phist};
+    const uint32_t gp = std::min<uint32_t>(div_up(nr, 4), 4096);
+    if (lds)
+      hipLaunchKernelGGL(k_sd_prefix<true>, dim3(gp), dim3(256), 0, s, (const uint32_t*)dist,
+                         (const uint32_t*)rstart, nr, w8, g8, bp);
+    else
+      hipLaunchKernelGGL(k_sd_prefix<false>, dim3(gp), dim3(256), 0, s, (const uint32_t*)dist,
+                         (const uint32_t*)rstart, nr, w8, g8, bp);
+    KV_HIP(hipGetLastError());
+    hipLaunchKernelGGL(k_hist_cum, dim3(1), dim3(4 * KV_MAX_GROUPS), 0, s, phist, off_dev,
+                       ts.n_groups);
+    KV_HIP(hipGetLastError());
+  }
   }
   StageTimer tm(kStStackFinal, s);
   // final occupancy: reuse `partial` for the scanned last-occurrence weights

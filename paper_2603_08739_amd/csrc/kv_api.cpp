@@ -222,7 +222,7 @@ kv_status validate_configs(const Trace& t, const kv_config* cfg, uint32_t n_cfg)
   for (uint32_t c = 0; c < n_cfg; ++c) {
     const kv_config& C = cfg[c];
     const std::string at = "kv_eval_configs: config " + std::to_string(c) + ": ";
-    if (C.mode > KV_MODE_EXCLUSIVE_DEMOTE) return fail(KV_ERR_INVALID, at + "unknown mode");
+    if (C.mode > KV_MODE_INCLUSIVE_PREFIX) return fail(KV_ERR_INVALID, at + "unknown mode");
     if (C.partitioned > 1) return fail(KV_ERR_INVALID, at + "partitioned must be 0 or 1");
     for (int r = 0; r < 6; ++r)
       if (C.reserved[r]) return fail(KV_ERR_INVALID, at + "reserved bytes must be zero");
@@ -245,6 +245,9 @@ kv_status validate_configs(const Trace& t, const kv_config* cfg, uint32_t n_cfg)
         if (sum > C.cap[k]) return fail(KV_ERR_INVALID, at + "group capacities exceed the tier");
       }
     }
+    if (C.mode == KV_MODE_INCLUSIVE_PREFIX &&
+        (C.partitioned || C.policy[0] != KV_POLICY_LRU))
+      return fail(KV_ERR_UNSUPPORTED, at + "prefix reuse supports shared LRU tiers only");
     if (C.mode == KV_MODE_EXCLUSIVE_DEMOTE) {
       for (uint32_t g = 0; g < ng; ++g)
         if (C.policy[g] != KV_POLICY_LRU)
@@ -261,7 +264,7 @@ uint32_t clamp32(uint64_t x) { return x > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_
 // Capacities the closed-form LRU records will look up, per group.
 void add_thresholds(std::vector<std::vector<uint32_t>>& per_group, const kv_config& C, uint32_t g,
                     uint32_t slot, uint64_t w0) {
-  if (C.mode == KV_MODE_INCLUSIVE) {
+  if (C.mode == KV_MODE_INCLUSIVE || C.mode == KV_MODE_INCLUSIVE_PREFIX) {
     for (int k = 0; k < 3; ++k) {
       const uint64_t x = group_cap(C, k, g);
       if (x) per_group[slot].push_back(clamp32(x));
@@ -292,11 +295,11 @@ void finish_set(ThresholdSet& ts, std::vector<std::vector<uint32_t>>& per_group,
 }
 
 struct StackSlot {
-  int ws_thr, ws_hist;
+  int ws_thr, ws_hist, ws_phist;  // ws_phist < 0: no prefix-reuse histogram
 };
 
 kv_status run_stack(Trace& t, Order& o, bool partitioned, ThresholdSet& ts, StackSlot slot,
-                    OrderView& view, hipStream_t s) {
+                    OrderView& view, OrderView& pview, hipStream_t s) {
   kv_status st;
   DevBuf& bt = t.ws[slot.ws_thr];
   DevBuf& bh = t.ws[slot.ws_hist];
@@ -309,10 +312,20 @@ kv_status run_stack(Trace& t, Order& o, bool partitioned, ThresholdSet& ts, Stac
   if (nthr) KV_HIP(hipMemcpyAsync(thr, ts.values.data(), nthr * 4, hipMemcpyHostToDevice, s));
   KV_HIP(hipMemcpyAsync(off, ts.off, (KV_MAX_GROUPS + 1) * 4, hipMemcpyHostToDevice, s));
   if ((st = fill_u64(bh.as<uint64_t>(), 0, nbins * 4, s)) != KV_OK) return st;
-  if ((st = stack_pass(t, o, partitioned, ts, thr, off, bh.as<uint64_t>(), s)) != KV_OK) return st;
+  uint64_t* ph = nullptr;
+  if (slot.ws_phist >= 0) {
+    DevBuf& bp = t.ws[slot.ws_phist];
+    if ((st = bp.reserve(nbins * 4 * 8)) != KV_OK) return st;
+    if ((st = fill_u64(bp.as<uint64_t>(), 0, nbins * 4, s)) != KV_OK) return st;
+    ph = bp.as<uint64_t>();
+  }
+  if ((st = stack_pass(t, o, partitioned, ts, thr, off, bh.as<uint64_t>(), ph, s)) != KV_OK)
+    return st;
   view.thr = thr;
   view.off = off;
   view.hist = bh.as<uint64_t>();
+  pview = view;
+  if (ph) pview.hist = ph;
   return KV_OK;
 }
 
@@ -450,7 +463,7 @@ kv_status kv_eval_configs(const kv_trace* h, const kv_config* cfg, uint32_t n_cf
 
   // ---- plan: thresholds per order, replay jobs
   std::vector<std::vector<uint32_t>> tsh(G), tpt(G);
-  bool need_shared = false, need_part = false;
+  bool need_shared = false, need_part = false, need_prefix = false;
   const uint64_t w0 = t->st.w_max;
   std::map<std::tuple<uint32_t, uint32_t, uint32_t, uint64_t>, uint32_t> job_index;
   std::vector<ReplayJob> jobs;
@@ -461,6 +474,7 @@ kv_status kv_eval_configs(const kv_trace* h, const kv_config* cfg, uint32_t n_cf
     for (uint32_t g = 0; g < ng; ++g) {
       const uint32_t pol = group_policy(C, g);
       if (pol == KV_POLICY_LRU) {
+        need_prefix |= C.mode == KV_MODE_INCLUSIVE_PREFIX;
         if (part_order) {
           need_part = true;
           add_thresholds(tpt, C, g, g, w0);
@@ -517,19 +531,21 @@ kv_status kv_eval_configs(const kv_trace* h, const kv_config* cfg, uint32_t n_cf
   // ---- LRU: stack-distance passes + closed forms
   auto lru = [&]() -> kv_status {
     kv_status r;
-    OrderView vsh, vpt;
+    OrderView vsh, vpt, vpx, unused;
     if (need_shared) {
       finish_set(t->shared_ts, tsh, G);
-      if ((r = run_stack(*t, t->shared, false, t->shared_ts, StackSlot{5, 6}, vsh, s)) != KV_OK)
+      if ((r = run_stack(*t, t->shared, false, t->shared_ts,
+                         StackSlot{5, 6, need_prefix ? 24 : -1}, vsh, vpx, s)) != KV_OK)
         return r;
     }
     if (need_part) {
       finish_set(t->part_ts, tpt, G);
-      if ((r = run_stack(*t, t->part, true, t->part_ts, StackSlot{7, 8}, vpt, s)) != KV_OK)
+      if ((r = run_stack(*t, t->part, true, t->part_ts, StackSlot{7, 8, -1}, vpt, unused, s)) !=
+          KV_OK)
         return r;
     }
     if (need_shared || need_part)
-      return lru_counts(cfg_dev, n_cfg, G, vsh, vpt, bgs.as<GroupStats>(), counts, s);
+      return lru_counts(cfg_dev, n_cfg, G, vsh, vpt, vpx, bgs.as<GroupStats>(), counts, s);
     return KV_OK;
   };
   // ---- FIFO / LFU: replay jobs, with the LRU work running meanwhile

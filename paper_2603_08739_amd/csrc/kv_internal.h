@@ -89,7 +89,7 @@ struct Trace {
   DevBuf req;         // u32[n] request of each access (trace order)
   DevBuf req_time;    // f64[n_req] arrival time of each request
   // workspace reused across kv_eval_configs calls on this trace
-  DevBuf ws[24];
+  DevBuf ws[27];
   // host staging of the latest kv_eval_configs call (alive across its copies)
   ThresholdSet shared_ts, part_ts;
   std::vector<kv_config> cfg_stage;
@@ -137,9 +137,11 @@ kv_status canon_partition(Trace& t, hipStream_t s);
 // hist: u64[total_bins][4] = {count, weight, final count, final weight},
 // made cumulative over the bins of each group on return.
 // thr_dev / off_dev: device copies of ts.values / ts.off; hist must be zeroed.
+// phist (zeroed, same layout, or NULL; trace order only): fields 0 and 1
+// count the accesses by their request-prefix distance (prefix reuse).
 kv_status stack_pass(Trace& t, Order& o, bool partitioned, const ThresholdSet& ts,
                      const uint32_t* thr_dev, const uint32_t* off_dev, uint64_t* hist,
-                     hipStream_t s);
+                     uint64_t* phist, hipStream_t s);
 
 // per-configuration evaluation (k_eval.hip)
 
@@ -150,10 +152,11 @@ struct OrderView {
   const uint64_t* hist = nullptr;
 };
 // Writes the records of every (config, group) whose policy is LRU.  Groups of
-// partitioned configs read `part` when n_groups > 1, `shared` otherwise.
+// partitioned configs read `part` when n_groups > 1, `shared` otherwise;
+// prefix-reuse configs take their hits from `prefix` (trace order).
 kv_status lru_counts(const kv_config* cfg_dev, uint32_t n_cfg, uint32_t n_groups,
-                     OrderView shared, OrderView part, const GroupStats* gs_dev,
-                     uint64_t* counts, hipStream_t s);
+                     OrderView shared, OrderView part, OrderView prefix,
+                     const GroupStats* gs_dev, uint64_t* counts, hipStream_t s);
 kv_status objectives(const kv_config* cfg_dev, uint32_t n_cfg, uint32_t n_groups,
                      const uint64_t* counts, const kv_cost_model& m, double gb, double tpg,
                      double span, double n_req, uint64_t n_w, double* obj, hipStream_t s);

@@ -9,12 +9,12 @@ from .workloads import (Trace, Recipe, recipe, make, tiny, chat, tenant, longctx
                         random_trace, WORKLOADS)
 from .configs import (ConfigBatch, configs_for, grid, from_list, empty, split_capacity,
                       random_configs,
-                      DEFAULT_COST, MODE_INCLUSIVE, MODE_EXCLUSIVE_DEMOTE, POLICY_LRU,
+                      DEFAULT_COST, MODE_INCLUSIVE, MODE_EXCLUSIVE_DEMOTE, MODE_INCLUSIVE_PREFIX, POLICY_LRU,
                       POLICY_FIFO, POLICY_LFU, MAX_GROUPS, GIB, TIB)
 
 __all__ = [
     "Trace", "Recipe", "recipe", "make", "tiny", "chat", "tenant", "longctx", "full", "from_blocks",
     "random_trace", "WORKLOADS", "ConfigBatch", "configs_for", "grid", "from_list",
-    "empty", "split_capacity", "random_configs", "DEFAULT_COST", "MODE_INCLUSIVE", "MODE_EXCLUSIVE_DEMOTE",
+    "empty", "split_capacity", "random_configs", "DEFAULT_COST", "MODE_INCLUSIVE", "MODE_EXCLUSIVE_DEMOTE", "MODE_INCLUSIVE_PREFIX",
     "POLICY_LRU", "POLICY_FIFO", "POLICY_LFU", "MAX_GROUPS", "GIB", "TIB",
 ]

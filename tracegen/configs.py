@@ -8,7 +8,9 @@ group.  The planner in the paper emits such candidates on a grid (Section
 Encodings (shared input format of the library and the oracle):
 
 * mode:   0 = inclusive (every tier an independent cache over all
-          accesses), 1 = exclusive with write-back demotion (LRU only).
+          accesses), 1 = exclusive with write-back demotion (LRU only),
+          2 = inclusive with prefix reuse (a request reuses a run of its
+          blocks from its first block on; LRU, shared caches only).
 * policy: 0 = LRU, 1 = FIFO, 2 = LFU.
 * partitioned: 0 = one cache per tier shared by all groups (policy[0]);
                1 = tier capacity split per group (cap_group[k][g], policy[g]).
@@ -27,6 +29,7 @@ MAX_GROUPS = 16
 
 MODE_INCLUSIVE = 0
 MODE_EXCLUSIVE_DEMOTE = 1
+MODE_INCLUSIVE_PREFIX = 2
 
 POLICY_LRU = 0
 POLICY_FIFO = 1
