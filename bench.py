@@ -225,6 +225,36 @@ def group_ttl(dev, rec, torch, K, k=7, budget_fracs=(0.02, 0.05, 0.25)):
             "grouping_and_curves_s": t1 - t0, "optimise_s": t2 - t1}
 
 
+def prefix_reuse(h, cfgs, G, model, torch, K):
+    """The workload's 10,000 LRU configurations with radix-tree prefix reuse
+    against the plain inclusive mode: device time of one evaluation each and
+    the share of accesses the tiers serve."""
+    import tracegen as tg
+    from paper_2603_08739_amd import host
+    lru = cfgs.subset(np.nonzero(cfgs.policy[:, 0] == tg.POLICY_LRU)[0])
+    out = {}
+    for name, mode in (("plain", tg.MODE_INCLUSIVE), ("prefix", tg.MODE_INCLUSIVE_PREFIX)):
+        b = lru.subset(np.arange(lru.n))
+        b.mode[:] = mode
+        arr, n_cfg = host.config_array(b)
+        counts = torch.zeros((n_cfg, G, 3, 8), dtype=torch.int64, device="cuda")
+        K.kv_eval_configs(h, arr, n_cfg, model, counts, None)
+        torch.cuda.synchronize()
+        K.kv_timing_read(reset=True)
+        K.kv_timing_enable(True)
+        K.kv_eval_configs(h, arr, n_cfg, model, counts, None)
+        torch.cuda.synchronize()
+        K.kv_timing_enable(False)
+        tm = K.kv_timing_read(reset=True)
+        served = counts[..., 0].sum(dim=(1, 2)).double().mean().item()
+        out[name] = {"device_ms": round(sum(v[1] for v in tm.values()), 3),
+                     "mean_served_accesses": served}
+    print(f"[bench] prefix reuse: {out['prefix']['device_ms']} ms against "
+          f"{out['plain']['device_ms']} ms", file=sys.stderr, flush=True)
+    out["configs"] = lru.n
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -323,6 +353,7 @@ def main():
     K.kv_timing_enable(False)
     t_calls, t_ms = K.kv_timing_read(reset=True)["ttl_curves"]
     search = adaptive_search(h, rec, G, model, torch, K)
+    prefix = prefix_reuse(h, cfgs, G, model, torch, K)
     h.free()
     gttl = group_ttl(dev, rec, torch, K)
     ttl_ms = t_ms / max(t_calls, 1)
@@ -343,7 +374,7 @@ def main():
         "config": {"workload": WORKLOAD_TEXT[args.workload], "name": args.workload,
                    "n_accesses": n, "n_configs": n_cfg, "n_requests": int(rec.len0.shape[0])},
         "roofline": roof, "cpu_baseline": cpu, "ttl_curves": ttl, "adaptive_search": search,
-        "group_ttl": gttl,
+        "group_ttl": gttl, "prefix_reuse": prefix,
     }
     print(json.dumps(out))
 

@@ -49,6 +49,12 @@ def full_run():
     counts, obj = host.evaluate(h, cfgs, tg.DEFAULT_COST, rec.n_groups)
     say("  full sweep: TTL curves")
     ttl_out = host.ttl_curves(h, TTL_FULL, rec.n_groups)
+    say("  full sweep: prefix reuse")
+    lru = cfgs.subset(np.nonzero(cfgs.policy[:, 0] == tg.POLICY_LRU)[0][::20])
+    pref = lru.subset(np.arange(lru.n))
+    pref.mode[:] = tg.MODE_INCLUSIVE_PREFIX
+    plain_c, _ = host.evaluate(h, lru, tg.DEFAULT_COST, rec.n_groups)
+    pref_c, _ = host.evaluate(h, pref, tg.DEFAULT_COST, rec.n_groups)
     h.free()
     say("  full sweep: Pareto fronts")
     front, nfront = host.pareto(obj)
@@ -92,7 +98,8 @@ def full_run():
     say("  full sweep: done")
     return dict(cfgs=cfgs, counts=counts.astype(np.int64), obj=obj, front=front,
                 nfront=nfront, front_seg=front_seg, st=st, n=n, n_w=n_w, u=u,
-                distinct_w=distinct_w, ttl=ttl_out, ref_ttl=ref_ttl, regap=regap)
+                distinct_w=distinct_w, ttl=ttl_out, ref_ttl=ref_ttl, regap=regap,
+                plain_c=plain_c.astype(np.int64), pref_c=pref_c.astype(np.int64))
 
 
 def test_trace_statistics(full_run):
@@ -242,3 +249,13 @@ def test_ttl_curves_match_torch(full_run):
     assert (store[:, 0] == 0.0).all()
     assert (np.diff(hits.astype(np.int64), axis=1) >= 0).all()
     assert (np.diff(store, axis=1) >= 0).all()
+
+
+def test_prefix_reuse_properties(full_run):
+    """The workload's block hashes are prefix chains (a block's hash covers
+    its whole prefix), so every request touches a block's prefix right
+    before the block itself: under LRU the earlier blocks of a request are
+    never deeper in the stack than the later ones, the running maximum of
+    the distances over a request is the distance itself, and prefix reuse
+    must give exactly the plain inclusive records."""
+    np.testing.assert_array_equal(full_run["pref_c"], full_run["plain_c"])
