@@ -1904,7 +1904,7 @@ __global__ __launch_bounds__(256) void k_combine(const RecDev* __restrict__ recs
 constexpr int kCbB = 32;          // words per batch
 constexpr int kCbSrc = 128;       // hit-bit sources at most
 constexpr int kCbNT = 1024;       // records per launch
-constexpr int kCbRows = kCbSrc + 16 + KV_MAX_GROUPS;  // sources, 2 x 8 planes, group masks
+constexpr int kCbRows = kCbSrc + 16 + KV_MAX_GROUPS;  // sources, 2 x 8 planes, group masks (most)
 constexpr int kCbLd = (kCbRows * kCbB + kCbNT - 1) / kCbNT;  // staged words per thread
 
 struct CbSrc {
@@ -1928,17 +1928,16 @@ struct CombineTileArgs {
 
 __device__ __forceinline__ uint64_t cb_load(const CombineTileArgs& a, uint32_t row, uint64_t w) {
   if (w >= a.nwords) return 0ull;
-  if (row < (uint32_t)kCbSrc) {
-    if (row >= a.n_src) return 0ull;
+  if (row < a.n_src) {
     const CbSrc c = a.src[row];
     return (w >= c.wlo && w <= c.whi) ? c.p[w - c.wlo] : 0ull;
   }
-  if (row < (uint32_t)kCbSrc + 16) {
-    const uint32_t o = (row - kCbSrc) >> 3, b = (row - kCbSrc) & 7;
+  if (row < a.n_src + 16) {
+    const uint32_t o = (row - a.n_src) >> 3, b = (row - a.n_src) & 7;
     if (!a.planes[o] || !((a.plane_mask >> b) & 1u)) return 0ull;
     return a.planes[o][(uint64_t)b * a.nwords + w];
   }
-  const uint32_t g = row - kCbSrc - 16;
+  const uint32_t g = row - a.n_src - 16;
   return g < a.n_gm ? a.gmask[(uint64_t)g * a.nwords + w] : 0ull;
 }
 
@@ -1950,6 +1949,8 @@ __global__ __launch_bounds__(kCbNT) void k_combine_tile(CombineTileArgs a) {
   if (tid < a.n_src) ssrc[tid] = a.src[tid];
   __syncthreads();
   a.src = ssrc;
+  // staged rows: the sources, then 2 x 8 weight planes, then the group masks
+  const uint32_t n_items = (a.n_src + 16 + a.n_gm) * kCbB;
   const uint32_t ri = a.rec0 + tid;
   const bool have = ri < a.n_recs;
   RecDev r{};
@@ -1964,14 +1965,14 @@ __global__ __launch_bounds__(kCbNT) void k_combine_tile(CombineTileArgs a) {
 #pragma unroll
     for (int q = 0; q < kCbLd; ++q) {
       const uint32_t item = tid + q * kCbNT;
-      nxt[q] = item < (uint32_t)(kCbRows * kCbB) ? cb_load(a, item / kCbB, wb + item % kCbB) : 0ull;
+      nxt[q] = item < n_items ? cb_load(a, item / kCbB, wb + item % kCbB) : 0ull;
     }
   };
   auto put = [&](int buf) {
 #pragma unroll
     for (int q = 0; q < kCbLd; ++q) {
       const uint32_t item = tid + q * kCbNT;
-      if (item < (uint32_t)(kCbRows * kCbB)) sw[buf][item / kCbB][item % kCbB] = nxt[q];
+      if (item < n_items) sw[buf][item / kCbB][item % kCbB] = nxt[q];
     }
   };
   if (w0 < w1) {
@@ -1983,14 +1984,14 @@ __global__ __launch_bounds__(kCbNT) void k_combine_tile(CombineTileArgs a) {
   for (uint64_t wb = w0; wb < w1; wb += kCbB) {
     if (wb + kCbB < w1) fetch(wb + kCbB);
     if (live && wb <= rwhi && wb + kCbB > rwlo) {
-      const uint32_t po = kCbSrc + 8 * r.order;
+      const uint32_t po = a.n_src + 8 * r.order;
       for (int b = 0; b < kCbB; ++b) {
         const uint64_t w = wb + b;
         if (w < rwlo || w > rwhi || w >= w1) continue;
         uint64_t m = ~0ull;
         if (w == rwlo) m &= ~0ull << (r.begin & 63);
         if (w == rwhi && (r.end & 63)) m &= (1ull << (r.end & 63)) - 1;
-        if (r.filter) m &= sw[cur][kCbSrc + 16 + r.group][b];
+        if (r.filter) m &= sw[cur][a.n_src + 16 + r.group][b];
         const uint64_t p0 = r.src[0] >= 0 ? sw[cur][r.src[0]][b] : 0ull;
         const uint64_t p1 = r.src[1] >= 0 ? sw[cur][r.src[1]][b] : 0ull;
         const uint64_t p2 = r.src[2] >= 0 ? sw[cur][r.src[2]][b] : 0ull;
@@ -2190,20 +2191,34 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
       }
     }
   }
-  // hit-bit sources of the tiled combine: one per replayed job, one per
-  // order for jobs whose cache holds everything (a hit is a re-access)
-  std::vector<int32_t> src_of(jd.size() + 2, -1);  // jobs, then the two orders
-  uint32_t n_src = 0;
-  for (RecDev& r : recs) {
+  // FIFO records first: they are combined on the FIFO jobs' stream as soon
+  // as those are done, the others once every job is
+  auto rec_fifo = [&](const RecDev& r) {
+    for (int k = 0; k < 3; ++k)
+      if (r.job[k] >= 0) return jd[r.job[k]].policy == KV_POLICY_FIFO;
+    return true;
+  };
+  std::stable_partition(recs.begin(), recs.end(), rec_fifo);
+  uint32_t nf = 0;
+  while (nf < recs.size() && rec_fifo(recs[nf])) ++nf;
+  // hit-bit sources of the tiled combine, per record class (FIFO / other):
+  // one per replayed job, one per order for jobs whose cache holds
+  // everything (a hit is a re-access)
+  std::vector<int32_t> src_of[2] = {std::vector<int32_t>(jd.size() + 2, -1),
+                                    std::vector<int32_t>(jd.size() + 2, -1)};
+  uint32_t n_src[2] = {0, 0};
+  for (size_t i = 0; i < recs.size(); ++i) {
+    RecDev& r = recs[i];
+    const int cls = i < nf ? 0 : 1;
     for (int k = 0; k < 3; ++k) {
       r.src[k] = -1;
       if (r.job[k] < 0) continue;
       const size_t key = jd[r.job[k]].closed ? jd.size() + r.order : (size_t)r.job[k];
-      if (src_of[key] < 0) src_of[key] = (int32_t)n_src++;
-      r.src[k] = (int16_t)std::min<int32_t>(src_of[key], 0x7FFF);
+      if (src_of[cls][key] < 0) src_of[cls][key] = (int32_t)n_src[cls]++;
+      r.src[k] = (int16_t)std::min<int32_t>(src_of[cls][key], 0x7FFF);
     }
   }
-  const bool tiled = n_src <= (uint32_t)kCbSrc;
+  const bool tiled = n_src[0] <= (uint32_t)kCbSrc && n_src[1] <= (uint32_t)kCbSrc;
   DevBuf& bj = t.ws[11];
   DevBuf& bstate = t.ws[12];
   DevBuf& bcls = t.ws[13];
@@ -2271,6 +2286,88 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
     KV_HIP(hipGetLastError());
     tm.reset();
   }
+  // the combine's inputs, staged before the streams fork (the FIFO records
+  // are combined on the FIFO stream)
+  CombineArgs ca{};
+  ca.jobs = bj.as<JobDev>();
+  ca.bits = bbits.as<uint64_t>();
+  ca.jcnt = bjc.as<unsigned long long>();
+  ca.reuse[0] = reuse[0];
+  ca.reuse[1] = have_part ? reuse[1] : reuse[0];
+  ca.planes[0] = planes[0];
+  ca.planes[1] = have_part ? planes[1] : planes[0];
+  ca.gmask = gmask[0];
+  ca.nwords = nwords;
+  ca.n_groups = G;
+  ca.uniform_w = (t.st.w_min == t.st.w_max) ? t.st.w_max : 0u;
+  uint32_t pm = 0;
+  for (uint32_t w = t.st.w_min; w <= t.st.w_max; ++w) pm |= w;
+  ca.plane_mask = pm;
+  const uint32_t nrec = (uint32_t)recs.size();
+  CombineTileArgs ta{};
+  DevBuf& bsrc = t.ws[18];
+  DevBuf& bpart = t.ws[19];
+  if (tiled && nrec) {
+    std::vector<CbSrc> srcs(n_src[0] + n_src[1]);
+    for (int cls = 0; cls < 2; ++cls) {
+      for (size_t key = 0; key < src_of[cls].size(); ++key) {
+        const int32_t sl = src_of[cls][key];
+        if (sl < 0) continue;
+        CbSrc c{};
+        if (key >= jd.size()) {
+          c.p = ca.reuse[key - jd.size()];
+          c.wlo = 0;
+          c.whi = nwords - 1;
+        } else {
+          const JobDev& q = jd[key];
+          c.p = bbits.as<uint64_t>() + q.bits_off;
+          c.wlo = q.word0;
+          c.whi = (q.end - 1) >> 6;
+        }
+        srcs[(cls ? n_src[0] : 0) + sl] = c;
+      }
+    }
+    if ((st = bsrc.reserve(std::max<size_t>(srcs.size(), 1) * sizeof(CbSrc))) != KV_OK) return st;
+    if ((st = bpart.reserve((size_t)nrec * 6 * 8)) != KV_OK) return st;
+    t.src_stage.resize(srcs.size() * sizeof(CbSrc));
+    std::memcpy(t.src_stage.data(), srcs.data(), t.src_stage.size());
+    if (!srcs.empty())
+      KV_HIP(hipMemcpyAsync(bsrc.p, t.src_stage.data(), t.src_stage.size(),
+                            hipMemcpyHostToDevice, s));
+    if ((st = fill_u64(bpart.as<uint64_t>(), 0, (uint64_t)nrec * 6, s)) != KV_OK) return st;
+    bool any_filter = false;
+    for (const RecDev& r : recs) any_filter |= r.filter != 0;
+    ta.recs = brec.as<RecDev>();
+    ta.planes[0] = planes[0];
+    ta.planes[1] = have_part ? planes[1] : nullptr;
+    ta.plane_mask = pm;
+    ta.uniform_w = ca.uniform_w;
+    ta.gmask = gmask[0];
+    ta.n_gm = any_filter ? G : 0u;
+    ta.nwords = nwords;
+    ta.part = bpart.as<unsigned long long>();
+    int ncu = 0;
+    KV_HIP(hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, t.device));
+    const uint64_t nb0 = std::max<uint64_t>(1, std::min<uint64_t>((uint64_t)std::max(ncu, 1),
+                                                                  div_up(nwords, kCbB)));
+    ta.wpb = (uint64_t)div_up(div_up(nwords, nb0), kCbB) * kCbB;
+  }
+  // records [r0, r1) of one class, tile by tile
+  auto combine_range = [&](uint32_t r0, uint32_t r1, hipStream_t sk) -> kv_status {
+    if (r0 >= r1) return KV_OK;
+    CombineTileArgs x = ta;
+    const int cls = r0 < nf ? 0 : 1;
+    x.src = bsrc.as<CbSrc>() + (cls ? n_src[0] : 0);
+    x.n_src = n_src[cls];
+    x.n_recs = r1;
+    const uint32_t nb = div_up(nwords, x.wpb);
+    for (uint32_t q = r0; q < r1; q += kCbNT) {
+      x.rec0 = q;
+      hipLaunchKernelGGL(k_combine_tile, dim3(nb), dim3(kCbNT), 0, sk, x);
+      KV_HIP(hipGetLastError());
+    }
+    return KV_OK;
+  };
   // LFU jobs of one group, other LFU jobs, FIFO jobs and the caller's other
   // work (the LRU stack pass) run concurrently: the replay kernels on
   // streams forked from the caller's and joined back into it before the
@@ -2308,6 +2405,11 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
                          bjc.as<unsigned long long>());
     KV_HIP(hipGetLastError());
     tm.reset();
+    if (k == 2 && tiled && nf) {
+      tm.emplace(kStCombine, sk);
+      if ((st = combine_range(0, nf, sk)) != KV_OK) return st;
+      tm.reset();
+    }
     KV_HIP(hipEventRecord(aux->join[k], sk));
   }
   const kv_status st_mid = meanwhile();
@@ -2345,76 +2447,9 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
   tm.reset();
   if (!recs.empty()) {
     tm.emplace(kStCombine, s);
-    CombineArgs ca{};
-    ca.jobs = bj.as<JobDev>();
-    ca.bits = bbits.as<uint64_t>();
-    ca.jcnt = bjc.as<unsigned long long>();
-    ca.reuse[0] = reuse[0];
-    ca.reuse[1] = have_part ? reuse[1] : reuse[0];
-    ca.planes[0] = planes[0];
-    ca.planes[1] = have_part ? planes[1] : planes[0];
-    ca.gmask = gmask[0];
-    ca.nwords = nwords;
-    ca.n_groups = G;
-    ca.uniform_w = (t.st.w_min == t.st.w_max) ? t.st.w_max : 0u;
-    uint32_t pm = 0;
-    for (uint32_t w = t.st.w_min; w <= t.st.w_max; ++w) pm |= w;
-    ca.plane_mask = pm;
-    const uint32_t nrec = (uint32_t)recs.size();
     if (tiled) {
-      std::vector<CbSrc> srcs(n_src);
-      for (size_t key = 0; key < src_of.size(); ++key) {
-        const int32_t sl = src_of[key];
-        if (sl < 0) continue;
-        CbSrc c{};
-        if (key >= jd.size()) {
-          c.p = ca.reuse[key - jd.size()];
-          c.wlo = 0;
-          c.whi = nwords - 1;
-        } else {
-          const JobDev& q = jd[key];
-          c.p = bbits.as<uint64_t>() + q.bits_off;
-          c.wlo = q.word0;
-          c.whi = (q.end - 1) >> 6;
-        }
-        srcs[sl] = c;
-      }
-      DevBuf& bsrc = t.ws[18];
-      DevBuf& bpart = t.ws[19];
-      if ((st = bsrc.reserve(std::max<size_t>(n_src, 1) * sizeof(CbSrc))) != KV_OK) return st;
-      if ((st = bpart.reserve((size_t)nrec * 6 * 8)) != KV_OK) return st;
-      t.src_stage.resize(srcs.size() * sizeof(CbSrc));
-      std::memcpy(t.src_stage.data(), srcs.data(), t.src_stage.size());
-      if (n_src)
-        KV_HIP(hipMemcpyAsync(bsrc.p, t.src_stage.data(), t.src_stage.size(),
-                              hipMemcpyHostToDevice, s));
-      if ((st = fill_u64(bpart.as<uint64_t>(), 0, (uint64_t)nrec * 6, s)) != KV_OK) return st;
-      bool any_filter = false;
-      for (const RecDev& r : recs) any_filter |= r.filter != 0;
-      CombineTileArgs ta{};
-      ta.recs = brec.as<RecDev>();
-      ta.n_recs = nrec;
-      ta.src = bsrc.as<CbSrc>();
-      ta.n_src = n_src;
-      ta.planes[0] = planes[0];
-      ta.planes[1] = have_part ? planes[1] : nullptr;
-      ta.plane_mask = pm;
-      ta.uniform_w = ca.uniform_w;
-      ta.gmask = gmask[0];
-      ta.n_gm = any_filter ? G : 0u;
-      ta.nwords = nwords;
-      ta.part = bpart.as<unsigned long long>();
-      int ncu = 0;
-      KV_HIP(hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, t.device));
-      const uint64_t nb0 = std::max<uint64_t>(1, std::min<uint64_t>((uint64_t)std::max(ncu, 1),
-                                                                    div_up(nwords, kCbB)));
-      ta.wpb = (uint64_t)div_up(div_up(nwords, nb0), kCbB) * kCbB;
-      const uint32_t nb = div_up(nwords, ta.wpb);
-      for (uint32_t r0 = 0; r0 < nrec; r0 += kCbNT) {
-        ta.rec0 = r0;
-        hipLaunchKernelGGL(k_combine_tile, dim3(nb), dim3(kCbNT), 0, s, ta);
-        KV_HIP(hipGetLastError());
-      }
+      if (!any[2] && (st = combine_range(0, nf, s)) != KV_OK) return st;
+      if ((st = combine_range(nf, nrec, s)) != KV_OK) return st;
       hipLaunchKernelGGL(k_combine_fin, dim3(div_up(nrec, 256)), dim3(256), 0, s,
                          brec.as<RecDev>(), nrec, bpart.as<unsigned long long>(),
                          bjc.as<unsigned long long>(), G, counts);
