@@ -61,6 +61,9 @@ def parse():
     ap.add_argument("--workload", default="full", choices=sorted(WORKLOAD_TEXT))
     ap.add_argument("--cpu-baseline-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the TTL-curve, adaptive-search, group-TTL and prefix-reuse "
+                         "measurements that follow the timed steps")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="first run one plain device-to-device copy of BYTES (a reference "
                          "for hardware byte counters)")
@@ -255,6 +258,39 @@ def prefix_reuse(h, cfgs, G, model, torch, K):
     return out
 
 
+def extras(dev, rec, cfgs, G, model, n, torch, K):
+    """Measurements outside the timed step: TTL curves, Alg. 1, prefix reuse,
+    Alg. 2."""
+    # TTL curves (disk-tier retention for the group TTL) over the same trace,
+    # outside the step: one call per measured launch, timed by the library
+    h = K.kv_trace_load(dev["hash"], dev["req"], dev["req_time"], group=dev["group"],
+                        weight=dev["weight"], n_groups=G,
+                        tokens_per_granule=rec.tokens_per_granule,
+                        granule_bytes=rec.granule_bytes)
+    t_hits = torch.zeros((G, len(TTL_GRID)), dtype=torch.int64, device="cuda")
+    t_hitw = torch.zeros_like(t_hits)
+    t_store = torch.zeros((G, len(TTL_GRID)), dtype=torch.float64, device="cuda")
+    K.kv_ttl_curves(h, TTL_GRID, t_hits, t_hitw, t_store)
+    torch.cuda.synchronize()
+    K.kv_timing_enable(True)
+    for _ in range(5):
+        K.kv_ttl_curves(h, TTL_GRID, t_hits, t_hitw, t_store)
+    torch.cuda.synchronize()
+    K.kv_timing_enable(False)
+    t_calls, t_ms = K.kv_timing_read(reset=True)["ttl_curves"]
+    search = adaptive_search(h, rec, G, model, torch, K)
+    prefix = prefix_reuse(h, cfgs, G, model, torch, K)
+    h.free()
+    gttl = group_ttl(dev, rec, torch, K)
+    ttl_ms = t_ms / max(t_calls, 1)
+    ttl_ach = ALGO_BYTES["ttl_curves"] * n / (ttl_ms / 1000.0) / 1e9
+    ttl = {"n_ttl": len(TTL_GRID), "avg_launch_ms": ttl_ms, "launches": t_calls,
+           "bound": "hbm", "achieved": ttl_ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+           "frac": ttl_ach / HBM_PEAK_GBS, "traffic": traffic_for("ttl_curves")}
+    print(f"[bench] TTL curves {ttl_ms:.3f} ms", file=sys.stderr, flush=True)
+    return ttl, search, prefix, gttl
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -335,33 +371,9 @@ def main():
             "avg_launch_ms": avg_ms, "launches": calls,
             "stage_ms_per_step": {k: round(v[1] / args.steps, 3) for k, v in timing.items()
                                   if v[0]}}
-    # TTL curves (disk-tier retention for the group TTL) over the same trace,
-    # outside the step: one call per measured launch, timed by the library
-    h = K.kv_trace_load(dev["hash"], dev["req"], dev["req_time"], group=dev["group"],
-                        weight=dev["weight"], n_groups=G,
-                        tokens_per_granule=rec.tokens_per_granule,
-                        granule_bytes=rec.granule_bytes)
-    t_hits = torch.zeros((G, len(TTL_GRID)), dtype=torch.int64, device="cuda")
-    t_hitw = torch.zeros_like(t_hits)
-    t_store = torch.zeros((G, len(TTL_GRID)), dtype=torch.float64, device="cuda")
-    K.kv_ttl_curves(h, TTL_GRID, t_hits, t_hitw, t_store)
-    torch.cuda.synchronize()
-    K.kv_timing_enable(True)
-    for _ in range(5):
-        K.kv_ttl_curves(h, TTL_GRID, t_hits, t_hitw, t_store)
-    torch.cuda.synchronize()
-    K.kv_timing_enable(False)
-    t_calls, t_ms = K.kv_timing_read(reset=True)["ttl_curves"]
-    search = adaptive_search(h, rec, G, model, torch, K)
-    prefix = prefix_reuse(h, cfgs, G, model, torch, K)
-    h.free()
-    gttl = group_ttl(dev, rec, torch, K)
-    ttl_ms = t_ms / max(t_calls, 1)
-    ttl_ach = ALGO_BYTES["ttl_curves"] * n / (ttl_ms / 1000.0) / 1e9
-    ttl = {"n_ttl": len(TTL_GRID), "avg_launch_ms": ttl_ms, "launches": t_calls,
-           "bound": "hbm", "achieved": ttl_ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-           "frac": ttl_ach / HBM_PEAK_GBS, "traffic": traffic_for("ttl_curves")}
-    print(f"[bench] TTL curves {ttl_ms:.3f} ms", file=sys.stderr, flush=True)
+    ttl = search = prefix = gttl = None
+    if not args.no_extras:
+        ttl, search, prefix, gttl = extras(dev, rec, cfgs, G, model, n, torch, K)
     cpu = None
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
