@@ -92,3 +92,15 @@ def test_unsupported(lib):
         host.evaluate(h, part, tg.DEFAULT_COST, 2)
     assert e.value.status == K.KV_ERR_UNSUPPORTED
     h.free()
+
+
+def test_request_ids_with_gaps(lib, oracle_mod):
+    """Request indices may skip values (requests without blocks): every
+    request still starts where its first block is."""
+    rng = np.random.default_rng(5)
+    t = tg.random_trace(960, 6_000, 700, zipf_s=0.8, reuse_bias=0.3, per_request=7)
+    gaps = rng.integers(1, 4, int(t.req[-1]) + 1).cumsum()   # request r -> r-th id with gaps
+    t.req = gaps[t.req].astype(np.uint32)
+    t.req_time = np.sort(rng.uniform(0, 100, int(t.req[-1]) + 3))
+    caps = [(c, d, 0) for c in (16, 64, 256) for d in (0, 512)]
+    compare(lib, oracle_mod, t, batch(caps), "prefix-gaps")
