@@ -1897,15 +1897,19 @@ __global__ __launch_bounds__(256) void k_combine(const RecDev* __restrict__ recs
 
 // Records combined tile by tile.  A block owns a range of words (64 accesses
 // each) and every record of the launch (one per thread); each batch of kCbB
-// words of every hit-bit source (job bitmaps, re-access bits), weight plane
-// and group mask is staged once in LDS and read by all records, so the
-// sources cross HBM once instead of once per record.  The next batch is
-// loaded while the current one is counted.
+// words of every hit-bit source (job bitmaps, re-access bits), group mask
+// and (mixed weights only) weight plane is staged once in LDS and read by
+// all records, so the sources cross HBM once instead of once per record.
+// The next batch is loaded while the current one is counted.  Two constant
+// rows (all zeros, all ones) stand in for an absent tier and for the mask
+// of a record that counts every group, so a batch inside a record's range
+// is counted without a branch or a mask.
 constexpr int kCbB = 32;          // words per batch
 constexpr int kCbSrc = 128;       // hit-bit sources at most
 constexpr int kCbNT = 1024;       // records per launch
-constexpr int kCbRows = kCbSrc + 16 + KV_MAX_GROUPS;  // sources, 2 x 8 planes, group masks (most)
-constexpr int kCbLd = (kCbRows * kCbB + kCbNT - 1) / kCbNT;  // staged words per thread
+constexpr int kCbZero = 0, kCbOnes = 1, kCbRow0 = 2;   // constant rows, first staged row
+constexpr int kCbRows = kCbRow0 + kCbSrc + KV_MAX_GROUPS + 16;  // + sources, masks, 2 x 8 planes
+constexpr int kCbLd = ((kCbRows - kCbRow0) * kCbB + kCbNT - 1) / kCbNT;  // staged words per thread
 
 struct CbSrc {
   const uint64_t* p;   // word w at p[w - wlo]
@@ -1926,37 +1930,96 @@ struct CombineTileArgs {
   unsigned long long* part;  // [n_recs][6]: hits of u0, u1, u2, then their weights
 };
 
-__device__ __forceinline__ uint64_t cb_load(const CombineTileArgs& a, uint32_t row, uint64_t w) {
+// Staged row `row` (counted from the first staged row): the sources, the
+// group masks, then (mixed weights) the 2 x 8 weight planes.
+__device__ __forceinline__ uint64_t cb_load(const CombineTileArgs& a, const CbSrc* src,
+                                            uint32_t row, uint64_t w) {
   if (w >= a.nwords) return 0ull;
   if (row < a.n_src) {
-    const CbSrc c = a.src[row];
+    const CbSrc c = src[row];
     return (w >= c.wlo && w <= c.whi) ? c.p[w - c.wlo] : 0ull;
   }
-  if (row < a.n_src + 16) {
-    const uint32_t o = (row - a.n_src) >> 3, b = (row - a.n_src) & 7;
-    if (!a.planes[o] || !((a.plane_mask >> b) & 1u)) return 0ull;
-    return a.planes[o][(uint64_t)b * a.nwords + w];
-  }
-  const uint32_t g = row - a.n_src - 16;
-  return g < a.n_gm ? a.gmask[(uint64_t)g * a.nwords + w] : 0ull;
+  row -= a.n_src;
+  if (row < a.n_gm) return a.gmask[(uint64_t)row * a.nwords + w];
+  row -= a.n_gm;
+  const uint32_t o = row >> 3, b = row & 7;
+  if (!a.planes[o] || !((a.plane_mask >> b) & 1u)) return 0ull;
+  return a.planes[o][(uint64_t)b * a.nwords + w];
 }
 
-__global__ __launch_bounds__(kCbNT) void k_combine_tile(CombineTileArgs a) {
+// One word's three union counts (and, with weight planes, their weights)
+// under mask m.  rows = the staged batch, s* = the rows of the record's
+// tiers, p = its order's first weight plane, pm = the weight bits present.
+template <bool kPlanes>
+__device__ __forceinline__ void cb_count(const uint64_t (*rows)[kCbB + 1], int b, uint64_t m,
+                                         uint32_t s0, uint32_t s1, uint32_t s2, uint32_t p,
+                                         uint32_t pm, uint32_t* c, uint32_t* cw) {
+  const uint64_t p0 = rows[s0][b], p1 = rows[s1][b], p2 = rows[s2][b];
+  const uint64_t u0 = p0 & m, u1 = (p0 | p1) & m, u2 = (p0 | p1 | p2) & m;
+  c[0] += __popcll(u0);
+  c[1] += __popcll(u1);
+  c[2] += __popcll(u2);
+  if (kPlanes) {
+#pragma unroll
+    for (int pb = 0; pb < 8; ++pb) {
+      if (!((pm >> pb) & 1u)) continue;
+      const uint64_t pl = rows[p + pb][b];
+      cw[0] += (uint32_t)__popcll(u0 & pl) << pb;
+      cw[1] += (uint32_t)__popcll(u1 & pl) << pb;
+      cw[2] += (uint32_t)__popcll(u2 & pl) << pb;
+    }
+  }
+}
+
+// A batch of the record's words: the interior ones (every access inside the
+// record's range) without range checks, the others one by one.
+template <bool kPlanes>
+__device__ __forceinline__ void cb_batch(const uint64_t (*rows)[kCbB + 1], uint64_t wb,
+                                         uint64_t w1, const RecDev& r, uint32_t rm, uint32_t s0,
+                                         uint32_t s1, uint32_t s2, uint32_t p, uint32_t pm,
+                                         uint32_t* c, uint32_t* cw) {
+  const uint64_t rwlo = r.begin >> 6, rwhi = (r.end - 1) >> 6;
+  const uint64_t fwlo = (r.begin + 63) >> 6, fwhi = r.end >> 6;
+  if (wb >= fwlo && wb + kCbB <= fwhi && wb + kCbB <= w1) {
+#pragma unroll(kPlanes ? 2 : 8)
+    for (int b = 0; b < kCbB; ++b) cb_count<kPlanes>(rows, b, rows[rm][b], s0, s1, s2, p, pm, c, cw);
+  } else {
+    for (int b = 0; b < kCbB; ++b) {
+      const uint64_t w = wb + b;
+      if (w < rwlo || w > rwhi || w >= w1) continue;
+      uint64_t m = rows[rm][b];
+      if (w == rwlo) m &= ~0ull << (r.begin & 63);
+      if (w == rwhi && (r.end & 63)) m &= (1ull << (r.end & 63)) - 1;
+      cb_count<kPlanes>(rows, b, m, s0, s1, s2, p, pm, c, cw);
+    }
+  }
+}
+
+__global__ __launch_bounds__(kCbNT) void k_combine_tile(const CombineTileArgs a) {
   // rows padded by one word: records read different rows at the same word
   __shared__ uint64_t sw[2][kCbRows][kCbB + 1];
   __shared__ CbSrc ssrc[kCbSrc];
   const uint32_t tid = threadIdx.x;
   if (tid < a.n_src) ssrc[tid] = a.src[tid];
+  if (tid < 2 * (kCbB + 1)) {
+    const uint32_t bf = tid / (kCbB + 1), b = tid % (kCbB + 1);
+    sw[bf][kCbZero][b] = 0ull;
+    sw[bf][kCbOnes][b] = ~0ull;
+  }
   __syncthreads();
-  a.src = ssrc;
-  // staged rows: the sources, then 2 x 8 weight planes, then the group masks
-  const uint32_t n_items = (a.n_src + 16 + a.n_gm) * kCbB;
+  const bool weighted = a.uniform_w == 0;
+  const uint32_t n_items = (a.n_src + a.n_gm + (weighted ? 16u : 0u)) * kCbB;
   const uint32_t ri = a.rec0 + tid;
   const bool have = ri < a.n_recs;
   RecDev r{};
   if (have) r = a.recs[ri];
-  const uint64_t rwlo = r.begin >> 6, rwhi = r.end > r.begin ? (r.end - 1) >> 6 : 0;
   const bool live = have && r.end > r.begin;
+  const uint64_t rwlo = r.begin >> 6, rwhi = live ? (r.end - 1) >> 6 : 0;
+  const uint32_t s0 = r.src[0] >= 0 ? kCbRow0 + r.src[0] : kCbZero;
+  const uint32_t s1 = r.src[1] >= 0 ? kCbRow0 + r.src[1] : kCbZero;
+  const uint32_t s2 = r.src[2] >= 0 ? kCbRow0 + r.src[2] : kCbZero;
+  const uint32_t rm = r.filter ? kCbRow0 + a.n_src + r.group : kCbOnes;
+  const uint32_t rp = kCbRow0 + a.n_src + a.n_gm + 8 * r.order;
   const uint64_t w0 = (uint64_t)blockIdx.x * a.wpb;
   const uint64_t w1 = min<uint64_t>(a.nwords, w0 + a.wpb);
   unsigned long long acc[6] = {0, 0, 0, 0, 0, 0};
@@ -1965,14 +2028,14 @@ __global__ __launch_bounds__(kCbNT) void k_combine_tile(CombineTileArgs a) {
 #pragma unroll
     for (int q = 0; q < kCbLd; ++q) {
       const uint32_t item = tid + q * kCbNT;
-      nxt[q] = item < n_items ? cb_load(a, item / kCbB, wb + item % kCbB) : 0ull;
+      nxt[q] = item < n_items ? cb_load(a, ssrc, item / kCbB, wb + item % kCbB) : 0ull;
     }
   };
   auto put = [&](int buf) {
 #pragma unroll
     for (int q = 0; q < kCbLd; ++q) {
       const uint32_t item = tid + q * kCbNT;
-      if (item < n_items) sw[buf][item / kCbB][item % kCbB] = nxt[q];
+      if (item < n_items) sw[buf][kCbRow0 + item / kCbB][item % kCbB] = nxt[q];
     }
   };
   if (w0 < w1) {
@@ -1984,40 +2047,15 @@ __global__ __launch_bounds__(kCbNT) void k_combine_tile(CombineTileArgs a) {
   for (uint64_t wb = w0; wb < w1; wb += kCbB) {
     if (wb + kCbB < w1) fetch(wb + kCbB);
     if (live && wb <= rwhi && wb + kCbB > rwlo) {
-      const uint32_t po = a.n_src + 8 * r.order;
-      for (int b = 0; b < kCbB; ++b) {
-        const uint64_t w = wb + b;
-        if (w < rwlo || w > rwhi || w >= w1) continue;
-        uint64_t m = ~0ull;
-        if (w == rwlo) m &= ~0ull << (r.begin & 63);
-        if (w == rwhi && (r.end & 63)) m &= (1ull << (r.end & 63)) - 1;
-        if (r.filter) m &= sw[cur][a.n_src + 16 + r.group][b];
-        const uint64_t p0 = r.src[0] >= 0 ? sw[cur][r.src[0]][b] : 0ull;
-        const uint64_t p1 = r.src[1] >= 0 ? sw[cur][r.src[1]][b] : 0ull;
-        const uint64_t p2 = r.src[2] >= 0 ? sw[cur][r.src[2]][b] : 0ull;
-        const uint64_t u0 = p0 & m, u1 = (p0 | p1) & m, u2 = (p0 | p1 | p2) & m;
-        const uint32_t c0 = __popcll(u0), c1 = __popcll(u1), c2 = __popcll(u2);
-        acc[0] += c0;
-        acc[1] += c1;
-        acc[2] += c2;
-        if (a.uniform_w) {
-          acc[3] += (unsigned long long)c0 * a.uniform_w;
-          acc[4] += (unsigned long long)c1 * a.uniform_w;
-          acc[5] += (unsigned long long)c2 * a.uniform_w;
-        } else {
-          uint32_t s0 = 0, s1 = 0, s2 = 0;
+      uint32_t c[3] = {0, 0, 0}, cw[3] = {0, 0, 0};   // at most 64 x 255 x kCbB each
+      if (weighted)
+        cb_batch<true>(sw[cur], wb, w1, r, rm, s0, s1, s2, rp, a.plane_mask, c, cw);
+      else
+        cb_batch<false>(sw[cur], wb, w1, r, rm, s0, s1, s2, rp, 0u, c, cw);
 #pragma unroll
-          for (int pb = 0; pb < 8; ++pb) {
-            if (!((a.plane_mask >> pb) & 1u)) continue;
-            const uint64_t pl = sw[cur][po + pb][b];
-            s0 += (uint32_t)__popcll(u0 & pl) << pb;
-            s1 += (uint32_t)__popcll(u1 & pl) << pb;
-            s2 += (uint32_t)__popcll(u2 & pl) << pb;
-          }
-          acc[3] += s0;
-          acc[4] += s1;
-          acc[5] += s2;
-        }
+      for (int k = 0; k < 3; ++k) {
+        acc[k] += c[k];
+        acc[3 + k] += cw[k];
       }
     }
     if (wb + kCbB < w1) put(cur ^ 1);
@@ -2025,6 +2063,8 @@ __global__ __launch_bounds__(kCbNT) void k_combine_tile(CombineTileArgs a) {
     cur ^= 1;
   }
   if (live) {
+    if (!weighted)
+      for (int k = 0; k < 3; ++k) acc[3 + k] = acc[k] * a.uniform_w;
     unsigned long long* o = a.part + (uint64_t)ri * 6;
 #pragma unroll
     for (int f = 0; f < 6; ++f)
