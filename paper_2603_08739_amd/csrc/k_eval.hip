@@ -154,30 +154,48 @@ __device__ __forceinline__ bool feasible(double o0, double o1, double o2, const 
   return true;
 }
 
-// All-pairs dominance, candidate rows staged through LDS 256 at a time.
+// Flag of every point: 1 if it meets the bounds (and has no NaN), else 0;
+// the NaN flag of the call.
+__global__ __launch_bounds__(256) void k_pareto_init(const double* __restrict__ obj, uint32_t n,
+                                                     Bounds bd, uint8_t* __restrict__ flag,
+                                                     uint32_t* __restrict__ counters) {
+  const uint32_t b = blockIdx.x * 256 + threadIdx.x;
+  if (b >= n) return;
+  const double o0 = obj[3 * (uint64_t)b], o1 = obj[3 * (uint64_t)b + 1],
+               o2 = obj[3 * (uint64_t)b + 2];
+  flag[b] = feasible(o0, o1, o2, bd) ? 1 : 0;
+  if (o0 != o0 || o1 != o1 || o2 != o2) atomicOr(&counters[1], 1u);
+}
+
+// All-pairs dominance over a grid of (points, candidates) tiles: block
+// (x, y) tests points [256 x, 256 x + 256) against the feasible candidates
+// of its slice [y * per, (y + 1) * per), staged through LDS 256 at a time,
+// and clears the flag of every point a candidate of its segment dominates.
+// Every writer stores 0, so the blocks need no ordering; the result is the
+// same whichever candidates a block sees as still flagged, as dominance is
+// transitive (only the objectives and the bounds decide a candidate).
 __global__ __launch_bounds__(256) void k_pareto(const double* __restrict__ obj,
                                                 const uint32_t* __restrict__ seg, uint32_t n,
-                                                Bounds bd, uint8_t* __restrict__ flag,
-                                                uint32_t* __restrict__ counters) {
+                                                uint32_t per, Bounds bd, uint8_t* __restrict__ flag) {
   __shared__ double so[3][256];
   __shared__ uint32_t ss[256];
   __shared__ uint32_t sf[256];
   const uint32_t b = blockIdx.x * 256 + threadIdx.x;
   double ob0 = 0, ob1 = 0, ob2 = 0;
   uint32_t sb = 0;
-  bool fb = false, nan = false;
-  if (b < n) {
+  bool live = false;
+  if (b < n && flag[b]) {
     ob0 = obj[3 * (uint64_t)b];
     ob1 = obj[3 * (uint64_t)b + 1];
     ob2 = obj[3 * (uint64_t)b + 2];
     sb = seg ? seg[b] : 0u;
-    nan = (ob0 != ob0) || (ob1 != ob1) || (ob2 != ob2);
-    fb = feasible(ob0, ob1, ob2, bd);
+    live = true;
   }
+  const uint32_t c0 = blockIdx.y * per, c1 = min(n, c0 + per);
   bool dom = false;
-  for (uint32_t a0 = 0; a0 < n; a0 += 256) {
+  for (uint32_t a0 = c0; a0 < c1; a0 += 256) {
     const uint32_t a = a0 + threadIdx.x;
-    if (a < n) {
+    if (a < c1) {
       const double x0 = obj[3 * (uint64_t)a], x1 = obj[3 * (uint64_t)a + 1],
                    x2 = obj[3 * (uint64_t)a + 2];
       so[0][threadIdx.x] = x0;
@@ -187,8 +205,8 @@ __global__ __launch_bounds__(256) void k_pareto(const double* __restrict__ obj,
       sf[threadIdx.x] = feasible(x0, x1, x2, bd) ? 1u : 0u;
     }
     __syncthreads();
-    const uint32_t m = min(256u, n - a0);
-    if (fb && !dom) {
+    const uint32_t m = min(256u, c1 - a0);
+    if (live && !dom) {
       for (uint32_t j = 0; j < m; ++j) {
         if (a0 + j == b || !sf[j] || ss[j] != sb) continue;
         const double x0 = so[0][j], x1 = so[1][j], x2 = so[2][j];
@@ -202,12 +220,15 @@ __global__ __launch_bounds__(256) void k_pareto(const double* __restrict__ obj,
     }
     __syncthreads();
   }
-  if (b < n) {
-    const bool on = fb && !dom;
-    flag[b] = on ? 1 : 0;
-    if (on) atomicAdd(&counters[0], 1u);
-    if (nan) atomicOr(&counters[1], 1u);
-  }
+  if (dom) flag[b] = 0;
+}
+
+// Points left on the front.
+__global__ __launch_bounds__(256) void k_pareto_count(const uint8_t* __restrict__ flag, uint32_t n,
+                                                      uint32_t* __restrict__ counters) {
+  const uint32_t b = blockIdx.x * 256 + threadIdx.x;
+  const uint64_t on = __ballot(b < n && flag[b]);
+  if ((threadIdx.x & 63) == 0 && on) atomicAdd(&counters[0], (uint32_t)__popcll(on));
 }
 
 }  // namespace
@@ -243,8 +264,17 @@ kv_status pareto(const double* obj, const uint32_t* segment, uint32_t n, const d
   const double nan = __builtin_nan("");
   Bounds bd{bounds ? bounds[0] : nan, bounds ? bounds[1] : nan, bounds ? bounds[2] : nan};
   StageTimer tm(kStPareto, s);
-  hipLaunchKernelGGL(k_pareto, dim3(div_up(n, 256)), dim3(256), 0, s, obj, segment, n, bd, flag,
-                     counters_dev);
+  if (n == 0) return KV_OK;
+  // point tiles x candidate slices: about 2,048 blocks, slices of whole tiles
+  const uint32_t nt = div_up(n, 256);
+  const uint32_t ny = std::max<uint32_t>(1, std::min<uint32_t>(nt, div_up(2048, nt)));
+  const uint32_t per = div_up(nt, ny) * 256;
+  hipLaunchKernelGGL(k_pareto_init, dim3(nt), dim3(256), 0, s, obj, n, bd, flag, counters_dev);
+  KV_HIP(hipGetLastError());
+  hipLaunchKernelGGL(k_pareto, dim3(nt, div_up(n, per)), dim3(256), 0, s, obj, segment, n, per,
+                     bd, flag);
+  KV_HIP(hipGetLastError());
+  hipLaunchKernelGGL(k_pareto_count, dim3(nt), dim3(256), 0, s, flag, n, counters_dev);
   KV_HIP(hipGetLastError());
   return KV_OK;
 }

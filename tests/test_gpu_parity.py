@@ -160,6 +160,25 @@ def test_pareto_parity(lib, oracle_mod):
         assert cnt == int(ref.sum())
 
 
+def test_pareto_parity_many_slices(lib, oracle_mod):
+    """Point sets that span many 256-point tiles and candidate slices (with a
+    ragged last tile): anti-correlated objectives give large fronts, integer
+    values give ties and duplicates."""
+    host, _ = lib
+    rng = np.random.default_rng(9)
+    for n in (256, 257, 4099, 13001):
+        x = rng.uniform(0, 1, n)
+        obj = np.stack([x, x + rng.normal(0, 0.05, n), 1.0 - x + rng.normal(0, 0.05, n)], 1)
+        obj[: n // 4] = np.round(obj[: n // 4] * 8)
+        for seg, bounds in ((None, None), (rng.integers(0, 3, n).astype(np.uint32), None),
+                            (rng.integers(0, 5, n).astype(np.uint32), [0.9, 0.1, float("nan")])):
+            say(f"  pareto n={n} seg={seg is not None} bounds={bounds is not None}")
+            f, cnt = host.pareto(obj, seg, bounds)
+            ref = oracle_mod.pareto(obj, seg, bounds)
+            np.testing.assert_array_equal(f, ref)
+            assert cnt == int(ref.sum()) and cnt > 0
+
+
 def test_pareto_on_objectives(lib, oracle_mod):
     host, _ = lib
     t = tg.tiny()
