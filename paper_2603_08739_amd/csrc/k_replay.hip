@@ -970,13 +970,25 @@ __device__ __forceinline__ void block_suffix_min_flag(uint32_t v, bool flag, uin
 // eviction, which moves head1 past them).
 // G1: every access of the job belongs to group g0 (counters add up per
 // wavefront); otherwise each access's group is read.
+// The next full chunk's weights and next-access links and the block links
+// of the chunk after it, loaded at the end of a full chunk (after its last
+// awaited load, so that no wait of its own covers them) and kept in
+// registers until the next chunk reads them.
+template <int IT>
+struct LfuAhead {
+  uint32_t w[IT / 4];   // four weights per word
+  uint4 nx[IT / 4];
+  uint4 key[IT / 4];
+};
+
 template <int NT, bool G1>
 __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
                                          uint32_t* __restrict__ cnt, const Classes& cl,
                                          GroupCounters& gc, LfuLds& S,
                                          uint64_t* __restrict__ bits, uint32_t c0, uint32_t c1,
                                          uint32_t g0, BlockAny& block_any, bool have_pref,
-                                         uint64_t& used_io, uint32_t& head1_io) {
+                                         uint64_t& used_io, uint32_t& head1_io,
+                                         LfuAhead<kLChunk / NT>& ahead) {
   constexpr bool g1 = G1;
   constexpr int IT = kLChunk / NT;               // accesses per thread
   // queue entries per thread: the queue rarely holds more than about a
@@ -1000,11 +1012,20 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   bool cm[IT], res0[IT];
   if (have_pref) {
     lds_get<IT>(S.pkey + l0, kk);
+#pragma unroll
+    for (int q = 0; q < IT / 4; ++q) {
+      const uint32_t xn[4] = {ahead.nx[q].x, ahead.nx[q].y, ahead.nx[q].z, ahead.nx[q].w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        ww[4 * q + e] = v[4 * q + e] ? (ahead.w[q] >> (8 * e)) & 0xFFu : 0u;
+        nx[4 * q + e] = v[4 * q + e] ? xn[e] : 0u;
+      }
+    }
   } else {
     loadn_u32<IT>(a.key[o], p0, a.n, v, kk);
+    loadn_u8<IT>(a.w8[o], p0, a.n, v, ww);
+    loadn_u32<IT>(a.nxt[o], p0, a.n, v, nx);
   }
-  loadn_u8<IT>(a.w8[o], p0, a.n, v, ww);
-  loadn_u32<IT>(a.nxt[o], p0, a.n, v, nx);
   {
     // the next full chunk's block links.  The read position is clamped to
     // the arrays' readable slack; whatever lies outside the job (or past n,
@@ -1014,7 +1035,8 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     uint32_t nk[IT];
 #pragma unroll
     for (int q = 0; q < IT / 4; ++q) {
-      const uint4 x = *reinterpret_cast<const uint4*>(a.key[o] + pn + 4 * q);
+      const uint4 x = have_pref ? ahead.key[q]
+                                : *reinterpret_cast<const uint4*>(a.key[o] + pn + 4 * q);
       const uint32_t xv[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
@@ -1562,6 +1584,19 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     const uint32_t k = nk[e];
     if (!(k != 0 && k - 1 >= c0 && k - 1 < c0 + kLChunk)) S.pcnt[l0 + e] = nold[e];
   }
+  if (L == kLChunk) {
+    // read positions clamped as for the links above: a clamped group lies
+    // wholly past n, where the next chunks mask every item
+    const uint32_t nmax = (uint32_t)a.n & ~3u;
+    const uint32_t pn1 = min<uint32_t>(c0 + kLChunk + l0, nmax);
+    const uint32_t pn2 = min<uint32_t>(c0 + 2 * kLChunk + l0, nmax);
+#pragma unroll
+    for (int q = 0; q < IT / 4; ++q) {
+      ahead.w[q] = *reinterpret_cast<const uint32_t*>(a.w8[o] + pn1 + 4 * q);
+      ahead.nx[q] = *reinterpret_cast<const uint4*>(a.nxt[o] + pn1 + 4 * q);
+      ahead.key[q] = *reinterpret_cast<const uint4*>(a.key[o] + pn2 + 4 * q);
+    }
+  }
   // the nonempty-class bitmap is rebuilt only when class 1 is empty (the
   // serial walk rebuilds it before it starts)
   RCLK(t_f1);
@@ -1632,10 +1667,11 @@ __device__ __forceinline__ void lfu_chunked(const JobDev& j, const JobArgs& a,
   uint64_t ppos = ~0ull;  // the chunk whose links and counts are prefetched in LDS
   uint64_t used = 0;                    // cached weight
   uint32_t head1 = (uint32_t)j.begin;   // no live count-1 member before head1
+  LfuAhead<kLChunk / NT> ahead;
   while (pos < j.end) {
     const uint32_t l = (uint32_t)min<uint64_t>(len, j.end - pos);
     if (lfu_fast<NT, G1>(j, a, cnt, cl, gc, S, bits, (uint32_t)pos, (uint32_t)(pos + l), g0,
-                         block_any, ppos == pos, used, head1)) {
+                         block_any, ppos == pos, used, head1, ahead)) {
       ppos = (l == kLChunk) ? pos + l : ~0ull;
       pos += l;
       len = min<uint32_t>(len * 2, j.chunk);
