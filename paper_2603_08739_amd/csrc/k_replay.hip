@@ -1050,6 +1050,28 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   for (int e = 0; e < IT; ++e) gg[e] = g0;
   if constexpr (!G1) loadn_u8<IT>(a.g8[o], p0, a.n, v, gg);
   uint32_t h = head1_io;
+  // the candidate scan's first step, loaded ahead (whether it runs is known
+  // only after the first block scan).  The links and weights never change;
+  // a hit word is taken from here only for positions at least a full chunk
+  // back, whose words were stored before a barrier every wave has passed
+  // (the previous chunk stores its own after its last one).
+  uint64_t sc_word[kCScan];
+  uint32_t sc_nx[kCScan], sc_w[kCScan];
+  {
+    const uint32_t hend = min(min<uint32_t>(h + NT * kCScan, h + kCand), c0);
+#pragma unroll
+    for (int e = 0; e < kCScan; ++e) {
+      const uint32_t q = h + tid * kCScan + e;
+      sc_word[e] = 0;
+      sc_nx[e] = kNone;
+      sc_w[e] = 0;
+      if (q < hend) {
+        if (q + kLChunk < c0) sc_word[e] = bits[(q >> 6) - jw0];
+        sc_nx[e] = a.nxt[o][q];
+        sc_w[e] = a.w8[o][q];
+      }
+    }
+  }
   // stored counts at the latest earlier accesses (prefetched by the
   // previous chunk when it covered the whole chunk before this one); only a
   // block's first access in the chunk needs one
@@ -1126,7 +1148,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     // victims), the chunk start is reached, or the buffer is full
     uint32_t n0 = 0;
     uint64_t vw = 0;
-    for (;;) {
+    for (bool first = true;; first = false) {
       if (vw >= ev0 || h >= c0 || n0 >= kCand) break;
       RSTAT(blockIdx.x, kStScanned, 1);
       // each position lists at most one entry: near the end of the buffer
@@ -1142,9 +1164,9 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
         aq[e] = kInf16;
         wq[e] = 0;
         if (q < hend) {
-          const uint64_t word = bits[(q >> 6) - jw0];
-          const uint32_t nxq = a.nxt[o][q];
-          wq[e] = a.w8[o][q];
+          const uint64_t word = (first && q + kLChunk < c0) ? sc_word[e] : bits[(q >> 6) - jw0];
+          const uint32_t nxq = first ? sc_nx[e] : a.nxt[o][q];
+          wq[e] = first ? sc_w[e] : a.w8[o][q];
           live[e] = !((word >> (q & 63)) & 1ull) && (nxq == kNone || nxq >= c0);
           touched[e] = live[e] && nxq != kNone && nxq < c1;
           aq[e] = touched[e] ? nxq - c0 : kInf16;
