@@ -78,7 +78,8 @@ def stage_units(stage, n, jobs_accesses):
 
 def replay_job_accesses(cfgs, stats, n):
     """Accesses walked by replay jobs per step (closed-form jobs excluded),
-    per policy: {"fifo": ..., "lfu": ...}."""
+    per policy: {"fifo": ..., "lfu": ...}, and the number of such jobs (one
+    workgroup each) per policy."""
     import tracegen as tg
     G = stats.n_groups
     jobs = set()
@@ -93,10 +94,12 @@ def replay_job_accesses(cfgs, stats, n):
                 dw = stats.u_w_g[g] if part else stats.distinct_w
                 if x and x < dw:
                     jobs.add((part, g if part else -1, pol, x))
-    total = {"fifo": 0, "lfu": 0}
+    total, count = {"fifo": 0, "lfu": 0}, {"fifo": 0, "lfu": 0}
     for (part, g, pol, _) in jobs:
-        total["lfu" if pol == tg.POLICY_LFU else "fifo"] += stats.n_g[g] if part else n
-    return total
+        key = "lfu" if pol == tg.POLICY_LFU else "fifo"
+        total[key] += stats.n_g[g] if part else n
+        count[key] += 1
+    return total, count
 
 
 def dominant_kernel(timing, steps):
@@ -361,7 +364,7 @@ def main():
     value = n * n_cfg / (ms_per_step / 1000.0)
 
     # replay work: distinct (order, group, policy, capacity) jobs that are replayed
-    jobs_accesses = replay_job_accesses(cfgs, stats, n)
+    jobs_accesses, jobs_count = replay_job_accesses(cfgs, stats, n)
     kern, avg_ms, calls = dominant_kernel(timing, args.steps)
     units = stage_units(kern, n, jobs_accesses)
     algo = ALGO_BYTES.get(kern, 5.0) * units
@@ -369,6 +372,8 @@ def main():
     roof = {"bound": "hbm", "kernel": kern, "achieved": achieved, "peak": HBM_PEAK_GBS,
             "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic_for(kern),
             "avg_launch_ms": avg_ms, "launches": calls,
+            # a replay launch runs one workgroup (on one compute unit) per job
+            "workgroups": jobs_count.get(kern[7:]) if kern.startswith("replay_") else None,
             "stage_ms_per_step": {k: round(v[1] / args.steps, 3) for k, v in timing.items()
                                   if v[0]}}
     ttl = search = prefix = gttl = None
