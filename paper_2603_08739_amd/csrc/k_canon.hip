@@ -121,7 +121,9 @@ __global__ __launch_bounds__(kRsNT) void k_rs_count(const uint64_t* __restrict__
   counts[(uint64_t)threadIdx.x * ntiles + blockIdx.x] = h[threadIdx.x];
 }
 
-// Stable scatter of one tile given the exclusive digit offsets.
+// Stable scatter of one tile given the exclusive digit offsets.  The tile
+// is first put in digit order in LDS, then written out position by position,
+// so that neighbouring threads write neighbouring words of one digit's run.
 __global__ __launch_bounds__(kRsNT) void k_rs_scatter(const uint64_t* __restrict__ kin,
                                                       const uint32_t* __restrict__ vin,
                                                       uint64_t* __restrict__ kout,
@@ -130,13 +132,17 @@ __global__ __launch_bounds__(kRsNT) void k_rs_scatter(const uint64_t* __restrict
                                                       const uint32_t* __restrict__ offsets,
                                                       uint32_t ntiles) {
   __shared__ uint32_t wcnt[kRsWaves][256];
-  __shared__ uint32_t gbase[256];
+  __shared__ uint32_t gbase[256];   // the digit's first output position, less its tile start
+  __shared__ uint32_t red[kRsWaves];
+  __shared__ uint64_t sk[kRsTile];
+  __shared__ uint32_t sv[kRsTile];
   const int w = threadIdx.x / 64;
   const uint32_t lane = lane_id();
   for (int d = threadIdx.x; d < kRsWaves * 256; d += kRsNT) (&wcnt[0][0])[d] = 0;
-  gbase[threadIdx.x] = offsets[(uint64_t)threadIdx.x * ntiles + blockIdx.x];
+  const uint32_t g0 = offsets[(uint64_t)threadIdx.x * ntiles + blockIdx.x];
   __syncthreads();
-  const uint64_t base = (uint64_t)blockIdx.x * kRsTile + (uint64_t)w * (kRsItems * 64);
+  const uint64_t t0 = (uint64_t)blockIdx.x * kRsTile;
+  const uint64_t base = t0 + (uint64_t)w * (kRsItems * 64);
   uint64_t k[kRsItems];
   uint32_t v[kRsItems], d[kRsItems], rk[kRsItems];
   const uint64_t lt = lanemask_lt();
@@ -163,24 +169,40 @@ __global__ __launch_bounds__(kRsNT) void k_rs_scatter(const uint64_t* __restrict
   }
   __syncthreads();
   {
-    // turn per-wave digit counts into per-wave offsets inside the tile
+    // per digit (one per thread): the tile's count, its start in the tile's
+    // digit order (a block scan), and each wave's start inside it
     const int dg = threadIdx.x;
-    uint32_t run = gbase[dg];
+    uint32_t tot = 0;
+#pragma unroll
+    for (int ww = 0; ww < kRsWaves; ++ww) tot += wcnt[ww][dg];
+    uint32_t all;
+    const uint32_t ls = block_excl_scan_u32<kRsNT, false>(tot, red, all);
+    uint32_t run = ls;
+#pragma unroll
     for (int ww = 0; ww < kRsWaves; ++ww) {
-      uint32_t c = wcnt[ww][dg];
+      const uint32_t c = wcnt[ww][dg];
       wcnt[ww][dg] = run;
       run += c;
     }
+    gbase[dg] = g0 - ls;
   }
   __syncthreads();
 #pragma unroll
   for (int r = 0; r < kRsItems; ++r) {
     const uint64_t i = base + (uint64_t)r * 64 + lane;
     if (i < n) {
-      const uint32_t dst = wcnt[w][d[r]] + rk[r];
-      kout[dst] = k[r];
-      vout[dst] = v[r];
+      const uint32_t lp = wcnt[w][d[r]] + rk[r];
+      sk[lp] = k[r];
+      sv[lp] = v[r];
     }
+  }
+  __syncthreads();
+  const uint32_t m = (uint32_t)min<uint64_t>(kRsTile, n - t0);
+  for (uint32_t p = threadIdx.x; p < m; p += kRsNT) {
+    const uint64_t key = sk[p];
+    const uint32_t dst = gbase[(uint32_t)(key >> shift) & 255u] + p;
+    kout[dst] = key;
+    vout[dst] = sv[p];
   }
 }
 
