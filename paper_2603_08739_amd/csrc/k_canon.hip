@@ -206,35 +206,77 @@ __global__ __launch_bounds__(kRsNT) void k_rs_scatter(const uint64_t* __restrict
   }
 }
 
+// Run starts in hash order: the first element of every group of equal
+// hashes (its first occurrence: ties in the sort go by position).
+__global__ __launch_bounds__(256) void k_run_flags(const uint64_t* __restrict__ K, uint64_t n,
+                                                   uint32_t* __restrict__ newflag) {
+  for (uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; k < n;
+       k += (uint64_t)gridDim.x * blockDim.x)
+    newflag[k] = (k == 0 || K[k - 1] != K[k]) ? 1u : 0u;
+}
+
 // Neighbours in hash order are the previous / next occurrences.  Both links
-// of a position go out in one 8-byte scatter (link | next << 32), split
-// into the two arrays by a pass in position order.
+// of a position and its block id go out in one 16-byte scatter (link, next,
+// id), split into the three arrays by a pass in position order.  Dense block
+// ids follow the order of first occurrence (the rank of the block's first
+// position among all first positions), so that blocks met close together in
+// the trace sit close together in the per-block state arrays.  At a run
+// start the block's weight and group go into the per-block tables.
 __global__ __launch_bounds__(256) void k_links(const uint64_t* __restrict__ K,
                                                const uint32_t* __restrict__ V, uint64_t n,
-                                               uint64_t* __restrict__ kn,
-                                               uint32_t* __restrict__ newflag) {
+                                               const uint32_t* __restrict__ incl,
+                                               const uint32_t* __restrict__ newflag,
+                                               const uint32_t* __restrict__ firstpos,
+                                               const uint32_t* __restrict__ fincl,
+                                               uint4* __restrict__ kn,
+                                               uint8_t* __restrict__ blk_w,
+                                               uint8_t* __restrict__ blk_g,
+                                               uint32_t* __restrict__ runstart,
+                                               const uint8_t* __restrict__ w8,
+                                               const uint8_t* __restrict__ g8, DevStats* st) {
+  __shared__ unsigned long long su[KV_MAX_GROUPS], suw[KV_MAX_GROUPS];
+  if (threadIdx.x < KV_MAX_GROUPS) {
+    su[threadIdx.x] = 0;
+    suw[threadIdx.x] = 0;
+  }
+  __syncthreads();
   for (uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; k < n;
        k += (uint64_t)gridDim.x * blockDim.x) {
     const uint64_t h = K[k];
     const uint32_t pos = V[k];
-    const bool sp = k > 0 && K[k - 1] == h;
+    const bool sp = newflag[k] == 0u;
     const bool sn = k + 1 < n && K[k + 1] == h;
-    const uint32_t pv = sp ? V[k - 1] : 0u;
-    const uint32_t key = sp ? pv + 1u : 0u;
+    const uint32_t key = sp ? V[k - 1] + 1u : 0u;
     const uint32_t nx = sn ? V[k + 1] : kNone;
-    kn[pos] = (uint64_t)key | ((uint64_t)nx << 32);
-    newflag[k] = sp ? 0u : 1u;
+    const uint32_t run = incl[k] - 1u;
+    const uint32_t id = fincl[firstpos[run]] - 1u;
+    kn[pos] = make_uint4(key, nx, id, 0u);
+    if (!sp) {
+      const uint8_t w = w8[pos], g = g8[pos];
+      blk_w[id] = w;
+      blk_g[id] = g;
+      runstart[run] = (uint32_t)k;
+      atomicAdd(&su[g], 1ull);
+      atomicAdd(&suw[g], (unsigned long long)w);
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x < KV_MAX_GROUPS) {
+    if (su[threadIdx.x]) atomicAdd(&st->u_g[threadIdx.x], su[threadIdx.x]);
+    if (suw[threadIdx.x]) atomicAdd(&st->u_w_g[threadIdx.x], suw[threadIdx.x]);
   }
 }
 
-__global__ __launch_bounds__(256) void k_split_links(const uint64_t* __restrict__ kn,
-                                                     uint64_t n, uint32_t* __restrict__ key,
-                                                     uint32_t* __restrict__ nxt) {
+__global__ __launch_bounds__(256) void k_split_links(const uint4* __restrict__ kn, uint64_t n,
+                                                     uint32_t* __restrict__ key,
+                                                     uint32_t* __restrict__ nxt,
+                                                     uint32_t* __restrict__ bid) {
   for (uint64_t p = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n;
        p += (uint64_t)gridDim.x * blockDim.x) {
-    const uint64_t x = kn[p];
-    key[p] = (uint32_t)x;
-    nxt[p] = (uint32_t)(x >> 32);
+    const uint4 x = kn[p];
+    key[p] = x.x;
+    nxt[p] = x.y;
+    bid[p] = x.z;
   }
 }
 
@@ -255,65 +297,20 @@ __global__ __launch_bounds__(256) void k_check_blocks(const uint32_t* __restrict
   if (__ballot(bad) != 0ull && lane_id() == 0) atomicOr(&st->err, (uint32_t)kErrInconsistent);
 }
 
-// First occurrences in trace order: flag[pos] = 1 where the block appears
-// for the first time.
-__global__ __launch_bounds__(256) void k_first_flags(const uint32_t* __restrict__ key,
-                                                     uint64_t n, uint32_t* __restrict__ flag) {
-  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-       i += (uint64_t)gridDim.x * blockDim.x)
-    flag[i] = key[i] == 0u ? 1u : 0u;
-}
-
-// Position of each hash group's first element (its first occurrence: ties
-// in the sort go by position).
+// Position of each hash group's first element (its first occurrence), and
+// a flag at that position in trace order.
 __global__ __launch_bounds__(256) void k_first_pos(const uint32_t* __restrict__ V,
                                                    const uint32_t* __restrict__ incl,
                                                    const uint32_t* __restrict__ newflag,
-                                                   uint64_t n, uint32_t* __restrict__ firstpos) {
+                                                   uint64_t n, uint32_t* __restrict__ firstpos,
+                                                   uint32_t* __restrict__ firstflag) {
   for (uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; k < n;
        k += (uint64_t)gridDim.x * blockDim.x)
-    if (newflag[k]) firstpos[incl[k] - 1u] = V[k];
-}
-
-// Dense block ids in order of first occurrence, so that blocks met close
-// together in the trace sit close together in the per-block state arrays.
-__global__ __launch_bounds__(256) void k_ids(const uint32_t* __restrict__ V,
-                                             const uint32_t* __restrict__ incl,
-                                             const uint32_t* __restrict__ newflag,
-                                             const uint32_t* __restrict__ firstpos,
-                                             const uint32_t* __restrict__ fincl, uint64_t n,
-                                             uint32_t* __restrict__ bid,
-                                             uint8_t* __restrict__ blk_w,
-                                             uint8_t* __restrict__ blk_g,
-                                             uint32_t* __restrict__ runstart,
-                                             const uint8_t* __restrict__ w8,
-                                             const uint8_t* __restrict__ g8, DevStats* st) {
-  __shared__ unsigned long long su[KV_MAX_GROUPS], suw[KV_MAX_GROUPS];
-  if (threadIdx.x < KV_MAX_GROUPS) {
-    su[threadIdx.x] = 0;
-    suw[threadIdx.x] = 0;
-  }
-  __syncthreads();
-  for (uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; k < n;
-       k += (uint64_t)gridDim.x * blockDim.x) {
-    const uint32_t pos = V[k];
-    const uint32_t grp = incl[k] - 1u;
-    const uint32_t id = fincl[firstpos[grp]] - 1u;
-    bid[pos] = id;
     if (newflag[k]) {
-      const uint8_t w = w8[pos], g = g8[pos];
-      blk_w[id] = w;
-      blk_g[id] = g;
-      runstart[grp] = (uint32_t)k;
-      atomicAdd(&su[g], 1ull);
-      atomicAdd(&suw[g], (unsigned long long)w);
+      const uint32_t pos = V[k];
+      firstpos[incl[k] - 1u] = pos;
+      firstflag[pos] = 1u;
     }
-  }
-  __syncthreads();
-  if (threadIdx.x < KV_MAX_GROUPS) {
-    if (su[threadIdx.x]) atomicAdd(&st->u_g[threadIdx.x], su[threadIdx.x]);
-    if (suw[threadIdx.x]) atomicAdd(&st->u_w_g[threadIdx.x], suw[threadIdx.x]);
-  }
 }
 
 __global__ __launch_bounds__(256) void k_mult(const uint32_t* __restrict__ incl,
@@ -406,12 +403,15 @@ kv_status canon_build(Trace& t, const kv_trace_desc& d, hipStream_t s) {
   const uint32_t ntiles = div_up(n, kRsTile);
   const uint64_t ncount = (uint64_t)ntiles * 256;
   const uint64_t scratch_elems = std::max(scan_scratch_elems(ncount), scan_scratch_elems(n));
-  DevBuf ka, kb, va, vb, kn, counts, scratch, dst;
+  DevBuf ka, kb, va, vb, kn, fl, counts, scratch, dst;
   if ((st = ka.reserve(n * 8)) != KV_OK) return st;
   if ((st = kb.reserve(n * 8)) != KV_OK) return st;
   if ((st = va.reserve(n * 4)) != KV_OK) return st;
   if ((st = vb.reserve(n * 4)) != KV_OK) return st;
-  if ((st = kn.reserve(n * 8)) != KV_OK) return st;
+  if ((st = kn.reserve(n * 16)) != KV_OK) return st;
+  // trace-order first-occurrence flags, their inclusive sums, the groups'
+  // first positions (u <= n)
+  if ((st = fl.reserve(n * 12)) != KV_OK) return st;
   if ((st = counts.reserve(std::max<uint64_t>(ncount, 1) * 4)) != KV_OK) return st;
   if ((st = scratch.reserve(std::max<uint64_t>(scratch_elems, 1) * 4)) != KV_OK) return st;
   if ((st = dst.reserve(sizeof(DevStats))) != KV_OK) return st;
@@ -453,39 +453,37 @@ kv_status canon_build(Trace& t, const kv_trace_desc& d, hipStream_t s) {
   // kin / vin now hold the sorted pairs; the other pair of buffers is free.
   uint32_t* newflag = reinterpret_cast<uint32_t*>(kout);          // n u32
   uint32_t* incl = reinterpret_cast<uint32_t*>(kout) + n;         // n u32
+  uint32_t* firstflag = fl.as<uint32_t>();
+  uint32_t* fincl = firstflag + n;
+  uint32_t* firstpos = fincl + n;
+  uint32_t* runstart = vout;  // n >= u entries available
   uint32_t u32 = 0;
   {
   StageTimer tm(kStLoadLinks, s);
-  hipLaunchKernelGGL(k_links, dim3(grid_of(n)), dim3(256), 0, s, kin, vin, n,
-                     kn.as<uint64_t>(), newflag);
-  KV_HIP(hipGetLastError());
-  hipLaunchKernelGGL(k_split_links, dim3(grid_of(n)), dim3(256), 0, s, kn.as<uint64_t>(), n,
-                     o.key.as<uint32_t>(), o.nxt.as<uint32_t>());
+  hipLaunchKernelGGL(k_run_flags, dim3(grid_of(n)), dim3(256), 0, s, kin, n, newflag);
   KV_HIP(hipGetLastError());
   if ((st = scan_u32(newflag, incl, n, true, scratch.as<uint32_t>(), s)) != KV_OK) return st;
+  if ((st = fill_u32(firstflag, 0u, n, s)) != KV_OK) return st;
+  hipLaunchKernelGGL(k_first_pos, dim3(grid_of(n)), dim3(256), 0, s, vin, incl, newflag, n,
+                     firstpos, firstflag);
+  KV_HIP(hipGetLastError());
+  if ((st = scan_u32(firstflag, fincl, n, true, scratch.as<uint32_t>(), s)) != KV_OK) return st;
   }
   KV_HIP(hipMemcpyAsync(&u32, incl + (n - 1), 4, hipMemcpyDeviceToHost, s));
   KV_HIP(hipStreamSynchronize(s));
   const uint64_t u = u32;
   if ((st = t.blk_w.reserve(u)) != KV_OK) return st;
   if ((st = t.blk_g.reserve(u)) != KV_OK) return st;
-  uint32_t* runstart = vout;  // n >= u entries available
-  // the sorted keys are no longer needed: their buffer holds the first-
-  // occurrence flags / ranks (n) and the groups' first positions (u <= n)
-  uint32_t* fincl = reinterpret_cast<uint32_t*>(kin);
-  uint32_t* firstpos = fincl + n;
   {
   StageTimer tm(kStLoadLinks, s);
-  hipLaunchKernelGGL(k_first_flags, dim3(grid_of(n)), dim3(256), 0, s, o.key.as<uint32_t>(), n,
-                     firstpos);
+  hipLaunchKernelGGL(k_links, dim3(grid_of(n)), dim3(256), 0, s, kin, vin, n, incl, newflag,
+                     firstpos, fincl, reinterpret_cast<uint4*>(kn.p), t.blk_w.as<uint8_t>(),
+                     t.blk_g.as<uint8_t>(), runstart, o.w.as<uint8_t>(), o.g.as<uint8_t>(),
+                     dstats);
   KV_HIP(hipGetLastError());
-  if ((st = scan_u32(firstpos, fincl, n, true, scratch.as<uint32_t>(), s)) != KV_OK) return st;
-  hipLaunchKernelGGL(k_first_pos, dim3(grid_of(n)), dim3(256), 0, s, vin, incl, newflag, n,
-                     firstpos);
-  KV_HIP(hipGetLastError());
-  hipLaunchKernelGGL(k_ids, dim3(grid_of(n)), dim3(256), 0, s, vin, incl, newflag, firstpos,
-                     fincl, n, o.bid.as<uint32_t>(), t.blk_w.as<uint8_t>(), t.blk_g.as<uint8_t>(),
-                     runstart, o.w.as<uint8_t>(), o.g.as<uint8_t>(), dstats);
+  hipLaunchKernelGGL(k_split_links, dim3(grid_of(n)), dim3(256), 0, s,
+                     reinterpret_cast<const uint4*>(kn.p), n, o.key.as<uint32_t>(),
+                     o.nxt.as<uint32_t>(), o.bid.as<uint32_t>());
   KV_HIP(hipGetLastError());
   hipLaunchKernelGGL(k_mult, dim3(grid_of(n)), dim3(256), 0, s, incl, newflag, n, runstart,
                      dstats);
