@@ -140,9 +140,10 @@ def cpu_baseline(rec, cfgs, budget_s):
     t0 = time.time()
     O.replay(t, sample, threads)
     dt = time.time() - t0
-    # grow the prefix until the run takes a good part of the budget
-    while dt < budget_s / 4 and n_req < rec.len0.shape[0]:
-        n_req = min(rec.len0.shape[0], int(n_req * min(8.0, max(2.0, budget_s / 2 / max(dt, 1e-3)))))
+    # grow the prefix (aiming at the budget) until one run takes at least
+    # half of it
+    while dt < budget_s / 2 and n_req < rec.len0.shape[0]:
+        n_req = min(rec.len0.shape[0], int(n_req * min(8.0, max(1.5, budget_s / max(dt, 1e-3)))))
         t = rec.to_trace(max_requests=n_req)
         t0 = time.time()
         O.replay(t, sample, threads)
