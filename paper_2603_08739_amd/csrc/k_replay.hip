@@ -669,6 +669,11 @@ struct LfuLds {
   // at that link (each thread reads and writes only its own accesses)
   alignas(16) uint32_t pkey[kLChunk];
   alignas(16) uint32_t pcnt[kLChunk];
+  // apply: the pointer jumping's second copies of lp, occ and lmiss (rounds
+  // read one copy and write the other, so one barrier ends a round)
+  int16_t lp2[kLChunk];
+  uint16_t occ2[kLChunk];
+  int16_t lmiss2[kLChunk];
 };
 
 // A thread's IT consecutive words of an LDS array (16-byte aligned), moved
@@ -1439,6 +1444,9 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     S.occ[loc] = S.lp[loc] >= 0 ? 1 : 0;
   }
   __syncthreads();
+  // rounds read copy A and write copy B; the final values end up in B
+  int16_t *lpA = S.lp, *lpB = S.lp2, *lmA = S.lmiss, *lmB = S.lmiss2;
+  uint16_t *ocA = S.occ, *ocB = S.occ2;
   for (;;) {
     int16_t np[IT], nl[IT];
     uint16_t no[IT];
@@ -1446,29 +1454,37 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
 #pragma unroll
     for (int e = 0; e < IT; ++e) {
       const uint32_t loc = l0 + e;
-      const int16_t p = S.lp[loc];
-      no[e] = S.occ[loc];
+      const int16_t p = lpA[loc];
+      no[e] = ocA[loc];
       np[e] = p;
-      nl[e] = S.lmiss[loc];
+      nl[e] = lmA[loc];
       if (p >= 0) {
-        const int16_t pp = S.lp[p];
+        const int16_t pp = lpA[p];
         if (pp >= 0) {
-          no[e] = (uint16_t)(no[e] + S.occ[p]);
+          no[e] = (uint16_t)(no[e] + ocA[p]);
           np[e] = pp;
           moved = true;
         }
-        if (nl[e] < 0) nl[e] = S.lmiss[p];
+        if (nl[e] < 0) nl[e] = lmA[p];
       }
     }
-    __syncthreads();
 #pragma unroll
     for (int e = 0; e < IT; ++e) {
       const uint32_t loc = l0 + e;
-      S.lp[loc] = np[e];
-      S.occ[loc] = no[e];
-      S.lmiss[loc] = nl[e];
+      lpB[loc] = np[e];
+      ocB[loc] = no[e];
+      lmB[loc] = nl[e];
     }
     if (!block_any(moved)) break;
+    int16_t* t16 = lpA;
+    lpA = lpB;
+    lpB = t16;
+    t16 = lmA;
+    lmA = lmB;
+    lmB = t16;
+    uint16_t* tu = ocA;
+    ocA = ocB;
+    ocB = tu;
   }
   RCLK(t_e);
   RTIME(kStT3, t_d, t_e);
@@ -1505,16 +1521,16 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     const uint32_t loc = l0 + e;
     mc[e] = S.mcons[loc];
     nxl[e] = S.nxloc[loc];
-    lm[e] = (uint32_t)(int32_t)S.lmiss[loc];
-    oc[e] = S.occ[loc];
+    lm[e] = (uint32_t)(int32_t)lmB[loc];
+    oc[e] = ocB[loc];
   }
   uint32_t mocc[IT], mcm[IT], rf0[IT];
 #pragma unroll
   for (int e = 0; e < IT; ++e) {
     const uint32_t m = (int32_t)lm[e] >= 0 ? lm[e] : 0u;
-    mocc[e] = S.occ[m];
+    mocc[e] = ocB[m];
     mcm[e] = S.mcons[m];
-    const int16_t r = S.lp[l0 + e];  // the block's first access in the chunk
+    const int16_t r = lpB[l0 + e];  // the block's first access in the chunk
     rf0[e] = r >= 0 ? S.mneed[r] : f0[e];
   }
   bool hit[IT];
