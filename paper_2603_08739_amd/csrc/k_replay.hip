@@ -674,6 +674,7 @@ struct LfuLds {
   int16_t lp2[kLChunk];
   uint16_t occ2[kLChunk];
   int16_t lmiss2[kLChunk];
+  uint8_t cmf[kLChunk];       // a block's first touch in the chunk misses (no count at the start)
 };
 
 // A thread's IT consecutive words of an LDS array (16-byte aligned), moved
@@ -1105,6 +1106,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
                                                                         : kInf16;
     S.pw[loc] = (uint8_t)ww[e];
     S.capm[loc] = 0;
+    S.cmf[loc] = cm[e] ? 1 : 0;
     S.mskip[loc] = again ? 1 : 0;
     S.mcons[loc] = 0;
   }
@@ -1215,6 +1217,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   uint32_t nmiss = nm0;     // and their number
   bool converged = ev0 == 0;
   bool capnow[IT];  // capacity misses of the latest iteration
+  uint32_t ns_last = 0;  // the latest iteration's stamp in capm (0: none ran)
 #pragma unroll
   for (int e = 0; e < IT; ++e) capnow[e] = false;
   for (int it = 0; !converged && it < 24; ++it) {
@@ -1366,6 +1369,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     // the inputs of an iteration are the skip flags and the capacity
     // misses; the consumption flags are its outputs
     const uint8_t ns = (uint8_t)(it + 1);
+    ns_last = ns;
     bool changed = false;
 #pragma unroll
     for (int e = 0; e < CPT; ++e) {
@@ -1432,59 +1436,82 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   }
   // Pointer jumping gives each touch the number of earlier touches of its
   // block in the chunk and the latest miss among them.
-  // (The fixed point's fields are dead: its last reads came before the
-  // barrier that ended it.)
   bool miss[IT];
 #pragma unroll
   for (int e = 0; e < IT; ++e) {
-    const uint32_t loc = l0 + e;
     miss[e] = cm[e] || capnow[e];
-    S.lmiss[loc] = miss[e] ? (int16_t)loc : (int16_t)-1;
-    S.mneed[loc] = f0[e];  // a block's count at the chunk start, read via its first access
-    S.occ[loc] = S.lp[loc] >= 0 ? 1 : 0;
+    S.mneed[l0 + e] = f0[e];  // a block's count at the chunk start, read via its first access
   }
-  __syncthreads();
-  // rounds read copy A and write copy B; the final values end up in B
+  // Rounds read copy A of (lp, occ, lmiss) and write copy B; the final
+  // values end up in B.  Round 0 needs no copy A: a touch's initial occ is
+  // 1 if it has an earlier touch in the chunk, and its initial lmiss is
+  // itself if it misses (a first-touch miss, or a capacity miss of the
+  // fixed point's last iteration), from fields every thread sees already.
+  // (Copy A's occ and lmiss share storage with the fixed point's pw, capm,
+  // mskip and mpos: round 0 still reads capm, and copy A is first written
+  // in round 1, after the barrier that ends round 0.)
   int16_t *lpA = S.lp, *lpB = S.lp2, *lmA = S.lmiss, *lmB = S.lmiss2;
   uint16_t *ocA = S.occ, *ocB = S.occ2;
-  for (;;) {
-    int16_t np[IT], nl[IT];
-    uint16_t no[IT];
-    bool moved = false;
+  bool moved0 = false;
 #pragma unroll
-    for (int e = 0; e < IT; ++e) {
-      const uint32_t loc = l0 + e;
-      const int16_t p = lpA[loc];
-      no[e] = ocA[loc];
-      np[e] = p;
-      nl[e] = lmA[loc];
-      if (p >= 0) {
-        const int16_t pp = lpA[p];
-        if (pp >= 0) {
-          no[e] = (uint16_t)(no[e] + ocA[p]);
-          np[e] = pp;
-          moved = true;
-        }
-        if (nl[e] < 0) nl[e] = lmA[p];
+  for (int e = 0; e < IT; ++e) {
+    const uint32_t loc = l0 + e;
+    const int16_t p = S.lp[loc];
+    uint16_t no = p >= 0 ? 1 : 0;
+    int16_t np = p, nl = miss[e] ? (int16_t)loc : (int16_t)-1;
+    if (p >= 0) {
+      const int16_t pp = S.lp[p];
+      if (pp >= 0) {
+        no = (uint16_t)(no + 1);
+        np = pp;
+        moved0 = true;
       }
+      if (nl < 0 && (S.cmf[p] || (ns_last != 0 && S.capm[p] == ns_last))) nl = p;
     }
+    lpB[loc] = np;
+    ocB[loc] = no;
+    lmB[loc] = nl;
+  }
+  if (block_any(moved0)) {
+    for (;;) {
+      int16_t* t16 = lpA;
+      lpA = lpB;
+      lpB = t16;
+      t16 = lmA;
+      lmA = lmB;
+      lmB = t16;
+      uint16_t* tu = ocA;
+      ocA = ocB;
+      ocB = tu;
+      int16_t np[IT], nl[IT];
+      uint16_t no[IT];
+      bool moved = false;
 #pragma unroll
-    for (int e = 0; e < IT; ++e) {
-      const uint32_t loc = l0 + e;
-      lpB[loc] = np[e];
-      ocB[loc] = no[e];
-      lmB[loc] = nl[e];
+      for (int e = 0; e < IT; ++e) {
+        const uint32_t loc = l0 + e;
+        const int16_t p = lpA[loc];
+        no[e] = ocA[loc];
+        np[e] = p;
+        nl[e] = lmA[loc];
+        if (p >= 0) {
+          const int16_t pp = lpA[p];
+          if (pp >= 0) {
+            no[e] = (uint16_t)(no[e] + ocA[p]);
+            np[e] = pp;
+            moved = true;
+          }
+          if (nl[e] < 0) nl[e] = lmA[p];
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < IT; ++e) {
+        const uint32_t loc = l0 + e;
+        lpB[loc] = np[e];
+        ocB[loc] = no[e];
+        lmB[loc] = nl[e];
+      }
+      if (!block_any(moved)) break;
     }
-    if (!block_any(moved)) break;
-    int16_t* t16 = lpA;
-    lpA = lpB;
-    lpB = t16;
-    t16 = lmA;
-    lmA = lmB;
-    lmB = t16;
-    uint16_t* tu = ocA;
-    ocA = ocB;
-    ocB = tu;
   }
   RCLK(t_e);
   RTIME(kStT3, t_d, t_e);
