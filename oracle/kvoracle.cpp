@@ -14,6 +14,9 @@
 //
 //   oracle_replay      per configuration, per tenant group, per tier:
 //                      {hit, miss, ins, evict} and their granule-weighted twins.
+//   oracle_replay_memo the same, replaying each distinct inclusive tier cache
+//                      once (inclusive tiers are independent caches) and
+//                      classifying every configuration from presence bits.
 //   oracle_objectives  (cost, throughput, latency) from those counts.
 //   oracle_pareto      non-dominated flags under optional bounds.
 //
@@ -47,6 +50,7 @@
 //
 // Build: g++ -O2 -std=c++17 -ffp-contract=off -fPIC -shared -pthread
 #include <algorithm>
+#include <array>
 #include <atomic>
 #include <cmath>
 #include <cstdint>
@@ -68,9 +72,9 @@ enum Mode { M_INCLUSIVE = 0, M_EXCLUSIVE = 1, M_INCLUSIVE_PREFIX = 2 };
 
 struct Block {
   uint64_t hash;
-  uint32_t w;
-  uint32_t g;
   uint32_t req;
+  uint8_t w;  // granules, 1..255
+  uint8_t g;  // tenant group
 };
 
 // Counts of one configuration: [group][tier][field].
@@ -358,6 +362,130 @@ int replay_one(const std::vector<Block>& acc, const std::vector<std::vector<uint
   return 0;
 }
 
+// ---------------------------------------------------------------------------
+// Memo mode.  In the inclusive hierarchy every tier is an independent cache
+// that sees every access of its partition, so what one tier does depends only
+// on (partition, policy, capacity).  Memo mode replays each distinct such
+// cache once, literally, keeping one presence bit per access and its own
+// insert / eviction tallies, then classifies every configuration from its
+// tiers' bits: served by k = present in k and in no faster present tier.
+// Non-inclusive configurations take the literal path above.
+// ---------------------------------------------------------------------------
+struct MemoJob {
+  uint32_t part;    // index into the partition lists (group g, or n_groups = shared)
+  int policy;
+  uint64_t cap;
+  std::vector<uint64_t> bits;  // presence before the access, one bit per list entry
+  uint64_t ins[kMaxGroups] = {}, ins_w[kMaxGroups] = {}, ev[kMaxGroups] = {}, ev_w[kMaxGroups] = {};
+};
+
+void memo_run(const std::vector<Block>& acc, const std::vector<uint32_t>& idx, MemoJob& j) {
+  Tier* t = make_tier(j.policy, j.cap);
+  j.bits.assign((idx.size() + 63) / 64, 0);
+  for (int g = 0; g < kMaxGroups; ++g) j.ins[g] = j.ins_w[g] = j.ev[g] = j.ev_w[g] = 0;
+  for (size_t q = 0; q < idx.size(); ++q) {
+    const uint32_t i = idx[q];
+    const Block& b = acc[i];
+    if (t->contains(b.hash)) {
+      j.bits[q >> 6] |= 1ull << (q & 63);
+      t->hit(b.hash, i);
+    } else {
+      j.ins[b.g] += 1;
+      j.ins_w[b.g] += b.w;
+      t->insert(b, i, [&](const Block& v) {
+        j.ev[v.g] += 1;
+        j.ev_w[v.g] += v.w;
+      });
+    }
+  }
+  delete t;
+}
+
+// Per-list masks: one bit plane per group and per weight bit.
+struct ListMasks {
+  std::vector<std::vector<uint64_t>> group;   // [g] -> words
+  std::vector<std::vector<uint64_t>> wplane;  // [bit] -> words
+  std::vector<uint64_t> valid;
+};
+
+void build_masks(const std::vector<Block>& acc, const std::vector<uint32_t>& idx,
+                 uint32_t n_groups, ListMasks& m) {
+  const size_t W = (idx.size() + 63) / 64;
+  m.group.assign(n_groups, std::vector<uint64_t>(W, 0));
+  m.wplane.assign(8, std::vector<uint64_t>(W, 0));
+  m.valid.assign(W, 0);
+  for (size_t q = 0; q < idx.size(); ++q) {
+    const Block& b = acc[idx[q]];
+    const uint64_t bit = 1ull << (q & 63);
+    m.valid[q >> 6] |= bit;
+    m.group[b.g][q >> 6] |= bit;
+    for (int p = 0; p < 8; ++p)
+      if ((b.w >> p) & 1u) m.wplane[p][q >> 6] |= bit;
+  }
+}
+
+uint64_t popc(uint64_t x) { return (uint64_t)__builtin_popcountll(x); }
+
+// Adds the (hit, miss) counts and weights of one partition of one
+// configuration: tiers[k] = job or NULL (absent).
+void memo_classify(const ListMasks& m, uint32_t n_groups, const MemoJob* tiers[kTiers],
+                   Counts& out) {
+  const size_t W = m.valid.size();
+  bool wp[8];
+  for (int p = 0; p < 8; ++p) {
+    wp[p] = false;
+    for (size_t x = 0; x < W && !wp[p]; ++x) wp[p] = m.wplane[p][x] != 0;
+  }
+  for (size_t x = 0; x < W; ++x) {
+    uint64_t seen = 0;  // present in some faster (or this) present tier
+    for (int k = 0; k < kTiers; ++k) {
+      if (!tiers[k]) continue;
+      const uint64_t pk = tiers[k]->bits[x];
+      const uint64_t hit = pk & ~seen;
+      seen |= pk;
+      const uint64_t miss = m.valid[x] & ~seen;
+      for (uint32_t g = 0; g < n_groups; ++g) {
+        const uint64_t gm = m.group[g][x];
+        const uint64_t h = hit & gm, ms = miss & gm;
+        if (!(h | ms)) continue;
+        out.v[g][k][F_HIT] += popc(h);
+        out.v[g][k][F_MISS] += popc(ms);
+        for (int p = 0; p < 8; ++p) {
+          if (!wp[p]) continue;
+          out.v[g][k][F_HIT_W] += popc(h & m.wplane[p][x]) << p;
+          out.v[g][k][F_MISS_W] += popc(ms & m.wplane[p][x]) << p;
+        }
+      }
+    }
+  }
+  for (int k = 0; k < kTiers; ++k) {
+    if (!tiers[k]) continue;
+    for (uint32_t g = 0; g < n_groups; ++g) {
+      out.v[g][k][F_INS] += tiers[k]->ins[g];
+      out.v[g][k][F_INS_W] += tiers[k]->ins_w[g];
+      out.v[g][k][F_EVICT] += tiers[k]->ev[g];
+      out.v[g][k][F_EVICT_W] += tiers[k]->ev_w[g];
+    }
+  }
+}
+
+template <class F>
+void parallel_for(uint32_t n, uint32_t n_threads, F&& f) {
+  std::atomic<uint32_t> next{0};
+  auto work = [&]() {
+    for (;;) {
+      const uint32_t j = next.fetch_add(1);
+      if (j >= n) break;
+      f(j);
+    }
+  };
+  const uint32_t nt = std::max<uint32_t>(1, std::min<uint32_t>(n_threads, n));
+  std::vector<std::thread> th;
+  for (uint32_t t = 1; t < nt; ++t) th.emplace_back(work);
+  work();
+  for (auto& t : th) t.join();
+}
+
 }  // namespace
 
 extern "C" {
@@ -380,7 +508,7 @@ int oracle_replay(uint64_t n, const uint64_t* hash, const uint8_t* group, const 
     uint32_t g = group ? group[i] : 0;
     uint32_t w = weight ? weight[i] : 1;
     if (g >= n_groups || w == 0) return -2;
-    acc[i] = Block{hash[i], w, g, req ? req[i] : (uint32_t)i};
+    acc[i] = Block{hash[i], req ? req[i] : (uint32_t)i, (uint8_t)w, (uint8_t)g};
     by_group[g].push_back((uint32_t)i);
     all[i] = (uint32_t)i;
     w_max = std::max(w_max, w);
@@ -493,6 +621,121 @@ int64_t oracle_pareto(uint32_t n, const double* obj, const uint32_t* segment,
     }
   }
   return count;
+}
+
+}  // extern "C"
+
+extern "C" {
+
+// Memo-mode replay: the same results as oracle_replay (same arguments and
+// return codes), with every distinct inclusive tier cache (partition,
+// policy, capacity) replayed once and shared by the configurations that
+// use it.  Exclusive and prefix-reuse configurations replay literally.
+int oracle_replay_memo(uint64_t n, const uint64_t* hash, const uint8_t* group,
+                       const uint8_t* weight, const uint32_t* req, uint32_t n_groups,
+                       uint32_t n_cfg, const uint64_t* cap, const uint64_t* cap_group,
+                       const uint8_t* mode, const uint8_t* partitioned, const uint8_t* policy,
+                       uint32_t n_threads, uint64_t* counts) {
+  if (n_groups < 1 || n_groups > (uint32_t)kMaxGroups) return -2;
+  std::vector<Block> acc(n);
+  // partition lists: [g] = group g's accesses, [n_groups] = every access
+  // (with one group the two are the same list, kept once)
+  std::vector<std::vector<uint32_t>> lists(n_groups + 1);
+  const uint32_t all_list = n_groups == 1 ? 0u : n_groups;
+  uint32_t w_max = 1;
+  for (uint64_t i = 0; i < n; ++i) {
+    uint32_t g = group ? group[i] : 0;
+    uint32_t w = weight ? weight[i] : 1;
+    if (g >= n_groups || w == 0) return -2;
+    acc[i] = Block{hash[i], req ? req[i] : (uint32_t)i, (uint8_t)w, (uint8_t)g};
+    lists[g].push_back((uint32_t)i);
+    if (all_list != 0) lists[all_list].push_back((uint32_t)i);
+    w_max = std::max(w_max, w);
+  }
+  std::vector<std::vector<uint32_t>> by_group;
+  if (n_groups > 1) by_group.assign(lists.begin(), lists.begin() + n_groups);
+  auto bad_cap = [&](uint64_t x) { return x > 0 && x < w_max; };
+
+  // plan: distinct (partition, policy, capacity) caches of the inclusive configs
+  std::vector<MemoJob> jobs;
+  std::vector<std::tuple<uint32_t, int, uint64_t>> keys;
+  // per config and partition, the job of each tier (-1 absent)
+  std::vector<std::vector<std::array<int64_t, kTiers>>> use(n_cfg);
+  std::vector<uint8_t> literal(n_cfg, 0);
+  auto job_of = [&](uint32_t part, int pol, uint64_t c) -> int64_t {
+    const auto key = std::make_tuple(part, pol, c);
+    for (size_t q = 0; q < keys.size(); ++q)
+      if (keys[q] == key) return (int64_t)q;
+    keys.push_back(key);
+    MemoJob j;
+    j.part = part;
+    j.policy = pol;
+    j.cap = c;
+    jobs.push_back(std::move(j));
+    return (int64_t)keys.size() - 1;
+  };
+  for (uint32_t c = 0; c < n_cfg; ++c) {
+    const uint64_t* cp = cap + 3 * (size_t)c;
+    const uint64_t* cg = cap_group + 3 * kMaxGroups * (size_t)c;
+    const uint8_t* pol = policy + kMaxGroups * (size_t)c;
+    for (int k = 0; k < kTiers; ++k)
+      if (bad_cap(cp[k])) return -1;
+    if (mode[c] != M_INCLUSIVE) {
+      literal[c] = 1;
+      continue;
+    }
+    if (partitioned[c]) {
+      for (uint32_t g = 0; g < n_groups; ++g) {
+        std::array<int64_t, kTiers> t{-1, -1, -1};
+        for (int k = 0; k < kTiers; ++k) {
+          const uint64_t x = cg[k * kMaxGroups + g];
+          if (bad_cap(x)) return -1;
+          if (x) t[k] = job_of(g, pol[g], x);
+        }
+        use[c].push_back(t);
+      }
+    } else {
+      std::array<int64_t, kTiers> t{-1, -1, -1};
+      for (int k = 0; k < kTiers; ++k)
+        if (cp[k]) t[k] = job_of(all_list, pol[0], cp[k]);
+      use[c].push_back(t);
+    }
+  }
+
+  // replay every distinct cache once
+  parallel_for((uint32_t)jobs.size(), n_threads,
+               [&](uint32_t q) { memo_run(acc, lists[jobs[q].part], jobs[q]); });
+  std::vector<ListMasks> masks(n_groups + 1);
+  parallel_for(n_groups + 1, n_threads, [&](uint32_t p) {
+    if (p == 0 || p < n_groups || p == all_list) build_masks(acc, lists[p], n_groups, masks[p]);
+  });
+
+  // classify every configuration
+  std::atomic<int> status{0};
+  parallel_for(n_cfg, n_threads, [&](uint32_t c) {
+    Counts* out = new Counts;
+    std::fill(&out->v[0][0][0], &out->v[0][0][0] + kMaxGroups * kTiers * kFields, 0);
+    if (literal[c]) {
+      ConfigView v{cap + 3 * (size_t)c, cap_group + 3 * kMaxGroups * (size_t)c, mode[c],
+                   partitioned[c], policy + kMaxGroups * (size_t)c};
+      const int rc = replay_one(acc, n_groups > 1 ? by_group : lists, lists[all_list], n_groups,
+                                w_max, v, *out);
+      if (rc != 0) status.store(rc);
+    } else {
+      for (size_t u = 0; u < use[c].size(); ++u) {
+        const uint32_t part = partitioned[c] ? (uint32_t)u : all_list;
+        const MemoJob* t[kTiers];
+        for (int k = 0; k < kTiers; ++k) t[k] = use[c][u][k] >= 0 ? &jobs[use[c][u][k]] : nullptr;
+        memo_classify(masks[part], n_groups, t, *out);
+      }
+    }
+    uint64_t* dst = counts + (size_t)c * n_groups * kTiers * kFields;
+    for (uint32_t g = 0; g < n_groups; ++g)
+      for (int k = 0; k < kTiers; ++k)
+        for (int f = 0; f < kFields; ++f) dst[(g * kTiers + k) * kFields + f] = out->v[g][k][f];
+    delete out;
+  });
+  return status.load();
 }
 
 }  // extern "C"

@@ -7,6 +7,10 @@ module never imports the GPU library.
 * :func:`replay`     literal per-configuration tiered replay -> counts
                      uint64[n_cfg, n_groups, 3, 8] with fields
                      (hit, miss, ins, evict, hit_w, miss_w, ins_w, evict_w).
+* :func:`replay_memo` the same counts, with each distinct inclusive tier
+                     cache (partition, policy, capacity) replayed once and
+                     shared by the configurations that use it (for the
+                     full-size expected values).
 * :func:`objectives` (cost, throughput, latency) per configuration.
 * :func:`pareto`     non-dominated flags by brute force.
 * :func:`ttl_curves` per group and time-to-live, the disk tier's hits and
@@ -52,6 +56,8 @@ def _load():
         lib.oracle_replay.restype = ctypes.c_int
         lib.oracle_replay.argtypes = [ctypes.c_uint64, p, p, p, p, ctypes.c_uint32,
                                       ctypes.c_uint32, p, p, p, p, p, ctypes.c_uint32, p]
+        lib.oracle_replay_memo.restype = ctypes.c_int
+        lib.oracle_replay_memo.argtypes = lib.oracle_replay.argtypes
         lib.oracle_objectives.restype = ctypes.c_int
         lib.oracle_objectives.argtypes = [ctypes.c_uint32, p, p, ctypes.c_uint32, p,
                                           ctypes.c_double, ctypes.c_double, ctypes.c_double,
@@ -70,8 +76,15 @@ def default_threads() -> int:
     return max(1, len(os.sched_getaffinity(0)))
 
 
-def replay(trace, cfgs, threads: int | None = None) -> np.ndarray:
-    """Literal replay of every configuration of ``cfgs`` over ``trace``."""
+def replay(trace, cfgs, threads: int | None = None, memo: bool = False) -> np.ndarray:
+    """Literal replay of every configuration of ``cfgs`` over ``trace``.
+
+    With ``memo`` the inclusive configurations share their tier caches: an
+    inclusive tier is an independent cache that sees every access of its
+    partition, so each distinct (partition, policy, capacity) cache is
+    replayed once, literally, with a presence bit per access, and every
+    configuration is classified from its tiers' bits (served by k = present
+    in k and in no faster present tier).  The results are the same."""
     lib = _load()
     n_cfg = cfgs.n
     g = trace.n_groups
@@ -85,12 +98,17 @@ def replay(trace, cfgs, threads: int | None = None) -> np.ndarray:
     part = np.ascontiguousarray(cfgs.partitioned, dtype=np.uint8)
     pol = np.ascontiguousarray(cfgs.policy, dtype=np.uint8)
     rq = np.ascontiguousarray(trace.req, dtype=np.uint32)
-    rc = lib.oracle_replay(trace.n, _ptr(h), _ptr(gr), _ptr(w), _ptr(rq), g, n_cfg, _ptr(cap), _ptr(cg),
+    fn = lib.oracle_replay_memo if memo else lib.oracle_replay
+    rc = fn(trace.n, _ptr(h), _ptr(gr), _ptr(w), _ptr(rq), g, n_cfg, _ptr(cap), _ptr(cg),
                            _ptr(mode), _ptr(part), _ptr(pol),
                            threads or default_threads(), _ptr(out))
     if rc != 0:
         raise ValueError(f"oracle_replay rejected the batch (code {rc})")
     return out
+
+
+def replay_memo(trace, cfgs, threads: int | None = None) -> np.ndarray:
+    return replay(trace, cfgs, threads, memo=True)
 
 
 def cost_vector(cost: dict) -> np.ndarray:

@@ -39,6 +39,10 @@ import numpy as np
 
 from ._hash import chain_streams, mix64
 
+# Bumped whenever a generator's output changes; stored expected values are
+# keyed by it (and by a digest of the generated arrays).
+GENERATOR_VERSION = 1
+
 GRANULE_128K = 128 * 1024
 GRANULE_512K = 512 * 1024
 SPAN_2H = 7200.0
