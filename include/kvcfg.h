@@ -167,7 +167,12 @@ kv_status kv_trace_load(const kv_trace_desc* desc, void* stream, kv_trace** out)
  * rejected with KV_ERR_INVALID while its memory has not been reused. */
 kv_status kv_trace_free(kv_trace* t);
 
-/* Copy the trace's summary statistics into a host struct (synchronous). */
+/* Copy the trace's summary statistics into a host struct (synchronous).
+ * Also waits for the latest kv_eval_configs call on the trace and returns
+ * KV_ERR_DEVICE (with *out filled) if one of its FIFO/LFU replay jobs failed
+ * the replay's internal state check, in which case that call's counts are
+ * invalid; kv_last_error() names the job (policy, capacity, group).  A
+ * failure is reported once, by whichever call on the trace sees it first. */
 kv_status kv_trace_info(const kv_trace* t, kv_trace_stats* out);
 
 /* Evaluate n_cfg configurations over the trace (the simulator's per-candidate
@@ -185,11 +190,17 @@ kv_status kv_trace_info(const kv_trace* t, kv_trace_stats* out);
  *   cost = (price_gpu_per_hour + sum_k capGiB[k]*price_per_gib_hour[k]) * T_wall/3600
  *   throughput = N_w*tpg/T_wall (tokens/s);  latency = T_busy/n_req (s)
  * evaluated left to right in IEEE double without contraction.
+ * FIFO/LFU tiers are replayed once per distinct (order, group, policy,
+ * capacity); when the replay state of all of them (4 bytes per access per LFU
+ * job, 4 bytes per distinct block per FIFO job) does not fit in device
+ * memory, the jobs run in consecutive waves that share one state buffer.
  * Errors: KV_ERR_INVALID for a capacity in (0, w_max), partitioned capacities
  * that exceed cap[k], an unknown mode or policy, nonzero reserved bytes, or a
  * nonpositive cost-model rate; KV_ERR_UNSUPPORTED for the exclusive mode with
  * FIFO/LFU or with blocks of different weights, and for the prefix-reuse
- * mode with FIFO/LFU or partitioned capacities.  n_cfg == 0 is a no-op. */
+ * mode with FIFO/LFU or partitioned capacities; KV_ERR_NOMEM when not even
+ * one replay job's state fits; KV_ERR_DEVICE when an earlier call's replay
+ * failure (see kv_trace_info) has already arrived.  n_cfg == 0 is a no-op. */
 kv_status kv_eval_configs(const kv_trace* t, const kv_config* cfg, uint32_t n_cfg,
                           const kv_cost_model* model, uint64_t* counts, double* obj,
                           void* stream);
@@ -206,6 +217,9 @@ kv_status kv_eval_configs(const kv_trace* t, const kv_config* cfg, uint32_t n_cf
  *   n_front   host, or NULL; when non-NULL the call waits for the stream and
  *             stores the number of flagged rows
  * A row with a NaN objective is never on the front and never dominates.
+ * Without n_front the call is asynchronous and cannot report a NaN: such rows
+ * simply get flag 0 and dominate nothing.  Calls on different streams of one
+ * device take turns (they share the device's result counters).
  * Errors: KV_ERR_INVALID for NULL obj/on_front with n > 0, or n > 2^26; when
  * n_front is non-NULL, also KV_ERR_INVALID if any objective is NaN (flags are
  * still written).  n == 0 is a no-op (n_front = 0). */

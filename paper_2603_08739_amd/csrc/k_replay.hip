@@ -22,6 +22,7 @@
 //        and a per-class head pointer that only moves forward finds the
 //        oldest live member.
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <functional>
 #include <map>
@@ -62,6 +63,9 @@ struct JobArgs {
   uint64_t n;           // accesses per order; arrays hold 16 readable bytes past n
   uint32_t n_groups;
   uint32_t n_class;     // LFU class heads per job (kLdsClass)
+  uint32_t job_lo, job_hi;  // the jobs of this launch (a wave); others return at once
+  uint32_t fail_job;    // test hook: this job reports a failed state check (kNone: none)
+  uint32_t* err;        // {code, job}: code 1 = an LFU job failed its state check
 };
 
 constexpr int kRNT = 1024;                 // threads of a replay workgroup
@@ -126,6 +130,7 @@ struct GroupCounters {
 __global__ __launch_bounds__(256) void k_replay_init(const JobDev* __restrict__ jobs,
                                                      uint64_t* __restrict__ state,
                                                      uint32_t* __restrict__ cls, JobArgs a) {
+  if (blockIdx.y < a.job_lo || blockIdx.y >= a.job_hi) return;
   const JobDev j = jobs[blockIdx.y];
   if (j.closed) return;
   // FIFO: u32 insertion totals per block (two per word, all-ones = never
@@ -1801,6 +1806,7 @@ __global__ __launch_bounds__(kRNT) void k_replay(const JobDev* __restrict__ jobs
                                                  unsigned long long* __restrict__ jcnt) {
   __shared__ FifoLds lds;
   __shared__ GroupCounters gc;
+  if (blockIdx.x < a_in.job_lo || blockIdx.x >= a_in.job_hi) return;
   JobDev j = jobs[blockIdx.x];
   if (j.closed || j.kind == kJobLfu) return;
   const JobArgs a = job_args(a_in, j);
@@ -1837,6 +1843,7 @@ __global__ __launch_bounds__(NT) void k_replay_lfu(const JobDev* __restrict__ jo
                                                    unsigned long long* __restrict__ jcnt) {
   __shared__ LfuLds lds;
   __shared__ GroupCounters gc;
+  if (blockIdx.x < a_in.job_lo || blockIdx.x >= a_in.job_hi) return;
   JobDev j = jobs[blockIdx.x];
   if (j.closed || j.kind != kJobLfu) return;
   if (lfu_one_group(j, a_in.n_groups) != G1) return;
@@ -1859,10 +1866,11 @@ __global__ __launch_bounds__(NT) void k_replay_lfu(const JobDev* __restrict__ jo
   unsigned long long* cnt = jcnt + (uint64_t)blockIdx.x * a.n_groups * 4;
   lfu_chunked<NT, G1>(j, a, reinterpret_cast<uint32_t*>(state + j.state_off), cls,
                       bits + j.bits_off, gc, lds, g0);
-  const bool ok = lds.ok != 0;
+  const bool ok = lds.ok != 0 && blockIdx.x != a.fail_job;
   __syncthreads();
   write_counters(gc, a.n_groups, cnt);
-  if (tid == 0 && !ok) cnt[0] = ~0ull;  // poison: surfaced as an impossible count
+  // a failed state check is recorded for the host (the first failing job wins)
+  if (tid == 0 && !ok && atomicCAS(&a.err[0], 0u, 1u) == 0u) atomicExch(&a.err[1], blockIdx.x);
 #ifdef KV_REPLAY_STATS
   RSTAT(blockIdx.x, kStJob, wall_clock64() - tj0);
   __syncthreads();
@@ -2233,6 +2241,20 @@ static kv_status aux_stream(AuxStream** out) {
   return KV_OK;
 }
 
+// Test hooks, read at every call: KVCFG_TEST_REPLAY_BUDGET caps the replay
+// state of one wave (bytes), so that a small batch needs several waves;
+// KVCFG_TEST_FAIL_JOB makes that replay job report a failed state check
+// (its kernel still runs to completion), so that the error path is seen.
+static uint64_t replay_test_budget() {
+  const char* e = std::getenv("KVCFG_TEST_REPLAY_BUDGET");
+  return e ? std::strtoull(e, nullptr, 10) : 0ull;
+}
+
+static uint32_t replay_test_fail_job() {
+  const char* e = std::getenv("KVCFG_TEST_FAIL_JOB");
+  return e ? (uint32_t)std::strtoul(e, nullptr, 10) : kNone;
+}
+
 kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_config* cfg_host,
                      const kv_config* cfg_dev, uint32_t n_cfg, uint64_t* counts,
                      hipStream_t s, const std::function<kv_status()>& meanwhile) {
@@ -2245,6 +2267,7 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
   const uint32_t class_words = n_class;  // u32 words per LFU job: class heads
   // layout of job state, class arrays and bitmaps
   std::vector<JobDev> jd(jobs.size());
+  std::vector<uint64_t> jw(jobs.size(), 0);  // replay-state words of each job
   uint64_t state_words = 0, class_total = 0, bit_words = 0;
   for (size_t i = 0; i < jobs.size(); ++i) {
     const ReplayJob& r = jobs[i];
@@ -2266,9 +2289,9 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
       j.chunk = kLChunk;
     }
     if (!r.closed && r.end > r.begin) {
-      j.state_off = state_words;
-      // LFU: one count per position, and a spare slot past the end
-      state_words += (r.policy == KV_POLICY_FIFO) ? (t.u + 1) / 2 : (r.end - r.begin + 2) / 2;
+      // FIFO: one u32 per block; LFU: one count per position and a spare slot
+      jw[i] = (r.policy == KV_POLICY_FIFO) ? (t.u + 1) / 2 : (r.end - r.begin + 2) / 2;
+      state_words += jw[i];
       if (r.policy == KV_POLICY_LFU) {
         j.class_off = class_total;
         class_total += class_words;
@@ -2279,6 +2302,38 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
       j.closed = 1;  // an empty segment behaves like a closed job
     }
   }
+  // Waves: the replay state of every job at once, or, when that does not fit
+  // the device (or the test budget), consecutive groups of jobs that share
+  // one state buffer and run one group after another.
+  std::vector<uint32_t> wave_lo;  // first job of each wave
+  uint64_t wave_words = 0;        // state words of the largest wave
+  auto plan_waves = [&](uint64_t budget_words) {
+    wave_lo.assign(1, 0);
+    wave_words = 0;
+    uint64_t cur = 0;
+    for (size_t i = 0; i < jd.size(); ++i) {
+      if (cur && cur + jw[i] > budget_words) {
+        wave_lo.push_back((uint32_t)i);
+        cur = 0;
+      }
+      jd[i].state_off = cur;
+      cur += jw[i];
+      wave_words = std::max(wave_words, cur);
+    }
+  };
+  uint64_t max_job = 0;
+  for (uint64_t x : jw) max_job = std::max(max_job, x);
+  uint64_t budget = std::max<uint64_t>(state_words, 1);
+  if (const uint64_t tb = replay_test_budget()) budget = std::max<uint64_t>(tb / 8, 1);
+  DevBuf& bstate = t.ws[12];
+  for (;;) {
+    plan_waves(std::max(budget, max_job));
+    if ((st = bstate.reserve(std::max<uint64_t>(wave_words, 1) * 8)) == KV_OK) break;
+    if (st != KV_ERR_NOMEM || budget <= max_job) return st;
+    budget = budget / 2;  // retry with smaller waves
+  }
+  const uint32_t n_waves = (uint32_t)wave_lo.size();
+  wave_lo.push_back((uint32_t)jd.size());
   // job counters, closed jobs preset: every distinct block inserted once
   std::vector<unsigned long long> jc(jobs.size() * G * 4, 0ull);
   for (size_t i = 0; i < jobs.size(); ++i) {
@@ -2361,14 +2416,12 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
   }
   const bool tiled = n_src[0] <= (uint32_t)kCbSrc && n_src[1] <= (uint32_t)kCbSrc;
   DevBuf& bj = t.ws[11];
-  DevBuf& bstate = t.ws[12];
   DevBuf& bcls = t.ws[13];
   DevBuf& bbits = t.ws[14];
   DevBuf& bjc = t.ws[15];
   DevBuf& brec = t.ws[16];
   DevBuf& bord = t.ws[17];
   if ((st = bj.reserve(jd.size() * sizeof(JobDev))) != KV_OK) return st;
-  if ((st = bstate.reserve(std::max<uint64_t>(state_words, 1) * 8)) != KV_OK) return st;
   if ((st = bcls.reserve(std::max<uint64_t>(class_total, 2) * 4)) != KV_OK) return st;
   if ((st = bbits.reserve(std::max<uint64_t>(bit_words, 1) * 8)) != KV_OK) return st;
   if ((st = bjc.reserve(std::max<size_t>(jc.size(), 1) * 8)) != KV_OK) return st;
@@ -2420,13 +2473,21 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
   ja.n = t.n;
   ja.n_groups = G;
   ja.n_class = n_class;
+  ja.err = t.err.as<uint32_t>();
+  ja.fail_job = replay_test_fail_job();
   const uint32_t nj = (uint32_t)jd.size();
+  auto wave_args = [&](uint32_t w) {
+    JobArgs x = ja;
+    x.job_lo = wave_lo[w];
+    x.job_hi = wave_lo[w + 1];
+    return x;
+  };
   if (nj) {
     hipLaunchKernelGGL(k_replay_init, dim3(64, nj), dim3(256), 0, s, bj.as<JobDev>(),
-                       bstate.as<uint64_t>(), bcls.as<uint32_t>(), ja);
+                       bstate.as<uint64_t>(), bcls.as<uint32_t>(), wave_args(0));
     KV_HIP(hipGetLastError());
-    tm.reset();
   }
+  tm.reset();
   // the combine's inputs, staged before the streams fork (the FIFO records
   // are combined on the FIFO stream)
   CombineArgs ca{};
@@ -2520,44 +2581,71 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
     else if (lfu_one_group(q, G)) any[0] = true;
     else any[1] = true;
   }
-  AuxStream* aux = nullptr;
-  std::unique_lock<std::mutex> lk;
-  if (any[0] || any[1] || any[2]) {
-    if ((st = aux_stream(&aux)) != KV_OK) return st;
-    lk = std::unique_lock<std::mutex>(aux->mu);
-    KV_HIP(hipEventRecord(aux->fork, s));
-  }
-  for (int k = 0; k < kAux; ++k) {
-    if (!any[k]) continue;
-    hipStream_t sk = aux->s[k];
-    KV_HIP(hipStreamWaitEvent(sk, aux->fork, 0));
+  // one replay kernel (k: LFU one-group, other LFU, FIFO) over the jobs of x
+  auto launch = [&](int k, hipStream_t sk, const JobArgs& x) -> kv_status {
     tm.emplace(k == 2 ? kStReplayFifo : kStReplay, sk);
     if (k == 0)
       hipLaunchKernelGGL((k_replay_lfu<kLfuNT, true>), dim3(nj), dim3(kLfuNT), 0, sk,
-                         bj.as<JobDev>(), ja, bstate.as<uint64_t>(), bcls.as<uint32_t>(),
+                         bj.as<JobDev>(), x, bstate.as<uint64_t>(), bcls.as<uint32_t>(),
                          bbits.as<uint64_t>(), bjc.as<unsigned long long>());
     else if (k == 1)
       hipLaunchKernelGGL((k_replay_lfu<kLfuNT, false>), dim3(nj), dim3(kLfuNT), 0, sk,
-                         bj.as<JobDev>(), ja, bstate.as<uint64_t>(), bcls.as<uint32_t>(),
+                         bj.as<JobDev>(), x, bstate.as<uint64_t>(), bcls.as<uint32_t>(),
                          bbits.as<uint64_t>(), bjc.as<unsigned long long>());
     else
-      hipLaunchKernelGGL(k_replay, dim3(nj), dim3(kRNT), 0, sk, bj.as<JobDev>(), ja,
+      hipLaunchKernelGGL(k_replay, dim3(nj), dim3(kRNT), 0, sk, bj.as<JobDev>(), x,
                          bstate.as<uint64_t>(), bbits.as<uint64_t>(),
                          bjc.as<unsigned long long>());
     KV_HIP(hipGetLastError());
     tm.reset();
-    if (k == 2 && tiled && nf) {
-      tm.emplace(kStCombine, sk);
-      if ((st = combine_range(0, nf, sk)) != KV_OK) return st;
-      tm.reset();
+    return KV_OK;
+  };
+  bool fifo_combined = false;
+  if (n_waves == 1) {
+    // LFU jobs of one group, other LFU jobs, FIFO jobs and the caller's other
+    // work (the LRU stack pass) run concurrently: the replay kernels on
+    // streams forked from the caller's and joined back into it before the
+    // records are combined
+    AuxStream* aux = nullptr;
+    std::unique_lock<std::mutex> lk;
+    if (any[0] || any[1] || any[2]) {
+      if ((st = aux_stream(&aux)) != KV_OK) return st;
+      lk = std::unique_lock<std::mutex>(aux->mu);
+      KV_HIP(hipEventRecord(aux->fork, s));
     }
-    KV_HIP(hipEventRecord(aux->join[k], sk));
+    for (int k = 0; k < kAux; ++k) {
+      if (!any[k]) continue;
+      hipStream_t sk = aux->s[k];
+      KV_HIP(hipStreamWaitEvent(sk, aux->fork, 0));
+      if ((st = launch(k, sk, wave_args(0))) != KV_OK) return st;
+      if (k == 2 && tiled && nf) {
+        tm.emplace(kStCombine, sk);
+        if ((st = combine_range(0, nf, sk)) != KV_OK) return st;
+        tm.reset();
+        fifo_combined = true;
+      }
+      KV_HIP(hipEventRecord(aux->join[k], sk));
+    }
+    const kv_status st_mid = meanwhile();
+    for (int k = 0; k < kAux; ++k)
+      if (any[k]) KV_HIP(hipStreamWaitEvent(s, aux->join[k], 0));
+    lk = std::unique_lock<std::mutex>();
+    if (st_mid != KV_OK) return st_mid;
+  } else {
+    // waves share the state buffer: the caller's other work, then every
+    // wave's kernels, one after another on the caller's stream
+    if ((st = meanwhile()) != KV_OK) return st;
+    for (uint32_t w = 0; w < n_waves; ++w) {
+      const JobArgs x = wave_args(w);
+      if (w > 0) {
+        hipLaunchKernelGGL(k_replay_init, dim3(64, nj), dim3(256), 0, s, bj.as<JobDev>(),
+                           bstate.as<uint64_t>(), bcls.as<uint32_t>(), x);
+        KV_HIP(hipGetLastError());
+      }
+      for (int k = 0; k < kAux; ++k)
+        if (any[k] && (st = launch(k, s, x)) != KV_OK) return st;
+    }
   }
-  const kv_status st_mid = meanwhile();
-  for (int k = 0; k < kAux; ++k)
-    if (any[k]) KV_HIP(hipStreamWaitEvent(s, aux->join[k], 0));
-  lk = std::unique_lock<std::mutex>();
-  if (st_mid != KV_OK) return st_mid;
 #ifdef KV_REPLAY_STATS
   {
     KV_HIP(hipStreamSynchronize(s));
@@ -2589,7 +2677,7 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
   if (!recs.empty()) {
     tm.emplace(kStCombine, s);
     if (tiled) {
-      if (!any[2] && (st = combine_range(0, nf, s)) != KV_OK) return st;
+      if (!fifo_combined && (st = combine_range(0, nf, s)) != KV_OK) return st;
       if ((st = combine_range(nf, nrec, s)) != KV_OK) return st;
       hipLaunchKernelGGL(k_combine_fin, dim3(div_up(nrec, 256)), dim3(256), 0, s,
                          brec.as<RecDev>(), nrec, bpart.as<unsigned long long>(),
@@ -2599,6 +2687,16 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
       hipLaunchKernelGGL(k_combine, dim3(nrec), dim3(256), 0, s, brec.as<RecDev>(), ca, counts);
       KV_HIP(hipGetLastError());
     }
+  }
+  tm.reset();
+  if (any[0] || any[1]) {
+    // the LFU jobs' error record, read by the next call on this trace
+    t.err_jobs.resize(jd.size());
+    for (size_t i = 0; i < jd.size(); ++i)
+      t.err_jobs[i] = ReplayJobInfo{jd[i].policy, jd[i].group, jd[i].cap};
+    KV_HIP(hipMemcpyAsync(t.err_host, t.err.p, 2 * sizeof(uint32_t), hipMemcpyDeviceToHost, s));
+    KV_HIP(hipEventRecord(t.err_ev, s));
+    t.err_pending = true;
   }
   return KV_OK;
 }

@@ -33,6 +33,9 @@
 // of blocks whose final stack depth (the weight of distinct blocks accessed
 // at or after their last access) falls in the bin; cumulative over bins on
 // return, so hits(C) is one lookup.
+#include <algorithm>
+#include <cstdlib>
+
 #include "kv_device.h"
 #include "kv_internal.h"
 
@@ -54,7 +57,7 @@ __host__ __device__ __forceinline__ uint64_t tri_off(uint64_t x) { return x * (x
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_sd_rowhist(const uint32_t* __restrict__ key,
                                                     const uint8_t* __restrict__ w8, uint64_t n,
-                                                    uint32_t* __restrict__ Q) {
+                                                    uint32_t row_chunk, uint32_t* __restrict__ Q) {
   __shared__ uint32_t h[kRowChunk];
   __shared__ uint32_t sh[8];
   const uint32_t X = blockIdx.x;
@@ -62,8 +65,8 @@ __global__ __launch_bounds__(256) void k_sd_rowhist(const uint32_t* __restrict__
   const uint64_t base = (uint64_t)X * kSdB;
   const uint32_t nb = (uint32_t)min<uint64_t>(kSdB, n - base);
   const uint64_t row = tri_off(X);
-  for (uint32_t c0 = 0; c0 < X; c0 += kRowChunk) {
-    const uint32_t width = min(kRowChunk, X - c0);
+  for (uint32_t c0 = 0; c0 < X; c0 += row_chunk) {
+    const uint32_t width = min(row_chunk, X - c0);
     for (uint32_t j = threadIdx.x; j < width; j += 256) h[j] = 0;
     __syncthreads();
     uint32_t carry = 0;
@@ -577,6 +580,18 @@ __global__ void k_hist_cum(uint64_t* hist, const uint32_t* __restrict__ off, uin
   }
 }
 
+// Test hooks, read at every call: KVCFG_TEST_ROW_CHUNK narrows the LDS
+// histogram of a block-matrix row (so that short traces take the
+// column-chunk path of long ones); KVCFG_TEST_THR_LDS lowers the number of
+// thresholds binned in LDS (so that few thresholds take the global-atomic
+// path of very many).  Both only select among paths of the same result.
+uint32_t env_limit(const char* name, uint32_t dflt, uint32_t lo) {
+  const char* e = std::getenv(name);
+  if (!e) return dflt;
+  const unsigned long v = std::strtoul(e, nullptr, 10);
+  return (uint32_t)std::max<unsigned long>(lo, std::min<unsigned long>(v, dflt));
+}
+
 uint32_t grid_of(uint64_t m, uint32_t cap = 32768) {
   uint64_t g = (m + 255) / 256;
   if (g > cap) g = cap;
@@ -620,7 +635,8 @@ kv_status stack_pass(Trace& t, Order& o, bool partitioned, const ThresholdSet& t
   uint32_t* Q = b_Q.as<uint32_t>();
   if (G >= 2) {
     StageTimer tm(kStStackMatrix, s);
-    hipLaunchKernelGGL(k_sd_rowhist, dim3(G), dim3(256), 0, s, key, w8, n, Q);
+    const uint32_t row_chunk = env_limit("KVCFG_TEST_ROW_CHUNK", kRowChunk, 1);
+    hipLaunchKernelGGL(k_sd_rowhist, dim3(G), dim3(256), 0, s, key, w8, n, row_chunk, Q);
     KV_HIP(hipGetLastError());
     const dim3 cg(div_up(G, 256), nchunks);
     hipLaunchKernelGGL(k_sd_colsum, cg, dim3(256), 0, s, Q, G, b_csum.as<uint32_t>());
@@ -639,7 +655,7 @@ kv_status stack_pass(Trace& t, Order& o, bool partitioned, const ThresholdSet& t
     KV_HIP(hipGetLastError());
   }
   BinArgs ba{thr_dev, off_dev, (uint32_t)ts.values.size(), ts.n_groups, hist};
-  const bool lds = ts.values.size() + ts.n_groups <= kThrLds;
+  const bool lds = ts.values.size() + ts.n_groups <= env_limit("KVCFG_TEST_THR_LDS", kThrLds, 0);
   const uint32_t ga = std::min<uint32_t>(G, 2048);
   {
   StageTimer tm(kStStackAssemble, s);

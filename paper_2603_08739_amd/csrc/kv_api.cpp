@@ -192,6 +192,37 @@ void DevBuf::release() {
   bytes = 0;
 }
 
+Trace::~Trace() {
+  if (err_ev) (void)hipEventDestroy(err_ev);
+  if (err_host) (void)hipHostFree(err_host);
+}
+
+kv_status check_device_error(Trace& t, bool wait, const char* who) {
+  if (!t.err_pending) return KV_OK;
+  if (wait) {
+    KV_HIP(hipEventSynchronize(t.err_ev));
+  } else {
+    const hipError_t q = hipEventQuery(t.err_ev);
+    if (q == hipErrorNotReady) return KV_OK;  // that call is still running
+    if (q != hipSuccess) return hip_fail(q, "hipEventQuery");
+  }
+  t.err_pending = false;
+  const uint32_t code = t.err_host[0], job = t.err_host[1];
+  if (code == 0) return KV_OK;
+  t.err_host[0] = t.err_host[1] = 0;
+  KV_HIP(hipMemset(t.err.p, 0, 2 * sizeof(uint32_t)));
+  std::string what = "replay job " + std::to_string(job);
+  if (job < t.err_jobs.size()) {
+    const ReplayJobInfo& j = t.err_jobs[job];
+    what += std::string(" (") + (j.policy == KV_POLICY_LFU ? "LFU" : "FIFO") + ", capacity " +
+            std::to_string(j.cap) + " granules, " +
+            (j.group == KV_MAX_GROUPS ? std::string("shared") : "group " + std::to_string(j.group)) +
+            ")";
+  }
+  return fail(KV_ERR_DEVICE, std::string(who) + ": an earlier kv_eval_configs call on this trace "
+              "returned invalid counts: " + what + " failed its internal state check");
+}
+
 namespace {
 
 bool finite_pos(double x) { return std::isfinite(x) && x > 0; }
@@ -329,6 +360,44 @@ kv_status run_stack(Trace& t, Order& o, bool partitioned, ThresholdSet& ts, Stac
   return KV_OK;
 }
 
+// kv_pareto's device counters, one set per device, kept until the process
+// ends; `done` is recorded after each call's last use of them.
+struct PareCounters {
+  std::mutex mu;
+  DevBuf buf;
+  uint32_t* host = nullptr;  // pinned
+  hipEvent_t done = nullptr;
+};
+
+kv_status pareto_counters(PareCounters** out) {
+  static std::mutex mu;
+  static PareCounters* per_dev[64] = {};
+  int d = 0;
+  KV_HIP(hipGetDevice(&d));
+  if (d < 0 || d >= 64) return fail(KV_ERR_DEVICE, "device index out of range");
+  std::lock_guard<std::mutex> lk(mu);
+  if (!per_dev[d]) {
+    auto* pc = new PareCounters();
+    kv_status st = pc->buf.reserve(2 * sizeof(uint32_t));
+    if (st != KV_OK) {
+      delete pc;
+      return st;
+    }
+    hipError_t e = hipHostMalloc((void**)&pc->host, 2 * sizeof(uint32_t), hipHostMallocDefault);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&pc->done, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventRecord(pc->done, nullptr);
+    if (e != hipSuccess) {
+      if (pc->done) (void)hipEventDestroy(pc->done);
+      if (pc->host) (void)hipHostFree(pc->host);
+      delete pc;
+      return hip_fail(e, "kv_pareto: counters");
+    }
+    per_dev[d] = pc;
+  }
+  *out = per_dev[d];
+  return KV_OK;
+}
+
 }  // namespace
 }  // namespace kv
 
@@ -382,6 +451,14 @@ kv_status kv_trace_load(const kv_trace_desc* d, void* stream, kv_trace** out) {
   if (st == KV_OK && t->st.n_w >= 0xFFFFFFFFull) {
     st = fail(KV_ERR_UNSUPPORTED, "kv_trace_load: total weight must stay below 2^32 granules");
   }
+  if (st == KV_OK) st = t->err.reserve(2 * sizeof(uint32_t));
+  if (st == KV_OK) st = fill_u32(t->err.as<uint32_t>(), 0, 2, s);
+  if (st == KV_OK) {
+    hipError_t e = hipHostMalloc((void**)&t->err_host, 2 * sizeof(uint32_t), hipHostMallocDefault);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&t->err_ev, hipEventDisableTiming);
+    if (e != hipSuccess) st = hip_fail(e, "kv_trace_load: error record");
+    else t->err_host[0] = t->err_host[1] = 0;
+  }
   if (st != KV_OK) {
     (void)hipStreamSynchronize(s);
     delete t;
@@ -403,6 +480,7 @@ kv_status kv_ttl_curves(const kv_trace* h, const double* ttl, uint32_t n_ttl, ui
   if (!h) return fail(KV_ERR_INVALID, "kv_ttl_curves: trace is NULL");
   Trace* t = const_cast<Trace*>(reinterpret_cast<const Trace*>(h));
   if (!is_live(t)) return fail(KV_ERR_INVALID, "kv_ttl_curves: not a live trace handle");
+  if (kv_status e = check_device_error(*t, false, "kv_ttl_curves")) return e;
   if (!ttl || !hits || !hitw || !store)
     return fail(KV_ERR_INVALID, "kv_ttl_curves: ttl, hits, hitw and store are required");
   if (n_ttl == 0) return fail(KV_ERR_INVALID, "kv_ttl_curves: n_ttl must be >= 1");
@@ -440,10 +518,10 @@ kv_status kv_trace_free(kv_trace* h) {
 
 kv_status kv_trace_info(const kv_trace* h, kv_trace_stats* out) {
   if (!h || !out) return fail(KV_ERR_INVALID, "kv_trace_info: NULL argument");
-  const Trace* t = reinterpret_cast<const Trace*>(h);
+  Trace* t = const_cast<Trace*>(reinterpret_cast<const Trace*>(h));
   if (!is_live(t)) return fail(KV_ERR_INVALID, "kv_trace_info: not a live trace handle");
   *out = t->st;
-  return KV_OK;
+  return check_device_error(*t, true, "kv_trace_info");
 }
 
 kv_status kv_eval_configs(const kv_trace* h, const kv_config* cfg, uint32_t n_cfg,
@@ -453,6 +531,7 @@ kv_status kv_eval_configs(const kv_trace* h, const kv_config* cfg, uint32_t n_cf
   Trace* t = const_cast<Trace*>(reinterpret_cast<const Trace*>(h));
   if (!is_live(t)) return fail(KV_ERR_INVALID, "kv_eval_configs: not a live trace handle");
   kv_status st;
+  if ((st = check_device_error(*t, false, "kv_eval_configs")) != KV_OK) return st;
   if ((st = validate_model(model)) != KV_OK) return st;
   if (n_cfg == 0) return KV_OK;
   if (!cfg || !counts) return fail(KV_ERR_INVALID, "kv_eval_configs: cfg and counts are required");
@@ -572,21 +651,27 @@ kv_status kv_pareto(const double* obj, const uint32_t* segment, uint32_t n, cons
   if (!obj || !on_front) return fail(KV_ERR_INVALID, "kv_pareto: obj and on_front are required");
   if (n > (1u << 26)) return fail(KV_ERR_INVALID, "kv_pareto: n must be <= 2^26");
   hipStream_t s = (hipStream_t)stream;
-  uint32_t* counters = nullptr;
-  KV_HIP(hipMallocAsync((void**)&counters, 2 * sizeof(uint32_t), s));
-  kv_status st = fill_u32(counters, 0, 2, s);
+  // the per-device counters {flagged rows, NaN seen}, allocated on the first
+  // call; calls on different streams take turns through `done`
+  PareCounters* pc = nullptr;
+  kv_status st = pareto_counters(&pc);
+  if (st != KV_OK) return st;
+  std::lock_guard<std::mutex> lk(pc->mu);
+  KV_HIP(hipStreamWaitEvent(s, pc->done, 0));
+  uint32_t* counters = pc->buf.as<uint32_t>();
+  st = fill_u32(counters, 0, 2, s);
   if (st == KV_OK) st = pareto(obj, segment, n, bounds, on_front, counters, s);
-  uint32_t hc[2] = {0, 0};
   if (st == KV_OK && n_front) {
-    hipError_t e = hipMemcpyAsync(hc, counters, sizeof(hc), hipMemcpyDeviceToHost, s);
-    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    hipError_t e = hipMemcpyAsync(pc->host, counters, 2 * sizeof(uint32_t),
+                                  hipMemcpyDeviceToHost, s);
     if (e != hipSuccess) st = hip_fail(e, "kv_pareto result copy");
   }
-  (void)hipFreeAsync(counters, s);
+  KV_HIP(hipEventRecord(pc->done, s));
   if (st != KV_OK) return st;
   if (n_front) {
-    *n_front = hc[0];
-    if (hc[1]) return fail(KV_ERR_INVALID, "kv_pareto: an objective is NaN");
+    KV_HIP(hipEventSynchronize(pc->done));
+    *n_front = pc->host[0];
+    if (pc->host[1]) return fail(KV_ERR_INVALID, "kv_pareto: an objective is NaN");
   }
   return KV_OK;
 }

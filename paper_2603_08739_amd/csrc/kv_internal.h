@@ -70,6 +70,12 @@ struct ThresholdSet {
   uint32_t bin_base(uint32_t g) const { return off[g] + g; }
 };
 
+// What an error message needs to name a replay job.
+struct ReplayJobInfo {
+  uint32_t policy, group;
+  uint64_t cap;
+};
+
 struct GroupStats {
   uint64_t n_g, n_w_g, u_g, w0;  // accesses, weight, distinct blocks, uniform weight
 };
@@ -90,6 +96,15 @@ struct Trace {
   DevBuf req_time;    // f64[n_req] arrival time of each request
   // workspace reused across kv_eval_configs calls on this trace
   DevBuf ws[27];
+  // Device error record {code, job} written by a replay kernel that fails
+  // its internal state check; copied after every kv_eval_configs call that
+  // replays into `err_host` (pinned), with `err_ev` recorded after the copy.
+  DevBuf err;
+  uint32_t* err_host = nullptr;
+  hipEvent_t err_ev = nullptr;
+  bool err_pending = false;
+  std::vector<ReplayJobInfo> err_jobs;  // the replayed jobs of the latest call
+  ~Trace();
   // host staging of the latest kv_eval_configs call (alive across its copies)
   ThresholdSet shared_ts, part_ts;
   std::vector<kv_config> cfg_stage;
@@ -167,6 +182,11 @@ kv_status pareto(const double* obj, const uint32_t* segment, uint32_t n, const d
 // thresholds on the device.
 kv_status ttl_curves(Trace& t, const double* ttl_dev, uint32_t n_ttl, uint64_t* hits,
                      uint64_t* hitw, double* store, hipStream_t s);
+
+// Reports (and clears) a replay failure recorded on the device by an earlier
+// kv_eval_configs call on `t`: with `wait`, waits for that call's error
+// copy; otherwise reports only what has already arrived.
+kv_status check_device_error(Trace& t, bool wait, const char* who);
 
 // replay of non-LRU policies (k_replay.hip)
 struct ReplayJob {

@@ -14,8 +14,7 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-# KVCFG_LIB names another build of the same library (e.g. a diagnostics build)
-LIB_PATH = os.environ.get("KVCFG_LIB") or os.path.join(_HERE, "libkvcfg.so")
+LIB_PATH = os.path.join(_HERE, "libkvcfg.so")
 
 KV_OK, KV_ERR_INVALID, KV_ERR_NOMEM, KV_ERR_DEVICE, KV_ERR_UNSUPPORTED = 0, -1, -2, -3, -4
 KV_MAX_GROUPS, KV_TIERS, KV_FIELDS = 16, 3, 8
@@ -136,11 +135,39 @@ def _ptr(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
 
+def _dev(t, name, dtypes, numel, optional=False):
+    """Checks that a tensor the library writes or reads on the device is a
+    contiguous CUDA tensor of an allowed dtype holding at least `numel`
+    elements (the library trusts the pointer it is given)."""
+    if t is None:
+        if optional:
+            return None
+        raise ValueError(f"{name} is required")
+    import torch
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a CUDA tensor")
+    if t.dtype not in dtypes:
+        raise ValueError(f"{name} has dtype {t.dtype}; expected one of {dtypes}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.numel() < numel:
+        raise ValueError(f"{name} holds {t.numel()} elements; the call needs {numel}")
+    return _ptr(t)
+
+
+def _dt():
+    import torch
+    i64 = (torch.int64, torch.uint64) if hasattr(torch, "uint64") else (torch.int64,)
+    i32 = (torch.int32, torch.uint32) if hasattr(torch, "uint32") else (torch.int32,)
+    return i64, i32, (torch.uint8,), (torch.float64,)
+
+
 class Trace:
     """A device-resident canonical trace (owns the kv_trace handle)."""
 
     def __init__(self, handle):
         self.handle = handle
+        self.n_groups = int(self.info().n_groups)
 
     def info(self) -> kv_trace_stats:
         st = kv_trace_stats()
@@ -164,14 +191,16 @@ def kv_trace_load(hash, req, req_time, group=None, weight=None, n_groups=1,
                   tokens_per_granule=16, granule_bytes=128 * 1024, stream=None) -> Trace:
     """hash: int64/uint64 device tensor [n]; req: int32 [n]; req_time: float64 [n_req];
     group, weight: uint8 [n] or None."""
+    i64, i32, u8, f64 = _dt()
+    n = int(hash.numel())
     d = kv_trace_desc()
-    d.n = int(hash.numel())
-    d.hash = _ptr(hash)
-    d.req = _ptr(req)
-    d.group = _ptr(group)
-    d.weight = _ptr(weight)
+    d.n = n
+    d.hash = _dev(hash, "hash", i64, n)
+    d.req = _dev(req, "req", i32, n)
+    d.group = _dev(group, "group", u8, n, optional=True)
+    d.weight = _dev(weight, "weight", u8, n, optional=True)
     d.n_req = int(req_time.numel())
-    d.req_time = _ptr(req_time)
+    d.req_time = _dev(req_time, "req_time", f64, d.n_req)
     d.n_groups = int(n_groups)
     d.tokens_per_granule = int(tokens_per_granule)
     d.granule_bytes = int(granule_bytes)
@@ -213,27 +242,45 @@ def cost_model(price_gpu_per_hour, price_per_gib_hour, bw_dram, ssd_bw_base, ssd
 def kv_eval_configs(trace: Trace, cfg_arr, n_cfg: int, model: kv_cost_model, counts, obj=None,
                     stream=None):
     """counts: int64/uint64 device tensor [n_cfg, n_groups, 3, 8]; obj: float64 [n_cfg, 3]."""
+    i64, _, _, f64 = _dt()
+    n_cfg = int(n_cfg)
+    if n_cfg > len(cfg_arr):
+        raise ValueError("n_cfg exceeds the configuration array")
+    pc = _dev(counts, "counts", i64, n_cfg * trace.n_groups * KV_TIERS * KV_FIELDS)
+    po = _dev(obj, "obj", f64, n_cfg * 3, optional=True)
     _check(LIB.kv_eval_configs(trace.handle, ctypes.cast(cfg_arr, _vp), n_cfg,
-                               ctypes.byref(model), _ptr(counts), _ptr(obj), _stream(stream)))
+                               ctypes.byref(model), pc, po, _stream(stream)))
 
 
 def kv_pareto(obj, on_front, segment=None, bounds=None, want_count=True, stream=None):
     """obj: float64 device [n,3]; on_front: uint8 device [n]; segment: int32/uint32 device [n]."""
+    _, i32, u8, f64 = _dt()
     n = int(obj.shape[0])
+    if obj.dim() != 2 or obj.shape[1] != 3:
+        raise ValueError("obj must have shape [n, 3]")
+    po = _dev(obj, "obj", f64, 3 * n)
+    pf = _dev(on_front, "on_front", u8, n)
+    ps = _dev(segment, "segment", i32, n, optional=True)
     b = None
     if bounds is not None:
         barr = (ctypes.c_double * 3)(*[float(x) for x in bounds])
         b = ctypes.cast(barr, _vp)
     cnt = _u32(0)
-    _check(LIB.kv_pareto(_ptr(obj), _ptr(segment), n, b, _ptr(on_front),
-                         ctypes.byref(cnt) if want_count else None, _stream(stream)))
+    _check(LIB.kv_pareto(po, ps, n, b, pf, ctypes.byref(cnt) if want_count else None,
+                         _stream(stream)))
     return int(cnt.value) if want_count else None
 
 
 def kv_ttl_curves(trace: Trace, ttl, hits, hitw, store, stream=None):
     """ttl: host sequence of float seconds (non-decreasing); hits, hitw: int64/uint64
     device tensors [n_groups, n_ttl]; store: float64 device [n_groups, n_ttl]."""
+    i64, _, _, f64 = _dt()
     vals = [float(x) for x in ttl]
     arr = (ctypes.c_double * max(len(vals), 1))(*vals)
-    _check(LIB.kv_ttl_curves(trace.handle, ctypes.cast(arr, _vp), len(vals), _ptr(hits),
-                             _ptr(hitw), _ptr(store), _stream(stream)))
+    m = trace.n_groups * len(vals)
+    ph = _dev(hits, "hits", i64, m)
+    pw = _dev(hitw, "hitw", i64, m)
+    pst = _dev(store, "store", f64, m)
+    _check(LIB.kv_ttl_curves(trace.handle, ctypes.cast(arr, _vp), len(vals), ph, pw, pst,
+                             _stream(stream)))
+
