@@ -33,6 +33,21 @@ def test_digests_match_generators(name):
     assert g["counts"].shape == (len(g["idx"]), t.n_groups, 3, 8)
 
 
+@pytest.mark.parametrize("name", ["longctx"])
+def test_large_files_present(name):
+    g = _gold(name)
+    assert int(g["generator_version"]) == tg.GENERATOR_VERSION
+    c = g["counts"].astype(np.int64)
+    assert c.shape[0] == len(g["idx"]) > 0
+    # every access reaches the first present tier: its hits + misses count
+    # all of the group's accesses, and no other tier counts more
+    n = int(g["n"])
+    for i in range(c.shape[0]):
+        reach = [int(c[i, 0, k, 0] + c[i, 0, k, 1]) for k in range(3)]
+        live = [r for r in reach if r]
+        assert live and live[0] == n and max(live) <= n
+
+
 def test_tiny_counts_recomputed_literally(oracle_mod):
     g = _gold("tiny")
     t = tg.recipe("tiny").to_trace()

@@ -23,7 +23,7 @@ from tracegen.digest import configs_digest, trace_digest
 pytestmark = pytest.mark.gpu
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-NAMES = ("tiny", "chat", "tenant")
+NAMES = ("tiny", "chat", "tenant", "longctx")
 FIELDS = ("hit", "miss", "ins", "evict", "hit_w", "miss_w", "ins_w", "evict_w")
 
 
