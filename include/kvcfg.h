@@ -256,6 +256,22 @@ kv_status kv_pareto(const double* obj, const uint32_t* segment, uint32_t n,
 kv_status kv_ttl_curves(const kv_trace* t, const double* ttl, uint32_t n_ttl, uint64_t* hits,
                         uint64_t* hitw, double* store, void* stream);
 
+/* kv_ttl_curves for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same arguments, checks and results, but the TTL values and the gap
+ * histograms live in a fixed per-device scratch array of the library (about
+ * 104 KiB, held by every device the library runs on until the process ends),
+ * so the call makes no hipMalloc, hipFree or other allocating call.
+ *   - At most 4096 histogram bins: n_groups * (n_ttl + 1) <= 4096 and
+ *     n_ttl <= 1024, else KV_ERR_UNSUPPORTED.
+ *   - ttl (host) is copied to the device through `stream`; keep it unchanged
+ *     until the stream has reached this call.
+ *   - Every call on one device shares that device's scratch array: calls
+ *     that overlap on one device (concurrent streams or threads) race and
+ *     must be serialised by the caller.  Each call clears what it needs. */
+kv_status kv_ttl_curves_noalloc(const kv_trace* t, const double* ttl, uint32_t n_ttl,
+                                uint64_t* hits, uint64_t* hitw, double* store, void* stream);
+
 /* Message describing the calling thread's most recent failure ("" if none). */
 const char* kv_last_error(void);
 

@@ -15,6 +15,8 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <mutex>
+#include <string>
 
 #include "kv_device.h"
 #include "kv_internal.h"
@@ -133,6 +135,53 @@ __global__ void k_ttl_fin(const unsigned long long* __restrict__ cnt,
 
 }  // namespace
 
+// The no-allocation variant's device memory: the TTL values, then the three
+// gap histograms (count, weight, weight * gap) of at most kTtlBins bins.
+// Each device holds its own copy for the life of the process; host code
+// reaches it only through the address hipGetSymbolAddress returns.
+constexpr size_t kScratchTtlBytes = (size_t)kTtlMax * sizeof(double);
+constexpr size_t kScratchBytes = kScratchTtlBytes + (size_t)kTtlBins * 3 * sizeof(uint64_t);
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+namespace {
+kv_status scratch_ptr(uint8_t** out) {
+  static std::mutex mu;
+  static void* per_dev[64] = {};
+  int d = 0;
+  KV_HIP(hipGetDevice(&d));
+  if (d < 0 || d >= 64) return fail(KV_ERR_DEVICE, "device index out of range");
+  std::lock_guard<std::mutex> lk(mu);
+  if (!per_dev[d]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) {
+      (void)hipGetLastError();
+      return fail(KV_ERR_DEVICE, std::string("kv_ttl_curves_noalloc: no address for the "
+                                             "scratch array: ") + hipGetErrorString(e));
+    }
+    per_dev[d] = p;
+  }
+  *out = static_cast<uint8_t*>(per_dev[d]);
+  return KV_OK;
+}
+}  // namespace
+
+kv_status ttl_curves_noalloc(Trace& t, const double* ttl_host, uint32_t n_ttl, uint64_t* hits,
+                             uint64_t* hitw, double* store, hipStream_t s) {
+  if (n_ttl > kTtlMax || (uint64_t)t.n_groups * (n_ttl + 1) > kTtlBins)
+    return fail(KV_ERR_UNSUPPORTED,
+                "kv_ttl_curves_noalloc: n_groups * (n_ttl + 1) must be <= 4096");
+  uint8_t* base = nullptr;
+  kv_status st;
+  if ((st = scratch_ptr(&base)) != KV_OK) return st;
+  double* ttl_dev = reinterpret_cast<double*>(base);
+  KV_HIP(hipMemcpyAsync(ttl_dev, ttl_host, (size_t)n_ttl * sizeof(double),
+                        hipMemcpyHostToDevice, s));
+  return ttl_curves_into(t, ttl_dev, n_ttl,
+                         reinterpret_cast<unsigned long long*>(base + kScratchTtlBytes), hits,
+                         hitw, store, s);
+}
+
 kv_status ttl_curves(Trace& t, const double* ttl_dev, uint32_t n_ttl, uint64_t* hits,
                      uint64_t* hitw, double* store, hipStream_t s) {
   const uint32_t G = t.n_groups;
@@ -142,7 +191,15 @@ kv_status ttl_curves(Trace& t, const double* ttl_dev, uint32_t n_ttl, uint64_t* 
   DevBuf& bh = t.ws[22];
   kv_status st;
   if ((st = bh.reserve((uint64_t)bins * 24)) != KV_OK) return st;
-  unsigned long long* cnt = bh.as<unsigned long long>();
+  return ttl_curves_into(t, ttl_dev, n_ttl, bh.as<unsigned long long>(), hits, hitw, store, s);
+}
+
+kv_status ttl_curves_into(Trace& t, const double* ttl_dev, uint32_t n_ttl,
+                          unsigned long long* cnt, uint64_t* hits, uint64_t* hitw,
+                          double* store, hipStream_t s) {
+  const uint32_t G = t.n_groups;
+  const uint32_t bins = G * (n_ttl + 1);
+  kv_status st;
   unsigned long long* wsum = cnt + bins;
   double* wd = reinterpret_cast<double*>(wsum + bins);
   StageTimer tm(kStTtl, s);

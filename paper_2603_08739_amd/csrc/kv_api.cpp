@@ -502,6 +502,24 @@ kv_status kv_ttl_curves(const kv_trace* h, const double* ttl, uint32_t n_ttl, ui
   return ttl_curves(*t, bt.as<double>(), n_ttl, hits, hitw, store, s);
 }
 
+kv_status kv_ttl_curves_noalloc(const kv_trace* h, const double* ttl, uint32_t n_ttl,
+                                uint64_t* hits, uint64_t* hitw, double* store, void* stream) {
+  if (!h) return fail(KV_ERR_INVALID, "kv_ttl_curves_noalloc: trace is NULL");
+  Trace* t = const_cast<Trace*>(reinterpret_cast<const Trace*>(h));
+  if (!is_live(t)) return fail(KV_ERR_INVALID, "kv_ttl_curves_noalloc: not a live trace handle");
+  if (kv_status e = check_device_error(*t, false, "kv_ttl_curves_noalloc")) return e;
+  if (!ttl || !hits || !hitw || !store)
+    return fail(KV_ERR_INVALID, "kv_ttl_curves_noalloc: ttl, hits, hitw and store are required");
+  if (n_ttl == 0) return fail(KV_ERR_INVALID, "kv_ttl_curves_noalloc: n_ttl must be >= 1");
+  for (uint32_t k = 0; k < n_ttl; ++k) {
+    if (!std::isfinite(ttl[k]) || ttl[k] < 0.0)
+      return fail(KV_ERR_INVALID, "kv_ttl_curves_noalloc: ttl values must be finite and >= 0");
+    if (k && ttl[k] < ttl[k - 1])
+      return fail(KV_ERR_INVALID, "kv_ttl_curves_noalloc: ttl values must be non-decreasing");
+  }
+  return ttl_curves_noalloc(*t, ttl, n_ttl, hits, hitw, store, (hipStream_t)stream);
+}
+
 kv_status kv_trace_free(kv_trace* h) {
   if (!h) return KV_OK;
   Trace* t = reinterpret_cast<Trace*>(h);

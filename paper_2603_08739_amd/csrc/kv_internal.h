@@ -182,6 +182,14 @@ kv_status pareto(const double* obj, const uint32_t* segment, uint32_t n, const d
 // thresholds on the device.
 kv_status ttl_curves(Trace& t, const double* ttl_dev, uint32_t n_ttl, uint64_t* hits,
                      uint64_t* hitw, double* store, hipStream_t s);
+// The same with the histograms at `hist` (3 * n_groups * (n_ttl + 1) words).
+kv_status ttl_curves_into(Trace& t, const double* ttl_dev, uint32_t n_ttl,
+                          unsigned long long* hist, uint64_t* hits, uint64_t* hitw,
+                          double* store, hipStream_t s);
+// The same in the library's per-device scratch array (no allocation); the
+// TTL values are copied from the host through the stream.
+kv_status ttl_curves_noalloc(Trace& t, const double* ttl_host, uint32_t n_ttl, uint64_t* hits,
+                             uint64_t* hitw, double* store, hipStream_t s);
 
 // Reports (and clears) a replay failure recorded on the device by an earlier
 // kv_eval_configs call on `t`: with `wait`, waits for that call's error

@@ -88,6 +88,8 @@ def _load():
     lib.kv_pareto.argtypes = [_vp, _vp, _u32, _vp, _vp, ctypes.POINTER(_u32), _vp]
     lib.kv_ttl_curves.restype = ctypes.c_int
     lib.kv_ttl_curves.argtypes = [_vp, _vp, _u32, _vp, _vp, _vp, _vp]
+    lib.kv_ttl_curves_noalloc.restype = ctypes.c_int
+    lib.kv_ttl_curves_noalloc.argtypes = [_vp, _vp, _u32, _vp, _vp, _vp, _vp]
     lib.kv_last_error.restype = ctypes.c_char_p
     lib.kv_last_error.argtypes = []
     lib.kv_timing_enable.restype = ctypes.c_int
@@ -99,7 +101,8 @@ def _load():
 
 LIB = _load()
 EXPORTS = ("kv_trace_load", "kv_trace_free", "kv_trace_info", "kv_eval_configs", "kv_pareto",
-           "kv_ttl_curves", "kv_last_error", "kv_timing_enable", "kv_timing_read")
+           "kv_ttl_curves", "kv_ttl_curves_noalloc", "kv_last_error", "kv_timing_enable",
+           "kv_timing_read")
 
 
 def kv_timing_enable(on: bool = True):
@@ -284,3 +287,18 @@ def kv_ttl_curves(trace: Trace, ttl, hits, hitw, store, stream=None):
     _check(LIB.kv_ttl_curves(trace.handle, ctypes.cast(arr, _vp), len(vals), ph, pw, pst,
                              _stream(stream)))
 
+
+def kv_ttl_curves_noalloc(trace: Trace, ttl, hits, hitw, store, stream=None):
+    """kv_ttl_curves without device allocation (the library's scratch array);
+    the TTL values are staged in a host array that lives until the stream
+    has completed the call."""
+    i64, _, _, f64 = _dt()
+    vals = [float(x) for x in ttl]
+    arr = (ctypes.c_double * max(len(vals), 1))(*vals)
+    m = trace.n_groups * len(vals)
+    ph = _dev(hits, "hits", i64, m)
+    pw = _dev(hitw, "hitw", i64, m)
+    pst = _dev(store, "store", f64, m)
+    _check(LIB.kv_ttl_curves_noalloc(trace.handle, ctypes.cast(arr, _vp), len(vals), ph, pw, pst,
+                                     _stream(stream)))
+    return arr

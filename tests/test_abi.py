@@ -19,6 +19,7 @@ def declared_functions():
 def test_header_declares_the_boundary():
     assert declared_functions() == sorted(["kv_trace_load", "kv_trace_free", "kv_trace_info",
                                            "kv_eval_configs", "kv_pareto", "kv_ttl_curves",
+                                           "kv_ttl_curves_noalloc",
                                            "kv_last_error", "kv_timing_enable",
                                            "kv_timing_read"])
 
