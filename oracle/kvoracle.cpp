@@ -198,6 +198,80 @@ Tier* make_tier(int policy, uint64_t cap) {
   return new LfuTier(cap);
 }
 
+// The disk TTL tier: a block is held for ttl[g] seconds after each of its
+// accesses (g = the block's group); with a capacity it is also evicted least
+// recently accessed first when full (then every group has the same ttl, so
+// blocks also expire in that order).  Expired blocks are dropped by
+// expire(now) before each lookup.  The tier integrates its occupancy:
+// every residency adds weight x (its last access + ttl - its insertion).
+struct TtlSpec {
+  const double* ttl;       // [kMaxGroups] seconds, by group
+  const double* req_time;  // request times
+  const std::vector<Block>* acc;
+};
+
+class TtlTier : public Tier {
+ public:
+  TtlTier(uint64_t cap, const TtlSpec& s, uint32_t n_groups)
+      : Tier(cap ? cap : ~0ull), bounded_(cap != 0), s_(s), lists_(cap ? 1 : n_groups) {}
+  bool contains(uint64_t h) const override { return pos_.count(h) != 0; }
+  void hit(uint64_t h, uint64_t t) override {
+    auto it = pos_.at(h);
+    it->last = time_of(t);
+    auto& l = lists_[list_of(it->b)];
+    l.splice(l.begin(), l, it);
+  }
+  template <class F>
+  void expire(double now, F&& ev) {
+    for (size_t l = 0; l < lists_.size(); ++l) {
+      auto& lst = lists_[l];
+      while (!lst.empty()) {
+        const Entry& e = lst.back();
+        const double ttl = s_.ttl[bounded_ ? 0 : l];
+        if (!(e.last + ttl < now)) break;
+        store_ += (double)e.b.w * ((e.last + ttl) - e.since);
+        used_ -= e.b.w;
+        ev(e.b);
+        pos_.erase(e.b.hash);
+        lst.pop_back();
+      }
+    }
+  }
+  // occupancy of the blocks still held, each until its last access + ttl
+  double finish() {
+    for (size_t l = 0; l < lists_.size(); ++l)
+      for (const Entry& e : lists_[l])
+        store_ += (double)e.b.w * ((e.last + s_.ttl[bounded_ ? 0 : l]) - e.since);
+    return store_;
+  }
+
+ protected:
+  struct Entry {
+    Block b;
+    double last, since;  // latest access, insertion (seconds)
+  };
+  double time_of(uint64_t t) const { return s_.req_time[(*s_.acc)[t].req]; }
+  size_t list_of(const Block& b) const { return bounded_ ? 0 : b.g; }
+  Block pop_victim() override {
+    auto& lst = lists_[0];  // bounded: one list, least recent at the back
+    Entry e = lst.back();
+    lst.pop_back();
+    pos_.erase(e.b.hash);
+    return e.b;
+  }
+  void push(const Block& b, uint64_t t) override {
+    const double now = time_of(t);
+    auto& l = lists_[list_of(b)];
+    l.push_front(Entry{b, now, now});
+    pos_[b.hash] = l.begin();
+  }
+  bool bounded_;
+  TtlSpec s_;
+  std::vector<std::list<Entry>> lists_;
+  std::unordered_map<uint64_t, std::list<Entry>::iterator> pos_;
+  double store_ = 0.0;
+};
+
 void add(Counts& c, uint32_t g, int k, Field f, uint64_t cnt_field_weight) {
   c.v[g][k][f] += cnt_field_weight;
 }
@@ -206,10 +280,14 @@ void add(Counts& c, uint32_t g, int k, Field f, uint64_t cnt_field_weight) {
 // block is available from a tier only while its request's earlier blocks
 // were.
 void replay_inclusive(const std::vector<Block>& acc, const std::vector<uint32_t>& idx,
-                      const uint64_t cap[kTiers], int policy, bool prefix, Counts& out) {
+                      const uint64_t cap[kTiers], int policy, bool prefix, Counts& out,
+                      const TtlSpec* ttl = nullptr, uint32_t n_groups = 1,
+                      double* store = nullptr) {
   Tier* tier[kTiers] = {nullptr, nullptr, nullptr};
+  TtlTier* tt = nullptr;
   for (int k = 0; k < kTiers; ++k)
-    if (cap[k] > 0) tier[k] = make_tier(policy, cap[k]);
+    if (cap[k] > 0 && !(k == 2 && ttl)) tier[k] = make_tier(policy, cap[k]);
+  if (ttl) tier[2] = tt = new TtlTier(cap[2], *ttl, n_groups);
   bool run[kTiers] = {false, false, false};  // the request's blocks so far all available
   bool first = true;
   uint32_t cur_req = 0;
@@ -220,6 +298,11 @@ void replay_inclusive(const std::vector<Block>& acc, const std::vector<uint32_t>
       cur_req = b.req;
       first = false;
     }
+    if (tt)
+      tt->expire(ttl->req_time[b.req], [&](const Block& v) {
+        add(out, v.g, 2, F_EVICT, 1);
+        add(out, v.g, 2, F_EVICT_W, v.w);
+      });
     bool present[kTiers] = {false, false, false};
     int served = -1;
     for (int k = 0; k < kTiers; ++k) {
@@ -252,6 +335,10 @@ void replay_inclusive(const std::vector<Block>& acc, const std::vector<uint32_t>
         });
       }
     }
+  }
+  if (tt && store) {
+    const double s = tt->finish();
+    if (cap[2] == 0) *store += s;  // an unbounded tier is billed by occupancy
   }
   for (int k = 0; k < kTiers; ++k) delete tier[k];
 }
@@ -325,12 +412,37 @@ struct ConfigView {
   uint8_t mode;
   uint8_t partitioned;
   const uint8_t* policy;  // [16]
+  uint8_t disk_ttl;       // tier 2 is a TTL tier
+  const double* ttl;      // [16] seconds by group
 };
+
+// A disk TTL tier is supported in the inclusive LRU shared mode; a bounded
+// one needs the same ttl in every group.  0, -1 (invalid) or -4.
+int check_ttl(const ConfigView& c, uint32_t n_groups) {
+  if (!c.disk_ttl) return 0;
+  if (c.disk_ttl > 1) return -1;
+  for (uint32_t g = 0; g < n_groups; ++g)
+    if (!std::isfinite(c.ttl[g]) || c.ttl[g] < 0) return -1;
+  if (c.mode != M_INCLUSIVE || c.partitioned || c.policy[0] != P_LRU) return -4;
+  if (c.cap[2])
+    for (uint32_t g = 1; g < n_groups; ++g)
+      if (c.ttl[g] != c.ttl[0]) return -4;
+  return 0;
+}
 
 int replay_one(const std::vector<Block>& acc, const std::vector<std::vector<uint32_t>>& by_group,
                const std::vector<uint32_t>& all, uint32_t n_groups, uint32_t w_max,
-               const ConfigView& c, Counts& out) {
+               const ConfigView& c, Counts& out, const double* req_time = nullptr,
+               double* store = nullptr) {
   auto bad_cap = [&](uint64_t x) { return x > 0 && x < w_max; };
+  if (const int rc = check_ttl(c, n_groups)) return rc;
+  if (c.disk_ttl) {
+    for (int k = 0; k < kTiers; ++k)
+      if (bad_cap(c.cap[k])) return -1;
+    const TtlSpec spec{c.ttl, req_time, &acc};
+    replay_inclusive(acc, all, c.cap, P_LRU, false, out, &spec, n_groups, store);
+    return 0;
+  }
   if (c.partitioned) {
     for (uint32_t g = 0; g < n_groups; ++g) {
       uint64_t cg[kTiers];
@@ -373,19 +485,29 @@ int replay_one(const std::vector<Block>& acc, const std::vector<std::vector<uint
 // ---------------------------------------------------------------------------
 struct MemoJob {
   uint32_t part;    // index into the partition lists (group g, or n_groups = shared)
-  int policy;
+  int policy;       // P_*, or -1 for a disk TTL tier
   uint64_t cap;
+  double ttl[kMaxGroups] = {};  // TTL tier: seconds by group
+  double store = 0.0;           // TTL tier: occupancy integral (unbounded)
   std::vector<uint64_t> bits;  // presence before the access, one bit per list entry
   uint64_t ins[kMaxGroups] = {}, ins_w[kMaxGroups] = {}, ev[kMaxGroups] = {}, ev_w[kMaxGroups] = {};
 };
 
-void memo_run(const std::vector<Block>& acc, const std::vector<uint32_t>& idx, MemoJob& j) {
-  Tier* t = make_tier(j.policy, j.cap);
+void memo_run(const std::vector<Block>& acc, const std::vector<uint32_t>& idx, MemoJob& j,
+              const double* req_time, uint32_t n_groups) {
+  TtlTier* tt = nullptr;
+  TtlSpec spec{j.ttl, req_time, &acc};
+  Tier* t = j.policy < 0 ? (tt = new TtlTier(j.cap, spec, n_groups)) : make_tier(j.policy, j.cap);
   j.bits.assign((idx.size() + 63) / 64, 0);
   for (int g = 0; g < kMaxGroups; ++g) j.ins[g] = j.ins_w[g] = j.ev[g] = j.ev_w[g] = 0;
   for (size_t q = 0; q < idx.size(); ++q) {
     const uint32_t i = idx[q];
     const Block& b = acc[i];
+    if (tt)
+      tt->expire(req_time[b.req], [&](const Block& v) {
+        j.ev[v.g] += 1;
+        j.ev_w[v.g] += v.w;
+      });
     if (t->contains(b.hash)) {
       j.bits[q >> 6] |= 1ull << (q & 63);
       t->hit(b.hash, i);
@@ -397,6 +519,10 @@ void memo_run(const std::vector<Block>& acc, const std::vector<uint32_t>& idx, M
         j.ev_w[v.g] += v.w;
       });
     }
+  }
+  if (tt) {
+    const double st = tt->finish();
+    j.store = j.cap == 0 ? st : 0.0;
   }
   delete t;
 }
@@ -498,7 +624,8 @@ extern "C" {
 int oracle_replay(uint64_t n, const uint64_t* hash, const uint8_t* group, const uint8_t* weight,
                   const uint32_t* req, uint32_t n_groups, uint32_t n_cfg, const uint64_t* cap,
                   const uint64_t* cap_group, const uint8_t* mode, const uint8_t* partitioned,
-                  const uint8_t* policy, uint32_t n_threads, uint64_t* counts) {
+                  const uint8_t* policy, const uint8_t* disk_ttl, const double* ttl,
+                  const double* req_time, uint32_t n_threads, uint64_t* counts, double* store) {
   if (n_groups < 1 || n_groups > (uint32_t)kMaxGroups) return -2;
   std::vector<Block> acc(n);
   std::vector<std::vector<uint32_t>> by_group(n_groups);
@@ -522,9 +649,12 @@ int oracle_replay(uint64_t n, const uint64_t* hash, const uint8_t* group, const 
       if (j >= n_cfg) break;
       std::fill(&c->v[0][0][0], &c->v[0][0][0] + kMaxGroups * kTiers * kFields, 0);
       ConfigView v{cap + 3 * (size_t)j, cap_group + 3 * kMaxGroups * (size_t)j, mode[j],
-                   partitioned[j], policy + kMaxGroups * (size_t)j};
-      int rc = replay_one(acc, by_group, all, n_groups, w_max, v, *c);
+                   partitioned[j], policy + kMaxGroups * (size_t)j, disk_ttl[j],
+                   ttl + kMaxGroups * (size_t)j};
+      double st = 0.0;
+      int rc = replay_one(acc, by_group, all, n_groups, w_max, v, *c, req_time, &st);
       if (rc != 0) status.store(rc);
+      store[j] = st;
       uint64_t* dst = counts + (size_t)j * n_groups * kTiers * kFields;
       for (uint32_t g = 0; g < n_groups; ++g)
         for (int k = 0; k < kTiers; ++k)
@@ -542,21 +672,27 @@ int oracle_replay(uint64_t n, const uint64_t* hash, const uint8_t* group, const 
 
 // Objectives per configuration (cost, throughput, latency), all fp64, each
 // step in the order written.  cost_model: [price_gpu_per_hour, price_gib_hour[3],
-// bw_dram, ssd_bw_base, ssd_bw_per_gib, ssd_bw_max, t_prefill_per_token].
+// bw_dram, ssd_bw_base, ssd_bw_per_gib, ssd_bw_max, t_prefill_per_token,
+// n_media, then per medium (price_gib_hour, bw_base, bw_per_gib, bw_max)].
 // The counts enter as granule totals over groups: H_w[k] = sum_g hit_w,
 // I_w2 = sum_g ins_w of the SSD tier; recompute R_w = N_w - sum_k H_w[k].
-//   capGiB[k] = cap[k] * gb / 2^30
-//   bw_ssd    = min(ssd_bw_base + ssd_bw_per_gib * capGiB[2], ssd_bw_max)
+//   capGiB[k] = cap[k] * gb / 2^30, except an unbounded disk TTL tier:
+//               capGiB[2] = (store * gb / 2^30) / span (mean occupancy; 0 if span = 0)
+//   (p2, base, per_gib, max) = the disk's price and bandwidth terms, from
+//               media[medium] when n_media > 0
+//   bw_ssd    = min(base + per_gib * capGiB[2], max)
 //   t_dram    = H_w[1] * gb / bw_dram
 //   t_ssd     = (H_w[2] + I_w2) * gb / bw_ssd
 //   t_rec     = R_w * tpg * t_prefill_per_token
 //   T_busy    = t_rec + t_dram + t_ssd;   T_wall = max(span, T_busy)
 //   throughput = N_w * tpg / T_wall;      latency = T_busy / n_req
-//   cost = (price_gpu + sum_k capGiB[k] * price_k) * T_wall / 3600
+//   cost = (price_gpu + capGiB[0] * p0 + capGiB[1] * p1 + capGiB[2] * p2) * T_wall / 3600
 int oracle_objectives(uint32_t n_cfg, const uint64_t* cap, const uint64_t* counts,
                       uint32_t n_groups, const double* cm, double gb, double tpg,
-                      double span, double n_req, uint64_t n_w, double* obj) {
+                      double span, double n_req, uint64_t n_w, const uint8_t* disk_ttl,
+                      const uint8_t* medium, const double* store, double* obj) {
   const double kGiB = 1073741824.0;
+  const uint32_t n_media = (uint32_t)cm[9];
   for (uint32_t j = 0; j < n_cfg; ++j) {
     const uint64_t* c = counts + (size_t)j * n_groups * kTiers * kFields;
     uint64_t hw[kTiers] = {0, 0, 0};
@@ -568,7 +704,17 @@ int oracle_objectives(uint32_t n_cfg, const uint64_t* cap, const uint64_t* count
     uint64_t rw = n_w - (hw[0] + hw[1] + hw[2]);
     double capgib[kTiers];
     for (int k = 0; k < kTiers; ++k) capgib[k] = ((double)cap[3 * (size_t)j + k] * gb) / kGiB;
-    double bw_ssd = std::min(cm[5] + cm[6] * capgib[2], cm[7]);
+    if (disk_ttl[j] && cap[3 * (size_t)j + 2] == 0)
+      capgib[2] = span > 0 ? ((store[j] * gb) / kGiB) / span : 0.0;
+    double p2 = cm[3], base = cm[5], per_gib = cm[6], bmax = cm[7];
+    if (n_media) {
+      const double* md = cm + 10 + 4 * (size_t)medium[j];
+      p2 = md[0];
+      base = md[1];
+      per_gib = md[2];
+      bmax = md[3];
+    }
+    double bw_ssd = std::min(base + per_gib * capgib[2], bmax);
     double t_dram = ((double)hw[1] * gb) / cm[4];
     double t_ssd = ((double)(hw[2] + iw2) * gb) / bw_ssd;
     double t_rec = ((double)rw * tpg) * cm[8];
@@ -576,7 +722,7 @@ int oracle_objectives(uint32_t n_cfg, const uint64_t* cap, const uint64_t* count
     double t_wall = std::max(span, t_busy);
     double thr = ((double)n_w * tpg) / t_wall;
     double lat = t_busy / n_req;
-    double cost = (((cm[0] + capgib[0] * cm[1]) + capgib[1] * cm[2]) + capgib[2] * cm[3]) *
+    double cost = (((cm[0] + capgib[0] * cm[1]) + capgib[1] * cm[2]) + capgib[2] * p2) *
                   (t_wall / 3600.0);
     obj[3 * (size_t)j + 0] = cost;
     obj[3 * (size_t)j + 1] = thr;
@@ -635,7 +781,8 @@ int oracle_replay_memo(uint64_t n, const uint64_t* hash, const uint8_t* group,
                        const uint8_t* weight, const uint32_t* req, uint32_t n_groups,
                        uint32_t n_cfg, const uint64_t* cap, const uint64_t* cap_group,
                        const uint8_t* mode, const uint8_t* partitioned, const uint8_t* policy,
-                       uint32_t n_threads, uint64_t* counts) {
+                       const uint8_t* disk_ttl, const double* ttl, const double* req_time,
+                       uint32_t n_threads, uint64_t* counts, double* store) {
   if (n_groups < 1 || n_groups > (uint32_t)kMaxGroups) return -2;
   std::vector<Block> acc(n);
   // partition lists: [g] = group g's accesses, [n_groups] = every access
@@ -658,28 +805,33 @@ int oracle_replay_memo(uint64_t n, const uint64_t* hash, const uint8_t* group,
 
   // plan: distinct (partition, policy, capacity) caches of the inclusive configs
   std::vector<MemoJob> jobs;
-  std::vector<std::tuple<uint32_t, int, uint64_t>> keys;
   // per config and partition, the job of each tier (-1 absent)
   std::vector<std::vector<std::array<int64_t, kTiers>>> use(n_cfg);
   std::vector<uint8_t> literal(n_cfg, 0);
-  auto job_of = [&](uint32_t part, int pol, uint64_t c) -> int64_t {
-    const auto key = std::make_tuple(part, pol, c);
-    for (size_t q = 0; q < keys.size(); ++q)
-      if (keys[q] == key) return (int64_t)q;
-    keys.push_back(key);
+  auto job_of = [&](uint32_t part, int pol, uint64_t c, const double* tl) -> int64_t {
+    for (size_t q = 0; q < jobs.size(); ++q) {
+      const MemoJob& j = jobs[q];
+      if (j.part != part || j.policy != pol || j.cap != c) continue;
+      if (pol < 0 && !std::equal(j.ttl, j.ttl + n_groups, tl)) continue;
+      return (int64_t)q;
+    }
     MemoJob j;
     j.part = part;
     j.policy = pol;
     j.cap = c;
+    if (pol < 0) std::copy(tl, tl + n_groups, j.ttl);
     jobs.push_back(std::move(j));
-    return (int64_t)keys.size() - 1;
+    return (int64_t)jobs.size() - 1;
   };
   for (uint32_t c = 0; c < n_cfg; ++c) {
     const uint64_t* cp = cap + 3 * (size_t)c;
     const uint64_t* cg = cap_group + 3 * kMaxGroups * (size_t)c;
     const uint8_t* pol = policy + kMaxGroups * (size_t)c;
+    const double* tl = ttl + kMaxGroups * (size_t)c;
     for (int k = 0; k < kTiers; ++k)
       if (bad_cap(cp[k])) return -1;
+    const ConfigView cv{cp, cg, mode[c], partitioned[c], pol, disk_ttl[c], tl};
+    if (const int rc = check_ttl(cv, n_groups)) return rc;
     if (mode[c] != M_INCLUSIVE) {
       literal[c] = 1;
       continue;
@@ -690,21 +842,23 @@ int oracle_replay_memo(uint64_t n, const uint64_t* hash, const uint8_t* group,
         for (int k = 0; k < kTiers; ++k) {
           const uint64_t x = cg[k * kMaxGroups + g];
           if (bad_cap(x)) return -1;
-          if (x) t[k] = job_of(g, pol[g], x);
+          if (x) t[k] = job_of(g, pol[g], x, nullptr);
         }
         use[c].push_back(t);
       }
     } else {
       std::array<int64_t, kTiers> t{-1, -1, -1};
       for (int k = 0; k < kTiers; ++k)
-        if (cp[k]) t[k] = job_of(all_list, pol[0], cp[k]);
+        if (cp[k] && !(k == 2 && disk_ttl[c])) t[k] = job_of(all_list, pol[0], cp[k], nullptr);
+      if (disk_ttl[c]) t[2] = job_of(all_list, -1, cp[2], tl);
       use[c].push_back(t);
     }
   }
 
   // replay every distinct cache once
-  parallel_for((uint32_t)jobs.size(), n_threads,
-               [&](uint32_t q) { memo_run(acc, lists[jobs[q].part], jobs[q]); });
+  parallel_for((uint32_t)jobs.size(), n_threads, [&](uint32_t q) {
+    memo_run(acc, lists[jobs[q].part], jobs[q], req_time, n_groups);
+  });
   std::vector<ListMasks> masks(n_groups + 1);
   parallel_for(n_groups + 1, n_threads, [&](uint32_t p) {
     if (p == 0 || p < n_groups || p == all_list) build_masks(acc, lists[p], n_groups, masks[p]);
@@ -715,11 +869,13 @@ int oracle_replay_memo(uint64_t n, const uint64_t* hash, const uint8_t* group,
   parallel_for(n_cfg, n_threads, [&](uint32_t c) {
     Counts* out = new Counts;
     std::fill(&out->v[0][0][0], &out->v[0][0][0] + kMaxGroups * kTiers * kFields, 0);
+    store[c] = 0.0;
     if (literal[c]) {
       ConfigView v{cap + 3 * (size_t)c, cap_group + 3 * kMaxGroups * (size_t)c, mode[c],
-                   partitioned[c], policy + kMaxGroups * (size_t)c};
+                   partitioned[c], policy + kMaxGroups * (size_t)c, disk_ttl[c],
+                   ttl + kMaxGroups * (size_t)c};
       const int rc = replay_one(acc, n_groups > 1 ? by_group : lists, lists[all_list], n_groups,
-                                w_max, v, *out);
+                                w_max, v, *out, req_time, &store[c]);
       if (rc != 0) status.store(rc);
     } else {
       for (size_t u = 0; u < use[c].size(); ++u) {
@@ -727,6 +883,7 @@ int oracle_replay_memo(uint64_t n, const uint64_t* hash, const uint8_t* group,
         const MemoJob* t[kTiers];
         for (int k = 0; k < kTiers; ++k) t[k] = use[c][u][k] >= 0 ? &jobs[use[c][u][k]] : nullptr;
         memo_classify(masks[part], n_groups, t, *out);
+        if (disk_ttl[c] && t[2]) store[c] += t[2]->store;
       }
     }
     uint64_t* dst = counts + (size_t)c * n_groups * kTiers * kFields;

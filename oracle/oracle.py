@@ -55,13 +55,14 @@ def _load():
         p = ctypes.c_void_p
         lib.oracle_replay.restype = ctypes.c_int
         lib.oracle_replay.argtypes = [ctypes.c_uint64, p, p, p, p, ctypes.c_uint32,
-                                      ctypes.c_uint32, p, p, p, p, p, ctypes.c_uint32, p]
+                                      ctypes.c_uint32, p, p, p, p, p, p, p, p,
+                                      ctypes.c_uint32, p, p]
         lib.oracle_replay_memo.restype = ctypes.c_int
         lib.oracle_replay_memo.argtypes = lib.oracle_replay.argtypes
         lib.oracle_objectives.restype = ctypes.c_int
         lib.oracle_objectives.argtypes = [ctypes.c_uint32, p, p, ctypes.c_uint32, p,
                                           ctypes.c_double, ctypes.c_double, ctypes.c_double,
-                                          ctypes.c_double, ctypes.c_uint64, p]
+                                          ctypes.c_double, ctypes.c_uint64, p, p, p, p]
         lib.oracle_pareto.restype = ctypes.c_int64
         lib.oracle_pareto.argtypes = [ctypes.c_uint32, p, p, p, p]
         _lib = lib
@@ -76,7 +77,8 @@ def default_threads() -> int:
     return max(1, len(os.sched_getaffinity(0)))
 
 
-def replay(trace, cfgs, threads: int | None = None, memo: bool = False) -> np.ndarray:
+def replay(trace, cfgs, threads: int | None = None, memo: bool = False,
+           with_store: bool = False):
     """Literal replay of every configuration of ``cfgs`` over ``trace``.
 
     With ``memo`` the inclusive configurations share their tier caches: an
@@ -84,7 +86,10 @@ def replay(trace, cfgs, threads: int | None = None, memo: bool = False) -> np.nd
     partition, so each distinct (partition, policy, capacity) cache is
     replayed once, literally, with a presence bit per access, and every
     configuration is classified from its tiers' bits (served by k = present
-    in k and in no faster present tier).  The results are the same."""
+    in k and in no faster present tier).  The results are the same.
+
+    With ``with_store`` also returns, per configuration, the occupancy
+    integral (granule-seconds) of an unbounded disk TTL tier (0 otherwise)."""
     lib = _load()
     n_cfg = cfgs.n
     g = trace.n_groups
@@ -98,13 +103,17 @@ def replay(trace, cfgs, threads: int | None = None, memo: bool = False) -> np.nd
     part = np.ascontiguousarray(cfgs.partitioned, dtype=np.uint8)
     pol = np.ascontiguousarray(cfgs.policy, dtype=np.uint8)
     rq = np.ascontiguousarray(trace.req, dtype=np.uint32)
+    dt = np.ascontiguousarray(cfgs.disk_ttl, dtype=np.uint8)
+    tl = np.ascontiguousarray(cfgs.ttl, dtype=np.float64)
+    rt = np.ascontiguousarray(trace.req_time, dtype=np.float64)
+    store = np.zeros(n_cfg, dtype=np.float64)
     fn = lib.oracle_replay_memo if memo else lib.oracle_replay
     rc = fn(trace.n, _ptr(h), _ptr(gr), _ptr(w), _ptr(rq), g, n_cfg, _ptr(cap), _ptr(cg),
-                           _ptr(mode), _ptr(part), _ptr(pol),
-                           threads or default_threads(), _ptr(out))
+            _ptr(mode), _ptr(part), _ptr(pol), _ptr(dt), _ptr(tl), _ptr(rt),
+            threads or default_threads(), _ptr(out), _ptr(store))
     if rc != 0:
         raise ValueError(f"oracle_replay rejected the batch (code {rc})")
-    return out
+    return (out, store) if with_store else out
 
 
 def replay_memo(trace, cfgs, threads: int | None = None) -> np.ndarray:
@@ -112,13 +121,27 @@ def replay_memo(trace, cfgs, threads: int | None = None) -> np.ndarray:
 
 
 def cost_vector(cost: dict) -> np.ndarray:
-    return np.array([cost["price_gpu_per_hour"], *cost["price_per_gib_hour"],
-                     cost["bw_dram"], cost["ssd_bw_base"], cost["ssd_bw_per_gib"],
-                     cost["ssd_bw_max"], cost["t_prefill_per_token"]], dtype=np.float64)
+    media = list(cost.get("media", ()))
+    v = [cost["price_gpu_per_hour"], *cost["price_per_gib_hour"], cost["bw_dram"],
+         cost["ssd_bw_base"], cost["ssd_bw_per_gib"], cost["ssd_bw_max"],
+         cost["t_prefill_per_token"], float(len(media))]
+    for m in media:
+        v.extend(float(x) for x in m)
+    return np.array(v, dtype=np.float64)
 
 
-def objectives(trace, cfgs, counts, cost: dict) -> np.ndarray:
+def objectives(trace, cfgs, counts, cost: dict, store=None) -> np.ndarray:
+    """(cost, throughput, latency) per configuration.  ``store`` is the
+    occupancy integral of unbounded disk TTL tiers (from ``replay(...,
+    with_store=True)``); when omitted and needed it is replayed here."""
     lib = _load()
+    need = (np.asarray(cfgs.disk_ttl) != 0) & (np.asarray(cfgs.cap)[:, 2] == 0)
+    if store is None:
+        store = np.zeros(cfgs.n, dtype=np.float64)
+        if need.any():
+            sub = cfgs.subset(np.nonzero(need)[0])
+            store[need] = replay(trace, sub, memo=True, with_store=True)[1]
+    store = np.ascontiguousarray(store, dtype=np.float64)
     n_cfg = cfgs.n
     obj = np.zeros((n_cfg, 3), dtype=np.float64)
     cap = np.ascontiguousarray(cfgs.cap, dtype=np.uint64)
@@ -126,9 +149,12 @@ def objectives(trace, cfgs, counts, cost: dict) -> np.ndarray:
     cm = cost_vector(cost)
     n_w = int(trace.weight.astype(np.uint64).sum())
     span = float(trace.req_time[-1] - trace.req_time[0])
+    dt = np.ascontiguousarray(cfgs.disk_ttl, dtype=np.uint8)
+    md = np.ascontiguousarray(cfgs.medium, dtype=np.uint8)
     lib.oracle_objectives(n_cfg, _ptr(cap), _ptr(cnt), trace.n_groups, _ptr(cm),
                           float(trace.granule_bytes), float(trace.tokens_per_granule),
-                          span, float(trace.n_req), n_w, _ptr(obj))
+                          span, float(trace.n_req), n_w, _ptr(dt), _ptr(md), _ptr(store),
+                          _ptr(obj))
     return obj
 
 

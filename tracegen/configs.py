@@ -39,6 +39,10 @@ GIB = 1 << 30
 TIB = 1 << 40
 
 
+_FIELDS = ("cap", "cap_group", "mode", "partitioned", "policy", "segment", "disk_ttl",
+           "medium", "ttl")
+
+
 @dataclass
 class ConfigBatch:
     cap: np.ndarray          # uint64[n,3] granules per tier (0 = absent)
@@ -47,6 +51,18 @@ class ConfigBatch:
     partitioned: np.ndarray  # uint8[n]
     policy: np.ndarray       # uint8[n,16]
     segment: np.ndarray      # uint32[n] Pareto segment id
+    disk_ttl: np.ndarray = None  # uint8[n]: 1 = the disk tier is a TTL tier
+    medium: np.ndarray = None    # uint8[n]: disk medium index of the cost model
+    ttl: np.ndarray = None       # float64[n,16]: disk TTL (s) by the block's group
+
+    def __post_init__(self):
+        n = self.cap.shape[0]
+        if self.disk_ttl is None:
+            self.disk_ttl = np.zeros(n, np.uint8)
+        if self.medium is None:
+            self.medium = np.zeros(n, np.uint8)
+        if self.ttl is None:
+            self.ttl = np.zeros((n, MAX_GROUPS), np.float64)
 
     @property
     def n(self) -> int:
@@ -54,15 +70,11 @@ class ConfigBatch:
 
     def subset(self, idx) -> "ConfigBatch":
         idx = np.asarray(idx)
-        return ConfigBatch(self.cap[idx].copy(), self.cap_group[idx].copy(),
-                           self.mode[idx].copy(), self.partitioned[idx].copy(),
-                           self.policy[idx].copy(), self.segment[idx].copy())
+        return ConfigBatch(*[getattr(self, f)[idx].copy() for f in _FIELDS])
 
     @staticmethod
     def concat(parts) -> "ConfigBatch":
-        return ConfigBatch(*[np.concatenate([getattr(p, f) for p in parts])
-                             for f in ("cap", "cap_group", "mode", "partitioned",
-                                       "policy", "segment")])
+        return ConfigBatch(*[np.concatenate([getattr(p, f) for p in parts]) for f in _FIELDS])
 
 
 def empty(n: int) -> ConfigBatch:
@@ -90,6 +102,15 @@ def from_list(items) -> ConfigBatch:
             cg = np.asarray(it["cap_group"], dtype=np.uint64)
             b.cap_group[i, :, :cg.shape[1]] = cg
         b.segment[i] = it.get("segment", 0)
+        if "ttl" in it:
+            b.disk_ttl[i] = 1
+            t = it["ttl"]
+            if np.isscalar(t):
+                b.ttl[i, :] = float(t)
+            else:
+                t = np.asarray(t, dtype=np.float64)
+                b.ttl[i, :len(t)] = t
+        b.medium[i] = it.get("medium", 0)
     return b
 
 
