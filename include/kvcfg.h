@@ -140,8 +140,44 @@ typedef struct kv_config {
                                         policy[0]; 1: group g owns cap_group[k][g]
                                         of tier k and uses policy[g]          */
   uint8_t policy[KV_MAX_GROUPS];     /* KV_POLICY_* (same policy on every tier) */
-  uint8_t reserved[6];               /* must be 0                             */
+  uint8_t disk_ttl;                  /* 1: tier 2 (disk) is a TTL tier (below);
+                                        0: an ordinary capacity tier           */
+  uint8_t medium;                    /* disk medium: index into the cost model's
+                                        media (0 when it has none)            */
+  uint8_t reserved[4];               /* must be 0                             */
+  double ttl[KV_MAX_GROUPS];         /* disk TTL tier: seconds a block stays on
+                                        disk after each access, by the block's
+                                        group (shared configurations too)     */
 } kv_config;
+
+/* The disk TTL tier (Section 4.1 planner: a TTL for KV blocks on disk;
+ * Section 4.3: a block is kept for the TTL after each access).  With
+ * disk_ttl = 1, tier 2 holds a block while the time since its latest access
+ * is at most ttl[g] (g = the block's group; a re-access at a gap delta hits
+ * iff delta <= ttl[g]):
+ *   - cap[2] == 0: unbounded; the tier's storage is billed as its mean
+ *     occupancy over the trace span, S / span granules, where S is the
+ *     storage-time integral sum over blocks of w_b * (ttl + sum of
+ *     min(ttl, gap) over the block's re-access gaps) (C_g(t) of Section 4.3);
+ *   - cap[2] > 0: also bounded by cap[2] granules, least recently accessed
+ *     block first (with one TTL the blocks expire in that order too), billed
+ *     as provisioned capacity; every group needs the same ttl.
+ * Its records: hit / miss as for any tier; ins = accesses that found the
+ * block absent from the tier (it is written again); evict = blocks that left
+ * the tier before the trace's last access (expired or displaced), i.e. ins
+ * minus the blocks still held at the time of the last access's request.
+ * Requires KV_MODE_INCLUSIVE, LRU on every tier and a shared configuration. */
+
+/* A disk medium (e.g. cloud SSD classes that differ in price and I/O
+ * bandwidth, Section 4.1 planner). */
+typedef struct kv_disk_medium {
+  double price_per_gib_hour;         /* >= 0                                  */
+  double bw_base;                    /* bytes/s at zero capacity, > 0         */
+  double bw_per_gib;                 /* extra bytes/s per provisioned GiB, >= 0 */
+  double bw_max;                     /* bytes/s cap, > 0                      */
+} kv_disk_medium;
+
+enum { KV_MAX_MEDIA = 4 };
 
 /* Inputs of the objective proxy (all > 0). */
 typedef struct kv_cost_model {
@@ -152,6 +188,12 @@ typedef struct kv_cost_model {
   double ssd_bw_per_gib;             /* extra disk bytes/s per provisioned GiB */
   double ssd_bw_max;                 /* disk bytes/s cap                      */
   double t_prefill_per_token;        /* seconds to recompute one token's KV   */
+  uint32_t n_media;                  /* 0: the disk is priced by the fields
+                                        above; else media[kv_config.medium]
+                                        replaces price_per_gib_hour[2] and the
+                                        ssd_bw_* fields                       */
+  uint32_t reserved;                 /* must be 0                             */
+  kv_disk_medium media[KV_MAX_MEDIA];
 } kv_cost_model;
 
 /* Canonicalise a trace (Section 4.1: the simulator replays request arrival
@@ -189,14 +231,22 @@ kv_status kv_trace_info(const kv_trace* t, kv_trace_stats* out);
  *   T_wall = max(span, T_busy)
  *   cost = (price_gpu_per_hour + sum_k capGiB[k]*price_per_gib_hour[k]) * T_wall/3600
  *   throughput = N_w*tpg/T_wall (tokens/s);  latency = T_busy/n_req (s)
- * evaluated left to right in IEEE double without contraction.
+ * evaluated left to right in IEEE double without contraction.  An unbounded
+ * disk TTL tier takes capGiB[2] = (S*gb/2^30)/span (its mean occupancy; 0
+ * when span is 0), S its storage-time integral summed in double in an order
+ * of the library's choosing; with media, price_per_gib_hour[2] and the
+ * ssd_bw_* terms are those of media[cfg.medium].
  * FIFO/LFU tiers are replayed once per distinct (order, group, policy,
  * capacity); when the replay state of all of them (4 bytes per access per LFU
  * job, 4 bytes per distinct block per FIFO job) does not fit in device
  * memory, the jobs run in consecutive waves that share one state buffer.
  * Errors: KV_ERR_INVALID for a capacity in (0, w_max), partitioned capacities
- * that exceed cap[k], an unknown mode or policy, nonzero reserved bytes, or a
- * nonpositive cost-model rate; KV_ERR_UNSUPPORTED for the exclusive mode with
+ * that exceed cap[k], an unknown mode or policy, nonzero reserved bytes, a
+ * nonpositive cost-model rate, n_media > KV_MAX_MEDIA, a medium >= n_media
+ * (when n_media > 0, else nonzero), disk_ttl > 1, or a disk TTL that is
+ * negative or not finite; KV_ERR_UNSUPPORTED for a disk TTL tier outside
+ * the inclusive LRU shared mode or bounded with unequal group TTLs, for more
+ * than 1,024 distinct TTLs per group in one call, for the exclusive mode with
  * FIFO/LFU or with blocks of different weights, and for the prefix-reuse
  * mode with FIFO/LFU or partitioned capacities; KV_ERR_NOMEM when not even
  * one replay job's state fits; KV_ERR_DEVICE when an earlier call's replay

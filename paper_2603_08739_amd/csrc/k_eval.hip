@@ -24,11 +24,63 @@ __device__ __forceinline__ uint64_t cum_at(const OrderView& ov, uint32_t g, uint
 //             (a block crosses depth S_k once per reuse interval whose distance
 //             exceeds S_k and once more if it ends deeper); ins of the top tier
 //             = N - hit_top, of a lower tier = evictions of the tier above.
+// Cumulative joint value of field f over accesses (or final blocks, `fin`)
+// with stack distance <= cap (cap = ~0: any, cold accesses included) and gap
+// <= the TTL value at index k of group g.
+__device__ __forceinline__ uint64_t joint_at(const OrderView& ov, const JointView& jv,
+                                             uint32_t g, uint64_t cap, uint32_t k, int f,
+                                             bool fin) {
+  if (cap == 0) return 0;
+  const uint32_t lo = ov.off[g], hi = ov.off[g + 1];
+  const uint32_t d = cap == ~0ull ? hi - lo
+                                  : lower_bound(ov.thr, lo, hi,
+                                                cap > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)cap) - lo;
+  const uint32_t nt = jv.toff[g + 1] - jv.toff[g] + 1;
+  const uint64_t b = jv.jbase[g] + (uint64_t)d * nt + k;
+  return (fin ? jv.fh : jv.jh)[2 * b + f];
+}
+
+// Tier 2 as a disk TTL tier (trace order): present at an access iff its
+// stack distance fits cap2 (unbounded: cap2 = ~0) and its gap fits the TTL;
+// the faster tiers' largest capacity M decides which accesses reach it.
+__device__ __forceinline__ void ttl_tier_record(const OrderView& ov, const JointView& jv,
+                                                const kv_config& C, uint32_t g, uint64_t M,
+                                                const GroupStats& s, uint64_t* r,
+                                                double* store) {
+  const double t = C.ttl[g];
+  const uint32_t tlo = jv.toff[g], thi = jv.toff[g + 1];
+  const uint32_t k = lower_bound(jv.tthr, tlo, thi, t) - tlo;
+  const uint64_t c2 = C.cap[2] ? C.cap[2] : ~0ull;
+  const uint64_t N = s.n_g, NW = s.n_w_g;
+  const uint64_t pc = joint_at(ov, jv, g, c2, k, 0, false), pw = joint_at(ov, jv, g, c2, k, 1, false);
+  const uint64_t lo_cap = (M == 0) ? 0 : (M < c2 ? M : c2);
+  const uint64_t mc = joint_at(ov, jv, g, lo_cap, k, 0, false);
+  const uint64_t mw = joint_at(ov, jv, g, lo_cap, k, 1, false);
+  const uint64_t hc = pc - mc, hw = pw - mw;
+  const uint64_t rc = N - cum_at(ov, g, M, 0), rw = NW - cum_at(ov, g, M, 1);  // reach the disk
+  r[KV_F_HIT] = hc;
+  r[KV_F_HIT_W] = hw;
+  r[KV_F_MISS] = rc - hc;
+  r[KV_F_MISS_W] = rw - hw;
+  r[KV_F_INS] = N - pc;
+  r[KV_F_INS_W] = NW - pw;
+  r[KV_F_EVICT] = (N - pc) - joint_at(ov, jv, g, c2, k, 0, true);
+  r[KV_F_EVICT_W] = (NW - pw) - joint_at(ov, jv, g, c2, k, 1, true);
+  if (C.cap[2] == 0) {
+    // W_g t + sum over gaps <= t of w gap + t (weight of the longer gaps)
+    const double sd = jv.wd[tlo + g + k];
+    const uint64_t gapw = NW - s.u_w_g;               // re-accesses
+    const uint64_t inw = joint_at(ov, jv, g, ~0ull, k, 1, false);  // re-accesses within t
+    *store = ((double)s.u_w_g * t + sd) + t * (double)(gapw - inw);
+  }
+}
+
 __global__ __launch_bounds__(256) void k_lru_counts(const kv_config* __restrict__ cfg,
                                                     uint32_t n_cfg, uint32_t G, OrderView sh,
-                                                    OrderView pt, OrderView px,
+                                                    OrderView pt, OrderView px, JointView jv,
                                                     const GroupStats* __restrict__ gs,
-                                                    uint64_t* __restrict__ counts) {
+                                                    uint64_t* __restrict__ counts,
+                                                    double* __restrict__ store_cg) {
   const uint64_t tid = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (tid >= (uint64_t)n_cfg * G) return;
   const uint32_t c = (uint32_t)(tid / G), g = (uint32_t)(tid % G);
@@ -41,6 +93,34 @@ __global__ __launch_bounds__(256) void k_lru_counts(const kv_config* __restrict_
   for (int k = 0; k < 3; ++k) cap[k] = part ? C.cap_group[k][g] : C.cap[k];
   const uint64_t N = gs[g].n_g, NW = gs[g].n_w_g;
   uint64_t* out = counts + ((uint64_t)c * G + g) * 3 * 8;
+  if (store_cg) store_cg[(uint64_t)c * G + g] = 0.0;
+  if (C.disk_ttl) {
+    uint64_t M = 0;
+    for (int k = 0; k < 2; ++k) {
+      uint64_t* r = out + k * 8;
+      if (cap[k] == 0) {
+        for (int f = 0; f < 8; ++f) r[f] = 0;
+        continue;
+      }
+      const uint64_t Mx = cap[k] > M ? cap[k] : M;
+      const uint64_t hC = cum_at(ov, g, cap[k], 0), wC = cum_at(ov, g, cap[k], 1);
+      const uint64_t hM = cum_at(ov, g, M, 0), wM = cum_at(ov, g, M, 1);
+      const uint64_t hX = cum_at(ov, g, Mx, 0), wX = cum_at(ov, g, Mx, 1);
+      r[KV_F_HIT] = cap[k] > M ? hC - hM : 0;
+      r[KV_F_HIT_W] = cap[k] > M ? wC - wM : 0;
+      r[KV_F_MISS] = N - hX;
+      r[KV_F_MISS_W] = NW - wX;
+      r[KV_F_INS] = N - hC;
+      r[KV_F_INS_W] = NW - wC;
+      r[KV_F_EVICT] = (N - hC) - cum_at(ov, g, cap[k], 2);
+      r[KV_F_EVICT_W] = (NW - wC) - cum_at(ov, g, cap[k], 3);
+      M = Mx;
+    }
+    double st = 0.0;
+    ttl_tier_record(ov, jv, C, g, M, gs[g], out + 2 * 8, &st);
+    if (store_cg) store_cg[(uint64_t)c * G + g] = st;
+    return;
+  }
   if (C.mode == KV_MODE_INCLUSIVE || C.mode == KV_MODE_INCLUSIVE_PREFIX) {
     // which accesses a tier serves: by stack distance, or with prefix reuse
     // by the running maximum over the request; what it holds: by distance
@@ -105,12 +185,15 @@ struct CostArgs {
   double pg, p0, p1, p2, bw_dram, ssd_base, ssd_per_gib, ssd_max, tpf;
   double gb, tpg, span, n_req;
   uint64_t n_w;
+  uint32_t n_media;
+  kv_disk_medium media[KV_MAX_MEDIA];
 };
 
 // (cost, throughput, latency) in IEEE double, left to right, no contraction.
 __global__ __launch_bounds__(256) void k_objectives(const kv_config* __restrict__ cfg,
                                                     uint32_t n_cfg, uint32_t G,
                                                     const uint64_t* __restrict__ counts,
+                                                    const double* __restrict__ store_cg,
                                                     CostArgs a, double* __restrict__ obj) {
   const uint32_t c = blockIdx.x * blockDim.x + threadIdx.x;
   if (c >= n_cfg) return;
@@ -126,9 +209,23 @@ __global__ __launch_bounds__(256) void k_objectives(const kv_config* __restrict_
   const double kGiB = 1073741824.0;
   const double c0 = ((double)cfg[c].cap[0] * a.gb) / kGiB;
   const double c1 = ((double)cfg[c].cap[1] * a.gb) / kGiB;
-  const double c2 = ((double)cfg[c].cap[2] * a.gb) / kGiB;
-  const double bw_lin = a.ssd_base + a.ssd_per_gib * c2;
-  const double bw_ssd = (a.ssd_max < bw_lin) ? a.ssd_max : bw_lin;
+  double c2 = ((double)cfg[c].cap[2] * a.gb) / kGiB;
+  if (cfg[c].disk_ttl && cfg[c].cap[2] == 0) {
+    // an unbounded TTL tier: its mean occupancy over the span
+    double st = 0.0;
+    for (uint32_t g = 0; g < G; ++g) st += store_cg[(uint64_t)c * G + g];
+    c2 = a.span > 0 ? ((st * a.gb) / kGiB) / a.span : 0.0;
+  }
+  double p2 = a.p2, base = a.ssd_base, per_gib = a.ssd_per_gib, bmax = a.ssd_max;
+  if (a.n_media) {
+    const kv_disk_medium& md = a.media[cfg[c].medium];
+    p2 = md.price_per_gib_hour;
+    base = md.bw_base;
+    per_gib = md.bw_per_gib;
+    bmax = md.bw_max;
+  }
+  const double bw_lin = base + per_gib * c2;
+  const double bw_ssd = (bmax < bw_lin) ? bmax : bw_lin;
   const double t_dram = ((double)hw1 * a.gb) / a.bw_dram;
   const double t_ssd = ((double)(hw2 + iw2) * a.gb) / bw_ssd;
   const double t_rec = ((double)rw * a.tpg) * a.tpf;
@@ -136,7 +233,7 @@ __global__ __launch_bounds__(256) void k_objectives(const kv_config* __restrict_
   const double t_wall = (a.span < t_busy) ? t_busy : a.span;
   const double thr = ((double)a.n_w * a.tpg) / t_wall;
   const double lat = t_busy / a.n_req;
-  const double cost = (((a.pg + c0 * a.p0) + c1 * a.p1) + c2 * a.p2) * (t_wall / 3600.0);
+  const double cost = (((a.pg + c0 * a.p0) + c1 * a.p1) + c2 * p2) * (t_wall / 3600.0);
   obj[3 * (uint64_t)c + 0] = cost;
   obj[3 * (uint64_t)c + 1] = thr;
   obj[3 * (uint64_t)c + 2] = lat;
@@ -234,27 +331,30 @@ __global__ __launch_bounds__(256) void k_pareto_count(const uint8_t* __restrict_
 }  // namespace
 
 kv_status lru_counts(const kv_config* cfg_dev, uint32_t n_cfg, uint32_t n_groups,
-                     OrderView shared, OrderView part, OrderView prefix,
-                     const GroupStats* gs_dev, uint64_t* counts, hipStream_t s) {
+                     OrderView shared, OrderView part, OrderView prefix, JointView joint,
+                     const GroupStats* gs_dev, uint64_t* counts, double* store_cg,
+                     hipStream_t s) {
   const uint64_t m = (uint64_t)n_cfg * n_groups;
   if (m == 0) return KV_OK;
   StageTimer tm(kStLruCounts, s);
   hipLaunchKernelGGL(k_lru_counts, dim3(div_up(m, 256)), dim3(256), 0, s, cfg_dev, n_cfg,
-                     n_groups, shared, part, prefix, gs_dev, counts);
+                     n_groups, shared, part, prefix, joint, gs_dev, counts, store_cg);
   KV_HIP(hipGetLastError());
   return KV_OK;
 }
 
 kv_status objectives(const kv_config* cfg_dev, uint32_t n_cfg, uint32_t n_groups,
-                     const uint64_t* counts, const kv_cost_model& m, double gb, double tpg,
-                     double span, double n_req, uint64_t n_w, double* obj, hipStream_t s) {
+                     const uint64_t* counts, const double* store_cg, const kv_cost_model& m,
+                     double gb, double tpg, double span, double n_req, uint64_t n_w,
+                     double* obj, hipStream_t s) {
   if (n_cfg == 0) return KV_OK;
   CostArgs a{m.price_gpu_per_hour, m.price_per_gib_hour[0], m.price_per_gib_hour[1],
              m.price_per_gib_hour[2], m.bw_dram, m.ssd_bw_base, m.ssd_bw_per_gib,
-             m.ssd_bw_max, m.t_prefill_per_token, gb, tpg, span, n_req, n_w};
+             m.ssd_bw_max, m.t_prefill_per_token, gb, tpg, span, n_req, n_w, m.n_media, {}};
+  for (uint32_t i = 0; i < KV_MAX_MEDIA; ++i) a.media[i] = m.media[i];
   StageTimer tm(kStObjectives, s);
   hipLaunchKernelGGL(k_objectives, dim3(div_up(n_cfg, 256)), dim3(256), 0, s, cfg_dev, n_cfg,
-                     n_groups, counts, a, obj);
+                     n_groups, counts, store_cg, a, obj);
   KV_HIP(hipGetLastError());
   return KV_OK;
 }

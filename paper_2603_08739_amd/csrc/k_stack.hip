@@ -568,6 +568,181 @@ __global__ __launch_bounds__(256) void k_sd_finocc(const uint32_t* __restrict__ 
   }
 }
 
+// ---------------------------------------------------------------------------
+// Disk TTL tiers.  A bounded TTL tier (capacity C, TTL t, least recently
+// accessed block displaced first) holds a block at access i iff D_i <= C and
+// its gap delta_i <= t: the blocks it holds are the top of the LRU stack up
+// to C, minus those not accessed for t, and with one TTL the latter are a
+// bottom part of the stack (ages grow with depth).  An unbounded one is
+// C = infinity.  So per group one joint histogram of (D bin, gap bin) serves
+// every (capacity, TTL), and one of (final depth bin, end-age bin) gives the
+// blocks held at the last request.
+// ---------------------------------------------------------------------------
+constexpr uint32_t kJointNT = 1024;
+constexpr uint32_t kJThrLds = 2048;     // stack-distance thresholds in LDS
+constexpr uint32_t kJTtlLds = 1024;     // TTL values (+ groups) in LDS
+constexpr uint32_t kJBinsLds = 4096;    // joint bins in LDS
+
+struct JointLds {
+  uint32_t thr[kJThrLds];
+  double tthr[kJTtlLds];
+  double wd[kJTtlLds];
+  uint32_t jc[kJBinsLds], jw[kJBinsLds];
+  uint32_t off[KV_MAX_GROUPS + 1], toff[KV_MAX_GROUPS + 1], jbase[KV_MAX_GROUPS + 1];
+};
+
+template <bool kLds>
+__device__ __forceinline__ void joint_setup(JointLds& L, const BinArgs& ba, const JointArgs& ja) {
+  const uint32_t G = ba.n_groups;
+  if (threadIdx.x <= G) {
+    L.off[threadIdx.x] = ba.off[threadIdx.x];
+    L.toff[threadIdx.x] = ja.toff[threadIdx.x];
+    L.jbase[threadIdx.x] = ja.jbase[threadIdx.x];
+  }
+  if (kLds) {
+    for (uint32_t j = threadIdx.x; j < ba.n_thr; j += kJointNT) L.thr[j] = ba.thr[j];
+    for (uint32_t j = threadIdx.x; j < ja.n_tthr; j += kJointNT) L.tthr[j] = ja.tthr[j];
+    for (uint32_t j = threadIdx.x; j < ja.n_tthr + G; j += kJointNT) L.wd[j] = 0.0;
+    for (uint32_t j = threadIdx.x; j < ja.n_joint; j += kJointNT) L.jc[j] = L.jw[j] = 0;
+  }
+  __syncthreads();
+}
+
+// bin of (d, x) in group g: d against the capacities, x against the TTLs
+template <bool kLds>
+__device__ __forceinline__ uint32_t joint_bin(const JointLds& L, const BinArgs& ba,
+                                              const JointArgs& ja, uint32_t g, uint32_t d,
+                                              bool has_x, double x, uint32_t* tb) {
+  const uint32_t lo = L.off[g], hi = L.off[g + 1];
+  const uint32_t db = d == kNone ? hi - lo
+                                 : (kLds ? lower_bound(L.thr, lo, hi, d) : lower_bound(ba.thr, lo, hi, d)) - lo;
+  const uint32_t tlo = L.toff[g], thi = L.toff[g + 1];
+  const uint32_t t = !has_x ? thi - tlo
+                            : (kLds ? lower_bound(L.tthr, tlo, thi, x) : lower_bound(ja.tthr, tlo, thi, x)) - tlo;
+  *tb = tlo + g + t;
+  return L.jbase[g] + db * (thi - tlo + 1) + t;
+}
+
+template <bool kLds>
+__device__ __forceinline__ void joint_flush(JointLds& L, const JointArgs& ja, uint64_t* h,
+                                            uint32_t n_groups, bool with_wd) {
+  if (!kLds) return;
+  __syncthreads();
+  for (uint32_t j = threadIdx.x; j < ja.n_joint; j += kJointNT) {
+    if (L.jc[j]) {
+      atomicAdd((unsigned long long*)&h[2 * (uint64_t)j], (unsigned long long)L.jc[j]);
+      atomicAdd((unsigned long long*)&h[2 * (uint64_t)j + 1], (unsigned long long)L.jw[j]);
+    }
+  }
+  if (with_wd)
+    for (uint32_t j = threadIdx.x; j < ja.n_tthr + n_groups; j += kJointNT)
+      if (L.wd[j] != 0.0) atomicAdd(&ja.wd[j], L.wd[j]);
+}
+
+// Accesses by (stack distance, gap to the block's previous access), plus the
+// weighted gaps per gap bin (for the storage integral).
+template <bool kLds>
+__global__ __launch_bounds__(kJointNT) void k_sd_joint(const uint32_t* __restrict__ dist,
+                                                       const uint32_t* __restrict__ key,
+                                                       const uint32_t* __restrict__ req,
+                                                       const double* __restrict__ rt,
+                                                       const uint8_t* __restrict__ w8,
+                                                       const uint8_t* __restrict__ g8, uint64_t n,
+                                                       BinArgs ba, JointArgs ja) {
+  __shared__ JointLds L;
+  joint_setup<kLds>(L, ba, ja);
+  for (uint64_t i = (uint64_t)blockIdx.x * kJointNT + threadIdx.x; i < n;
+       i += (uint64_t)gridDim.x * kJointNT) {
+    const uint32_t k = key[i];
+    const uint32_t g = g8[i], w = w8[i];
+    const double gap = k ? rt[req[i]] - rt[req[k - 1]] : 0.0;
+    uint32_t tb;
+    const uint32_t b = joint_bin<kLds>(L, ba, ja, g, dist[i], k != 0, gap, &tb);
+    if (kLds) {
+      atomicAdd(&L.jc[b], 1u);
+      atomicAdd(&L.jw[b], w);
+      if (k) atomicAdd(&L.wd[tb], (double)w * gap);
+    } else {
+      atomicAdd((unsigned long long*)&ja.jh[2 * (uint64_t)b], 1ull);
+      atomicAdd((unsigned long long*)&ja.jh[2 * (uint64_t)b + 1], (unsigned long long)w);
+      if (k) atomicAdd(&ja.wd[tb], (double)w * gap);
+    }
+  }
+  joint_flush<kLds>(L, ja, ja.jh, ba.n_groups, true);
+}
+
+// Blocks by (final stack depth, age at the last request), at their last access.
+template <bool kLds>
+__global__ __launch_bounds__(kJointNT) void k_sd_finjoint(const uint32_t* __restrict__ nxt,
+                                                          const uint32_t* __restrict__ req,
+                                                          const double* __restrict__ rt,
+                                                          const uint8_t* __restrict__ w8,
+                                                          const uint8_t* __restrict__ g8,
+                                                          uint64_t n,
+                                                          const uint32_t* __restrict__ S,
+                                                          BinArgs ba, JointArgs ja) {
+  __shared__ JointLds L;
+  joint_setup<kLds>(L, ba, ja);
+  const uint32_t segend = S[n - 1];
+  const double t_end = rt[req[n - 1]];  // the last access's request
+  for (uint64_t i = (uint64_t)blockIdx.x * kJointNT + threadIdx.x; i < n;
+       i += (uint64_t)gridDim.x * kJointNT) {
+    if (nxt[i] != kNone) continue;
+    const uint32_t g = g8[i], w = w8[i];
+    const uint32_t depth = segend - (S[i] - w);
+    uint32_t tb;
+    const uint32_t b = joint_bin<kLds>(L, ba, ja, g, depth, true, t_end - rt[req[i]], &tb);
+    if (kLds) {
+      atomicAdd(&L.jc[b], 1u);
+      atomicAdd(&L.jw[b], w);
+    } else {
+      atomicAdd((unsigned long long*)&ja.fh[2 * (uint64_t)b], 1ull);
+      atomicAdd((unsigned long long*)&ja.fh[2 * (uint64_t)b + 1], (unsigned long long)w);
+    }
+  }
+  joint_flush<kLds>(L, ja, ja.fh, ba.n_groups, false);
+}
+
+// Cumulative over both bin dimensions, one block per group; wd over gap bins.
+__global__ __launch_bounds__(256) void k_joint_cum(uint64_t* __restrict__ jh,
+                                                   uint64_t* __restrict__ fh,
+                                                   double* __restrict__ wd,
+                                                   const uint32_t* __restrict__ off,
+                                                   const uint32_t* __restrict__ toff,
+                                                   const uint32_t* __restrict__ jbase) {
+  const uint32_t g = blockIdx.x;
+  const uint32_t nd = off[g + 1] - off[g] + 1, nt = toff[g + 1] - toff[g] + 1;
+  const uint64_t b0 = jbase[g];
+  for (uint32_t q = threadIdx.x; q < 4 * nd; q += blockDim.x) {  // along gap bins
+    uint64_t* h = (q & 2) ? fh : jh;
+    const uint32_t f = q & 1, d = q >> 2;
+    uint64_t run = 0;
+    for (uint32_t t = 0; t < nt; ++t) {
+      uint64_t& x = h[2 * (b0 + (uint64_t)d * nt + t) + f];
+      run += x;
+      x = run;
+    }
+  }
+  __syncthreads();
+  for (uint32_t q = threadIdx.x; q < 4 * nt; q += blockDim.x) {  // along distance bins
+    uint64_t* h = (q & 2) ? fh : jh;
+    const uint32_t f = q & 1, t = q >> 2;
+    uint64_t run = 0;
+    for (uint32_t d = 0; d < nd; ++d) {
+      uint64_t& x = h[2 * (b0 + (uint64_t)d * nt + t) + f];
+      run += x;
+      x = run;
+    }
+  }
+  if (threadIdx.x == 0) {
+    double run = 0.0;
+    for (uint32_t t = 0; t < nt; ++t) {
+      run += wd[toff[g] + g + t];
+      wd[toff[g] + g + t] = run;
+    }
+  }
+}
+
 // cumulative over the bins of each group, one thread per (group, field)
 __global__ void k_hist_cum(uint64_t* hist, const uint32_t* __restrict__ off, uint32_t n_groups) {
   const uint32_t g = threadIdx.x / 4, f = threadIdx.x % 4;
@@ -602,7 +777,7 @@ uint32_t grid_of(uint64_t m, uint32_t cap = 32768) {
 
 kv_status stack_pass(Trace& t, Order& o, bool partitioned, const ThresholdSet& ts,
                      const uint32_t* thr_dev, const uint32_t* off_dev, uint64_t* hist,
-                     uint64_t* phist, hipStream_t s) {
+                     uint64_t* phist, const JointArgs* ja, hipStream_t s) {
   const uint64_t n = t.n;
   const uint32_t G = div_up(n, kSdB);
   kv_status st;
@@ -618,14 +793,17 @@ kv_status stack_pass(Trace& t, Order& o, bool partitioned, const ThresholdSet& t
   if ((st = b_Q.reserve(tri * 4)) != KV_OK) return st;
   if ((st = b_csum.reserve((uint64_t)nchunks * G * 4)) != KV_OK) return st;
   if ((st = b_scan.reserve(std::max<uint64_t>(scan_scratch_elems(n), 1) * 4)) != KV_OK) return st;
-  // prefix reuse (trace order only): every access's distance, request starts
+  // prefix reuse and disk TTL tiers (trace order only): every access's
+  // distance; request starts
   uint32_t* dist = nullptr;
   uint32_t* rstart = nullptr;
-  if (phist) {
-    if (partitioned) return fail(KV_ERR_UNSUPPORTED, "prefix reuse needs the trace order");
+  if (phist || ja) {
+    if (partitioned) return fail(KV_ERR_UNSUPPORTED, "this mode needs the trace order");
     if ((st = t.ws[25].reserve(n * 4)) != KV_OK) return st;
-    if ((st = t.ws[26].reserve(((uint64_t)t.st.n_req + 1) * 4)) != KV_OK) return st;
     dist = t.ws[25].as<uint32_t>();
+  }
+  if (phist) {
+    if ((st = t.ws[26].reserve(((uint64_t)t.st.n_req + 1) * 4)) != KV_OK) return st;
     rstart = t.ws[26].as<uint32_t>();
   }
   const uint32_t* key = o.key.as<uint32_t>();
@@ -655,7 +833,11 @@ kv_status stack_pass(Trace& t, Order& o, bool partitioned, const ThresholdSet& t
     KV_HIP(hipGetLastError());
   }
   BinArgs ba{thr_dev, off_dev, (uint32_t)ts.values.size(), ts.n_groups, hist};
-  const bool lds = ts.values.size() + ts.n_groups <= env_limit("KVCFG_TEST_THR_LDS", kThrLds, 0);
+  const uint32_t lds_limit = env_limit("KVCFG_TEST_THR_LDS", kThrLds, 0);
+  const bool lds = ts.values.size() + ts.n_groups <= lds_limit;
+  const bool jlds = ja && lds_limit > 0 && ts.values.size() <= kJThrLds &&
+                    ja->n_tthr + ts.n_groups <= kJTtlLds && ja->n_joint <= kJBinsLds;
+  const uint32_t gj = std::min<uint32_t>(div_up(n, kJointNT), 1024);
   const uint32_t ga = std::min<uint32_t>(G, 2048);
   {
   StageTimer tm(kStStackAssemble, s);
@@ -686,6 +868,17 @@ kv_status stack_pass(Trace& t, Order& o, bool partitioned, const ThresholdSet& t
                        ts.n_groups);
     KV_HIP(hipGetLastError());
   }
+  if (ja) {
+    const uint32_t* rq = t.req.as<uint32_t>();
+    const double* rt = t.req_time.as<double>();
+    if (jlds)
+      hipLaunchKernelGGL(k_sd_joint<true>, dim3(gj), dim3(kJointNT), 0, s, (const uint32_t*)dist,
+                         key, rq, rt, w8, g8, n, ba, *ja);
+    else
+      hipLaunchKernelGGL(k_sd_joint<false>, dim3(gj), dim3(kJointNT), 0, s,
+                         (const uint32_t*)dist, key, rq, rt, w8, g8, n, ba, *ja);
+    KV_HIP(hipGetLastError());
+  }
   }
   StageTimer tm(kStStackFinal, s);
   // final occupancy: reuse `partial` for the scanned last-occurrence weights
@@ -707,6 +900,20 @@ kv_status stack_pass(Trace& t, Order& o, bool partitioned, const ThresholdSet& t
   hipLaunchKernelGGL(k_hist_cum, dim3(1), dim3(4 * KV_MAX_GROUPS), 0, s, hist, off_dev,
                      ts.n_groups);
   KV_HIP(hipGetLastError());
+  if (ja) {
+    const uint32_t* rq = t.req.as<uint32_t>();
+    const double* rt = t.req_time.as<double>();
+    if (jlds)
+      hipLaunchKernelGGL(k_sd_finjoint<true>, dim3(gj), dim3(kJointNT), 0, s, nxt, rq, rt, w8,
+                         g8, n, (const uint32_t*)S, ba, *ja);
+    else
+      hipLaunchKernelGGL(k_sd_finjoint<false>, dim3(gj), dim3(kJointNT), 0, s, nxt, rq, rt, w8,
+                         g8, n, (const uint32_t*)S, ba, *ja);
+    KV_HIP(hipGetLastError());
+    hipLaunchKernelGGL(k_joint_cum, dim3(ts.n_groups), dim3(256), 0, s, ja->jh, ja->fh, ja->wd,
+                       off_dev, ja->toff, ja->jbase);
+    KV_HIP(hipGetLastError());
+  }
   return KV_OK;
 }
 

@@ -15,6 +15,7 @@
 #include <atomic>
 #include <cmath>
 #include <cstdlib>
+#include <cstring>
 #include <map>
 #include <mutex>
 #include <set>
@@ -236,6 +237,14 @@ kv_status validate_model(const kv_cost_model* m) {
   if (!finite_pos(m->bw_dram) || !finite_pos(m->ssd_bw_base) || !finite_pos(m->ssd_bw_max) ||
       !finite_nonneg(m->ssd_bw_per_gib) || !finite_pos(m->t_prefill_per_token))
     return fail(KV_ERR_INVALID, "kv_eval_configs: bandwidths and t_prefill must be finite and > 0");
+  if (m->n_media > KV_MAX_MEDIA || m->reserved)
+    return fail(KV_ERR_INVALID, "kv_eval_configs: n_media must be <= 4 and reserved 0");
+  for (uint32_t i = 0; i < m->n_media; ++i) {
+    const kv_disk_medium& d = m->media[i];
+    if (!finite_nonneg(d.price_per_gib_hour) || !finite_pos(d.bw_base) ||
+        !finite_nonneg(d.bw_per_gib) || !finite_pos(d.bw_max))
+      return fail(KV_ERR_INVALID, "kv_eval_configs: a disk medium has a bad price or bandwidth");
+  }
   return KV_OK;
 }
 
@@ -247,7 +256,8 @@ uint64_t group_cap(const kv_config& c, int k, uint32_t g) {
   return c.partitioned ? c.cap_group[k][g] : c.cap[k];
 }
 
-kv_status validate_configs(const Trace& t, const kv_config* cfg, uint32_t n_cfg) {
+kv_status validate_configs(const Trace& t, const kv_config* cfg, uint32_t n_cfg,
+                           uint32_t n_media) {
   const uint32_t G = t.n_groups;
   const uint64_t wmax = t.st.w_max;
   for (uint32_t c = 0; c < n_cfg; ++c) {
@@ -255,8 +265,23 @@ kv_status validate_configs(const Trace& t, const kv_config* cfg, uint32_t n_cfg)
     const std::string at = "kv_eval_configs: config " + std::to_string(c) + ": ";
     if (C.mode > KV_MODE_INCLUSIVE_PREFIX) return fail(KV_ERR_INVALID, at + "unknown mode");
     if (C.partitioned > 1) return fail(KV_ERR_INVALID, at + "partitioned must be 0 or 1");
-    for (int r = 0; r < 6; ++r)
+    for (int r = 0; r < 4; ++r)
       if (C.reserved[r]) return fail(KV_ERR_INVALID, at + "reserved bytes must be zero");
+    if (C.medium >= std::max<uint32_t>(n_media, 1))
+      return fail(KV_ERR_INVALID, at + "the disk medium is not in the cost model");
+    if (C.disk_ttl > 1) return fail(KV_ERR_INVALID, at + "disk_ttl must be 0 or 1");
+    if (C.disk_ttl) {
+      for (uint32_t g = 0; g < G; ++g)
+        if (!finite_nonneg(C.ttl[g]))
+          return fail(KV_ERR_INVALID, at + "disk TTLs must be finite and >= 0");
+      if (C.mode != KV_MODE_INCLUSIVE || C.partitioned || C.policy[0] != KV_POLICY_LRU)
+        return fail(KV_ERR_UNSUPPORTED,
+                    at + "a disk TTL tier needs the inclusive mode, LRU and shared tiers");
+      if (C.cap[2])
+        for (uint32_t g = 1; g < G; ++g)
+          if (C.ttl[g] != C.ttl[0])
+            return fail(KV_ERR_UNSUPPORTED, at + "a bounded disk TTL tier needs one TTL");
+    }
     for (int k = 0; k < 3; ++k)
       if (C.cap[k] != 0 && C.cap[k] < wmax)
         return fail(KV_ERR_INVALID, at + "a tier capacity is below the largest block weight");
@@ -325,12 +350,70 @@ void finish_set(ThresholdSet& ts, std::vector<std::vector<uint32_t>>& per_group,
   for (uint32_t g = G + 1; g <= KV_MAX_GROUPS; ++g) ts.off[g] = ts.off[G];
 }
 
+// The disk TTL tiers' bins: per group its sorted distinct TTL values, the
+// joint histograms' layout (bins of group g: (capacities + 1) x (TTLs + 1)),
+// zeroed device histograms.  Needs the shared threshold set built.
+kv_status plan_joint(Trace& t, std::vector<std::vector<double>>& per_group, JointArgs& ja,
+                     JointView& jv, hipStream_t s) {
+  const uint32_t G = t.n_groups;
+  TtlSet& ts = t.ttl_ts;
+  ts.values.clear();
+  ts.n_groups = G;
+  ts.off[0] = 0;
+  std::vector<uint32_t> jbase(G + 1, 0);
+  for (uint32_t g = 0; g < G; ++g) {
+    auto& v = per_group[g];
+    std::sort(v.begin(), v.end());
+    v.erase(std::unique(v.begin(), v.end()), v.end());
+    if (v.size() > 1024)
+      return fail(KV_ERR_UNSUPPORTED, "kv_eval_configs: more than 1,024 disk TTLs in one group");
+    ts.values.insert(ts.values.end(), v.begin(), v.end());
+    ts.off[g + 1] = (uint32_t)ts.values.size();
+    const uint64_t nd = (uint64_t)t.shared_ts.off[g + 1] - t.shared_ts.off[g] + 1;
+    const uint64_t nb = (uint64_t)jbase[g] + nd * (v.size() + 1);
+    if (nb > 0x7FFFFFFFull) return fail(KV_ERR_UNSUPPORTED, "kv_eval_configs: too many joint bins");
+    jbase[g + 1] = (uint32_t)nb;
+  }
+  const uint32_t nt = (uint32_t)ts.values.size(), nj = jbase[G];
+  // device: TTL values (doubles), then toff and jbase (u32)
+  t.joint_stage.assign(2 * nt + 2 * (G + 1), 0);
+  std::memcpy(t.joint_stage.data(), ts.values.data(), nt * sizeof(double));
+  for (uint32_t g = 0; g <= G; ++g) {
+    t.joint_stage[2 * nt + g] = ts.off[g];
+    t.joint_stage[2 * nt + G + 1 + g] = jbase[g];
+  }
+  kv_status st;
+  DevBuf& bt = t.ws[27];
+  DevBuf& bh = t.ws[28];
+  if ((st = bt.reserve(t.joint_stage.size() * 4)) != KV_OK) return st;
+  const uint64_t hwords = 4ull * nj + nt + G;
+  if ((st = bh.reserve(hwords * 8)) != KV_OK) return st;
+  KV_HIP(hipMemcpyAsync(bt.p, t.joint_stage.data(), t.joint_stage.size() * 4,
+                        hipMemcpyHostToDevice, s));
+  if ((st = fill_u64(bh.as<uint64_t>(), 0, hwords, s)) != KV_OK) return st;
+  ja.tthr = bt.as<double>();
+  ja.toff = bt.as<uint32_t>() + 2 * nt;
+  ja.jbase = ja.toff + G + 1;
+  ja.n_tthr = nt;
+  ja.n_joint = nj;
+  ja.jh = bh.as<uint64_t>();
+  ja.fh = ja.jh + 2ull * nj;
+  ja.wd = reinterpret_cast<double*>(ja.fh + 2ull * nj);
+  jv.tthr = ja.tthr;
+  jv.toff = ja.toff;
+  jv.jbase = ja.jbase;
+  jv.jh = ja.jh;
+  jv.fh = ja.fh;
+  jv.wd = ja.wd;
+  return KV_OK;
+}
+
 struct StackSlot {
   int ws_thr, ws_hist, ws_phist;  // ws_phist < 0: no prefix-reuse histogram
 };
 
 kv_status run_stack(Trace& t, Order& o, bool partitioned, ThresholdSet& ts, StackSlot slot,
-                    OrderView& view, OrderView& pview, hipStream_t s) {
+                    OrderView& view, OrderView& pview, const JointArgs* ja, hipStream_t s) {
   kv_status st;
   DevBuf& bt = t.ws[slot.ws_thr];
   DevBuf& bh = t.ws[slot.ws_hist];
@@ -350,7 +433,7 @@ kv_status run_stack(Trace& t, Order& o, bool partitioned, ThresholdSet& ts, Stac
     if ((st = fill_u64(bp.as<uint64_t>(), 0, nbins * 4, s)) != KV_OK) return st;
     ph = bp.as<uint64_t>();
   }
-  if ((st = stack_pass(t, o, partitioned, ts, thr, off, bh.as<uint64_t>(), ph, s)) != KV_OK)
+  if ((st = stack_pass(t, o, partitioned, ts, thr, off, bh.as<uint64_t>(), ph, ja, s)) != KV_OK)
     return st;
   view.thr = thr;
   view.off = off;
@@ -553,14 +636,15 @@ kv_status kv_eval_configs(const kv_trace* h, const kv_config* cfg, uint32_t n_cf
   if ((st = validate_model(model)) != KV_OK) return st;
   if (n_cfg == 0) return KV_OK;
   if (!cfg || !counts) return fail(KV_ERR_INVALID, "kv_eval_configs: cfg and counts are required");
-  if ((st = validate_configs(*t, cfg, n_cfg)) != KV_OK) return st;
+  if ((st = validate_configs(*t, cfg, n_cfg, model->n_media)) != KV_OK) return st;
   hipStream_t s = (hipStream_t)stream;
   const uint32_t G = t->n_groups;
   t->cfg_stage.assign(cfg, cfg + n_cfg);
 
   // ---- plan: thresholds per order, replay jobs
   std::vector<std::vector<uint32_t>> tsh(G), tpt(G);
-  bool need_shared = false, need_part = false, need_prefix = false;
+  std::vector<std::vector<double>> tttl(G);  // disk TTL values per group
+  bool need_shared = false, need_part = false, need_prefix = false, need_joint = false;
   const uint64_t w0 = t->st.w_max;
   std::map<std::tuple<uint32_t, uint32_t, uint32_t, uint64_t>, uint32_t> job_index;
   std::vector<ReplayJob> jobs;
@@ -572,6 +656,10 @@ kv_status kv_eval_configs(const kv_trace* h, const kv_config* cfg, uint32_t n_cf
       const uint32_t pol = group_policy(C, g);
       if (pol == KV_POLICY_LRU) {
         need_prefix |= C.mode == KV_MODE_INCLUSIVE_PREFIX;
+        if (C.disk_ttl) {
+          need_joint = true;
+          for (uint32_t gg = 0; gg < G; ++gg) tttl[gg].push_back(C.ttl[gg]);
+        }
         if (part_order) {
           need_part = true;
           add_thresholds(tpt, C, g, g, w0);
@@ -619,30 +707,40 @@ kv_status kv_eval_configs(const kv_trace* h, const kv_config* cfg, uint32_t n_cf
   if ((st = bcfg.reserve((uint64_t)n_cfg * sizeof(kv_config))) != KV_OK) return st;
   if ((st = bgs.reserve(sizeof(GroupStats) * KV_MAX_GROUPS)) != KV_OK) return st;
   for (uint32_t g = 0; g < KV_MAX_GROUPS; ++g)
-    t->gs_stage[g] = GroupStats{t->st.n_g[g], t->st.n_w_g[g], t->st.u_g[g], w0};
+    t->gs_stage[g] = GroupStats{t->st.n_g[g], t->st.n_w_g[g], t->st.u_g[g], w0, t->st.u_w_g[g]};
   KV_HIP(hipMemcpyAsync(bcfg.p, t->cfg_stage.data(), (uint64_t)n_cfg * sizeof(kv_config),
                         hipMemcpyHostToDevice, s));
   KV_HIP(hipMemcpyAsync(bgs.p, t->gs_stage, sizeof(t->gs_stage), hipMemcpyHostToDevice, s));
   const kv_config* cfg_dev = bcfg.as<kv_config>();
+  double* store_cg = nullptr;  // unbounded disk TTL tiers' storage integrals
+  if (need_joint) {
+    if ((st = t->ws[29].reserve((uint64_t)n_cfg * G * sizeof(double))) != KV_OK) return st;
+    store_cg = t->ws[29].as<double>();
+  }
 
   // ---- LRU: stack-distance passes + closed forms
   auto lru = [&]() -> kv_status {
     kv_status r;
     OrderView vsh, vpt, vpx, unused;
+    JointArgs ja;
+    JointView jv;
     if (need_shared) {
       finish_set(t->shared_ts, tsh, G);
+      if (need_joint && (r = plan_joint(*t, tttl, ja, jv, s)) != KV_OK) return r;
       if ((r = run_stack(*t, t->shared, false, t->shared_ts,
-                         StackSlot{5, 6, need_prefix ? 24 : -1}, vsh, vpx, s)) != KV_OK)
+                         StackSlot{5, 6, need_prefix ? 24 : -1}, vsh, vpx,
+                         need_joint ? &ja : nullptr, s)) != KV_OK)
         return r;
     }
     if (need_part) {
       finish_set(t->part_ts, tpt, G);
-      if ((r = run_stack(*t, t->part, true, t->part_ts, StackSlot{7, 8, -1}, vpt, unused, s)) !=
-          KV_OK)
+      if ((r = run_stack(*t, t->part, true, t->part_ts, StackSlot{7, 8, -1}, vpt, unused,
+                         nullptr, s)) != KV_OK)
         return r;
     }
     if (need_shared || need_part)
-      return lru_counts(cfg_dev, n_cfg, G, vsh, vpt, vpx, bgs.as<GroupStats>(), counts, s);
+      return lru_counts(cfg_dev, n_cfg, G, vsh, vpt, vpx, jv, bgs.as<GroupStats>(), counts,
+                        store_cg, s);
     return KV_OK;
   };
   // ---- FIFO / LFU: replay jobs, with the LRU work running meanwhile
@@ -653,7 +751,7 @@ kv_status kv_eval_configs(const kv_trace* h, const kv_config* cfg, uint32_t n_cf
   }
   // ---- objectives
   if (obj) {
-    st = objectives(cfg_dev, n_cfg, G, counts, *model, (double)t->gb, (double)t->tpg,
+    st = objectives(cfg_dev, n_cfg, G, counts, store_cg, *model, (double)t->gb, (double)t->tpg,
                     t->st.span, (double)t->st.n_req, t->st.n_w, obj, s);
     if (st != KV_OK) return st;
   }

@@ -78,6 +78,28 @@ struct ReplayJobInfo {
 
 struct GroupStats {
   uint64_t n_g, n_w_g, u_g, w0;  // accesses, weight, distinct blocks, uniform weight
+  uint64_t u_w_g;                // distinct weight
+};
+
+// The TTL values disk TTL tiers use, per group (sorted, distinct).
+struct TtlSet {
+  std::vector<double> values;
+  uint32_t off[KV_MAX_GROUPS + 1] = {0};
+  uint32_t n_groups = 1;
+};
+
+// Disk TTL tiers (trace order): per group, a joint histogram of accesses by
+// (stack-distance bin, gap bin) and of blocks by (final-depth bin, end-age
+// bin), bin (d, t) of group g at jbase[g] + d * (tbins of g) + t; gap bins
+// cut at the group's TTL values (bin t = #{ttl < gap}; no gap = last bin).
+struct JointArgs {
+  const double* tthr = nullptr;    // [toff[G]] TTL values, device
+  const uint32_t* toff = nullptr;  // [G + 1], device
+  const uint32_t* jbase = nullptr; // [G + 1], device
+  uint32_t n_tthr = 0, n_joint = 0;
+  uint64_t* jh = nullptr;          // [n_joint][2] count, weight (zeroed)
+  uint64_t* fh = nullptr;          // [n_joint][2] count, weight (zeroed)
+  double* wd = nullptr;            // [n_tthr + G] sum of w * gap per (group, gap bin) (zeroed)
 };
 
 struct Trace {
@@ -95,7 +117,7 @@ struct Trace {
   DevBuf req;         // u32[n] request of each access (trace order)
   DevBuf req_time;    // f64[n_req] arrival time of each request
   // workspace reused across kv_eval_configs calls on this trace
-  DevBuf ws[27];
+  DevBuf ws[32];
   // Device error record {code, job} written by a replay kernel that fails
   // its internal state check; copied after every kv_eval_configs call that
   // replays into `err_host` (pinned), with `err_ev` recorded after the copy.
@@ -107,6 +129,8 @@ struct Trace {
   ~Trace();
   // host staging of the latest kv_eval_configs call (alive across its copies)
   ThresholdSet shared_ts, part_ts;
+  TtlSet ttl_ts;
+  std::vector<uint32_t> joint_stage;
   std::vector<kv_config> cfg_stage;
   GroupStats gs_stage[KV_MAX_GROUPS];
   std::vector<uint8_t> job_stage, rec_stage, src_stage;
@@ -154,9 +178,11 @@ kv_status canon_partition(Trace& t, hipStream_t s);
 // thr_dev / off_dev: device copies of ts.values / ts.off; hist must be zeroed.
 // phist (zeroed, same layout, or NULL; trace order only): fields 0 and 1
 // count the accesses by their request-prefix distance (prefix reuse).
+// ja (or NULL; trace order only): the joint histograms of disk TTL tiers,
+// made cumulative over both bin dimensions (and wd over gap bins) on return.
 kv_status stack_pass(Trace& t, Order& o, bool partitioned, const ThresholdSet& ts,
                      const uint32_t* thr_dev, const uint32_t* off_dev, uint64_t* hist,
-                     uint64_t* phist, hipStream_t s);
+                     uint64_t* phist, const JointArgs* ja, hipStream_t s);
 
 // per-configuration evaluation (k_eval.hip)
 
@@ -166,15 +192,29 @@ struct OrderView {
   const uint32_t* off = nullptr;
   const uint64_t* hist = nullptr;
 };
+// Device view of the cumulative joint histograms (trace order).
+struct JointView {
+  const double* tthr = nullptr;
+  const uint32_t* toff = nullptr;
+  const uint32_t* jbase = nullptr;
+  const uint64_t* jh = nullptr;
+  const uint64_t* fh = nullptr;
+  const double* wd = nullptr;
+};
 // Writes the records of every (config, group) whose policy is LRU.  Groups of
 // partitioned configs read `part` when n_groups > 1, `shared` otherwise;
 // prefix-reuse configs take their hits from `prefix` (trace order).
+// Disk TTL tiers take tier 2 from `joint` and write the storage-time
+// integral of each unbounded one per (config, group) to store_cg.
 kv_status lru_counts(const kv_config* cfg_dev, uint32_t n_cfg, uint32_t n_groups,
-                     OrderView shared, OrderView part, OrderView prefix,
-                     const GroupStats* gs_dev, uint64_t* counts, hipStream_t s);
+                     OrderView shared, OrderView part, OrderView prefix, JointView joint,
+                     const GroupStats* gs_dev, uint64_t* counts, double* store_cg,
+                     hipStream_t s);
+// store_cg: [n_cfg][n_groups] or NULL (no disk TTL tier in the batch).
 kv_status objectives(const kv_config* cfg_dev, uint32_t n_cfg, uint32_t n_groups,
-                     const uint64_t* counts, const kv_cost_model& m, double gb, double tpg,
-                     double span, double n_req, uint64_t n_w, double* obj, hipStream_t s);
+                     const uint64_t* counts, const double* store_cg, const kv_cost_model& m,
+                     double gb, double tpg, double span, double n_req, uint64_t n_w,
+                     double* obj, hipStream_t s);
 kv_status pareto(const double* obj, const uint32_t* segment, uint32_t n, const double* bounds,
                  uint8_t* flag, uint32_t* counters_dev, hipStream_t s);
 

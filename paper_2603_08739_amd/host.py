@@ -32,13 +32,14 @@ def load(trace, dev=None, stream=None):
 
 def config_array(cfgs):
     return kvcfg.config_array(cfgs.cap, cfgs.cap_group, cfgs.mode, cfgs.partitioned,
-                              cfgs.policy)
+                              cfgs.policy, cfgs.disk_ttl, cfgs.medium, cfgs.ttl)
 
 
 def cost_model(cost: dict):
     return kvcfg.cost_model(cost["price_gpu_per_hour"], cost["price_per_gib_hour"],
                             cost["bw_dram"], cost["ssd_bw_base"], cost["ssd_bw_per_gib"],
-                            cost["ssd_bw_max"], cost["t_prefill_per_token"])
+                            cost["ssd_bw_max"], cost["t_prefill_per_token"],
+                            cost.get("media", ()))
 
 
 def evaluate(handle, cfgs, cost: dict, n_groups: int, device="cuda", stream=None):

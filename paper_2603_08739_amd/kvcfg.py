@@ -40,16 +40,27 @@ class kv_trace_stats(ctypes.Structure):
                 ("w_min", _u32), ("w_max", _u32), ("span", _f64)]
 
 
+KV_MAX_MEDIA = 4
+CONFIG_BYTES = 560
+
+
 class kv_config(ctypes.Structure):
     _fields_ = [("cap", _u64 * KV_TIERS), ("cap_group", (_u64 * KV_MAX_GROUPS) * KV_TIERS),
                 ("mode", _u8), ("partitioned", _u8), ("policy", _u8 * KV_MAX_GROUPS),
-                ("reserved", _u8 * 6)]
+                ("disk_ttl", _u8), ("medium", _u8), ("reserved", _u8 * 4),
+                ("ttl", _f64 * KV_MAX_GROUPS)]
+
+
+class kv_disk_medium(ctypes.Structure):
+    _fields_ = [("price_per_gib_hour", _f64), ("bw_base", _f64), ("bw_per_gib", _f64),
+                ("bw_max", _f64)]
 
 
 class kv_cost_model(ctypes.Structure):
     _fields_ = [("price_gpu_per_hour", _f64), ("price_per_gib_hour", _f64 * KV_TIERS),
                 ("bw_dram", _f64), ("ssd_bw_base", _f64), ("ssd_bw_per_gib", _f64),
-                ("ssd_bw_max", _f64), ("t_prefill_per_token", _f64)]
+                ("ssd_bw_max", _f64), ("t_prefill_per_token", _f64), ("n_media", _u32),
+                ("reserved", _u32), ("media", kv_disk_medium * KV_MAX_MEDIA)]
 
 
 KV_STAGES = 16
@@ -63,7 +74,7 @@ class kv_timing(ctypes.Structure):
     _fields_ = [("calls", _u64 * KV_STAGES), ("ms", _f64 * KV_STAGES)]
 
 
-assert ctypes.sizeof(kv_config) == 432
+assert ctypes.sizeof(kv_config) == CONFIG_BYTES
 
 
 class KvError(RuntimeError):
@@ -212,11 +223,12 @@ def kv_trace_load(hash, req, req_time, group=None, weight=None, n_groups=1,
     return Trace(h)
 
 
-def config_array(cap, cap_group, mode, partitioned, policy):
-    """numpy arrays (n,3) (n,3,16) (n,) (n,) (n,16) -> ctypes kv_config[n]."""
+def config_array(cap, cap_group, mode, partitioned, policy, disk_ttl=None, medium=None,
+                 ttl=None):
+    """numpy arrays (n,3) (n,3,16) (n,) (n,) (n,16) [(n,) (n,) (n,16)] -> ctypes kv_config[n]."""
     n = int(np.asarray(cap).shape[0])
     arr = (kv_config * max(n, 1))()
-    raw = np.frombuffer(arr, dtype=np.uint8).reshape(max(n, 1), 432)
+    raw = np.frombuffer(arr, dtype=np.uint8).reshape(max(n, 1), CONFIG_BYTES)
     if n:
         raw[:n, 0:24] = np.ascontiguousarray(cap, dtype=np.uint64).view(np.uint8).reshape(n, 24)
         raw[:n, 24:408] = np.ascontiguousarray(cap_group, dtype=np.uint64).view(
@@ -224,13 +236,25 @@ def config_array(cap, cap_group, mode, partitioned, policy):
         raw[:n, 408] = np.asarray(mode, dtype=np.uint8)
         raw[:n, 409] = np.asarray(partitioned, dtype=np.uint8)
         raw[:n, 410:426] = np.asarray(policy, dtype=np.uint8)
-        raw[:n, 426:432] = 0
+        raw[:n, 426] = 0 if disk_ttl is None else np.asarray(disk_ttl, dtype=np.uint8)
+        raw[:n, 427] = 0 if medium is None else np.asarray(medium, dtype=np.uint8)
+        raw[:n, 428:432] = 0
+        if ttl is not None:
+            raw[:n, 432:560] = np.ascontiguousarray(ttl, dtype=np.float64).view(
+                np.uint8).reshape(n, 128)
     return arr, n
 
 
 def cost_model(price_gpu_per_hour, price_per_gib_hour, bw_dram, ssd_bw_base, ssd_bw_per_gib,
-               ssd_bw_max, t_prefill_per_token) -> kv_cost_model:
+               ssd_bw_max, t_prefill_per_token, media=()) -> kv_cost_model:
+    """media: sequence of (price_per_gib_hour, bw_base, bw_per_gib, bw_max) tuples."""
     m = kv_cost_model()
+    if len(media) > KV_MAX_MEDIA:
+        raise ValueError("too many disk media")
+    m.n_media = len(media)
+    for i, md in enumerate(media):
+        m.media[i].price_per_gib_hour, m.media[i].bw_base, m.media[i].bw_per_gib, \
+            m.media[i].bw_max = [float(x) for x in md]
     m.price_gpu_per_hour = price_gpu_per_hour
     for k in range(3):
         m.price_per_gib_hour[k] = price_per_gib_hour[k]

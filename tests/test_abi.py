@@ -29,7 +29,7 @@ def test_library_exports_every_declared_symbol():
     for name in declared_functions():
         assert hasattr(kvcfg.LIB, name), name
         assert name in kvcfg.EXPORTS
-    assert ctypes.sizeof(kvcfg.kv_config) == 432
+    assert ctypes.sizeof(kvcfg.kv_config) == 560
 
 
 def test_struct_layouts_match_header():
@@ -47,6 +47,9 @@ int main(void) {
          offsetof(kv_trace_desc, granule_bytes), offsetof(kv_trace_stats, span));
   printf("%zu %zu %zu\n", offsetof(kv_config, mode), offsetof(kv_config, policy),
          offsetof(kv_cost_model, t_prefill_per_token));
+  printf("%zu %zu %zu %zu %zu\n", offsetof(kv_config, disk_ttl), offsetof(kv_config, medium),
+         offsetof(kv_config, ttl), offsetof(kv_cost_model, n_media),
+         offsetof(kv_cost_model, media));
   return 0;
 }
 '''
@@ -63,7 +66,9 @@ int main(void) {
             K.kv_trace_desc.n_req.offset, K.kv_trace_desc.req_time.offset,
             K.kv_trace_desc.granule_bytes.offset, K.kv_trace_stats.span.offset,
             K.kv_config.mode.offset, K.kv_config.policy.offset,
-            K.kv_cost_model.t_prefill_per_token.offset]
+            K.kv_cost_model.t_prefill_per_token.offset, K.kv_config.disk_ttl.offset,
+            K.kv_config.medium.offset, K.kv_config.ttl.offset, K.kv_cost_model.n_media.offset,
+            K.kv_cost_model.media.offset]
     assert got == want
 
 
