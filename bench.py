@@ -127,6 +127,44 @@ def traffic_for(kernel):
     return rec["bytes_per_launch"]
 
 
+# What bounds a kernel that is not bound by HBM: its VALU instruction count
+# per launch (from the committed rocprofv3 SQ counter run, valid while the
+# kernel source is unchanged) against the issue rate of the compute units it
+# occupies (one wave64 VALU instruction per cycle per compute unit: 4 SIMDs,
+# 4 cycles each, at 2.4 GHz).
+CU_COUNT, CLOCK_HZ = 256, 2.4e9
+
+
+def limiter_for(kernel, avg_ms, workgroups):
+    path = os.path.join(ROOT, "profiles", "valu.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path)).get(kernel)
+    if not rec:
+        return None
+    src = os.path.join(ROOT, "paper_2603_08739_amd", "csrc", rec["source"])
+    if hashlib.sha256(open(src, "rb").read()).hexdigest()[:16] != rec.get("source_sha"):
+        return None
+    rate = rec["valu_insts_per_launch"] / (avg_ms / 1000.0)
+    cus = min(workgroups or CU_COUNT, CU_COUNT)
+    return {"bound": "valu issue and dependent latency of one workgroup per job",
+            "valu_wave_insts_per_launch": rec["valu_insts_per_launch"],
+            "achieved": rate, "unit": "wave64 VALU instructions/s",
+            "peak_occupied_cus": cus * CLOCK_HZ, "frac_occupied_cus": rate / (cus * CLOCK_HZ),
+            "peak_chip": CU_COUNT * CLOCK_HZ, "frac_chip": rate / (CU_COUNT * CLOCK_HZ),
+            "occupied_cus": cus}
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline(rec, cfgs, budget_s):
     """The oracle on a bounded sample: a prefix of the trace x a config sample."""
     from oracle import oracle as O
@@ -149,44 +187,83 @@ def cpu_baseline(rec, cfgs, budget_s):
         O.replay(t, sample, threads)
         dt = time.time() - t0
     value = t.n * sample.n / dt
+    # one core on the same configurations over a shorter prefix (a quarter
+    # of the budget at the all-core rate's per-core share)
+    n1 = max(200, int(n_req * min(1.0, 0.25 * budget_s / max(dt * threads, 1e-3))))
+    t1s = rec.to_trace(max_requests=n1)
+    t0 = time.time()
+    O.replay(t1s, sample, 1)
+    dt1 = time.time() - t0
     return {"value": value, "unit": "block-accesses×configs/s", "cores": threads,
-            "kind": "oracle",
+            "kind": "oracle", "cpu_model": cpu_model(),
+            "value_one_core": t1s.n * sample.n / dt1,
             "sample": f"first {n_req} requests ({t.n} accesses) x {sample.n} configs sampled "
-                      f"from the workload's batch (seed 11), literal replay, {dt:.1f} s"}
+                      f"from the workload's batch (seed 11), literal replay, {dt:.1f} s on "
+                      f"{threads} threads; one core: first {n1} requests ({t1s.n} accesses), "
+                      f"{dt1:.1f} s"}
 
 
-def adaptive_search(h, rec, G, model, torch, K):
-    """Alg. 1 over (DRAM, disk) at one HBM size of the workload's grid, against
-    that grid's 20 x 20 slice: evaluations, rounds, time and the hypervolume
-    of its front relative to the slice's front."""
-    from paper_2603_08739_amd import search as P
-    gran = lambda nbytes: int(nbytes // rec.granule_bytes)
-    gib, tib = 1 << 30, 1 << 40
-    hbm = gran(40 * gib)
-    d_rng = (0, gran(2048 * gib), gran(512 * gib))
-    t_rng = (0, gran(8 * tib), gran(2 * tib))
-    res = (gran(128 * gib), gran(tib // 2))
+def _search_vs_grid(h, rec, G, model, P, hbm, second, d_rng, t_rng, res, grid_d, grid_t,
+                    ttl_unit=1.0):
+    """One Alg. 1 run against the full grid: evaluations, rounds, wall time,
+    fronts and the hypervolume ratio under one reference point strictly
+    worse than every configuration either evaluated."""
+    import torch
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    ex = P.Explorer(h, G, model, hbm=hbm)
+    ex = P.Explorer(h, G, model, hbm=hbm, second=second, ttl_unit=ttl_unit)
     rounds = ex.run(d_rng, t_rng, 0.02, 0.05, 0.02, res=res)
     flags = ex.front()
     wall = time.perf_counter() - t0
-    grid_pts = [(gran(128 * gib) * i, gran(tib // 2) * j) for i in range(20) for j in range(20)]
-    grid_obj = P.Explorer(h, G, model, hbm=hbm).evaluate(grid_pts)
-    gx = P.Explorer(h, G, model, hbm=hbm)
-    gx.obj = grid_obj
+    grid_pts = [(d, t) for d in grid_d for t in grid_t]
+    gx = P.Explorer(h, G, model, hbm=hbm, second=second, ttl_unit=ttl_unit)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    gx.obj = gx.evaluate(grid_pts)
     gflags = gx.front()
-    a, b = P.minimised(ex.obj), P.minimised(grid_obj)
+    gwall = time.perf_counter() - t1
+    a, b = P.minimised(ex.obj), P.minimised(gx.obj)
     ref = np.maximum(a.max(axis=0), b.max(axis=0))
     ref = ref + 0.01 * np.abs(ref) + 1e-12
     hv_s, hv_g = P.hypervolume(a[flags], ref), P.hypervolume(b[gflags], ref)
-    print(f"[bench] adaptive search: {len(ex.points)} evaluations in {rounds} rounds, "
-          f"{wall:.2f} s", file=sys.stderr, flush=True)
-    return {"algorithm": "Alg. 1 over (DRAM, disk capacity) at 40 GiB HBM, LRU inclusive",
-            "evaluations": len(ex.points), "rounds": rounds, "wall_s": wall,
-            "front": int(flags.sum()), "grid_points": len(grid_pts), "grid_front": int(gflags.sum()),
+    return {"evaluations": len(ex.points), "rounds": rounds, "wall_s": wall,
+            "front": int(flags.sum()), "grid_points": len(grid_pts),
+            "grid_front": int(gflags.sum()), "grid_wall_s": gwall,
             "hypervolume_vs_grid": hv_s / hv_g if hv_g > 0 else None}
+
+
+def adaptive_search(h, rec, G, model, torch, K):
+    """Alg. 1 (Section 4.2) at 40 GiB HBM, LRU inclusive, against full grids
+    of 17 x 31 = 527 configurations:
+    * the paper's ablation (Section 5.3.1): DRAM x disk capacity, grid DRAM
+      0-4096 GiB step 256 x disk 0-3600 GiB step 120; the search starts from
+      DRAM 0-2048 step 512 x disk 0-2400 step 600 and refines down to the
+      grid's steps;
+    * the planner's dimensions (Section 4.1): DRAM x disk TTL (an unbounded
+      TTL tier), grid TTL 0-3600 s step 120, start 0-2400 s step 600."""
+    from paper_2603_08739_amd import search as P
+    gran = lambda nbytes: int(nbytes // rec.granule_bytes)
+    gib = 1 << 30
+    hbm = gran(40 * gib)
+    d_rng = (0, gran(2048 * gib), gran(512 * gib))
+    grid_d = [gran(256 * gib) * i for i in range(17)]
+    out = {}
+    cap = _search_vs_grid(h, rec, G, model, P, hbm, "disk", d_rng,
+                          (0, gran(2400 * gib), gran(600 * gib)),
+                          (gran(256 * gib), gran(120 * gib)), grid_d,
+                          [gran(120 * gib) * j for j in range(31)])
+    cap["algorithm"] = "Alg. 1 over (DRAM, disk capacity) at 40 GiB HBM, LRU inclusive"
+    out["dram_x_disk"] = cap
+    ttl = _search_vs_grid(h, rec, G, model, P, hbm, "ttl", d_rng, (0, 20, 5),
+                          (gran(256 * gib), 1), grid_d, list(range(31)), ttl_unit=120.0)
+    ttl["algorithm"] = ("Alg. 1 over (DRAM, disk TTL) at 40 GiB HBM, LRU inclusive, "
+                        "unbounded TTL disk tier, TTL step 120 s")
+    out["dram_x_ttl"] = ttl
+    for k, v in out.items():
+        print(f"[bench] adaptive search {k}: {v['evaluations']} evaluations in {v['rounds']} "
+              f"rounds ({v['wall_s']:.2f} s) against {v['grid_points']}; hypervolume "
+              f"{v['hypervolume_vs_grid']:.4f} of the grid's", file=sys.stderr, flush=True)
+    return out
 
 
 def group_ttl(dev, rec, torch, K, k=7, budget_fracs=(0.02, 0.05, 0.25)):
@@ -295,27 +372,13 @@ def extras(dev, rec, cfgs, G, model, n, torch, K):
     return ttl, search, prefix, gttl
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU only (asked for {args.gpus}); multi-GPU sharding "
-              "is described in the design notes but not built.", file=sys.stderr)
-        sys.exit(2)
-    import torch
-    import tracegen as tg
-    from paper_2603_08739_amd import host, kvcfg as K
-
-    if args.copy_calibration:
-        src = torch.ones(args.copy_calibration // 4, dtype=torch.int32, device="cuda")
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        print(f"[bench] copy calibration: {src.numel() * 4} bytes", file=sys.stderr, flush=True)
-        del src, dst
-    print(f"[bench] generating workload {args.workload}", file=sys.stderr, flush=True)
-    rec = tg.recipe(args.workload)
-    cfgs = tg.configs_for(args.workload, rec)
+def measure(name, steps, warmup, torch, tg, host, K, keep=False):
+    """Times `steps` whole steps (load + eval + two Pareto passes) of one
+    workload on the device; returns the figures, and with `keep` also the
+    device inputs for the measurements that follow."""
+    print(f"[bench] generating workload {name}", file=sys.stderr, flush=True)
+    rec = tg.recipe(name)
+    cfgs = tg.configs_for(name, rec)
     dev = rec.expand("cuda")
     torch.cuda.synchronize()
     n = int(dev["hash"].numel())
@@ -327,7 +390,7 @@ def main():
     front = torch.zeros(n_cfg, dtype=torch.uint8, device="cuda")
     front_seg = torch.zeros(n_cfg, dtype=torch.uint8, device="cuda")
     seg = torch.from_numpy(cfgs.segment.astype(np.int32)).to("cuda")
-    print(f"[bench] {n} accesses, {n_cfg} configs", file=sys.stderr, flush=True)
+    print(f"[bench] {name}: {n} accesses, {n_cfg} configs", file=sys.stderr, flush=True)
     h0 = K.kv_trace_load(dev["hash"], dev["req"], dev["req_time"], group=dev["group"],
                          weight=dev["weight"], n_groups=G,
                          tokens_per_granule=rec.tokens_per_granule,
@@ -346,53 +409,97 @@ def main():
         torch.cuda.synchronize()
         h.free()
 
-    for w in range(args.warmup):
+    for w in range(warmup):
         t0 = time.time()
         step()
-        print(f"[bench] warmup {w} {time.time() - t0:.3f} s", file=sys.stderr, flush=True)
+        print(f"[bench] {name} warmup {w} {time.time() - t0:.3f} s", file=sys.stderr, flush=True)
     K.kv_timing_read(reset=True)
     K.kv_timing_enable(True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for k in range(args.steps):
+    for k in range(steps):
         step()
-        print(f"[bench] step {k} done", file=sys.stderr, flush=True)
+        print(f"[bench] {name} step {k} done", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     K.kv_timing_enable(False)
     timing = K.kv_timing_read(reset=True)
-    ms_per_step = (t1 - t0) * 1000.0 / args.steps
+    ms_per_step = (t1 - t0) * 1000.0 / steps
     value = n * n_cfg / (ms_per_step / 1000.0)
-
     # replay work: distinct (order, group, policy, capacity) jobs that are replayed
     jobs_accesses, jobs_count = replay_job_accesses(cfgs, stats, n)
-    kern, avg_ms, calls = dominant_kernel(timing, args.steps)
+    kern, avg_ms, calls = dominant_kernel(timing, steps)
     units = stage_units(kern, n, jobs_accesses)
     algo = ALGO_BYTES.get(kern, 5.0) * units
     achieved = algo / (avg_ms / 1000.0) / 1e9
     roof = {"bound": "hbm", "kernel": kern, "achieved": achieved, "peak": HBM_PEAK_GBS,
             "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic_for(kern),
             "avg_launch_ms": avg_ms, "launches": calls,
+            "algorithmic_bytes_per_launch": algo,
             # a replay launch runs one workgroup (on one compute unit) per job
             "workgroups": jobs_count.get(kern[7:]) if kern.startswith("replay_") else None,
-            "stage_ms_per_step": {k: round(v[1] / args.steps, 3) for k, v in timing.items()
+            "stage_ms_per_step": {k: round(v[1] / steps, 3) for k, v in timing.items()
                                   if v[0]}}
+    lim = limiter_for(kern, avg_ms, roof["workgroups"])
+    if lim:
+        roof["limiter"] = lim
+    res = {"name": name, "workload": WORKLOAD_TEXT[name], "value": value,
+           "ms_per_step": ms_per_step, "steps": steps, "warmup": warmup, "n_accesses": n,
+           "n_configs": n_cfg, "n_requests": int(rec.len0.shape[0]), "roofline": roof}
+    if keep:
+        return res, (rec, cfgs, dev, G, model, n)
+    del dev, counts, obj
+    return res, None
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for {args.gpus}); multi-GPU sharding "
+              "is described in the design notes but not built.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import tracegen as tg
+    from paper_2603_08739_amd import host, kvcfg as K
+
+    if args.copy_calibration:
+        src = torch.ones(args.copy_calibration // 4, dtype=torch.int32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(f"[bench] copy calibration: {src.numel() * 4} bytes", file=sys.stderr, flush=True)
+        del src, dst
+    head, ctx = measure(args.workload, args.steps, args.warmup, torch, tg, host, K, keep=True)
+    rec, cfgs, dev, G, model, n = ctx
     ttl = search = prefix = gttl = None
+    workloads = None
     if not args.no_extras:
         ttl, search, prefix, gttl = extras(dev, rec, cfgs, G, model, n, torch, K)
+        del dev
+        torch.cuda.empty_cache()
+        workloads = {}
+        for w in ("tiny", "chat", "tenant", "longctx", "full"):
+            if w == args.workload:
+                continue
+            r, _ = measure(w, 3, 1, torch, tg, host, K)
+            workloads[w] = r
     cpu = None
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
         cpu = cpu_baseline(rec, cfgs, args.cpu_baseline_seconds)
     out = {
-        "metric": METRIC, "value": value, "unit": "block-accesses×configs/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u32",
+        "metric": METRIC, "value": head["value"], "unit": "block-accesses×configs/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": head["ms_per_step"], "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "u32",
         "data": "synthetic (seeded generators shaped like the paper's traces)",
-        "config": {"workload": WORKLOAD_TEXT[args.workload], "name": args.workload,
-                   "n_accesses": n, "n_configs": n_cfg, "n_requests": int(rec.len0.shape[0])},
-        "roofline": roof, "cpu_baseline": cpu, "ttl_curves": ttl, "adaptive_search": search,
-        "group_ttl": gttl, "prefix_reuse": prefix,
+        "config": {"workload": head["workload"], "name": args.workload,
+                   "n_accesses": head["n_accesses"], "n_configs": head["n_configs"],
+                   "n_requests": head["n_requests"]},
+        "roofline": head["roofline"], "cpu_baseline": cpu, "workloads": workloads,
+        "ttl_curves": ttl, "adaptive_search": search, "group_ttl": gttl,
+        "prefix_reuse": prefix,
     }
     print(json.dumps(out))
 

@@ -10,9 +10,12 @@ round's new configurations are evaluated in one ``kv_eval_configs`` call and
 the front comes from ``kv_pareto``: this module only proposes configurations
 and keeps the books.
 
-Conventions (where the paper leaves them open): d and t are integer
-granule capacities of the DRAM and disk tiers (the HBM capacity, mode and
-policy are fixed per search; the paper's second dimension is a disk TTL);
+Conventions (where the paper leaves them open): d is an integer granule
+capacity of the DRAM tier and t either an integer granule capacity of the
+disk tier (the paper's ablation grid, Section 5.3.1) or the disk TTL in
+integer multiples of `ttl_unit` seconds (the paper's planner and Alg. 1:
+an unbounded disk TTL tier, TTL 0 holding nothing); the HBM capacity, mode
+and policy are fixed per search;
 differences are relative, |a - b| / max(|a|, |b|); neighbours are
 consecutive evaluated configurations on a line of constant t or constant d;
 a midpoint must be a new point on the axis' resolution grid,
@@ -36,9 +39,13 @@ class Explorer:
     """One Alg. 1 search over a loaded trace."""
 
     def __init__(self, trace: kvcfg.Trace, n_groups: int, cost_model: kvcfg.kv_cost_model,
-                 hbm: int, mode: int = 0, policy: int = 0, stream=None):
+                 hbm: int, mode: int = 0, policy: int = 0, stream=None, second: str = "disk",
+                 ttl_unit: float = 1.0):
+        if second not in ("disk", "ttl"):
+            raise ValueError("second dimension: 'disk' or 'ttl'")
         self.trace, self.G, self.model = trace, n_groups, cost_model
         self.hbm, self.mode, self.policy, self.stream = hbm, mode, policy, stream
+        self.second, self.ttl_unit = second, float(ttl_unit)
         self.points: list[tuple[int, int]] = []   # evaluation order
         self.obj = np.zeros((0, 3))
         self.index: dict[tuple[int, int], int] = {}
@@ -47,14 +54,22 @@ class Explorer:
     def evaluate(self, pts):
         """(cost, throughput, latency) of configurations (hbm, d, t), one call."""
         n = len(pts)
+        p = np.asarray(pts, dtype=np.int64).reshape(n, 2)
         cap = np.zeros((n, 3), dtype=np.uint64)
         cap[:, 0] = self.hbm
-        cap[:, 1:] = np.asarray(pts, dtype=np.uint64)
+        cap[:, 1] = p[:, 0]
+        disk_ttl = np.zeros(n, dtype=np.uint8)
+        ttl = np.zeros((n, kvcfg.KV_MAX_GROUPS), dtype=np.float64)
+        if self.second == "disk":
+            cap[:, 2] = p[:, 1]
+        else:
+            disk_ttl[:] = 1
+            ttl[:, :] = (p[:, 1] * self.ttl_unit)[:, None]
         cap_group = np.zeros((n, 3, kvcfg.KV_MAX_GROUPS), dtype=np.uint64)
         mode = np.full(n, self.mode, dtype=np.uint8)
         part = np.zeros(n, dtype=np.uint8)
         pol = np.full((n, kvcfg.KV_MAX_GROUPS), self.policy, dtype=np.uint8)
-        arr, n_cfg = kvcfg.config_array(cap, cap_group, mode, part, pol)
+        arr, n_cfg = kvcfg.config_array(cap, cap_group, mode, part, pol, disk_ttl, None, ttl)
         counts = torch.zeros((n, self.G, 3, 8), dtype=torch.int64, device="cuda")
         obj = torch.zeros((n, 3), dtype=torch.float64, device="cuda")
         kvcfg.kv_eval_configs(self.trace, arr, n_cfg, self.model, counts, obj,
