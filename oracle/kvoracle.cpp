@@ -67,7 +67,7 @@ constexpr int kMaxGroups = 16;
 constexpr int kTiers = 3;
 constexpr int kFields = 8;  // hit, miss, ins, evict, hit_w, miss_w, ins_w, evict_w
 enum Field { F_HIT = 0, F_MISS, F_INS, F_EVICT, F_HIT_W, F_MISS_W, F_INS_W, F_EVICT_W };
-enum Policy { P_LRU = 0, P_FIFO = 1, P_LFU = 2 };
+enum Policy { P_LRU = 0, P_FIFO = 1, P_LFU = 2, P_LEAF = 3 };
 enum Mode { M_INCLUSIVE = 0, M_EXCLUSIVE = 1, M_INCLUSIVE_PREFIX = 2 };
 
 struct Block {
@@ -192,10 +192,96 @@ class LfuTier : public Tier {
   std::unordered_map<uint64_t, Info> info_;
 };
 
-Tier* make_tier(int policy, uint64_t cap) {
+// Radix-tree eviction (the prefix tree of a radix KV cache, Section 3.2):
+// the blocks of a request form a chain, each block's parent being the block
+// accessed just before it in the same request.  A cached block is a leaf
+// when no cached block has it as parent; the victim is the leaf whose latest
+// access is the oldest.
+class LeafTier : public Tier {
+ public:
+  LeafTier(uint64_t cap, const std::vector<Block>* acc) : Tier(cap), acc_(acc) {}
+  bool contains(uint64_t h) const override { return node_.count(h) != 0; }
+  void hit(uint64_t h, uint64_t t) override {
+    Node& n = node_.at(h);
+    if (n.kids == 0) {
+      leaves_.erase({n.last, h});
+      leaves_.insert({t, h});
+    }
+    n.last = t;
+  }
+
+ protected:
+  struct Node {
+    Block b;
+    uint64_t last;
+    bool has_parent;
+    uint64_t parent;
+    uint32_t kids;  // cached children
+  };
+  Block pop_victim() override {
+    const auto v = *leaves_.begin();
+    leaves_.erase(leaves_.begin());
+    const Node n = node_.at(v.second);
+    node_.erase(v.second);
+    if (n.has_parent) {
+      auto it = node_.find(n.parent);
+      if (it != node_.end() && --it->second.kids == 0) leaves_.insert({it->second.last, n.parent});
+    }
+    return n.b;
+  }
+  void push(const Block& b, uint64_t t) override {
+    Node n{b, t, false, 0, 0};
+    if (t > 0 && (*acc_)[t - 1].req == b.req) {
+      n.has_parent = true;
+      n.parent = (*acc_)[t - 1].hash;
+      auto it = node_.find(n.parent);
+      if (it != node_.end() && it->second.kids++ == 0) leaves_.erase({it->second.last, n.parent});
+    }
+    node_[b.hash] = n;
+    leaves_.insert({t, b.hash});
+  }
+  const std::vector<Block>* acc_;
+  std::unordered_map<uint64_t, Node> node_;
+  std::set<std::pair<uint64_t, uint64_t>> leaves_;  // (latest access, hash) of the leaves
+};
+
+Tier* make_tier(int policy, uint64_t cap, const std::vector<Block>* acc = nullptr) {
   if (policy == P_LRU) return new LruTier(cap);
   if (policy == P_FIFO) return new FifoTier(cap);
+  if (policy == P_LEAF) return new LeafTier(cap, acc);
   return new LfuTier(cap);
+}
+
+// Radix-tree eviction needs a trace whose requests are prefix chains (a
+// block is re-accessed only in a later request and always after the same
+// parent block) and capacities that hold any one request (a request never
+// evicts its own blocks).  Returns 0 or -4.
+// Whether the requests are prefix chains, and the heaviest request.
+void leaf_trace_info(const std::vector<Block>& acc, bool* chained, uint64_t* max_req_w) {
+  std::unordered_map<uint64_t, std::pair<uint64_t, uint64_t>> seen;  // hash -> (parent+1, req)
+  uint64_t req_w = 0;
+  *chained = true;
+  *max_req_w = 0;
+  for (size_t i = 0; i < acc.size(); ++i) {
+    const bool same = i > 0 && acc[i - 1].req == acc[i].req;
+    const uint64_t par = same ? acc[i - 1].hash + 1 : 0;  // +1: 0 means no parent
+    req_w = same ? req_w + acc[i].w : acc[i].w;
+    *max_req_w = std::max(*max_req_w, req_w);
+    auto it = seen.find(acc[i].hash);
+    if (it != seen.end() && (it->second.first != par || it->second.second == acc[i].req))
+      *chained = false;
+    seen[acc[i].hash] = {par, acc[i].req};
+  }
+}
+
+int check_leaf(const std::vector<Block>& acc, const uint64_t cap[kTiers]) {
+  bool chained;
+  uint64_t max_req_w;
+  leaf_trace_info(acc, &chained, &max_req_w);
+  if (!chained) return -4;
+  for (int k = 0; k < kTiers; ++k)
+    if (cap[k] && cap[k] < max_req_w) return -4;
+  return 0;
 }
 
 // The disk TTL tier: a block is held for ttl[g] seconds after each of its
@@ -286,7 +372,7 @@ void replay_inclusive(const std::vector<Block>& acc, const std::vector<uint32_t>
   Tier* tier[kTiers] = {nullptr, nullptr, nullptr};
   TtlTier* tt = nullptr;
   for (int k = 0; k < kTiers; ++k)
-    if (cap[k] > 0 && !(k == 2 && ttl)) tier[k] = make_tier(policy, cap[k]);
+    if (cap[k] > 0 && !(k == 2 && ttl)) tier[k] = make_tier(policy, cap[k], &acc);
   if (ttl) tier[2] = tt = new TtlTier(cap[2], *ttl, n_groups);
   bool run[kTiers] = {false, false, false};  // the request's blocks so far all available
   bool first = true;
@@ -443,6 +529,16 @@ int replay_one(const std::vector<Block>& acc, const std::vector<std::vector<uint
     replay_inclusive(acc, all, c.cap, P_LRU, false, out, &spec, n_groups, store);
     return 0;
   }
+  for (uint32_t g = 0; g < (c.partitioned ? n_groups : 1u); ++g)
+    if (c.policy[g] > P_LEAF) return -1;
+  if (c.policy[0] == P_LEAF || (c.partitioned && std::count(c.policy, c.policy + n_groups, P_LEAF))) {
+    if (c.partitioned || c.mode != M_INCLUSIVE) return -4;
+    for (int k = 0; k < kTiers; ++k)
+      if (bad_cap(c.cap[k])) return -1;
+    if (const int rc = check_leaf(acc, c.cap)) return rc;
+    replay_inclusive(acc, all, c.cap, P_LEAF, false, out);
+    return 0;
+  }
   if (c.partitioned) {
     for (uint32_t g = 0; g < n_groups; ++g) {
       uint64_t cg[kTiers];
@@ -497,7 +593,8 @@ void memo_run(const std::vector<Block>& acc, const std::vector<uint32_t>& idx, M
               const double* req_time, uint32_t n_groups) {
   TtlTier* tt = nullptr;
   TtlSpec spec{j.ttl, req_time, &acc};
-  Tier* t = j.policy < 0 ? (tt = new TtlTier(j.cap, spec, n_groups)) : make_tier(j.policy, j.cap);
+  Tier* t = j.policy < 0 ? (tt = new TtlTier(j.cap, spec, n_groups))
+                         : make_tier(j.policy, j.cap, &acc);
   j.bits.assign((idx.size() + 63) / 64, 0);
   for (int g = 0; g < kMaxGroups; ++g) j.ins[g] = j.ins_w[g] = j.ev[g] = j.ev_w[g] = 0;
   for (size_t q = 0; q < idx.size(); ++q) {
@@ -805,6 +902,8 @@ int oracle_replay_memo(uint64_t n, const uint64_t* hash, const uint8_t* group,
 
   // plan: distinct (partition, policy, capacity) caches of the inclusive configs
   std::vector<MemoJob> jobs;
+  bool leaf_known = false, leaf_chained = false;
+  uint64_t leaf_max_w = 0;
   // per config and partition, the job of each tier (-1 absent)
   std::vector<std::vector<std::array<int64_t, kTiers>>> use(n_cfg);
   std::vector<uint8_t> literal(n_cfg, 0);
@@ -832,6 +931,18 @@ int oracle_replay_memo(uint64_t n, const uint64_t* hash, const uint8_t* group,
       if (bad_cap(cp[k])) return -1;
     const ConfigView cv{cp, cg, mode[c], partitioned[c], pol, disk_ttl[c], tl};
     if (const int rc = check_ttl(cv, n_groups)) return rc;
+    for (uint32_t g = 0; g < (partitioned[c] ? n_groups : 1u); ++g)
+      if (pol[g] > P_LEAF) return -1;
+    if (pol[0] == P_LEAF || (partitioned[c] && std::count(pol, pol + n_groups, P_LEAF))) {
+      if (partitioned[c] || mode[c] != M_INCLUSIVE) return -4;
+      if (!leaf_known) {
+        leaf_trace_info(acc, &leaf_chained, &leaf_max_w);
+        leaf_known = true;
+      }
+      if (!leaf_chained) return -4;
+      for (int k = 0; k < kTiers; ++k)
+        if (cp[k] && cp[k] < leaf_max_w) return -4;
+    }
     if (mode[c] != M_INCLUSIVE) {
       literal[c] = 1;
       continue;

@@ -96,3 +96,61 @@ def lfu_scan(labels, weights, cap):
         res[b] = [1, t]
         used += weights[b]
     return hits, ev
+
+
+def chain_trace_labels(seed, n_req, n_sys=3, n_docs=12, sys_len=(2, 6), doc_len=(1, 9)):
+    """Requests that are prefix chains of a small tree: each document hangs
+    below one of a few system prompts; a request reads a prefix of
+    (system prompt + document).  Labels: (system s, index j) -> 1000 * s + j,
+    (document d, index j) -> 100000 + 1000 * d + j.  Returns (labels, request
+    index per access)."""
+    import random
+    rnd = random.Random(seed)
+    sys_l = [rnd.randint(*sys_len) for _ in range(n_sys)]
+    docs = [(rnd.randrange(n_sys), rnd.randint(*doc_len)) for _ in range(n_docs)]
+    labels, req = [], []
+    for r in range(n_req):
+        d = min(int(rnd.paretovariate(1.2)) - 1, n_docs - 1)
+        s, dl = docs[d]
+        full = [1000 * s + j for j in range(sys_l[s])] + [100000 + 1000 * d + j for j in range(dl)]
+        k = rnd.randint(1, len(full))
+        labels += full[:k]
+        req += [r] * k
+    return labels, req
+
+
+def leaf_first_distances(labels, req, weights):
+    """Radix-tree eviction as a priority order: a block ranks by (request of
+    its latest access, then shallower first), so at access i of block b,
+    with q the request of b's previous access, the blocks ranked above b
+    are those accessed after request q (up to i); D'_i = w_b + their weight
+    (INF for a first access)."""
+    out, last_req = [], {}
+    end = {}
+    for i, r in enumerate(req):
+        end[r] = i
+    for i, b in enumerate(labels):
+        if b not in last_req:
+            out.append(INF)
+        else:
+            e = end[last_req[b]]
+            seen = set(labels[e + 1:i])
+            out.append(weights[b] + sum(weights[x] for x in seen))
+        last_req[b] = req[i]
+    return out
+
+
+def leaf_first_final(labels, req, weights, cap):
+    """Blocks held at the end: the maximal prefix, of weight <= cap, of the
+    blocks ordered by (latest request descending, position in it ascending)."""
+    last = {}
+    for i, b in enumerate(labels):
+        last[b] = (req[i], i)
+    order = sorted(last, key=lambda b: (-last[b][0], last[b][1]))
+    res, used = [], 0
+    for b in order:
+        if used + weights[b] > cap:
+            break
+        used += weights[b]
+        res.append(b)
+    return res
