@@ -87,7 +87,7 @@ def replay_job_accesses(cfgs, stats, n):
         part = bool(cfgs.partitioned[c]) and G > 1
         for g in range(G if cfgs.partitioned[c] else 1):
             pol = int(cfgs.policy[c, g])
-            if pol == tg.POLICY_LRU:
+            if pol in (tg.POLICY_LRU, tg.POLICY_LEAF):
                 continue
             for k in range(3):
                 x = int(cfgs.cap_group[c, k, g] if cfgs.partitioned[c] else cfgs.cap[c, k])

@@ -75,8 +75,16 @@ enum {
  * victims until used + w <= capacity.  LRU evicts the least recently used
  * block (Section 2.1 names LRU); FIFO the oldest insertion; LFU the smallest
  * (in-cache access count, last access position) - the count starts at 1 on
- * insertion and is forgotten on eviction. */
-enum { KV_POLICY_LRU = 0, KV_POLICY_FIFO = 1, KV_POLICY_LFU = 2 };
+ * insertion and is forgotten on eviction.  LEAF is the eviction of a radix
+ * (prefix-tree) KV cache (Section 3.2): a request's blocks form a chain, the
+ * parent of a block being the block accessed just before it in the same
+ * request; a cached block is a leaf when no cached block has it as parent,
+ * and the victim is the leaf whose latest access is the oldest.  LEAF needs
+ * a trace whose requests are prefix chains (a block is re-accessed only in a
+ * later request, always after the same parent block) and tier capacities
+ * that each hold the heaviest request; it is supported in the inclusive
+ * mode on shared tiers, without a disk TTL tier. */
+enum { KV_POLICY_LRU = 0, KV_POLICY_FIFO = 1, KV_POLICY_LFU = 2, KV_POLICY_LEAF = 3 };
 
 /* Record fields of kv_eval_configs' counts, per (config, group, tier).
  *   hit    accesses served by this tier
@@ -246,7 +254,9 @@ kv_status kv_trace_info(const kv_trace* t, kv_trace_stats* out);
  * (when n_media > 0, else nonzero), disk_ttl > 1, or a disk TTL that is
  * negative or not finite; KV_ERR_UNSUPPORTED for a disk TTL tier outside
  * the inclusive LRU shared mode or bounded with unequal group TTLs, for more
- * than 1,024 distinct TTLs per group in one call, for the exclusive mode with
+ * than 1,024 distinct TTLs per group in one call, for LEAF outside the
+ * inclusive shared mode, on a trace whose requests are not prefix chains, or
+ * with a nonzero capacity below the heaviest request, for the exclusive mode with
  * FIFO/LFU or with blocks of different weights, and for the prefix-reuse
  * mode with FIFO/LFU or partitioned capacities; KV_ERR_NOMEM when not even
  * one replay job's state fits; KV_ERR_DEVICE when an earlier call's replay

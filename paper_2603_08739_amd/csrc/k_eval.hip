@@ -77,7 +77,8 @@ __device__ __forceinline__ void ttl_tier_record(const OrderView& ov, const Joint
 
 __global__ __launch_bounds__(256) void k_lru_counts(const kv_config* __restrict__ cfg,
                                                     uint32_t n_cfg, uint32_t G, OrderView sh,
-                                                    OrderView pt, OrderView px, JointView jv,
+                                                    OrderView pt, OrderView px, OrderView lf,
+                                                    JointView jv,
                                                     const GroupStats* __restrict__ gs,
                                                     uint64_t* __restrict__ counts,
                                                     double* __restrict__ store_cg) {
@@ -87,8 +88,9 @@ __global__ __launch_bounds__(256) void k_lru_counts(const kv_config* __restrict_
   const kv_config& C = cfg[c];
   const bool part = C.partitioned != 0;
   const uint32_t pol = part ? C.policy[g] : C.policy[0];
-  if (pol != KV_POLICY_LRU) return;
-  const OrderView& ov = (part && G > 1) ? pt : sh;
+  if (pol != KV_POLICY_LRU && pol != KV_POLICY_LEAF) return;
+  // radix-tree eviction: distances of the re-touched order (shared tiers only)
+  const OrderView& ov = pol == KV_POLICY_LEAF ? lf : (part && G > 1) ? pt : sh;
   uint64_t cap[3];
   for (int k = 0; k < 3; ++k) cap[k] = part ? C.cap_group[k][g] : C.cap[k];
   const uint64_t N = gs[g].n_g, NW = gs[g].n_w_g;
@@ -331,14 +333,15 @@ __global__ __launch_bounds__(256) void k_pareto_count(const uint8_t* __restrict_
 }  // namespace
 
 kv_status lru_counts(const kv_config* cfg_dev, uint32_t n_cfg, uint32_t n_groups,
-                     OrderView shared, OrderView part, OrderView prefix, JointView joint,
+                     OrderView shared, OrderView part, OrderView prefix, OrderView leaf,
+                     JointView joint,
                      const GroupStats* gs_dev, uint64_t* counts, double* store_cg,
                      hipStream_t s) {
   const uint64_t m = (uint64_t)n_cfg * n_groups;
   if (m == 0) return KV_OK;
   StageTimer tm(kStLruCounts, s);
   hipLaunchKernelGGL(k_lru_counts, dim3(div_up(m, 256)), dim3(256), 0, s, cfg_dev, n_cfg,
-                     n_groups, shared, part, prefix, joint, gs_dev, counts, store_cg);
+                     n_groups, shared, part, prefix, leaf, joint, gs_dev, counts, store_cg);
   KV_HIP(hipGetLastError());
   return KV_OK;
 }

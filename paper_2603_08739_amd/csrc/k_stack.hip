@@ -357,7 +357,8 @@ __global__ __launch_bounds__(256) void k_sd_assemble(const uint32_t* __restrict_
                                                      const uint32_t* __restrict__ partial,
                                                      const uint32_t* __restrict__ E,
                                                      const uint32_t* __restrict__ RQ,
-                                                     BinArgs ba, uint32_t* __restrict__ dout) {
+                                                     BinArgs ba, uint32_t* __restrict__ dout,
+                                                     const uint8_t* __restrict__ real) {
   __shared__ uint32_t sthr[kLds ? kThrLds : 1];
   __shared__ uint32_t scnt[kLds ? kThrLds + KV_MAX_GROUPS : 1];
   __shared__ uint32_t sw[kLds ? kThrLds + KV_MAX_GROUPS : 1];
@@ -378,6 +379,7 @@ __global__ __launch_bounds__(256) void k_sd_assemble(const uint32_t* __restrict_
     const uint64_t row = X >= 2 ? tri_off(X - 1) : 0;
     for (uint32_t j = threadIdx.x; j < nb; j += 256) {
       const uint64_t i = base + j;
+      if (real && !real[i]) continue;  // a re-touch of the radix-tree order: not binned
       const uint32_t kk = key[i];
       if (kk == 0) {
         if (dout) dout[i] = kNone;  // a first access: no finite distance
@@ -777,8 +779,8 @@ uint32_t grid_of(uint64_t m, uint32_t cap = 32768) {
 
 kv_status stack_pass(Trace& t, Order& o, bool partitioned, const ThresholdSet& ts,
                      const uint32_t* thr_dev, const uint32_t* off_dev, uint64_t* hist,
-                     uint64_t* phist, const JointArgs* ja, hipStream_t s) {
-  const uint64_t n = t.n;
+                     uint64_t* phist, const JointArgs* ja, const uint8_t* real, hipStream_t s) {
+  const uint64_t n = o.n ? o.n : t.n;
   const uint32_t G = div_up(n, kSdB);
   kv_status st;
   const uint64_t tri = G >= 2 ? tri_off(G) : 1;
@@ -844,11 +846,11 @@ kv_status stack_pass(Trace& t, Order& o, bool partitioned, const ThresholdSet& t
   if (lds)
     hipLaunchKernelGGL(k_sd_assemble<true>, dim3(ga), dim3(256), 0, s, key, w8, g8, n, G,
                        (const uint32_t*)b_partial.as<uint32_t>(),
-                       (const uint32_t*)b_E.as<uint32_t>(), (const uint32_t*)Q, ba, dist);
+                       (const uint32_t*)b_E.as<uint32_t>(), (const uint32_t*)Q, ba, dist, real);
   else
     hipLaunchKernelGGL(k_sd_assemble<false>, dim3(ga), dim3(256), 0, s, key, w8, g8, n, G,
                        (const uint32_t*)b_partial.as<uint32_t>(),
-                       (const uint32_t*)b_E.as<uint32_t>(), (const uint32_t*)Q, ba, dist);
+                       (const uint32_t*)b_E.as<uint32_t>(), (const uint32_t*)Q, ba, dist, real);
   KV_HIP(hipGetLastError());
   if (phist) {
     const uint32_t nr = t.st.n_req;

@@ -286,8 +286,13 @@ kv_status validate_configs(const Trace& t, const kv_config* cfg, uint32_t n_cfg,
       if (C.cap[k] != 0 && C.cap[k] < wmax)
         return fail(KV_ERR_INVALID, at + "a tier capacity is below the largest block weight");
     const uint32_t ng = C.partitioned ? G : 1;
-    for (uint32_t g = 0; g < ng; ++g)
-      if (C.policy[g] > KV_POLICY_LFU) return fail(KV_ERR_INVALID, at + "unknown policy");
+    for (uint32_t g = 0; g < ng; ++g) {
+      if (C.policy[g] > KV_POLICY_LEAF) return fail(KV_ERR_INVALID, at + "unknown policy");
+      if (C.policy[g] == KV_POLICY_LEAF &&
+          (C.partitioned || C.mode != KV_MODE_INCLUSIVE || C.disk_ttl))
+        return fail(KV_ERR_UNSUPPORTED,
+                    at + "radix-tree eviction needs the inclusive mode on shared tiers");
+    }
     if (C.partitioned) {
       for (int k = 0; k < 3; ++k) {
         uint64_t sum = 0;
@@ -413,7 +418,8 @@ struct StackSlot {
 };
 
 kv_status run_stack(Trace& t, Order& o, bool partitioned, ThresholdSet& ts, StackSlot slot,
-                    OrderView& view, OrderView& pview, const JointArgs* ja, hipStream_t s) {
+                    OrderView& view, OrderView& pview, const JointArgs* ja, const uint8_t* real,
+                    hipStream_t s) {
   kv_status st;
   DevBuf& bt = t.ws[slot.ws_thr];
   DevBuf& bh = t.ws[slot.ws_hist];
@@ -433,7 +439,8 @@ kv_status run_stack(Trace& t, Order& o, bool partitioned, ThresholdSet& ts, Stac
     if ((st = fill_u64(bp.as<uint64_t>(), 0, nbins * 4, s)) != KV_OK) return st;
     ph = bp.as<uint64_t>();
   }
-  if ((st = stack_pass(t, o, partitioned, ts, thr, off, bh.as<uint64_t>(), ph, ja, s)) != KV_OK)
+  if ((st = stack_pass(t, o, partitioned, ts, thr, off, bh.as<uint64_t>(), ph, ja, real, s)) !=
+      KV_OK)
     return st;
   view.thr = thr;
   view.off = off;
@@ -638,11 +645,29 @@ kv_status kv_eval_configs(const kv_trace* h, const kv_config* cfg, uint32_t n_cf
   if (!cfg || !counts) return fail(KV_ERR_INVALID, "kv_eval_configs: cfg and counts are required");
   if ((st = validate_configs(*t, cfg, n_cfg, model->n_media)) != KV_OK) return st;
   hipStream_t s = (hipStream_t)stream;
+  bool need_leaf = false;
+  for (uint32_t c = 0; c < n_cfg; ++c) need_leaf |= !cfg[c].partitioned && cfg[c].policy[0] == KV_POLICY_LEAF;
+  if (need_leaf) {
+    // radix-tree eviction: a trace of prefix-chain requests, each fitting every tier
+    if ((st = leaf_prepare(*t, s)) != KV_OK) return st;
+    if (!t->leaf_chained)
+      return fail(KV_ERR_UNSUPPORTED, "kv_eval_configs: radix-tree eviction needs requests that "
+                                      "are prefix chains of blocks");
+    for (uint32_t c = 0; c < n_cfg; ++c) {
+      if (cfg[c].partitioned || cfg[c].policy[0] != KV_POLICY_LEAF) continue;
+      for (int k = 0; k < 3; ++k)
+        if (cfg[c].cap[k] && cfg[c].cap[k] < t->max_req_w)
+          return fail(KV_ERR_UNSUPPORTED, "kv_eval_configs: config " + std::to_string(c) +
+                                              ": radix-tree eviction needs every tier to hold "
+                                              "the heaviest request (" +
+                                              std::to_string(t->max_req_w) + " granules)");
+    }
+  }
   const uint32_t G = t->n_groups;
   t->cfg_stage.assign(cfg, cfg + n_cfg);
 
   // ---- plan: thresholds per order, replay jobs
-  std::vector<std::vector<uint32_t>> tsh(G), tpt(G);
+  std::vector<std::vector<uint32_t>> tsh(G), tpt(G), tlf(G);
   std::vector<std::vector<double>> tttl(G);  // disk TTL values per group
   bool need_shared = false, need_part = false, need_prefix = false, need_joint = false;
   const uint64_t w0 = t->st.w_max;
@@ -654,6 +679,10 @@ kv_status kv_eval_configs(const kv_trace* h, const kv_config* cfg, uint32_t n_cf
     const uint32_t ng = C.partitioned ? G : 1;
     for (uint32_t g = 0; g < ng; ++g) {
       const uint32_t pol = group_policy(C, g);
+      if (pol == KV_POLICY_LEAF) {
+        for (uint32_t gg = 0; gg < G; ++gg) add_thresholds(tlf, C, 0, gg, w0);
+        continue;
+      }
       if (pol == KV_POLICY_LRU) {
         need_prefix |= C.mode == KV_MODE_INCLUSIVE_PREFIX;
         if (C.disk_ttl) {
@@ -721,7 +750,7 @@ kv_status kv_eval_configs(const kv_trace* h, const kv_config* cfg, uint32_t n_cf
   // ---- LRU: stack-distance passes + closed forms
   auto lru = [&]() -> kv_status {
     kv_status r;
-    OrderView vsh, vpt, vpx, unused;
+    OrderView vsh, vpt, vpx, vlf, unused;
     JointArgs ja;
     JointView jv;
     if (need_shared) {
@@ -729,17 +758,23 @@ kv_status kv_eval_configs(const kv_trace* h, const kv_config* cfg, uint32_t n_cf
       if (need_joint && (r = plan_joint(*t, tttl, ja, jv, s)) != KV_OK) return r;
       if ((r = run_stack(*t, t->shared, false, t->shared_ts,
                          StackSlot{5, 6, need_prefix ? 24 : -1}, vsh, vpx,
-                         need_joint ? &ja : nullptr, s)) != KV_OK)
+                         need_joint ? &ja : nullptr, nullptr, s)) != KV_OK)
+        return r;
+    }
+    if (need_leaf) {
+      finish_set(t->leaf_ts, tlf, G);
+      if ((r = run_stack(*t, t->leaf, false, t->leaf_ts, StackSlot{30, 31, -1}, vlf, unused,
+                         nullptr, t->leaf_real.as<uint8_t>(), s)) != KV_OK)
         return r;
     }
     if (need_part) {
       finish_set(t->part_ts, tpt, G);
       if ((r = run_stack(*t, t->part, true, t->part_ts, StackSlot{7, 8, -1}, vpt, unused,
-                         nullptr, s)) != KV_OK)
+                         nullptr, nullptr, s)) != KV_OK)
         return r;
     }
-    if (need_shared || need_part)
-      return lru_counts(cfg_dev, n_cfg, G, vsh, vpt, vpx, jv, bgs.as<GroupStats>(), counts,
+    if (need_shared || need_part || need_leaf)
+      return lru_counts(cfg_dev, n_cfg, G, vsh, vpt, vpx, vlf, jv, bgs.as<GroupStats>(), counts,
                         store_cg, s);
     return KV_OK;
   };

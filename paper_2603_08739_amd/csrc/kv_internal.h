@@ -57,6 +57,7 @@ struct Order {
   DevBuf w;     // u8[n]
   DevBuf g;     // u8[n]
   uint64_t seg[KV_MAX_GROUPS + 1] = {0};  // group segments (partitioned order)
+  uint64_t n = 0;                          // positions (0: the trace's accesses)
   bool built = false;
 };
 
@@ -112,6 +113,13 @@ struct Trace {
   uint32_t tpg = 0;   // tokens per granule
   Order shared;       // trace order
   Order part;         // partitioned order (built on first use when n_groups > 1)
+  // Radix-tree eviction: the trace with every request followed by a re-touch
+  // of its blocks, deepest first (built on first use); `leaf_real` flags
+  // the positions that are accesses of the trace.
+  Order leaf;
+  DevBuf leaf_real;   // u8[2n]
+  bool leaf_checked = false, leaf_chained = false;
+  uint64_t max_req_w = 0;  // heaviest request (granules)
   DevBuf blk_w;       // u8[u]  weight per dense block id
   DevBuf blk_g;       // u8[u]  group per dense block id
   DevBuf req;         // u32[n] request of each access (trace order)
@@ -128,7 +136,7 @@ struct Trace {
   std::vector<ReplayJobInfo> err_jobs;  // the replayed jobs of the latest call
   ~Trace();
   // host staging of the latest kv_eval_configs call (alive across its copies)
-  ThresholdSet shared_ts, part_ts;
+  ThresholdSet shared_ts, part_ts, leaf_ts;
   TtlSet ttl_ts;
   std::vector<uint32_t> joint_stage;
   std::vector<kv_config> cfg_stage;
@@ -172,6 +180,11 @@ kv_status fill_u64(uint64_t* p, uint64_t v, uint64_t m, hipStream_t s);
 kv_status canon_build(Trace& t, const kv_trace_desc& d, hipStream_t s);
 kv_status canon_partition(Trace& t, hipStream_t s);
 
+// radix-tree eviction (k_leaf.hip): checks once whether the requests are
+// prefix chains and finds the heaviest request; if they are chains, builds
+// t.leaf and t.leaf_real.
+kv_status leaf_prepare(Trace& t, hipStream_t s);
+
 // stack-distance pass (k_stack.hip)
 // hist: u64[total_bins][4] = {count, weight, final count, final weight},
 // made cumulative over the bins of each group on return.
@@ -180,9 +193,11 @@ kv_status canon_partition(Trace& t, hipStream_t s);
 // count the accesses by their request-prefix distance (prefix reuse).
 // ja (or NULL; trace order only): the joint histograms of disk TTL tiers,
 // made cumulative over both bin dimensions (and wd over gap bins) on return.
+// real (or NULL): per position, whether it is binned (the radix-tree order's
+// re-touches are not).
 kv_status stack_pass(Trace& t, Order& o, bool partitioned, const ThresholdSet& ts,
                      const uint32_t* thr_dev, const uint32_t* off_dev, uint64_t* hist,
-                     uint64_t* phist, const JointArgs* ja, hipStream_t s);
+                     uint64_t* phist, const JointArgs* ja, const uint8_t* real, hipStream_t s);
 
 // per-configuration evaluation (k_eval.hip)
 
@@ -207,7 +222,8 @@ struct JointView {
 // Disk TTL tiers take tier 2 from `joint` and write the storage-time
 // integral of each unbounded one per (config, group) to store_cg.
 kv_status lru_counts(const kv_config* cfg_dev, uint32_t n_cfg, uint32_t n_groups,
-                     OrderView shared, OrderView part, OrderView prefix, JointView joint,
+                     OrderView shared, OrderView part, OrderView prefix, OrderView leaf,
+                     JointView joint,
                      const GroupStats* gs_dev, uint64_t* counts, double* store_cg,
                      hipStream_t s);
 // store_cg: [n_cfg][n_groups] or NULL (no disk TTL tier in the batch).

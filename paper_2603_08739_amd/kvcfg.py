@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libkvcfg.so")
 KV_OK, KV_ERR_INVALID, KV_ERR_NOMEM, KV_ERR_DEVICE, KV_ERR_UNSUPPORTED = 0, -1, -2, -3, -4
 KV_MAX_GROUPS, KV_TIERS, KV_FIELDS = 16, 3, 8
 KV_MODE_INCLUSIVE, KV_MODE_EXCLUSIVE_DEMOTE, KV_MODE_INCLUSIVE_PREFIX = 0, 1, 2
-KV_POLICY_LRU, KV_POLICY_FIFO, KV_POLICY_LFU = 0, 1, 2
+KV_POLICY_LRU, KV_POLICY_FIFO, KV_POLICY_LFU, KV_POLICY_LEAF = 0, 1, 2, 3
 FIELDS = ("hit", "miss", "ins", "evict", "hit_w", "miss_w", "ins_w", "evict_w")
 
 _u64, _u32, _u8, _f64, _vp = (ctypes.c_uint64, ctypes.c_uint32, ctypes.c_uint8,

@@ -10,11 +10,11 @@ from .workloads import (Trace, Recipe, recipe, make, tiny, chat, tenant, longctx
 from .configs import (ConfigBatch, configs_for, grid, from_list, empty, split_capacity,
                       random_configs,
                       DEFAULT_COST, MODE_INCLUSIVE, MODE_EXCLUSIVE_DEMOTE, MODE_INCLUSIVE_PREFIX, POLICY_LRU,
-                      POLICY_FIFO, POLICY_LFU, MAX_GROUPS, GIB, TIB)
+                      POLICY_FIFO, POLICY_LFU, POLICY_LEAF, MAX_GROUPS, GIB, TIB)
 
 __all__ = [
     "Trace", "Recipe", "recipe", "make", "tiny", "chat", "tenant", "longctx", "full", "from_blocks",
     "random_trace", "WORKLOADS", "GENERATOR_VERSION", "ConfigBatch", "configs_for", "grid", "from_list",
     "empty", "split_capacity", "random_configs", "DEFAULT_COST", "MODE_INCLUSIVE", "MODE_EXCLUSIVE_DEMOTE", "MODE_INCLUSIVE_PREFIX",
-    "POLICY_LRU", "POLICY_FIFO", "POLICY_LFU", "MAX_GROUPS", "GIB", "TIB",
+    "POLICY_LRU", "POLICY_FIFO", "POLICY_LFU", "POLICY_LEAF", "MAX_GROUPS", "GIB", "TIB",
 ]

@@ -11,7 +11,7 @@ Encodings (shared input format of the library and the oracle):
           accesses), 1 = exclusive with write-back demotion (LRU only),
           2 = inclusive with prefix reuse (a request reuses a run of its
           blocks from its first block on; LRU, shared caches only).
-* policy: 0 = LRU, 1 = FIFO, 2 = LFU.
+* policy: 0 = LRU, 1 = FIFO, 2 = LFU, 3 = radix-tree leaf-first LRU.
 * partitioned: 0 = one cache per tier shared by all groups (policy[0]);
                1 = tier capacity split per group (cap_group[k][g], policy[g]).
 
@@ -34,6 +34,7 @@ MODE_INCLUSIVE_PREFIX = 2
 POLICY_LRU = 0
 POLICY_FIFO = 1
 POLICY_LFU = 2
+POLICY_LEAF = 3
 
 GIB = 1 << 30
 TIB = 1 << 40
