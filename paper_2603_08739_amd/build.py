@@ -45,7 +45,7 @@ def _compile(src: str, objdir: str = BUILD, extra=()) -> str:
 
 def build(jobs: int = 6, out: str = LIB, extra=()) -> str:
     """Compile and link; `out` and `extra` (more hipcc flags) give variant
-    builds, e.g. a diagnostics build with -DKV_REPLAY_STATS elsewhere."""
+    builds elsewhere."""
     objdir = BUILD if out == LIB else os.path.join(BUILD, "variant")
     os.makedirs(objdir, exist_ok=True)
     with cf.ThreadPoolExecutor(max_workers=jobs) as ex:

@@ -77,42 +77,14 @@ constexpr int kCScan = 2;                  // candidate positions per thread and
 constexpr uint32_t kMinFast = 256;         // shorter LFU chunks go serial
 constexpr uint32_t kHeadLds = 64;          // class heads held in LDS during a serial walk
 constexpr uint16_t kInf16 = 0xFFFF;
-#ifndef KV_LFU_NT
-#define KV_LFU_NT 1024
-#endif
-constexpr int kLfuNT = KV_LFU_NT;           // threads of an LFU replay workgroup
-#ifndef KV_LFU_CHUNK
-#define KV_LFU_CHUNK 4096
-#endif
-constexpr uint32_t kLChunk = KV_LFU_CHUNK;  // longest LFU chunk
+constexpr int kLfuNT = 1024;               // threads of an LFU replay workgroup
+constexpr uint32_t kLChunk = 4096;         // longest LFU chunk
 constexpr uint32_t kLdsClass = 1024;       // LFU count classes (held in LDS)
 constexpr uint32_t kTopClass = kLdsClass - 1;  // the class of every count >= kTopClass
 constexpr uint32_t kLdsClassWords = kLdsClass / 64;
 static_assert(kRIt == 4, "hit words are assembled from four ballots");
 
 // Optional per-job replay statistics (diagnostics build only).
-#ifdef KV_REPLAY_STATS
-enum { kStFastOk = 0, kStFailPool, kStFailElig, kStFailConv, kStSerialAcc, kStIters,
-       kStScanned, kStFastAcc, kStT0, kStT1, kStT2, kStT3, kStT4, kStT5, kStT6, kStT7, kStT8, kStW0, kStW1, kStW2, kStW3, kStW4, kStW5, kStW6, kStW7, kStF0, kStF1, kStF2, kStF3, kStF4, kStG0, kStG1, kStG2, kStQpt, kStNc0, kStNm, kStJob, kStSer, kStFR1, kStFR2, kStFR3, kStFPos, kStFLen, kStats };
-__shared__ unsigned int s_fr, s_fpos;
-__device__ unsigned long long g_rstats[256][kStats];
-__shared__ unsigned long long s_rstats[kStats];  // flushed to g_rstats when the job ends
-__shared__ unsigned long long s_rwave[8];
-#define RSTAT(j, k, v) do { if (threadIdx.x == 0) s_rstats[k] += (unsigned long long)(v); } while (0)
-#define RCLK(t) const unsigned long long t = clock64()
-// per chunk, the latest wave's (clock - t0) at this point, summed over chunks
-#define RWAVE(k, t0) do { unsigned long long _d = clock64() - (t0); \
-    if (lane_id() == 0) atomicMax(&s_rwave[k], _d); } while (0)
-#define RWAVE_FLUSH() do { __syncthreads(); if (threadIdx.x < 4) { s_rstats[kStT6 + threadIdx.x % 3] += 0; } \
-    if (threadIdx.x == 0) { for (int _q = 0; _q < 8; ++_q) { s_rstats[kStW0 + _q] += s_rwave[_q]; s_rwave[_q] = 0; } } } while (0)
-#define RTIME(k, t0, t1) RSTAT(blockIdx.x, k, (t1) - (t0))
-#else
-#define RSTAT(j, k, v) do { } while (0)
-#define RCLK(t) do { } while (0)
-#define RTIME(k, t0, t1) do { } while (0)
-#define RWAVE(k, t0) do { } while (0)
-#define RWAVE_FLUSH() do { } while (0)
-#endif
 
 __device__ __forceinline__ uint32_t ld_acq(const uint32_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -406,7 +378,6 @@ __device__ __forceinline__ void fifo_chunked(const JobDev& j, const JobArgs& a,
   BlockAny block_any{F.anyflag, 0};
   uint32_t W0 = 0;
   for (uint64_t c0 = cstart; c0 < j.end; c0 += L) {
-    RCLK(f_a);
     bool v[kRIt], vb[kRIt], miss[kRIt];
     chunk_valid(j, c0, L, v);
     chunk_valid(j, c0 + L, L, vb);
@@ -416,8 +387,6 @@ __device__ __forceinline__ void fifo_chunked(const JobDev& j, const JobArgs& a,
     uint32_t warm[kRIt];
 #pragma unroll
     for (int e = 0; e < kRIt; ++e) warm[e] = S[vb[e] ? B.b[e] : 0u];
-    RWAVE(0, f_a);
-    RWAVE(1, f_a);
     int lp[kRIt];
     uint32_t ww[kRIt], wi[kRIt];
 #pragma unroll
@@ -428,18 +397,11 @@ __device__ __forceinline__ void fifo_chunked(const JobDev& j, const JobArgs& a,
       miss[e] = false;
     }
     uint32_t tot = 0;
-    RWAVE(2, f_a);
-    RCLK(f_b);
-    RTIME(kStT0, f_a, f_b);
     for (uint32_t it = 0; it < L + 2; ++it) {
-      RSTAT(blockIdx.x, kStIters, 1);
       uint32_t x = 0;
 #pragma unroll
       for (int e = 0; e < kRIt; ++e) x += miss[e] ? ww[e] : 0u;
-      RCLK(g_a);
       const uint32_t pre = block_excl_scan_u32<kRNT>(x, F.red, tot);
-      RCLK(g_b);
-      RTIME(kStT6, g_a, g_b);
       uint32_t run = W0 + pre;
       uint32_t exw = 0;
 #pragma unroll
@@ -451,8 +413,6 @@ __device__ __forceinline__ void fifo_chunked(const JobDev& j, const JobArgs& a,
       }
       *reinterpret_cast<uint32_t*>(&F.ex[l0]) = exw;
       __syncthreads();
-      RCLK(g_c);
-      RTIME(kStT7, g_b, g_c);
       bool changed = false;
 #pragma unroll
       for (int e = 0; e < kRIt; ++e) {
@@ -462,13 +422,9 @@ __device__ __forceinline__ void fifo_chunked(const JobDev& j, const JobArgs& a,
         miss[e] = nm;
       }
       const bool again = block_any(changed);
-      RCLK(g_d);
-      RTIME(kStT8, g_c, g_d);
       if (!again) break;
     }
     // tot and wi belong to the final miss set
-    RCLK(f_c);
-    RTIME(kStT1, f_b, f_c);
     bool hit[kRIt];
     uint32_t ci = 0, cw = 0;
 #pragma unroll
@@ -489,9 +445,7 @@ __device__ __forceinline__ void fifo_chunked(const JobDev& j, const JobArgs& a,
     if (g1) add_uniform(&gc.ins[g0], &gc.insw[g0], ci, cw);
     W0 += tot;
     store_hits(hit, c0, L, j, bits);
-    RWAVE(3, f_a);
     __syncthreads();
-    RWAVE_FLUSH();
     // the next chunk's states after this chunk's insertions (the early
     // loads are kept alive, not used, so that they are issued)
 #pragma unroll
@@ -503,9 +457,6 @@ __device__ __forceinline__ void fifo_chunked(const JobDev& j, const JobArgs& a,
     B = C;
 #pragma unroll
     for (int e = 0; e < kRIt; ++e) sa[e] = sb[e];
-    RCLK(f_d);
-    RTIME(kStT2, f_c, f_d);
-    RSTAT(blockIdx.x, kStFastOk, 1);
   }
   // evictions = insertions - blocks still queued at the end
   if (tid < KV_MAX_GROUPS) F.fin[tid] = F.finw[tid] = 0;
@@ -1015,7 +966,6 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   const uint32_t L = c1 - c0;
   const uint32_t l0 = tid * IT;
   const uint32_t p0 = c0 + l0;
-  RCLK(t_a);
   ItemBits v;
 #pragma unroll
   for (int e = 0; e < IT; ++e) v.set(e, l0 + e < L && p0 + e >= jb);
@@ -1123,7 +1073,6 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     xc += cm[e] ? 1u : 0u;
   }
   uint32_t itot0, nm0, wpre0, mpre0;
-  RWAVE(0, t_a);
   // block scans alternate between two LDS buffers and skip their trailing
   // barrier (every call has a barrier, so a buffer is reused only after
   // all threads have left the call before)
@@ -1149,9 +1098,6 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       }
     }
   }
-  RCLK(t_b);
-  RTIME(kStT0, t_a, t_b);
-  RWAVE(1, t_a);
   uint32_t nc0 = 0;
   bool reached = false;
   if (ev0 > 0) {
@@ -1162,7 +1108,6 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     uint64_t vw = 0;
     for (bool first = true;; first = false) {
       if (vw >= ev0 || h >= c0 || n0 >= kCand) break;
-      RSTAT(blockIdx.x, kStScanned, 1);
       // each position lists at most one entry: near the end of the buffer
       // the step shrinks to the room left
       const uint32_t hend = min(min<uint32_t>(h + NT * kCScan, h + (kCand - n0)), c0);
@@ -1214,9 +1159,6 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   } else {
     h = head1_io;
   }
-  RCLK(t_c);
-  RTIME(kStT1, t_b, t_c);
-  RWAVE(2, t_a);
   // ---- fixed point over (misses, promotions, evictions)
   uint32_t itot = itot0;   // weight of the chunk's misses (insertions)
   uint32_t nmiss = nm0;     // and their number
@@ -1226,8 +1168,6 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
 #pragma unroll
   for (int e = 0; e < IT; ++e) capnow[e] = false;
   for (int it = 0; !converged && it < 24; ++it) {
-    RSTAT(blockIdx.x, kStIters, 1);
-    RCLK(t_it);
     bool mi[IT], oldcap[IT];
     uint32_t nm = nm0;
 #pragma unroll
@@ -1265,12 +1205,8 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     const uint32_t nq = nc0 + nm;
     const uint32_t qpt = (nq + NT - 1) / NT;
     if (qpt > (uint32_t)CPT) {
-      RSTAT(blockIdx.x, kStFailPool, 1);
       return false;
     }
-    RSTAT(blockIdx.x, kStQpt, qpt);
-    RSTAT(blockIdx.x, kStNc0, nc0);
-    RSTAT(blockIdx.x, kStNm, nm);
     uint32_t qw[CPT];
     uint32_t xs = 0;
 #pragma unroll
@@ -1286,8 +1222,6 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     }
     uint32_t elig;
     uint32_t run = block_excl_scan_u32<NT, false>(xs, S.red[rg++ & 1], elig);
-    RCLK(t_f0);
-    RTIME(kStF0, t_it, t_f0);
     bool bad = elig < evtot;
     // entry k is consumed by the first miss whose demand exceeds the
     // eligible weight queued before k.  Demands and prefixes both rise, so
@@ -1333,17 +1267,11 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
             // a new entry can only go after it was inserted, and only once
             // every old one is gone
             if (evk[e] <= S.mpos[k - nc0] || !reached) bad = true;
-#ifdef KV_REPLAY_STATS
-            if (evk[e] <= S.mpos[k - nc0]) { atomicOr(&s_fr, 2u); atomicMin(&s_fpos, evk[e]); }
-            if (!reached) atomicOr(&s_fr, 4u);
-#endif
           }
         }
         run += qw[e];
       }
     }
-    RCLK(t_f2);
-    RTIME(kStF1, t_f0, t_f2);
     // the pointer reaches entry k when the first consumed entry at or after k goes
     uint32_t suf[CPT];
     uint32_t mn = kInf16;
@@ -1355,17 +1283,6 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     uint32_t tmin;
     bool anybad;
     block_suffix_min_flag<NT>(mn, bad, S.sfx, tmin, anybad);
-    RCLK(t_f3);
-    RTIME(kStF2, t_f2, t_f3);
-#ifdef KV_REPLAY_STATS
-    if (anybad && tid == 0) {
-      if (elig < evtot) s_rstats[kStFR1] += 1;
-      if (s_fr & 2u) { s_rstats[kStFR2] += 1; s_rstats[kStFPos] += s_fpos; s_rstats[kStFLen] += L; }
-      if (s_fr & 4u) s_rstats[kStFR3] += 1;
-      s_fr = 0;
-      s_fpos = 0xFFFFFFFFu;
-    }
-#endif
     // A shortfall of count-1 victims found here may be an artefact of the
     // skip flags, which start out assuming that every entry touched in the
     // chunk is touched before its turn: the update below can make such an
@@ -1399,8 +1316,6 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       if (ncap) S.capm[ak] = ns;  // each touch position is the next touch of one entry
     }
     __syncthreads();
-    RCLK(t_f4);
-    RTIME(kStF3, t_f3, t_f4);
 #pragma unroll
     for (int e = 0; e < IT; ++e) {
       const uint32_t loc = l0 + e;
@@ -1410,23 +1325,16 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       // miss status changed with the capacity misses, counted above)
       if (v[e] && !mi[e] && S.mcons[loc]) S.mcons[loc] = 0;
     }
-    RWAVE(3, t_a);
     if (!block_any(changed)) {
       if (anybad) {
-        RSTAT(blockIdx.x, kStFailElig, 1);
         return false;
       }
       converged = true;
     }
-    RCLK(t_f5);
-    RTIME(kStF4, t_f4, t_f5);
   }
   if (!converged) {
-    RSTAT(blockIdx.x, kStFailConv, 1);
     return false;
   }
-  RCLK(t_d);
-  RTIME(kStT2, t_c, t_d);
   // ---- consistent: apply.  First the next chunk's stored counts at links
   // before this chunk (final already; a link inside it reads this chunk's
   // final counts once they are known).
@@ -1518,9 +1426,6 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       if (!block_any(moved)) break;
     }
   }
-  RCLK(t_e);
-  RTIME(kStT3, t_d, t_e);
-  RWAVE(4, t_a);
   // per-thread partials: evictions (and, 16 bits up, old count-1 entries
   // leaving class 1), evicted weight, last entries taken.  Insertions are
   // the misses, counted by the fixed point.
@@ -1544,8 +1449,6 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     // it: no store)
     if (untouched) p_evn += 1u << 16;
   }
-  RCLK(t_e1);
-  RTIME(kStT6, t_e, t_e1);
   // per-access chunk data, loaded for all items at once
   uint32_t mc[IT], nxl[IT], lm[IT], oc[IT];
 #pragma unroll
@@ -1587,8 +1490,6 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       p_lastm = max(p_lastm, loc + 1);
     }
   }
-  RCLK(t_e2);
-  RTIME(kStT7, t_e1, t_e2);
   // final state of every touched block, at its last touch.  Moves into and
   // out of classes 1 and 2 (the crowded ones) add up per wavefront by
   // ballot; the others go one by one.
@@ -1625,8 +1526,6 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   // end), so that waits for the earlier gather need not cover them.
 #pragma unroll
   for (int e = 0; e < IT; ++e) cnt[v[e] ? c0 + l0 + e - jb : je - jb] = fin[e] ? fnew[e] : 0u;
-  RCLK(t_e3);
-  RTIME(kStT8, t_e2, t_e3);
   if (lane_id() == 0) {
     if (d12[0]) atomicAdd(&S.ccnt[1], (uint32_t)d12[0]);
     if (d12[1]) atomicAdd(&S.ccnt[2], (uint32_t)d12[1]);
@@ -1642,10 +1541,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
       if (r[0] >> 16) atomicSub(&S.ccnt[1], r[0] >> 16);
     }
   }
-  RWAVE(5, t_a);
   __syncthreads();
-  RCLK(t_f);
-  RTIME(kStT4, t_e, t_f);
   // the next chunk's stored counts at links before this chunk (a link
   // inside it was filled in by its last touch above; only a link before the
   // next chunk is ever read)
@@ -1669,8 +1565,6 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   }
   // the nonempty-class bitmap is rebuilt only when class 1 is empty (the
   // serial walk rebuilds it before it starts)
-  RCLK(t_f1);
-  RTIME(kStG0, t_f, t_f1);
   const bool c1empty = S.ccnt[1] == 0u;
   if (c1empty) class_bits_rebuild<NT>(S);
   store_hits_n<IT>(hit, c0, L, j, bits);
@@ -1689,9 +1583,6 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   if (t_lastm) head1_io = c0 + t_lastm;                 // last new entry taken + 1
   else if (t_lastp) head1_io = S.cq[t_lastp - 1] + 1;   // last old entry taken + 1
   else head1_io = h;
-  RWAVE(6, t_a);
-  RCLK(t_f2);
-  RTIME(kStG1, t_f1, t_f2);
   if (c1empty) {
     // the lowest nonempty class, for the serial walk (class 1 otherwise)
     __syncthreads();
@@ -1702,14 +1593,6 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   } else if (tid == 0) {
     S.fmin = 1;
   }
-  RCLK(t_f3);
-  RTIME(kStG2, t_f2, t_f3);
-  RCLK(t_g);
-  RTIME(kStT5, t_f, t_g);
-  RWAVE(7, t_a);
-  RWAVE_FLUSH();
-  RSTAT(blockIdx.x, kStFastOk, 1);
-  RSTAT(blockIdx.x, kStFastAcc, L);
   return true;
 }
 
@@ -1753,7 +1636,6 @@ __device__ __forceinline__ void lfu_chunked(const JobDev& j, const JobArgs& a,
       class_bits_rebuild<NT>(S);
       lfu_serial_stage<NT>(j, a, cnt, head, a.n_class, S, (uint32_t)pos, (uint32_t)(pos + l));
       __syncthreads();
-      RCLK(t_s0);
       if (wave_id() == 0) {
         const bool ok = lfu_serial_wave(j, a, cnt, head, a.n_class, cl, S, gc, bits,
                                         (uint32_t)pos, (uint32_t)(pos + l), used, head1);
@@ -1763,9 +1645,6 @@ __device__ __forceinline__ void lfu_chunked(const JobDev& j, const JobArgs& a,
           S.head1 = head1;
         }
       }
-      RSTAT(blockIdx.x, kStSerialAcc, l);
-      RCLK(t_s1);
-      RTIME(kStSer, t_s0, t_s1);
       __syncthreads();
       used = S.used;
       head1 = S.head1;
@@ -1812,10 +1691,6 @@ __global__ __launch_bounds__(kRNT) void k_replay(const JobDev* __restrict__ jobs
   const JobArgs a = job_args(a_in, j);
   const uint32_t tid = threadIdx.x;
   if (tid < KV_MAX_GROUPS) gc.ins[tid] = gc.insw[tid] = gc.ev[tid] = gc.evw[tid] = 0;
-#ifdef KV_REPLAY_STATS
-  if (tid < kStats) s_rstats[tid] = 0;
-  if (tid < 8) s_rwave[tid] = 0;
-#endif
   __syncthreads();
   // one group for every access of the job: counters add up per wavefront
   const bool g1 = a.n_groups == 1 || j.group != KV_MAX_GROUPS;
@@ -1828,9 +1703,6 @@ __global__ __launch_bounds__(kRNT) void k_replay(const JobDev* __restrict__ jobs
     fifo_serial(j, a, reinterpret_cast<uint32_t*>(state + j.state_off), bits + j.bits_off, gc);
   __syncthreads();
   write_counters(gc, a.n_groups, cnt);
-#ifdef KV_REPLAY_STATS
-  if (tid < kStats) g_rstats[blockIdx.x & 255][tid] += s_rstats[tid];
-#endif
 }
 
 // LFU jobs, NT threads per job; G1: the jobs whose accesses all belong to
@@ -1847,20 +1719,9 @@ __global__ __launch_bounds__(NT) void k_replay_lfu(const JobDev* __restrict__ jo
   JobDev j = jobs[blockIdx.x];
   if (j.closed || j.kind != kJobLfu) return;
   if (lfu_one_group(j, a_in.n_groups) != G1) return;
-#ifdef KV_REPLAY_STATS
-  const unsigned long long tj0 = wall_clock64();
-  if (threadIdx.x == 0) {
-    s_fr = 0;
-    s_fpos = 0xFFFFFFFFu;
-  }
-#endif
   const JobArgs a = job_args(a_in, j);
   const uint32_t tid = threadIdx.x;
   if (tid < KV_MAX_GROUPS) gc.ins[tid] = gc.insw[tid] = gc.ev[tid] = gc.evw[tid] = 0;
-#ifdef KV_REPLAY_STATS
-  if (tid < kStats) s_rstats[tid] = 0;
-  if (tid < 8) s_rwave[tid] = 0;
-#endif
   __syncthreads();
   const uint32_t g0 = j.group == KV_MAX_GROUPS ? 0u : j.group;
   unsigned long long* cnt = jcnt + (uint64_t)blockIdx.x * a.n_groups * 4;
@@ -1871,11 +1732,6 @@ __global__ __launch_bounds__(NT) void k_replay_lfu(const JobDev* __restrict__ jo
   write_counters(gc, a.n_groups, cnt);
   // a failed state check is recorded for the host (the first failing job wins)
   if (tid == 0 && !ok && atomicCAS(&a.err[0], 0u, 1u) == 0u) atomicExch(&a.err[1], blockIdx.x);
-#ifdef KV_REPLAY_STATS
-  RSTAT(blockIdx.x, kStJob, wall_clock64() - tj0);
-  __syncthreads();
-  if (tid < kStats) g_rstats[blockIdx.x & 255][tid] += s_rstats[tid];
-#endif
 }
 
 // Per order: re-access bits (key != 0), weight bit-planes, group masks.
@@ -2646,33 +2502,6 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
         if (any[k] && (st = launch(k, s, x)) != KV_OK) return st;
     }
   }
-#ifdef KV_REPLAY_STATS
-  {
-    KV_HIP(hipStreamSynchronize(s));
-    unsigned long long hs[256][kStats];
-    KV_HIP(hipMemcpyFromSymbol(hs, HIP_SYMBOL(g_rstats), sizeof(hs)));
-    for (uint32_t q = 0; q < nj && q < 256; ++q) {
-      if (jd[q].closed) continue;
-      fprintf(stderr, "[replay-stats] %s job %u cap %llu: fast %llu (acc %llu) failpool %llu "
-              "failelig %llu failconv %llu serial_acc %llu iters %llu scanned %llu "
-              "clk load %llu scan %llu fix %llu jump %llu apply %llu fin %llu x6 %llu x7 %llu x8 %llu "
-              "w0 %llu w1 %llu w2 %llu w3 %llu w4 %llu w5 %llu w6 %llu w7 %llu "
-              "f0 %llu f1 %llu f2 %llu f3 %llu f4 %llu g0 %llu g1 %llu g2 %llu qpt %llu "
-              "nc0 %llu nm %llu job %llu ser %llu fr1 %llu fr2 %llu fr3 %llu fpos %llu flen %llu\n",
-              jd[q].kind == kJobLfu ? "lfu" : "fifo", q,
-              (unsigned long long)jd[q].cap, hs[q][kStFastOk], hs[q][kStFastAcc],
-              hs[q][kStFailPool], hs[q][kStFailElig], hs[q][kStFailConv], hs[q][kStSerialAcc],
-              hs[q][kStIters], hs[q][kStScanned], hs[q][kStT0], hs[q][kStT1], hs[q][kStT2],
-              hs[q][kStT3], hs[q][kStT4], hs[q][kStT5], hs[q][kStT6], hs[q][kStT7], hs[q][kStT8],
-              hs[q][kStW0], hs[q][kStW1], hs[q][kStW2], hs[q][kStW3], hs[q][kStW4],
-              hs[q][kStW5], hs[q][kStW6], hs[q][kStW7], hs[q][kStF0], hs[q][kStF1],
-              hs[q][kStF2], hs[q][kStF3], hs[q][kStF4], hs[q][kStG0], hs[q][kStG1],
-              hs[q][kStG2], hs[q][kStQpt], hs[q][kStNc0], hs[q][kStNm], hs[q][kStJob],
-              hs[q][kStSer], hs[q][kStFR1], hs[q][kStFR2], hs[q][kStFR3], hs[q][kStFPos],
-              hs[q][kStFLen]);
-    }
-  }
-#endif
   tm.reset();
   if (!recs.empty()) {
     tm.emplace(kStCombine, s);

@@ -25,10 +25,7 @@ namespace kv {
 namespace {
 
 constexpr int kTtlNT = 1024;       // threads per workgroup
-#ifndef KV_TTL_U
-#define KV_TTL_U 8
-#endif
-constexpr int kTtlU = KV_TTL_U;    // accesses per thread per step (gathers in flight)
+constexpr int kTtlU = 8;           // accesses per thread per step (gathers in flight)
 static_assert(kTtlU % 4 == 0, "accesses are read four at a time");
 constexpr uint32_t kTtlMax = 1024; // TTL values per call
 constexpr uint32_t kTtlBins = 4096;  // groups * (TTL values + 1)
