@@ -134,12 +134,28 @@ __global__ __launch_bounds__(256) void k_sd_colapply(uint32_t* __restrict__ Q, u
 // ---------------------------------------------------------------------------
 // In-block dominance by LDS merge sort.
 // ---------------------------------------------------------------------------
+// Element i of a block-wide LDS array lives at pd(i): one padding word after
+// every 16, so that the 16-element runs of the threads of a wavefront (and
+// the merge positions inside them, about 8 apart) fall into different banks.
+constexpr uint32_t kSdPad = kSdB + kSdB / 16;
+__device__ __forceinline__ uint32_t pd(uint32_t i) { return i + (i >> 4); }
+
 struct SortLds {
-  uint32_t v[kSdB];     // sorted keys of the current runs
-  uint32_t pw[kSdB];    // inclusive prefix weight inside each run
-  uint32_t acc[kSdB];   // accumulated weight of smaller keys at earlier positions
-  uint16_t idx[kSdB];   // local position of the element
+  uint32_t v[kSdPad];     // sorted keys of the current runs
+  uint32_t pw[kSdPad];    // inclusive prefix weight inside each run
+  uint32_t acc[kSdPad];   // accumulated weight of smaller keys at earlier positions
+  uint16_t idx[kSdPad];   // local position of the element
 };
+
+// First index in S.v[lo, hi) (padded, sorted) with a value > x.
+__device__ __forceinline__ uint32_t upper_bound_pd(const uint32_t* a, uint32_t lo, uint32_t hi,
+                                                   uint32_t x) {
+  while (lo < hi) {
+    const uint32_t mid = (lo + hi) >> 1;
+    if (a[pd(mid)] <= x) lo = mid + 1; else hi = mid;
+  }
+  return lo;
+}
 
 template <int N>
 __device__ __forceinline__ void cswap(uint32_t (&v)[N], uint32_t (&w)[N], uint32_t (&a)[N],
@@ -187,7 +203,7 @@ __device__ void block_sort_dominance(SortLds& S, const uint32_t (&vin)[kLocItems
 #pragma unroll
   for (int e = 0; e < kLocItems; ++e) {
     run += w[e];
-    const uint32_t s = t * kLocItems + e;
+    const uint32_t s = pd(t * kLocItems + e);
     S.v[s] = v[e];
     S.pw[s] = run;
     S.acc[s] = a[e];
@@ -203,31 +219,32 @@ __device__ void block_sort_dominance(SortLds& S, const uint32_t (&vin)[kLocItems
     uint32_t lo = d0 > s ? d0 - s : 0u, hi = min(d0, s);
     while (lo < hi) {
       const uint32_t mid = (lo + hi) >> 1;
-      if (S.v[Lb + mid] <= S.v[Rb + d0 - mid - 1]) lo = mid + 1; else hi = mid;
+      if (S.v[pd(Lb + mid)] <= S.v[pd(Rb + d0 - mid - 1)]) lo = mid + 1; else hi = mid;
     }
     uint32_t ia = lo, ib = d0 - lo;
 #pragma unroll
     for (int e = 0; e < kLocItems; ++e) {
-      const bool takeL = (ib >= s) || (ia < s && S.v[Lb + ia] <= S.v[Rb + ib]);
+      const uint32_t li = pd(Lb + ia), ri = pd(Rb + ib);
+      const bool takeL = (ib >= s) || (ia < s && S.v[li] <= S.v[ri]);
       if (takeL) {
-        v[e] = S.v[Lb + ia];
-        a[e] = S.acc[Lb + ia];
-        x[e] = S.idx[Lb + ia];
-        pw[e] = S.pw[Lb + ia] + (ib ? S.pw[Rb + ib - 1] : 0u);
+        v[e] = S.v[li];
+        a[e] = S.acc[li];
+        x[e] = S.idx[li];
+        pw[e] = S.pw[li] + (ib ? S.pw[pd(Rb + ib - 1)] : 0u);
         ++ia;
       } else {
-        const uint32_t pl = ia ? S.pw[Lb + ia - 1] : 0u;
-        v[e] = S.v[Rb + ib];
-        a[e] = S.acc[Rb + ib] + pl;
-        x[e] = S.idx[Rb + ib];
-        pw[e] = pl + S.pw[Rb + ib];
+        const uint32_t pl = ia ? S.pw[pd(Lb + ia - 1)] : 0u;
+        v[e] = S.v[ri];
+        a[e] = S.acc[ri] + pl;
+        x[e] = S.idx[ri];
+        pw[e] = pl + S.pw[ri];
         ++ib;
       }
     }
     __syncthreads();
 #pragma unroll
     for (int e = 0; e < kLocItems; ++e) {
-      const uint32_t o = o0 + e;
+      const uint32_t o = pd(o0 + e);
       S.v[o] = v[e];
       S.acc[o] = a[e];
       S.idx[o] = (uint16_t)x[e];
@@ -246,7 +263,7 @@ __global__ __launch_bounds__(kLocNT, 1) void k_sd_local(const uint32_t* __restri
                                                         uint32_t* __restrict__ partial,
                                                         uint32_t* __restrict__ E) {
   __shared__ SortLds S;
-  __shared__ uint32_t P[kSdB];
+  __shared__ uint32_t P[kSdPad];   // padded like S
   __shared__ uint32_t sh[kLocNT / 64 + 1];
   const uint32_t X = blockIdx.x;
   const uint64_t base = (uint64_t)X * kSdB;
@@ -254,15 +271,15 @@ __global__ __launch_bounds__(kLocNT, 1) void k_sd_local(const uint32_t* __restri
   const uint32_t t = threadIdx.x;
   for (uint32_t j = t; j < kSdB; j += kLocNT) {
     const bool in = j < nb;
-    S.v[j] = in ? key[base + j] : kSentinel;
-    S.acc[j] = in ? nxt[base + j] : kNone;
-    S.pw[j] = in ? (uint32_t)w8[base + j] : 0u;
+    S.v[pd(j)] = in ? key[base + j] : kSentinel;
+    S.acc[pd(j)] = in ? nxt[base + j] : kNone;
+    S.pw[pd(j)] = in ? (uint32_t)w8[base + j] : 0u;
   }
   __syncthreads();
   uint32_t k[kLocItems], nx[kLocItems], w[kLocItems];
 #pragma unroll
   for (int e = 0; e < kLocItems; ++e) {
-    const uint32_t j = t * kLocItems + e;
+    const uint32_t j = pd(t * kLocItems + e);
     k[e] = S.v[j];
     nx[e] = S.acc[j];
     w[e] = S.pw[j];
@@ -284,21 +301,21 @@ __global__ __launch_bounds__(kLocNT, 1) void k_sd_local(const uint32_t* __restri
   const uint32_t pre2 = block_excl_scan<kLocNT>(run2, sh, &tot);
 #pragma unroll
   for (int e = 0; e < kLocItems; ++e) {
-    P[t * kLocItems + e] = loc[e] + pre;
+    P[pd(t * kLocItems + e)] = loc[e] + pre;
     sn[e] += pre2;
   }
   // ---- sort 1: keys -> A(i)
   block_sort_dominance(S, k, w);
 #pragma unroll
   for (int e = 0; e < kLocItems; ++e) {
-    const uint32_t s = t * kLocItems + e;
-    const uint32_t i = S.idx[s];
-    const uint32_t kk = S.v[s];
+    const uint32_t s = t * kLocItems + e, sp = pd(s);
+    const uint32_t i = S.idx[sp];
+    const uint32_t kk = S.v[sp];
     if (i < nb && kk != 0u) {
-      const uint32_t wi = S.pw[s] - (s ? S.pw[s - 1] : 0u);
+      const uint32_t wi = S.pw[sp] - (s ? S.pw[pd(s - 1)] : 0u);
       const uint32_t p = kk - 1u;
-      uint32_t d = wi + S.acc[s];
-      if ((uint64_t)p >= base) d -= P[p - base];
+      uint32_t d = wi + S.acc[sp];
+      if ((uint64_t)p >= base) d -= P[pd((uint32_t)(p - base))];
       partial[base + i] = d;
     }
   }
@@ -310,8 +327,8 @@ __global__ __launch_bounds__(kLocNT, 1) void k_sd_local(const uint32_t* __restri
     ev[e] = 0;
     if (lp < nb && nx[e] != kNone && (nx[e] >> kSdLogB) > X) {
       const uint32_t p = (uint32_t)(base + lp);
-      const uint32_t ub = upper_bound(S.v, 0u, kSdB, p);
-      ev[e] = (ub ? S.pw[ub - 1] : 0u) - P[lp];
+      const uint32_t ub = upper_bound_pd(S.v, 0u, kSdB, p);
+      ev[e] = (ub ? S.pw[pd(ub - 1)] : 0u) - P[pd(lp)];
     }
   }
   __syncthreads();
@@ -326,16 +343,16 @@ __global__ __launch_bounds__(kLocNT, 1) void k_sd_local(const uint32_t* __restri
   block_sort_dominance(S, v2, w);
 #pragma unroll
   for (int e = 0; e < kLocItems; ++e) {
-    const uint32_t s = t * kLocItems + e;
+    const uint32_t s = pd(t * kLocItems + e);
     const uint32_t i = S.idx[s];
-    if (i < nb) P[i] = S.acc[s];
+    if (i < nb) P[pd(i)] = S.acc[s];
   }
   __syncthreads();
 #pragma unroll
   for (int e = 0; e < kLocItems; ++e) {
     const uint32_t lp = t * kLocItems + e;
     if (lp < nb && nx[e] != kNone && (nx[e] >> kSdLogB) > X)
-      E[base + lp] = ev[e] + (P[lp] - sn[e]);
+      E[base + lp] = ev[e] + (P[pd(lp)] - sn[e]);
   }
 }
 
