@@ -42,8 +42,8 @@
 namespace kv {
 namespace {
 
-constexpr int kLocNT = 512;
-constexpr int kLocItems = 16;
+constexpr int kLocNT = 1024;
+constexpr int kLocItems = 8;
 static_assert(kLocNT * kLocItems == (int)kSdB, "block tile mismatch");
 constexpr uint32_t kSentinel = 0xFFFFFFFFu;
 constexpr uint32_t kRowChunk = 16384;   // LDS histogram bins per row chunk
