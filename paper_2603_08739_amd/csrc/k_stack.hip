@@ -170,6 +170,14 @@ __device__ __forceinline__ void cswap(uint32_t (&v)[N], uint32_t (&w)[N], uint32
   }
 }
 
+// LDS exchange among the lanes of one wavefront: its LDS operations execute
+// in issue order, so a compiler fence at wavefront scope suffices.
+__device__ __forceinline__ void wave_sync_lds() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // On return S holds the block's elements sorted by v, each with
 // acc = sum over earlier positions j of w_j [v_j < v] (exact whenever v is
 // unique in the block, i.e. for every element whose acc is used).
@@ -187,7 +195,7 @@ __device__ void block_sort_dominance(SortLds& S, const uint32_t (&vin)[kLocItems
     for (int f = 0; f < e; ++f) s += (vin[f] < vin[e]) ? win[f] : 0u;
     a[e] = s;
   }
-  // bitonic network on 16 register-resident elements
+  // bitonic network on the thread's register-resident elements
 #pragma unroll
   for (int k = 2; k <= kLocItems; k <<= 1) {
 #pragma unroll
@@ -211,7 +219,9 @@ __device__ void block_sort_dominance(SortLds& S, const uint32_t (&vin)[kLocItems
   }
   uint32_t pw[kLocItems];
   for (uint32_t s = kLocItems; s < kSdB; s <<= 1) {
-    __syncthreads();
+    // a pair of runs of s spans 2s / kLocItems threads: up to 64, one wavefront
+    const bool in_wave = 2 * s <= 64u * kLocItems;
+    if (in_wave) wave_sync_lds(); else __syncthreads();
     const uint32_t o0 = t * kLocItems;
     const uint32_t pair = o0 & ~(2 * s - 1);
     const uint32_t d0 = o0 - pair;
@@ -241,7 +251,7 @@ __device__ void block_sort_dominance(SortLds& S, const uint32_t (&vin)[kLocItems
         ++ib;
       }
     }
-    __syncthreads();
+    if (in_wave) wave_sync_lds(); else __syncthreads();
 #pragma unroll
     for (int e = 0; e < kLocItems; ++e) {
       const uint32_t o = pd(o0 + e);
