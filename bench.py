@@ -70,6 +70,50 @@ def parse():
     return ap.parse_args()
 
 
+# Groups of library stages reported together, with the method's minimum bytes
+# per access (A1: read hash 8 + weight 1 + group 1, write both links 8; A3:
+# read each key 4 and weight 1 once for every LRU capacity).
+STAGE_GROUPS = {
+    "load": (("load_validate", "load_sort", "load_links"), 18.0),
+    "stack_pass": (("stack_matrix", "stack_local", "stack_assemble", "stack_final"), 5.0),
+}
+
+
+def stage_table(timing, steps, n, jobs_accesses, jobs_count):
+    """Per hot stage: average launch time and algorithmic bytes per launch
+    against the HBM peak (the dominant stage is reported on its own)."""
+    out = {}
+
+    def put(name, ms_step, calls_step, algo_launch, extra=None):
+        if not calls_step or ms_step <= 0:
+            return
+        avg = ms_step / calls_step
+        ach = algo_launch / (avg / 1000.0) / 1e9
+        rec = {"avg_launch_ms": round(avg, 3), "launches_per_step": calls_step,
+               "algorithmic_bytes_per_launch": algo_launch, "achieved": ach,
+               "unit": "GB/s", "frac": ach / HBM_PEAK_GBS, "traffic": traffic_for(name)}
+        rec.update(extra or {})
+        out[name] = rec
+
+    for g, (names, per) in STAGE_GROUPS.items():
+        ms = sum(timing[k][1] for k in names if k in timing) / steps
+        # one launch of the group per step (the load and the stack pass run once)
+        put(g, ms, 1, per * n, {"stages": list(names)})
+    for k in ("stack_local", "replay_fifo", "replay_lfu"):
+        if k in timing and timing[k][0]:
+            calls = timing[k][0] / steps
+            put(k, timing[k][1] / steps, calls,
+                ALGO_BYTES[k] * stage_units(k, n, jobs_accesses) / calls,
+                {"workgroups": jobs_count.get(k[7:])} if k.startswith("replay_") else None)
+    if "replay_combine" in timing and timing["replay_combine"][0]:
+        calls = timing["replay_combine"][0] / steps
+        # each launch reads the hit bits of its jobs and 8 weight bit-planes once
+        jobs = sum(jobs_count.values())
+        put("replay_combine", timing["replay_combine"][1] / steps, calls,
+            (jobs + 8 * calls) * n / 8.0 / calls)
+    return out
+
+
 def stage_units(stage, n, jobs_accesses):
     if stage.startswith("replay_") and stage[7:] in jobs_accesses:
         return jobs_accesses[stage[7:]]
@@ -118,13 +162,18 @@ def traffic_for(kernel):
     if not os.path.exists(path):
         return None
     rec = json.load(open(path)).get(kernel)
-    if not rec:
-        return None
-    src = os.path.join(ROOT, "paper_2603_08739_amd", "csrc", rec["source"])
-    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
-    if sha != rec.get("source_sha"):
+    if not rec or source_sha(rec["source"]) != rec.get("source_sha"):
         return None
     return rec["bytes_per_launch"]
+
+
+def source_sha(files):
+    """Hash of the kernel sources a counter record was taken with (one file
+    or a list of files, concatenated)."""
+    h = hashlib.sha256()
+    for f in [files] if isinstance(files, str) else files:
+        h.update(open(os.path.join(ROOT, "paper_2603_08739_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
 
 
 # What bounds a kernel that is not bound by HBM: its VALU instruction count
@@ -142,8 +191,7 @@ def limiter_for(kernel, avg_ms, workgroups):
     rec = json.load(open(path)).get(kernel)
     if not rec:
         return None
-    src = os.path.join(ROOT, "paper_2603_08739_amd", "csrc", rec["source"])
-    if hashlib.sha256(open(src, "rb").read()).hexdigest()[:16] != rec.get("source_sha"):
+    if source_sha(rec["source"]) != rec.get("source_sha"):
         return None
     rate = rec["valu_insts_per_launch"] / (avg_ms / 1000.0)
     cus = min(workgroups or CU_COUNT, CU_COUNT)
@@ -442,7 +490,14 @@ def measure(name, steps, warmup, torch, tg, host, K, keep=False):
                                   if v[0]}}
     lim = limiter_for(kern, avg_ms, roof["workgroups"])
     if lim:
-        roof["limiter"] = lim
+        # the replay is bound by instruction issue and latency, not by HBM:
+        # the roofline is the chip's VALU issue rate, the HBM figures stay
+        # beside it
+        roof["hbm"] = {"achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                       "frac": achieved / HBM_PEAK_GBS}
+        roof.update({"bound": "alu", "achieved": lim["achieved"], "peak": lim["peak_chip"],
+                     "unit": lim["unit"], "frac": lim["frac_chip"], "limiter": lim})
+    roof["stages"] = stage_table(timing, steps, n, jobs_accesses, jobs_count)
     res = {"name": name, "workload": WORKLOAD_TEXT[name], "value": value,
            "ms_per_step": ms_per_step, "steps": steps, "warmup": warmup, "n_accesses": n,
            "n_configs": n_cfg, "n_requests": int(rec.len0.shape[0]), "roofline": roof}

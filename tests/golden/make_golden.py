@@ -8,9 +8,13 @@ replayed literally one by one) over the trace the seeded generator builds on
 the CPU.  Nothing here touches the GPU library.  Each file records the
 generator version, the seed, a sha256 of the trace arrays and of the
 configuration batch, and the indices of the configurations it covers: all
-of them, except the long-context workload's 2,048 exclusive configurations,
-where the 8 corners of its 8 x 16 x 16 grid plus 56 seeded draws (exclusive
-configurations cannot share caches, so each one is a full literal replay).
+of them, except for the two largest batches: of the long-context workload's
+2,048 exclusive configurations the 8 corners of its 8 x 16 x 16 grid plus 56
+seeded draws (exclusive configurations cannot share caches, so each one is a
+full literal replay), and of the full workload's 11,000 configurations over
+387 M accesses the 8 corners of its LRU grid, 8 more LRU draws and 8 draws
+each of its FIFO and LFU points (every distinct tier cache is a literal
+replay of the whole trace).
 """
 from __future__ import annotations
 
@@ -39,6 +43,16 @@ def golden_path(name: str) -> str:
 
 
 def subset(name: str, n_cfg: int) -> np.ndarray:
+    if name == "full":
+        # 10,000 LRU grid points (25 x 20 x 20, index (h * 20 + d) * 20 + s),
+        # then 500 FIFO and 500 LFU points: the 8 LRU grid corners, 8 more
+        # LRU draws and 8 draws of each replay policy
+        corners = [(h * 20 + d) * 20 + s for h in (0, 24) for d in (0, 19) for s in (0, 19)]
+        rng = np.random.default_rng([5, 23])
+        lru = rng.choice(np.setdiff1d(np.arange(10000), corners), size=8, replace=False)
+        fifo = 10000 + rng.choice(500, size=8, replace=False)
+        lfu = 10500 + rng.choice(500, size=8, replace=False)
+        return np.sort(np.concatenate([corners, lru, fifo, lfu])).astype(np.uint32)
     if name != "longctx":
         return np.arange(n_cfg, dtype=np.uint32)
     # grid index = (h * 16 + d) * 16 + s over the 8 x 16 x 16 grid
