@@ -58,8 +58,12 @@ __host__ __device__ __forceinline__ uint64_t tri_off(uint64_t x) { return x * (x
 __global__ __launch_bounds__(256) void k_sd_rowhist(const uint32_t* __restrict__ key,
                                                     const uint8_t* __restrict__ w8, uint64_t n,
                                                     uint32_t row_chunk, uint32_t* __restrict__ Q) {
-  __shared__ uint32_t h[kRowChunk];
+  // bin j lives at hp(j), one padding word after every 64: the scan below
+  // gives each thread a run of up to 64 bins, which would otherwise put every
+  // lane of a wavefront on one bank
+  __shared__ uint32_t h[kRowChunk + kRowChunk / 64];
   __shared__ uint32_t sh[8];
+  const auto hp = [](uint32_t j) { return j + (j >> 6); };
   const uint32_t X = blockIdx.x;
   if (X == 0) return;
   const uint64_t base = (uint64_t)X * kSdB;
@@ -67,29 +71,29 @@ __global__ __launch_bounds__(256) void k_sd_rowhist(const uint32_t* __restrict__
   const uint64_t row = tri_off(X);
   for (uint32_t c0 = 0; c0 < X; c0 += row_chunk) {
     const uint32_t width = min(row_chunk, X - c0);
-    for (uint32_t j = threadIdx.x; j < width; j += 256) h[j] = 0;
+    for (uint32_t j = threadIdx.x; j < width; j += 256) h[hp(j)] = 0;
     __syncthreads();
     uint32_t carry = 0;
     for (uint32_t j = threadIdx.x; j < nb; j += 256) {
       const uint32_t c = (key[base + j] + (kSdB - 1)) >> kSdLogB;
       const uint32_t w = w8[base + j];
       if (c < c0) carry += w;
-      else if (c < c0 + width) atomicAdd(&h[c - c0], w);
+      else if (c < c0 + width) atomicAdd(&h[hp(c - c0)], w);
     }
     carry = block_sum<256>(carry, sh);
     // inclusive scan of h[0, width) in LDS, each thread a contiguous run
     const uint32_t per = (width + 255) / 256;
     const uint32_t a = min(width, threadIdx.x * per), b = min(width, a + per);
     uint32_t run = 0;
-    for (uint32_t j = a; j < b; ++j) run += h[j];
+    for (uint32_t j = a; j < b; ++j) run += h[hp(j)];
     uint32_t tot;
     uint32_t pre = block_excl_scan<256>(run, sh, &tot) + carry;
     for (uint32_t j = a; j < b; ++j) {
-      pre += h[j];
-      h[j] = pre;
+      pre += h[hp(j)];
+      h[hp(j)] = pre;
     }
     __syncthreads();
-    for (uint32_t j = threadIdx.x; j < width; j += 256) Q[row + c0 + j] = h[j];
+    for (uint32_t j = threadIdx.x; j < width; j += 256) Q[row + c0 + j] = h[hp(j)];
     __syncthreads();
   }
 }
