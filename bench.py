@@ -63,7 +63,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the TTL-curve, adaptive-search, group-TTL and prefix-reuse "
-                         "measurements that follow the timed steps")
+                         "measurements and the other workloads' lines that follow the "
+                         "timed steps")
+    ap.add_argument("--ttl-extra-only", action="store_true",
+                    help="of the measurements after the timed steps, only the TTL curves")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="first run one plain device-to-device copy of BYTES (a reference "
                          "for hardware byte counters)")
@@ -79,7 +82,7 @@ STAGE_GROUPS = {
 }
 
 
-def stage_table(timing, steps, n, jobs_accesses, jobs_count):
+def stage_table(workload, timing, steps, n, jobs_accesses, jobs_count):
     """Per hot stage: average launch time and algorithmic bytes per launch
     against the HBM peak (the dominant stage is reported on its own)."""
     out = {}
@@ -91,7 +94,7 @@ def stage_table(timing, steps, n, jobs_accesses, jobs_count):
         ach = algo_launch / (avg / 1000.0) / 1e9
         rec = {"avg_launch_ms": round(avg, 3), "launches_per_step": calls_step,
                "algorithmic_bytes_per_launch": algo_launch, "achieved": ach,
-               "unit": "GB/s", "frac": ach / HBM_PEAK_GBS, "traffic": traffic_for(name)}
+               "unit": "GB/s", "frac": ach / HBM_PEAK_GBS, "traffic": traffic_for(workload, name)}
         rec.update(extra or {})
         out[name] = rec
 
@@ -156,12 +159,13 @@ def dominant_kernel(timing, steps):
     return best, best_ms / max(calls, 1), calls
 
 
-def traffic_for(kernel):
-    """HBM bytes per launch from committed rocprofv3 counter runs, if still valid."""
+def traffic_for(workload, stage):
+    """HBM bytes per launch of a stage on a workload, from committed
+    rocprofv3 counter runs, while the kernel sources are unchanged."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
-    rec = json.load(open(path)).get(kernel)
+    rec = json.load(open(path)).get(workload, {}).get(stage)
     if not rec or source_sha(rec["source"]) != rec.get("source_sha"):
         return None
     return rec["bytes_per_launch"]
@@ -184,11 +188,11 @@ def source_sha(files):
 CU_COUNT, CLOCK_HZ = 256, 2.4e9
 
 
-def limiter_for(kernel, avg_ms, workgroups):
+def limiter_for(workload, kernel, avg_ms, workgroups):
     path = os.path.join(ROOT, "profiles", "valu.json")
     if not os.path.exists(path):
         return None
-    rec = json.load(open(path)).get(kernel)
+    rec = json.load(open(path)).get(workload, {}).get(kernel)
     if not rec:
         return None
     if source_sha(rec["source"]) != rec.get("source_sha"):
@@ -387,7 +391,7 @@ def prefix_reuse(h, cfgs, G, model, torch, K):
     return out
 
 
-def extras(dev, rec, cfgs, G, model, n, torch, K):
+def extras(dev, rec, cfgs, G, model, n, torch, K, ttl_only=False):
     """Measurements outside the timed step: TTL curves, Alg. 1, prefix reuse,
     Alg. 2."""
     # TTL curves (disk-tier retention for the group TTL) over the same trace,
@@ -407,15 +411,18 @@ def extras(dev, rec, cfgs, G, model, n, torch, K):
     torch.cuda.synchronize()
     K.kv_timing_enable(False)
     t_calls, t_ms = K.kv_timing_read(reset=True)["ttl_curves"]
-    search = adaptive_search(h, rec, G, model, torch, K)
-    prefix = prefix_reuse(h, cfgs, G, model, torch, K)
+    search = prefix = gttl = None
+    if not ttl_only:
+        search = adaptive_search(h, rec, G, model, torch, K)
+        prefix = prefix_reuse(h, cfgs, G, model, torch, K)
     h.free()
-    gttl = group_ttl(dev, rec, torch, K)
+    if not ttl_only:
+        gttl = group_ttl(dev, rec, torch, K)
     ttl_ms = t_ms / max(t_calls, 1)
     ttl_ach = ALGO_BYTES["ttl_curves"] * n / (ttl_ms / 1000.0) / 1e9
     ttl = {"n_ttl": len(TTL_GRID), "avg_launch_ms": ttl_ms, "launches": t_calls,
            "bound": "hbm", "achieved": ttl_ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-           "frac": ttl_ach / HBM_PEAK_GBS, "traffic": traffic_for("ttl_curves")}
+           "frac": ttl_ach / HBM_PEAK_GBS, "traffic": traffic_for(rec.name, "ttl_curves")}
     print(f"[bench] TTL curves {ttl_ms:.3f} ms", file=sys.stderr, flush=True)
     return ttl, search, prefix, gttl
 
@@ -481,14 +488,14 @@ def measure(name, steps, warmup, torch, tg, host, K, keep=False):
     algo = ALGO_BYTES.get(kern, 5.0) * units
     achieved = algo / (avg_ms / 1000.0) / 1e9
     roof = {"bound": "hbm", "kernel": kern, "achieved": achieved, "peak": HBM_PEAK_GBS,
-            "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic_for(kern),
+            "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic_for(name, kern),
             "avg_launch_ms": avg_ms, "launches": calls,
             "algorithmic_bytes_per_launch": algo,
             # a replay launch runs one workgroup (on one compute unit) per job
             "workgroups": jobs_count.get(kern[7:]) if kern.startswith("replay_") else None,
             "stage_ms_per_step": {k: round(v[1] / steps, 3) for k, v in timing.items()
                                   if v[0]}}
-    lim = limiter_for(kern, avg_ms, roof["workgroups"])
+    lim = limiter_for(name, kern, avg_ms, roof["workgroups"])
     if lim:
         # the replay is bound by instruction issue and latency, not by HBM:
         # the roofline is the chip's VALU issue rate, the HBM figures stay
@@ -497,7 +504,7 @@ def measure(name, steps, warmup, torch, tg, host, K, keep=False):
                        "frac": achieved / HBM_PEAK_GBS}
         roof.update({"bound": "alu", "achieved": lim["achieved"], "peak": lim["peak_chip"],
                      "unit": lim["unit"], "frac": lim["frac_chip"], "limiter": lim})
-    roof["stages"] = stage_table(timing, steps, n, jobs_accesses, jobs_count)
+    roof["stages"] = stage_table(name, timing, steps, n, jobs_accesses, jobs_count)
     res = {"name": name, "workload": WORKLOAD_TEXT[name], "value": value,
            "ms_per_step": ms_per_step, "steps": steps, "warmup": warmup, "n_accesses": n,
            "n_configs": n_cfg, "n_requests": int(rec.len0.shape[0]), "roofline": roof}
@@ -530,9 +537,11 @@ def main():
     ttl = search = prefix = gttl = None
     workloads = None
     if not args.no_extras:
-        ttl, search, prefix, gttl = extras(dev, rec, cfgs, G, model, n, torch, K)
+        ttl, search, prefix, gttl = extras(dev, rec, cfgs, G, model, n, torch, K,
+                                           ttl_only=args.ttl_extra_only)
         del dev
         torch.cuda.empty_cache()
+    if not args.no_extras and not args.ttl_extra_only:
         workloads = {}
         for w in ("tiny", "chat", "tenant", "longctx", "full"):
             if w == args.workload:
