@@ -7,6 +7,7 @@ with the literal (non-memo) oracle, so a drifted generator or a corrupted
 file is caught without a GPU.
 """
 import os
+import sys
 
 import numpy as np
 import pytest
@@ -33,10 +34,14 @@ def test_digests_match_generators(name):
     assert g["counts"].shape == (len(g["idx"]), t.n_groups, 3, 8)
 
 
-@pytest.mark.parametrize("name", ["longctx"])
+@pytest.mark.parametrize("name", ["longctx", "full"])
 def test_large_files_present(name):
     g = _gold(name)
     assert int(g["generator_version"]) == tg.GENERATOR_VERSION
+    # the stored configurations are the documented seeded subset
+    sys.path.insert(0, os.path.join(HERE, "golden"))
+    import make_golden
+    assert np.array_equal(g["idx"], make_golden.subset(name, int(g["n_cfg_total"])))
     c = g["counts"].astype(np.int64)
     assert c.shape[0] == len(g["idx"]) > 0
     # every access reaches the first present tier: its hits + misses count

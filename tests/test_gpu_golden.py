@@ -4,8 +4,9 @@ For each workload the trace is generated on the device exactly as the
 benchmark does, its arrays are digested and matched to the stored expected
 values (written by ``tests/golden/make_golden.py`` from the CPU oracle
 alone), and the GPU library evaluates the stored configurations (every
-configuration of the workload; 64 of the long-context workload's 2,048
-exclusive ones).  Counts must be equal element by element; objectives match
+configuration of the tiny, chat and tenant workloads; 64 of the
+long-context workload's 2,048 exclusive ones; 32 of the full workload's
+11,000: its LRU grid corners and seeded draws of each policy).  Counts must be equal element by element; objectives match
 the oracle's objectives of the stored counts to 1e-6 relative (the formula
 is evaluated left to right in IEEE double on both sides, so they agree bit
 for bit in practice); Pareto flags equal the oracle's brute force over those
@@ -23,7 +24,7 @@ from tracegen.digest import configs_digest, trace_digest
 pytestmark = pytest.mark.gpu
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-NAMES = ("tiny", "chat", "tenant", "longctx")
+NAMES = ("tiny", "chat", "tenant", "longctx", "full")
 FIELDS = ("hit", "miss", "ins", "evict", "hit_w", "miss_w", "ins_w", "evict_w")
 
 
