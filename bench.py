@@ -547,6 +547,10 @@ def main():
             if w == args.workload:
                 continue
             r, _ = measure(w, 3, 1, torch, tg, host, K)
+            if not args.no_cpu_baseline:
+                # the oracle on a short sample of this workload too (5 s budget)
+                wrec = tg.recipe(w)
+                r["cpu_baseline"] = cpu_baseline(wrec, tg.configs_for(w, wrec), 5.0)
             workloads[w] = r
     cpu = None
     if not args.no_cpu_baseline:
