@@ -1,6 +1,6 @@
 """Writes the stored expected counts of the five benchmark workloads.
 
-    python tests/golden/make_golden.py [tiny chat tenant longctx full] [--threads N]
+    python tests/golden/make_golden.py [tiny chat tenant longctx full chat_leaf chat_ttl] [--threads N]
 
 Every count comes from the CPU oracle (``oracle.replay_memo``: each distinct
 inclusive tier cache replayed once, literally; exclusive configurations
@@ -14,7 +14,10 @@ seeded draws (exclusive configurations cannot share caches, so each one is a
 full literal replay), and of the full workload's 11,000 configurations over
 387 M accesses the 8 corners of its LRU grid, 8 more LRU draws and 8 draws
 each of its FIFO and LFU points (every distinct tier cache is a literal
-replay of the whole trace).
+replay of the whole trace).  Two variants evaluate the chat trace under other
+batches: its grid under radix-tree (leaf-first) eviction (``chat_leaf``) and
+an HBM x DRAM x disk-TTL grid over an unbounded TTL disk tier
+(``chat_ttl``), all configurations of each.
 """
 from __future__ import annotations
 
@@ -35,7 +38,7 @@ import tracegen as tg  # noqa: E402
 from tracegen.digest import configs_digest, trace_digest  # noqa: E402
 from oracle import oracle as O  # noqa: E402
 
-NAMES = ("tiny", "chat", "tenant", "longctx", "full")
+NAMES = ("tiny", "chat", "tenant", "longctx", "full", "chat_leaf", "chat_ttl")
 
 
 def golden_path(name: str) -> str:
@@ -65,7 +68,7 @@ def subset(name: str, n_cfg: int) -> np.ndarray:
 
 def make(name: str, threads: int) -> str:
     t0 = time.time()
-    rec = tg.recipe(name)
+    rec = tg.recipe(tg.trace_of(name))
     tr = rec.to_trace()
     seed = int(tr.meta.get("seed", -1))
     cfgs = tg.configs_for(name, tr)

@@ -6,10 +6,13 @@ values (written by ``tests/golden/make_golden.py`` from the CPU oracle
 alone), and the GPU library evaluates the stored configurations (every
 configuration of the tiny, chat and tenant workloads; 64 of the
 long-context workload's 2,048 exclusive ones; 32 of the full workload's
-11,000: its LRU grid corners and seeded draws of each policy).  Counts must be equal element by element; objectives match
-the oracle's objectives of the stored counts to 1e-6 relative (the formula
-is evaluated left to right in IEEE double on both sides, so they agree bit
-for bit in practice); Pareto flags equal the oracle's brute force over those
+11,000: its LRU grid corners and seeded draws of each policy).  Two
+variants evaluate the chat trace under radix-tree (leaf-first) eviction on
+its whole grid and under an HBM x DRAM x disk-TTL grid (unbounded TTL disk
+tier; the objectives then include its storage integral, a double sum whose
+order differs between the two sides).  Counts must be equal element by
+element; objectives match the oracle's objectives of the stored counts to
+1e-6 relative; Pareto flags equal the oracle's brute force over those
 objectives, in one segment and per policy.
 """
 import os
@@ -24,7 +27,7 @@ from tracegen.digest import configs_digest, trace_digest
 pytestmark = pytest.mark.gpu
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-NAMES = ("tiny", "chat", "tenant", "longctx", "full")
+NAMES = ("tiny", "chat", "tenant", "longctx", "full", "chat_leaf", "chat_ttl")
 FIELDS = ("hit", "miss", "ins", "evict", "hit_w", "miss_w", "ins_w", "evict_w")
 
 
@@ -48,7 +51,7 @@ def test_golden_workload(name, oracle_mod):
     gold = np.load(os.path.join(HERE, "golden", f"counts_{name}.npz"))
     assert int(gold["generator_version"]) == tg.GENERATOR_VERSION, "stale expected values"
     say(f"  {name}: generating the trace on the device")
-    rec = tg.recipe(name)
+    rec = tg.recipe(tg.trace_of(name))
     dev = rec.expand("cuda")
     torch.cuda.synchronize()
     hst = tg.Trace(name=name, hash=dev["hash"].cpu().numpy().view(np.uint64),

@@ -210,8 +210,37 @@ def full_configs(granule_bytes, seed=4, n_replay=1000) -> ConfigBatch:
     return ConfigBatch.concat([lru, rep])
 
 
+def chat_leaf_configs(granule_bytes) -> ConfigBatch:
+    """The chat grid under radix-tree (leaf-first) eviction on every tier."""
+    return grid([1, 2, 4, 8, 16, 32, 64, 128], [0, 16, 32, 64, 128, 256, 512, 1024],
+                [0, 0.25, 0.5, 1, 2, 4, 8, 16], granule_bytes, policy=POLICY_LEAF)
+
+
+def chat_ttl_configs(granule_bytes) -> ConfigBatch:
+    """64 = HBM {1, 4, 16, 64} GiB x DRAM {0, 64, 256, 1024} GiB x disk TTL
+    {0, 60, 600, 3600} s: LRU HBM and DRAM over an unbounded TTL disk tier."""
+    items = []
+    for h, d, t in itertools.product([1, 4, 16, 64], [0, 64, 256, 1024], [0.0, 60.0, 600.0, 3600.0]):
+        items.append({"cap": (_granules(h * GIB, granule_bytes), _granules(d * GIB, granule_bytes), 0),
+                      "ttl": t})
+    return from_list(items)
+
+
+# Workload variants: the same trace under other configuration batches.
+VARIANTS = {"chat_leaf": "chat", "chat_ttl": "chat"}
+
+
+def trace_of(name: str) -> str:
+    """The workload whose trace a (variant) name evaluates."""
+    return VARIANTS.get(name, name)
+
+
 def configs_for(name: str, trace) -> ConfigBatch:
     gb = trace.granule_bytes
+    if name == "chat_leaf":
+        return chat_leaf_configs(gb)
+    if name == "chat_ttl":
+        return chat_ttl_configs(gb)
     if name == "tiny":
         return tiny_configs(gb)
     if name == "chat":
