@@ -47,6 +47,7 @@ constexpr int kLocItems = 8;
 static_assert(kLocNT * kLocItems == (int)kSdB, "block tile mismatch");
 constexpr uint32_t kSentinel = 0xFFFFFFFFu;
 constexpr uint32_t kRowChunk = 16384;   // LDS histogram bins per row chunk
+constexpr int kRowNT = 1024;            // threads per row of the block matrix
 constexpr uint32_t kColRows = 64;       // rows per column-scan chunk
 constexpr uint32_t kThrLds = 6144;      // thresholds kept in LDS for binning
 
@@ -55,14 +56,14 @@ __host__ __device__ __forceinline__ uint64_t tri_off(uint64_t x) { return x * (x
 // ---------------------------------------------------------------------------
 // Q rows: Q[X][Y] for Y < X, inclusive prefix over ceil(key / 8192).
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_sd_rowhist(const uint32_t* __restrict__ key,
+__global__ __launch_bounds__(kRowNT) void k_sd_rowhist(const uint32_t* __restrict__ key,
                                                     const uint8_t* __restrict__ w8, uint64_t n,
                                                     uint32_t row_chunk, uint32_t* __restrict__ Q) {
   // bin j lives at hp(j), one padding word after every 64: the scan below
-  // gives each thread a run of up to 64 bins, which would otherwise put every
-  // lane of a wavefront on one bank
+  // gives each thread a run of up to kRowChunk / kRowNT bins, which would
+  // otherwise put the lanes of a wavefront on a few banks
   __shared__ uint32_t h[kRowChunk + kRowChunk / 64];
-  __shared__ uint32_t sh[8];
+  __shared__ uint32_t sh[kRowNT / 64 + 1];
   const auto hp = [](uint32_t j) { return j + (j >> 6); };
   const uint32_t X = blockIdx.x;
   if (X == 0) return;
@@ -71,29 +72,29 @@ __global__ __launch_bounds__(256) void k_sd_rowhist(const uint32_t* __restrict__
   const uint64_t row = tri_off(X);
   for (uint32_t c0 = 0; c0 < X; c0 += row_chunk) {
     const uint32_t width = min(row_chunk, X - c0);
-    for (uint32_t j = threadIdx.x; j < width; j += 256) h[hp(j)] = 0;
+    for (uint32_t j = threadIdx.x; j < width; j += kRowNT) h[hp(j)] = 0;
     __syncthreads();
     uint32_t carry = 0;
-    for (uint32_t j = threadIdx.x; j < nb; j += 256) {
+    for (uint32_t j = threadIdx.x; j < nb; j += kRowNT) {
       const uint32_t c = (key[base + j] + (kSdB - 1)) >> kSdLogB;
       const uint32_t w = w8[base + j];
       if (c < c0) carry += w;
       else if (c < c0 + width) atomicAdd(&h[hp(c - c0)], w);
     }
-    carry = block_sum<256>(carry, sh);
+    carry = block_sum<kRowNT>(carry, sh);
     // inclusive scan of h[0, width) in LDS, each thread a contiguous run
-    const uint32_t per = (width + 255) / 256;
+    const uint32_t per = (width + kRowNT - 1) / kRowNT;
     const uint32_t a = min(width, threadIdx.x * per), b = min(width, a + per);
     uint32_t run = 0;
     for (uint32_t j = a; j < b; ++j) run += h[hp(j)];
     uint32_t tot;
-    uint32_t pre = block_excl_scan<256>(run, sh, &tot) + carry;
+    uint32_t pre = block_excl_scan<kRowNT>(run, sh, &tot) + carry;
     for (uint32_t j = a; j < b; ++j) {
       pre += h[hp(j)];
       h[hp(j)] = pre;
     }
     __syncthreads();
-    for (uint32_t j = threadIdx.x; j < width; j += 256) Q[row + c0 + j] = h[hp(j)];
+    for (uint32_t j = threadIdx.x; j < width; j += kRowNT) Q[row + c0 + j] = h[hp(j)];
     __syncthreads();
   }
 }
@@ -847,7 +848,7 @@ kv_status stack_pass(Trace& t, Order& o, bool partitioned, const ThresholdSet& t
   if (G >= 2) {
     StageTimer tm(kStStackMatrix, s);
     const uint32_t row_chunk = env_limit("KVCFG_TEST_ROW_CHUNK", kRowChunk, 1);
-    hipLaunchKernelGGL(k_sd_rowhist, dim3(G), dim3(256), 0, s, key, w8, n, row_chunk, Q);
+    hipLaunchKernelGGL(k_sd_rowhist, dim3(G), dim3(kRowNT), 0, s, key, w8, n, row_chunk, Q);
     KV_HIP(hipGetLastError());
     const dim3 cg(div_up(G, 256), nchunks);
     hipLaunchKernelGGL(k_sd_colsum, cg, dim3(256), 0, s, Q, G, b_csum.as<uint32_t>());
