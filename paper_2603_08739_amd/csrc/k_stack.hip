@@ -48,6 +48,7 @@ static_assert(kLocNT * kLocItems == (int)kSdB, "block tile mismatch");
 constexpr uint32_t kSentinel = 0xFFFFFFFFu;
 constexpr uint32_t kRowChunk = 16384;   // LDS histogram bins per row chunk
 constexpr int kRowNT = 1024;            // threads per row of the block matrix
+constexpr int kAsmNT = 1024;            // threads per workgroup of the distance assembly
 constexpr uint32_t kColRows = 64;       // rows per column-scan chunk
 constexpr uint32_t kThrLds = 6144;      // thresholds kept in LDS for binning
 
@@ -382,7 +383,7 @@ struct BinArgs {
 };
 
 template <bool kLds>
-__global__ __launch_bounds__(256) void k_sd_assemble(const uint32_t* __restrict__ key,
+__global__ __launch_bounds__(kAsmNT) void k_sd_assemble(const uint32_t* __restrict__ key,
                                                      const uint8_t* __restrict__ w8,
                                                      const uint8_t* __restrict__ g8, uint64_t n,
                                                      uint32_t G,
@@ -398,8 +399,8 @@ __global__ __launch_bounds__(256) void k_sd_assemble(const uint32_t* __restrict_
   const uint32_t nbins = ba.n_thr + ba.n_groups;
   if (threadIdx.x <= ba.n_groups) soff[threadIdx.x] = ba.off[threadIdx.x];
   if (kLds) {
-    for (uint32_t j = threadIdx.x; j < ba.n_thr; j += 256) sthr[j] = ba.thr[j];
-    for (uint32_t j = threadIdx.x; j < nbins; j += 256) {
+    for (uint32_t j = threadIdx.x; j < ba.n_thr; j += kAsmNT) sthr[j] = ba.thr[j];
+    for (uint32_t j = threadIdx.x; j < nbins; j += kAsmNT) {
       scnt[j] = 0;
       sw[j] = 0;
     }
@@ -409,7 +410,7 @@ __global__ __launch_bounds__(256) void k_sd_assemble(const uint32_t* __restrict_
     const uint64_t base = (uint64_t)X * kSdB;
     const uint32_t nb = (uint32_t)min<uint64_t>(kSdB, n - base);
     const uint64_t row = X >= 2 ? tri_off(X - 1) : 0;
-    for (uint32_t j = threadIdx.x; j < nb; j += 256) {
+    for (uint32_t j = threadIdx.x; j < nb; j += kAsmNT) {
       const uint64_t i = base + j;
       if (real && !real[i]) continue;  // a re-touch of the radix-tree order: not binned
       const uint32_t kk = key[i];
@@ -443,7 +444,7 @@ __global__ __launch_bounds__(256) void k_sd_assemble(const uint32_t* __restrict_
   }
   if (kLds) {
     __syncthreads();
-    for (uint32_t j = threadIdx.x; j < nbins; j += 256) {
+    for (uint32_t j = threadIdx.x; j < nbins; j += kAsmNT) {
       if (scnt[j]) {
         atomicAdd((unsigned long long*)&ba.hist[j * 4 + 0], (unsigned long long)scnt[j]);
         atomicAdd((unsigned long long*)&ba.hist[j * 4 + 1], (unsigned long long)sw[j]);
@@ -872,15 +873,17 @@ kv_status stack_pass(Trace& t, Order& o, bool partitioned, const ThresholdSet& t
   const bool jlds = ja && lds_limit > 0 && ts.values.size() <= kJThrLds &&
                     ja->n_tthr + ts.n_groups <= kJTtlLds && ja->n_joint <= kJBinsLds;
   const uint32_t gj = std::min<uint32_t>(div_up(n, kJointNT), 1024);
-  const uint32_t ga = std::min<uint32_t>(G, 2048);
+  // two workgroups per compute unit (their LDS histograms allow two): each
+  // flushes its histogram once, so fewer and larger ones flush less
+  const uint32_t ga = std::min<uint32_t>(G, 512);
   {
   StageTimer tm(kStStackAssemble, s);
   if (lds)
-    hipLaunchKernelGGL(k_sd_assemble<true>, dim3(ga), dim3(256), 0, s, key, w8, g8, n, G,
+    hipLaunchKernelGGL(k_sd_assemble<true>, dim3(ga), dim3(kAsmNT), 0, s, key, w8, g8, n, G,
                        (const uint32_t*)b_partial.as<uint32_t>(),
                        (const uint32_t*)b_E.as<uint32_t>(), (const uint32_t*)Q, ba, dist, real);
   else
-    hipLaunchKernelGGL(k_sd_assemble<false>, dim3(ga), dim3(256), 0, s, key, w8, g8, n, G,
+    hipLaunchKernelGGL(k_sd_assemble<false>, dim3(ga), dim3(kAsmNT), 0, s, key, w8, g8, n, G,
                        (const uint32_t*)b_partial.as<uint32_t>(),
                        (const uint32_t*)b_E.as<uint32_t>(), (const uint32_t*)Q, ba, dist, real);
   KV_HIP(hipGetLastError());
