@@ -48,7 +48,7 @@ static_assert(kLocNT * kLocItems == (int)kSdB, "block tile mismatch");
 constexpr uint32_t kSentinel = 0xFFFFFFFFu;
 constexpr uint32_t kRowChunk = 16384;   // LDS histogram bins per row chunk
 constexpr int kRowNT = 1024;            // threads per row of the block matrix
-constexpr int kAsmNT = 1024;            // threads per workgroup of the distance assembly
+constexpr int kAsmNT = 1024;            // threads per workgroup of the distance binning kernels
 constexpr uint32_t kColRows = 64;       // rows per column-scan chunk
 constexpr uint32_t kThrLds = 6144;      // thresholds kept in LDS for binning
 
@@ -549,7 +549,7 @@ struct SegArgs {
 // Final stack depth of each block = weight of distinct blocks whose last
 // access is at or after its own (inside its segment); bin it.
 template <bool kLds>
-__global__ __launch_bounds__(256) void k_sd_finocc(const uint32_t* __restrict__ nxt,
+__global__ __launch_bounds__(kAsmNT) void k_sd_finocc(const uint32_t* __restrict__ nxt,
                                                    const uint8_t* __restrict__ w8,
                                                    const uint8_t* __restrict__ g8, uint64_t n,
                                                    const uint32_t* __restrict__ S,
@@ -567,8 +567,8 @@ __global__ __launch_bounds__(256) void k_sd_finocc(const uint32_t* __restrict__ 
     send[threadIdx.x] = (e > b) ? S[e - 1] : 0u;
   }
   if (kLds) {
-    for (uint32_t j = threadIdx.x; j < ba.n_thr; j += 256) sthr[j] = ba.thr[j];
-    for (uint32_t j = threadIdx.x; j < nbins; j += 256) {
+    for (uint32_t j = threadIdx.x; j < ba.n_thr; j += kAsmNT) sthr[j] = ba.thr[j];
+    for (uint32_t j = threadIdx.x; j < nbins; j += kAsmNT) {
       scnt[j] = 0;
       sw[j] = 0;
     }
@@ -594,7 +594,7 @@ __global__ __launch_bounds__(256) void k_sd_finocc(const uint32_t* __restrict__ 
   }
   if (kLds) {
     __syncthreads();
-    for (uint32_t j = threadIdx.x; j < nbins; j += 256) {
+    for (uint32_t j = threadIdx.x; j < nbins; j += kAsmNT) {
       if (scnt[j]) {
         atomicAdd((unsigned long long*)&ba.hist[j * 4 + 2], (unsigned long long)scnt[j]);
         atomicAdd((unsigned long long*)&ba.hist[j * 4 + 3], (unsigned long long)sw[j]);
@@ -926,12 +926,12 @@ kv_status stack_pass(Trace& t, Order& o, bool partitioned, const ThresholdSet& t
   SegArgs sa{};
   for (int g = 0; g <= KV_MAX_GROUPS; ++g) sa.seg[g] = o.seg[g];
   sa.partitioned = partitioned ? 1u : 0u;
-  const uint32_t gf = grid_of(n, 2048);
+  const uint32_t gf = std::min<uint32_t>(div_up(n, kAsmNT), 512);  // two per compute unit, as above
   if (lds)
-    hipLaunchKernelGGL(k_sd_finocc<true>, dim3(gf), dim3(256), 0, s, nxt, w8, g8, n,
+    hipLaunchKernelGGL(k_sd_finocc<true>, dim3(gf), dim3(kAsmNT), 0, s, nxt, w8, g8, n,
                        (const uint32_t*)S, sa, ba);
   else
-    hipLaunchKernelGGL(k_sd_finocc<false>, dim3(gf), dim3(256), 0, s, nxt, w8, g8, n,
+    hipLaunchKernelGGL(k_sd_finocc<false>, dim3(gf), dim3(kAsmNT), 0, s, nxt, w8, g8, n,
                        (const uint32_t*)S, sa, ba);
   KV_HIP(hipGetLastError());
   hipLaunchKernelGGL(k_hist_cum, dim3(1), dim3(4 * KV_MAX_GROUPS), 0, s, hist, off_dev,
