@@ -656,9 +656,10 @@ __device__ __forceinline__ void lds_put(uint32_t* p, const uint32_t* v) {
 // Nonempty-class bits from the class counts (whole block).
 template <int NT>
 __device__ __forceinline__ void class_bits_rebuild(LfuLds& S) {
-  for (uint32_t f = threadIdx.x; f < kLdsClass; f += NT) {
-    const uint64_t bal = __ballot(S.ccnt[f] != 0u);
-    if (lane_id() == 0) S.cnz[f / 64] = bal;
+  // each wavefront takes whole 64-class words (kLdsClass is a multiple of 64)
+  for (uint32_t wd = (uint32_t)wave_id(); wd < kLdsClassWords; wd += NT / 64) {
+    const uint64_t bal = __ballot(S.ccnt[wd * 64 + lane_id()] != 0u);
+    if (lane_id() == 0) S.cnz[wd] = bal;
   }
 }
 
@@ -1429,7 +1430,7 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   // per-thread partials: evictions (and, 16 bits up, old count-1 entries
   // leaving class 1), evicted weight, last entries taken.  Insertions are
   // the misses, counted by the fixed point.
-  uint32_t p_evn = 0, p_vw = 0, p_lastp = 0, p_lastm = 0;
+  uint32_t p_evn = 0, p_vw = 0, p_lastp = 0, p_laste = 0;
   // old entries evicted (loads issued unconditionally, several in flight)
   for (uint32_t k = tid; k < nc0; k += NT) {
     const bool cons = S.ccons[k] != 0;
@@ -1473,7 +1474,6 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
   for (int e = 0; e < IT; ++e) {
     hit[e] = v[e] && !miss[e];
     if (!(v[e] && miss[e])) continue;
-    const uint32_t loc = l0 + e;
     const bool cons = mc[e] != 0;  // inserted here, evicted later in the chunk
     if (g1) {
       p_evn += cons ? 1u : 0u;
@@ -1487,9 +1487,10 @@ __device__ __forceinline__ bool lfu_fast(const JobDev& j, const JobArgs& a,
     }
     if (cons) {
       p_vw += ww[e];
-      p_lastm = max(p_lastm, loc + 1);
+      p_laste = e + 1;  // items run in position order: the last one wins
     }
   }
+  const uint32_t p_lastm = p_laste ? l0 + p_laste : 0u;
   // final state of every touched block, at its last touch.  Moves into and
   // out of classes 1 and 2 (the crowded ones) add up per wavefront by
   // ballot; the others go one by one.
