@@ -1,6 +1,6 @@
 """Writes the stored expected counts of the five benchmark workloads.
 
-    python tests/golden/make_golden.py [tiny chat tenant longctx full chat_leaf chat_ttl] [--threads N]
+    python tests/golden/make_golden.py [tiny chat ... longctx_leaf] [--threads N]
 
 Every count comes from the CPU oracle (``oracle.replay_memo``: each distinct
 inclusive tier cache replayed once, literally; exclusive configurations
@@ -17,7 +17,10 @@ each of its FIFO and LFU points (every distinct tier cache is a literal
 replay of the whole trace).  Two variants evaluate the chat trace under other
 batches: its grid under radix-tree (leaf-first) eviction (``chat_leaf``) and
 an HBM x DRAM x disk-TTL grid over an unbounded TTL disk tier
-(``chat_ttl``), all configurations of each.
+(``chat_ttl``), all configurations of each; and two over the large traces:
+the full workload's trace over a 16-point HBM x DRAM x disk-TTL grid
+(``full_ttl``) and the long-context trace under leaf-first eviction on a
+64-point inclusive subset of its grid (``longctx_leaf``).
 """
 from __future__ import annotations
 
@@ -38,7 +41,8 @@ import tracegen as tg  # noqa: E402
 from tracegen.digest import configs_digest, trace_digest  # noqa: E402
 from oracle import oracle as O  # noqa: E402
 
-NAMES = ("tiny", "chat", "tenant", "longctx", "full", "chat_leaf", "chat_ttl")
+NAMES = ("tiny", "chat", "tenant", "longctx", "full", "chat_leaf", "chat_ttl", "full_ttl",
+         "longctx_leaf")
 
 
 def golden_path(name: str) -> str:
@@ -78,7 +82,13 @@ def make(name: str, threads: int) -> str:
     t1 = time.time()
     print(f"[golden] {name}: {tr.n} accesses, {sub.n} of {cfgs.n} configs, trace {t1 - t0:.1f} s",
           flush=True)
-    counts = O.replay_memo(tr, sub, threads=threads)
+    # with a disk TTL tier, also the oracle's storage-time integral of the
+    # unbounded ones (the objectives bill it)
+    store = None
+    if np.any(sub.disk_ttl):
+        counts, store = O.replay(tr, sub, threads, memo=True, with_store=True)
+    else:
+        counts = O.replay_memo(tr, sub, threads=threads)
     t2 = time.time()
     src = open(os.path.join(ROOT, "oracle", "kvoracle.cpp"), "rb").read()
     out = golden_path(name)
@@ -88,7 +98,8 @@ def make(name: str, threads: int) -> str:
         generator_version=np.uint32(tg.GENERATOR_VERSION), seed=np.int64(seed),
         n=np.uint64(tr.n), n_groups=np.uint32(tr.n_groups),
         oracle_sha=np.array(hashlib.sha256(src).hexdigest()),
-        oracle_seconds=np.float64(t2 - t1), threads=np.uint32(threads))
+        oracle_seconds=np.float64(t2 - t1), threads=np.uint32(threads),
+        **({"store": store} if store is not None else {}))
     print(f"[golden] {name}: oracle {t2 - t1:.1f} s on {threads} threads -> {out}", flush=True)
     return out
 

@@ -34,7 +34,7 @@ def test_digests_match_generators(name):
     assert g["counts"].shape == (len(g["idx"]), t.n_groups, 3, 8)
 
 
-@pytest.mark.parametrize("name", ["longctx", "full"])
+@pytest.mark.parametrize("name", ["longctx", "full", "full_ttl", "longctx_leaf"])
 def test_large_files_present(name):
     g = _gold(name)
     assert int(g["generator_version"]) == tg.GENERATOR_VERSION

@@ -10,7 +10,10 @@ long-context workload's 2,048 exclusive ones; 32 of the full workload's
 variants evaluate the chat trace under radix-tree (leaf-first) eviction on
 its whole grid and under an HBM x DRAM x disk-TTL grid (unbounded TTL disk
 tier; the objectives then include its storage integral, a double sum whose
-order differs between the two sides).  Counts must be equal element by
+order differs between the two sides, stored beside the counts); two more
+evaluate the full workload's trace over a 16-point HBM x DRAM x disk-TTL
+grid and the long-context trace under leaf-first eviction on 64 inclusive
+points of its grid.  Counts must be equal element by
 element; objectives match the oracle's objectives of the stored counts to
 1e-6 relative; Pareto flags equal the oracle's brute force over those
 objectives, in one segment and per policy.
@@ -27,7 +30,8 @@ from tracegen.digest import configs_digest, trace_digest
 pytestmark = pytest.mark.gpu
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-NAMES = ("tiny", "chat", "tenant", "longctx", "full", "chat_leaf", "chat_ttl")
+NAMES = ("tiny", "chat", "tenant", "longctx", "full", "chat_leaf", "chat_ttl", "full_ttl",
+         "longctx_leaf")
 FIELDS = ("hit", "miss", "ins", "evict", "hit_w", "miss_w", "ins_w", "evict_w")
 
 
@@ -77,7 +81,9 @@ def test_golden_workload(name, oracle_mod):
     assert counts.shape == ref.shape
     assert np.array_equal(counts, ref), f"{name}: " + first_mismatch(counts, ref)
     say(f"  {name}: counts equal; objectives and Pareto fronts")
-    ref_obj = O.objectives(hst, sub, ref, tg.DEFAULT_COST)
+    # the storage integral of unbounded disk TTL tiers comes with the stored counts
+    ref_obj = O.objectives(hst, sub, ref, tg.DEFAULT_COST,
+                           store=gold["store"] if "store" in gold else None)
     np.testing.assert_allclose(obj, ref_obj, rtol=1e-6, atol=0)
     for seg in (None, sub.segment):
         flags, n = host.pareto(obj, segment=seg)

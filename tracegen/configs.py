@@ -226,8 +226,27 @@ def chat_ttl_configs(granule_bytes) -> ConfigBatch:
     return from_list(items)
 
 
+def full_ttl_configs(granule_bytes) -> ConfigBatch:
+    """16 = HBM {4, 40} GiB x DRAM {0, 512} GiB x disk TTL {0, 60, 600, 3600} s:
+    LRU HBM and DRAM over an unbounded TTL disk tier."""
+    items = []
+    for h, d, t in itertools.product([4, 40], [0, 512], [0.0, 60.0, 600.0, 3600.0]):
+        items.append({"cap": (_granules(h * GIB, granule_bytes), _granules(d * GIB, granule_bytes), 0),
+                      "ttl": t})
+    return from_list(items)
+
+
+def longctx_leaf_configs(granule_bytes) -> ConfigBatch:
+    """64 = HBM {1, 8, 32, 128} GiB x DRAM {0, 512, 4096, 16384} GiB x SSD
+    {0, 8, 64, 256} TiB of the long-context grid, inclusive tiers under
+    radix-tree (leaf-first) eviction."""
+    return grid([1, 8, 32, 128], [0, 512, 4096, 16384], [0, 8, 64, 256], granule_bytes,
+                policy=POLICY_LEAF)
+
+
 # Workload variants: the same trace under other configuration batches.
-VARIANTS = {"chat_leaf": "chat", "chat_ttl": "chat"}
+VARIANTS = {"chat_leaf": "chat", "chat_ttl": "chat", "full_ttl": "full",
+            "longctx_leaf": "longctx"}
 
 
 def trace_of(name: str) -> str:
@@ -241,6 +260,10 @@ def configs_for(name: str, trace) -> ConfigBatch:
         return chat_leaf_configs(gb)
     if name == "chat_ttl":
         return chat_ttl_configs(gb)
+    if name == "full_ttl":
+        return full_ttl_configs(gb)
+    if name == "longctx_leaf":
+        return longctx_leaf_configs(gb)
     if name == "tiny":
         return tiny_configs(gb)
     if name == "chat":
