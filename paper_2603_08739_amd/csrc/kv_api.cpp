@@ -648,7 +648,12 @@ kv_status kv_eval_configs(const kv_trace* h, const kv_config* cfg, uint32_t n_cf
   bool need_leaf = false;
   for (uint32_t c = 0; c < n_cfg; ++c) need_leaf |= !cfg[c].partitioned && cfg[c].policy[0] == KV_POLICY_LEAF;
   if (need_leaf) {
-    // radix-tree eviction: a trace of prefix-chain requests, each fitting every tier
+    // radix-tree eviction: a trace of prefix-chain requests, each fitting
+    // every tier; its stack pass runs over 2N positions, within kMaxN
+    if (2 * t->n > kMaxN)
+      return fail(KV_ERR_UNSUPPORTED, "kv_eval_configs: radix-tree eviction evaluates an order of "
+                                      "2N positions, at most " + std::to_string(kMaxN) +
+                                      " (N = " + std::to_string(t->n) + ")");
     if ((st = leaf_prepare(*t, s)) != KV_OK) return st;
     if (!t->leaf_chained)
       return fail(KV_ERR_UNSUPPORTED, "kv_eval_configs: radix-tree eviction needs requests that "

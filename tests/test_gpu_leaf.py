@@ -121,3 +121,25 @@ def test_refusals():
                               tg.DEFAULT_COST, 1)
     h.free()
     assert counts[0, 0, 0, 0] > 0
+
+
+def test_refuses_a_trace_beyond_half_the_position_limit():
+    """The augmented order has 2N positions; above 2^28 accesses the call is
+    refused before anything is built (the trace itself loads: N <= 2^29)."""
+    import torch
+    from paper_2603_08739_amd import host, kvcfg as K
+    n = (1 << 28) + 64
+    say(f"  loading {n} cold accesses")
+    hsh = torch.arange(1, n + 1, dtype=torch.int64, device="cuda") * 0x9E3779B97F4A7C15
+    req = (torch.arange(n, dtype=torch.int64, device="cuda") // 64).to(torch.int32)
+    n_req = int(req[-1].item()) + 1
+    rt = torch.arange(n_req, dtype=torch.float64, device="cuda")
+    h = K.kv_trace_load(hsh, req, rt, n_groups=1, tokens_per_granule=16, granule_bytes=131072)
+    del hsh, req, rt
+    counts = torch.zeros((1, 1, 3, 8), dtype=torch.int64, device="cuda")
+    arr, n_cfg = host.config_array(tg.from_list([{"cap": (1024, 0, 0), "policy": LEAF}]))
+    with pytest.raises(K.KvError) as e:
+        K.kv_eval_configs(h, arr, n_cfg, host.cost_model(tg.DEFAULT_COST), counts, None)
+    assert e.value.status == K.KV_ERR_UNSUPPORTED and "2N positions" in str(e.value)
+    h.free()
+    torch.cuda.empty_cache()
