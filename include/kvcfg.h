@@ -255,9 +255,9 @@ kv_status kv_trace_info(const kv_trace* t, kv_trace_stats* out);
  * negative or not finite; KV_ERR_UNSUPPORTED for a disk TTL tier outside
  * the inclusive LRU shared mode or bounded with unequal group TTLs, for more
  * than 1,024 distinct TTLs per group in one call, for LEAF outside the
- * inclusive shared mode, on a trace whose requests are not prefix chains or
- * of more than 2^28 accesses, or with a nonzero capacity below the heaviest
- * request, for the exclusive mode with
+ * inclusive shared mode, on a trace whose requests are not prefix chains,
+ * of more than 2^28 accesses or of total weight 2^31 granules or more, or
+ * with a nonzero capacity below the heaviest request, for the exclusive mode with
  * FIFO/LFU or with blocks of different weights, and for the prefix-reuse
  * mode with FIFO/LFU or partitioned capacities; KV_ERR_NOMEM when not even
  * one replay job's state fits; KV_ERR_DEVICE when an earlier call's replay

@@ -654,6 +654,10 @@ kv_status kv_eval_configs(const kv_trace* h, const kv_config* cfg, uint32_t n_cf
       return fail(KV_ERR_UNSUPPORTED, "kv_eval_configs: radix-tree eviction evaluates an order of "
                                       "2N positions, at most " + std::to_string(kMaxN) +
                                       " (N = " + std::to_string(t->n) + ")");
+    // that order carries every access's weight twice: its sums stay below 2^32
+    if (2 * t->st.n_w >= 0xFFFFFFFFull)
+      return fail(KV_ERR_UNSUPPORTED, "kv_eval_configs: radix-tree eviction needs the total "
+                                      "weight below 2^31 granules");
     if ((st = leaf_prepare(*t, s)) != KV_OK) return st;
     if (!t->leaf_chained)
       return fail(KV_ERR_UNSUPPORTED, "kv_eval_configs: radix-tree eviction needs requests that "

@@ -143,3 +143,23 @@ def test_refuses_a_trace_beyond_half_the_position_limit():
     assert e.value.status == K.KV_ERR_UNSUPPORTED and "2N positions" in str(e.value)
     h.free()
     torch.cuda.empty_cache()
+
+
+def test_refuses_a_total_weight_of_2_31():
+    """The augmented order carries every access's weight twice, and its sums
+    are 32-bit: a trace of 2^31 granules or more is refused."""
+    import torch
+    from paper_2603_08739_amd import host, kvcfg as K
+    n = (1 << 31) // 255 + 64
+    hsh = torch.arange(1, n + 1, dtype=torch.int64, device="cuda") * 0x9E3779B97F4A7C15
+    req = (torch.arange(n, dtype=torch.int64, device="cuda") // 64).to(torch.int32)
+    rt = torch.arange(int(req[-1].item()) + 1, dtype=torch.float64, device="cuda")
+    w = torch.full((n,), 255, dtype=torch.uint8, device="cuda")
+    h = K.kv_trace_load(hsh, req, rt, weight=w, n_groups=1, tokens_per_granule=16,
+                        granule_bytes=131072)
+    counts = torch.zeros((1, 1, 3, 8), dtype=torch.int64, device="cuda")
+    arr, n_cfg = host.config_array(tg.from_list([{"cap": (1 << 20, 0, 0), "policy": LEAF}]))
+    with pytest.raises(K.KvError) as e:
+        K.kv_eval_configs(h, arr, n_cfg, host.cost_model(tg.DEFAULT_COST), counts, None)
+    assert e.value.status == K.KV_ERR_UNSUPPORTED and "2^31" in str(e.value)
+    h.free()
