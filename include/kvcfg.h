@@ -257,9 +257,9 @@ kv_status kv_trace_info(const kv_trace* t, kv_trace_stats* out);
  * than 1,024 distinct TTLs per group in one call, for LEAF outside the
  * inclusive shared mode, on a trace whose requests are not prefix chains,
  * of more than 2^28 accesses or of total weight 2^31 granules or more, or
- * with a nonzero capacity below the heaviest request, for the exclusive mode with
- * FIFO/LFU or with blocks of different weights, and for the prefix-reuse
- * mode with FIFO/LFU or partitioned capacities; KV_ERR_NOMEM when not even
+ * with a nonzero capacity below the heaviest request, for the exclusive
+ * mode with FIFO/LFU or with blocks of different weights, and for the
+ * prefix-reuse mode with FIFO/LFU or partitioned capacities; KV_ERR_NOMEM when not even
  * one replay job's state fits; KV_ERR_DEVICE when an earlier call's replay
  * failure (see kv_trace_info) has already arrived.  n_cfg == 0 is a no-op. */
 kv_status kv_eval_configs(const kv_trace* t, const kv_config* cfg, uint32_t n_cfg,
