@@ -18,9 +18,10 @@
 namespace kv {
 namespace {
 
-constexpr int kRsNT = 256;
-constexpr int kRsItems = 16;
-constexpr uint32_t kRsTile = kRsNT * kRsItems;  // 4096
+constexpr int kRsNT = 1024;
+constexpr int kRsItems = 8;
+constexpr uint32_t kRsTile = kRsNT * kRsItems;  // 8192
+constexpr int kRsDigits = 256;                   // 8-bit digits
 constexpr int kRsWaves = kRsNT / 64;
 
 enum : uint32_t {
@@ -109,8 +110,8 @@ __global__ void k_check_times(const double* __restrict__ t, uint32_t n_req, DevS
 __global__ __launch_bounds__(kRsNT) void k_rs_count(const uint64_t* __restrict__ keys, uint64_t n,
                                                     int shift, uint32_t* __restrict__ counts,
                                                     uint32_t ntiles) {
-  __shared__ uint32_t h[256];
-  h[threadIdx.x] = 0;
+  __shared__ uint32_t h[kRsDigits];
+  if (threadIdx.x < kRsDigits) h[threadIdx.x] = 0;
   __syncthreads();
   const uint64_t base = (uint64_t)blockIdx.x * kRsTile;
   for (int e = 0; e < kRsItems; ++e) {
@@ -118,7 +119,7 @@ __global__ __launch_bounds__(kRsNT) void k_rs_count(const uint64_t* __restrict__
     if (i < n) atomicAdd(&h[(uint32_t)(keys[i] >> shift) & 255u], 1u);
   }
   __syncthreads();
-  counts[(uint64_t)threadIdx.x * ntiles + blockIdx.x] = h[threadIdx.x];
+  if (threadIdx.x < kRsDigits) counts[(uint64_t)threadIdx.x * ntiles + blockIdx.x] = h[threadIdx.x];
 }
 
 // Stable scatter of one tile given the exclusive digit offsets.  The tile
@@ -131,15 +132,16 @@ __global__ __launch_bounds__(kRsNT) void k_rs_scatter(const uint64_t* __restrict
                                                       int shift,
                                                       const uint32_t* __restrict__ offsets,
                                                       uint32_t ntiles) {
-  __shared__ uint32_t wcnt[kRsWaves][256];
-  __shared__ uint32_t gbase[256];   // the digit's first output position, less its tile start
+  __shared__ uint32_t wcnt[kRsWaves][kRsDigits];
+  __shared__ uint32_t gbase[kRsDigits];   // the digit's first output position, less its tile start
   __shared__ uint32_t red[kRsWaves];
   __shared__ uint64_t sk[kRsTile];
   __shared__ uint32_t sv[kRsTile];
   const int w = threadIdx.x / 64;
   const uint32_t lane = lane_id();
-  for (int d = threadIdx.x; d < kRsWaves * 256; d += kRsNT) (&wcnt[0][0])[d] = 0;
-  const uint32_t g0 = offsets[(uint64_t)threadIdx.x * ntiles + blockIdx.x];
+  for (int d = threadIdx.x; d < kRsWaves * kRsDigits; d += kRsNT) (&wcnt[0][0])[d] = 0;
+  const uint32_t g0 =
+      threadIdx.x < kRsDigits ? offsets[(uint64_t)threadIdx.x * ntiles + blockIdx.x] : 0u;
   __syncthreads();
   const uint64_t t0 = (uint64_t)blockIdx.x * kRsTile;
   const uint64_t base = t0 + (uint64_t)w * (kRsItems * 64);
@@ -169,22 +171,28 @@ __global__ __launch_bounds__(kRsNT) void k_rs_scatter(const uint64_t* __restrict
   }
   __syncthreads();
   {
-    // per digit (one per thread): the tile's count, its start in the tile's
-    // digit order (a block scan), and each wave's start inside it
+    // per digit (one per thread of the first kRsDigits): the tile's count,
+    // its start in the tile's digit order (a block scan), and each wave's
+    // start inside it
     const int dg = threadIdx.x;
+    const bool has = dg < kRsDigits;
     uint32_t tot = 0;
+    if (has) {
 #pragma unroll
-    for (int ww = 0; ww < kRsWaves; ++ww) tot += wcnt[ww][dg];
+      for (int ww = 0; ww < kRsWaves; ++ww) tot += wcnt[ww][dg];
+    }
     uint32_t all;
     const uint32_t ls = block_excl_scan_u32<kRsNT, false>(tot, red, all);
-    uint32_t run = ls;
+    if (has) {
+      uint32_t run = ls;
 #pragma unroll
-    for (int ww = 0; ww < kRsWaves; ++ww) {
-      const uint32_t c = wcnt[ww][dg];
-      wcnt[ww][dg] = run;
-      run += c;
+      for (int ww = 0; ww < kRsWaves; ++ww) {
+        const uint32_t c = wcnt[ww][dg];
+        wcnt[ww][dg] = run;
+        run += c;
+      }
+      gbase[dg] = g0 - ls;
     }
-    gbase[dg] = g0 - ls;
   }
   __syncthreads();
 #pragma unroll
