@@ -258,7 +258,10 @@ __global__ __launch_bounds__(256) void k_links(const uint64_t* __restrict__ K,
     const uint32_t nx = sn ? V[k + 1] : kNone;
     const uint32_t run = incl[k] - 1u;
     const uint32_t id = fincl[firstpos[run]] - 1u;
-    kn[pos] = make_uint4(key, nx, id, 0u);
+    // a streaming store: each record lands alone in its line
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    const u32x4 rec = {key, nx, id, 0u};
+    __builtin_nontemporal_store(rec, reinterpret_cast<u32x4*>(kn) + pos);
     if (!sp) {
       const uint8_t w = w8[pos], g = g8[pos];
       blk_w[id] = w;
