@@ -65,6 +65,11 @@ __global__ __launch_bounds__(256) void k_validate(const uint64_t* __restrict__ h
   }
   __syncthreads();
   uint32_t err = 0, wmin = 0xFFFFFFFFu, wmax = 0;
+  // per-group totals add up in registers while the thread's group stays
+  // the same (always, with one group) and go to LDS when it changes: LDS
+  // atomics of a wavefront on one address are taken one lane at a time
+  uint32_t cg = 0xFFFFFFFFu;
+  unsigned long long cn = 0, cw = 0;
   for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (uint64_t)gridDim.x * blockDim.x) {
     uint32_t g = group ? group[i] : 0u;
@@ -77,10 +82,23 @@ __global__ __launch_bounds__(256) void k_validate(const uint64_t* __restrict__ h
     w8[i] = (uint8_t)w;
     keys[i] = hash[i];
     vals[i] = (uint32_t)i;
-    atomicAdd(&sn[g], 1ull);
-    atomicAdd(&sw[g], (unsigned long long)w);
+    if (g != cg) {
+      if (cn) {
+        atomicAdd(&sn[cg], cn);
+        atomicAdd(&sw[cg], cw);
+      }
+      cg = g;
+      cn = 0;
+      cw = 0;
+    }
+    ++cn;
+    cw += w;
     wmin = min(wmin, w);
     wmax = max(wmax, w);
+  }
+  if (cn) {
+    atomicAdd(&sn[cg], cn);
+    atomicAdd(&sw[cg], cw);
   }
   atomicMin(&smin, wmin);
   atomicMax(&smax, wmax);
