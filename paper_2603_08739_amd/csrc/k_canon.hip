@@ -132,9 +132,22 @@ __global__ __launch_bounds__(kRsNT) void k_rs_count(const uint64_t* __restrict__
   if (threadIdx.x < kRsDigits) h[threadIdx.x] = 0;
   __syncthreads();
   const uint64_t base = (uint64_t)blockIdx.x * kRsTile;
+  const uint32_t lane = lane_id();
+#pragma unroll
   for (int e = 0; e < kRsItems; ++e) {
-    uint64_t i = base + (uint64_t)e * kRsNT + threadIdx.x;
-    if (i < n) atomicAdd(&h[(uint32_t)(keys[i] >> shift) & 255u], 1u);
+    const uint64_t i = base + (uint64_t)e * kRsNT + threadIdx.x;
+    const bool valid = i < n;
+    const uint32_t d = valid ? (uint32_t)(keys[i] >> shift) & 255u : 0u;
+    // lanes of the wavefront with the same digit (8 ballots): the highest
+    // adds their number, so no two lanes of one atomic share an address
+    uint64_t peers = __ballot(valid);
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+      const bool bit = (d >> b) & 1u;
+      const uint64_t bb = __ballot(bit);
+      peers &= bit ? bb : ~bb;
+    }
+    if (valid && (peers >> lane) == 1ull) atomicAdd(&h[d], (uint32_t)__popcll(peers));
   }
   __syncthreads();
   if (threadIdx.x < kRsDigits) counts[(uint64_t)threadIdx.x * ntiles + blockIdx.x] = h[threadIdx.x];
