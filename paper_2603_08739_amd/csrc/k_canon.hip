@@ -370,7 +370,16 @@ __global__ __launch_bounds__(256) void k_mult(const uint32_t* __restrict__ incl,
   }
 #pragma unroll
   for (int dd = 32; dd >= 1; dd >>= 1) best = max(best, (unsigned long long)__shfl_xor(best, dd, 64));
-  if (lane_id() == 0 && best) atomicMax(&st->mult, best);
+  // one global atomic per block: atomics of many blocks on one address
+  // are taken one at a time
+  __shared__ unsigned long long sb[256 / 64];
+  if (lane_id() == 0) sb[threadIdx.x / 64] = best;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    unsigned long long m = 0;
+    for (int w = 0; w < 256 / 64; ++w) m = max(m, sb[w]);
+    if (m) atomicMax(&st->mult, m);
+  }
 }
 
 // Partitioned order: inverse permutation and remapped links.
@@ -409,11 +418,16 @@ __global__ void k_group_keys(const uint8_t* __restrict__ g8, uint64_t n,
   }
 }
 
-uint32_t grid_of(uint64_t m) {
+uint32_t grid_of(uint64_t m, uint64_t cap = 32768) {
   uint64_t g = (m + 255) / 256;
-  if (g > 32768) g = 32768;
+  if (g > cap) g = cap;
   return (uint32_t)(g ? g : 1);
 }
+
+// Grids of the kernels that end with global atomics on one address per
+// block (trace statistics): a few blocks per compute unit, so that few
+// atomics queue on each address.
+constexpr uint64_t kReduceGrid = 1024;
 
 // One stable LSD pass over (keys, vals) on digit `shift`.
 kv_status radix_pass(const uint64_t* kin, const uint32_t* vin, uint64_t* kout, uint32_t* vout,
@@ -470,8 +484,9 @@ kv_status canon_build(Trace& t, const kv_trace_desc& d, hipStream_t s) {
 
   {
   StageTimer tm(kStLoadValidate, s);
-  hipLaunchKernelGGL(k_validate, dim3(grid_of(n)), dim3(256), 0, s, d.hash, d.req, d.group,
-                     d.weight, n, d.n_req, d.n_groups, o.g.as<uint8_t>(), o.w.as<uint8_t>(),
+  hipLaunchKernelGGL(k_validate, dim3(grid_of(n, 4 * kReduceGrid)), dim3(256), 0, s, d.hash, d.req,
+                     d.group, d.weight, n, d.n_req, d.n_groups, o.g.as<uint8_t>(),
+                     o.w.as<uint8_t>(),
                      ka.as<uint64_t>(), va.as<uint32_t>(), dstats);
   KV_HIP(hipGetLastError());
   hipLaunchKernelGGL(k_check_times, dim3(std::min<uint32_t>(div_up(d.n_req, 256), 4096)),
@@ -518,8 +533,9 @@ kv_status canon_build(Trace& t, const kv_trace_desc& d, hipStream_t s) {
   if ((st = t.blk_g.reserve(u)) != KV_OK) return st;
   {
   StageTimer tm(kStLoadLinks, s);
-  hipLaunchKernelGGL(k_links, dim3(grid_of(n)), dim3(256), 0, s, kin, vin, n, incl, newflag,
-                     firstpos, fincl, reinterpret_cast<uint4*>(kn.p), t.blk_w.as<uint8_t>(),
+  hipLaunchKernelGGL(k_links, dim3(grid_of(n, 4 * kReduceGrid)), dim3(256), 0, s, kin, vin, n,
+                     incl, newflag, firstpos, fincl, reinterpret_cast<uint4*>(kn.p),
+                     t.blk_w.as<uint8_t>(),
                      t.blk_g.as<uint8_t>(), runstart, o.w.as<uint8_t>(), o.g.as<uint8_t>(),
                      dstats);
   KV_HIP(hipGetLastError());
@@ -527,8 +543,8 @@ kv_status canon_build(Trace& t, const kv_trace_desc& d, hipStream_t s) {
                      reinterpret_cast<const uint4*>(kn.p), n, o.key.as<uint32_t>(),
                      o.nxt.as<uint32_t>(), o.bid.as<uint32_t>());
   KV_HIP(hipGetLastError());
-  hipLaunchKernelGGL(k_mult, dim3(grid_of(n)), dim3(256), 0, s, incl, newflag, n, runstart,
-                     dstats);
+  hipLaunchKernelGGL(k_mult, dim3(grid_of(n, kReduceGrid)), dim3(256), 0, s, incl, newflag, n,
+                     runstart, dstats);
   KV_HIP(hipGetLastError());
   hipLaunchKernelGGL(k_check_blocks, dim3(grid_of(n)), dim3(256), 0, s, o.bid.as<uint32_t>(),
                      t.blk_w.as<uint8_t>(), t.blk_g.as<uint8_t>(), o.w.as<uint8_t>(),
