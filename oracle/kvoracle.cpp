@@ -38,10 +38,16 @@
 //     request is available iff the tier holds it and block j-1 of the same
 //     request was available there (the first block needs only presence); the
 //     access is served by the fastest tier where it is available.
-//   * Exclusive hierarchy with write-back demotion (LRU only): a block lives
-//     in at most one tier; a hit in a lower tier removes it there and promotes
-//     it to the top tier; an overfull tier demotes its LRU block to the next
-//     tier's MRU end; blocks pushed past the last tier are dropped.
+//   * Exclusive hierarchy with write-back demotion: a block lives in at most
+//     one tier; a hit in a lower tier removes it there and promotes it to the
+//     top tier; an overfull tier demotes its victim to the next tier; blocks
+//     pushed past the last tier are dropped.  With LRU the demoted block
+//     enters the next tier's MRU end.  With FIFO or LFU a tier takes every
+//     block that enters it (a miss, a promotion, a demotion) as its newest
+//     member - FIFO: the newest insertion; LFU: frequency 1, touched now,
+//     the touches of the whole hierarchy being numbered in one sequence -
+//     and first passes its own victims down, each taken by the next tier the
+//     same way, before it admits the block.
 //   * Counts: hit_k = accesses served by k; miss_k = accesses that reached k
 //     (not served by a faster tier) and were not served by k; ins_k = blocks
 //     that entered k; evict_k = blocks that left k for lack of room (a
@@ -54,6 +60,9 @@
 #include <atomic>
 #include <cmath>
 #include <cstdint>
+#include <cstdlib>
+#include <functional>
+#include <memory>
 #include <list>
 #include <set>
 #include <thread>
@@ -103,8 +112,16 @@ class Tier {
     used_ += b.w;
   }
   uint64_t used() const { return used_; }
+  // Take a resident block out without an eviction (a promotion).
+  Block remove(uint64_t h) {
+    Block b = take(h);
+    used_ -= b.w;
+    return b;
+  }
 
  protected:
+  // policies of the exclusive mode only (LRU, FIFO, LFU) implement it
+  virtual Block take(uint64_t) { std::abort(); }
   virtual Block pop_victim() = 0;
   virtual void push(const Block& b, uint64_t t) = 0;
   uint64_t cap_;
@@ -122,6 +139,13 @@ class LruTier : public Tier {
   }
 
  protected:
+  Block take(uint64_t h) override {
+    auto it = pos_.at(h);
+    Block b = *it;
+    order_.erase(it);
+    pos_.erase(h);
+    return b;
+  }
   Block pop_victim() override {
     Block v = order_.back();
     order_.pop_back();
@@ -144,6 +168,13 @@ class FifoTier : public Tier {
   void hit(uint64_t, uint64_t) override {}
 
  protected:
+  Block take(uint64_t h) override {
+    auto it = pos_.at(h);
+    Block b = *it;
+    order_.erase(it);
+    pos_.erase(h);
+    return b;
+  }
   Block pop_victim() override {
     Block v = order_.back();
     order_.pop_back();
@@ -176,6 +207,12 @@ class LfuTier : public Tier {
     uint64_t freq, last;
     Block b;
   };
+  Block take(uint64_t h) override {
+    const Info in = info_.at(h);
+    order_.erase(std::make_tuple(in.freq, in.last, h));
+    info_.erase(h);
+    return in.b;
+  }
   Block pop_victim() override {
     auto first = *order_.begin();
     order_.erase(order_.begin());
@@ -492,6 +529,59 @@ void replay_exclusive(const std::vector<Block>& acc, const std::vector<uint32_t>
   }
 }
 
+// Exclusive hierarchy with write-back demotion under FIFO or LFU over the
+// accesses in `idx`: every tier is a cache of the policy; a block that enters
+// a tier is its newest member (LFU: frequency 1, touch number now), and the
+// tier passes its victims down before admitting it.
+void replay_exclusive_policy(const std::vector<Block>& acc, const std::vector<uint32_t>& idx,
+                             const uint64_t cap[kTiers], int policy, Counts& out) {
+  std::vector<int> live;  // non-absent tiers, fastest first
+  for (int k = 0; k < kTiers; ++k)
+    if (cap[k] > 0) live.push_back(k);
+  if (live.empty()) return;
+  std::vector<std::unique_ptr<Tier>> tier(kTiers);
+  for (int k : live) tier[k].reset(make_tier(policy, cap[k]));
+  std::unordered_map<uint64_t, int> where;  // hash -> tier holding it
+  uint64_t touch = 0;                       // one sequence for the hierarchy
+  // block b enters live tier number li; victims go to li + 1 first
+  std::function<void(size_t, const Block&)> enter = [&](size_t li, const Block& b) {
+    const int k = live[li];
+    tier[k]->insert(b, touch++, [&](const Block& v) {
+      where.erase(v.hash);
+      add(out, v.g, k, F_EVICT, 1);
+      add(out, v.g, k, F_EVICT_W, v.w);
+      if (li + 1 < live.size()) enter(li + 1, v);
+    });
+    where[b.hash] = k;
+    add(out, b.g, k, F_INS, 1);
+    add(out, b.g, k, F_INS_W, b.w);
+  };
+  const int top = live[0];
+  for (uint32_t i : idx) {
+    const Block& b = acc[i];
+    auto it = where.find(b.hash);
+    const int at = (it == where.end()) ? -1 : it->second;
+    for (int k : live) {
+      if (k == at) {
+        add(out, b.g, k, F_HIT, 1);
+        add(out, b.g, k, F_HIT_W, b.w);
+        break;
+      }
+      add(out, b.g, k, F_MISS, 1);
+      add(out, b.g, k, F_MISS_W, b.w);
+    }
+    if (at == top) {  // a hit in the top tier: the policy's update
+      tier[top]->hit(b.hash, touch++);
+      continue;
+    }
+    if (at >= 0) {  // a hit in a lower tier: taken out for promotion
+      tier[at]->remove(b.hash);
+      where.erase(b.hash);
+    }
+    enter(0, b);
+  }
+}
+
 struct ConfigView {
   const uint64_t* cap;        // [3]
   const uint64_t* cap_group;  // [3][16]
@@ -548,8 +638,8 @@ int replay_one(const std::vector<Block>& acc, const std::vector<std::vector<uint
       }
       if (c.mode == M_INCLUSIVE_PREFIX) return -4;
       if (c.mode == M_EXCLUSIVE) {
-        if (c.policy[g] != P_LRU) return -4;
-        replay_exclusive(acc, by_group[g], cg, out);
+        if (c.policy[g] == P_LRU) replay_exclusive(acc, by_group[g], cg, out);
+        else replay_exclusive_policy(acc, by_group[g], cg, c.policy[g], out);
       } else {
         replay_inclusive(acc, by_group[g], cg, c.policy[g], false, out);
       }
@@ -558,8 +648,8 @@ int replay_one(const std::vector<Block>& acc, const std::vector<std::vector<uint
     for (int k = 0; k < kTiers; ++k)
       if (bad_cap(c.cap[k])) return -1;
     if (c.mode == M_EXCLUSIVE) {
-      if (c.policy[0] != P_LRU) return -4;
-      replay_exclusive(acc, all, c.cap, out);
+      if (c.policy[0] == P_LRU) replay_exclusive(acc, all, c.cap, out);
+      else replay_exclusive_policy(acc, all, c.cap, c.policy[0], out);
     } else if (c.mode == M_INCLUSIVE_PREFIX) {
       if (c.policy[0] != P_LRU) return -4;
       replay_inclusive(acc, all, c.cap, P_LRU, true, out);
@@ -715,9 +805,10 @@ extern "C" {
 
 // Replays every configuration literally.  counts: uint64[n_cfg][n_groups][3][8].
 // req: request of every access (NULL: one request per access).  Returns 0,
-// or -1 for an invalid capacity (between 0 and the largest block), -4 for an
-// exclusive or prefix hierarchy with a policy other than LRU (or a
-// partitioned prefix one), -2 for bad sizes.
+// or -1 for an invalid capacity (between 0 and the largest block), -4 for a
+// prefix hierarchy with a policy other than LRU (or a partitioned one), for
+// radix-tree eviction outside the shared inclusive mode, or for a disk TTL
+// tier outside the shared inclusive LRU mode, -2 for bad sizes.
 int oracle_replay(uint64_t n, const uint64_t* hash, const uint8_t* group, const uint8_t* weight,
                   const uint32_t* req, uint32_t n_groups, uint32_t n_cfg, const uint64_t* cap,
                   const uint64_t* cap_group, const uint8_t* mode, const uint8_t* partitioned,

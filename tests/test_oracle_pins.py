@@ -205,6 +205,6 @@ def test_invalid_capacity_rejected(oracle_mod):
     t = tg.from_blocks([1, 2, 3], weights={1: 4, 2: 4, 3: 4})
     with pytest.raises(ValueError):
         oracle_mod.replay(t, tg.from_list([{"cap": (3, 0, 0)}]))
-    with pytest.raises(ValueError):
+    with pytest.raises(ValueError):   # prefix reuse is defined for LRU only
         oracle_mod.replay(tg.from_blocks([1, 2]),
-                          tg.from_list([{"cap": (3, 0, 0), "mode": 1, "policy": 1}]))
+                          tg.from_list([{"cap": (3, 0, 0), "mode": 2, "policy": 1}]))

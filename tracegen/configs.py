@@ -295,12 +295,14 @@ DEFAULT_COST = {
 
 def random_configs(seed: int, n: int, n_groups: int, w_max: int, cap_hi: int,
                    policies=(POLICY_LRU, POLICY_FIFO, POLICY_LFU), exclusive: bool = False,
-                   partitioned_frac: float = 0.5, zero_frac: float = 0.25) -> ConfigBatch:
+                   partitioned_frac: float = 0.5, zero_frac: float = 0.25,
+                   exclusive_policies=(POLICY_LRU,)) -> ConfigBatch:
     """Random candidate configurations for correctness tests.
 
     Capacities are 0 (absent, with probability ``zero_frac``) or uniform in
     [w_max, cap_hi]; with ``exclusive`` every configuration uses the
-    exclusive LRU hierarchy, otherwise the inclusive one with random policies.
+    exclusive hierarchy with group policies drawn from ``exclusive_policies``
+    (LRU only by default), otherwise the inclusive one with random policies.
     """
     rng = np.random.default_rng([seed, 7])
     b = empty(n)
@@ -317,7 +319,10 @@ def random_configs(seed: int, n: int, n_groups: int, w_max: int, cap_hi: int,
         part = n_groups > 1 and rng.random() < partitioned_frac
         if exclusive:
             b.mode[i] = MODE_EXCLUSIVE_DEMOTE
-            pol = [POLICY_LRU] * MAX_GROUPS
+            if len(exclusive_policies) == 1:
+                pol = [exclusive_policies[0]] * MAX_GROUPS
+            else:
+                pol = [int(rng.choice(exclusive_policies)) for _ in range(MAX_GROUPS)]
         else:
             pol = [int(rng.choice(policies)) for _ in range(MAX_GROUPS)]
         b.policy[i] = pol
