@@ -67,6 +67,9 @@ def parse():
                          "timed steps")
     ap.add_argument("--ttl-extra-only", action="store_true",
                     help="of the measurements after the timed steps, only the TTL curves")
+    ap.add_argument("--exclusive-extra-only", action="store_true",
+                    help="of the measurements after the timed steps, only the exclusive "
+                         "hierarchies replayed access by access")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="first run one plain device-to-device copy of BYTES (a reference "
                          "for hardware byte counters)")
@@ -409,6 +412,51 @@ def prefix_reuse(h, cfgs, G, model, torch, K):
     return out
 
 
+def exclusive_replay(torch, tg, host, K):
+    """Exclusive (write-back demotion) hierarchies that are no split stack,
+    replayed access by access: the tiny workload's 64 configurations as FIFO
+    and as LFU hierarchies, one wavefront walking the trace per
+    configuration.  Bound by the dependent memory accesses of that walk, so
+    the figure is the time per access of one configuration's walk."""
+    rec = tg.recipe("tiny")
+    base = tg.configs_for("tiny", rec)
+    parts = []
+    for p in (tg.POLICY_FIFO, tg.POLICY_LFU):
+        c = base.subset(np.arange(base.n))
+        c.mode[:] = tg.MODE_EXCLUSIVE_DEMOTE
+        c.policy[:, :] = p
+        parts.append(c)
+    cfgs = tg.ConfigBatch.concat(parts)
+    dev = rec.expand("cuda")
+    n = int(dev["hash"].numel())
+    G = rec.n_groups
+    h = K.kv_trace_load(dev["hash"], dev["req"], dev["req_time"], group=dev["group"],
+                        weight=dev["weight"], n_groups=G,
+                        tokens_per_granule=rec.tokens_per_granule,
+                        granule_bytes=rec.granule_bytes)
+    arr, n_cfg = host.config_array(cfgs)
+    model = host.cost_model(tg.DEFAULT_COST)
+    counts = torch.zeros((n_cfg, G, 3, 8), dtype=torch.int64, device="cuda")
+    K.kv_eval_configs(h, arr, n_cfg, model, counts, None)
+    torch.cuda.synchronize()
+    K.kv_timing_read(reset=True)
+    K.kv_timing_enable(True)
+    for _ in range(3):
+        K.kv_eval_configs(h, arr, n_cfg, model, counts, None)
+    torch.cuda.synchronize()
+    K.kv_timing_enable(False)
+    calls, ms = K.kv_timing_read(reset=True)["replay_excl"]
+    h.free()
+    per = ms / max(calls, 1)
+    print(f"[bench] exclusive replay: {per:.1f} ms for {n_cfg} configurations",
+          file=sys.stderr, flush=True)
+    return {"workload": "tiny", "n_accesses": n, "configs": n_cfg,
+            "policies": "FIFO and LFU, write-back demotion", "avg_launch_ms": per,
+            "launches": calls, "value": n * n_cfg / (per / 1000.0),
+            "unit": "block-accesses×configs/s", "ns_per_access": per * 1e6 / n,
+            "bound": "dependent memory latency of one lane's walk per configuration"}
+
+
 def extras(dev, rec, cfgs, G, model, n, torch, K, ttl_only=False):
     """Measurements outside the timed step: TTL curves, Alg. 1, prefix reuse,
     Alg. 2."""
@@ -579,12 +627,15 @@ def main():
     rec, cfgs, dev, G, model, n = ctx
     ttl = search = prefix = gttl = None
     workloads = None
-    if not args.no_extras:
+    if not args.no_extras and not args.exclusive_extra_only:
         ttl, search, prefix, gttl = extras(dev, rec, cfgs, G, model, n, torch, K,
                                            ttl_only=args.ttl_extra_only)
         del dev
         torch.cuda.empty_cache()
+    excl = None
     if not args.no_extras and not args.ttl_extra_only:
+        excl = exclusive_replay(torch, tg, host, K)
+    if not args.no_extras and not args.ttl_extra_only and not args.exclusive_extra_only:
         workloads = {}
         for w in ("tiny", "chat", "tenant", "longctx", "full"):
             if w == args.workload:
@@ -611,7 +662,7 @@ def main():
         "calls_ms": head["calls_ms"],
         "roofline": head["roofline"], "cpu_baseline": cpu, "workloads": workloads,
         "ttl_curves": ttl, "adaptive_search": search, "group_ttl": gttl,
-        "prefix_reuse": prefix,
+        "prefix_reuse": prefix, "exclusive_replay": excl,
     }
     print(json.dumps(out))
 

@@ -53,11 +53,19 @@ enum {
    * served by the fastest tier holding its block, then each tier applies its
    * own hit or insert (with eviction) rule. */
   KV_MODE_INCLUSIVE = 0,
-  /* LRU hierarchy with write-back demotion: a block lives in at most one
-   * tier; a hit in a lower tier promotes the block to the top tier, and an
-   * overfull tier demotes its least recently used block to the next tier
-   * (dropping it past the last tier).  Requires LRU and a trace whose
-   * blocks all have the same weight. */
+  /* Hierarchy with write-back demotion: a block lives in at most one tier;
+   * a hit in a lower tier promotes the block to the top tier, and an
+   * overfull tier demotes its victim to the next tier (dropping it past the
+   * last tier).  A block entering a tier (a miss, a promotion, a demotion)
+   * is that tier's newest member - LRU: most recently used; FIFO: newest
+   * insertion; LFU: count 1, touched now (one touch sequence per
+   * hierarchy) - and the tier passes its own victims down, each entering
+   * the next tier the same way, before it admits the block.  LRU over blocks
+   * of one weight is evaluated as a split stack; FIFO, LFU and LRU over
+   * mixed weights replay the trace once per configuration, one access after
+   * another (about a microsecond per access and configuration: meant for
+   * traces of up to some millions of accesses).  Not with LEAF, prefix
+   * reuse or a disk TTL tier. */
   KV_MODE_EXCLUSIVE_DEMOTE = 1,
   /* The inclusive hierarchy with prefix reuse, as in a radix-tree KV cache
    * (blocks are prefix-chained, Section 3.2): contents evolve exactly as in
@@ -346,10 +354,10 @@ const char* kv_last_error(void);
  *   6 stack: assembly, bins   7 stack: final depths    8 LRU records
  *   9 replay: job setup       10 replay: LFU jobs      11 replay: combine
  *   12 objectives             13 Pareto filter         14 replay: FIFO jobs
- *   15 TTL curves
+ *   15 TTL curves             16 replay: exclusive hierarchies
  * The replay kernels run on streams of their own, concurrently with the LRU
  * stages, so stage times may overlap. */
-enum { KV_STAGES = 16 };
+enum { KV_STAGES = 17 };
 typedef struct kv_timing {
   uint64_t calls[KV_STAGES];
   double ms[KV_STAGES];

@@ -20,7 +20,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libkvcfg.so")
 SOURCES = ["kv_api.cpp", "k_util.hip", "k_canon.hip", "k_stack.hip", "k_eval.hip",
-           "k_replay.hip", "k_ttl.hip", "k_leaf.hip"]
+           "k_replay.hip", "k_ttl.hip", "k_leaf.hip", "k_excl.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = ["-x", "hip", "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -80,6 +80,7 @@ __global__ __launch_bounds__(256) void k_lru_counts(const kv_config* __restrict_
                                                     OrderView pt, OrderView px, OrderView lf,
                                                     JointView jv,
                                                     const GroupStats* __restrict__ gs,
+                                                    uint32_t mixed,
                                                     uint64_t* __restrict__ counts,
                                                     double* __restrict__ store_cg) {
   const uint64_t tid = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -89,6 +90,8 @@ __global__ __launch_bounds__(256) void k_lru_counts(const kv_config* __restrict_
   const bool part = C.partitioned != 0;
   const uint32_t pol = part ? C.policy[g] : C.policy[0];
   if (pol != KV_POLICY_LRU && pol != KV_POLICY_LEAF) return;
+  // an exclusive hierarchy over mixed weights is no split stack: replayed
+  if (C.mode == KV_MODE_EXCLUSIVE_DEMOTE && mixed) return;
   // radix-tree eviction: distances of the re-touched order (shared tiers only)
   const OrderView& ov = pol == KV_POLICY_LEAF ? lf : (part && G > 1) ? pt : sh;
   uint64_t cap[3];
@@ -335,13 +338,14 @@ __global__ __launch_bounds__(256) void k_pareto_count(const uint8_t* __restrict_
 kv_status lru_counts(const kv_config* cfg_dev, uint32_t n_cfg, uint32_t n_groups,
                      OrderView shared, OrderView part, OrderView prefix, OrderView leaf,
                      JointView joint,
-                     const GroupStats* gs_dev, uint64_t* counts, double* store_cg,
+                     const GroupStats* gs_dev, bool mixed, uint64_t* counts, double* store_cg,
                      hipStream_t s) {
   const uint64_t m = (uint64_t)n_cfg * n_groups;
   if (m == 0) return KV_OK;
   StageTimer tm(kStLruCounts, s);
   hipLaunchKernelGGL(k_lru_counts, dim3(div_up(m, 256)), dim3(256), 0, s, cfg_dev, n_cfg,
-                     n_groups, shared, part, prefix, leaf, joint, gs_dev, counts, store_cg);
+                     n_groups, shared, part, prefix, leaf, joint, gs_dev, mixed ? 1u : 0u, counts,
+                     store_cg);
   KV_HIP(hipGetLastError());
   return KV_OK;
 }

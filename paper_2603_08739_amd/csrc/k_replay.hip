@@ -2214,6 +2214,7 @@ kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_conf
     for (uint32_t g = 0; g < ng; ++g) {
       const uint32_t pol = C.partitioned ? C.policy[g] : C.policy[0];
       if (pol == KV_POLICY_LRU || pol == KV_POLICY_LEAF) continue;
+      if (C.mode == KV_MODE_EXCLUSIVE_DEMOTE) continue;  // replayed access by access
       const uint32_t ord = part_order ? 1u : 0u;
       const uint32_t grp = part_order ? g : (uint32_t)KV_MAX_GROUPS;
       // a shared cache reports every group; a partitioned one only its own

@@ -213,7 +213,9 @@ kv_status check_device_error(Trace& t, bool wait, const char* who) {
   t.err_host[0] = t.err_host[1] = 0;
   KV_HIP(hipMemset(t.err.p, 0, 2 * sizeof(uint32_t)));
   std::string what = "replay job " + std::to_string(job);
-  if (job < t.err_jobs.size()) {
+  if (code == 2) {
+    what = "the exclusive hierarchy of configuration " + std::to_string(job);
+  } else if (job < t.err_jobs.size()) {
     const ReplayJobInfo& j = t.err_jobs[job];
     what += std::string(" (") + (j.policy == KV_POLICY_LFU ? "LFU" : "FIFO") + ", capacity " +
             std::to_string(j.cap) + " granules, " +
@@ -309,13 +311,6 @@ kv_status validate_configs(const Trace& t, const kv_config* cfg, uint32_t n_cfg,
     if (C.mode == KV_MODE_INCLUSIVE_PREFIX &&
         (C.partitioned || C.policy[0] != KV_POLICY_LRU))
       return fail(KV_ERR_UNSUPPORTED, at + "prefix reuse supports shared LRU tiers only");
-    if (C.mode == KV_MODE_EXCLUSIVE_DEMOTE) {
-      for (uint32_t g = 0; g < ng; ++g)
-        if (C.policy[g] != KV_POLICY_LRU)
-          return fail(KV_ERR_UNSUPPORTED, at + "the exclusive mode supports LRU only");
-      if (t.st.w_min != t.st.w_max)
-        return fail(KV_ERR_UNSUPPORTED, at + "the exclusive mode needs uniform block weights");
-    }
   }
   return KV_OK;
 }
@@ -680,6 +675,8 @@ kv_status kv_eval_configs(const kv_trace* h, const kv_config* cfg, uint32_t n_cf
   std::vector<std::vector<double>> tttl(G);  // disk TTL values per group
   bool need_shared = false, need_part = false, need_prefix = false, need_joint = false;
   const uint64_t w0 = t->st.w_max;
+  const bool mixed = t->st.w_min != t->st.w_max;
+  bool need_excl = false;
   std::map<std::tuple<uint32_t, uint32_t, uint32_t, uint64_t>, uint32_t> job_index;
   std::vector<ReplayJob> jobs;
   for (uint32_t c = 0; c < n_cfg; ++c) {
@@ -688,6 +685,10 @@ kv_status kv_eval_configs(const kv_trace* h, const kv_config* cfg, uint32_t n_cf
     const uint32_t ng = C.partitioned ? G : 1;
     for (uint32_t g = 0; g < ng; ++g) {
       const uint32_t pol = group_policy(C, g);
+      if (excl_replayed(C, g, mixed)) {  // replayed access by access
+        need_excl = true;
+        continue;
+      }
       if (pol == KV_POLICY_LEAF) {
         for (uint32_t gg = 0; gg < G; ++gg) add_thresholds(tlf, C, 0, gg, w0);
         continue;
@@ -783,8 +784,8 @@ kv_status kv_eval_configs(const kv_trace* h, const kv_config* cfg, uint32_t n_cf
         return r;
     }
     if (need_shared || need_part || need_leaf)
-      return lru_counts(cfg_dev, n_cfg, G, vsh, vpt, vpx, vlf, jv, bgs.as<GroupStats>(), counts,
-                        store_cg, s);
+      return lru_counts(cfg_dev, n_cfg, G, vsh, vpt, vpx, vlf, jv, bgs.as<GroupStats>(), mixed,
+                        counts, store_cg, s);
     return KV_OK;
   };
   // ---- FIFO / LFU: replay jobs, with the LRU work running meanwhile
@@ -793,6 +794,8 @@ kv_status kv_eval_configs(const kv_trace* h, const kv_config* cfg, uint32_t n_cf
   } else if ((st = lru()) != KV_OK) {
     return st;
   }
+  // ---- exclusive hierarchies without a split stack
+  if (need_excl && (st = excl_run(*t, cfg, cfg_dev, n_cfg, counts, s)) != KV_OK) return st;
   // ---- objectives
   if (obj) {
     st = objectives(cfg_dev, n_cfg, G, counts, store_cg, *model, (double)t->gb, (double)t->tpg,

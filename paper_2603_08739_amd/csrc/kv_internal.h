@@ -144,6 +144,7 @@ struct Trace {
   std::vector<uint8_t> job_stage, rec_stage, src_stage;
   std::vector<double> ttl_stage;
   std::vector<unsigned long long> jc_stage;
+  std::vector<uint8_t> excl_stage;
 };
 
 constexpr uint64_t kTraceMagic = 0x6b7663666774726bull;  // "kvcfgtrk"
@@ -155,7 +156,7 @@ constexpr uint64_t kDeadMagic = 0x646561646b766366ull;
 enum Stage {
   kStLoadValidate = 0, kStLoadSort, kStLoadLinks, kStPartition, kStStackMatrix,
   kStStackLocal, kStStackAssemble, kStStackFinal, kStLruCounts, kStReplayInit, kStReplay,
-  kStCombine, kStObjectives, kStPareto, kStReplayFifo, kStTtl
+  kStCombine, kStObjectives, kStPareto, kStReplayFifo, kStTtl, kStReplayExcl
 };
 // Records an event pair around a scope when timing is enabled.
 struct StageTimer {
@@ -216,7 +217,9 @@ struct JointView {
   const uint64_t* fh = nullptr;
   const double* wd = nullptr;
 };
-// Writes the records of every (config, group) whose policy is LRU.  Groups of
+// Writes the records of every (config, group) whose policy is LRU, except
+// exclusive hierarchies over blocks of mixed weights (`mixed`), which are
+// replayed.  Groups of
 // partitioned configs read `part` when n_groups > 1, `shared` otherwise;
 // prefix-reuse configs take their hits from `prefix` (trace order).
 // Disk TTL tiers take tier 2 from `joint` and write the storage-time
@@ -224,7 +227,7 @@ struct JointView {
 kv_status lru_counts(const kv_config* cfg_dev, uint32_t n_cfg, uint32_t n_groups,
                      OrderView shared, OrderView part, OrderView prefix, OrderView leaf,
                      JointView joint,
-                     const GroupStats* gs_dev, uint64_t* counts, double* store_cg,
+                     const GroupStats* gs_dev, bool mixed, uint64_t* counts, double* store_cg,
                      hipStream_t s);
 // store_cg: [n_cfg][n_groups] or NULL (no disk TTL tier in the batch).
 kv_status objectives(const kv_config* cfg_dev, uint32_t n_cfg, uint32_t n_groups,
@@ -267,5 +270,15 @@ struct ReplayJob {
 kv_status replay_run(Trace& t, const std::vector<ReplayJob>& jobs, const kv_config* cfg_host,
                      const kv_config* cfg_dev, uint32_t n_cfg, uint64_t* counts,
                      hipStream_t s, const std::function<kv_status()>& meanwhile);
+
+// exclusive hierarchies replayed access by access (k_excl.hip)
+// Whether hierarchy g of C (group g when partitioned, 0 otherwise) is
+// replayed there: the exclusive mode under FIFO or LFU, or under LRU when
+// the trace's blocks have mixed weights (otherwise a split stack serves it).
+bool excl_replayed(const kv_config& C, uint32_t g, bool mixed);
+// Writes the records of every replayed hierarchy of the batch (the records
+// of a shared hierarchy: every group).
+kv_status excl_run(Trace& t, const kv_config* cfg_host, const kv_config* cfg_dev,
+                   uint32_t n_cfg, uint64_t* counts, hipStream_t s);
 
 }  // namespace kv

@@ -63,11 +63,11 @@ class kv_cost_model(ctypes.Structure):
                 ("reserved", _u32), ("media", kv_disk_medium * KV_MAX_MEDIA)]
 
 
-KV_STAGES = 16
+KV_STAGES = 17
 STAGE_NAMES = ("load_validate", "load_sort", "load_links", "partition", "stack_matrix",
                "stack_local", "stack_assemble", "stack_final", "lru_counts", "replay_init",
                "replay_lfu", "replay_combine", "objectives", "pareto", "replay_fifo",
-               "ttl_curves")
+               "ttl_curves", "replay_excl")
 
 
 class kv_timing(ctypes.Structure):

@@ -210,7 +210,7 @@ def test_error_paths(lib):
     st = h.info()
     assert (st.n, st.n_distinct, st.w_min, st.w_max) == (4, 3, 1, 4)
     for bad, status in [({"cap": (2, 0, 0)}, kvcfg.KV_ERR_INVALID),
-                        ({"cap": (8, 0, 0), "mode": 1}, kvcfg.KV_ERR_UNSUPPORTED),
+                        ({"cap": (8, 0, 0), "mode": 2, "policy": 1}, kvcfg.KV_ERR_UNSUPPORTED),
                         ({"cap": (8, 0, 0), "policy": 5}, kvcfg.KV_ERR_INVALID)]:
         with pytest.raises(kvcfg.KvError) as e:
             host.evaluate(h, tg.from_list([bad]), tg.DEFAULT_COST, 1)
