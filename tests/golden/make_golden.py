@@ -15,9 +15,10 @@ full literal replay), and of the full workload's 11,000 configurations over
 387 M accesses the 8 corners of its LRU grid, 8 more LRU draws and 8 draws
 each of its FIFO and LFU points (every distinct tier cache is a literal
 replay of the whole trace).  Two variants evaluate the chat trace under other
-batches: its grid under radix-tree (leaf-first) eviction (``chat_leaf``) and
-an HBM x DRAM x disk-TTL grid over an unbounded TTL disk tier
-(``chat_ttl``), all configurations of each; and two over the large traces:
+batches: its grid under radix-tree (leaf-first) eviction (``chat_leaf``), an
+HBM x DRAM x disk-TTL grid over an unbounded TTL disk tier (``chat_ttl``),
+and a 32-point grid of exclusive FIFO and LFU hierarchies (``chat_excl``), all
+configurations of each; and two over the large traces:
 the full workload's trace over a 16-point HBM x DRAM x disk-TTL grid
 (``full_ttl``) and the long-context trace under leaf-first eviction on a
 64-point inclusive subset of its grid (``longctx_leaf``).
@@ -41,8 +42,8 @@ import tracegen as tg  # noqa: E402
 from tracegen.digest import configs_digest, trace_digest  # noqa: E402
 from oracle import oracle as O  # noqa: E402
 
-NAMES = ("tiny", "chat", "tenant", "longctx", "full", "chat_leaf", "chat_ttl", "full_ttl",
-         "longctx_leaf")
+NAMES = ("tiny", "chat", "tenant", "longctx", "full", "chat_leaf", "chat_ttl", "chat_excl",
+         "full_ttl", "longctx_leaf")
 
 
 def golden_path(name: str) -> str:

@@ -9,7 +9,8 @@ oracle element by element, objectives to 1e-6.
   configuration (an LRU group over unit weights keeps its split stack), and
   small capacities that cascade demotions through every tier;
 * batches mixing these with inclusive and split-stack configurations;
-* workload-shaped slices (the mixed tenant and long-context traces);
+* workload-shaped slices (the mixed tenant and long-context traces, and
+  the full workload's weighted blocks under exclusive LRU, FIFO and LFU);
 * state buffers forced small, so that the configurations run in waves.
 """
 import os
@@ -125,3 +126,18 @@ def test_waves(oracle_mod):
     one = compare(oracle_mod, t, cfgs, "one-wave")
     for b in (40_000, 1):
         assert np.array_equal(one, compare(oracle_mod, t, cfgs, f"waves{b}", budget=b))
+
+
+def test_full_slice_weighted(oracle_mod):
+    """A slice of the full workload (16- and 64-token blocks, weights 1 and
+    4) as exclusive LRU, FIFO and LFU hierarchies at scaled-down
+    capacities: weighted LRU, no split stack, is replayed too."""
+    t = tg.full(n_req=4000)
+    cfgs = tg.configs_for("full", t)
+    pick = np.concatenate([np.arange(0, 10000, 1667), np.arange(10000, 11000, 200)])
+    sub = cfgs.subset(pick)
+    sub.cap //= 16
+    sub.cap[(sub.cap > 0) & (sub.cap < 4)] = 4
+    sub.mode[:] = tg.MODE_EXCLUSIVE_DEMOTE
+    assert set(sub.policy[:, 0]) == {tg.POLICY_LRU, tg.POLICY_FIFO, tg.POLICY_LFU}
+    compare(oracle_mod, t, sub, "full-slice-exclusive")

@@ -30,8 +30,8 @@ from tracegen.digest import configs_digest, trace_digest
 pytestmark = pytest.mark.gpu
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-NAMES = ("tiny", "chat", "tenant", "longctx", "full", "chat_leaf", "chat_ttl", "full_ttl",
-         "longctx_leaf")
+NAMES = ("tiny", "chat", "tenant", "longctx", "full", "chat_leaf", "chat_ttl", "chat_excl",
+         "full_ttl", "longctx_leaf")
 FIELDS = ("hit", "miss", "ins", "evict", "hit_w", "miss_w", "ins_w", "evict_w")
 
 

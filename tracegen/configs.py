@@ -226,6 +226,17 @@ def chat_ttl_configs(granule_bytes) -> ConfigBatch:
     return from_list(items)
 
 
+def chat_excl_configs(granule_bytes) -> ConfigBatch:
+    """32 = HBM {1, 4, 16, 64} GiB x DRAM {16, 256} GiB x SSD {0, 1} TiB x
+    {FIFO, LFU}: write-back-demotion (exclusive) hierarchies, which have no
+    stack property under these policies and are replayed access by access."""
+    parts = []
+    for p in (POLICY_FIFO, POLICY_LFU):
+        parts.append(grid([1, 4, 16, 64], [16, 256], [0, 1], granule_bytes,
+                          mode=MODE_EXCLUSIVE_DEMOTE, policy=p, segment=p))
+    return ConfigBatch.concat(parts)
+
+
 def full_ttl_configs(granule_bytes) -> ConfigBatch:
     """16 = HBM {4, 40} GiB x DRAM {0, 512} GiB x disk TTL {0, 60, 600, 3600} s:
     LRU HBM and DRAM over an unbounded TTL disk tier."""
@@ -245,7 +256,7 @@ def longctx_leaf_configs(granule_bytes) -> ConfigBatch:
 
 
 # Workload variants: the same trace under other configuration batches.
-VARIANTS = {"chat_leaf": "chat", "chat_ttl": "chat", "full_ttl": "full",
+VARIANTS = {"chat_leaf": "chat", "chat_ttl": "chat", "chat_excl": "chat", "full_ttl": "full",
             "longctx_leaf": "longctx"}
 
 
@@ -260,6 +271,8 @@ def configs_for(name: str, trace) -> ConfigBatch:
         return chat_leaf_configs(gb)
     if name == "chat_ttl":
         return chat_ttl_configs(gb)
+    if name == "chat_excl":
+        return chat_excl_configs(gb)
     if name == "full_ttl":
         return full_ttl_configs(gb)
     if name == "longctx_leaf":
