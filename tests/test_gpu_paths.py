@@ -166,3 +166,67 @@ def test_binding_rejects_bad_outputs():
                                                               device="cuda"))
     K.kv_eval_configs(h, arr, n, model, good)
     h.free()
+
+
+def test_maximum_trace_size():
+    """A trace of exactly 2^29 accesses, the library's limit (the position
+    range every kernel's 32-bit positions and the stack pass's block matrix
+    are sized for), checked by facts that hold exactly at any size: at
+    capacity 1 an LRU cache hits exactly the immediate repeats; a capacity
+    holding every block misses only the first accesses; LRU hits never fall
+    as the capacity grows; inclusive tiers split the single-cache hits of
+    their capacities; an exclusive LRU hierarchy of unit blocks hits like
+    one LRU cache of the summed capacity in total and like its top tier's
+    capacity at the top; FIFO and LFU replays conserve their counts."""
+    import torch
+    from paper_2603_08739_amd import host, kvcfg as K
+    n = 1 << 29
+    say(f"  case max-size: n={n}")
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(29)
+    pool = 1 << 22
+    u = torch.rand(n, device="cuda", generator=gen)
+    ids = (u.pow(3.0) * pool).long().clamp_(max=pool - 1)  # low ids hot
+    del u
+    # distinct ids -> distinct 64-bit hashes (an odd multiplier is a bijection mod 2^64)
+    mult = 0x9E3779B97F4A7C15 - (1 << 64)
+    hashes = ids * mult + 0x2545F4914F6CDD1D
+    req = (torch.arange(n, device="cuda", dtype=torch.int64) // 64).to(torch.int32)
+    req_time = torch.arange(n // 64, device="cuda", dtype=torch.float64) * 0.01
+    distinct = int(torch.unique(ids).numel())
+    repeats = int((ids[1:] == ids[:-1]).sum())
+    del ids
+    torch.cuda.synchronize()
+    h = K.kv_trace_load(hashes, req, req_time)
+    del hashes, req
+    st = h.info()
+    assert st.n == n and st.n_distinct == distinct
+    say(f"  {distinct} distinct blocks, {repeats} immediate repeats")
+    caps = [1, 16, 4096, 65536, 1 << 20, distinct]
+    items = [{"cap": (c, 0, 0)} for c in caps]
+    items += [{"cap": (4096, 65536, 1 << 20)},
+              {"cap": (4096, 61440, 0), "mode": tg.MODE_EXCLUSIVE_DEMOTE},
+              {"cap": (65536, 0, 0), "policy": tg.POLICY_FIFO},
+              {"cap": (65536, 0, 0), "policy": tg.POLICY_LFU},
+              {"cap": (distinct, 0, 0), "policy": tg.POLICY_LFU}]
+    cfgs = tg.from_list(items)
+    counts, _ = host.evaluate(h, cfgs, tg.DEFAULT_COST, 1)
+    h.free()
+    c = counts[:, 0].astype(np.int64)
+    lru = c[:len(caps), 0, 0]
+    assert lru[0] == repeats
+    assert lru[-1] == n - distinct
+    assert np.all(np.diff(lru) >= 0)
+    hit = dict(zip(caps, lru))
+    inc = c[len(caps)]
+    assert inc[0, 0] == hit[4096] and inc[1, 0] == hit[65536] - hit[4096]
+    assert inc[2, 0] == hit[1 << 20] - hit[65536]
+    exc = c[len(caps) + 1]
+    assert exc[0, 0] == hit[4096] and exc[0, 0] + exc[1, 0] == hit[65536]
+    for r in c[len(caps) + 2:]:
+        top = r[0]
+        assert top[0] + top[1] == n and top[2] == top[1]      # hits + misses; every miss inserts
+        assert 0 <= top[2] - top[3] <= 65536 or top[3] == 0   # what stays fits
+        assert repeats <= top[0] <= n - distinct
+    assert c[-1, 0, 0] == n - distinct and c[-1, 0, 3] == 0   # holds every block
+    torch.cuda.empty_cache()
