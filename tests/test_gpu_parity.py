@@ -209,6 +209,11 @@ def test_error_paths(lib):
     h = host.load(t)
     st = h.info()
     assert (st.n, st.n_distinct, st.w_min, st.w_max) == (4, 3, 1, 4)
+    # an empty batch and an empty Pareto call are no-ops on a live trace
+    counts, obj = host.evaluate(h, tg.from_list([]), tg.DEFAULT_COST, 1)
+    assert counts.shape == (0, 1, 3, 8) and obj.shape == (0, 3)
+    flags, n_front = host.pareto(np.zeros((0, 3)))
+    assert flags.shape == (0,) and n_front == 0
     for bad, status in [({"cap": (2, 0, 0)}, kvcfg.KV_ERR_INVALID),
                         ({"cap": (8, 0, 0), "mode": 2, "policy": 1}, kvcfg.KV_ERR_UNSUPPORTED),
                         ({"cap": (8, 0, 0), "policy": 5}, kvcfg.KV_ERR_INVALID)]:
