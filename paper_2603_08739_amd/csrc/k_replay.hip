@@ -458,15 +458,42 @@ __device__ __forceinline__ void fifo_chunked(const JobDev& j, const JobArgs& a,
 #pragma unroll
     for (int e = 0; e < kRIt; ++e) sa[e] = sb[e];
   }
-  // evictions = insertions - blocks still queued at the end
+  // evictions = insertions - blocks still queued at the end.  The pass over
+  // every block's state is bound by load latency: each thread keeps kEndU
+  // loads in flight, and with one group the queued blocks add up in
+  // registers (LDS atomics on one address are taken one lane at a time).
   if (tid < KV_MAX_GROUPS) F.fin[tid] = F.finw[tid] = 0;
   __syncthreads();
-  for (uint64_t b = tid; b < a.u; b += kRNT) {
-    const uint32_t s = S[b];
-    if (s != kNoIns32 && (uint64_t)(W0 - s) <= j.cap) {
-      const uint32_t g = a.blk_g[b];
-      atomicAdd(&F.fin[g], 1ull);
-      atomicAdd(&F.finw[g], (unsigned long long)a.blk_w[b]);
+  constexpr int kEndU = 8;
+  unsigned long long fc = 0, fw = 0;
+  for (uint64_t b0 = tid; b0 < a.u; b0 += (uint64_t)kRNT * kEndU) {
+    uint32_t s[kEndU], bw[kEndU], bg[kEndU];
+#pragma unroll
+    for (int q = 0; q < kEndU; ++q) {
+      const uint64_t b = b0 + (uint64_t)q * kRNT;
+      const bool in = b < a.u;
+      s[q] = in ? S[b] : kNoIns32;
+      bw[q] = in ? a.blk_w[b] : 0u;
+      bg[q] = in ? a.blk_g[b] : 0u;
+    }
+#pragma unroll
+    for (int q = 0; q < kEndU; ++q) {
+      if (s[q] == kNoIns32 || (uint64_t)(W0 - s[q]) > j.cap) continue;
+      if (g1) {
+        ++fc;
+        fw += bw[q];
+      } else {
+        atomicAdd(&F.fin[bg[q]], 1ull);
+        atomicAdd(&F.finw[bg[q]], (unsigned long long)bw[q]);
+      }
+    }
+  }
+  if (g1) {
+    fc = wave_sum(fc);
+    fw = wave_sum(fw);
+    if (lane_id() == 0 && fc) {
+      atomicAdd(&F.fin[g0], fc);
+      atomicAdd(&F.finw[g0], fw);
     }
   }
   __syncthreads();
