@@ -245,6 +245,71 @@ __global__ __launch_bounds__(kRsNT) void k_rs_scatter(const uint64_t* __restrict
   }
 }
 
+// The sort runs its passes over the hashes' high 32 bits only; hashes that
+// share them sit interleaved (in position order) in one run of equal high
+// bits, and only such mixed runs are sorted again, by (run, low 32 bits).
+// Runs of equal high bits: a flag at each run's first element.
+__global__ __launch_bounds__(256) void k_hi_starts(const uint64_t* __restrict__ K, uint64_t n,
+                                                   uint32_t* __restrict__ start) {
+  for (uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; k < n;
+       k += (uint64_t)gridDim.x * blockDim.x)
+    start[k] = (k == 0 || (K[k - 1] >> 32) != (K[k] >> 32)) ? 1u : 0u;
+}
+
+// A run (0-based id = inclusive run count - 1) is mixed when two neighbours
+// in it differ in their low bits.
+__global__ __launch_bounds__(256) void k_hi_mixed(const uint64_t* __restrict__ K, uint64_t n,
+                                                  const uint32_t* __restrict__ runincl,
+                                                  uint32_t* __restrict__ mixed) {
+  for (uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x + 1; k < n;
+       k += (uint64_t)gridDim.x * blockDim.x)
+    if (K[k - 1] != K[k] && (K[k - 1] >> 32) == (K[k] >> 32)) mixed[runincl[k] - 1u] = 1u;
+}
+
+// Elements of mixed runs.
+__global__ __launch_bounds__(256) void k_hi_inmixed(const uint32_t* __restrict__ runincl,
+                                                    const uint32_t* __restrict__ mixed,
+                                                    uint64_t n, uint32_t* __restrict__ flag) {
+  for (uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; k < n;
+       k += (uint64_t)gridDim.x * blockDim.x)
+    flag[k] = mixed[runincl[k] - 1u];
+}
+
+// Gathers the elements of mixed runs in order: key (run id, low bits),
+// position, and where the element sits.
+__global__ __launch_bounds__(256) void k_hi_gather(const uint64_t* __restrict__ K,
+                                                   const uint32_t* __restrict__ V, uint64_t n,
+                                                   const uint32_t* __restrict__ runincl,
+                                                   const uint32_t* __restrict__ flag,
+                                                   const uint32_t* __restrict__ at,
+                                                   uint64_t* __restrict__ ck,
+                                                   uint32_t* __restrict__ cv,
+                                                   uint32_t* __restrict__ ci) {
+  for (uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; k < n;
+       k += (uint64_t)gridDim.x * blockDim.x) {
+    if (!flag[k]) continue;
+    const uint32_t j = at[k];
+    ck[j] = ((uint64_t)(runincl[k] - 1u) << 32) | (K[k] & 0xFFFFFFFFull);
+    cv[j] = V[k];
+    ci[j] = (uint32_t)k;
+  }
+}
+
+// Puts the sorted elements of the mixed runs back in their runs' slots (the
+// gathered slots of a run are contiguous and keep their order).
+__global__ __launch_bounds__(256) void k_hi_scatter(const uint64_t* __restrict__ ck,
+                                                    const uint32_t* __restrict__ cv,
+                                                    const uint32_t* __restrict__ ci, uint64_t m,
+                                                    uint64_t* __restrict__ K,
+                                                    uint32_t* __restrict__ V) {
+  for (uint64_t j = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; j < m;
+       j += (uint64_t)gridDim.x * blockDim.x) {
+    const uint32_t k = ci[j];
+    K[k] = (K[k] & 0xFFFFFFFF00000000ull) | (ck[j] & 0xFFFFFFFFull);
+    V[k] = cv[j];
+  }
+}
+
 // Run starts in hash order: the first element of every group of equal
 // hashes (its first occurrence: ties in the sort go by position).
 __global__ __launch_bounds__(256) void k_run_flags(const uint64_t* __restrict__ K, uint64_t n,
@@ -429,6 +494,15 @@ uint32_t grid_of(uint64_t m, uint64_t cap = 32768) {
 // atomics queue on each address.
 constexpr uint64_t kReduceGrid = 1024;
 
+// Traces from this length on are sorted by their hashes' high bits first;
+// KVCFG_TEST_HIGH_FIRST=1 (read at every load) takes that path for any
+// length, so that short test traces reach it.
+constexpr uint64_t kHighFirstN = 1ull << 23;
+bool high_first_forced() {
+  const char* e = std::getenv("KVCFG_TEST_HIGH_FIRST");
+  return e && e[0] == '1';
+}
+
 // One stable LSD pass over (keys, vals) on digit `shift`.
 kv_status radix_pass(const uint64_t* kin, const uint32_t* vin, uint64_t* kout, uint32_t* vout,
                      uint64_t n, int shift, uint32_t* counts, uint32_t* scan_scratch,
@@ -494,17 +568,69 @@ kv_status canon_build(Trace& t, const kv_trace_desc& d, hipStream_t s) {
   KV_HIP(hipGetLastError());
   }
 
-  // 8 stable passes of 8 bits: (hash, position) sorted by hash, ties by position
+  // (hash, position) sorted by hash, ties by position.  Long traces: 4
+  // stable passes of 8 bits over the high 32 bits, then the runs of equal
+  // high bits that mix hashes sorted again by (run, low 32 bits) - for
+  // random hashes a few thousand short runs, in the worst case every element.
+  // Shorter ones: all 8 passes (the second sort's launches and its host
+  // round trip would cost more than the 4 passes they save).
   uint64_t *kin = ka.as<uint64_t>(), *kout = kb.as<uint64_t>();
   uint32_t *vin = va.as<uint32_t>(), *vout = vb.as<uint32_t>();
+  const bool high_first = n >= kHighFirstN || high_first_forced();
   {
     StageTimer tm(kStLoadSort, s);
-    for (int shift = 0; shift < 64; shift += 8) {
+    for (int shift = high_first ? 32 : 0; shift < 64; shift += 8) {
       st = radix_pass(kin, vin, kout, vout, n, shift, counts.as<uint32_t>(),
                       scratch.as<uint32_t>(), s);
       if (st != KV_OK) return st;
       std::swap(kin, kout);
       std::swap(vin, vout);
+    }
+  }
+  if (high_first) {
+    StageTimer tm(kStLoadSort, s);
+    // free now: kout (2n u32), vout (n u32), fl (3n u32), kn (4n u32)
+    uint32_t* flag = vout;
+    uint32_t* runincl = reinterpret_cast<uint32_t*>(kout);
+    uint32_t* mixed = runincl + n;  // per run, run ids < n
+    uint32_t* at = fl.as<uint32_t>();
+    hipLaunchKernelGGL(k_hi_starts, dim3(grid_of(n)), dim3(256), 0, s, kin, n, flag);
+    KV_HIP(hipGetLastError());
+    if ((st = scan_u32(flag, runincl, n, true, scratch.as<uint32_t>(), s)) != KV_OK) return st;
+    if ((st = fill_u32(mixed, 0u, n, s)) != KV_OK) return st;
+    hipLaunchKernelGGL(k_hi_mixed, dim3(grid_of(n)), dim3(256), 0, s, kin, n, runincl, mixed);
+    KV_HIP(hipGetLastError());
+    hipLaunchKernelGGL(k_hi_inmixed, dim3(grid_of(n)), dim3(256), 0, s, runincl, mixed, n, flag);
+    KV_HIP(hipGetLastError());
+    if ((st = scan_u32(flag, at, n, false, scratch.as<uint32_t>(), s)) != KV_OK) return st;
+    uint32_t last[3] = {0, 0, 0};
+    KV_HIP(hipMemcpyAsync(&last[0], at + (n - 1), 4, hipMemcpyDeviceToHost, s));
+    KV_HIP(hipMemcpyAsync(&last[1], flag + (n - 1), 4, hipMemcpyDeviceToHost, s));
+    KV_HIP(hipMemcpyAsync(&last[2], runincl + (n - 1), 4, hipMemcpyDeviceToHost, s));
+    KV_HIP(hipStreamSynchronize(s));
+    const uint64_t m = (uint64_t)last[0] + last[1];
+    // the second sort's key: run id (below the run count) above the low 32 bits
+    int key_bits = 32;
+    while (key_bits < 64 && (uint64_t)(last[2] - 1) >> (key_bits - 32)) ++key_bits;
+    if (m) {
+      uint64_t* ck = reinterpret_cast<uint64_t*>(kn.p);  // m u64, then m more
+      uint64_t* ck2 = ck + m;
+      uint32_t* cv = at + n;                             // m u32, then m more
+      uint32_t* cv2 = cv + m;
+      uint32_t* ci = mixed;                              // free after k_hi_inmixed
+      hipLaunchKernelGGL(k_hi_gather, dim3(grid_of(n)), dim3(256), 0, s, kin, vin, n, runincl,
+                         flag, at, ck, cv, ci);
+      KV_HIP(hipGetLastError());
+      for (int shift = 0; shift < key_bits; shift += 8) {
+        st = radix_pass(ck, cv, ck2, cv2, m, shift, counts.as<uint32_t>(),
+                        scratch.as<uint32_t>(), s);
+        if (st != KV_OK) return st;
+        std::swap(ck, ck2);
+        std::swap(cv, cv2);
+      }
+      hipLaunchKernelGGL(k_hi_scatter, dim3(grid_of(m)), dim3(256), 0, s, ck, cv, ci, m, kin,
+                         vin);
+      KV_HIP(hipGetLastError());
     }
   }
   // kin / vin now hold the sorted pairs; the other pair of buffers is free.

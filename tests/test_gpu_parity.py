@@ -348,3 +348,47 @@ def test_lfu_long_victim_queue(lib, oracle_mod, seed):
     caps = [2_000, 3_000, 6_000, 9_000, 11_000]
     items = [{"cap": (c, 0, 0), "policy": 2} for c in caps]
     compare(lib, oracle_mod, t, tg.from_list(items), label=f"longq{seed}")
+
+
+@pytest.mark.parametrize("high_first", [False, True])
+@pytest.mark.parametrize("layout", ["high_zero", "shared_high", "shared_low", "few_high"])
+def test_hashes_sharing_bits(lib, oracle_mod, layout, high_first):
+    """Hash layouts that make the load's sort work.  Long traces are sorted
+    by the hashes' high 32 bits first, and runs of equal high bits holding
+    several hashes again by their low bits (KVCFG_TEST_HIGH_FIRST=1 takes
+    that path at this length); hashes below 2^32 put every access in one
+    such run, pools that share high (or low) bits make many."""
+    rng = np.random.default_rng([61, len(layout)])
+    n, u = 30_000, 900
+    if layout == "high_zero":
+        pool = rng.choice(1 << 32, size=u, replace=False).astype(np.uint64)
+    elif layout == "few_high":
+        pool = (rng.integers(0, 3, size=u).astype(np.uint64) << np.uint64(32)) | \
+            rng.choice(1 << 20, size=u, replace=False).astype(np.uint64)
+    else:
+        hi = rng.integers(1, 1 << 32, size=u // 9, dtype=np.uint64)
+        lo = rng.integers(0, 1 << 32, size=u // 9, dtype=np.uint64)
+        if layout == "shared_high":   # 9 blocks per high value
+            pool = (np.repeat(hi, 9) << np.uint64(32)) | \
+                rng.choice(1 << 32, size=u, replace=False).astype(np.uint64)
+        else:                          # 9 blocks per low value
+            pool = (rng.choice(1 << 31, size=u, replace=False).astype(np.uint64) << np.uint64(32)) | \
+                np.repeat(lo, 9)
+    pool = np.unique(pool.astype(np.uint64))
+    zipf = 1.0 / np.arange(1, pool.size + 1) ** 0.8
+    pick = rng.choice(pool.size, size=n, p=zipf / zipf.sum())
+    t = tg.Trace(layout, pool[pick], (np.arange(n) // 8).astype(np.uint32),
+                 np.zeros(n, np.uint8), np.where(pick % 3 == 0, 4, 1).astype(np.uint8),
+                 np.arange((n + 7) // 8, dtype=np.float64), 1)
+    cfgs = tg.from_list([{"cap": (c, d, 0), "policy": p} for c in (8, 200) for d in (0, 900)
+                         for p in range(3)] + [{"cap": (100, 300, 0), "mode": 1, "policy": 1}])
+    import os
+    old = os.environ.get("KVCFG_TEST_HIGH_FIRST")
+    os.environ["KVCFG_TEST_HIGH_FIRST"] = "1" if high_first else "0"
+    try:
+        compare(lib, oracle_mod, t, cfgs, label=f"hash-{layout}-{high_first}")
+    finally:
+        if old is None:
+            os.environ.pop("KVCFG_TEST_HIGH_FIRST", None)
+        else:
+            os.environ["KVCFG_TEST_HIGH_FIRST"] = old
