@@ -655,11 +655,16 @@ def main():
     print(f"[bench] device copy: {copy_gbs:.0f} GB/s", file=sys.stderr, flush=True)
     head, ctx = measure(args.workload, args.steps, args.warmup, torch, tg, host, K, keep=True)
     rec, cfgs, dev, G, model, n = ctx
-    # the HBM figures against the measured copy rate too
-    roof = head["roofline"]
-    hb = roof.get("hbm", roof if roof["bound"] == "hbm" else None)
-    if hb is not None:
-        hb["frac_of_copy"] = hb["achieved"] / copy_gbs
+    def against_copy(res):
+        # the HBM figures against the measured copy rate too
+        roof = res["roofline"]
+        hb = roof.get("hbm", roof if roof["bound"] == "hbm" else None)
+        if hb is not None:
+            hb["frac_of_copy"] = hb["achieved"] / copy_gbs
+        for rec in roof.get("stages", {}).values():
+            rec["frac_of_copy"] = rec["achieved"] / copy_gbs
+
+    against_copy(head)
     ttl = search = prefix = gttl = None
     workloads = None
     if not args.no_extras and not args.exclusive_extra_only:
@@ -676,6 +681,7 @@ def main():
             if w == args.workload:
                 continue
             r, _ = measure(w, 5, 1, torch, tg, host, K)
+            against_copy(r)
             if not args.no_cpu_baseline:
                 # the oracle on a short sample of this workload too (5 s budget)
                 wrec = tg.recipe(w)
