@@ -15,9 +15,12 @@
 //
 // One wavefront per configuration: its lanes stage slices of the trace
 // (block id, weight, group) in LDS, and its first lane walks them in order.
-// The block state (tier, list links, LFU count buckets) is indexed by the
-// trace's dense block ids in device memory; the list ends, the used weight
-// of every (hierarchy, tier) and the counters stay in LDS.  LRU and FIFO
+// The block state (tier, list links, LFU bucket of the block) is indexed by
+// the trace's dense block ids in device memory; the list ends, the used
+// weight of every (hierarchy, tier), the counters and the records of the
+// first 2,048 LFU buckets stay in LDS.  The walk records which live tier
+// served each access; all lanes turn a slice's records into hit, miss and
+// insertion counts at once, so the walk itself counts only evictions.  LRU and FIFO
 // tiers are doubly linked lists, oldest first; an LFU tier is a list of
 // count buckets in increasing count, each a list of its blocks oldest touch
 // first, so that the victim (least count, then least recent touch) heads the
@@ -37,9 +40,13 @@ namespace {
 
 constexpr uint32_t kNil = 0xFFFFFFFFu;
 constexpr uint8_t kNoTier = 0xFF;
+constexpr uint32_t kNoServe = 0xFF;  // an access of a hierarchy with no live tier, or not replayed here
 constexpr int kXNT = 64;        // one wavefront per configuration
 constexpr int kXStage = 1024;   // trace positions staged in LDS at a time
 constexpr int kXH = KV_MAX_GROUPS * KV_TIERS;  // (hierarchy, tier) slots
+constexpr uint32_t kXPool = 2048;  // LFU buckets whose records sit in LDS (40 KB)
+// the five fields of an LFU bucket record
+enum BucketField { kBF = 0, kBH, kBT, kBP, kBN, kBFields };
 
 struct ExclJobDev {
   uint32_t cfg;    // configuration
@@ -84,10 +91,25 @@ struct ExclLayout {
   }
 };
 
-// One job's replay state, used by the walking lane only.
+// Bucket records past the LDS pool.  Kept out of line: merged with the LDS
+// access into one access through a selected pointer, the pair does not
+// compile for gfx950.
+__host__ __device__ __attribute__((noinline)) uint32_t dev_get(const uint32_t* p, uint32_t x) {
+  return p[x];
+}
+__host__ __device__ __attribute__((noinline)) void dev_set(uint32_t* p, uint32_t x, uint32_t v) {
+  p[x] = v;
+}
+
+// One job's replay state, used by the walking lane only.  Buckets are taken
+// from the free list (last freed first) before a new index is used, so the
+// live buckets keep low indices: the records of the first kXPool buckets
+// sit in LDS, the others in device memory.
 struct XWalk {
   uint8_t* tier;
-  uint32_t *prv, *nxt, *node, *bf, *bh, *bt, *bp, *bn;
+  uint32_t *prv, *nxt, *node;
+  uint32_t* bdev[kBFields];  // bucket records in device memory, by field
+  uint32_t* blds[kBFields];  // the first kXPool of them in LDS
   uint32_t* lh;             // [kXH] first list member / first bucket
   uint32_t* lt;             // [kXH] last list member / last bucket
   unsigned long long* used; // [kXH]
@@ -106,8 +128,8 @@ struct XWalk {
     cnt[(g * KV_TIERS + k) * 8 + f + 4] += w;
   }
   // ---- LRU / FIFO lists (first = oldest)
-  __host__ __device__ void list_unlink(uint32_t hk, uint32_t b) {
-    const uint32_t p = prv[b], q = nxt[b];
+  // unlinks b, whose neighbours are p and q
+  __host__ __device__ void list_unlink(uint32_t hk, uint32_t p, uint32_t q) {
     if (p != kNil) nxt[p] = q; else lh[hk] = q;
     if (q != kNil) prv[q] = p; else lt[hk] = p;
   }
@@ -118,52 +140,83 @@ struct XWalk {
     if (p != kNil) nxt[p] = b; else lh[hk] = b;
     lt[hk] = b;
   }
-  // ---- LFU count buckets
+  // ---- LFU count buckets: count, first and last block, previous and next
+  // bucket
+  __host__ __device__ uint32_t bget(int k, uint32_t x) const {
+    if (x < kXPool) return blds[k][x];
+    return dev_get(bdev[k], x);
+  }
+  __host__ __device__ void bset(int k, uint32_t x, uint32_t v) {
+    if (x < kXPool) blds[k][x] = v;
+    else dev_set(bdev[k], x, v);
+  }
   __host__ __device__ uint32_t bucket_new(uint32_t f) {
     uint32_t r = free_b;
     if (r != kNil) {
-      free_b = bn[r];
+      free_b = bget(kBN, r);
     } else if (bump < limit) {
       r = bump++;
     } else {
       bad = true;  // more buckets than blocks: never with a consistent state
       return kNil;
     }
-    bf[r] = f;
-    bh[r] = bt[r] = kNil;
+    bset(kBF, r, f);
+    bset(kBH, r, kNil);
+    bset(kBT, r, kNil);
     return r;
   }
   __host__ __device__ void bucket_free(uint32_t hk, uint32_t x) {
-    const uint32_t p = bp[x], q = bn[x];
-    if (p != kNil) bn[p] = q; else lh[hk] = q;
-    if (q != kNil) bp[q] = p; else lt[hk] = p;
-    bn[x] = free_b;
+    const uint32_t p = bget(kBP, x), q = bget(kBN, x);
+    if (p != kNil) bset(kBN, p, q); else lh[hk] = q;
+    if (q != kNil) bset(kBP, q, p); else lt[hk] = p;
+    bset(kBN, x, free_b);
     free_b = x;
   }
   __host__ __device__ void bucket_push(uint32_t x, uint32_t b) {
-    const uint32_t p = bt[x];
+    const uint32_t p = bget(kBT, x);
     prv[b] = p;
     nxt[b] = kNil;
-    if (p != kNil) nxt[p] = b; else bh[x] = b;
-    bt[x] = b;
+    if (p != kNil) nxt[p] = b; else bset(kBH, x, b);
+    bset(kBT, x, b);
     node[b] = x;
   }
-  // takes b out of its bucket, freeing the bucket when it empties
-  __host__ __device__ void bucket_pull(uint32_t hk, uint32_t b) {
-    const uint32_t x = node[b], p = prv[b], q = nxt[b];
-    if (p != kNil) nxt[p] = q; else bh[x] = q;
-    if (q != kNil) prv[q] = p; else bt[x] = p;
-    if (bh[x] == kNil) bucket_free(hk, x);
+  // takes a block out of its bucket x, between blocks p and q, freeing the
+  // bucket when it empties
+  __host__ __device__ void bucket_pull(uint32_t hk, uint32_t x, uint32_t p, uint32_t q) {
+    if (p != kNil) nxt[p] = q; else bset(kBH, x, q);
+    if (q != kNil) prv[q] = p; else bset(kBT, x, p);
+    if (bget(kBH, x) == kNil) bucket_free(hk, x);
   }
   // ---- policy-level operations on tier slot hk
-  __host__ __device__ uint32_t victim(uint32_t hk, uint32_t pol) {
+  __host__ __device__ uint32_t victim(uint32_t hk, uint32_t pol) const {
     const uint32_t f = lh[hk];
     if (pol != KV_POLICY_LFU || f == kNil) return f;
-    return bh[f];
+    return bget(kBH, f);
   }
-  __host__ __device__ void take(uint32_t hk, uint32_t pol, uint32_t b) {
-    if (pol == KV_POLICY_LFU) bucket_pull(hk, b);
-    else list_unlink(hk, b);
+  // A block's links: its bucket (LFU only) and its list neighbours.  All are
+  // indexed by the block alone, so their loads go out together.
+  struct Links {
+    uint32_t x, p, q;
+  };
+  __host__ __device__ Links links(uint32_t pol, uint32_t b) const {
+    return Links{pol == KV_POLICY_LFU ? node[b] : kNil, prv[b], nxt[b]};
+  }
+  // What an access reads of its block before it is known whether it hits,
+  // all in one round of loads: the tier, and the links a top-tier hit moves
+  // (none for FIFO, whose hits move nothing).
+  struct Fields {
+    uint32_t t;
+    Links l;
+  };
+  __host__ __device__ Fields fields(uint32_t pol, uint32_t b) const {
+    Fields f;
+    f.t = tier[b];
+    f.l = pol == KV_POLICY_FIFO ? Links{kNil, kNil, kNil} : links(pol, b);
+    return f;
+  }
+  __host__ __device__ void take(uint32_t hk, uint32_t pol, const Links& l) {
+    if (pol == KV_POLICY_LFU) bucket_pull(hk, l.x, l.p, l.q);
+    else list_unlink(hk, l.p, l.q);
   }
   __host__ __device__ void admit(uint32_t hk, uint32_t pol, uint32_t b) {
     if (pol != KV_POLICY_LFU) {
@@ -171,34 +224,34 @@ struct XWalk {
       return;
     }
     uint32_t x = lh[hk];
-    if (x == kNil || bf[x] != 1u) {
+    if (x == kNil || bget(kBF, x) != 1u) {
       const uint32_t y = bucket_new(1u);
       if (y == kNil) return;
-      bp[y] = kNil;
-      bn[y] = x;
-      if (x != kNil) bp[x] = y; else lt[hk] = y;
+      bset(kBP, y, kNil);
+      bset(kBN, y, x);
+      if (x != kNil) bset(kBP, x, y); else lt[hk] = y;
       lh[hk] = y;
       x = y;
     }
     bucket_push(x, b);
   }
   // a hit in the top tier
-  __host__ __device__ void touch(uint32_t hk, uint32_t pol, uint32_t b) {
+  __host__ __device__ void touch(uint32_t hk, uint32_t pol, uint32_t b, const Links& l) {
     if (pol == KV_POLICY_LRU) {
-      list_unlink(hk, b);
+      list_unlink(hk, l.p, l.q);
       list_append(hk, b);
     } else if (pol == KV_POLICY_LFU) {
-      const uint32_t x = node[b], f = bf[x], q = bn[x];
+      const uint32_t x = l.x, f = bget(kBF, x), q = bget(kBN, x);
       uint32_t y = q;
-      if (q == kNil || bf[q] != f + 1u) {
+      if (q == kNil || bget(kBF, q) != f + 1u) {
         y = bucket_new(f + 1u);
         if (y == kNil) return;
-        bp[y] = x;
-        bn[y] = q;
-        bn[x] = y;
-        if (q != kNil) bp[q] = y; else lt[hk] = y;
+        bset(kBP, y, x);
+        bset(kBN, y, q);
+        bset(kBN, x, y);
+        if (q != kNil) bset(kBP, q, y); else lt[hk] = y;
       }
-      bucket_pull(hk, b);
+      bucket_pull(hk, x, l.p, l.q);
       bucket_push(y, b);
     }
   }
@@ -214,10 +267,10 @@ struct XWalk {
         return;
       }
       const uint32_t vw = blk_w[v], vg = blk_g[v];
-      take(hk, p, v);
+      take(hk, p, links(p, v));
       used[hk] -= vw;
       tier[v] = kNoTier;
-      count(vg, k, KV_F_EVICT, vw);
+      count(vg, k, KV_F_EVICT, vw);  // its insertion below follows from this count
       if constexpr (D + 1 < KV_TIERS) {
         if (D + 1 < nlive[h]) enter<D + 1>(h, v, vw, vg);
       }
@@ -226,32 +279,65 @@ struct XWalk {
     admit(hk, p, b);
     used[hk] += w;
     tier[b] = (uint8_t)k;
-    count(g, k, KV_F_INS, w);
   }
-  // one access of hierarchy h
-  __host__ __device__ void access(uint32_t h, uint32_t b, uint32_t w, uint32_t g) {
+  // One access of hierarchy h.  Returns what served it: live tier number d
+  // (fastest first), the number of live tiers for a miss in every tier, or
+  // kNoServe with no live tier.  Its hit, miss and top-tier insertion
+  // counts are left to `tally`.
+  __host__ __device__ uint32_t access(uint32_t h, uint32_t b, uint32_t w, uint32_t g) {
     const uint32_t nl = nlive[h];
-    if (nl == 0) return;
-    const uint32_t t = tier[b];
-    for (uint32_t i = 0; i < nl; ++i) {
-      const uint32_t k = live[h * KV_TIERS + i];
-      if (k == t) {
-        count(g, k, KV_F_HIT, w);
-        break;
-      }
-      count(g, k, KV_F_MISS, w);
-    }
-    const uint32_t top = live[h * KV_TIERS];
-    if (t == top) {
-      touch(h * KV_TIERS + top, pol[h], b);
-      return;
+    if (nl == 0) return kNoServe;
+    const uint32_t p = pol[h];
+    const Fields f = fields(p, b);  // in bounds either way; the links go unused after a miss
+    const uint32_t t = f.t;
+    const Links& l = f.l;
+    uint32_t d = 0;
+    while (d < nl && live[h * KV_TIERS + d] != t) ++d;
+    if (d == 0) {
+      touch(h * KV_TIERS + t, p, b, l);
+      return 0;
     }
     if (t != kNoTier) {  // a hit below the top: taken out for promotion
-      take(h * KV_TIERS + t, pol[h], b);
+      take(h * KV_TIERS + t, p, p == KV_POLICY_FIFO ? links(p, b) : l);
       used[h * KV_TIERS + t] -= w;
       tier[b] = kNoTier;
     }
     enter<0>(h, b, w, g);
+    return d;
+  }
+  // The counts of an access that `access` left out: a miss in each live tier
+  // faster than the one that served it, its hit, and its insertion into the
+  // top tier unless the top tier served it.  `add(p, v)` adds v to *p.
+  template <class Add>
+  __host__ __device__ void tally(uint32_t h, uint32_t d, uint32_t g, uint32_t w, Add add) const {
+    if (d == kNoServe) return;
+    const uint32_t nl = nlive[h];
+    unsigned long long* c = cnt + g * KV_TIERS * 8;
+    for (uint32_t j = 0; j < nl && j <= d; ++j) {
+      const uint32_t k = live[h * KV_TIERS + j];
+      const int f = j == d ? KV_F_HIT : KV_F_MISS;
+      add(&c[k * 8 + f], 1ull);
+      add(&c[k * 8 + f + 4], (unsigned long long)w);
+    }
+    if (d != 0) {
+      const uint32_t k = live[h * KV_TIERS];
+      add(&c[k * 8 + KV_F_INS], 1ull);
+      add(&c[k * 8 + KV_F_INS + 4], (unsigned long long)w);
+    }
+  }
+  // After the walk: every block a live tier demotes enters the next live
+  // tier, so that tier's insertions are the evictions above it.
+  __host__ __device__ void finish(uint32_t n_groups, bool part, uint32_t mask) {
+    for (uint32_t g = 0; g < n_groups; ++g) {
+      const uint32_t h = part ? g : 0u;
+      if (!((mask >> h) & 1u)) continue;
+      unsigned long long* c = cnt + g * KV_TIERS * 8;
+      for (uint32_t d = 1; d < nlive[h]; ++d) {
+        const uint32_t k = live[h * KV_TIERS + d], a = live[h * KV_TIERS + d - 1];
+        c[k * 8 + KV_F_INS] += c[a * 8 + KV_F_EVICT];
+        c[k * 8 + KV_F_INS + 4] += c[a * 8 + KV_F_EVICT + 4];
+      }
+    }
   }
 };
 
@@ -279,7 +365,8 @@ __global__ __launch_bounds__(kXNT) void k_excl_replay(ExclArgs a) {
   __shared__ unsigned long long cnt[KV_MAX_GROUPS * KV_TIERS * 8];
   __shared__ uint8_t pol[KV_MAX_GROUPS], live[KV_MAX_GROUPS * KV_TIERS], nlive[KV_MAX_GROUPS];
   __shared__ uint32_t sb[kXStage];
-  __shared__ uint8_t sw[kXStage], sg[kXStage];
+  __shared__ uint8_t sw[kXStage], sg[kXStage], sv[kXStage];
+  __shared__ uint32_t sbf[kXPool], sbh[kXPool], sbt[kXPool], sbp[kXPool], sbn[kXPool];
   const uint32_t lane = threadIdx.x;
   for (uint32_t i = lane; i < (uint32_t)kXH; i += kXNT) {
     const uint32_t h = i / KV_TIERS, k = i % KV_TIERS;
@@ -308,11 +395,16 @@ __global__ __launch_bounds__(kXNT) void k_excl_replay(ExclArgs a) {
   x.prv = reinterpret_cast<uint32_t*>(base + L.prv);
   x.nxt = reinterpret_cast<uint32_t*>(base + L.nxt);
   x.node = reinterpret_cast<uint32_t*>(base + L.node);
-  x.bf = reinterpret_cast<uint32_t*>(base + L.bf);
-  x.bh = reinterpret_cast<uint32_t*>(base + L.bh);
-  x.bt = reinterpret_cast<uint32_t*>(base + L.bt);
-  x.bp = reinterpret_cast<uint32_t*>(base + L.bp);
-  x.bn = reinterpret_cast<uint32_t*>(base + L.bn);
+  x.bdev[kBF] = reinterpret_cast<uint32_t*>(base + L.bf);
+  x.bdev[kBH] = reinterpret_cast<uint32_t*>(base + L.bh);
+  x.bdev[kBT] = reinterpret_cast<uint32_t*>(base + L.bt);
+  x.bdev[kBP] = reinterpret_cast<uint32_t*>(base + L.bp);
+  x.bdev[kBN] = reinterpret_cast<uint32_t*>(base + L.bn);
+  x.blds[kBF] = sbf;
+  x.blds[kBH] = sbh;
+  x.blds[kBT] = sbt;
+  x.blds[kBP] = sbp;
+  x.blds[kBN] = sbn;
   x.lh = lh;
   x.lt = lt;
   x.used = used;
@@ -339,13 +431,20 @@ __global__ __launch_bounds__(kXNT) void k_excl_replay(ExclArgs a) {
     if (lane == 0 && !x.bad) {
       for (uint32_t i = 0; i < m; ++i) {
         const uint32_t g = sg[i], h = part ? g : 0u;
-        if (!((job.mask >> h) & 1u)) continue;
-        x.access(h, sb[i], sw[i], g);
+        sv[i] = (uint8_t)(((job.mask >> h) & 1u) ? x.access(h, sb[i], sw[i], g) : kNoServe);
         if (x.bad) break;
       }
     }
     __syncthreads();
+    // the slice's hit, miss and top-tier insertion counts, by every lane
+    for (uint32_t i = lane; i < m; i += kXNT) {
+      const uint32_t g = sg[i];
+      x.tally(part ? g : 0u, sv[i], g, sw[i],
+              [](unsigned long long* p, unsigned long long v) { atomicAdd(p, v); });
+    }
   }
+  __syncthreads();
+  if (lane == 0) x.finish(G, part, job.mask);
   // the records this job owns: every group of a shared hierarchy, the
   // replayed groups of a partitioned one
   if (lane == 0 && x.bad && atomicCAS(&a.err[0], 0u, 2u) == 0u) atomicExch(&a.err[1], job.cfg);

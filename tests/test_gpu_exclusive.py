@@ -11,7 +11,8 @@ oracle element by element, objectives to 1e-6.
 * batches mixing these with inclusive and split-stack configurations;
 * workload-shaped slices (the mixed tenant and long-context traces, and
   the full workload's weighted blocks under exclusive LRU, FIFO and LFU);
-* state buffers forced small, so that the configurations run in waves.
+* state buffers forced small, so that the configurations run in waves;
+* an LFU trace that keeps more count buckets live than the walk holds in LDS.
 """
 import os
 import sys
@@ -141,3 +142,18 @@ def test_full_slice_weighted(oracle_mod):
     sub.mode[:] = tg.MODE_EXCLUSIVE_DEMOTE
     assert set(sub.policy[:, 0]) == {tg.POLICY_LRU, tg.POLICY_FIFO, tg.POLICY_LFU}
     compare(oracle_mod, t, sub, "full-slice-exclusive")
+
+
+def test_lfu_many_counts(oracle_mod):
+    """Block j of 2,200 accessed j + 1 times in shuffled order: a top tier
+    that holds every block ends with 2,200 count buckets, more than the
+    walk keeps in LDS, so bucket records in device memory are used too;
+    smaller tiers cascade demotions across many buckets."""
+    rng = np.random.default_rng(5)
+    u = 2200
+    labels = np.repeat(np.arange(u), np.arange(1, u + 1))
+    rng.shuffle(labels)
+    t = tg.from_blocks(labels, per_request=8)
+    c = tg.from_list([{"cap": cap, "policy": tg.POLICY_LFU, "mode": tg.MODE_EXCLUSIVE_DEMOTE}
+                      for cap in ((u, 0, 0), (1500, 400, 0), (2100, 50, 10), (600, 600, 600))])
+    compare(oracle_mod, t, c, "lfu-many-counts")
