@@ -101,7 +101,8 @@ __host__ __device__ __attribute__((noinline)) void dev_set(uint32_t* p, uint32_t
   p[x] = v;
 }
 
-// One job's replay state, used by the walking lane only.  Buckets are taken
+// One job's replay state.  The walk (`access`, `finish`) runs in one lane;
+// `tally` runs in every lane over a slice's served tiers.  Buckets are taken
 // from the free list (last freed first) before a new index is used, so the
 // live buckets keep low indices: the records of the first kXPool buckets
 // sit in LDS, the others in device memory.
