@@ -256,11 +256,12 @@ struct XWalk {
       bucket_push(y, b);
     }
   }
-  // Block b (weight w, group g) enters live tier number D of hierarchy h:
-  // the tier first passes victims to live tier D + 1 (or drops them).
-  template <int D>
+  // Block b (weight w, group g) enters live tier number D of hierarchy h,
+  // whose policy is P: the tier first passes victims to live tier D + 1 (or
+  // drops them).
+  template <int D, uint32_t P>
   __host__ __device__ void enter(uint32_t h, uint32_t b, uint32_t w, uint32_t g) {
-    const uint32_t k = live[h * KV_TIERS + D], hk = h * KV_TIERS + k, p = pol[h];
+    const uint32_t k = live[h * KV_TIERS + D], hk = h * KV_TIERS + k, p = P;
     while (used[hk] + w > cap[hk]) {
       const uint32_t v = victim(hk, p);
       if (v == kNil) {  // an empty tier holds any block: never with a consistent state
@@ -273,7 +274,7 @@ struct XWalk {
       tier[v] = kNoTier;
       count(vg, k, KV_F_EVICT, vw);  // its insertion below follows from this count
       if constexpr (D + 1 < KV_TIERS) {
-        if (D + 1 < nlive[h]) enter<D + 1>(h, v, vw, vg);
+        if (D + 1 < nlive[h]) enter<D + 1, P>(h, v, vw, vg);
       }
       if (bad) return;
     }
@@ -284,11 +285,21 @@ struct XWalk {
   // One access of hierarchy h.  Returns what served it: live tier number d
   // (fastest first), the number of live tiers for a miss in every tier, or
   // kNoServe with no live tier.  Its hit, miss and top-tier insertion
-  // counts are left to `tally`.
+  // counts are left to `tally`.  The policy is dispatched once per access:
+  // the walk below it is compiled for each policy.
   __host__ __device__ uint32_t access(uint32_t h, uint32_t b, uint32_t w, uint32_t g) {
     const uint32_t nl = nlive[h];
     if (nl == 0) return kNoServe;
-    const uint32_t p = pol[h];
+    switch (pol[h]) {
+      case KV_POLICY_FIFO: return access_p<KV_POLICY_FIFO>(h, b, w, g, nl);
+      case KV_POLICY_LFU: return access_p<KV_POLICY_LFU>(h, b, w, g, nl);
+      default: return access_p<KV_POLICY_LRU>(h, b, w, g, nl);
+    }
+  }
+  template <uint32_t P>
+  __host__ __device__ uint32_t access_p(uint32_t h, uint32_t b, uint32_t w, uint32_t g,
+                                        uint32_t nl) {
+    const uint32_t p = P;
     const Fields f = fields(p, b);  // in bounds either way; the links go unused after a miss
     const uint32_t t = f.t;
     const Links& l = f.l;
@@ -303,7 +314,7 @@ struct XWalk {
       used[h * KV_TIERS + t] -= w;
       tier[b] = kNoTier;
     }
-    enter<0>(h, b, w, g);
+    enter<0, P>(h, b, w, g);
     return d;
   }
   // The counts of an access that `access` left out: a miss in each live tier
