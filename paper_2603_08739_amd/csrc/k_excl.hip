@@ -186,7 +186,7 @@ struct XWalk {
   __host__ __device__ void bucket_pull(uint32_t hk, uint32_t x, uint32_t p, uint32_t q) {
     if (p != kNil) nxt[p] = q; else bset(kBH, x, q);
     if (q != kNil) prv[q] = p; else bset(kBT, x, p);
-    if (bget(kBH, x) == kNil) bucket_free(hk, x);
+    if (p == kNil && q == kNil) bucket_free(hk, x);  // it was the bucket's only block
   }
   // ---- policy-level operations on tier slot hk
   __host__ __device__ uint32_t victim(uint32_t hk, uint32_t pol) const {
@@ -441,9 +441,16 @@ __global__ __launch_bounds__(kXNT) void k_excl_replay(ExclArgs a) {
     }
     __syncthreads();
     if (lane == 0 && !x.bad) {
+      // the next access's staged fields are read before this access runs
+      uint32_t nb = sb[0], nw = sw[0], ng = sg[0];
       for (uint32_t i = 0; i < m; ++i) {
-        const uint32_t g = sg[i], h = part ? g : 0u;
-        sv[i] = (uint8_t)(((job.mask >> h) & 1u) ? x.access(h, sb[i], sw[i], g) : kNoServe);
+        const uint32_t b = nb, w = nw, g = ng, h = part ? g : 0u;
+        if (i + 1 < m) {
+          nb = sb[i + 1];
+          nw = sw[i + 1];
+          ng = sg[i + 1];
+        }
+        sv[i] = (uint8_t)(((job.mask >> h) & 1u) ? x.access(h, b, w, g) : kNoServe);
         if (x.bad) break;
       }
     }
